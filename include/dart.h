@@ -1,0 +1,199 @@
+/*
+ * dart.h -- C ABI of the DART hot-path library (libdart.so) for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * DART ("Decoded Attention over Recurrent sTates", arXiv 2608.02032) augments
+ * the Mamba-2 chunked SSD scan: the scan keeps each chunk's state
+ * contribution dH_[c] (a "chunk state memory", N x P per head), and
+ * state-memory attention (SMA) lets every token attend over the memories of
+ * strictly earlier chunks, decoding a token-conditioned key K = r (.) (dH E)
+ * and value V = C dH from each memory, before a SiLU-gated residual adds the
+ * readout to the SSM output.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensor pointers are DEVICE pointers to contiguous row-major arrays in the
+ *    tensor order of the paper's App. B.2 (Table 7).  Symbols:
+ *      B = batch, L = sequence length, H = heads, G = projection groups
+ *      (G divides H; head h uses group h*G/H), P = head dim, N = state size,
+ *      S = chunk size, M = ceil(L/S) chunks, Mcap = memory capacity >= M.
+ *  - "storage dtype" (dims.dtype) is the element type of x, Bm, Cm, q, e, z,
+ *    y_ssd, y and the memories: DART_FP32 (float) or DART_BF16 (bfloat16).
+ *    dt, A, lse, h0, h_last, h_state and chunk_acc are always float.  All
+ *    arithmetic accumulates in float.
+ *  - Ownership: the caller allocates and owns every buffer, including the
+ *    workspace.  The library allocates no memory, keeps no state between
+ *    calls and is thread-safe; work is enqueued on `stream` (a hipStream_t;
+ *    NULL = the null stream) and runs asynchronously.
+ *  - Errors: every argument check runs on the host before any launch.  A
+ *    failing check returns DART_ERR_INVALID_ARG (malformed arguments) or
+ *    DART_ERR_UNSUPPORTED (well-formed shapes this build has no kernel for)
+ *    and enqueues nothing; a failed launch returns DART_ERR_HIP.
+ *    dart_last_error() gives a message for the last non-OK status of the
+ *    calling thread.  Numeric contracts (dt > 0, A < 0) are the caller's.
+ *  - Supported shapes: P = 64; N in {32, 64, 128}; S in {64, 128, 256};
+ *    any L >= 1 (a partial last chunk is allowed); any B, H with H % G == 0.
+ */
+#ifndef DART_H
+#define DART_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DART_OK = 0,
+    DART_ERR_INVALID_ARG = 1,
+    DART_ERR_UNSUPPORTED = 2,
+    DART_ERR_HIP = 3
+} dart_status;
+
+typedef enum { DART_FP32 = 0, DART_BF16 = 1 } dart_dtype;
+
+/* Problem dimensions (App. B.2 Table 7 symbols). */
+typedef struct {
+    int64_t batch;        /* B  >= 1 */
+    int64_t seqlen;       /* L  >= 1 (ignored by the decode entry points) */
+    int32_t nheads;       /* H  >= 1 */
+    int32_t ngroups;      /* G  >= 1, H % G == 0 (the paper uses G = 1) */
+    int32_t headdim;      /* P */
+    int32_t dstate;       /* N */
+    int32_t chunk;        /* S */
+    int32_t dtype;        /* dart_dtype: storage dtype */
+    int64_t mem_capacity; /* Mcap: slots in the memory array; 0 means ceil(L/S) */
+} dart_dims;
+
+/* State-memory attention options (Sec. 3 and App. B.1). */
+typedef struct {
+    float eps;              /* RMS epsilon for RMSNorm(Q), RMSNorm(E) and the memory
+                               row inverse-RMS r; the paper leaves it open; > 0
+                               required when normalize = 1 (1e-6 is the default of
+                               the Python binding) */
+    const float* q_norm_w;  /* device [N] RMSNorm weight of Q, or NULL for ones */
+    const float* e_norm_w;  /* device [P] RMSNorm weight of E, or NULL for ones */
+    int32_t normalize;      /* 1: normalised score branch of App. B.1;
+                               0: Alg. 1 as printed (raw Q, E and r = 1) */
+    int32_t z_per_head;     /* 1: z is [B][L][H] (one gate per head);
+                               0: z is [B][L] (one scalar gate per token) */
+} dart_sma_opts;
+
+/* Bytes of workspace dart_ssd_chunk_scan needs for `dims`. */
+size_t dart_scan_workspace_bytes(const dart_dims* dims);
+
+/*
+ * Mamba-2 chunked SSD scan that retains the chunk state memories.
+ * Sec. 2 (SSD recurrence), Sec. 3 (chunk state memory dH_[c]) and App. A
+ * (chunk-state, inter-chunk state passing, intra/inter-chunk outputs).  With
+ * a_t = exp(dt_t * A_h) it computes, exactly up to rounding, the recurrence
+ *     H_t = a_t H_{t-1} + dt_t B_t^T x_t,   y_ssd_t = C_t H_t,
+ * starting from h0 (zero if NULL), and every chunk's contribution
+ *     dH_[c] = sum_{s in chunk c} (prod_{k=s+1}^{e(c)} a_k) dt_s B_s^T x_s.
+ *
+ *   x      [B][L][H][P]     storage dtype, in
+ *   dt     [B][L][H]        float, in (step sizes, already positive)
+ *   A      [H]              float, in (negative decay rates)
+ *   Bm, Cm [B][L][G][N]     storage dtype, in
+ *   h0     [B][H][N][P]     float, in, or NULL
+ *   y_ssd  [B][L][H][P]     storage dtype, out
+ *   mem    [B][Mcap][H][N][P] storage dtype, out: slots 0..M-1 written (the
+ *                           last one holds a partial chunk when L % S != 0),
+ *                           slots >= M untouched.  Same layout as the decode
+ *                           cache, so a prefill writes straight into it.
+ *   h_last [B][H][N][P]     float, out, or NULL: H_{L-1}
+ *   workspace               device buffer of >= dart_scan_workspace_bytes()
+ */
+dart_status dart_ssd_chunk_scan(const dart_dims* dims, const void* x, const float* dt,
+                                const float* A, const void* Bm, const void* Cm, const float* h0,
+                                void* y_ssd, void* mem, float* h_last, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace dart_sma_fwd needs for `dims`. */
+size_t dart_sma_workspace_bytes(const dart_dims* dims);
+
+/*
+ * State-memory attention forward with the fused gated residual.
+ * Sec. 3 ("State-Memory Attention", "Gated Residual Integration"), Alg. 1
+ * (streaming over historical chunks with an online softmax; keys and values
+ * decoded on chip) and App. B.1 (normalised score branch).  For token t of
+ * chunk i = floor(t/S) and every memory j < i:
+ *     Qb = RMSNorm(q_t) * q_norm_w,  Eb = RMSNorm(e_t) * e_norm_w,
+ *     r_j[n] = (mean_p dH_j[n,p]^2 + eps)^-1/2,
+ *     K = r_j (.) (dH_j Eb),  l_j = Qb . K / sqrt(N),  V_j = C_t dH_j,
+ *     R_t = sum_j softmax_j(l)_j V_j,   LSE_t = log sum_j exp(l_j),
+ *     y_t = y_ssd_t + SiLU(z_t) R_t.
+ * Tokens of the first chunk have no history: R_t = 0, LSE_t = -inf and
+ * y_t = y_ssd_t exactly.  r is computed from the memory values as stored.
+ *
+ *   q      [B][L][G][N]     storage dtype, in
+ *   e      [B][L][G][P]     storage dtype, in
+ *   Cm     [B][L][G][N]     storage dtype, in (the SSM read vector, shared)
+ *   mem    [B][Mcap][H][N][P] storage dtype, in (slots 0..M-2 are read)
+ *   z      [B][L][H] or [B][L] (opts->z_per_head) storage dtype, in: gate
+ *                           pre-activation
+ *   y_ssd  [B][L][H][P]     storage dtype, in
+ *   y      [B][L][H][P]     storage dtype, out; may alias y_ssd exactly
+ *   lse    [B][L][H]        float, out, or NULL
+ *   workspace               device buffer of >= dart_sma_workspace_bytes()
+ */
+dart_status dart_sma_fwd(const dart_dims* dims, const dart_sma_opts* opts, const void* q,
+                         const void* e, const void* Cm, const void* mem, const void* z,
+                         const void* y_ssd, void* y, float* lse, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace dart_decode_step needs (dims->seqlen is ignored; the
+ * worst case over positions that fit dims->mem_capacity is returned). */
+size_t dart_decode_workspace_bytes(const dart_dims* dims);
+
+/*
+ * One autoregressive decode step at 0-based position `pos` (host value, the
+ * same for every sequence), over the cached chunk memories.  The paper gives
+ * no algorithm for it (Sec. 4 "Inference Cache" names the caches); the order
+ * is the one that reproduces the forward pass token by token:
+ *   1. if pos % S == 0: chunk_acc = 0 (a new chunk starts);
+ *   2. a = exp(dt A_h); h_state = a h_state + dt B^T x; chunk_acc likewise;
+ *   3. y_ssd = C h_state;
+ *   4. SMA (as in dart_sma_fwd) over memories 0 .. m-1, m = floor(pos/S);
+ *   5. y = y_ssd + SiLU(z) R;
+ *   6. if pos % S == S-1: mem_cache[m] = chunk_acc (rounded to storage dtype).
+ * After step 6 chunk_acc equals dH_[m] and h_state equals H_pos.
+ *
+ *   x       [B][H][P]       storage dtype, in
+ *   dt      [B][H]          float, in
+ *   A       [H]             float, in
+ *   Bm, Cm, q [B][G][N]     storage dtype, in
+ *   e       [B][G][P]       storage dtype, in
+ *   z       [B][H] or [B]   storage dtype, in
+ *   h_state [B][H][N][P]    float, in/out
+ *   chunk_acc [B][H][N][P]  float, in/out
+ *   mem_cache [B][Mcap][H][N][P] storage dtype, in/out (slot m written on
+ *                           step 6 only); Mcap = dims->mem_capacity (> 0)
+ *   y       [B][H][P]       storage dtype, out
+ * Errors: DART_ERR_INVALID_ARG if pos < 0, if m > Mcap, or if the step would
+ * append (pos % S == S-1) with m >= Mcap.
+ */
+dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, int64_t pos,
+                             const void* x, const float* dt, const float* A, const void* Bm,
+                             const void* Cm, const void* q, const void* e, const void* z,
+                             float* h_state, float* chunk_acc, void* mem_cache, void* y,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Element count of the length-dependent decode cache for a context of
+ * `context` tokens: B * ceil(context/S) * H * N * P chunk-memory elements
+ * (Sec. 4 "Inference Cache": O(M N P) per head).  The matched token-attention
+ * KV cache is B * H * 2 * context * P elements, so for context % S == 0 the
+ * ratio is N / (2 S).  Returns 0 for malformed dims.
+ */
+int64_t dart_decode_cache_elems(const dart_dims* dims, int64_t context);
+
+const char* dart_status_string(dart_status status);
+const char* dart_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DART_H */

@@ -1,0 +1,212 @@
+"""Plain fp64 CPU oracle for DART's hot path (arXiv 2608.02032).
+
+TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` are the only users.  The product library
+(``paper_2608_02032_amd``) never imports this package, and this package never
+imports the product.
+
+The arithmetic lives in ``dart_oracle.c`` (literal loops in double precision,
+one function per definition of the paper; see its header for the citations).
+This module only compiles it with gcc, loads it with ctypes and marshals
+numpy arrays.  Every array argument is converted to a C-contiguous float64
+array; callers pass values already rounded to the storage precision of the
+GPU path (the rounding itself is input preparation, not oracle arithmetic).
+
+parity: see the header of ``dart_oracle.c``; the RMS epsilon, norm weights
+and gate granularity are conventions the paper leaves open (parity unpinned
+for those conventions beyond the oracle self-tests).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dart_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+_D = ctypes.POINTER(ctypes.c_double)
+_I64 = ctypes.c_int64
+_INT = ctypes.c_int
+
+
+def build(force: bool = True) -> str:
+    """Compile dart_oracle.c into liboracle.so (plain gcc, OpenMP over rows)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99", "-Wall",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB_PATH)
+        lib.dart_oracle_ssd_recurrence.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT,
+                                                   _D, _D, _D, _D, _D, _D, _D, _D]
+        lib.dart_oracle_ssd_recurrence.restype = None
+        lib.dart_oracle_chunk_memories.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
+                                                   _D, _D, _D, _D, _D]
+        lib.dart_oracle_chunk_memories.restype = None
+        lib.dart_oracle_sma.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
+                                        ctypes.c_double, _INT, _INT,
+                                        _D, _D, _D, _D, _D, _D, _D, _D, _D, _D, _D]
+        lib.dart_oracle_sma.restype = None
+        lib.dart_oracle_sma_rows.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
+                                             ctypes.c_double, _INT, _INT,
+                                             _D, _D, _D, _D, _D, _D, _D, _D,
+                                             _I64, ctypes.POINTER(ctypes.c_int64), _D, _D]
+        lib.dart_oracle_sma_rows.restype = None
+        lib.dart_oracle_decode_step.argtypes = [_I64, _INT, _INT, _INT, _INT, _INT, _I64, _I64,
+                                                ctypes.c_double, _INT, _INT,
+                                                _D, _D, _D, _D, _D, _D, _D, _D, _D, _D,
+                                                _D, _D, _D, _D]
+        lib.dart_oracle_decode_step.restype = ctypes.c_int
+        _lib = lib
+        return lib
+
+
+def _f64(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a):
+    if a is None:
+        return None
+    return a.ctypes.data_as(_D)
+
+
+def ssd_recurrence(x, dt, A, Bm, Cm, h0=None):
+    """Token-level SSD recurrence (Sec. 2).  Shapes as in Table 7.
+
+    x [B][L][H][P], dt [B][L][H], A [H], Bm/Cm [B][L][G][N], h0 [B][H][N][P] or None.
+    Returns (y_ssd [B][L][H][P], h_last [B][H][N][P]).
+    """
+    x, dt, A, Bm, Cm = map(_f64, (x, dt, A, Bm, Cm))
+    B_, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    h0 = None if h0 is None else _f64(h0)
+    y = np.empty((B_, L, H, P))
+    hl = np.empty((B_, H, N, P))
+    _load().dart_oracle_ssd_recurrence(B_, L, H, G, P, N, _ptr(x), _ptr(dt), _ptr(A), _ptr(Bm),
+                                       _ptr(Cm), _ptr(h0), _ptr(y), _ptr(hl))
+    return y, hl
+
+
+def chunk_memories(x, dt, A, Bm, S, mem_capacity=None):
+    """Chunk state memories dH_[c] by the brute-force definition (Sec. 3, App. A).
+
+    Returns mem [B][Mcap][H][N][P]; slots beyond ceil(L/S) are zero.
+    """
+    x, dt, A, Bm = map(_f64, (x, dt, A, Bm))
+    B_, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    M = -(-L // S)
+    Mcap = M if mem_capacity is None else int(mem_capacity)
+    mem = np.zeros((B_, Mcap, H, N, P))
+    _load().dart_oracle_chunk_memories(B_, L, H, G, P, N, int(S), Mcap, _ptr(x), _ptr(dt),
+                                       _ptr(A), _ptr(Bm), _ptr(mem))
+    return mem
+
+
+def sma(q, e, Cm, mem, z, y_ssd, S, eps=1e-6, normalize=True, q_norm_w=None, e_norm_w=None,
+        return_R=False):
+    """State-memory attention + gated residual (Sec. 3, App. B.1).
+
+    q [B][L][G][N], e [B][L][G][P], Cm [B][L][G][N], mem [B][Mcap][H][N][P],
+    z [B][L][H] (one gate per head) or [B][L] (one gate per token), y_ssd [B][L][H][P].
+    Returns (y, lse) or (y, lse, R).
+    """
+    q, e, Cm, mem, z, y_ssd = map(_f64, (q, e, Cm, mem, z, y_ssd))
+    B_, L, H, P = y_ssd.shape
+    G, N = q.shape[2], q.shape[3]
+    Mcap = mem.shape[1]
+    assert Mcap >= -(-L // S)
+    z_per_head = 1 if z.ndim == 3 else 0
+    qw = None if q_norm_w is None else _f64(q_norm_w)
+    ew = None if e_norm_w is None else _f64(e_norm_w)
+    y = np.empty((B_, L, H, P))
+    lse = np.empty((B_, L, H))
+    R = np.empty((B_, L, H, P)) if return_R else None
+    _load().dart_oracle_sma(B_, L, H, G, P, N, int(S), Mcap, float(eps), int(bool(normalize)),
+                            z_per_head, _ptr(q), _ptr(e), _ptr(Cm), _ptr(qw), _ptr(ew), _ptr(mem),
+                            _ptr(z), _ptr(y_ssd), _ptr(y), _ptr(lse), _ptr(R))
+    return (y, lse, R) if return_R else (y, lse)
+
+
+def sma_rows(q, e, Cm, mem, z, y_ssd, S, rows, eps=1e-6, normalize=True, q_norm_w=None,
+             e_norm_w=None):
+    """The SMA definition evaluated at selected rows only.
+
+    rows: int array [K][3] of (b, t, h).  Returns (y_rows [K][P], lse_rows [K]).
+    Arrays may be large; they are converted to float64 once.
+    """
+    q, e, Cm, mem, z, y_ssd = map(_f64, (q, e, Cm, mem, z, y_ssd))
+    B_, L, H, P = y_ssd.shape
+    G, N = q.shape[2], q.shape[3]
+    Mcap = mem.shape[1]
+    rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64).reshape(-1, 3))
+    z_per_head = 1 if z.ndim == 3 else 0
+    qw = None if q_norm_w is None else _f64(q_norm_w)
+    ew = None if e_norm_w is None else _f64(e_norm_w)
+    K = rows.shape[0]
+    yr = np.empty((K, P))
+    lr = np.empty((K,))
+    _load().dart_oracle_sma_rows(B_, L, H, G, P, N, int(S), Mcap, float(eps), int(bool(normalize)),
+                                 z_per_head, _ptr(q), _ptr(e), _ptr(Cm), _ptr(qw), _ptr(ew),
+                                 _ptr(mem), _ptr(z), _ptr(y_ssd), K,
+                                 rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                 _ptr(yr), _ptr(lr))
+    return yr, lr
+
+
+def forward(x, dt, A, Bm, Cm, q, e, z, S, eps=1e-6, normalize=True, q_norm_w=None,
+            e_norm_w=None, h0=None):
+    """Whole layer path from scratch: recurrence, brute-force memories, SMA, gate."""
+    y_ssd, h_last = ssd_recurrence(x, dt, A, Bm, Cm, h0)
+    mem = chunk_memories(x, dt, A, Bm, S)
+    y, lse = sma(q, e, Cm, mem, z, y_ssd, S, eps, normalize, q_norm_w, e_norm_w)
+    return {"y_ssd": y_ssd, "h_last": h_last, "mem": mem, "y": y, "lse": lse}
+
+
+def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem, S, eps=1e-6,
+                normalize=True, q_norm_w=None, e_norm_w=None):
+    """One autoregressive token at position ``pos`` for every sequence.
+
+    x [B][H][P], dt [B][H], Bm/Cm/q [B][G][N], e [B][G][P], z [B][H] or [B];
+    h_state, chunk_acc [B][H][N][P] and mem [B][Mcap][H][N][P] are updated IN PLACE
+    (they must be C-contiguous float64 arrays).  Returns y [B][H][P].
+    """
+    x, dt, A, Bm, Cm, q, e, z = map(_f64, (x, dt, A, Bm, Cm, q, e, z))
+    for arr in (h_state, chunk_acc, mem):
+        if not (isinstance(arr, np.ndarray) and arr.dtype == np.float64
+                and arr.flags["C_CONTIGUOUS"]):
+            raise TypeError("decode state arrays must be C-contiguous float64 ndarrays")
+    B_, H, P = x.shape
+    G, N = Bm.shape[1], Bm.shape[2]
+    Mcap = mem.shape[1]
+    z_per_head = 1 if z.ndim == 2 else 0
+    qw = None if q_norm_w is None else _f64(q_norm_w)
+    ew = None if e_norm_w is None else _f64(e_norm_w)
+    y = np.empty((B_, H, P))
+    rc = _load().dart_oracle_decode_step(B_, H, G, P, N, int(S), Mcap, int(pos), float(eps),
+                                         int(bool(normalize)), z_per_head, _ptr(x), _ptr(dt),
+                                         _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(q), _ptr(e), _ptr(qw),
+                                         _ptr(ew), _ptr(z), _ptr(h_state), _ptr(chunk_acc),
+                                         _ptr(mem), _ptr(y))
+    if rc != 0:
+        raise ValueError("decode position %d does not fit a cache of %d memories" % (pos, Mcap))
+    return y

@@ -1,0 +1,422 @@
+/*
+ * dart_oracle.c -- plain, slow, fp64 CPU oracle for the hot path of DART
+ * ("Decoded Attention over Recurrent sTates", arXiv 2608.02032).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product (the HIP library and its
+ * Python binding) may include, link, load or call this file.  Only the tests,
+ * the smoke check and the CPU-baseline leg of the benchmark use it.  It shares
+ * no code, header, table or helper with the GPU path.
+ *
+ * Every routine is the plain definition from the paper, written as literal
+ * loops in double precision, with no chunking, blocking, fusion or reordering
+ * beyond what the definition states:
+ *
+ *   dart_oracle_ssd_recurrence   Sec. 2 "State Space Duality": the token-level
+ *                                recurrence H_t = A_t H_{t-1} + B_t^T X_t,
+ *                                Y_t = C_t H_t, with the scalar transition
+ *                                A_t = a_t I_N and the discretisation
+ *                                a_t = exp(dt_t * A_h), input term
+ *                                dt_t * B_t^T X_t (the paper writes the
+ *                                recurrence without dt, while its kernel
+ *                                benchmark feeds precomputed X, dt, A, B, C;
+ *                                dt arrives already positive, no softplus).
+ *   dart_oracle_chunk_memories   Sec. 3 "Chunk State Memories" and App. A
+ *                                Eq. (mamba2_delta_h_chunk):
+ *                                dH_[c] = sum_{s in [c]} A_{s+1:e(c)} B_s^T X_s,
+ *                                the decay product taken literally, the empty
+ *                                product being 1.
+ *   dart_oracle_sma              Sec. 3 "State-Memory Attention" and
+ *                                "Gated Residual Integration", with the
+ *                                normalised score branch of App. B.1: for each
+ *                                token an explicit two-pass softmax over the
+ *                                strictly earlier chunks, then
+ *                                Y_t = C_t H_t + SiLU(z_t) R_t.
+ *   dart_oracle_decode_step      one autoregressive token (the paper gives no
+ *                                algorithm; the order used is: update the
+ *                                recurrent state and the running chunk
+ *                                contribution, read the cached memories of
+ *                                completed chunks, gate, and append the running
+ *                                contribution when the token closes a chunk).
+ *
+ * Precision: all arithmetic in double.  Callers pass the inputs already
+ * rounded to the storage precision the GPU sees, then widened to double.
+ *
+ * Layouts (row-major, App. B.2 Table 7 order; b = batch, t = token,
+ * h = head, g = group = h*G/H, c = chunk, n = state index, p = head-dim index):
+ *   x      [B][L][H][P]       dt  [B][L][H]       A  [H]
+ *   Bm, Cm [B][L][G][N]       q   [B][L][G][N]    e  [B][L][G][P]
+ *   z      [B][L][H] (z_per_head = 1) or [B][L] (z_per_head = 0)
+ *   y_ssd, y [B][L][H][P]     lse [B][L][H]
+ *   mem    [B][Mcap][H][N][P] with M = ceil(L/S) <= Mcap
+ *   h0, h_last, h_state, chunk_acc [B][H][N][P]
+ *
+ * parity: pinned by the oracle self-tests (SSD duality, boundary-state
+ * identity, S = L and S = 1 degenerate cases, closed-form softmax cases,
+ * normalisation invariances, decode == forward).  The conventions for the RMS
+ * epsilon, the optional norm weights and the gate granularity are readings of
+ * the paper, not fixed by it.
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#define X_AT(b, t, h, p) x[(((size_t)(b) * L + (t)) * H + (h)) * P + (p)]
+#define DT_AT(b, t, h) dt[((size_t)(b) * L + (t)) * H + (h)]
+#define BM_AT(b, t, g, n) Bm[(((size_t)(b) * L + (t)) * G + (g)) * N + (n)]
+#define CM_AT(b, t, g, n) Cm[(((size_t)(b) * L + (t)) * G + (g)) * N + (n)]
+#define Y_AT(arr, b, t, h, p) arr[(((size_t)(b) * L + (t)) * H + (h)) * P + (p)]
+#define ST_AT(arr, b, h, n, p) arr[(((size_t)(b) * H + (h)) * N + (n)) * P + (p)]
+#define MEM_AT(b, c, h, n, p) \
+    mem[((((size_t)(b) * Mcap + (c)) * H + (h)) * N + (n)) * P + (p)]
+
+static int group_of(int h, int H, int G) { return (int)(((long)h * G) / H); }
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 2 SSD recurrence (and App. A, token-level form).                     */
+/* ------------------------------------------------------------------------ */
+void dart_oracle_ssd_recurrence(int64_t B, int64_t L, int H, int G, int P, int N,
+                                const double* x, const double* dt, const double* A,
+                                const double* Bm, const double* Cm,
+                                const double* h0, /* may be NULL: zero state */
+                                double* y_ssd, double* h_last /* may be NULL */) {
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b) {
+        for (int h = 0; h < H; ++h) {
+            const int g = group_of(h, H, G);
+            double* Hs = (double*)malloc(sizeof(double) * (size_t)N * P);
+            for (int n = 0; n < N; ++n)
+                for (int p = 0; p < P; ++p)
+                    Hs[(size_t)n * P + p] = h0 ? ST_AT(h0, b, h, n, p) : 0.0;
+            for (int64_t t = 0; t < L; ++t) {
+                const double d = DT_AT(b, t, h);
+                const double a = exp(d * A[h]); /* scalar transition a_t */
+                /* H_t = a_t H_{t-1} + dt_t B_t^T X_t */
+                for (int n = 0; n < N; ++n)
+                    for (int p = 0; p < P; ++p)
+                        Hs[(size_t)n * P + p] =
+                            a * Hs[(size_t)n * P + p] + d * BM_AT(b, t, g, n) * X_AT(b, t, h, p);
+                /* Y_t = C_t H_t */
+                for (int p = 0; p < P; ++p) {
+                    double acc = 0.0;
+                    for (int n = 0; n < N; ++n) acc += CM_AT(b, t, g, n) * Hs[(size_t)n * P + p];
+                    Y_AT(y_ssd, b, t, h, p) = acc;
+                }
+            }
+            if (h_last)
+                for (int n = 0; n < N; ++n)
+                    for (int p = 0; p < P; ++p) ST_AT(h_last, b, h, n, p) = Hs[(size_t)n * P + p];
+            free(Hs);
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 3 chunk state memory, App. A Eq. (mamba2_delta_h_chunk).            */
+/* Chunk c (0-based) holds tokens [c*S, min((c+1)*S, L)); e(c) is its last   */
+/* token.  A partial last chunk is emitted like any other.                   */
+/* ------------------------------------------------------------------------ */
+void dart_oracle_chunk_memories(int64_t B, int64_t L, int H, int G, int P, int N, int S,
+                                int64_t Mcap, const double* x, const double* dt,
+                                const double* A, const double* Bm, double* mem) {
+    const int64_t M = (L + S - 1) / S;
+#pragma omp parallel for collapse(3) schedule(static)
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t c = 0; c < M; ++c) {
+            for (int h = 0; h < H; ++h) {
+                const int g = group_of(h, H, G);
+                const int64_t a0 = c * S;
+                const int64_t e = (c + 1) * S < L ? (c + 1) * S - 1 : L - 1;
+                for (int n = 0; n < N; ++n)
+                    for (int p = 0; p < P; ++p) MEM_AT(b, c, h, n, p) = 0.0;
+                for (int64_t s = a0; s <= e; ++s) {
+                    /* A_{s+1:e(c)} = prod_{k=s+1}^{e(c)} a_k, empty product = 1 */
+                    double decay = 1.0;
+                    for (int64_t k = s + 1; k <= e; ++k) decay *= exp(DT_AT(b, k, h) * A[h]);
+                    const double w = decay * DT_AT(b, s, h);
+                    for (int n = 0; n < N; ++n)
+                        for (int p = 0; p < P; ++p)
+                            MEM_AT(b, c, h, n, p) += w * BM_AT(b, s, g, n) * X_AT(b, s, h, p);
+                }
+            }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 3 state-memory attention + App. B.1 normalised score branch.         */
+/* ------------------------------------------------------------------------ */
+
+/* App. B.1: r_{c,n} = (P^{-1} sum_p dH[n,p]^2 + eps)^{-1/2}; r = 1 when the
+ * score branch is not normalised (Alg. 1 as printed). */
+static void inv_row_rms(const double* dH, int N, int P, double eps, int normalize, double* r) {
+    for (int n = 0; n < N; ++n) {
+        if (!normalize) {
+            r[n] = 1.0;
+            continue;
+        }
+        double ss = 0.0;
+        for (int p = 0; p < P; ++p) ss += dH[(size_t)n * P + p] * dH[(size_t)n * P + p];
+        r[n] = 1.0 / sqrt(ss / P + eps);
+    }
+}
+
+/* RMSNorm of a length-D vector with optional weight (App. B.1). */
+static void rms_normalise(const double* v, int D, double eps, const double* w, double* out) {
+    double ss = 0.0;
+    for (int k = 0; k < D; ++k) ss += v[k] * v[k];
+    const double inv = 1.0 / sqrt(ss / D + eps);
+    for (int k = 0; k < D; ++k) out[k] = v[k] * inv * (w ? w[k] : 1.0);
+}
+
+static double silu(double z) { return z / (1.0 + exp(-z)); }
+
+/*
+ * One query row (b, t, h): chunk index i = floor(t/S) (0-based form of
+ * c(t) = ceil(t/S)); softmax over memories j = 0..i-1 (strictly earlier
+ * chunks).  Empty history: R = 0 and LSE = -inf.  `rr` holds r for every
+ * memory of this (b, h): rr[j*N + n].  Writes R[P], *lse and y[P].
+ */
+static void sma_row(int64_t B, int64_t L, int H, int G, int P, int N, int S, int64_t Mcap,
+                    double eps, int normalize, int z_per_head, const double* q, const double* e,
+                    const double* Cm, const double* qw, const double* ew, const double* mem,
+                    const double* rr, const double* z, const double* y_ssd, int64_t b, int64_t t,
+                    int h, double* R, double* lse, double* y, double* work) {
+    (void)B;
+    const int g = group_of(h, H, G);
+    const int64_t i = t / S;
+    const double* qt = q + ((size_t)b * L + t) * G * N + (size_t)g * N;
+    const double* et = e + ((size_t)b * L + t) * G * P + (size_t)g * P;
+    const double* ct = Cm + ((size_t)b * L + t) * G * N + (size_t)g * N;
+    double* qbar = work;           /* N */
+    double* ebar = qbar + N;       /* P */
+    double* ell = ebar + P;        /* i logits */
+    double* V = ell + (i > 0 ? i : 1); /* i*P values */
+
+    for (int p = 0; p < P; ++p) R[p] = 0.0;
+    if (i == 0) {
+        *lse = -INFINITY;
+    } else {
+        if (normalize) {
+            rms_normalise(qt, N, eps, qw, qbar);
+            rms_normalise(et, P, eps, ew, ebar);
+        } else {
+            for (int n = 0; n < N; ++n) qbar[n] = qt[n];
+            for (int p = 0; p < P; ++p) ebar[p] = et[p];
+        }
+        for (int64_t j = 0; j < i; ++j) {
+            const double* dH = mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+            const double* r = rr + (size_t)j * N;
+            /* K_{t,j}[n] = r_j[n] * sum_p dH_j[n,p] Ebar_t[p];  l = Qbar . K / sqrt(N) */
+            double l = 0.0;
+            for (int n = 0; n < N; ++n) {
+                double k = 0.0;
+                for (int p = 0; p < P; ++p) k += dH[(size_t)n * P + p] * ebar[p];
+                l += qbar[n] * (r[n] * k);
+            }
+            ell[j] = l / sqrt((double)N);
+            /* V_{t,j}[p] = sum_n C_t[n] dH_j[n,p] */
+            for (int p = 0; p < P; ++p) {
+                double v = 0.0;
+                for (int n = 0; n < N; ++n) v += ct[n] * dH[(size_t)n * P + p];
+                V[(size_t)j * P + p] = v;
+            }
+        }
+        /* explicit two-pass softmax over j < i */
+        double m = -INFINITY;
+        for (int64_t j = 0; j < i; ++j) m = ell[j] > m ? ell[j] : m;
+        double d = 0.0;
+        for (int64_t j = 0; j < i; ++j) d += exp(ell[j] - m);
+        for (int64_t j = 0; j < i; ++j) {
+            const double gw = exp(ell[j] - m) / d;
+            for (int p = 0; p < P; ++p) R[p] += gw * V[(size_t)j * P + p];
+        }
+        *lse = m + log(d);
+    }
+    const double zz = z_per_head ? z[((size_t)b * L + t) * H + h] : z[(size_t)b * L + t];
+    const double gate = silu(zz);
+    for (int p = 0; p < P; ++p) y[p] = Y_AT(y_ssd, b, t, h, p) + gate * R[p];
+}
+
+static double* all_inv_rms(int64_t B, int H, int P, int N, int64_t Mcap, int64_t Mused,
+                           double eps, int normalize, const double* mem) {
+    double* rr = (double*)malloc(sizeof(double) * (size_t)B * H * (Mused > 0 ? Mused : 1) * N);
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b)
+        for (int h = 0; h < H; ++h)
+            for (int64_t j = 0; j < Mused; ++j)
+                inv_row_rms(mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P, N, P, eps,
+                            normalize, rr + (((size_t)b * H + h) * Mused + j) * N);
+    return rr;
+}
+
+/*
+ * Full forward SMA + gate over every (b, t, h).  R may be NULL.
+ * Memories 0..ceil(L/S)-1 of `mem` are read (only j < floor(t/S) matter).
+ */
+void dart_oracle_sma(int64_t B, int64_t L, int H, int G, int P, int N, int S, int64_t Mcap,
+                     double eps, int normalize, int z_per_head, const double* q, const double* e,
+                     const double* Cm, const double* qw, const double* ew, const double* mem,
+                     const double* z, const double* y_ssd, double* y, double* lse, double* R) {
+    const int64_t M = (L + S - 1) / S;
+    double* rr = all_inv_rms(B, H, P, N, Mcap, M, eps, normalize, mem);
+#pragma omp parallel
+    {
+        double* work = (double*)malloc(sizeof(double) * ((size_t)N + P + (M + 1) + (size_t)(M + 1) * P));
+        double* Rrow = (double*)malloc(sizeof(double) * P);
+#pragma omp for collapse(2) schedule(dynamic, 1)
+        for (int64_t b = 0; b < B; ++b)
+            for (int h = 0; h < H; ++h)
+                for (int64_t t = 0; t < L; ++t) {
+                    double l;
+                    sma_row(B, L, H, G, P, N, S, Mcap, eps, normalize, z_per_head, q, e, Cm, qw,
+                            ew, mem, rr + ((size_t)b * H + h) * M * N, z, y_ssd, b, t, h, Rrow,
+                            &l, &Y_AT(y, b, t, h, 0), work);
+                    lse[((size_t)b * L + t) * H + h] = l;
+                    if (R)
+                        for (int p = 0; p < P; ++p) Y_AT(R, b, t, h, p) = Rrow[p];
+                }
+        free(work);
+        free(Rrow);
+    }
+    free(rr);
+}
+
+/*
+ * The same definition evaluated only for a list of rows (b, t, h) given as
+ * int64 triples; used to check sampled outputs at sizes where the full
+ * oracle would take too long.  Outputs are packed: y_rows[k][P], lse_rows[k].
+ */
+void dart_oracle_sma_rows(int64_t B, int64_t L, int H, int G, int P, int N, int S, int64_t Mcap,
+                          double eps, int normalize, int z_per_head, const double* q,
+                          const double* e, const double* Cm, const double* qw, const double* ew,
+                          const double* mem, const double* z, const double* y_ssd,
+                          int64_t nrows, const int64_t* rows, double* y_rows, double* lse_rows) {
+    const int64_t M = (L + S - 1) / S;
+#pragma omp parallel
+    {
+        double* work = (double*)malloc(sizeof(double) * ((size_t)N + P + (M + 1) + (size_t)(M + 1) * P));
+        double* Rrow = (double*)malloc(sizeof(double) * P);
+        double* rr = (double*)malloc(sizeof(double) * (size_t)(M > 0 ? M : 1) * N);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t k = 0; k < nrows; ++k) {
+            const int64_t b = rows[3 * k], t = rows[3 * k + 1];
+            const int h = (int)rows[3 * k + 2];
+            const int64_t i = t / S;
+            for (int64_t j = 0; j < i; ++j)
+                inv_row_rms(mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P, N, P, eps,
+                            normalize, rr + (size_t)j * N);
+            sma_row(B, L, H, G, P, N, S, Mcap, eps, normalize, z_per_head, q, e, Cm, qw, ew, mem,
+                    rr, z, y_ssd, b, t, h, Rrow, &lse_rows[k], y_rows + (size_t)k * P, work);
+        }
+        free(work);
+        free(Rrow);
+        free(rr);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Autoregressive decode step for token `pos` (0-based) of every sequence.   */
+/* x [B][H][P], dt [B][H], Bm/Cm/q [B][G][N], e [B][G][P], z [B][H] or [B].  */
+/* h_state, chunk_acc [B][H][N][P] and mem [B][Mcap][H][N][P] are in/out;    */
+/* y [B][H][P] is out.                                                       */
+/* ------------------------------------------------------------------------ */
+int dart_oracle_decode_step(int64_t B, int H, int G, int P, int N, int S, int64_t Mcap,
+                            int64_t pos, double eps, int normalize, int z_per_head,
+                            const double* x, const double* dt, const double* A,
+                            const double* Bm, const double* Cm, const double* q, const double* e,
+                            const double* qw, const double* ew, const double* z,
+                            double* h_state, double* chunk_acc, double* mem, double* y) {
+    const int64_t m = pos / S; /* completed chunks before this token's chunk */
+    if (pos < 0 || m > Mcap || (pos % S == S - 1 && m >= Mcap)) return 1; /* no room */
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b) {
+        for (int h = 0; h < H; ++h) {
+            const int g = group_of(h, H, G);
+            const double d = dt[(size_t)b * H + h];
+            const double a = exp(d * A[h]);
+            const double* xb = x + ((size_t)b * H + h) * P;
+            const double* bb = Bm + ((size_t)b * G + g) * N;
+            const double* cb = Cm + ((size_t)b * G + g) * N;
+            const double* qb = q + ((size_t)b * G + g) * N;
+            const double* eb = e + ((size_t)b * G + g) * P;
+            double* hs = h_state + ((size_t)b * H + h) * (size_t)N * P;
+            double* ca = chunk_acc + ((size_t)b * H + h) * (size_t)N * P;
+            double* yb = y + ((size_t)b * H + h) * P;
+            /* 1. a new chunk starts with an empty running contribution */
+            if (pos % S == 0)
+                for (size_t k = 0; k < (size_t)N * P; ++k) ca[k] = 0.0;
+            /* 2. recurrent state and running chunk contribution */
+            for (int n = 0; n < N; ++n)
+                for (int p = 0; p < P; ++p) {
+                    const double u = d * bb[n] * xb[p];
+                    hs[(size_t)n * P + p] = a * hs[(size_t)n * P + p] + u;
+                    ca[(size_t)n * P + p] = a * ca[(size_t)n * P + p] + u;
+                }
+            /* 3. SSM readout C_t H_t */
+            double* ysd = (double*)malloc(sizeof(double) * P);
+            for (int p = 0; p < P; ++p) {
+                double acc = 0.0;
+                for (int n = 0; n < N; ++n) acc += cb[n] * hs[(size_t)n * P + p];
+                ysd[p] = acc;
+            }
+            /* 4. SMA over the m cached memories (explicit two-pass softmax) */
+            double* R = (double*)calloc((size_t)P, sizeof(double));
+            if (m > 0) {
+                double* qbar = (double*)malloc(sizeof(double) * N);
+                double* ebar = (double*)malloc(sizeof(double) * P);
+                double* ell = (double*)malloc(sizeof(double) * m);
+                double* V = (double*)malloc(sizeof(double) * (size_t)m * P);
+                double* r = (double*)malloc(sizeof(double) * N);
+                if (normalize) {
+                    rms_normalise(qb, N, eps, qw, qbar);
+                    rms_normalise(eb, P, eps, ew, ebar);
+                } else {
+                    for (int n = 0; n < N; ++n) qbar[n] = qb[n];
+                    for (int p = 0; p < P; ++p) ebar[p] = eb[p];
+                }
+                for (int64_t j = 0; j < m; ++j) {
+                    const double* dH = mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+                    inv_row_rms(dH, N, P, eps, normalize, r);
+                    double l = 0.0;
+                    for (int n = 0; n < N; ++n) {
+                        double k = 0.0;
+                        for (int p = 0; p < P; ++p) k += dH[(size_t)n * P + p] * ebar[p];
+                        l += qbar[n] * (r[n] * k);
+                    }
+                    ell[j] = l / sqrt((double)N);
+                    for (int p = 0; p < P; ++p) {
+                        double v = 0.0;
+                        for (int n = 0; n < N; ++n) v += cb[n] * dH[(size_t)n * P + p];
+                        V[(size_t)j * P + p] = v;
+                    }
+                }
+                double mx = -INFINITY;
+                for (int64_t j = 0; j < m; ++j) mx = ell[j] > mx ? ell[j] : mx;
+                double den = 0.0;
+                for (int64_t j = 0; j < m; ++j) den += exp(ell[j] - mx);
+                for (int64_t j = 0; j < m; ++j) {
+                    const double gw = exp(ell[j] - mx) / den;
+                    for (int p = 0; p < P; ++p) R[p] += gw * V[(size_t)j * P + p];
+                }
+                free(qbar);
+                free(ebar);
+                free(ell);
+                free(V);
+                free(r);
+            }
+            /* 5. gate */
+            const double zz = z_per_head ? z[(size_t)b * H + h] : z[b];
+            const double gate = silu(zz);
+            for (int p = 0; p < P; ++p) yb[p] = ysd[p] + gate * R[p];
+            free(ysd);
+            free(R);
+            /* 6. the token closes its chunk: the running contribution becomes memory m */
+            if (pos % S == S - 1) {
+                double* dst = mem + (((size_t)b * Mcap + m) * H + h) * (size_t)N * P;
+                for (size_t k = 0; k < (size_t)N * P; ++k) dst[k] = ca[k];
+            }
+        }
+    }
+    return 0;
+}

@@ -1,0 +1,464 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these checks re-types the oracle's own formula: each compares the
+oracle with an independent route to the same quantity (the SSD dual
+"masked attention" form, the chunk-boundary identity of App. A, degenerate
+chunk sizes, softmax closed forms, invariances of the normalisation, the
+decode path against the forward path, hand-computed scalars) so that a
+dropped term, a wrong sign or index, or a transposed operand in the oracle
+fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_02032_amd import synth
+
+
+def tiny_inputs(B=1, L=24, H=2, G=1, P=5, N=4, seed=0, scale_dt=1.0):
+    rng = np.random.default_rng(seed)
+    A = -np.exp(rng.uniform(0.0, math.log(16.0), size=H))
+    dt = rng.uniform(1e-3, 0.3, size=(B, L, H)) * scale_dt
+    x = rng.standard_normal((B, L, H, P))
+    Bm = rng.standard_normal((B, L, G, N)) / math.sqrt(N)
+    Cm = rng.standard_normal((B, L, G, N)) / math.sqrt(N)
+    q = rng.standard_normal((B, L, G, N))
+    e = rng.standard_normal((B, L, G, P))
+    z = rng.standard_normal((B, L, H))
+    return dict(A=A, dt=dt, x=x, Bm=Bm, Cm=Cm, q=q, e=e, z=z)
+
+
+def masked_attention_form(x, dt, A, Bm, Cm, h0=None):
+    """SSD dual form (Sec. 2): Y = (L_SSD o C B^T)(dt X), with
+    (L_SSD)_ij = prod_{k=j+1}^{i} a_k for i >= j, plus the decayed initial state."""
+    B_, L, H, P = x.shape
+    G = Bm.shape[2]
+    y = np.zeros_like(x)
+    for b in range(B_):
+        for h in range(H):
+            g = h * G // H
+            loga = dt[b, :, h] * A[h]
+            cum = np.cumsum(loga)
+            Lmask = np.tril(np.exp(cum[:, None] - cum[None, :]))
+            CB = Cm[b, :, g, :] @ Bm[b, :, g, :].T
+            y[b, :, h, :] = (Lmask * CB) @ (dt[b, :, h][:, None] * x[b, :, h, :])
+            if h0 is not None:
+                y[b, :, h, :] += np.exp(cum)[:, None] * (Cm[b, :, g, :] @ h0[b, h])
+    return y
+
+
+def chunked_form(x, dt, A, Bm, Cm, S):
+    """App. A chunked decomposition: H_[c] = decay * H_[c-1] + dH_[c];
+    Y = Y_intra + C_t A_{a_c:t} H_[c-1]; returns (y, dH per chunk, h_last)."""
+    B_, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    M = -(-L // S)
+    y = np.zeros_like(x)
+    mem = np.zeros((B_, M, H, N, P))
+    hl = np.zeros((B_, H, N, P))
+    for b in range(B_):
+        for h in range(H):
+            g = h * G // H
+            Hprev = np.zeros((N, P))
+            for c in range(M):
+                s0, s1 = c * S, min((c + 1) * S, L)
+                la = dt[b, s0:s1, h] * A[h]
+                cs = np.cumsum(la)
+                Xc = dt[b, s0:s1, h][:, None] * x[b, s0:s1, h, :]
+                Bc, Cc = Bm[b, s0:s1, g, :], Cm[b, s0:s1, g, :]
+                Lm = np.tril(np.exp(cs[:, None] - cs[None, :]))
+                y[b, s0:s1, h, :] = (Lm * (Cc @ Bc.T)) @ Xc + (np.exp(cs)[:, None] * Cc) @ Hprev
+                dH = (Bc * np.exp(cs[-1] - cs)[:, None]).T @ Xc
+                mem[b, c, h] = dH
+                Hprev = np.exp(cs[-1]) * Hprev + dH
+            hl[b, h] = Hprev
+    return y, mem, hl
+
+
+# --------------------------------------------------------------------------- #
+# Scan: recurrence (C-1) and memories (C-2)
+# --------------------------------------------------------------------------- #
+
+def test_recurrence_hand_computed_scalar():
+    # N = P = 1, L = 3: H_t = exp(dt_t A) H_{t-1} + dt_t B_t x_t, y_t = C_t H_t.
+    x = np.array([1.0, 2.0, 3.0]).reshape(1, 3, 1, 1)
+    dt = np.array([0.5, 0.25, 0.1]).reshape(1, 3, 1)
+    A = np.array([-1.0])
+    Bm = np.array([1.0, -2.0, 0.5]).reshape(1, 3, 1, 1)
+    Cm = np.array([2.0, 1.0, -1.0]).reshape(1, 3, 1, 1)
+    h1 = 0.5 * 1.0 * 1.0
+    h2 = math.exp(-0.25) * h1 + 0.25 * (-2.0) * 2.0
+    h3 = math.exp(-0.1) * h2 + 0.1 * 0.5 * 3.0
+    y, hl = oracle.ssd_recurrence(x, dt, A, Bm, Cm)
+    np.testing.assert_allclose(y.ravel(), [2.0 * h1, 1.0 * h2, -1.0 * h3], rtol=0, atol=1e-15)
+    assert hl.ravel()[0] == pytest.approx(h3, abs=1e-15)
+
+
+@pytest.mark.parametrize("L,S", [(24, 8), (23, 8), (17, 5)])
+def test_ssd_duality_recurrence_equals_masked_attention_and_chunked(L, S):
+    """Pin C-P1: recurrence == masked attention form == chunked decomposition."""
+    d = tiny_inputs(B=2, L=L, H=3, G=1, P=5, N=4, seed=L * 31 + S)
+    y_rec, hl = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"])
+    y_dual = masked_attention_form(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"])
+    y_chk, mem_chk, hl_chk = chunked_form(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], S)
+    np.testing.assert_allclose(y_rec, y_dual, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(y_rec, y_chk, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(hl, hl_chk, rtol=0, atol=1e-12)
+    mem = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], S)
+    np.testing.assert_allclose(mem, mem_chk, rtol=0, atol=1e-12)
+
+
+def test_recurrence_initial_state_matches_dual_form():
+    d = tiny_inputs(B=1, L=16, H=2, P=3, N=4, seed=5)
+    rng = np.random.default_rng(9)
+    h0 = rng.standard_normal((1, 2, 4, 3))
+    y_rec, _ = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], h0=h0)
+    y_dual = masked_attention_form(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], h0=h0)
+    np.testing.assert_allclose(y_rec, y_dual, rtol=0, atol=1e-12)
+
+
+def test_grouped_projections_head_to_group_map():
+    # H = 4 heads, G = 2 groups: heads 0,1 read group 0; heads 2,3 read group 1.
+    d = tiny_inputs(B=1, L=12, H=4, G=2, P=3, N=4, seed=3)
+    y, _ = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"])
+    y_dual = masked_attention_form(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"])
+    np.testing.assert_allclose(y, y_dual, rtol=0, atol=1e-12)
+    # swapping group 1's data must change heads 2,3 only
+    Bm2 = d["Bm"].copy()
+    Bm2[:, :, 1] = np.random.default_rng(1).standard_normal(Bm2[:, :, 1].shape)
+    y2, _ = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], Bm2, d["Cm"])
+    np.testing.assert_array_equal(y2[:, :, :2], y[:, :, :2])
+    assert np.abs(y2[:, :, 2:] - y[:, :, 2:]).max() > 1e-3
+
+
+@pytest.mark.parametrize("L,S", [(24, 8), (22, 8), (9, 3)])
+def test_memories_equal_boundary_state_differences(L, S):
+    """Pin C-P2: dH_[c] == H_[c] - A_{a_c:b_c} H_[c-1] (App. A, chunk-state
+    equation) with boundary states from the recurrence run on prefixes, and
+    H_[c] == sum_{c'<=c} A_{e(c')+1:e(c)} dH_[c']."""
+    d = tiny_inputs(B=1, L=L, H=2, P=4, N=3, seed=L + 7 * S)
+    mem = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], S)
+    M = -(-L // S)
+    prev = np.zeros((1, 2, 3, 4))
+    ends = [min((c + 1) * S, L) for c in range(M)]
+    for c, end in enumerate(ends):
+        sl = slice(0, end)
+        _, Hc = oracle.ssd_recurrence(d["x"][:, sl], d["dt"][:, sl], d["A"], d["Bm"][:, sl],
+                                      d["Cm"][:, sl])
+        start = c * S
+        decay = np.exp((d["dt"][0, start:end, :] * d["A"][None, :]).sum(axis=0))  # per head
+        np.testing.assert_allclose(mem[0, c], Hc[0] - decay[:, None, None] * prev[0],
+                                   rtol=0, atol=1e-12)
+        # H_[c] as a decayed sum of the memories so far
+        acc = np.zeros_like(prev[0])
+        for cp in range(c + 1):
+            e_cp = ends[cp]
+            dec = np.exp((d["dt"][0, e_cp:end, :] * d["A"][None, :]).sum(axis=0))
+            acc += dec[:, None, None] * mem[0, cp]
+        np.testing.assert_allclose(acc, Hc[0], rtol=0, atol=1e-12)
+        prev = Hc
+
+
+def test_memory_S_equals_L_is_final_state():
+    """Pin C-P3 (scan half): one chunk covering the sequence: dH_[1] == H_{L-1}."""
+    d = tiny_inputs(B=2, L=20, H=2, P=4, N=3, seed=2)
+    mem = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], 20)
+    _, hl = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"])
+    assert mem.shape[1] == 1
+    np.testing.assert_allclose(mem[:, 0], hl, rtol=0, atol=1e-12)
+
+
+def test_memory_S_equals_one_is_rank_one_write():
+    """Pin C-P4: with S = 1 every memory is dt_t B_t^T x_t (empty decay product)."""
+    d = tiny_inputs(B=1, L=6, H=2, P=4, N=3, seed=4)
+    mem = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], 1)
+    for t in range(6):
+        for h in range(2):
+            want = d["dt"][0, t, h] * np.outer(d["Bm"][0, t, 0], d["x"][0, t, h])
+            np.testing.assert_allclose(mem[0, t, h], want, rtol=0, atol=1e-15)
+
+
+def test_memory_underflowing_decay_is_finite():
+    # strong decay within a chunk (sum of dt*A far below the float range):
+    # the earliest tokens vanish, nothing becomes NaN or Inf.
+    d = tiny_inputs(B=1, L=16, H=1, P=2, N=2, seed=6)
+    d["A"] = np.array([-16.0])
+    d["dt"] = np.full((1, 16, 1), 50.0)
+    mem = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], 16)
+    assert np.isfinite(mem).all()
+    want = d["dt"][0, -1, 0] * np.outer(d["Bm"][0, -1, 0], d["x"][0, -1, 0])
+    np.testing.assert_allclose(mem[0, 0, 0], want, rtol=1e-12, atol=0)
+
+
+# --------------------------------------------------------------------------- #
+# SMA (C-3) and gate (C-4)
+# --------------------------------------------------------------------------- #
+
+def rand_sma_case(B=1, L=24, H=2, G=1, P=6, N=4, S=6, seed=0, mem_scale=1.0):
+    rng = np.random.default_rng(seed)
+    M = -(-L // S)
+    return dict(
+        q=rng.standard_normal((B, L, G, N)), e=rng.standard_normal((B, L, G, P)),
+        Cm=rng.standard_normal((B, L, G, N)),
+        mem=rng.standard_normal((B, M, H, N, P)) * mem_scale,
+        z=rng.standard_normal((B, L, H)), y_ssd=rng.standard_normal((B, L, H, P)), S=S)
+
+
+def silu(v):
+    return v / (1.0 + np.exp(-v))
+
+
+def test_sma_first_chunk_and_S_equals_L():
+    """Pin C-P3/C-4a: no history -> R = 0, LSE = -inf, y == y_ssd exactly."""
+    c = rand_sma_case(L=12, S=12, seed=1)
+    y, lse, R = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], c["S"],
+                           return_R=True)
+    assert np.all(R == 0.0)
+    assert np.all(np.isneginf(lse))
+    np.testing.assert_array_equal(y, c["y_ssd"])
+    c = rand_sma_case(L=24, S=6, seed=2)
+    y, lse = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], c["S"])
+    np.testing.assert_array_equal(y[:, :6], c["y_ssd"][:, :6])
+    assert np.all(np.isneginf(lse[:, :6])) and np.all(np.isfinite(lse[:, 6:]))
+
+
+def test_sma_second_chunk_reads_single_memory_value():
+    """Pin C-P5: tokens of chunk 1 see one memory: softmax weight 1, so
+    R_t = C_t dH_0 whatever Q and E are."""
+    c = rand_sma_case(L=18, S=6, N=4, P=5, seed=3)
+    _, _, R = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6, return_R=True)
+    for t in range(6, 12):
+        for h in range(2):
+            want = c["Cm"][0, t, 0] @ c["mem"][0, 0, h]
+            np.testing.assert_allclose(R[0, t, h], want, rtol=0, atol=1e-12)
+    # independent of Q and E
+    rng = np.random.default_rng(0)
+    _, _, R2 = oracle.sma(rng.standard_normal(c["q"].shape), rng.standard_normal(c["e"].shape),
+                          c["Cm"], c["mem"], c["z"], c["y_ssd"], 6, return_R=True)
+    np.testing.assert_allclose(R2[:, 6:12], R[:, 6:12], rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("normalize", [True, False])
+def test_sma_zero_query_gives_uniform_average(normalize):
+    """Pin C-P6: Q = 0 -> all logits 0 -> R_t = C_t mean_{j<i} dH_j and LSE = ln i."""
+    c = rand_sma_case(L=30, S=6, seed=4)
+    q0 = np.zeros_like(c["q"])
+    y, lse, R = oracle.sma(q0, c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6,
+                           normalize=normalize, return_R=True)
+    for t in range(6, 30):
+        i = t // 6
+        for h in range(2):
+            want = c["Cm"][0, t, 0] @ c["mem"][0, :i, h].mean(axis=0)
+            np.testing.assert_allclose(R[0, t, h], want, rtol=0, atol=1e-12)
+            assert lse[0, t, h] == pytest.approx(math.log(i), abs=1e-13)
+            np.testing.assert_allclose(y[0, t, h], c["y_ssd"][0, t, h] + silu(c["z"][0, t, h]) * want,
+                                       rtol=0, atol=1e-12)
+
+
+def test_sma_two_memories_closed_form_rank_one():
+    """Pin C-P7: rank-one memories dH_j = u_j v_j^T with u_j in {+-1}^N make the
+    normalised logit a closed form, l_j = (Qb . u_j) (v_j . Eb) / (rms(v_j) sqrt(N))
+    (eps -> 0), and the two-memory softmax weight is sigmoid(l_0 - l_1)."""
+    N, P, S = 4, 3, 2
+    rng = np.random.default_rng(11)
+    u0 = np.array([1.0, -1.0, 1.0, 1.0])
+    u1 = np.array([1.0, 1.0, -1.0, 1.0])
+    v0 = np.array([0.3, -1.2, 0.7])
+    v1 = np.array([-0.4, 0.5, 2.0])
+    mem = np.zeros((1, 3, 1, N, P))
+    mem[0, 0, 0] = np.outer(u0, v0)
+    mem[0, 1, 0] = np.outer(u1, v1)
+    L = 6
+    q = rng.standard_normal((1, L, 1, N))
+    e = rng.standard_normal((1, L, 1, P))
+    Cm = rng.standard_normal((1, L, 1, N))
+    z = rng.standard_normal((1, L, 1))
+    y_ssd = np.zeros((1, L, 1, P))
+    eps = 1e-14
+    y, lse, R = oracle.sma(q, e, Cm, mem, z, y_ssd, S, eps=eps, return_R=True)
+    for t in (4, 5):  # chunk 2 sees memories 0 and 1
+        qb = q[0, t, 0] / math.sqrt((q[0, t, 0] ** 2).mean())
+        eb = e[0, t, 0] / math.sqrt((e[0, t, 0] ** 2).mean())
+        l0 = (qb @ u0) * (v0 @ eb) / (math.sqrt((v0 ** 2).mean()) * math.sqrt(N))
+        l1 = (qb @ u1) * (v1 @ eb) / (math.sqrt((v1 ** 2).mean()) * math.sqrt(N))
+        g0 = 1.0 / (1.0 + math.exp(-(l0 - l1)))
+        V0 = (Cm[0, t, 0] @ u0) * v0
+        V1 = (Cm[0, t, 0] @ u1) * v1
+        np.testing.assert_allclose(R[0, t, 0], g0 * V0 + (1 - g0) * V1, rtol=0, atol=1e-10)
+        assert lse[0, t, 0] == pytest.approx(max(l0, l1) + math.log1p(math.exp(-abs(l0 - l1))),
+                                             abs=1e-10)
+
+
+def test_sma_unnormalised_closed_form():
+    """Alg. 1 as printed (normalize = 0): l_j = Q_t dH_j E_t / sqrt(N); two
+    memories: weights sigmoid(l_0 - l_1) (closed form with explicit vectors)."""
+    N, P, S = 3, 2, 3
+    mem = np.zeros((1, 3, 1, N, P))
+    mem[0, 0, 0] = [[1.0, 0.0], [0.0, 2.0], [0.5, 0.5]]
+    mem[0, 1, 0] = [[0.0, -1.0], [1.0, 1.0], [0.0, 0.0]]
+    L = 9
+    q = np.zeros((1, L, 1, N)); q[0, 7, 0] = [1.0, 2.0, -1.0]
+    e = np.zeros((1, L, 1, P)); e[0, 7, 0] = [0.5, -0.25]
+    Cm = np.zeros((1, L, 1, N)); Cm[0, 7, 0] = [1.0, 0.0, 2.0]
+    z = np.zeros((1, L, 1)); z[0, 7, 0] = 1.5
+    y_ssd = np.zeros((1, L, 1, P))
+    y, lse, R = oracle.sma(q, e, Cm, mem, z, y_ssd, S, normalize=False, return_R=True)
+    # l_0 = [1,2,-1] . (dH_0 [0.5,-0.25]) / sqrt(3) = [1,2,-1].[0.5,-0.5,0.125] / sqrt3
+    l0 = (0.5 - 1.0 - 0.125) / math.sqrt(3)
+    l1 = (1 * 0.25 + 2 * 0.25 + (-1) * 0.0) / math.sqrt(3)
+    g0 = 1.0 / (1.0 + math.exp(-(l0 - l1)))
+    V0 = np.array([1.0 + 1.0, 0.0 + 1.0])     # [1,0,2] dH_0
+    V1 = np.array([0.0, -1.0])                # [1,0,2] dH_1
+    np.testing.assert_allclose(R[0, 7, 0], g0 * V0 + (1 - g0) * V1, rtol=0, atol=1e-14)
+    assert lse[0, 7, 0] == pytest.approx(math.log(math.exp(l0) + math.exp(l1)), abs=1e-14)
+    np.testing.assert_allclose(y[0, 7, 0], silu(1.5) * R[0, 7, 0], rtol=0, atol=1e-14)
+
+
+def test_sma_normalisation_invariances():
+    """Pin C-P8 (eps -> 0): logits are invariant under row scaling of a memory
+    (dH_j -> diag(alpha) dH_j, alpha > 0) and under Q -> beta Q, E -> beta E."""
+    c = rand_sma_case(L=24, S=6, seed=5)
+    eps = 1e-15
+    y, lse, R = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6, eps=eps,
+                           return_R=True)
+    y2, lse2, R2 = oracle.sma(3.7 * c["q"], 0.2 * c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6,
+                              eps=eps, return_R=True)
+    np.testing.assert_allclose(lse2, lse, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(R2, R, rtol=0, atol=1e-11)
+    alpha = np.random.default_rng(3).uniform(0.1, 10.0, size=c["mem"].shape[:-1] + (1,))
+    _, lse3 = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"] * alpha, c["z"], c["y_ssd"], 6, eps=eps)
+    np.testing.assert_allclose(lse3, lse, rtol=0, atol=1e-11)
+
+
+def test_sma_permuting_history_leaves_output_unchanged():
+    """Pin C-P9: softmax over a set: permuting the memories of earlier chunks
+    changes nothing for tokens that see all of them."""
+    c = rand_sma_case(L=30, S=6, seed=6)
+    y, lse = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6)
+    perm = [2, 0, 3, 1]
+    mem2 = c["mem"].copy()
+    mem2[:, :4] = c["mem"][:, perm]
+    y2, lse2 = oracle.sma(c["q"], c["e"], c["Cm"], mem2, c["z"], c["y_ssd"], 6)
+    np.testing.assert_allclose(y2[:, 24:], y[:, 24:], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse2[:, 24:], lse[:, 24:], rtol=0, atol=1e-12)
+
+
+def test_online_softmax_recursion_equals_exact_softmax():
+    """App. C: the online recursion m, d, O gives the exact softmax average.
+    Exercised on the oracle's own outputs: feeding the per-memory logits and
+    values the oracle implies (rank-one memories, closed-form logits) through
+    the recursion reproduces the oracle's R and LSE."""
+    N, P = 4, 3
+    rng = np.random.default_rng(21)
+    nm = 5
+    us = rng.choice([-1.0, 1.0], size=(nm, N))
+    vs = rng.standard_normal((nm, P))
+    mem = np.zeros((1, nm + 1, 1, N, P))
+    for j in range(nm):
+        mem[0, j, 0] = np.outer(us[j], vs[j])
+    S, L = 2, 2 * (nm + 1)
+    q = rng.standard_normal((1, L, 1, N)); e = rng.standard_normal((1, L, 1, P))
+    Cm = rng.standard_normal((1, L, 1, N)); z = rng.standard_normal((1, L, 1))
+    _, lse, R = oracle.sma(q, e, Cm, mem, z, np.zeros((1, L, 1, P)), S, eps=1e-14, return_R=True)
+    t = L - 1
+    qb = q[0, t, 0] / math.sqrt((q[0, t, 0] ** 2).mean())
+    eb = e[0, t, 0] / math.sqrt((e[0, t, 0] ** 2).mean())
+    m, d, O = -math.inf, 0.0, np.zeros(P)
+    for j in range(nm):
+        lj = (qb @ us[j]) * (vs[j] @ eb) / (math.sqrt((vs[j] ** 2).mean()) * math.sqrt(N))
+        Vj = (Cm[0, t, 0] @ us[j]) * vs[j]
+        mn = max(m, lj)
+        d = math.exp(m - mn) * d + math.exp(lj - mn)
+        O = math.exp(m - mn) * O + math.exp(lj - mn) * Vj
+        m = mn
+    np.testing.assert_allclose(R[0, t, 0], O / d, rtol=0, atol=1e-10)
+    assert lse[0, t, 0] == pytest.approx(m + math.log(d), abs=1e-10)
+
+
+def test_gate_zero_returns_ssm_output_exactly():
+    """Pin C-P10: z = 0 (W_G zero-initialised) -> SiLU(0) = 0 -> y == y_ssd."""
+    c = rand_sma_case(L=24, S=6, seed=8)
+    y, _ = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], np.zeros_like(c["z"]), c["y_ssd"], 6)
+    np.testing.assert_array_equal(y, c["y_ssd"])
+
+
+def test_gate_per_token_broadcasts_over_heads():
+    c = rand_sma_case(L=18, S=6, H=3, seed=9)
+    zt = c["z"][:, :, 0]
+    y1, _ = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], zt, c["y_ssd"], 6)
+    zh = np.repeat(zt[:, :, None], 3, axis=2)
+    y2, _ = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], zh, c["y_ssd"], 6)
+    np.testing.assert_array_equal(y1, y2)
+
+
+def test_sma_rows_matches_full():
+    c = rand_sma_case(B=2, L=30, S=6, seed=10)
+    y, lse = oracle.sma(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6)
+    rows = np.array([[0, 0, 0], [1, 29, 1], [0, 13, 1], [1, 6, 0]])
+    yr, lr = oracle.sma_rows(c["q"], c["e"], c["Cm"], c["mem"], c["z"], c["y_ssd"], 6, rows)
+    for k, (b, t, h) in enumerate(rows):
+        np.testing.assert_array_equal(yr[k], y[b, t, h])
+        assert (lr[k] == lse[b, t, h]) or (np.isneginf(lr[k]) and np.isneginf(lse[b, t, h]))
+
+
+# --------------------------------------------------------------------------- #
+# Decode (C-5)
+# --------------------------------------------------------------------------- #
+
+@pytest.mark.parametrize("L,S,z_per_head", [(20, 4, True), (19, 5, False)])
+def test_decode_from_empty_cache_reproduces_forward(L, S, z_per_head):
+    """Pin C-P11: stepping the decode path token by token from an empty cache
+    reproduces the forward pass (recurrence + brute-force memories + explicit
+    softmax) at every token, the memories it appends and the final state."""
+    B_, H, G, P, N = 2, 2, 1, 4, 3
+    d = tiny_inputs(B=B_, L=L, H=H, G=G, P=P, N=N, seed=L)
+    z = d["z"] if z_per_head else d["z"][:, :, 0]
+    fwd = oracle.forward(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], d["q"], d["e"], z, S)
+    M = -(-L // S)
+    h_state = np.zeros((B_, H, N, P))
+    chunk_acc = np.zeros((B_, H, N, P))
+    cache = np.zeros((B_, M, H, N, P))
+    for t in range(L):
+        zt = z[:, t] if z_per_head else z[:, t]
+        yt = oracle.decode_step(t, d["x"][:, t], d["dt"][:, t], d["A"], d["Bm"][:, t],
+                                d["Cm"][:, t], d["q"][:, t], d["e"][:, t], zt, h_state,
+                                chunk_acc, cache, S)
+        np.testing.assert_allclose(yt, fwd["y"][:, t], rtol=0, atol=1e-12)
+    full = L // S
+    np.testing.assert_allclose(cache[:, :full], fwd["mem"][:, :full], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(h_state, fwd["h_last"], rtol=0, atol=1e-12)
+    if L % S:
+        # the running contribution of a partial chunk equals its forward memory
+        np.testing.assert_allclose(chunk_acc, fwd["mem"][:, M - 1], rtol=0, atol=1e-12)
+
+
+def test_decode_rejects_overflowing_append():
+    B_, H, P, N, S = 1, 1, 2, 2, 4
+    h = np.zeros((B_, H, N, P)); ca = np.zeros((B_, H, N, P)); mem = np.zeros((B_, 2, H, N, P))
+    args = (np.ones((1, 1, 2)), np.full((1, 1), 0.1), np.array([-1.0]), np.ones((1, 1, 2)),
+            np.ones((1, 1, 2)), np.ones((1, 1, 2)), np.ones((1, 1, 2)), np.zeros((1, 1)))
+    oracle.decode_step(7, *args, h, ca, mem, S)  # closes chunk 1 into slot 1: fits
+    with pytest.raises(ValueError):
+        oracle.decode_step(11, *args, h, ca, mem, S)  # would write slot 2
+
+
+# --------------------------------------------------------------------------- #
+# Input generator sanity (recipe, not method arithmetic)
+# --------------------------------------------------------------------------- #
+
+def test_synth_recipe_ranges_and_bf16_rounding():
+    w = synth.WORKLOADS["tiny_fp32_L512"].with_(seqlen=256, dtype="bf16")
+    d = synth.forward_inputs(w, seed=0)
+    assert d["dt"].min() >= 1e-3 - 1e-9 and d["dt"].max() <= 1e-1 + 1e-9
+    assert np.all(d["A"] < 0) and d["A"].min() >= -16.0 - 1e-5 and d["A"].max() <= -1.0 + 1e-6
+    for k in ("x", "Bm", "Cm", "q", "e", "z"):
+        bits = d[k].view(np.uint32)
+        assert np.all((bits & 0xFFFF) == 0), k
+    a = np.array([1.0, 1.00390625, 1.01171875, -2.5, 3.0e38], dtype=np.float32)
+    r = synth.round_bf16(a)
+    np.testing.assert_array_equal(r[:4], np.array([1.0, 1.0, 1.015625, -2.5], dtype=np.float32))
+    d2 = synth.forward_inputs(w, seed=0)
+    for k in d:
+        np.testing.assert_array_equal(d[k], d2[k])
