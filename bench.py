@@ -1,0 +1,275 @@
+#!/usr/bin/env python3
+"""Benchmark of the DART hot path on one MI355X (gfx950).
+
+One step = the whole hot path over one batch of seeded synthetic inputs that
+are already resident in HBM:
+  forward   chunked SSD scan (k_chunk_state, k_state_pass, k_chunk_out)
+            -> state-memory attention + gated residual (k_sma_prep, k_sma_main)
+            on the L = 8192 workload (batch 4, 32 heads, P = 64, N = 128, S = 256);
+  decode    one token (k_decode_partial, k_decode_finish) for batch 64, 32 heads,
+            N = 128, S = 256 over a 65536-token context (256 cached memories).
+`value` is forward tokens/s (batch * L / forward time).  Per-kernel times come
+from HIP events the library records around every launch on the launch stream
+(dart_profile_*), averaged over the timed steps.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="sweep_L8192_S256_N128")
+    ap.add_argument("--decode-workload", default="decode_B64_ctx65536")
+    ap.add_argument("--no-decode", action="store_true", help="time the forward only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-batches", type=int, default=1,
+                    help="batches of the workload the CPU oracle is timed on")
+    ap.add_argument("--extra-out", default=None,
+                    help="also write per-kernel detail as JSON to this file")
+    return ap.parse_args()
+
+
+# --------------------------------------------------------------------------- #
+# algorithmic work (what the method must compute or move; see the design notes)
+# --------------------------------------------------------------------------- #
+
+def scan_flops(w):
+    B, M, G, H, N, P, S = w.batch, w.nchunks, w.ngroups, w.nheads, w.dstate, w.headdim, w.chunk
+    return B * M * (G * N * S * (S + 1) + H * (P * S * (S + 1) + 4 * S * N * P + 2 * N * P))
+
+
+def scan_bytes(w, esize=2):
+    B, L, H, G, N, P, M = w.batch, w.seqlen, w.nheads, w.ngroups, w.dstate, w.headdim, w.nchunks
+    return (B * L * H * P * esize * 2          # read x, write y_ssd
+            + B * L * H * 4                    # read dt
+            + 2 * B * L * G * N * esize        # read B, C
+            + B * M * H * N * P * esize)       # write the memories
+
+
+def sma_pairs(w):
+    """(token, earlier memory) pairs per (b, h)."""
+    L, S = w.seqlen, w.chunk
+    return sum(max(0, min(L, (i + 1) * S) - i * S) * i for i in range(w.nchunks))
+
+
+def sma_flops(w):
+    return w.batch * w.nheads * 4 * w.dstate * w.headdim * sma_pairs(w)
+
+
+def sma_bytes(w, esize=2):
+    B, L, H, G, N, P, M = w.batch, w.seqlen, w.nheads, w.ngroups, w.dstate, w.headdim, w.nchunks
+    zsz = B * L * H if w.z_per_head else B * L
+    return (B * L * G * (2 * N + P) * esize    # read q, C, e
+            + B * max(M - 1, 0) * H * N * P * esize  # read the attended memories once
+            + zsz * esize                       # read z
+            + B * L * H * P * esize * 2         # read y_ssd, write y
+            + B * L * H * 4)                    # write lse
+
+
+def decode_bytes(d, esize=2):
+    B, H, N, P, G = d.batch, d.nheads, d.dstate, d.headdim, d.ngroups
+    m = d.context // d.chunk
+    return (B * H * m * N * P * esize           # stream every cached memory
+            + 4 * B * H * N * P * 4             # h_state and chunk_acc read + write
+            + B * H * P * esize * 2 + B * G * (3 * N + P) * esize + B * H * 8)
+
+
+# --------------------------------------------------------------------------- #
+
+def cpu_baseline(w, nbatch):
+    """Time the fp64 CPU oracle (as it stands) on `nbatch` batch rows of the
+    workload: recurrence + brute-force memories + explicit-softmax SMA + gate."""
+    import numpy as np
+    import oracle
+    from paper_2608_02032_amd import synth
+    ws = w.with_(batch=nbatch)
+    d = synth.forward_inputs(ws, seed=0)
+    f = {k: np.asarray(v, dtype=np.float64) for k, v in d.items()}
+    t0 = time.perf_counter()
+    oracle.forward(f["x"], f["dt"], f["A"], f["Bm"], f["Cm"], f["q"], f["e"], f["z"], ws.chunk)
+    sec = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    threads = min(threads, nbatch * ws.nheads)  # the oracle parallelises over (b, h)
+    return {"value": nbatch * ws.seqlen / sec, "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d of %d batch rows of %s (all %d heads, L=%d), fp64, %.1f s wall"
+                      % (nbatch, w.batch, w.name, w.nheads, w.seqlen, sec)}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(requested --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_02032_amd import dart, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.WORKLOADS[args.workload]
+    dw = synth.DECODE_WORKLOADS[args.decode_workload]
+    bf = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    # ---- resident inputs, outputs and workspaces --------------------------
+    d = synth.forward_inputs(w, seed=0)
+    T = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
+    for k in ("x", "Bm", "Cm", "q", "e", "z"):
+        T[k] = T[k].to(bf)
+    B, L, H, P, N, S = w.batch, w.seqlen, w.nheads, w.headdim, w.dstate, w.chunk
+    y_ssd = torch.empty((B, L, H, P), dtype=bf, device=dev)
+    mem = torch.empty((B, w.nchunks, H, N, P), dtype=bf, device=dev)
+    h_last = torch.empty((B, H, N, P), dtype=torch.float32, device=dev)
+    y = torch.empty_like(y_ssd)
+    lse = torch.empty((B, L, H), dtype=torch.float32, device=dev)
+    dims = dart.make_dims(B, L, H, P, N, S, w.dtype, w.ngroups)
+    ws_scan = torch.empty(dart.workspace_bytes("scan", dims), dtype=torch.uint8, device=dev)
+    ws_sma = torch.empty(max(1, dart.workspace_bytes("sma", dims)), dtype=torch.uint8, device=dev)
+
+    if not args.no_decode:
+        m = dw.context // dw.chunk
+        cache, _ = synth.torch_device_memories(dw.batch, m + 1, m, dw.nheads, dw.dstate,
+                                               dw.headdim, seed=1, device=dev)
+        g = torch.Generator(device=dev)
+        g.manual_seed(2)
+        h_state = torch.randn((dw.batch, dw.nheads, dw.dstate, dw.headdim), generator=g,
+                              device=dev) * 1e-2
+        chunk_acc = torch.zeros_like(h_state)
+        di = synth.decode_inputs(dw.batch, dw.nheads, dw.headdim, dw.dstate, dw.dtype, seed=3)
+        D = {k: torch.from_numpy(v).to(dev) for k, v in di.items()}
+        for k in ("x", "Bm", "Cm", "q", "e", "z"):
+            D[k] = D[k].to(torch.bfloat16)
+        y_dec = torch.empty_like(D["x"])
+        ddims = dart.make_dims(dw.batch, 0, dw.nheads, dw.headdim, dw.dstate, dw.chunk, dw.dtype,
+                               dw.ngroups, m + 1)
+        ws_dec = torch.empty(dart.workspace_bytes("decode", ddims), dtype=torch.uint8, device=dev)
+        pos = dw.context  # first token after the context: attends all m memories
+
+    stream = torch.cuda.current_stream()
+
+    def forward():
+        dart.ssd_chunk_scan(T["x"], T["dt"], T["A"], T["Bm"], T["Cm"], S, mem=mem, y_ssd=y_ssd,
+                            h_last=h_last, workspace=ws_scan, stream=stream)
+        dart.sma_fwd(T["q"], T["e"], T["Cm"], mem, T["z"], y_ssd, S, y=y, lse=lse,
+                     workspace=ws_sma, stream=stream)
+
+    def decode():
+        dart.decode_step(pos, D["x"], D["dt"], D["A"], D["Bm"], D["Cm"], D["q"], D["e"], D["z"],
+                         h_state, chunk_acc, cache, dw.chunk, y=y_dec, workspace=ws_dec,
+                         stream=stream)
+
+    for _ in range(args.warmup):
+        forward()
+        if not args.no_decode:
+            decode()
+    torch.cuda.synchronize()
+
+    # ---- timed region --------------------------------------------------------
+    dart.profile_reset()
+    dart.profile_enable(True)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        forward()
+        ev[k][1].record(stream)
+        if not args.no_decode:
+            decode()
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    dart.profile_enable(False)
+    kernels = dart.profile_read(reset=True)
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    dec_ms = [e[1].elapsed_time(e[2]) for e in ev]
+    step_ms = [e[0].elapsed_time(e[2]) for e in ev]
+    fwd_mean = sum(fwd_ms) / len(fwd_ms)
+    ms_per_step = sum(step_ms) / len(step_ms)
+    avg = {k: v[0] / max(v[1], 1) for k, v in kernels.items()}  # ms per launch
+
+    # ---- rooflines -----------------------------------------------------------
+    sflops, sbytes = scan_flops(w), scan_bytes(w)
+    mflops, mbytes = sma_flops(w), sma_bytes(w)
+    scan_ms = sum(avg.get(k, 0.0) for k in ("k_chunk_state", "k_state_pass", "k_chunk_out"))
+    sma_ms = sum(avg.get(k, 0.0) for k in ("k_sma_prep", "k_sma_main"))
+    main_ms = avg["k_sma_main"]
+    main_tflops = mflops / (main_ms * 1e-3) / 1e12
+    roofline = {"kernel": "k_sma_main", "bound": "mfma",
+                "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "avg_us": round(main_ms * 1e3, 2),
+                "algorithmic_flops_per_launch": mflops}
+    extra = {
+        "mfma_util": {"scan": round(sflops / (scan_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                      "sma": round(mflops / (sma_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
+        "scan": {"us": round(scan_ms * 1e3, 2), "hbm_gbps": round(sbytes / (scan_ms * 1e-3) / 1e9, 1),
+                 "hbm_frac": round(sbytes / (scan_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+                 "algorithmic_bytes": sbytes, "algorithmic_flops": sflops},
+        "sma": {"us": round(sma_ms * 1e3, 2), "algorithmic_flops": mflops, "algorithmic_bytes": mbytes},
+        "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(avg.items())},
+    }
+    if not args.no_decode:
+        dbytes = decode_bytes(dw)
+        dec_mean = sum(dec_ms) / len(dec_ms)
+        part_ms = avg["k_decode_partial"]
+        cache_bytes = dw.batch * dw.nheads * (dw.context // dw.chunk) * dw.dstate * dw.headdim * 2
+        extra["decode"] = {
+            "workload": dw.name, "us_per_step": round(dec_mean * 1e3, 2),
+            "hbm_gbps": round(dbytes / (dec_mean * 1e-3) / 1e9, 1),
+            "hbm_frac": round(dbytes / (dec_mean * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+            "algorithmic_bytes": dbytes,
+            "k_decode_partial_gbps": round(cache_bytes / (part_ms * 1e-3) / 1e9, 1)}
+
+    tokens = B * L
+    line = {
+        "metric": "DART layer fwd tokens/s @L=8192 bf16 + MFMA util %; decode step us & HBM GB/s",
+        "value": round(tokens / (fwd_mean * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "seq_len": L, "heads": H, "headdim": P,
+                   "dstate": N, "chunk": S, "fwd_ms": round(fwd_mean, 4),
+                   "decode_workload": None if args.no_decode else dw.name,
+                   "step": "scan+sma+gate forward" + ("" if args.no_decode else " + one decode token")},
+        "roofline": roofline,
+    }
+    line.update(extra)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_batches)
+    line["wall_s_timed"] = round(wall, 3)
+    if args.extra_out:
+        with open(args.extra_out, "w") as fh:
+            json.dump({"fwd_ms": fwd_ms, "dec_ms": dec_ms, "kernels": kernels}, fh, indent=1)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -192,6 +192,25 @@ int64_t dart_decode_cache_elems(const dart_dims* dims, int64_t context);
 const char* dart_status_string(dart_status status);
 const char* dart_last_error(void);
 
+/*
+ * Optional kernel timing (a tracing aid, off by default).  While enabled,
+ * every kernel the library launches is bracketed by two HIP events recorded
+ * on the stream it is launched on.  dart_profile_flush() waits for the
+ * pending events and adds each kernel's elapsed time to a per-kernel total;
+ * the totals are read by index (0 .. dart_profile_count()-1) and cleared by
+ * dart_profile_reset().  Events are created on first use and kept for reuse
+ * until dart_profile_reset(); this is the only state the library keeps, and
+ * these functions are not thread-safe.  dart_profile_flush() returns
+ * DART_ERR_HIP if an event query fails.
+ */
+dart_status dart_profile_enable(int enable);
+dart_status dart_profile_flush(void);
+int dart_profile_count(void);
+const char* dart_profile_name(int index);     /* kernel name, or NULL */
+double dart_profile_total_ms(int index);      /* summed elapsed ms */
+int64_t dart_profile_launches(int index);     /* number of timed launches */
+void dart_profile_reset(void);
+
 #ifdef __cplusplus
 }
 #endif

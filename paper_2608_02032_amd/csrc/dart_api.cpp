@@ -1,0 +1,230 @@
+// dart_api.cpp -- the C ABI of libdart.so (declared in include/dart.h):
+// argument validation on the host, workspace sizing, dispatch to the kernel
+// launchers, status codes and a per-thread error message.  Nothing here
+// allocates device memory or keeps state between calls.
+#include "dart.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "dart_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+dart_status fail(dart_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+dart_status ok() {
+    g_err[0] = '\0';
+    return DART_OK;
+}
+
+// Checks shared by every entry point; fills `s` on success.
+dart_status make_shape(const dart_dims* d, bool need_seqlen, dart::Shape& s) {
+    if (!d) return fail(DART_ERR_INVALID_ARG, "dims is NULL");
+    if (d->batch < 1) return fail(DART_ERR_INVALID_ARG, "batch must be >= 1 (got %lld)", (long long)d->batch);
+    if (need_seqlen && d->seqlen < 1)
+        return fail(DART_ERR_INVALID_ARG, "seqlen must be >= 1 (got %lld)", (long long)d->seqlen);
+    if (d->nheads < 1 || d->ngroups < 1)
+        return fail(DART_ERR_INVALID_ARG, "nheads and ngroups must be >= 1");
+    if (d->nheads % d->ngroups != 0)
+        return fail(DART_ERR_INVALID_ARG, "nheads (%d) must be a multiple of ngroups (%d)", d->nheads, d->ngroups);
+    if (d->headdim < 1 || d->dstate < 1 || d->chunk < 1)
+        return fail(DART_ERR_INVALID_ARG, "headdim, dstate and chunk must be >= 1");
+    if (d->dtype != DART_FP32 && d->dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", d->dtype);
+    if (d->mem_capacity < 0) return fail(DART_ERR_INVALID_ARG, "mem_capacity must be >= 0");
+    if (d->headdim != 64)
+        return fail(DART_ERR_UNSUPPORTED, "headdim %d not supported (this build has kernels for 64)", d->headdim);
+    if (d->dstate != 32 && d->dstate != 64 && d->dstate != 128)
+        return fail(DART_ERR_UNSUPPORTED, "dstate %d not supported (32, 64 or 128)", d->dstate);
+    if (d->chunk != 64 && d->chunk != 128 && d->chunk != 256)
+        return fail(DART_ERR_UNSUPPORTED, "chunk %d not supported (64, 128 or 256)", d->chunk);
+    if (d->batch > 65535 || d->nheads > 65535)
+        return fail(DART_ERR_UNSUPPORTED, "batch and nheads must be <= 65535");
+    s.B = d->batch;
+    s.L = need_seqlen ? d->seqlen : 0;
+    s.H = d->nheads;
+    s.G = d->ngroups;
+    s.P = d->headdim;
+    s.N = d->dstate;
+    s.S = d->chunk;
+    s.M = need_seqlen ? (s.L + s.S - 1) / s.S : 0;
+    s.Mcap = d->mem_capacity ? d->mem_capacity : s.M;
+    s.dtype = d->dtype;
+    if (need_seqlen && s.Mcap < s.M)
+        return fail(DART_ERR_INVALID_ARG, "mem_capacity %lld < ceil(L/S) = %lld", (long long)s.Mcap,
+                    (long long)s.M);
+    if (need_seqlen && s.M > 2147483647LL) return fail(DART_ERR_UNSUPPORTED, "too many chunks");
+    return DART_OK;
+}
+
+dart_status check_opts(const dart_sma_opts* o) {
+    if (!o) return fail(DART_ERR_INVALID_ARG, "opts is NULL");
+    if (o->normalize != 0 && o->normalize != 1) return fail(DART_ERR_INVALID_ARG, "normalize must be 0 or 1");
+    if (o->z_per_head != 0 && o->z_per_head != 1) return fail(DART_ERR_INVALID_ARG, "z_per_head must be 0 or 1");
+    if (o->normalize && !(o->eps > 0.0f)) return fail(DART_ERR_INVALID_ARG, "eps must be > 0 when normalize = 1");
+    if (!(o->eps >= 0.0f)) return fail(DART_ERR_INVALID_ARG, "eps must be >= 0");
+    return DART_OK;
+}
+
+dart_status hip_status(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(DART_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+#define REQUIRE_PTR(p) \
+    if (!(p)) return fail(DART_ERR_INVALID_ARG, "required pointer '%s' is NULL", #p)
+
+}  // namespace
+
+extern "C" {
+
+size_t dart_scan_workspace_bytes(const dart_dims* dims) {
+    dart::Shape s;
+    if (make_shape(dims, true, s) != DART_OK) return 0;
+    return dart::scan_workspace_bytes(s);
+}
+
+dart_status dart_ssd_chunk_scan(const dart_dims* dims, const void* x, const float* dt,
+                                const float* A, const void* Bm, const void* Cm, const float* h0,
+                                void* y_ssd, void* mem, float* h_last, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, true, s);
+    if (st != DART_OK) return st;
+    REQUIRE_PTR(x);
+    REQUIRE_PTR(dt);
+    REQUIRE_PTR(A);
+    REQUIRE_PTR(Bm);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(y_ssd);
+    REQUIRE_PTR(mem);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::scan_workspace_bytes(s);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return hip_status(dart::launch_scan(s, x, dt, A, Bm, Cm, h0, y_ssd, mem, h_last, workspace,
+                                        (hipStream_t)stream),
+                      "dart_ssd_chunk_scan launch");
+}
+
+size_t dart_sma_workspace_bytes(const dart_dims* dims) {
+    dart::Shape s;
+    if (make_shape(dims, true, s) != DART_OK) return 0;
+    return dart::sma_workspace_bytes(s);
+}
+
+dart_status dart_sma_fwd(const dart_dims* dims, const dart_sma_opts* opts, const void* q,
+                         const void* e, const void* Cm, const void* mem, const void* z,
+                         const void* y_ssd, void* y, float* lse, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, true, s);
+    if (st != DART_OK) return st;
+    st = check_opts(opts);
+    if (st != DART_OK) return st;
+    REQUIRE_PTR(q);
+    REQUIRE_PTR(e);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(mem);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(y_ssd);
+    REQUIRE_PTR(y);
+    const size_t need = dart::sma_workspace_bytes(s);
+    if (need > 0 && !workspace) return fail(DART_ERR_INVALID_ARG, "required pointer 'workspace' is NULL");
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    if (y != y_ssd) {
+        // partial overlap between y and y_ssd is not allowed (exact aliasing is)
+        const size_t bytes = (size_t)s.B * s.L * s.H * s.P * dart::elem_bytes(s.dtype);
+        const char* a0 = (const char*)y;
+        const char* b0 = (const char*)y_ssd;
+        if (a0 < b0 + bytes && b0 < a0 + bytes)
+            return fail(DART_ERR_INVALID_ARG, "y partially overlaps y_ssd (only exact aliasing is allowed)");
+    }
+    dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
+    return hip_status(dart::launch_sma(s, a, q, e, Cm, mem, z, y_ssd, y, lse, workspace,
+                                       (hipStream_t)stream),
+                      "dart_sma_fwd launch");
+}
+
+size_t dart_decode_workspace_bytes(const dart_dims* dims) {
+    dart::Shape s;
+    if (make_shape(dims, false, s) != DART_OK) return 0;
+    if (s.Mcap < 1) return 0;
+    return dart::decode_workspace_bytes(s);
+}
+
+dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, int64_t pos,
+                             const void* x, const float* dt, const float* A, const void* Bm,
+                             const void* Cm, const void* q, const void* e, const void* z,
+                             float* h_state, float* chunk_acc, void* mem_cache, void* y,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, false, s);
+    if (st != DART_OK) return st;
+    st = check_opts(opts);
+    if (st != DART_OK) return st;
+    if (s.Mcap < 1) return fail(DART_ERR_INVALID_ARG, "decode needs mem_capacity >= 1");
+    if (pos < 0) return fail(DART_ERR_INVALID_ARG, "pos must be >= 0 (got %lld)", (long long)pos);
+    const int64_t m = pos / s.S;
+    if (m > s.Mcap)
+        return fail(DART_ERR_INVALID_ARG, "pos %lld needs %lld cached memories > capacity %lld",
+                    (long long)pos, (long long)m, (long long)s.Mcap);
+    if (pos % s.S == s.S - 1 && m >= s.Mcap)
+        return fail(DART_ERR_INVALID_ARG, "pos %lld closes chunk %lld but the cache holds %lld memories",
+                    (long long)pos, (long long)m, (long long)s.Mcap);
+    REQUIRE_PTR(x);
+    REQUIRE_PTR(dt);
+    REQUIRE_PTR(A);
+    REQUIRE_PTR(Bm);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(q);
+    REQUIRE_PTR(e);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(h_state);
+    REQUIRE_PTR(chunk_acc);
+    REQUIRE_PTR(mem_cache);
+    REQUIRE_PTR(y);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::decode_workspace_bytes(s);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
+    return hip_status(dart::launch_decode(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc,
+                                          mem_cache, y, workspace, (hipStream_t)stream),
+                      "dart_decode_step launch");
+}
+
+int64_t dart_decode_cache_elems(const dart_dims* dims, int64_t context) {
+    if (!dims || context < 0 || dims->batch < 1 || dims->nheads < 1 || dims->headdim < 1 ||
+        dims->dstate < 1 || dims->chunk < 1)
+        return 0;
+    const int64_t mems = (context + dims->chunk - 1) / dims->chunk;
+    return dims->batch * mems * dims->nheads * (int64_t)dims->dstate * dims->headdim;
+}
+
+const char* dart_status_string(dart_status status) {
+    switch (status) {
+        case DART_OK: return "DART_OK";
+        case DART_ERR_INVALID_ARG: return "DART_ERR_INVALID_ARG";
+        case DART_ERR_UNSUPPORTED: return "DART_ERR_UNSUPPORTED";
+        case DART_ERR_HIP: return "DART_ERR_HIP";
+    }
+    return "DART_ERR_UNKNOWN";
+}
+
+const char* dart_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// dart_internal.hpp -- launcher interface between the C ABI layer and the
+// kernels.  Shapes are validated by the caller; launchers only enqueue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dart {
+
+struct Shape {
+    int64_t B, L;
+    int H, G, P, N, S;
+    int64_t M;     // ceil(L/S)
+    int64_t Mcap;  // memory slots
+    int dtype;     // 0 fp32, 1 bf16
+};
+
+// Workspace carve-up of the scan: per-chunk log decay [B][H][M] (float) and the
+// chunk-entry states [B][M][H][N][P] (storage dtype).
+size_t scan_workspace_bytes(const Shape& s);
+hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const float* A,
+                       const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
+                       float* h_last, void* ws, hipStream_t st);
+
+struct SmaArgs {
+    float eps;
+    const float* qw;
+    const float* ew;
+    int normalize;
+    int z_per_head;
+};
+
+// Workspace of the SMA forward: decoded-operand copies of memories 0..M-2
+// (key side scaled by the inverse row RMS, value side as stored), both in the
+// MFMA operand order, storage dtype.
+size_t sma_workspace_bytes(const Shape& s);
+hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                      const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
+                      float* lse, void* ws, hipStream_t st);
+
+// Decode: per-split partial softmax statistics [B][H][nsplit][P+2] (float).
+constexpr int kDecodeMemPerSplit = 16;
+size_t decode_workspace_bytes(const Shape& s);
+hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
+                         const float* dt, const float* A, const void* Bm, const void* Cm,
+                         const void* q, const void* e, const void* z, float* h_state,
+                         float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st);
+
+// Optional per-kernel timing (see dart_profile_* in dart.h).  Launchers
+// bracket each kernel launch with prof_begin/prof_end; both are no-ops unless
+// profiling is enabled.
+void prof_begin(const char* kernel, hipStream_t st);
+void prof_end(hipStream_t st);
+
+inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+inline size_t elem_bytes(int dtype) { return dtype == 1 ? 2 : 4; }
+
+}  // namespace dart

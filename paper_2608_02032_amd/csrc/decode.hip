@@ -1,0 +1,286 @@
+// decode.hip -- single-token decode step over the cached chunk memories.
+//
+// Paper: Sec. 4 "Inference Cache" (the decode cache is one N x P memory per
+// completed chunk plus the recurrent state), Sec. 3 (SMA over strictly earlier
+// chunks, gated residual) and App. B.1 (normalised score branch).  Keys depend
+// on the current token (K = r (.) (dH E_t)), so every step re-reads every
+// cached memory: the step is a stream over B*H*m*N*P storage elements and is
+// bound by HBM bandwidth.
+//
+//   k_decode_partial  grid (split, head, batch): each block streams up to
+//                     kDecodeMemPerSplit memories (one wave per memory at a
+//                     time, lanes own 8 consecutive p of N/8 rows), computes
+//                     r, the logit and C dH on the fly and keeps an online
+//                     softmax (m, d, O[P]); waves are merged in LDS and one
+//                     partial per split goes to the workspace.
+//   k_decode_finish   grid (head, batch): recurrent update of h_state and of
+//                     the running chunk contribution, y_ssd = C h_state,
+//                     deterministic merge of the split partials, the gate, and
+//                     the append of the running contribution when the token
+//                     closes its chunk (slot m, never read by this step).
+#include "dart_common.hpp"
+#include "dart_internal.hpp"
+
+namespace dart {
+namespace {
+
+constexpr int kP = 64;
+constexpr int kThreads = 256;
+constexpr int kMPS = kDecodeMemPerSplit;
+
+template <typename T, int N>
+__global__ __launch_bounds__(kThreads) void k_decode_partial(
+    const T* __restrict__ mem, const T* __restrict__ q, const T* __restrict__ e,
+    const T* __restrict__ Cm, const float* __restrict__ qw, const float* __restrict__ ew,
+    float* __restrict__ part, float eps, int normalize, int H, int G, int64_t Mcap, int64_t m,
+    int nsplit) {
+    constexpr int R = N / 8;  // rows per lane
+    const int s = blockIdx.x, h = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int g = (int)((int64_t)h * G / H);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int po = lane & 7, rg = lane >> 3;
+
+    __shared__ float s_q[N];
+    __shared__ float s_e[kP];
+    __shared__ float s_part[4][kP + 2];
+
+    if (wave == 0) {
+        const float v0 = lane < N ? to_f(q[(b * G + g) * N + lane]) : 0.f;
+        const float v1 = lane + 64 < N ? to_f(q[(b * G + g) * N + lane + 64]) : 0.f;
+        float ss = v0 * v0 + v1 * v1;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
+        const float inv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) *
+                          (kLog2e / sqrtf((float)N));
+        if (lane < N) s_q[lane] = v0 * inv * (qw ? qw[lane] : 1.0f);
+        if (lane + 64 < N) s_q[lane + 64] = v1 * inv * (qw ? qw[lane + 64] : 1.0f);
+    } else if (wave == 1) {
+        const float v = to_f(e[(b * G + g) * kP + lane]);
+        float ss = v * v;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
+        const float inv = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
+        s_e[lane] = v * inv * (ew ? ew[lane] : 1.0f);
+    }
+    __syncthreads();
+
+    float eb[8], qb[R], cb[R];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) eb[i] = s_e[po * 8 + i];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        qb[k] = s_q[rg + 8 * k];
+        cb[k] = to_f(Cm[(b * G + g) * N + rg + 8 * k]);
+    }
+
+    float mx = -INFINITY, den = 0.f, o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = 0.f;
+    const int64_t j0 = (int64_t)s * kMPS;
+    const int64_t j1 = (j0 + kMPS < m) ? j0 + kMPS : m;
+    for (int64_t j = j0 + wave; j < j1; j += 4) {
+        const T* src = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
+        float xv[R][8];
+#pragma unroll
+        for (int k = 0; k < R; ++k) load8(src + (rg + 8 * k) * kP + po * 8, xv[k]);
+        float lsum = 0.f, v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = 0.f;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            float ss = 0.f, kv = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                ss += xv[k][i] * xv[k][i];
+                kv += xv[k][i] * eb[i];
+                v[i] += cb[k] * xv[k][i];
+            }
+            ss += shfl_xor(ss, 1);
+            kv += shfl_xor(kv, 1);
+            ss += shfl_xor(ss, 2);
+            kv += shfl_xor(kv, 2);
+            ss += shfl_xor(ss, 4);
+            kv += shfl_xor(kv, 4);
+            const float r = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
+            lsum += qb[k] * r * kv;
+        }
+        lsum += shfl_xor(lsum, 8);
+        lsum += shfl_xor(lsum, 16);
+        lsum += shfl_xor(lsum, 32);
+        const float mn = fmaxf(mx, lsum);
+        const float al = fast_exp2(mx - mn), pw = fast_exp2(lsum - mn);
+        den = den * al + pw;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = o[i] * al + pw * v[i];
+        mx = mn;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        o[i] += shfl_xor(o[i], 8);
+        o[i] += shfl_xor(o[i], 16);
+        o[i] += shfl_xor(o[i], 32);
+    }
+    if (rg == 0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s_part[wave][po * 8 + i] = o[i];
+    }
+    if (lane == 0) {
+        s_part[wave][kP] = mx;
+        s_part[wave][kP + 1] = den;
+    }
+    __syncthreads();
+    if (tid < kP) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, s_part[w][kP]);
+        float D = 0.f, O = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float mw = s_part[w][kP];
+            if (mw == -INFINITY) continue;
+            const float sc = fast_exp2(mw - M);
+            D += s_part[w][kP + 1] * sc;
+            O += s_part[w][tid] * sc;
+        }
+        float* out = part + (((b * H + h) * nsplit) + s) * (kP + 2);
+        out[tid] = O;
+        if (tid == 0) {
+            out[kP] = M;
+            out[kP + 1] = D;
+        }
+    }
+}
+
+template <typename T, int N>
+__global__ __launch_bounds__(kThreads) void k_decode_finish(
+    const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
+    const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ z,
+    float* __restrict__ h_state, float* __restrict__ chunk_acc, T* __restrict__ mem,
+    T* __restrict__ y, const float* __restrict__ part, int H, int G, int S, int64_t Mcap,
+    int64_t pos, int64_t m, int nsplit, int z_per_head) {
+    const int h = blockIdx.x;
+    const int64_t b = blockIdx.y;
+    const int g = (int)((int64_t)h * G / H);
+    const int tid = threadIdx.x;
+    const int pq = tid & 15, rg = tid >> 4;  // p quad, row group
+    const bool reset = (pos % S) == 0;
+    const bool append = (pos % S) == S - 1;
+
+    __shared__ float s_x[kP], s_B[N], s_C[N];
+    __shared__ float s_y[16][kP];
+    if (tid < kP) s_x[tid] = to_f(x[(b * H + h) * kP + tid]);
+    if (tid < N) {
+        s_B[tid] = to_f(Bm[(b * G + g) * N + tid]);
+        s_C[tid] = to_f(Cm[(b * G + g) * N + tid]);
+    }
+    __syncthreads();
+    const float dtv = dt[b * H + h];
+    const float a = __expf(dtv * A[h]);
+    float yp[4] = {0.f, 0.f, 0.f, 0.f};
+    const int64_t sbase = (b * H + h) * (int64_t)N * kP;
+    T* mdst = mem + ((b * Mcap + m) * H + h) * (int64_t)N * kP;
+#pragma unroll 4
+    for (int k = 0; k < N / 16; ++k) {
+        const int n = rg + 16 * k;
+        const int64_t off = sbase + n * kP + 4 * pq;
+        float hs[4], ca[4];
+        load4(h_state + off, hs);
+        if (reset) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ca[i] = 0.f;
+        } else {
+            load4(chunk_acc + off, ca);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float u = dtv * s_B[n] * s_x[4 * pq + i];
+            hs[i] = a * hs[i] + u;
+            ca[i] = a * ca[i] + u;
+            yp[i] += s_C[n] * hs[i];
+        }
+        store4(h_state + off, hs);
+        store4(chunk_acc + off, ca);
+        if (append) store4(mdst + n * kP + 4 * pq, ca);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s_y[rg][4 * pq + i] = yp[i];
+    __syncthreads();
+    if (tid < kP) {
+        float ys = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ys += s_y[r][tid];
+        float R = 0.f;
+        if (m > 0) {
+            const int ns = (int)((m + kMPS - 1) / kMPS);
+            const float* pb = part + (b * H + h) * nsplit * (int64_t)(kP + 2);
+            float M = -INFINITY;
+            for (int s = 0; s < ns; ++s) M = fmaxf(M, pb[s * (kP + 2) + kP]);
+            float D = 0.f, O = 0.f;
+            for (int s = 0; s < ns; ++s) {
+                const float sc = fast_exp2(pb[s * (kP + 2) + kP] - M);
+                D += pb[s * (kP + 2) + kP + 1] * sc;
+                O += pb[s * (kP + 2) + tid] * sc;
+            }
+            R = O / D;
+        }
+        const float zz = to_f(z_per_head ? z[b * H + h] : z[b]);
+        y[(b * H + h) * kP + tid] = from_f<T>(ys + silu(zz) * R);
+    }
+}
+
+template <typename T, int N>
+hipError_t run_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
+                      const float* dt, const float* A, const void* Bm, const void* Cm,
+                      const void* q, const void* e, const void* z, float* h_state,
+                      float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st) {
+    const int64_t m = pos / s.S;
+    const int nsplit_cap = (int)((s.Mcap + kMPS - 1) / kMPS);
+    float* part = reinterpret_cast<float*>(ws);
+    if (m > 0) {
+        const int ns = (int)((m + kMPS - 1) / kMPS);
+        prof_begin("k_decode_partial", st);
+        k_decode_partial<T, N><<<dim3((unsigned)ns, (unsigned)s.H, (unsigned)s.B), kThreads, 0,
+                                 st>>>((const T*)mem, (const T*)q, (const T*)e, (const T*)Cm,
+                                       a.qw, a.ew, part, a.eps, a.normalize, s.H, s.G, s.Mcap, m,
+                                       nsplit_cap);
+        prof_end(st);
+    }
+    prof_begin("k_decode_finish", st);
+    k_decode_finish<T, N><<<dim3((unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
+        (const T*)x, dt, A, (const T*)Bm, (const T*)Cm, (const T*)z, h_state, chunk_acc, (T*)mem,
+        (T*)y, part, s.H, s.G, s.S, s.Mcap, pos, m, nsplit_cap, a.z_per_head);
+    prof_end(st);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t run_decode_n(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
+                        const float* dt, const float* A, const void* Bm, const void* Cm,
+                        const void* q, const void* e, const void* z, float* hs, float* ca,
+                        void* mem, void* y, void* ws, hipStream_t st) {
+    switch (s.N) {
+        case 32: return run_decode<T, 32>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+        case 64: return run_decode<T, 64>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+        case 128: return run_decode<T, 128>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+size_t decode_workspace_bytes(const Shape& s) {
+    const int64_t nsplit = (s.Mcap + kMPS - 1) / kMPS;
+    return align256(sizeof(float) * s.B * s.H * (size_t)(nsplit > 0 ? nsplit : 1) * (s.P + 2));
+}
+
+hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
+                         const float* dt, const float* A, const void* Bm, const void* Cm,
+                         const void* q, const void* e, const void* z, float* h_state,
+                         float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st) {
+    if (s.dtype == 1)
+        return run_decode_n<bf16>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem, y, ws, st);
+    return run_decode_n<float>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem, y, ws, st);
+}
+
+}  // namespace dart

@@ -1,0 +1,287 @@
+"""ctypes binding of libdart.so (C ABI in include/dart.h).
+
+Argument marshalling only: every step of the hot path runs in the library's
+HIP kernels.  PyTorch supplies device memory (tensors) and the stream.  If the
+library has not been built, every call raises -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdart.so")
+
+DART_OK, DART_ERR_INVALID_ARG, DART_ERR_UNSUPPORTED, DART_ERR_HIP = 0, 1, 2, 3
+DART_FP32, DART_BF16 = 0, 1
+DEFAULT_EPS = 1e-6
+
+
+class DartError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("%s: %s" % (_STATUS.get(status, "DART_ERR_%d" % status), msg))
+        self.status = status
+
+
+_STATUS = {0: "DART_OK", 1: "DART_ERR_INVALID_ARG", 2: "DART_ERR_UNSUPPORTED", 3: "DART_ERR_HIP"}
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64),
+                ("nheads", ctypes.c_int32), ("ngroups", ctypes.c_int32),
+                ("headdim", ctypes.c_int32), ("dstate", ctypes.c_int32),
+                ("chunk", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("mem_capacity", ctypes.c_int64)]
+
+
+class SmaOpts(ctypes.Structure):
+    _fields_ = [("eps", ctypes.c_float), ("q_norm_w", ctypes.c_void_p),
+                ("e_norm_w", ctypes.c_void_p), ("normalize", ctypes.c_int32),
+                ("z_per_head", ctypes.c_int32)]
+
+
+EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspace_bytes",
+           "dart_sma_fwd", "dart_decode_workspace_bytes", "dart_decode_step",
+           "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
+           "dart_profile_enable", "dart_profile_flush", "dart_profile_count",
+           "dart_profile_name", "dart_profile_total_ms", "dart_profile_launches",
+           "dart_profile_reset")
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libdart.so and declare its signatures.  Raises if it is missing."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(path):
+            raise RuntimeError("libdart.so not found at %s: build it with "
+                               "`python -m paper_2608_02032_amd.build` (no fallback path exists)"
+                               % path)
+        lib = ctypes.CDLL(path)
+        P, D, O = ctypes.c_void_p, ctypes.POINTER(Dims), ctypes.POINTER(SmaOpts)
+        sz, st, i64 = ctypes.c_size_t, ctypes.c_int, ctypes.c_int64
+        lib.dart_scan_workspace_bytes.argtypes = [D]
+        lib.dart_scan_workspace_bytes.restype = sz
+        lib.dart_ssd_chunk_scan.argtypes = [D, P, P, P, P, P, P, P, P, P, P, sz, P]
+        lib.dart_ssd_chunk_scan.restype = st
+        lib.dart_sma_workspace_bytes.argtypes = [D]
+        lib.dart_sma_workspace_bytes.restype = sz
+        lib.dart_sma_fwd.argtypes = [D, O, P, P, P, P, P, P, P, P, P, sz, P]
+        lib.dart_sma_fwd.restype = st
+        lib.dart_decode_workspace_bytes.argtypes = [D]
+        lib.dart_decode_workspace_bytes.restype = sz
+        lib.dart_decode_step.argtypes = [D, O, i64, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
+        lib.dart_decode_step.restype = st
+        lib.dart_decode_cache_elems.argtypes = [D, i64]
+        lib.dart_decode_cache_elems.restype = i64
+        lib.dart_status_string.argtypes = [st]
+        lib.dart_status_string.restype = ctypes.c_char_p
+        lib.dart_last_error.argtypes = []
+        lib.dart_last_error.restype = ctypes.c_char_p
+        lib.dart_profile_enable.argtypes = [ctypes.c_int]
+        lib.dart_profile_enable.restype = st
+        lib.dart_profile_flush.argtypes = []
+        lib.dart_profile_flush.restype = st
+        lib.dart_profile_count.argtypes = []
+        lib.dart_profile_count.restype = ctypes.c_int
+        lib.dart_profile_name.argtypes = [ctypes.c_int]
+        lib.dart_profile_name.restype = ctypes.c_char_p
+        lib.dart_profile_total_ms.argtypes = [ctypes.c_int]
+        lib.dart_profile_total_ms.restype = ctypes.c_double
+        lib.dart_profile_launches.argtypes = [ctypes.c_int]
+        lib.dart_profile_launches.restype = i64
+        lib.dart_profile_reset.argtypes = []
+        lib.dart_profile_reset.restype = None
+        _lib = lib
+        return lib
+
+
+def check(status: int):
+    if status != DART_OK:
+        raise DartError(status, load_library().dart_last_error().decode())
+
+
+def make_dims(batch, seqlen, nheads, headdim, dstate, chunk, dtype, ngroups=1, mem_capacity=0):
+    dt_code = {"fp32": DART_FP32, "bf16": DART_BF16}.get(dtype, dtype)
+    return Dims(int(batch), int(seqlen), int(nheads), int(ngroups), int(headdim), int(dstate),
+                int(chunk), int(dt_code), int(mem_capacity))
+
+
+# --------------------------------------------------------------------------- #
+# torch-facing helpers (device memory and streams only)
+# --------------------------------------------------------------------------- #
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return "bf16"
+    if t.dtype == torch.float32:
+        return "fp32"
+    raise TypeError("storage tensors must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _workspace(nbytes, device):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def _check_f32(t, name):
+    torch = _torch()
+    if t is not None and t.dtype != torch.float32:
+        raise TypeError("%s must be float32" % name)
+
+
+def ssd_chunk_scan(x, dt, A, Bm, Cm, chunk, h0=None, mem=None, mem_capacity=0, y_ssd=None,
+                   h_last=True, workspace=None, stream=None):
+    """Chunked SSD scan retaining the chunk state memories (dart_ssd_chunk_scan).
+
+    x [B][L][H][P], dt [B][L][H] f32, A [H] f32, Bm/Cm [B][L][G][N].
+    Returns (y_ssd [B][L][H][P], mem [B][Mcap][H][N][P], h_last [B][H][N][P] f32 or None).
+    """
+    torch = _torch()
+    lib = load_library()
+    B_, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    dtype = _dtype_code(x)
+    for t, nm in ((dt, "dt"), (A, "A"), (h0, "h0")):
+        _check_f32(t, nm)
+    M = -(-L // chunk)
+    if mem is not None:
+        mem_capacity = mem.shape[1]
+    Mcap = mem_capacity or M
+    dims = make_dims(B_, L, H, P, N, chunk, dtype, G, Mcap)
+    if y_ssd is None:
+        y_ssd = torch.empty_like(x)
+    if mem is None:
+        mem = torch.empty((B_, Mcap, H, N, P), dtype=x.dtype, device=x.device)
+    hl = torch.empty((B_, H, N, P), dtype=torch.float32, device=x.device) if h_last is True else (
+        h_last if h_last is not None and h_last is not False else None)
+    need = lib.dart_scan_workspace_bytes(ctypes.byref(dims))
+    if workspace is None:
+        workspace = _workspace(need, x.device)
+    check(lib.dart_ssd_chunk_scan(ctypes.byref(dims), _ptr(x), _ptr(dt), _ptr(A), _ptr(Bm),
+                                  _ptr(Cm), _ptr(h0), _ptr(y_ssd), _ptr(mem), _ptr(hl),
+                                  _ptr(workspace), workspace.numel(), _stream(stream)))
+    return y_ssd, mem, hl
+
+
+def sma_fwd(q, e, Cm, mem, z, y_ssd, chunk, eps=DEFAULT_EPS, normalize=True, q_norm_w=None,
+            e_norm_w=None, y=None, lse=True, workspace=None, stream=None):
+    """State-memory attention + gated residual (dart_sma_fwd).
+
+    q [B][L][G][N], e [B][L][G][P], Cm [B][L][G][N], mem [B][Mcap][H][N][P],
+    z [B][L][H] (one gate per head) or [B][L] (one per token), y_ssd [B][L][H][P].
+    Returns (y, lse) with lse [B][L][H] f32 (or None).  y may be y_ssd (in place).
+    """
+    torch = _torch()
+    lib = load_library()
+    B_, L, H, P = y_ssd.shape
+    G, N = q.shape[2], q.shape[3]
+    dtype = _dtype_code(y_ssd)
+    _check_f32(q_norm_w, "q_norm_w")
+    _check_f32(e_norm_w, "e_norm_w")
+    z_per_head = 1 if z.dim() == 3 else 0
+    dims = make_dims(B_, L, H, P, N, chunk, dtype, G, mem.shape[1])
+    opts = SmaOpts(float(eps), _ptr(q_norm_w), _ptr(e_norm_w), int(bool(normalize)), z_per_head)
+    if y is None:
+        y = torch.empty_like(y_ssd)
+    lse_t = torch.empty((B_, L, H), dtype=torch.float32, device=y_ssd.device) if lse is True else (
+        lse if lse is not None and lse is not False else None)
+    need = lib.dart_sma_workspace_bytes(ctypes.byref(dims))
+    if workspace is None:
+        workspace = _workspace(need, y_ssd.device)
+    check(lib.dart_sma_fwd(ctypes.byref(dims), ctypes.byref(opts), _ptr(q), _ptr(e), _ptr(Cm),
+                           _ptr(mem), _ptr(z), _ptr(y_ssd), _ptr(y), _ptr(lse_t), _ptr(workspace),
+                           workspace.numel(), _stream(stream)))
+    return y, lse_t
+
+
+def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache, chunk,
+                eps=DEFAULT_EPS, normalize=True, q_norm_w=None, e_norm_w=None, y=None,
+                workspace=None, stream=None):
+    """One decode step at position `pos` (dart_decode_step).  Updates h_state,
+    chunk_acc and mem_cache in place; returns y [B][H][P]."""
+    torch = _torch()
+    lib = load_library()
+    B_, H, P = x.shape
+    G, N = Bm.shape[1], Bm.shape[2]
+    dtype = _dtype_code(x)
+    for t, nm in ((dt, "dt"), (A, "A"), (h_state, "h_state"), (chunk_acc, "chunk_acc")):
+        _check_f32(t, nm)
+    z_per_head = 1 if z.dim() == 2 else 0
+    dims = make_dims(B_, 0, H, P, N, chunk, dtype, G, mem_cache.shape[1])
+    opts = SmaOpts(float(eps), _ptr(q_norm_w), _ptr(e_norm_w), int(bool(normalize)), z_per_head)
+    if y is None:
+        y = torch.empty_like(x)
+    need = lib.dart_decode_workspace_bytes(ctypes.byref(dims))
+    if workspace is None:
+        workspace = _workspace(need, x.device)
+    check(lib.dart_decode_step(ctypes.byref(dims), ctypes.byref(opts), int(pos), _ptr(x), _ptr(dt),
+                               _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(q), _ptr(e), _ptr(z),
+                               _ptr(h_state), _ptr(chunk_acc), _ptr(mem_cache), _ptr(y),
+                               _ptr(workspace), workspace.numel(), _stream(stream)))
+    return y
+
+
+def workspace_bytes(kind: str, dims: Dims) -> int:
+    lib = load_library()
+    fn = {"scan": lib.dart_scan_workspace_bytes, "sma": lib.dart_sma_workspace_bytes,
+          "decode": lib.dart_decode_workspace_bytes}[kind]
+    return int(fn(ctypes.byref(dims)))
+
+
+def decode_cache_elems(dims: Dims, context: int) -> int:
+    return int(load_library().dart_decode_cache_elems(ctypes.byref(dims), int(context)))
+
+
+# --------------------------------------------------------------------------- #
+# optional kernel timing (dart_profile_* in dart.h)
+# --------------------------------------------------------------------------- #
+
+def profile_enable(on: bool = True):
+    check(load_library().dart_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    load_library().dart_profile_reset()
+
+
+def profile_read(reset: bool = False):
+    """Flush pending kernel events and return {kernel: (total_ms, launches)}."""
+    lib = load_library()
+    check(lib.dart_profile_flush())
+    out = {}
+    for i in range(lib.dart_profile_count()):
+        out[lib.dart_profile_name(i).decode()] = (float(lib.dart_profile_total_ms(i)),
+                                                  int(lib.dart_profile_launches(i)))
+    if reset:
+        lib.dart_profile_reset()
+    return out

@@ -1,0 +1,255 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 CPU oracle on
+the same seeded inputs.  Tolerance (per (b, h) slice, max|gpu - ref| / max|ref|):
+1e-4 for fp32 storage, 2e-2 for bf16 storage with fp32 accumulation; LSE as
+|d| <= tol (1 + |ref|) on finite entries and -inf exactly where it must be."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_02032_amd import dart, synth
+from tests.helpers import (TOL, assert_close_slices, assert_lse_close, f32_dev, to_dev, to_np)
+
+pytestmark = pytest.mark.gpu
+
+
+def announce(msg):
+    print("\n[gpu-case] " + msg, flush=True)
+
+
+def run_scan(w, d, h0=None, mem_capacity=0):
+    import torch
+    x, Bm, Cm = (to_dev(d[k], w.dtype) for k in ("x", "Bm", "Cm"))
+    dt, A = f32_dev(d["dt"]), f32_dev(d["A"])
+    h0_t = None if h0 is None else f32_dev(h0)
+    y, mem, hl = dart.ssd_chunk_scan(x, dt, A, Bm, Cm, w.chunk, h0=h0_t, mem_capacity=mem_capacity)
+    torch.cuda.synchronize()
+    return y, mem, hl
+
+
+SCAN_CASES = [
+    synth.WORKLOADS["tiny_fp32_L512"],
+    synth.Workload("ragged_fp32_L200_N64", 2, 200, 3, 64, 64, 64, "fp32"),
+    synth.Workload("groups_fp32_L384_N128_S128", 1, 384, 4, 64, 128, 128, "fp32", ngroups=2),
+    synth.Workload("bf16_L1024_N128_S256", 2, 1024, 4, 64, 128, 256, "bf16"),
+    synth.Workload("bf16_L600_N64_S128", 1, 600, 3, 64, 64, 128, "bf16"),
+    synth.Workload("bf16_L320_N32_S64", 2, 320, 2, 64, 32, 64, "bf16"),
+]
+
+
+@pytest.mark.parametrize("w", SCAN_CASES, ids=lambda w: w.name)
+def test_scan_matches_recurrence_and_memories(w):
+    announce("scan %s" % (w,))
+    d = synth.forward_inputs(w, seed=1)
+    y, mem, hl = run_scan(w, d)
+    y_ref, hl_ref = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"])
+    mem_ref = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], w.chunk)
+    tol = TOL[w.dtype]
+    assert_close_slices(to_np(y), y_ref, tol, what="y_ssd")
+    assert_close_slices(to_np(mem), mem_ref, tol, axes_keep=(0, 1, 2), what="mem")
+    assert_close_slices(to_np(hl), hl_ref, tol, axes_keep=(0, 1), what="h_last")
+
+
+def test_scan_initial_state_and_capacity():
+    w = synth.Workload("h0_fp32_L300_N64", 1, 300, 2, 64, 64, 128, "fp32")
+    announce("scan with h0 %s" % (w,))
+    d = synth.forward_inputs(w, seed=2)
+    h0 = np.random.default_rng(5).standard_normal((1, 2, 64, 64)).astype(np.float32) * 0.1
+    y, mem, hl = run_scan(w, d, h0=h0, mem_capacity=7)
+    assert mem.shape[1] == 7
+    y_ref, hl_ref = oracle.ssd_recurrence(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], h0=h0)
+    assert_close_slices(to_np(y), y_ref, 1e-4, what="y_ssd")
+    assert_close_slices(to_np(hl), hl_ref, 1e-4, axes_keep=(0, 1), what="h_last")
+    mem_ref = oracle.chunk_memories(d["x"], d["dt"], d["A"], d["Bm"], 128)
+    assert_close_slices(to_np(mem)[:, :3], mem_ref, 1e-4, axes_keep=(0, 1, 2), what="mem")
+
+
+def test_scan_single_chunk_memory_is_final_state():
+    # S = L: the only memory equals the final state (h0 = 0)
+    w = synth.Workload("one_chunk_bf16", 2, 256, 2, 64, 128, 256, "bf16")
+    announce("scan one chunk %s" % (w,))
+    d = synth.forward_inputs(w, seed=3)
+    y, mem, hl = run_scan(w, d)
+    assert_close_slices(to_np(mem)[:, 0], to_np(hl), 2e-2, axes_keep=(0, 1), what="mem vs h_last")
+
+
+def sma_case(w, seed, nmem_extra=0):
+    d = synth.forward_inputs(w, seed=seed)
+    rng = np.random.default_rng(seed + 100)
+    mem = synth.synthetic_memories(rng, w.batch, w.nchunks + nmem_extra, w.nheads, w.dstate,
+                                   w.headdim, w.dtype)
+    y_ssd = synth.to_storage(rng.standard_normal((w.batch, w.seqlen, w.nheads, w.headdim))
+                             .astype(np.float32) * 0.05, w.dtype)
+    return d, mem, y_ssd
+
+
+def run_sma(w, d, mem, y_ssd, z=None, inplace=False, **kw):
+    import torch
+    q, e, Cm = (to_dev(d[k], w.dtype) for k in ("q", "e", "Cm"))
+    zz = to_dev(d["z"] if z is None else z, w.dtype)
+    mem_t = to_dev(mem, w.dtype)
+    ys = to_dev(y_ssd, w.dtype)
+    out = ys if inplace else None
+    y, lse = dart.sma_fwd(q, e, Cm, mem_t, zz, ys, w.chunk, y=out, **kw)
+    torch.cuda.synchronize()
+    return y, lse
+
+
+SMA_CASES = [
+    synth.WORKLOADS["tiny_fp32_L512"],
+    synth.Workload("fp32_L700_N64_S128", 1, 700, 2, 64, 64, 128, "fp32"),
+    synth.Workload("fp32_L512_N128_S256", 1, 768, 2, 64, 128, 256, "fp32"),
+    synth.Workload("bf16_L1280_N128_S256", 2, 1280, 3, 64, 128, 256, "bf16"),
+    synth.Workload("bf16_L700_N64_S64", 1, 700, 2, 64, 64, 64, "bf16"),
+    synth.Workload("bf16_L1024_N128_S128", 1, 1024, 2, 64, 128, 128, "bf16"),
+    synth.Workload("bf16_L1100_N32_S64_G2", 1, 1100, 4, 64, 32, 64, "bf16", ngroups=2),
+]
+
+
+@pytest.mark.parametrize("w", SMA_CASES, ids=lambda w: w.name)
+def test_sma_matches_explicit_softmax(w):
+    announce("sma %s" % (w,))
+    d, mem, y_ssd = sma_case(w, seed=7)
+    y, lse = run_sma(w, d, mem, y_ssd)
+    y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, w.chunk)
+    tol = TOL[w.dtype]
+    assert_close_slices(to_np(y), y_ref, tol, what="y")
+    assert_lse_close(to_np(lse), lse_ref, tol)
+    # first chunk: y == y_ssd bitwise, LSE = -inf
+    S = w.chunk
+    np.testing.assert_array_equal(to_np(y)[:, :S], y_ssd[:, :S].astype(np.float64))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_sma_options(dtype):
+    """Alg. 1 literal (normalize = 0), one gate per token, RMSNorm weights, in place."""
+    import torch
+    w = synth.Workload("opts_%s" % dtype, 1, 640, 2, 64, 64, 64, dtype, z_per_head=False)
+    announce("sma options %s" % (w,))
+    d, mem, y_ssd = sma_case(w, seed=11)
+    tol = TOL[dtype]
+    # unnormalised
+    y, lse = run_sma(w, d, mem, y_ssd, normalize=False)
+    y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, 64, normalize=False)
+    assert_close_slices(to_np(y), y_ref, tol, what="y (normalize=0)")
+    assert_lse_close(to_np(lse), lse_ref, tol)
+    # norm weights + in place
+    rng = np.random.default_rng(3)
+    qw = rng.uniform(0.5, 1.5, 64).astype(np.float32)
+    ew = rng.uniform(0.5, 1.5, 64).astype(np.float32)
+    y, lse = run_sma(w, d, mem, y_ssd, inplace=True, q_norm_w=f32_dev(qw), e_norm_w=f32_dev(ew))
+    y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, 64, q_norm_w=qw,
+                                e_norm_w=ew)
+    assert_close_slices(to_np(y), y_ref, tol, what="y (weights, in place)")
+    assert_lse_close(to_np(lse), lse_ref, tol)
+
+
+def test_sma_gate_zero_returns_ssm_output():
+    w = synth.Workload("gate0_bf16", 1, 768, 2, 64, 128, 256, "bf16")
+    announce("sma gate zero %s" % (w,))
+    d, mem, y_ssd = sma_case(w, seed=12)
+    y, _ = run_sma(w, d, mem, y_ssd, z=np.zeros_like(d["z"]))
+    np.testing.assert_array_equal(to_np(y), y_ssd.astype(np.float64))
+
+
+@pytest.mark.parametrize("w", [synth.WORKLOADS["tiny_fp32_L512"],
+                               synth.Workload("e2e_bf16", 2, 1024, 4, 64, 128, 256, "bf16")],
+                         ids=lambda w: w.name)
+def test_forward_end_to_end(w):
+    """GPU scan -> GPU SMA + gate, against the oracle run from scratch."""
+    import torch
+    announce("forward %s" % (w,))
+    d = synth.forward_inputs(w, seed=0)
+    y_ssd, mem, _ = run_scan(w, d)
+    q, e, Cm, z = (to_dev(d[k], w.dtype) for k in ("q", "e", "Cm", "z"))
+    y, lse = dart.sma_fwd(q, e, Cm, mem, z, y_ssd, w.chunk)
+    torch.cuda.synchronize()
+    ref = oracle.forward(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], d["q"], d["e"], d["z"],
+                         w.chunk)
+    tol = TOL[w.dtype]
+    assert_close_slices(to_np(y), ref["y"], tol, what="y")
+    assert_lse_close(to_np(lse), ref["lse"], tol)
+
+
+def test_scan_and_sma_are_deterministic():
+    import torch
+    w = synth.Workload("det_bf16", 2, 1024, 4, 64, 128, 256, "bf16")
+    announce("determinism %s" % (w,))
+    d = synth.forward_inputs(w, seed=4)
+    outs = []
+    for _ in range(2):
+        y_ssd, mem, hl = run_scan(w, d)
+        q, e, Cm, z = (to_dev(d[k], w.dtype) for k in ("q", "e", "Cm", "z"))
+        y, lse = dart.sma_fwd(q, e, Cm, mem, z, y_ssd, w.chunk)
+        torch.cuda.synchronize()
+        outs.append([t.cpu() for t in (y_ssd, mem, hl, y, lse)])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+# --------------------------------------------------------------------------- #
+# decode
+# --------------------------------------------------------------------------- #
+
+@pytest.mark.parametrize("dtype,S,N,L,z_per_head", [("fp32", 64, 32, 200, True),
+                                                    ("bf16", 64, 64, 160, False)])
+def test_decode_token_by_token_reproduces_forward(dtype, S, N, L, z_per_head):
+    import torch
+    w = synth.Workload("dec_%s" % dtype, 2, L, 2, 64, N, S, dtype, z_per_head=z_per_head)
+    announce("decode token-by-token %s" % (w,))
+    d = synth.forward_inputs(w, seed=21)
+    ref = oracle.forward(d["x"], d["dt"], d["A"], d["Bm"], d["Cm"], d["q"], d["e"], d["z"], S)
+    B_, H, P = w.batch, w.nheads, w.headdim
+    Mcap = -(-L // S)
+    dev = {k: to_dev(d[k], dtype) for k in ("x", "Bm", "Cm", "q", "e", "z")}
+    dt, A = f32_dev(d["dt"]), f32_dev(d["A"])
+    h_state = torch.zeros((B_, H, N, P), dtype=torch.float32, device="cuda")
+    chunk_acc = torch.zeros_like(h_state)
+    cache = torch.zeros((B_, Mcap, H, N, P), dtype=dev["x"].dtype, device="cuda")
+    ys = []
+    for t in range(L):
+        zt = dev["z"][:, t].contiguous()
+        y = dart.decode_step(t, dev["x"][:, t].contiguous(), dt[:, t].contiguous(), A,
+                             dev["Bm"][:, t].contiguous(), dev["Cm"][:, t].contiguous(),
+                             dev["q"][:, t].contiguous(), dev["e"][:, t].contiguous(), zt,
+                             h_state, chunk_acc, cache, S)
+        ys.append(y)
+    torch.cuda.synchronize()
+    y_all = np.stack([to_np(y) for y in ys], axis=1)
+    tol = TOL[dtype]
+    assert_close_slices(y_all, ref["y"], tol, what="decode y")
+    full = L // S
+    assert_close_slices(to_np(cache)[:, :full], ref["mem"][:, :full], tol, axes_keep=(0, 1, 2),
+                        what="cache")
+    assert_close_slices(to_np(h_state), ref["h_last"], tol, axes_keep=(0, 1), what="h_state")
+
+
+@pytest.mark.parametrize("dtype,N,S,m,offset", [("bf16", 128, 256, 40, 17), ("bf16", 128, 256, 19, 255),
+                                                ("fp32", 64, 64, 33, 0), ("bf16", 32, 128, 1, 5)])
+def test_decode_single_step_on_synthetic_cache(dtype, N, S, m, offset):
+    import torch
+    B_, H, P = 3, 4, 64
+    pos = m * S + offset
+    Mcap = m + 2
+    announce("decode step dtype=%s N=%d S=%d pos=%d" % (dtype, N, S, pos))
+    rng = np.random.default_rng(m)
+    mem = np.zeros((B_, Mcap, H, N, P), dtype=np.float32)
+    mem[:, :m] = synth.synthetic_memories(rng, B_, m, H, N, P, dtype)
+    h_state = (rng.standard_normal((B_, H, N, P)) * 0.01).astype(np.float32)
+    chunk_acc = (rng.standard_normal((B_, H, N, P)) * 0.01).astype(np.float32)
+    inp = synth.decode_inputs(B_, H, P, N, dtype, seed=m + 1)
+    hs_ref, ca_ref, mem_ref = (np.array(a, dtype=np.float64) for a in (h_state, chunk_acc, mem))
+    y_ref = oracle.decode_step(pos, inp["x"], inp["dt"], inp["A"], inp["Bm"], inp["Cm"], inp["q"],
+                               inp["e"], inp["z"], hs_ref, ca_ref, mem_ref, S)
+    hs, ca = f32_dev(h_state), f32_dev(chunk_acc)
+    cache = to_dev(mem, dtype)
+    dev = {k: to_dev(inp[k], dtype) for k in ("x", "Bm", "Cm", "q", "e", "z")}
+    y = dart.decode_step(pos, dev["x"], f32_dev(inp["dt"]), f32_dev(inp["A"]), dev["Bm"], dev["Cm"],
+                         dev["q"], dev["e"], dev["z"], hs, ca, cache, S)
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    assert_close_slices(to_np(y), y_ref, tol, axes_keep=(0, 1), what="y")
+    assert_close_slices(to_np(hs), hs_ref, 1e-5, axes_keep=(0, 1), what="h_state")
+    assert_close_slices(to_np(ca), ca_ref, 1e-5, axes_keep=(0, 1), what="chunk_acc")
+    assert_close_slices(to_np(cache), mem_ref, tol, axes_keep=(0, 1, 2), what="cache")
