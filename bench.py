@@ -41,7 +41,7 @@ def parse():
     ap.add_argument("--decode-workload", default="decode_B64_ctx65536")
     ap.add_argument("--no-decode", action="store_true", help="time the forward only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-batches", type=int, default=1,
+    ap.add_argument("--cpu-batches", type=int, default=4,
                     help="batches of the workload the CPU oracle is timed on")
     ap.add_argument("--extra-out", default=None,
                     help="also write per-kernel detail as JSON to this file")
