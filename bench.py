@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=4,
                     help="batches of the workload the CPU oracle is timed on")
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="after the timed steps, run one plain device copy of this many MiB "
+                         "(reference kernel for scaling HBM byte counters)")
     ap.add_argument("--extra-out", default=None,
                     help="also write per-kernel detail as JSON to this file")
     return ap.parse_args()
@@ -262,6 +265,15 @@ def main():
         "roofline": roofline,
     }
     line.update(extra)
+    if args.copy_calib_mb:
+        n = args.copy_calib_mb << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        line["copy_calib_bytes"] = n
+        del src, dst
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_batches)
     line["wall_s_timed"] = round(wall, 3)

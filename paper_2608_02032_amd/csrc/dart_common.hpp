@@ -136,4 +136,105 @@ __device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
 
+// ---- LDS tiles staged by DMA ------------------------------------------------
+// 16-byte global -> LDS copy by DMA (global_load_lds_dwordx4).  `lds_wave_base`
+// must be the same for the whole wave; lane i's 16 bytes land at
+// lds_wave_base + 16 i.  Completion is tracked by the wave's vmcnt.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, void* lds_wave_base) {
+    __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_wave_base,
+                                     16, 0, 0);
+}
+__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0); }
+
+// A natural-layout tile of rows of RB bytes in LDS whose 16-byte chunks are
+// XOR-swizzled by row (chunk c of row r is stored at chunk c ^ (r & MASK)), so
+// that column reads across consecutive rows spread over the banks.
+template <int RB>
+struct SwzTile {
+    static constexpr int CPR = RB / 16;                  // chunks per row
+    static constexpr int MASK = (CPR < 8 ? CPR : 8) - 1;
+    __device__ static __forceinline__ int off(int r, int byte_in_row) {
+        return r * RB + ((((byte_in_row >> 4) ^ (r & MASK)) << 4) | (byte_in_row & 15));
+    }
+};
+
+// Copy `rows` rows of RB bytes (global row stride gstride bytes) into a
+// swizzled LDS tile.  Rows >= rows_valid read the last valid row instead
+// (never out of bounds); callers mask their contribution.  rows_valid >= 1.
+template <int RB>
+__device__ __forceinline__ void dma_tile(char* lds, const char* g, int64_t gstride, int rows,
+                                         int rows_valid, int wave, int nwaves, int lane) {
+    using Tl = SwzTile<RB>;
+    const int total = rows * Tl::CPR;
+    for (int q0 = wave * 64; q0 < total; q0 += nwaves * 64) {
+        const int q = q0 + lane;
+        if (q < total) {
+            const int r = q / Tl::CPR, cs = q % Tl::CPR;
+            const int c = cs ^ (r & Tl::MASK);
+            const int rr = r < rows_valid ? r : rows_valid - 1;
+            lds_dma16(g + rr * gstride + c * 16, lds + q0 * 16);
+        }
+    }
+}
+
+// MFMA operand fragment from a k-major swizzled tile (rows = k, columns = the
+// operand's m or n index): lane l = 16 g + j receives, for its column
+// cbase + j, the 8 values of rows krow0(g) + 0..3 and krow1(g) + 0..3.
+// bf16 uses two ds_read_b64_tr_b16 (within each 16-lane group, lane j points at
+// row r0 + j/4, columns c0 + 4 (j%4); lane i then holds column c0 + i of rows
+// r0..r0+3); fp32 falls back to eight scalar reads.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+template <int RB>
+__device__ __forceinline__ bf16x8 frag_kmajor_bf16(const char* tile, int krow0, int krow1,
+                                                   int cbase, int lane) {
+    using Tl = SwzTile<RB>;
+    const int j = lane & 15;
+    const int col_b = (cbase + 4 * (j & 3)) * 2;
+    const char* a0 = tile + Tl::off(krow0 + (j >> 2), col_b);
+    const char* a1 = tile + Tl::off(krow1 + (j >> 2), col_b);
+    const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(a0));
+    const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(a1));
+    const bf16x4 b0 = __builtin_bit_cast(bf16x4, v0);
+    const bf16x4 b1 = __builtin_bit_cast(bf16x4, v1);
+    return bf16x8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+}
+template <int RB>
+__device__ __forceinline__ f32x8 frag_kmajor_f32(const char* tile, int krow0, int krow1,
+                                                 int cbase, int lane) {
+    using Tl = SwzTile<RB>;
+    const int col_b = (cbase + (lane & 15)) * 4;
+    f32x8 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        r[i] = *reinterpret_cast<const float*>(tile + Tl::off(krow0 + i, col_b));
+        r[4 + i] = *reinterpret_cast<const float*>(tile + Tl::off(krow1 + i, col_b));
+    }
+    return r;
+}
+template <typename T, int RB>
+__device__ __forceinline__ Frag<T> frag_km(const char* tile, int krow0, int krow1, int cbase,
+                                           int lane) {
+    if constexpr (sizeof(T) == 2) {
+        return frag_kmajor_bf16<RB>(tile, krow0, krow1, cbase, lane);
+    } else {
+        return frag_kmajor_f32<RB>(tile, krow0, krow1, cbase, lane);
+    }
+}
+
+// Fragment from a row-major swizzled tile (rows = the operand's m or n index,
+// 8 consecutive k per lane): one 16-byte read (two for fp32).
+template <typename T, int RB>
+__device__ __forceinline__ Frag<T> frag_rowmajor(const char* tile, int row, int kcol) {
+    using Tl = SwzTile<RB>;
+    if constexpr (sizeof(T) == 2) {
+        return *reinterpret_cast<const bf16x8*>(tile + Tl::off(row, kcol * 2));
+    } else {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(tile + Tl::off(row, kcol * 4));
+        const f32x4 b = *reinterpret_cast<const f32x4*>(tile + Tl::off(row, kcol * 4 + 16));
+        return f32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    }
+}
+
 }  // namespace dart

@@ -28,13 +28,37 @@ constexpr int kP = 64;
 constexpr int kThreads = 256;
 constexpr int kMPS = kDecodeMemPerSplit;
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ bf16x2 as_bf2(uint32_t u) { return __builtin_bit_cast(bf16x2, u); }
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(as_bf2(a), as_bf2(b), c, false);
+}
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
+    const bf16x2 v{(bf16)lo, (bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// One memory row chunk held by a lane: 8 consecutive p of one row n.
+template <typename T> struct RowChunk;
+template <> struct RowChunk<bf16> { uint4 v; };
+template <> struct RowChunk<float> { f32x4 a, b; };
+
+__device__ __forceinline__ void load_row(const bf16* p, RowChunk<bf16>& r) {
+    r.v = *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ void load_row(const float* p, RowChunk<float>& r) {
+    r.a = *reinterpret_cast<const f32x4*>(p);
+    r.b = *reinterpret_cast<const f32x4*>(p + 4);
+}
+
 template <typename T, int N>
 __global__ __launch_bounds__(kThreads) void k_decode_partial(
     const T* __restrict__ mem, const T* __restrict__ q, const T* __restrict__ e,
     const T* __restrict__ Cm, const float* __restrict__ qw, const float* __restrict__ ew,
     float* __restrict__ part, float eps, int normalize, int H, int G, int64_t Mcap, int64_t m,
     int nsplit) {
-    constexpr int R = N / 8;  // rows per lane
+    constexpr int R = N / 8;  // rows per lane (row n = rg + 8 k)
     const int s = blockIdx.x, h = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int g = (int)((int64_t)h * G / H);
@@ -73,6 +97,12 @@ __global__ __launch_bounds__(kThreads) void k_decode_partial(
         qb[k] = s_q[rg + 8 * k];
         cb[k] = to_f(Cm[(b * G + g) * N + rg + 8 * k]);
     }
+    // packed bf16 copies for the dot2 path
+    uint32_t ebp[4], cbp[R / 2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ebp[i] = pack_bf2(eb[2 * i], eb[2 * i + 1]);
+#pragma unroll
+    for (int k = 0; k < R / 2; ++k) cbp[k] = pack_bf2(cb[2 * k], cb[2 * k + 1]);
 
     float mx = -INFINITY, den = 0.f, o[8];
 #pragma unroll
@@ -81,20 +111,46 @@ __global__ __launch_bounds__(kThreads) void k_decode_partial(
     const int64_t j1 = (j0 + kMPS < m) ? j0 + kMPS : m;
     for (int64_t j = j0 + wave; j < j1; j += 4) {
         const T* src = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
-        float xv[R][8];
+        RowChunk<T> xr[R];
 #pragma unroll
-        for (int k = 0; k < R; ++k) load8(src + (rg + 8 * k) * kP + po * 8, xv[k]);
+        for (int k = 0; k < R; ++k) load_row(src + (rg + 8 * k) * kP + po * 8, xr[k]);
         float lsum = 0.f, v[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = 0.f;
 #pragma unroll
         for (int k = 0; k < R; ++k) {
-            float ss = 0.f, kv = 0.f;
+            float ss, kv;
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t w[4] = {xr[k].v.x, xr[k].v.y, xr[k].v.z, xr[k].v.w};
+                ss = dot2(w[0], w[0], 0.f);
+                kv = dot2(w[0], ebp[0], 0.f);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                ss += xv[k][i] * xv[k][i];
-                kv += xv[k][i] * eb[i];
-                v[i] += cb[k] * xv[k][i];
+                for (int i = 1; i < 4; ++i) {
+                    ss = dot2(w[i], w[i], ss);
+                    kv = dot2(w[i], ebp[i], kv);
+                }
+                if (k & 1) {
+                    // value side: pair rows k-1 and k so one dot2 covers both
+                    const uint32_t u[4] = {xr[k - 1].v.x, xr[k - 1].v.y, xr[k - 1].v.z, xr[k - 1].v.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t lo = (u[i] & 0xffffu) | (w[i] << 16);
+                        const uint32_t hi = (u[i] >> 16) | (w[i] & 0xffff0000u);
+                        v[2 * i] = dot2(lo, cbp[k >> 1], v[2 * i]);
+                        v[2 * i + 1] = dot2(hi, cbp[k >> 1], v[2 * i + 1]);
+                    }
+                }
+            } else {
+                const float xv[8] = {xr[k].a[0], xr[k].a[1], xr[k].a[2], xr[k].a[3],
+                                     xr[k].b[0], xr[k].b[1], xr[k].b[2], xr[k].b[3]};
+                ss = 0.f;
+                kv = 0.f;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    ss += xv[i] * xv[i];
+                    kv += xv[i] * eb[i];
+                    v[i] += cb[k] * xv[i];
+                }
             }
             ss += shfl_xor(ss, 1);
             kv += shfl_xor(kv, 1);

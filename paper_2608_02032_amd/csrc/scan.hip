@@ -48,82 +48,48 @@ __device__ float block_inclusive_scan(float v, float* sred) {
     return v + add;
 }
 
-// Load an 8x8 block (8 rows of 8 consecutive elements, row stride `ld`) and
-// write it transposed: dst[(k) * dld + r] = src[r * ld + k] * scale[r].
-template <typename T>
-__device__ __forceinline__ void transpose8x8(const T* src, int64_t ld, int nrows_valid, T* dst,
-                                             int dld, const float* scale) {
-    float v[8][8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-        if (r < nrows_valid) {
-            load8(src + r * ld, v[r]);
-            if (scale) {
-                const float sc = scale[r];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) v[r][k] *= sc;
-            }
-        } else {
-#pragma unroll
-            for (int k = 0; k < 8; ++k) v[r][k] = 0.f;
-        }
-    }
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        float col[8];
-#pragma unroll
-        for (int r = 0; r < 8; ++r) col[r] = v[r][k];
-        store8(dst + k * dld, col);
-    }
-}
-
-template <typename T>
-__device__ __forceinline__ Frag<T> load_frag_2x4(const T* p0, const T* p1);
-template <>
-__device__ __forceinline__ bf16x8 load_frag_2x4<bf16>(const bf16* p0, const bf16* p1) {
-    const bf16x4 a = *reinterpret_cast<const bf16x4*>(p0);
-    const bf16x4 b = *reinterpret_cast<const bf16x4*>(p1);
-    bf16x8 r;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        r[i] = a[i];
-        r[4 + i] = b[i];
-    }
-    return r;
-}
-template <>
-__device__ __forceinline__ f32x8 load_frag_2x4<float>(const float* p0, const float* p1) {
-    const f32x4 a = *reinterpret_cast<const f32x4*>(p0);
-    const f32x4 b = *reinterpret_cast<const f32x4*>(p1);
-    f32x8 r;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        r[i] = a[i];
-        r[4 + i] = b[i];
-    }
-    return r;
-}
-
 // ---------------------------------------------------------------------------
 // Chunk-state contraction: dH_[c] = sum_s exp(cs_e - cs_s) dt_s B_s^T x_s.
+// B_c and x_c stream through LDS in 64-token blocks (DMA, two stages held in
+// distinct LDS objects so the next block's copy overlaps this block's MFMAs);
+// both MFMA operands are read k-major with transpose loads.  Wave w owns
+// p-tile w and all n-tiles of the N x P result.
 // ---------------------------------------------------------------------------
 template <typename T, int N, int S>
 __global__ __launch_bounds__(kThreads) void k_chunk_state(
     const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const T* __restrict__ Bm, T* __restrict__ mem, float* __restrict__ chunk_lda, int64_t L, int H,
     int G, int64_t M, int64_t Mcap) {
+    constexpr int XRB = kP * (int)sizeof(T);   // bytes per x row
+    constexpr int BRB = N * (int)sizeof(T);    // bytes per B row
+    constexpr int XT = kSB * XRB, BT = kSB * BRB;
     const int c = blockIdx.x, h = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int g = (int)((int64_t)h * G / H);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = lane >> 4;
     const int64_t t0 = (int64_t)c * S;
     const int len = (int)(L - t0 < S ? L - t0 : S);
+    const int nsb = (len + kSB - 1) / kSB;
 
     __shared__ float s_w[S];
     __shared__ float s_red[4];
     __shared__ float s_cse;
-    __shared__ __attribute__((aligned(16))) T xT[kP][kSB + kPad];
-    __shared__ __attribute__((aligned(16))) T bT[N][kSB + kPad];
+    __shared__ __attribute__((aligned(16))) char xs0[XT];
+    __shared__ __attribute__((aligned(16))) char bs0[BT];
+    __shared__ __attribute__((aligned(16))) char xs1[XT];
+    __shared__ __attribute__((aligned(16))) char bs1[BT];
+    __shared__ __attribute__((aligned(16))) T so[4][N * 16];  // per-wave output strip
+
+    const char* xg = reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP);
+    const char* bg = reinterpret_cast<const char*>(Bm + ((b * L + t0) * G + g) * N);
+    const int64_t xstride = (int64_t)H * XRB, bstride = (int64_t)G * BRB;
+    auto stage = [&](int sb, char* xd, char* bd) {
+        const int rv = len - sb * kSB;
+        dma_tile<XRB>(xd, xg + sb * kSB * xstride, xstride, kSB, rv, wave, 4, lane);
+        dma_tile<BRB>(bd, bg + sb * kSB * bstride, bstride, kSB, rv, wave, 4, lane);
+    };
+    stage(0, xs0, bs0);
 
     // cumulative log decay within the chunk (tokens past L contribute 0)
     const float dts = (tid < len) ? dt[(b * L + t0 + tid) * H + h] : 0.f;
@@ -138,42 +104,50 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
 #pragma unroll
     for (int nt = 0; nt < N / 16; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int sb = 0; sb < S / kSB; ++sb) {
-        __syncthreads();
-        const int s0 = sb * kSB;
-        if (tid < 64) {
-            // x^T, scaled by the weights w_s: 8x8 sub-block (s8, p8)
-            const int s8 = tid >> 3, p8 = tid & 7;
-            const int srow = s0 + s8 * 8;
-            const int nv = len - srow;
-            transpose8x8<T>(x + ((b * L + t0 + srow) * H + h) * kP + p8 * 8, (int64_t)H * kP,
-                            nv, &xT[p8 * 8][s8 * 8], kSB + kPad, &s_w[srow]);
-        } else if (tid < 64 + N) {
-            const int u = tid - 64;
-            const int s8 = u & 7, n8 = u >> 3;
-            const int srow = s0 + s8 * 8;
-            const int nv = len - srow;
-            transpose8x8<T>(Bm + ((b * L + t0 + srow) * G + g) * N + n8 * 8, (int64_t)G * N, nv,
-                            &bT[n8 * 8][s8 * 8], kSB + kPad, nullptr);
-        }
-        __syncthreads();
+    auto consume = [&](int sb, const char* xt, const char* bt) {
 #pragma unroll
         for (int ks = 0; ks < kSB / 32; ++ks) {
-            const Frag<T> fx = load_frag(&xT[wave * 16 + (lane & 15)][ks * 32 + (lane >> 4) * 8]);
+            // x operand (k = s, column p), scaled by w_s
+            Frag<T> fx = frag_km<T, XRB>(xt, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, wave * 16, lane);
+            float xv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) xv[i] = to_f(fx[i]) * s_w[sb * kSB + ks * 32 + 8 * grp + i];
+            fx = make_frag<T>(xv);
 #pragma unroll
             for (int nt = 0; nt < N / 16; ++nt) {
-                const Frag<T> fb = load_frag(&bT[nt * 16 + (lane & 15)][ks * 32 + (lane >> 4) * 8]);
+                const Frag<T> fb = frag_km<T, BRB>(bt, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, nt * 16, lane);
                 acc[nt] = mma16(acc[nt], fb, fx);
             }
         }
+    };
+    wait_dma();
+    __syncthreads();
+    for (int sb = 0; sb < nsb; sb += 2) {
+        if (sb + 1 < nsb) stage(sb + 1, xs1, bs1);
+        consume(sb, xs0, bs0);
+        wait_dma();
+        __syncthreads();
+        if (sb + 1 >= nsb) break;
+        if (sb + 2 < nsb) stage(sb + 2, xs0, bs0);
+        consume(sb + 1, xs1, bs1);
+        wait_dma();
+        __syncthreads();
     }
-    // acc[nt][i] = dH[n = 16 nt + 4 (lane/16) + i][p = 16 wave + lane%16]
-    T* dst = mem + ((b * Mcap + c) * H + h) * (int64_t)N * kP;
+    // acc[nt][i] = dH[n = 16 nt + 4 (lane/16) + i][p = 16 wave + lane%16]:
+    // the wave's N x 16 strip goes through its own LDS scratch, then each row's
+    // 16 values leave as 16-byte stores
+    T* st = so[wave];
 #pragma unroll
     for (int nt = 0; nt < N / 16; ++nt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            dst[(nt * 16 + 4 * (lane >> 4) + i) * kP + wave * 16 + (lane & 15)] = from_f<T>(acc[nt][i]);
+        for (int i = 0; i < 4; ++i) st[(nt * 16 + 4 * grp + i) * 16 + (lane & 15)] = from_f<T>(acc[nt][i]);
+    T* dst = mem + ((b * Mcap + c) * H + h) * (int64_t)N * kP + wave * 16;
+    for (int e8 = lane; e8 < N * 2; e8 += 64) {
+        const int n = e8 >> 1, half = e8 & 1;
+        float v[8];
+        load8(st + n * 16 + half * 8, v);
+        store8(dst + n * kP + half * 8, v);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -207,14 +181,20 @@ __global__ __launch_bounds__(kThreads) void k_state_pass(
 // Chunk output: y_t = sum_{s<=t} (C_t.B_s) exp(cs_t - cs_s) dt_s x_s
 //                     + exp(cs_t) C_t H_[c-1].
 // Wave w owns the 16-row tiles rt = w, w+4, ... (interleaved for balance).
+// H_[c-1], B_c and x_c are DMA-staged in natural layout (B and x in two
+// 64-token stages held in distinct LDS objects); C rows stay in registers.
 // ---------------------------------------------------------------------------
 template <typename T, int N, int S>
-__global__ __launch_bounds__(kThreads) void k_chunk_out(
+__global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_chunk_out(
     const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ states,
     T* __restrict__ y, int64_t L, int H, int G, int64_t M) {
     constexpr int KS = N / 32;     // 32-deep k steps over the state dim
     constexpr int NQ = S / 64;     // row tiles per wave
+    constexpr int XRB = kP * (int)sizeof(T);
+    constexpr int BRB = N * (int)sizeof(T);
+    constexpr int XT = kSB * XRB, BT = kSB * BRB;
+    constexpr int HT = N * XRB;    // H_[c-1] tile, rows n of P values
     const int c = blockIdx.x, h = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int g = (int)((int64_t)h * G / H);
@@ -222,13 +202,29 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
     const int col = lane & 15, grp = lane >> 4;
     const int64_t t0 = (int64_t)c * S;
     const int len = (int)(L - t0 < S ? L - t0 : S);
+    const int nsb = (len + kSB - 1) / kSB;
 
     __shared__ float s_cs[S];  // within-chunk cumulative log decay, log2 units
     __shared__ float s_dt[S];
     __shared__ float s_red[4];
-    __shared__ __attribute__((aligned(16))) T hT[kP][N + kPad];   // H_[c-1]^T
-    __shared__ __attribute__((aligned(16))) T bS[kSB][N + kPad];  // B rows of the s-block
-    __shared__ __attribute__((aligned(16))) T xT[kP][kSB + kPad]; // x^T of the s-block
+    __shared__ __attribute__((aligned(16))) char ht[HT];
+    __shared__ __attribute__((aligned(16))) char xs0[XT];
+    __shared__ __attribute__((aligned(16))) char bs0[BT];
+    __shared__ __attribute__((aligned(16))) char xs1[XT];
+    __shared__ __attribute__((aligned(16))) char bs1[BT];
+    __shared__ __attribute__((aligned(16))) T so[4][16 * kP];  // per-wave output tile
+
+    const char* xg = reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP);
+    const char* bg = reinterpret_cast<const char*>(Bm + ((b * L + t0) * G + g) * N);
+    const int64_t xstride = (int64_t)H * XRB, bstride = (int64_t)G * BRB;
+    auto stage = [&](int sb, char* xd, char* bd) {
+        const int rv = len - sb * kSB;
+        dma_tile<XRB>(xd, xg + sb * kSB * xstride, xstride, kSB, rv, wave, 4, lane);
+        dma_tile<BRB>(bd, bg + sb * kSB * bstride, bstride, kSB, rv, wave, 4, lane);
+    };
+    dma_tile<XRB>(ht, reinterpret_cast<const char*>(states + ((b * M + c) * H + h) * (int64_t)N * kP),
+                  XRB, N, N, wave, 4, lane);
+    stage(0, xs0, bs0);
 
     const float dts = (tid < len) ? dt[(b * L + t0 + tid) * H + h] : 0.f;
     const float cs = block_inclusive_scan(tid < S ? dts * A[h] : 0.f, s_red);
@@ -236,12 +232,6 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
         s_cs[tid] = cs * kLog2e;
         s_dt[tid] = dts;
     }
-    if (tid < N) {
-        const int n8 = tid >> 3, p8 = tid & 7;
-        transpose8x8<T>(states + ((b * M + c) * H + h) * (int64_t)N * kP + (n8 * 8) * kP + p8 * 8,
-                        kP, 8, &hT[p8 * 8][n8 * 8], N + kPad, nullptr);
-    }
-    __syncthreads();
 
     // C rows of this wave's tiles, in fragment layout (row t = lane%16)
     Frag<T> cf[NQ][KS];
@@ -249,21 +239,21 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
         const int t = (wave + 4 * q) * 16 + col;
+        const int tc = t < len ? t : len - 1;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            float v[8];
-            if (t < len) {
-                load8(Cm + ((b * L + t0 + t) * G + g) * N + ks * 32 + grp * 8, v);
-            } else {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) v[i] = 0.f;
-            }
-            cf[q][ks] = make_frag<T>(v);
-        }
-        // inter-chunk term: (C_t exp(cs_t)) H_[c-1]
-        const float sc = fast_exp2(s_cs[t]);
+        for (int ks = 0; ks < KS; ++ks)
+            cf[q][ks] = load_frag(Cm + ((b * L + t0 + tc) * G + g) * N + ks * 32 + grp * 8);
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    wait_dma();
+    __syncthreads();
+
+    // inter-chunk term: (C_t exp(cs_t)) H_[c-1]; H read k-major (k = n)
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int t = (wave + 4 * q) * 16 + col;
+        const float sc = fast_exp2(s_cs[t]);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             float v[8];
@@ -272,33 +262,15 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
             const Frag<T> fa = make_frag<T>(v);
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) {
-                const Frag<T> fh = load_frag(&hT[pt * 16 + col][ks * 32 + grp * 8]);
+                const Frag<T> fh = frag_km<T, XRB>(ht, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4,
+                                                   pt * 16, lane);
                 yacc[q][pt] = mma16(yacc[q][pt], fa, fh);
             }
         }
     }
 
-    for (int sb = 0; sb < S / kSB; ++sb) {
-        __syncthreads();
+    auto consume = [&](int sb, const char* xt, const char* bt) {
         const int s0 = sb * kSB;
-        for (int ci = tid; ci < kSB * (N / 8); ci += kThreads) {
-            const int r = ci / (N / 8), k8 = ci % (N / 8);
-            float v[8];
-            if (s0 + r < len) {
-                load8(Bm + ((b * L + t0 + s0 + r) * G + g) * N + k8 * 8, v);
-            } else {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) v[i] = 0.f;
-            }
-            store8(&bS[r][k8 * 8], v);
-        }
-        if (tid < 64) {
-            const int s8 = tid >> 3, p8 = tid & 7;
-            const int srow = s0 + s8 * 8;
-            transpose8x8<T>(x + ((b * L + t0 + srow) * H + h) * kP + p8 * 8, (int64_t)H * kP,
-                            len - srow, &xT[p8 * 8][s8 * 8], kSB + kPad, nullptr);
-        }
-        __syncthreads();
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int tlo = (wave + 4 * q) * 16;
@@ -312,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
                 for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
                     for (int u = 0; u < 2; ++u) {
-                        const Frag<T> fb = load_frag(&bS[ss * 32 + u * 16 + col][ks * 32 + grp * 8]);
+                        const Frag<T> fb = frag_rowmajor<T, BRB>(bt, ss * 32 + u * 16 + col, ks * 32 + grp * 8);
                         gacc[u] = mma16(gacc[u], fb, cf[q][ks]);
                     }
                 }
@@ -331,25 +303,46 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
                 const Frag<T> fm = make_frag<T>(mv);
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
-                    const T* xr = &xT[pt * 16 + col][ss * 32 + 4 * grp];
-                    const Frag<T> fx = load_frag_2x4<T>(xr, xr + 16);
+                    // x operand rows s = sbase + {4 grp + 0..3, 16 + 4 grp + 0..3}, column p
+                    const Frag<T> fx = frag_km<T, XRB>(xt, ss * 32 + 4 * grp, ss * 32 + 16 + 4 * grp,
+                                                       pt * 16, lane);
                     yacc[q][pt] = mma16(yacc[q][pt], fm, fx);
                 }
             }
         }
+    };
+    for (int sb = 0; sb < nsb; sb += 2) {
+        if (sb + 1 < nsb) stage(sb + 1, xs1, bs1);
+        consume(sb, xs0, bs0);
+        wait_dma();
+        __syncthreads();
+        if (sb + 1 >= nsb) break;
+        if (sb + 2 < nsb) stage(sb + 2, xs0, bs0);
+        consume(sb + 1, xs1, bs1);
+        wait_dma();
+        __syncthreads();
     }
-    // yacc[q][pt][i] = y[t = 16 (wave + 4q) + 4 grp + i][p = 16 pt + col]
+    // yacc[q][pt][i] = y[t = 16 (wave + 4q) + 4 grp + i][p = 16 pt + col]:
+    // each 16-row tile goes through the wave's LDS scratch and leaves as
+    // 16-byte stores of whole rows
+    T* st = so[wave];
 #pragma unroll
-    for (int q = 0; q < NQ; ++q)
+    for (int q = 0; q < NQ; ++q) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int t = (wave + 4 * q) * 16 + 4 * grp + i;
-            if (t < len) {
-                T* yr = y + ((b * L + t0 + t) * H + h) * kP;
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int pt = 0; pt < 4; ++pt) yr[pt * 16 + col] = from_f<T>(yacc[q][pt][i]);
+            for (int pt = 0; pt < 4; ++pt) st[(4 * grp + i) * kP + pt * 16 + col] = from_f<T>(yacc[q][pt][i]);
+        const int tbase = (wave + 4 * q) * 16;
+#pragma unroll
+        for (int e8 = lane; e8 < 16 * (kP / 8); e8 += 64) {
+            const int r = e8 / (kP / 8), k8 = e8 % (kP / 8);
+            if (tbase + r < len) {
+                float v[8];
+                load8(st + r * kP + k8 * 8, v);
+                store8(y + ((b * L + t0 + tbase + r) * H + h) * kP + k8 * 8, v);
             }
         }
+    }
 }
 
 template <typename T, int N, int S>

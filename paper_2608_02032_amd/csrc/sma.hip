@@ -34,12 +34,6 @@ constexpr int kThreads = 256;
 constexpr int kPad = 8;
 constexpr int kTokPerBlock = 256;
 
-// 16-byte global -> LDS copy by DMA.  `lds_wave_base` must be the same for the
-// whole wave; lane i's 16 bytes land at lds_wave_base + 16 i.
-__device__ __forceinline__ void lds_dma16(const void* gsrc, void* lds_wave_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_wave_base, 16, 0, 0);
-}
-
 template <typename T, int N>
 __global__ __launch_bounds__(kThreads) void k_sma_prep(const T* __restrict__ mem,
                                                         T* __restrict__ kfrag,
@@ -121,8 +115,13 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
     const int iw = (int)(wbase / S);                        // this wave's chunk
     const int nj = active ? iw : 0;
 
-    __shared__ __attribute__((aligned(16))) T sk[2][MEMEL];
-    __shared__ __attribute__((aligned(16))) T sv[2][MEMEL];
+    // Two stages as distinct LDS objects: the compiler can then see that the
+    // DMA into one stage does not alias reads of the other, and does not wait
+    // for the prefetch before the current stage's reads.
+    __shared__ __attribute__((aligned(16))) T sk0[MEMEL];
+    __shared__ __attribute__((aligned(16))) T sv0[MEMEL];
+    __shared__ __attribute__((aligned(16))) T sk1[MEMEL];
+    __shared__ __attribute__((aligned(16))) T sv1[MEMEL];
 
     // ---- prologue: Qbar, C and Ebar of this wave's 64 tokens -------------
     Frag<T> qf[RT][KS], cf[RT][KS];
@@ -206,74 +205,78 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
     const int64_t mstride = (int64_t)H * MEMEL;
     const char* kbase = reinterpret_cast<const char*>(kfrag + (b * Mp * H + h) * (int64_t)MEMEL);
     const char* vbase = reinterpret_cast<const char*>(vfrag + (b * Mp * H + h) * (int64_t)MEMEL);
-    if (jmax > 0) {
+    auto fetch = [&](int j, T* kd, T* vd) {
+        const char* kj = kbase + (int64_t)j * mstride * (int64_t)sizeof(T);
+        const char* vj = vbase + (int64_t)j * mstride * (int64_t)sizeof(T);
         for (int pc = wave; pc < PIECES; pc += NW) {
-            lds_dma16(kbase + pc * 1024 + lane * 16, reinterpret_cast<char*>(sk[0]) + pc * 1024);
-            lds_dma16(vbase + pc * 1024 + lane * 16, reinterpret_cast<char*>(sv[0]) + pc * 1024);
+            lds_dma16(kj + pc * 1024 + lane * 16, reinterpret_cast<char*>(kd) + pc * 1024);
+            lds_dma16(vj + pc * 1024 + lane * 16, reinterpret_cast<char*>(vd) + pc * 1024);
         }
-        __builtin_amdgcn_s_waitcnt(0);
+    };
+    // one memory: scores, online softmax, values
+    auto consume = [&](const T* kc, const T* vc) {
+        float lp[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) {
+            f32x4 u[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const Frag<T> fa = load_frag(&kc[((ks * 4 + pt) * 64 + lane) * 8]);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fa, qf[rt][ks]);
+            }
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
+        }
+        float al[RT], pw[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            float l = lp[rt];
+            l += shfl_xor(l, 16);
+            l += shfl_xor(l, 32);
+            const float mn = fmaxf(m[rt], l);
+            al[rt] = fast_exp2(m[rt] - mn);
+            pw[rt] = fast_exp2(l - mn);
+            d[rt] = d[rt] * al[rt] + pw[rt];
+            m[rt] = mn;
+        }
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) {
+            f32x4 v[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const Frag<T> fa = load_frag(&vc[((ks * 4 + pt) * 64 + lane) * 8]);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fa, cf[rt][ks]);
+            }
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) o[rt][pt] = o[rt][pt] * al[rt] + pw[rt] * v[rt];
+        }
+    };
+    if (jmax > 0) {
+        fetch(0, sk0, sv0);
+        wait_dma();
     }
     __syncthreads();
-    for (int j = 0; j < jmax; ++j) {
-        const int cur = j & 1;
-        if (j + 1 < jmax) {
-            const char* kj = kbase + (int64_t)(j + 1) * mstride * (int64_t)sizeof(T);
-            const char* vj = vbase + (int64_t)(j + 1) * mstride * (int64_t)sizeof(T);
-            for (int pc = wave; pc < PIECES; pc += NW) {
-                lds_dma16(kj + pc * 1024 + lane * 16, reinterpret_cast<char*>(sk[cur ^ 1]) + pc * 1024);
-                lds_dma16(vj + pc * 1024 + lane * 16, reinterpret_cast<char*>(sv[cur ^ 1]) + pc * 1024);
-            }
-        }
-        if (j < nj) {
-            // scores: l_t = sum_p U^T[p,t] Ebar[t,p]
-            float lp[RT];
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                f32x4 u[RT];
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const Frag<T> fa = load_frag(&sk[cur][((ks * 4 + pt) * 64 + lane) * 8]);
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fa, qf[rt][ks]);
-                }
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
-            }
-            float al[RT], pw[RT];
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                float l = lp[rt];
-                l += shfl_xor(l, 16);
-                l += shfl_xor(l, 32);
-                const float mn = fmaxf(m[rt], l);
-                al[rt] = fast_exp2(m[rt] - mn);
-                pw[rt] = fast_exp2(l - mn);
-                d[rt] = d[rt] * al[rt] + pw[rt];
-                m[rt] = mn;
-            }
-            // values: O = alpha O + g V
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                f32x4 v[RT];
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const Frag<T> fa = load_frag(&sv[cur][((ks * 4 + pt) * 64 + lane) * 8]);
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fa, cf[rt][ks]);
-                }
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) o[rt][pt] = o[rt][pt] * al[rt] + pw[rt] * v[rt];
-            }
-        }
-        __builtin_amdgcn_s_waitcnt(0);  // this wave's copies of memory j+1 have landed
+    // ping-pong: memory j is consumed from one stage while j+1 streams into
+    // the other; one barrier per memory
+    for (int j = 0; j < jmax; j += 2) {
+        if (j + 1 < jmax) fetch(j + 1, sk1, sv1);
+        if (j < nj) consume(sk0, sv0);
+        wait_dma();
+        __syncthreads();
+        if (j + 1 >= jmax) break;
+        if (j + 2 < jmax) fetch(j + 2, sk0, sv0);
+        if (j + 1 < nj) consume(sk1, sv1);
+        wait_dma();
         __syncthreads();
     }
 
