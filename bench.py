@@ -129,6 +129,7 @@ def main():
     import numpy as np
     import torch
     from paper_2608_02032_amd import dart, synth
+    from paper_2608_02032_amd.profiling import traffic_for
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -225,7 +226,8 @@ def main():
     main_tflops = mflops / (main_ms * 1e-3) / 1e12
     roofline = {"kernel": "k_sma_main", "bound": "mfma",
                 "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": traffic_for("k_sma_main"),
                 "avg_us": round(main_ms * 1e3, 2),
                 "algorithmic_flops_per_launch": mflops}
     extra = {
@@ -247,7 +249,8 @@ def main():
             "hbm_gbps": round(dbytes / (dec_mean * 1e-3) / 1e9, 1),
             "hbm_frac": round(dbytes / (dec_mean * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
             "algorithmic_bytes": dbytes,
-            "k_decode_partial_gbps": round(cache_bytes / (part_ms * 1e-3) / 1e9, 1)}
+            "k_decode_partial_gbps": round(cache_bytes / (part_ms * 1e-3) / 1e9, 1),
+            "k_decode_partial_traffic": traffic_for("k_decode_partial")}
 
     tokens = B * L
     line = {

@@ -145,6 +145,14 @@ __device__ __forceinline__ void lds_dma16(const void* gsrc, void* lds_wave_base)
                                      16, 0, 0);
 }
 __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0); }
+// s_waitcnt immediate that waits until at most k vector-memory operations of
+// the wave are outstanding (expcnt and lgkmcnt left unconstrained; gfx9
+// encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+// Workgroup execution barrier without the memory fence of __syncthreads():
+// used in streaming loops where each wave first waits for its own LDS copies
+// (vmcnt) and every LDS read of a stage is consumed before the barrier.
+__device__ __forceinline__ void block_barrier() { __builtin_amdgcn_s_barrier(); }
+constexpr int vmcnt_imm(int k) { return (k & 15) | (7 << 4) | (15 << 8) | ((k >> 4) << 14); }
 
 // A natural-layout tile of rows of RB bytes in LDS whose 16-byte chunks are
 // XOR-swizzled by row (chunk c of row r is stored at chunk c ^ (r & MASK)), so

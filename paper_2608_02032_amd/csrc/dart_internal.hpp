@@ -39,8 +39,9 @@ hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const voi
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
                       float* lse, void* ws, hipStream_t st);
 
-// Decode: per-split partial softmax statistics [B][H][nsplit][P+2] (float).
-constexpr int kDecodeMemPerSplit = 16;
+// Decode: per-split partial softmax statistics [B][H][nsplit][P+2] and the
+// SSM readout y_ssd [B][H][P] (float).
+constexpr int kDecodeMinMemPerSplit = 8;  // smallest split size the workspace allows
 size_t decode_workspace_bytes(const Shape& s);
 hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
                          const float* dt, const float* A, const void* Bm, const void* Cm,

@@ -7,26 +7,47 @@
 // cached memory: the step is a stream over B*H*m*N*P storage elements and is
 // bound by HBM bandwidth.
 //
-//   k_decode_partial  grid (split, head, batch): each block streams up to
-//                     kDecodeMemPerSplit memories (one wave per memory at a
-//                     time, lanes own 8 consecutive p of N/8 rows), computes
-//                     r, the logit and C dH on the fly and keeps an online
-//                     softmax (m, d, O[P]); waves are merged in LDS and one
-//                     partial per split goes to the workspace.
-//   k_decode_finish   grid (head, batch): recurrent update of h_state and of
-//                     the running chunk contribution, y_ssd = C h_state,
-//                     deterministic merge of the split partials, the gate, and
-//                     the append of the running contribution when the token
-//                     closes its chunk (slot m, never read by this step).
+//   k_decode_partial      grid (split, head, batch): each block streams up to
+//                         decode_mps() memories, one wave per memory at a time;
+//                         lanes own 8 consecutive p of N/8 rows.  Each wave
+//                         keeps the next memory's rows in flight while it
+//                         reduces the current one (r, the logit and C dH on
+//                         the fly; online softmax (m, d, O[P])).  Waves merge
+//                         in LDS; one partial per split goes to the workspace.
+//   k_decode_state_merge  grid (head, batch): recurrent update of h_state and
+//                         of the running chunk contribution, y_ssd = C h_state,
+//                         the append of the running contribution when the
+//                         token closes its chunk (slot m, never read by this
+//                         step), the deterministic LSE merge of the split
+//                         partials and y = y_ssd + SiLU(z) R.
+// Keeping the state traffic out of the streaming kernel measured faster than
+// giving it to one split per head (that split then lags the others).
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
+
+#include <cstdlib>
 
 namespace dart {
 namespace {
 
 constexpr int kP = 64;
 constexpr int kThreads = 256;
-constexpr int kMPS = kDecodeMemPerSplit;
+// Memories per split.  Long splits amortise each block's set-up; the split
+// size is halved (down to 8) while that leaves fewer than 16384 blocks.
+// DART_DECODE_MPS in {8, 16, 32, 64} forces a size (tuning); the workspace is
+// sized for the smallest.
+int decode_mps(int64_t bh, int64_t m) {
+    static const int forced = [] {
+        const char* e = getenv("DART_DECODE_MPS");
+        const int x = e ? atoi(e) : 0;
+        return (x == 8 || x == 16 || x == 32 || x == 64) ? x : 0;
+    }();
+    if (forced) return forced;
+    int mps = 64;
+    while (mps > 8 && bh * ((m + mps - 1) / mps) < 16384) mps >>= 1;
+    return mps;
+}
+constexpr int kMinMPS = kDecodeMinMemPerSplit;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -52,179 +73,25 @@ __device__ __forceinline__ void load_row(const float* p, RowChunk<float>& r) {
     r.b = *reinterpret_cast<const f32x4*>(p + 4);
 }
 
-template <typename T, int N>
-__global__ __launch_bounds__(kThreads) void k_decode_partial(
-    const T* __restrict__ mem, const T* __restrict__ q, const T* __restrict__ e,
-    const T* __restrict__ Cm, const float* __restrict__ qw, const float* __restrict__ ew,
-    float* __restrict__ part, float eps, int normalize, int H, int G, int64_t Mcap, int64_t m,
-    int nsplit) {
-    constexpr int R = N / 8;  // rows per lane (row n = rg + 8 k)
-    const int s = blockIdx.x, h = blockIdx.y;
-    const int64_t b = blockIdx.z;
-    const int g = (int)((int64_t)h * G / H);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int po = lane & 7, rg = lane >> 3;
-
-    __shared__ float s_q[N];
-    __shared__ float s_e[kP];
-    __shared__ float s_part[4][kP + 2];
-
-    if (wave == 0) {
-        const float v0 = lane < N ? to_f(q[(b * G + g) * N + lane]) : 0.f;
-        const float v1 = lane + 64 < N ? to_f(q[(b * G + g) * N + lane + 64]) : 0.f;
-        float ss = v0 * v0 + v1 * v1;
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
-        const float inv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) *
-                          (kLog2e / sqrtf((float)N));
-        if (lane < N) s_q[lane] = v0 * inv * (qw ? qw[lane] : 1.0f);
-        if (lane + 64 < N) s_q[lane + 64] = v1 * inv * (qw ? qw[lane + 64] : 1.0f);
-    } else if (wave == 1) {
-        const float v = to_f(e[(b * G + g) * kP + lane]);
-        float ss = v * v;
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
-        const float inv = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
-        s_e[lane] = v * inv * (ew ? ew[lane] : 1.0f);
-    }
-    __syncthreads();
-
-    float eb[8], qb[R], cb[R];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) eb[i] = s_e[po * 8 + i];
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-        qb[k] = s_q[rg + 8 * k];
-        cb[k] = to_f(Cm[(b * G + g) * N + rg + 8 * k]);
-    }
-    // packed bf16 copies for the dot2 path
-    uint32_t ebp[4], cbp[R / 2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) ebp[i] = pack_bf2(eb[2 * i], eb[2 * i + 1]);
-#pragma unroll
-    for (int k = 0; k < R / 2; ++k) cbp[k] = pack_bf2(cb[2 * k], cb[2 * k + 1]);
-
-    float mx = -INFINITY, den = 0.f, o[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] = 0.f;
-    const int64_t j0 = (int64_t)s * kMPS;
-    const int64_t j1 = (j0 + kMPS < m) ? j0 + kMPS : m;
-    for (int64_t j = j0 + wave; j < j1; j += 4) {
-        const T* src = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
-        RowChunk<T> xr[R];
-#pragma unroll
-        for (int k = 0; k < R; ++k) load_row(src + (rg + 8 * k) * kP + po * 8, xr[k]);
-        float lsum = 0.f, v[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = 0.f;
-#pragma unroll
-        for (int k = 0; k < R; ++k) {
-            float ss, kv;
-            if constexpr (sizeof(T) == 2) {
-                const uint32_t w[4] = {xr[k].v.x, xr[k].v.y, xr[k].v.z, xr[k].v.w};
-                ss = dot2(w[0], w[0], 0.f);
-                kv = dot2(w[0], ebp[0], 0.f);
-#pragma unroll
-                for (int i = 1; i < 4; ++i) {
-                    ss = dot2(w[i], w[i], ss);
-                    kv = dot2(w[i], ebp[i], kv);
-                }
-                if (k & 1) {
-                    // value side: pair rows k-1 and k so one dot2 covers both
-                    const uint32_t u[4] = {xr[k - 1].v.x, xr[k - 1].v.y, xr[k - 1].v.z, xr[k - 1].v.w};
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const uint32_t lo = (u[i] & 0xffffu) | (w[i] << 16);
-                        const uint32_t hi = (u[i] >> 16) | (w[i] & 0xffff0000u);
-                        v[2 * i] = dot2(lo, cbp[k >> 1], v[2 * i]);
-                        v[2 * i + 1] = dot2(hi, cbp[k >> 1], v[2 * i + 1]);
-                    }
-                }
-            } else {
-                const float xv[8] = {xr[k].a[0], xr[k].a[1], xr[k].a[2], xr[k].a[3],
-                                     xr[k].b[0], xr[k].b[1], xr[k].b[2], xr[k].b[3]};
-                ss = 0.f;
-                kv = 0.f;
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    ss += xv[i] * xv[i];
-                    kv += xv[i] * eb[i];
-                    v[i] += cb[k] * xv[i];
-                }
-            }
-            ss += shfl_xor(ss, 1);
-            kv += shfl_xor(kv, 1);
-            ss += shfl_xor(ss, 2);
-            kv += shfl_xor(kv, 2);
-            ss += shfl_xor(ss, 4);
-            kv += shfl_xor(kv, 4);
-            const float r = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
-            lsum += qb[k] * r * kv;
-        }
-        lsum += shfl_xor(lsum, 8);
-        lsum += shfl_xor(lsum, 16);
-        lsum += shfl_xor(lsum, 32);
-        const float mn = fmaxf(mx, lsum);
-        const float al = fast_exp2(mx - mn), pw = fast_exp2(lsum - mn);
-        den = den * al + pw;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[i] = o[i] * al + pw * v[i];
-        mx = mn;
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        o[i] += shfl_xor(o[i], 8);
-        o[i] += shfl_xor(o[i], 16);
-        o[i] += shfl_xor(o[i], 32);
-    }
-    if (rg == 0) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s_part[wave][po * 8 + i] = o[i];
-    }
-    if (lane == 0) {
-        s_part[wave][kP] = mx;
-        s_part[wave][kP + 1] = den;
-    }
-    __syncthreads();
-    if (tid < kP) {
-        float M = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) M = fmaxf(M, s_part[w][kP]);
-        float D = 0.f, O = 0.f;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const float mw = s_part[w][kP];
-            if (mw == -INFINITY) continue;
-            const float sc = fast_exp2(mw - M);
-            D += s_part[w][kP + 1] * sc;
-            O += s_part[w][tid] * sc;
-        }
-        float* out = part + (((b * H + h) * nsplit) + s) * (kP + 2);
-        out[tid] = O;
-        if (tid == 0) {
-            out[kP] = M;
-            out[kP + 1] = D;
-        }
-    }
+// Workspace layout: partials [B][H][nsplit][P+2] (O[P], m, d), then y_ssd
+// [B][H][P] (float).
+inline size_t decode_part_floats(int64_t B, int H, int nsplit) {
+    return (size_t)B * H * nsplit * (kP + 2);
 }
 
 template <typename T, int N>
-__global__ __launch_bounds__(kThreads) void k_decode_finish(
-    const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
-    const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ z,
-    float* __restrict__ h_state, float* __restrict__ chunk_acc, T* __restrict__ mem,
-    T* __restrict__ y, const float* __restrict__ part, int H, int G, int S, int64_t Mcap,
-    int64_t pos, int64_t m, int nsplit, int z_per_head) {
-    const int h = blockIdx.x;
-    const int64_t b = blockIdx.y;
-    const int g = (int)((int64_t)h * G / H);
+__device__ __forceinline__ void state_update(const T* __restrict__ x, const float* __restrict__ dt,
+                                             const float* __restrict__ A, const T* __restrict__ Bm,
+                                             const T* __restrict__ Cm, float* __restrict__ h_state,
+                                             float* __restrict__ chunk_acc, T* __restrict__ mem,
+                                             float* __restrict__ yssd, int H, int G, int S,
+                                             int64_t Mcap, int64_t pos, int64_t m, int64_t b, int h,
+                                             int g, float* s_x, float* s_B, float* s_C,
+                                             float (*s_y)[kP]) {
     const int tid = threadIdx.x;
     const int pq = tid & 15, rg = tid >> 4;  // p quad, row group
     const bool reset = (pos % S) == 0;
     const bool append = (pos % S) == S - 1;
-
-    __shared__ float s_x[kP], s_B[N], s_C[N];
-    __shared__ float s_y[16][kP];
     if (tid < kP) s_x[tid] = to_f(x[(b * H + h) * kP + tid]);
     if (tid < N) {
         s_B[tid] = to_f(Bm[(b * G + g) * N + tid]);
@@ -266,23 +133,219 @@ __global__ __launch_bounds__(kThreads) void k_decode_finish(
         float ys = 0.f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) ys += s_y[r][tid];
-        float R = 0.f;
-        if (m > 0) {
-            const int ns = (int)((m + kMPS - 1) / kMPS);
-            const float* pb = part + (b * H + h) * nsplit * (int64_t)(kP + 2);
-            float M = -INFINITY;
-            for (int s = 0; s < ns; ++s) M = fmaxf(M, pb[s * (kP + 2) + kP]);
-            float D = 0.f, O = 0.f;
-            for (int s = 0; s < ns; ++s) {
-                const float sc = fast_exp2(pb[s * (kP + 2) + kP] - M);
-                D += pb[s * (kP + 2) + kP + 1] * sc;
-                O += pb[s * (kP + 2) + tid] * sc;
-            }
-            R = O / D;
-        }
-        const float zz = to_f(z_per_head ? z[b * H + h] : z[b]);
-        y[(b * H + h) * kP + tid] = from_f<T>(ys + silu(zz) * R);
+        yssd[(b * H + h) * kP + tid] = ys;
     }
+}
+
+template <typename T, int N>
+__global__ __launch_bounds__(kThreads) void k_decode_partial(
+    const T* __restrict__ mem_rd, const T* __restrict__ q, const T* __restrict__ e,
+    const T* __restrict__ Cm, const float* __restrict__ qw, const float* __restrict__ ew,
+    float* __restrict__ part, float eps, int normalize, int H, int G, int64_t Mcap, int64_t m,
+    int nsplit, int mps) {
+    constexpr int R = N / 8;  // rows per lane (row n = rg + 8 k)
+    const int s = blockIdx.x, h = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int g = (int)((int64_t)h * G / H);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int po = lane & 7, rg = lane >> 3;
+
+    __shared__ float s_q[N];
+    __shared__ float s_e[kP];
+    __shared__ float s_part[4][kP + 2];
+
+    const int64_t j0 = (int64_t)s * mps;
+    const int64_t j1 = (j0 + mps < m) ? j0 + mps : m;
+    if (j0 >= j1) return;  // block-uniform: no cached memory in this split
+
+    if (wave == 0) {
+        const float v0 = lane < N ? to_f(q[(b * G + g) * N + lane]) : 0.f;
+        const float v1 = lane + 64 < N ? to_f(q[(b * G + g) * N + lane + 64]) : 0.f;
+        float ss = v0 * v0 + v1 * v1;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
+        const float inv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) *
+                          (kLog2e / sqrtf((float)N));
+        if (lane < N) s_q[lane] = v0 * inv * (qw ? qw[lane] : 1.0f);
+        if (lane + 64 < N) s_q[lane + 64] = v1 * inv * (qw ? qw[lane + 64] : 1.0f);
+    } else if (wave == 1) {
+        const float v = to_f(e[(b * G + g) * kP + lane]);
+        float ss = v * v;
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) ss += shfl_xor(ss, o);
+        const float inv = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
+        s_e[lane] = v * inv * (ew ? ew[lane] : 1.0f);
+    }
+    __syncthreads();
+
+    float eb[8], qb[R], cb[R];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) eb[i] = s_e[po * 8 + i];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        qb[k] = s_q[rg + 8 * k];
+        cb[k] = to_f(Cm[(b * G + g) * N + rg + 8 * k]);
+    }
+    // packed bf16 copies for the dot2 path
+    uint32_t ebp[4], cbp[R / 2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) ebp[i] = pack_bf2(eb[2 * i], eb[2 * i + 1]);
+#pragma unroll
+    for (int k = 0; k < R / 2; ++k) cbp[k] = pack_bf2(cb[2 * k], cb[2 * k + 1]);
+
+    float mx = -INFINITY, den = 0.f, o[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = 0.f;
+
+    auto load_mem = [&](int64_t j, RowChunk<T>(&xr)[R]) {
+        const T* src = mem_rd + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
+#pragma unroll
+        for (int k = 0; k < R; ++k) load_row(src + (rg + 8 * k) * kP + po * 8, xr[k]);
+    };
+    auto reduce_mem = [&](const RowChunk<T>(&xr)[R]) {
+        float lsum = 0.f, v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = 0.f;
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            float ss, kv;
+            if constexpr (sizeof(T) == 2) {
+                const uint32_t w[4] = {xr[k].v.x, xr[k].v.y, xr[k].v.z, xr[k].v.w};
+                ss = dot2(w[0], w[0], 0.f);
+                kv = dot2(w[0], ebp[0], 0.f);
+#pragma unroll
+                for (int i = 1; i < 4; ++i) {
+                    ss = dot2(w[i], w[i], ss);
+                    kv = dot2(w[i], ebp[i], kv);
+                }
+                if (k & 1) {
+                    // value side: pair rows k-1 and k so one dot2 covers both
+                    const uint32_t u[4] = {xr[k - 1].v.x, xr[k - 1].v.y, xr[k - 1].v.z,
+                                           xr[k - 1].v.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const uint32_t lo = (u[i] & 0xffffu) | (w[i] << 16);
+                        const uint32_t hi = (u[i] >> 16) | (w[i] & 0xffff0000u);
+                        v[2 * i] = dot2(lo, cbp[k >> 1], v[2 * i]);
+                        v[2 * i + 1] = dot2(hi, cbp[k >> 1], v[2 * i + 1]);
+                    }
+                }
+            } else {
+                const float xv[8] = {xr[k].a[0], xr[k].a[1], xr[k].a[2], xr[k].a[3],
+                                     xr[k].b[0], xr[k].b[1], xr[k].b[2], xr[k].b[3]};
+                ss = 0.f;
+                kv = 0.f;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    ss += xv[i] * xv[i];
+                    kv += xv[i] * eb[i];
+                    v[i] += cb[k] * xv[i];
+                }
+            }
+            ss += shfl_xor(ss, 1);
+            kv += shfl_xor(kv, 1);
+            ss += shfl_xor(ss, 2);
+            kv += shfl_xor(kv, 2);
+            ss += shfl_xor(ss, 4);
+            kv += shfl_xor(kv, 4);
+            const float r = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
+            lsum += qb[k] * r * kv;
+        }
+        lsum += shfl_xor(lsum, 8);
+        lsum += shfl_xor(lsum, 16);
+        lsum += shfl_xor(lsum, 32);
+        const float mn = fmaxf(mx, lsum);
+        const float al = fast_exp2(mx - mn), pw = fast_exp2(lsum - mn);
+        den = den * al + pw;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = o[i] * al + pw * v[i];
+        mx = mn;
+    };
+    // wave w takes memories j0 + w, j0 + w + 4, ...; the next one's rows are
+    // loaded before the current one is reduced (two register buffers)
+    RowChunk<T> xa[R], xb[R];
+    int64_t j = j0 + wave;
+    if (j < j1) load_mem(j, xa);
+    while (j < j1) {
+        if (j + 4 < j1) load_mem(j + 4, xb);
+        reduce_mem(xa);
+        j += 4;
+        if (j >= j1) break;
+        if (j + 4 < j1) load_mem(j + 4, xa);
+        reduce_mem(xb);
+        j += 4;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        o[i] += shfl_xor(o[i], 8);
+        o[i] += shfl_xor(o[i], 16);
+        o[i] += shfl_xor(o[i], 32);
+    }
+    if (rg == 0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s_part[wave][po * 8 + i] = o[i];
+    }
+    if (lane == 0) {
+        s_part[wave][kP] = mx;
+        s_part[wave][kP + 1] = den;
+    }
+    __syncthreads();
+    if (tid < kP) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) M = fmaxf(M, s_part[w][kP]);
+        float D = 0.f, O = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float mw = s_part[w][kP];
+            if (mw == -INFINITY) continue;
+            const float sc = fast_exp2(mw - M);
+            D += s_part[w][kP + 1] * sc;
+            O += s_part[w][tid] * sc;
+        }
+        float* out = part + (((b * H + h) * nsplit) + s) * (kP + 2);
+        out[tid] = O;
+        if (tid == 0) {
+            out[kP] = M;
+            out[kP + 1] = D;
+        }
+    }
+}
+
+// Recurrent update (h_state, running chunk contribution, y_ssd, append), then
+// the deterministic LSE merge of the split partials and the gate.
+template <typename T, int N>
+__global__ __launch_bounds__(kThreads) void k_decode_state_merge(
+    const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
+    const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ z,
+    float* __restrict__ h_state, float* __restrict__ chunk_acc, T* __restrict__ mem,
+    T* __restrict__ y, const float* __restrict__ part, float* __restrict__ yssd, int H, int G,
+    int S, int64_t Mcap, int64_t pos, int64_t m, int nsplit, int z_per_head, int mps) {
+    const int h = blockIdx.x;
+    const int64_t b = blockIdx.y;
+    const int g = (int)((int64_t)h * G / H);
+    __shared__ float s_x[kP], s_B[N], s_C[N];
+    __shared__ float s_y[16][kP];
+    state_update<T, N>(x, dt, A, Bm, Cm, h_state, chunk_acc, mem, yssd, H, G, S, Mcap, pos, m, b,
+                       h, g, s_x, s_B, s_C, s_y);
+    const int p = threadIdx.x;
+    if (p >= kP) return;
+    float R = 0.f;
+    if (m > 0) {
+        const int ns = (int)((m + mps - 1) / mps);
+        const float* pb = part + (b * H + h) * nsplit * (int64_t)(kP + 2);
+        float M = -INFINITY;
+        for (int s = 0; s < ns; ++s) M = fmaxf(M, pb[s * (kP + 2) + kP]);
+        float D = 0.f, O = 0.f;
+        for (int s = 0; s < ns; ++s) {
+            const float sc = fast_exp2(pb[s * (kP + 2) + kP] - M);
+            D += pb[s * (kP + 2) + kP + 1] * sc;
+            O += pb[s * (kP + 2) + p] * sc;
+        }
+        R = O / D;
+    }
+    const float zz = to_f(z_per_head ? z[b * H + h] : z[b]);
+    y[(b * H + h) * kP + p] = from_f<T>(yssd[(b * H + h) * kP + p] + silu(zz) * R);
 }
 
 template <typename T, int N>
@@ -291,21 +354,22 @@ hipError_t run_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void*
                       const void* q, const void* e, const void* z, float* h_state,
                       float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st) {
     const int64_t m = pos / s.S;
-    const int nsplit_cap = (int)((s.Mcap + kMPS - 1) / kMPS);
+    const int mps = decode_mps(s.B * s.H, m);
+    const int nsplit_cap = (int)((s.Mcap + kMinMPS - 1) / kMinMPS);
     float* part = reinterpret_cast<float*>(ws);
+    float* yssd = part + decode_part_floats(s.B, s.H, nsplit_cap);
     if (m > 0) {
-        const int ns = (int)((m + kMPS - 1) / kMPS);
+        const int ns = (int)((m + mps - 1) / mps);
         prof_begin("k_decode_partial", st);
-        k_decode_partial<T, N><<<dim3((unsigned)ns, (unsigned)s.H, (unsigned)s.B), kThreads, 0,
-                                 st>>>((const T*)mem, (const T*)q, (const T*)e, (const T*)Cm,
-                                       a.qw, a.ew, part, a.eps, a.normalize, s.H, s.G, s.Mcap, m,
-                                       nsplit_cap);
+        k_decode_partial<T, N><<<dim3((unsigned)ns, (unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
+            (const T*)mem, (const T*)q, (const T*)e, (const T*)Cm, a.qw, a.ew, part, a.eps,
+            a.normalize, s.H, s.G, s.Mcap, m, nsplit_cap, mps);
         prof_end(st);
     }
-    prof_begin("k_decode_finish", st);
-    k_decode_finish<T, N><<<dim3((unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
+    prof_begin("k_decode_state_merge", st);
+    k_decode_state_merge<T, N><<<dim3((unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
         (const T*)x, dt, A, (const T*)Bm, (const T*)Cm, (const T*)z, h_state, chunk_acc, (T*)mem,
-        (T*)y, part, s.H, s.G, s.S, s.Mcap, pos, m, nsplit_cap, a.z_per_head);
+        (T*)y, part, yssd, s.H, s.G, s.S, s.Mcap, pos, m, nsplit_cap, a.z_per_head, mps);
     prof_end(st);
     return hipGetLastError();
 }
@@ -326,8 +390,9 @@ hipError_t run_decode_n(const Shape& s, const SmaArgs& a, int64_t pos, const voi
 }  // namespace
 
 size_t decode_workspace_bytes(const Shape& s) {
-    const int64_t nsplit = (s.Mcap + kMPS - 1) / kMPS;
-    return align256(sizeof(float) * s.B * s.H * (size_t)(nsplit > 0 ? nsplit : 1) * (s.P + 2));
+    const int64_t nsplit = (s.Mcap + kMinMPS - 1) / kMinMPS;
+    return align256(sizeof(float) * (decode_part_floats(s.B, s.H, (int)(nsplit > 0 ? nsplit : 1)) +
+                                     (size_t)s.B * s.H * s.P));
 }
 
 hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,

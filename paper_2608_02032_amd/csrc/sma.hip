@@ -97,10 +97,21 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
     static_assert(PIECES * 1024 == MEMEL * (int)sizeof(T), "memory must be whole fragments");
     static_assert(S >= WT, "a wave's tokens must lie in one chunk");
 
-    // heaviest token blocks first; consecutive blocks walk over (b, h)
+    // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
+    // index, and each XCD has its own L2.  When B*H is a multiple of 8, XCD x
+    // runs whole heads (b, h) = x, x+8, ... one after another, heaviest token
+    // block first, so all blocks reading one head's memories share one L2.
     const int64_t bid = blockIdx.x;
-    const int blk = nblk - 1 - (int)(bid / BH);
-    const int64_t bh = bid % BH;
+    int blk;
+    int64_t bh;
+    if (BH % 8 == 0) {
+        const int64_t slot = bid >> 3;
+        blk = nblk - 1 - (int)(slot % nblk);
+        bh = (slot / nblk) * 8 + (bid & 7);
+    } else {
+        blk = nblk - 1 - (int)(bid / BH);
+        bh = bid % BH;
+    }
     const int64_t b = bh / H;
     const int h = (int)(bh % H);
     const int g = (int)((int64_t)h * G / H);
@@ -115,13 +126,14 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
     const int iw = (int)(wbase / S);                        // this wave's chunk
     const int nj = active ? iw : 0;
 
-    // Two stages as distinct LDS objects: the compiler can then see that the
-    // DMA into one stage does not alias reads of the other, and does not wait
-    // for the prefetch before the current stage's reads.
-    __shared__ __attribute__((aligned(16))) T sk0[MEMEL];
-    __shared__ __attribute__((aligned(16))) T sv0[MEMEL];
-    __shared__ __attribute__((aligned(16))) T sk1[MEMEL];
-    __shared__ __attribute__((aligned(16))) T sv1[MEMEL];
+    // Three stages (key copy then value copy of one memory each) as distinct
+    // LDS objects: the compiler can see that a DMA into one stage does not
+    // alias reads of another, so prefetches two memories ahead overlap the
+    // MFMAs instead of being waited for.
+    constexpr bool kThree = 3 * 2 * MEMEL * (int)sizeof(T) <= 160 * 1024;
+    __shared__ __attribute__((aligned(16))) T st0[2 * MEMEL];
+    __shared__ __attribute__((aligned(16))) T st1[2 * MEMEL];
+    __shared__ __attribute__((aligned(16))) T st2[kThree ? 2 * MEMEL : 8];
 
     // ---- prologue: Qbar, C and Ebar of this wave's 64 tokens -------------
     Frag<T> qf[RT][KS], cf[RT][KS];
@@ -150,9 +162,12 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const float w = qw ? qw[ks * 32 + grp * 8 + i] : 1.0f;
-                qv[ks][i] *= qinv * w;
+            for (int i = 0; i < 8; ++i) qv[ks][i] *= qinv;
+            if (qw) {
+                float w[8];
+                load8(qw + ks * 32 + grp * 8, w);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) qv[ks][i] *= w[i];
             }
             qf[rt][ks] = make_frag<T>(qv[ks]);
             float cv[8];
@@ -180,12 +195,16 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
         es += shfl_xor(es, 32);
         const float einv = normalize ? 1.0f / sqrtf(es * (1.0f / kP) + eps) : 1.0f;
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt)
+        for (int pt = 0; pt < 4; ++pt) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float w = ew ? ew[pt * 16 + grp * 4 + i] : 1.0f;
-                ef[rt][pt][i] *= einv * w;
+            for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= einv;
+            if (ew) {
+                float w[4];
+                load4(ew + pt * 16 + grp * 4, w);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= w[i];
             }
+        }
     }
 
     float m[RT], d[RT];
@@ -205,15 +224,19 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
     const int64_t mstride = (int64_t)H * MEMEL;
     const char* kbase = reinterpret_cast<const char*>(kfrag + (b * Mp * H + h) * (int64_t)MEMEL);
     const char* vbase = reinterpret_cast<const char*>(vfrag + (b * Mp * H + h) * (int64_t)MEMEL);
-    auto fetch = [&](int j, T* kd, T* vd) {
+    static_assert(PIECES % NW == 0, "every wave copies the same number of fragments");
+    constexpr int kDmaPerMem = 2 * PIECES / NW;  // DMA instructions per memory per wave
+    auto fetch = [&](int j, T* dstage) {
         const char* kj = kbase + (int64_t)j * mstride * (int64_t)sizeof(T);
         const char* vj = vbase + (int64_t)j * mstride * (int64_t)sizeof(T);
+        char* kd = reinterpret_cast<char*>(dstage);
+        char* vd = kd + MEMEL * (int)sizeof(T);
+#pragma unroll
         for (int pc = wave; pc < PIECES; pc += NW) {
-            lds_dma16(kj + pc * 1024 + lane * 16, reinterpret_cast<char*>(kd) + pc * 1024);
-            lds_dma16(vj + pc * 1024 + lane * 16, reinterpret_cast<char*>(vd) + pc * 1024);
+            lds_dma16(kj + pc * 1024 + lane * 16, kd + pc * 1024);
+            lds_dma16(vj + pc * 1024 + lane * 16, vd + pc * 1024);
         }
     };
-    // one memory: scores, online softmax, values
     auto consume = [&](const T* kc, const T* vc) {
         float lp[RT];
 #pragma unroll
@@ -261,23 +284,53 @@ __global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
             for (int rt = 0; rt < RT; ++rt) o[rt][pt] = o[rt][pt] * al[rt] + pw[rt] * v[rt];
         }
     };
-    if (jmax > 0) {
-        fetch(0, sk0, sv0);
-        wait_dma();
-    }
-    __syncthreads();
-    // ping-pong: memory j is consumed from one stage while j+1 streams into
-    // the other; one barrier per memory
-    for (int j = 0; j < jmax; j += 2) {
-        if (j + 1 < jmax) fetch(j + 1, sk1, sv1);
-        if (j < nj) consume(sk0, sv0);
+    // wait until at most `pending` memories' copies of this wave are in flight
+    auto wait_copies = [&](bool one_pending) {
+        if (one_pending) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerMem));
+        } else {
+            wait_dma();
+        }
+    };
+    if constexpr (kThree) {
+        if (jmax > 0) fetch(0, st0);
+        if (jmax > 1) fetch(1, st1);
+        wait_copies(jmax > 1);
+        block_barrier();
+        // memory j is consumed from stage j % 3 while j+1 (already issued) and j+2
+        // stream into the other two; one barrier per memory
+        for (int j = 0; j < jmax; j += 3) {
+            if (j + 2 < jmax) fetch(j + 2, st2);
+            if (j < nj) consume(st0, st0 + MEMEL);
+            wait_copies(j + 2 < jmax);
+            block_barrier();
+            if (j + 1 >= jmax) break;
+            if (j + 3 < jmax) fetch(j + 3, st0);
+            if (j + 1 < nj) consume(st1, st1 + MEMEL);
+            wait_copies(j + 3 < jmax);
+            block_barrier();
+            if (j + 2 >= jmax) break;
+            if (j + 4 < jmax) fetch(j + 4, st1);
+            if (j + 2 < nj) consume(st2, st2 + MEMEL);
+            wait_copies(j + 4 < jmax);
+            block_barrier();
+        }
+    } else {
+        // two stages (when three do not fit in LDS): j+1 streams while j is consumed
+        if (jmax > 0) fetch(0, st0);
         wait_dma();
         __syncthreads();
-        if (j + 1 >= jmax) break;
-        if (j + 2 < jmax) fetch(j + 2, sk0, sv0);
-        if (j + 1 < nj) consume(sk1, sv1);
-        wait_dma();
-        __syncthreads();
+        for (int j = 0; j < jmax; j += 2) {
+            if (j + 1 < jmax) fetch(j + 1, st1);
+            if (j < nj) consume(st0, st0 + MEMEL);
+            wait_dma();
+            __syncthreads();
+            if (j + 1 >= jmax) break;
+            if (j + 2 < jmax) fetch(j + 2, st0);
+            if (j + 1 < nj) consume(st1, st1 + MEMEL);
+            wait_dma();
+            __syncthreads();
+        }
     }
 
     // ---- epilogue: y = y_ssd + SiLU(z) R, LSE ------------------------------

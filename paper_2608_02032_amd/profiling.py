@@ -1,0 +1,127 @@
+"""Summaries of rocprofv3 output for the committed profiles/ directory.
+
+    python -m paper_2608_02032_amd.profiling trace  <kernel_stats.csv> <out.md> "<command>"
+    python -m paper_2608_02032_amd.profiling traffic <fetch counter_collection.csv>
+           <write counter_collection.csv> <copy bytes> <out.json> <out.md> "<commands>"
+
+`traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
+launch of each library kernel.  Each counter is scaled by what it reads for a
+plain device copy of known size run in the same process (the copy kernel moves
+`copy bytes` in and out), so counter units and partial coverage cancel.  The
+JSON records a hash of every kernel source file, and bench.py reports the
+traffic of a kernel only while those sources are unchanged.
+"""
+from __future__ import annotations
+
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+from collections import defaultdict
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".hpp", ".cpp")):
+            with open(os.path.join(CSRC, name), "rb") as fh:
+                h.update(name.encode())
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_short(name: str):
+    if "dart" not in name:
+        return None
+    m = re.search(r"(k_[a-z_]+)", name)
+    return m.group(1) if m else None
+
+
+def trace_summary(stats_csv: str, out_md: str, command: str) -> str:
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = ["# Kernel trace", "", "Command:", "", "```", command, "```", "",
+             "Library kernels only.", "", "| kernel | calls | avg us | min us | max us |",
+             "|---|---|---|---|---|"]
+    for r in rows:
+        k = kernel_short(r["Name"])
+        if not k:
+            continue
+        lines.append("| %s | %s | %.1f | %.1f | %.1f |" % (
+            k, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+            float(r["MaxNs"]) / 1e3))
+    text = "\n".join(lines) + "\n"
+    with open(out_md, "w") as fh:
+        fh.write(text)
+    return text
+
+
+def _per_kernel(csv_path: str, counter: str):
+    vals = defaultdict(list)
+    copy_vals = []
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != counter:
+            continue
+        v = float(r["Counter_Value"])
+        if "copyBuffer" in r["Kernel_Name"]:
+            copy_vals.append(v)
+        k = kernel_short(r["Kernel_Name"])
+        if k:
+            vals[k].append(v)
+    return vals, copy_vals
+
+
+def traffic_summary(fetch_csv: str, write_csv: str, copy_bytes: int, out_json: str, out_md: str,
+                    commands: str) -> dict:
+    fetch, fcopy = _per_kernel(fetch_csv, "FETCH_SIZE")
+    write, wcopy = _per_kernel(write_csv, "WRITE_SIZE")
+    # the calibration copy is the largest copyBuffer dispatch
+    f_ref = max(fcopy) * 1024.0
+    w_ref = max(wcopy) * 1024.0
+    f_scale = copy_bytes / f_ref
+    w_scale = copy_bytes / w_ref
+    out = {"source_hash": source_hash(), "copy_bytes": copy_bytes,
+           "fetch_scale": f_scale, "write_scale": w_scale, "kernels": {}}
+    lines = ["# HBM traffic per launch (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             "Commands:", "", "```", commands, "```", "",
+             "Scale factors from a plain %d-byte device copy in the same process: FETCH_SIZE x %.3f, "
+             "WRITE_SIZE x %.3f." % (copy_bytes, f_scale, w_scale), "",
+             "| kernel | dispatches | fetch MB | write MB |", "|---|---|---|---|"]
+    for k in sorted(set(fetch) | set(write)):
+        fv = sum(fetch.get(k, [0.0])) / max(len(fetch.get(k, [])), 1) * 1024.0 * f_scale
+        wv = sum(write.get(k, [0.0])) / max(len(write.get(k, [])), 1) * 1024.0 * w_scale
+        out["kernels"][k] = {"fetch_bytes": fv, "write_bytes": wv, "traffic_bytes": fv + wv}
+        lines.append("| %s | %d | %.1f | %.1f |" % (k, len(fetch.get(k, [])), fv / 1e6, wv / 1e6))
+    with open(out_json, "w") as fh:
+        json.dump(out, fh, indent=1)
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    return out
+
+
+def traffic_for(kernel: str):
+    """Measured HBM bytes per launch of `kernel`, or None when no counters were
+    taken for the current kernel sources."""
+    if not os.path.exists(TRAFFIC_JSON):
+        return None
+    d = json.load(open(TRAFFIC_JSON))
+    if d.get("source_hash") != source_hash():
+        return None
+    k = d["kernels"].get(kernel)
+    return None if k is None else k["traffic_bytes"]
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "trace":
+        print(trace_summary(sys.argv[2], sys.argv[3], sys.argv[4]))
+    elif sys.argv[1] == "traffic":
+        print(json.dumps(traffic_summary(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5],
+                                         sys.argv[6], sys.argv[7]), indent=1))
+    else:
+        raise SystemExit(__doc__)
