@@ -4,7 +4,7 @@
 One step = the whole hot path over one batch of seeded synthetic inputs that
 are already resident in HBM:
   forward   chunked SSD scan (k_chunk_state, k_state_pass, k_chunk_out)
-            -> state-memory attention + gated residual (k_sma_prep, k_sma_main)
+            -> state-memory attention + gated residual (k_sma)
             on the L = 8192 workload (batch 4, 32 heads, P = 64, N = 128, S = 256);
   decode    one token (k_decode_partial, k_decode_finish) for batch 64, 32 heads,
             N = 128, S = 256 over a 65536-token context (256 cached memories).
@@ -221,13 +221,13 @@ def main():
     sflops, sbytes = scan_flops(w), scan_bytes(w)
     mflops, mbytes = sma_flops(w), sma_bytes(w)
     scan_ms = sum(avg.get(k, 0.0) for k in ("k_chunk_state", "k_state_pass", "k_chunk_out"))
-    sma_ms = sum(avg.get(k, 0.0) for k in ("k_sma_prep", "k_sma_main"))
-    main_ms = avg["k_sma_main"]
+    sma_ms = avg["k_sma"]
+    main_ms = sma_ms
     main_tflops = mflops / (main_ms * 1e-3) / 1e12
-    roofline = {"kernel": "k_sma_main", "bound": "mfma",
+    roofline = {"kernel": "k_sma", "bound": "mfma",
                 "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic_for("k_sma_main"),
+                "traffic": traffic_for("k_sma"),
                 "avg_us": round(main_ms * 1e3, 2),
                 "algorithmic_flops_per_launch": mflops}
     extra = {

@@ -110,7 +110,8 @@ dart_status dart_ssd_chunk_scan(const dart_dims* dims, const void* x, const floa
                                 void* y_ssd, void* mem, float* h_last, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
-/* Bytes of workspace dart_sma_fwd needs for `dims`. */
+/* Bytes of workspace dart_sma_fwd needs for `dims`.  This build streams the
+ * memories straight from `mem` and needs none (0; workspace may be NULL). */
 size_t dart_sma_workspace_bytes(const dart_dims* dims);
 
 /*

@@ -152,6 +152,14 @@ __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0); }
 // used in streaming loops where each wave first waits for its own LDS copies
 // (vmcnt) and every LDS read of a stage is consumed before the barrier.
 __device__ __forceinline__ void block_barrier() { __builtin_amdgcn_s_barrier(); }
+// Workgroup barrier that orders LDS only: this wave's LDS writes complete
+// before it and no LDS access moves across it, while global loads issued
+// earlier stay in flight (a fence on the local address space alone).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 constexpr int vmcnt_imm(int k) { return (k & 15) | (7 << 4) | (15 << 8) | ((k >> 4) << 14); }
 
 // A natural-layout tile of rows of RB bytes in LDS whose 16-byte chunks are

@@ -31,9 +31,7 @@ struct SmaArgs {
     int z_per_head;
 };
 
-// Workspace of the SMA forward: decoded-operand copies of memories 0..M-2
-// (key side scaled by the inverse row RMS, value side as stored), both in the
-// MFMA operand order, storage dtype.
+// Workspace of the SMA forward: none (the kernel reads the memories as stored).
 size_t sma_workspace_bytes(const Shape& s);
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,

@@ -8,21 +8,29 @@
 // query tile fixed, historical memories streamed, online softmax, only R and
 // the log-sum-exp leave the chip).
 //
-// Two kernels:
-//   k_sma_prep  per (b, memory j, head): r_j[n] = (mean_p dH_j[n,p]^2 + eps)^-1/2
-//               from the stored values; writes two copies of the memory in the
-//               MFMA A-operand order (key side scaled by r_j, value side as
-//               stored) so the main loop streams them with plain 16-byte loads.
-//   k_sma_main  per (b, head, 256-token block; 4 waves x 64 tokens, each wave
-//               inside one chunk): for every earlier memory j, on MFMA
-//                 U^T = (r_j (.) dH_j)^T Qbar^T   (P x tokens)
-//                 V^T = dH_j^T C^T                (P x tokens)
-//               then l_t = sum_p U^T[p,t] Ebar[t,p] (the P axis lives in the
-//               lane's own registers plus 2 cross-lane steps), an online
-//               softmax in base 2, O = alpha O + g V.  Epilogue:
-//               y = y_ssd + SiLU(z) O/d and LSE = (m + log2 d) ln 2.
-// The transposed products put one token per lane column, so each lane owns its
-// tokens' softmax statistics and no per-row broadcast is needed.
+// One kernel, k_sma: one workgroup per (b, head, token block).  The block's 8
+// waves form 4 pairs; each pair owns 16*RT consecutive tokens inside one
+// chunk.  In a pair, the score wave holds Qbar and Ebar and the value wave
+// holds C and the output accumulator O, so each wave keeps only half of the
+// per-token operands and every operand fragment it reads from LDS feeds RT
+// independent MFMA chains.
+//
+// The memories dH_j (j < the block's last chunk) stream from the memory cache
+// as stored ([N][P] rows, 16-byte loads into registers ahead of use).  When a
+// loaded memory is written to LDS, the lanes holding one row reduce its inverse
+// RMS r_j[n]; two swizzled [N][P] tiles are written, the key side
+// r_j (.) dH_j and the value side dH_j.  Step s of the streaming loop:
+//   score waves   U^T = (r_s (.) dH_s)^T Qbar^T (P x tokens, MFMA), logits
+//                 l_t = sum_p U^T[p,t] Ebar[t,p] (the lane's registers plus one
+//                 MFMA against a ones matrix for the 4 lanes of a column),
+//                 online softmax in base 2; the weights of memory s (and a
+//                 rescale factor when the running maximum moved) go to LDS;
+//   value waves   V^T = dH_{s-1}^T C^T (MFMA), O = alpha O + w_{s-1} V;
+//   all threads   write key tile s+1 and value tile s, load memory s+2.
+// One barrier per step.  Epilogue: the score wave publishes its softmax
+// denominators and writes LSE = (m + log2 d) ln 2; the value wave writes
+// y = y_ssd + SiLU(z) O/d.  Operand fragments are read with transposing LDS
+// loads (ds_read_b64_tr_b16 for bf16).
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
 
@@ -30,356 +38,503 @@ namespace dart {
 namespace {
 
 constexpr int kP = 64;
-constexpr int kThreads = 256;
-constexpr int kPad = 8;
-constexpr int kTokPerBlock = 256;
+constexpr int kWaves = 8;                  // 4 (score, value) pairs
+constexpr int kThreads = kWaves * 64;
+constexpr float kRescaleLog2 = 8.0f;       // lazy-rescale threshold (log2 units)
+constexpr int kHeadsPerBlock = 4;          // heads of one group served by a block (power of 2)
 
-template <typename T, int N>
-__global__ __launch_bounds__(kThreads) void k_sma_prep(const T* __restrict__ mem,
-                                                        T* __restrict__ kfrag,
-                                                        T* __restrict__ vfrag, float eps,
-                                                        int normalize, int H, int64_t Mp,
-                                                        int64_t Mcap) {
-    const int64_t j = blockIdx.x;
-    const int h = blockIdx.y;
-    const int64_t b = blockIdx.z;
-    const int tid = threadIdx.x;
-    __shared__ __attribute__((aligned(16))) T sm[N][kP + kPad];
-    __shared__ float sr[N];
-    const T* src = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
-    for (int ci = tid; ci < N * (kP / 8); ci += kThreads) {
-        const int r = ci >> 3, k8 = ci & 7;
-        float v[8];
-        load8(src + r * kP + k8 * 8, v);
-        store8(&sm[r][k8 * 8], v);
-    }
-    __syncthreads();
-    if (tid < N) {
-        float ss = 0.f;
-#pragma unroll 8
-        for (int p = 0; p < kP; ++p) {
-            const float v = to_f(sm[tid][p]);
-            ss += v * v;
-        }
-        sr[tid] = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
-    }
-    __syncthreads();
-    constexpr int kFrag = (N / 32) * 4;  // fragments (k step, p tile) per memory
-    const int64_t base = ((b * Mp + j) * H + h) * (int64_t)N * kP;
-    for (int pi = tid; pi < kFrag * 64; pi += kThreads) {
-        const int f = pi >> 6, l = pi & 63;
-        const int ks = f >> 2, pt = f & 3;
-        const int p = pt * 16 + (l & 15);
-        const int n0 = ks * 32 + (l >> 4) * 8;
-        float v[8], kv[8];
+// 16-token column tiles per pair: 4 for bf16 (64 tokens), 2 for fp32 (its
+// operand fragments take twice the registers).
+template <typename T> constexpr int sma_rt() { return sizeof(T) == 2 ? 4 : 2; }
+template <typename T> constexpr int sma_tokens_per_block() { return 4 * 16 * sma_rt<T>(); }
+
+// 8 operand values of a token row vector v (length N) in the lane's k order:
+// k-group g holds elements 32 ks + 4 g + {0..3} and 32 ks + 16 + 4 g + {0..3},
+// the order in which frag_km hands out the rows of a k-major tile.
+template <typename T>
+__device__ __forceinline__ void load_kperm(const T* row, int ks, int grp, float (&v)[8]) {
+    float a[4], b[4];
+    load4(row + ks * 32 + 4 * grp, a);
+    load4(row + ks * 32 + 16 + 4 * grp, b);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            v[i] = to_f(sm[n0 + i][p]);
-            kv[i] = v[i] * sr[n0 + i];
-        }
-        store8(vfrag + base + (int64_t)pi * 8, v);
-        store8(kfrag + base + (int64_t)pi * 8, kv);
+    for (int i = 0; i < 4; ++i) {
+        v[i] = a[i];
+        v[4 + i] = b[i];
     }
 }
 
-template <typename T, int N, int S, int RT>
-__global__ __launch_bounds__(16 / RT * 64) void k_sma_main(
-    const T* __restrict__ q, const T* __restrict__ e, const T* __restrict__ Cm,
-    const T* __restrict__ kfrag, const T* __restrict__ vfrag, const T* __restrict__ z,
-    const T* y_ssd, T* y, float* __restrict__ lse, const float* __restrict__ qw,
-    const float* __restrict__ ew, float eps, int normalize, int z_per_head, int64_t L, int H, int G,
-    int64_t Mp, int nblk, int64_t BH) {
-    constexpr int KS = N / 32;
-    constexpr int NW = 16 / RT;                            // waves; 16*RT tokens each
-    constexpr int WT = 16 * RT;                            // tokens per wave
-    constexpr int MEMEL = N * kP;                          // elements per memory
-    constexpr int PIECES = MEMEL * (int)sizeof(T) / 1024;  // 1 KiB operand fragments per copy
-    static_assert(PIECES * 1024 == MEMEL * (int)sizeof(T), "memory must be whole fragments");
-    static_assert(S >= WT, "a wave's tokens must lie in one chunk");
+// Four consecutive elements loaded as one vector (8 B for bf16, 16 B for fp32).
+template <typename T>
+using Vec4 = T __attribute__((ext_vector_type(4)));
+template <typename T>
+__device__ __forceinline__ Vec4<T> ld4(const T* p) { return *reinterpret_cast<const Vec4<T>*>(p); }
+template <typename T>
+__device__ __forceinline__ Frag<T> cat_frag(Vec4<T> a, Vec4<T> b) {
+    return Frag<T>{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
 
+// Sum of squares of the elements of one 16-byte piece, and the piece scaled.
+__device__ __forceinline__ float piece_sumsq(uint4 v, bf16) {
+    const bf16x8 h = __builtin_bit_cast(bf16x8, v);
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += (float)h[i] * (float)h[i];
+    return s;
+}
+__device__ __forceinline__ float piece_sumsq(uint4 v, float) {
+    const f32x4 f = __builtin_bit_cast(f32x4, v);
+    return f[0] * f[0] + f[1] * f[1] + f[2] * f[2] + f[3] * f[3];
+}
+__device__ __forceinline__ uint4 piece_scale(uint4 v, float r, bf16) {
+    const bf16x8 h = __builtin_bit_cast(bf16x8, v);
+    bf16x8 o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = (bf16)((float)h[i] * r);
+    return __builtin_bit_cast(uint4, o);
+}
+__device__ __forceinline__ uint4 piece_scale(uint4 v, float r, float) {
+    f32x4 f = __builtin_bit_cast(f32x4, v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f[i] *= r;
+    return __builtin_bit_cast(uint4, f);
+}
+
+template <typename T, int N, int S>
+__global__ __launch_bounds__(kThreads) void k_sma(
+    const T* __restrict__ q, const T* __restrict__ e, const T* __restrict__ Cm,
+    const T* __restrict__ mem, const T* __restrict__ z, const T* y_ssd, T* y,
+    float* __restrict__ lse, const float* __restrict__ qw, const float* __restrict__ ew, float eps,
+    int normalize, int z_per_head, int64_t L, int H, int G, int64_t Mcap, int nblk, int hpb,
+    int64_t BHC) {
+    constexpr int KS = N / 32;
+    constexpr int RT = sma_rt<T>();
+    constexpr int PT = 16 * RT;                  // tokens per pair
+    constexpr int TPB = sma_tokens_per_block<T>();
+    constexpr int RB = kP * (int)sizeof(T);      // bytes of one memory row (fixed n)
+    constexpr int MEMB = N * RB;                 // bytes of one memory
+    constexpr int PIECES = MEMB / 16;            // 16-byte pieces of one memory
+    constexpr int PPT = PIECES >= kThreads ? PIECES / kThreads : 1;
+    constexpr int RPC = RB / 16;                 // pieces per row
+    static_assert(PIECES < kThreads ? kThreads % PIECES == 0 : PIECES % kThreads == 0,
+                  "memory pieces must tile the block");
+    static_assert(PIECES >= kThreads || PIECES % 64 == 0, "partial copies must be whole waves");
+    static_assert(S >= PT, "a pair's tokens must lie in one chunk");
+    using Tl = SwzTile<RB>;
+
+    // A block serves `hpb` heads of one projection group (they share q, e and
+    // C, loaded once) for one token block, one head after another.
     // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
-    // index, and each XCD has its own L2.  When B*H is a multiple of 8, XCD x
-    // runs whole heads (b, h) = x, x+8, ... one after another, heaviest token
-    // block first, so all blocks reading one head's memories share one L2.
+    // index, and each XCD has its own L2.  When the number of head groups
+    // B*H/hpb is a multiple of 8, XCD x runs whole head groups x, x+8, ... one
+    // after another, heaviest token block first, so all blocks reading one
+    // head group's memories share one L2.
     const int64_t bid = blockIdx.x;
     int blk;
-    int64_t bh;
-    if (BH % 8 == 0) {
+    int64_t bhc;
+    if (BHC % 8 == 0) {
         const int64_t slot = bid >> 3;
         blk = nblk - 1 - (int)(slot % nblk);
-        bh = (slot / nblk) * 8 + (bid & 7);
+        bhc = (slot / nblk) * 8 + (bid & 7);
     } else {
-        blk = nblk - 1 - (int)(bid / BH);
-        bh = bid % BH;
+        blk = nblk - 1 - (int)(bid / BHC);
+        bhc = bid % BHC;
     }
-    const int64_t b = bh / H;
-    const int h = (int)(bh % H);
-    const int g = (int)((int64_t)h * G / H);
+    const int hgroups = H / hpb;
+    const int64_t b = bhc / hgroups;
+    const int h0 = (int)(bhc % hgroups) * hpb;
+    const int g = (int)((int64_t)h0 * G / H);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
+    const bool scorer = wave < 4;
+    const int pair = wave & 3;
 
-    const int64_t blk0 = (int64_t)blk * kTokPerBlock;
-    const int64_t wbase = blk0 + wave * WT;
-    const int64_t blk_end = (blk0 + kTokPerBlock < L) ? blk0 + kTokPerBlock : L;
-    const int jmax = (int)((blk_end - 1) / S);             // memories any wave of the block needs
-    const bool active = wbase < L;
-    const int iw = (int)(wbase / S);                        // this wave's chunk
-    const int nj = active ? iw : 0;
+    const int64_t blk0 = (int64_t)blk * TPB;
+    const int64_t pbase = blk0 + pair * PT;                  // first token of the pair
+    const int64_t blk_end = (blk0 + TPB < L) ? blk0 + TPB : L;
+    const int jmax = (int)((blk_end - 1) / S);              // memories any pair of the block needs
+    const bool active = pbase < L;
+    const int ip = (int)(pbase / S);                         // the pair's chunk
+    const int nj = active ? ip : 0;                          // memories the pair attends
 
-    // Three stages (key copy then value copy of one memory each) as distinct
-    // LDS objects: the compiler can see that a DMA into one stage does not
-    // alias reads of another, so prefetches two memories ahead overlap the
-    // MFMAs instead of being waited for.
-    constexpr bool kThree = 3 * 2 * MEMEL * (int)sizeof(T) <= 160 * 1024;
-    __shared__ __attribute__((aligned(16))) T st0[2 * MEMEL];
-    __shared__ __attribute__((aligned(16))) T st1[2 * MEMEL];
-    __shared__ __attribute__((aligned(16))) T st2[kThree ? 2 * MEMEL : 8];
+    // LDS: two key tiles and two value tiles (swizzled [N][P]), the softmax
+    // weights (and rescale factors) of the last scored memory per pair, and
+    // the final denominators (by head parity).
+    __shared__ __attribute__((aligned(16))) char kts[2 * MEMB];
+    __shared__ __attribute__((aligned(16))) char vts[2 * MEMB];
+    __shared__ float xw[2][4][PT];
+    __shared__ float xa[2][4][PT];
+    __shared__ int xr[2][4];
+    __shared__ float xd[2][4][PT];
 
-    // ---- prologue: Qbar, C and Ebar of this wave's 64 tokens -------------
-    Frag<T> qf[RT][KS], cf[RT][KS];
-    float ef[RT][4][4];
-    const float qscale = kLog2e / sqrtf((float)N);
+    // ---- streaming helpers ---------------------------------------------------
+    // Memory j of head h starts at a wave-uniform address; each lane adds a
+    // fixed 32-bit byte offset (kept in its own register so every load is a
+    // scalar base plus a lane offset).
+    const char* mbase0 = reinterpret_cast<const char*>(mem) + (b * Mcap * H + h0) * (int64_t)MEMB;
+    const int64_t jstride = (int64_t)H * MEMB;
+    const bool copier = PIECES >= kThreads || tid < PIECES;
+    struct Regs { uint4 p[PPT]; };
+    uint32_t loff[PPT];
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-        const int64_t t = wbase + rt * 16 + col;
-        const bool valid = active && t < L;
-        float qv[KS][8];
-        float ss = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            if (valid) {
-                load8(q + ((b * L + t) * G + g) * N + ks * 32 + grp * 8, qv[ks]);
-            } else {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) qv[ks][i] = 0.f;
-            }
-#pragma unroll
-            for (int i = 0; i < 8; ++i) ss += qv[ks][i] * qv[ks][i];
-        }
-        ss += shfl_xor(ss, 16);
-        ss += shfl_xor(ss, 32);
-        const float qinv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) * qscale;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) qv[ks][i] *= qinv;
-            if (qw) {
-                float w[8];
-                load8(qw + ks * 32 + grp * 8, w);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) qv[ks][i] *= w[i];
-            }
-            qf[rt][ks] = make_frag<T>(qv[ks]);
-            float cv[8];
-            if (valid) {
-                load8(Cm + ((b * L + t) * G + g) * N + ks * 32 + grp * 8, cv);
-            } else {
-#pragma unroll
-                for (int i = 0; i < 8; ++i) cv[i] = 0.f;
-            }
-            cf[rt][ks] = make_frag<T>(cv);
-        }
-        float es = 0.f;
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            if (valid) {
-                load4(e + ((b * L + t) * G + g) * kP + pt * 16 + grp * 4, ef[rt][pt]);
-            } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) ef[rt][pt][i] = 0.f;
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) es += ef[rt][pt][i] * ef[rt][pt][i];
-        }
-        es += shfl_xor(es, 16);
-        es += shfl_xor(es, 32);
-        const float einv = normalize ? 1.0f / sqrtf(es * (1.0f / kP) + eps) : 1.0f;
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= einv;
-            if (ew) {
-                float w[4];
-                load4(ew + pt * 16 + grp * 4, w);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= w[i];
-            }
-        }
+    for (int i = 0; i < PPT; ++i) {
+        loff[i] = (uint32_t)(tid + i * kThreads) * 16u;
+        asm volatile("" : "+v"(loff[i]));
     }
-
-    float m[RT], d[RT];
-    f32x4 o[RT][4];
+    // indices past the last memory re-read the last one, so loads are issued
+    // on every path and the compiler waits only for the set being written
+    auto load_regs = [&](int hh, int j) {
+        Regs r;
+        const int jj = j < jmax ? j : jmax - 1;
+        const char* src = mbase0 + (int64_t)hh * MEMB + (int64_t)jj * jstride;
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-        m[rt] = -INFINITY;
-        d[rt] = 0.f;
+        for (int i = 0; i < PPT; ++i) {
+            if (copier) r.p[i] = *reinterpret_cast<const uint4*>(src + loff[i]);
+        }
+        return r;
+    };
+    // key tile: the RPC lanes holding one row reduce its sum of squares to
+    // r_j[n] and write the pieces times r_j[n]
+    auto store_key = [&](const Regs& r, char* kt) {
+        if (!copier) return;
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt) o[rt][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-
-    // ---- stream the earlier memories through LDS (double buffered) -------
-    // Each wave copies whole 1 KiB operand fragments straight from global
-    // memory into LDS (global_load_lds_dwordx4: lane i writes 16 B at the
-    // wave-uniform LDS base + 16 i), so no registers hold the prefetch.
-    const int64_t mstride = (int64_t)H * MEMEL;
-    const char* kbase = reinterpret_cast<const char*>(kfrag + (b * Mp * H + h) * (int64_t)MEMEL);
-    const char* vbase = reinterpret_cast<const char*>(vfrag + (b * Mp * H + h) * (int64_t)MEMEL);
-    static_assert(PIECES % NW == 0, "every wave copies the same number of fragments");
-    constexpr int kDmaPerMem = 2 * PIECES / NW;  // DMA instructions per memory per wave
-    auto fetch = [&](int j, T* dstage) {
-        const char* kj = kbase + (int64_t)j * mstride * (int64_t)sizeof(T);
-        const char* vj = vbase + (int64_t)j * mstride * (int64_t)sizeof(T);
-        char* kd = reinterpret_cast<char*>(dstage);
-        char* vd = kd + MEMEL * (int)sizeof(T);
+        for (int i = 0; i < PPT; ++i) {
+            const int pc = tid + i * kThreads;
+            const int row = pc / RPC, c = pc % RPC;
+            float ss = piece_sumsq(r.p[i], T());
 #pragma unroll
-        for (int pc = wave; pc < PIECES; pc += NW) {
-            lds_dma16(kj + pc * 1024 + lane * 16, kd + pc * 1024);
-            lds_dma16(vj + pc * 1024 + lane * 16, vd + pc * 1024);
+            for (int msk = 1; msk < RPC; msk <<= 1) ss += shfl_xor(ss, msk);
+            const float rn = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
+            *reinterpret_cast<uint4*>(kt + Tl::off(row, c * 16)) = piece_scale(r.p[i], rn, T());
         }
     };
-    auto consume = [&](const T* kc, const T* vc) {
-        float lp[RT];
+    auto store_value = [&](const Regs& r, char* vt) {
+        if (!copier) return;
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            f32x4 u[RT];
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const Frag<T> fa = load_frag(&kc[((ks * 4 + pt) * 64 + lane) * 8]);
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fa, qf[rt][ks]);
-            }
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
+        for (int i = 0; i < PPT; ++i) {
+            const int pc = tid + i * kThreads;
+            *reinterpret_cast<uint4*>(vt + Tl::off(pc / RPC, (pc % RPC) * 16)) = r.p[i];
         }
-        float al[RT], pw[RT];
+    };
+    // operand fragments of one 16-column slice (P index pt) of a tile
+    auto read_slice = [&](const char* tile, int pt, Frag<T> (&f)[KS]) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            f[ks] = frag_km<T, RB>(tile, ks * 32 + 4 * grp, ks * 32 + 16 + 4 * grp, pt * 16, lane);
+    };
+
+    // The step loop, shared by both kinds of wave: step s runs `work(s)`, then
+    // writes key tile s+1 and value tile s and loads memory s+2.  Steps run
+    // for s = 0..jmax; register set s%2 holds memory s once its key tile is
+    // written (memories 0 and 1 are loaded before the token operands, so
+    // their latency overlaps the prologue).  Every wave executes the same
+    // barriers.
+    auto stream = [&](int hh, Regs& r0, Regs& r1, auto&& work) {
+        if (jmax == 0) return;
+        store_key(r0, kts);
+        lds_barrier();
+        for (int s = 0;; s += 2) {
+            work(s, kts, vts + MEMB, 0);
+            store_value(r0, vts);
+            store_key(r1, kts + MEMB);
+            r0 = load_regs(hh, s + 2);
+            lds_barrier();
+            if (s + 1 > jmax) break;
+            work(s + 1, kts + MEMB, vts, 1);
+            store_value(r1, vts + MEMB);
+            store_key(r0, kts);
+            r1 = load_regs(hh, s + 3);
+            lds_barrier();
+            if (s + 2 > jmax) break;
+        }
+    };
+
+    // token rows of the pair; rows past the end re-read the last token
+    // (their results are zeroed or discarded), so every load is issued up
+    // front without branches
+    int64_t trow[RT];
+    bool tvalid[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        const int64_t t = pbase + rt * 16 + col;
+        tvalid[rt] = t < L;
+        trow[rt] = b * L + (t < L ? t : L - 1);
+    }
+    Regs r0, r1;
+    if (jmax > 0) {
+        r0 = load_regs(0, 0);
+        r1 = load_regs(0, 1);
+    }
+    // after a head's last step: its successor's first two memories
+    auto preload_next = [&](int hh) {
+        if (jmax > 0 && hh + 1 < hpb) {
+            r0 = load_regs(hh + 1, 0);
+            r1 = load_regs(hh + 1, 1);
+        }
+    };
+    const bool hist = ip >= 1;
+
+    if (scorer) {
+        // ---- score wave: Qbar and Ebar of the pair's tokens -------------------
+        Vec4<T> qraw[RT][KS][2], eraw[RT][4];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
-            float l = lp[rt];
-            l += shfl_xor(l, 16);
-            l += shfl_xor(l, 32);
-            const float mn = fmaxf(m[rt], l);
-            al[rt] = fast_exp2(m[rt] - mn);
-            pw[rt] = fast_exp2(l - mn);
-            d[rt] = d[rt] * al[rt] + pw[rt];
-            m[rt] = mn;
-        }
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            f32x4 v[RT];
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const T* qrow = q + (trow[rt] * G + g) * N;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const Frag<T> fa = load_frag(&vc[((ks * 4 + pt) * 64 + lane) * 8]);
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fa, cf[rt][ks]);
+                qraw[rt][ks][0] = ld4(qrow + ks * 32 + 4 * grp);
+                qraw[rt][ks][1] = ld4(qrow + ks * 32 + 16 + 4 * grp);
             }
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) o[rt][pt] = o[rt][pt] * al[rt] + pw[rt] * v[rt];
+            for (int pt = 0; pt < 4; ++pt) eraw[rt][pt] = ld4(e + (trow[rt] * G + g) * kP + pt * 16 + grp * 4);
         }
-    };
-    // wait until at most `pending` memories' copies of this wave are in flight
-    auto wait_copies = [&](bool one_pending) {
-        if (one_pending) {
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDmaPerMem));
-        } else {
-            wait_dma();
+        Frag<T> qf[RT][KS];
+        float ef[RT][4][4];
+        const float qscale = kLog2e / sqrtf((float)N);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const float vmask = tvalid[rt] ? 1.0f : 0.0f;
+            float qv[KS][8];
+            float ss = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    qv[ks][i] = to_f(qraw[rt][ks][0][i]) * vmask;
+                    qv[ks][4 + i] = to_f(qraw[rt][ks][1][i]) * vmask;
+                }
+#pragma unroll
+                for (int i = 0; i < 8; ++i) ss += qv[ks][i] * qv[ks][i];
+            }
+            ss += shfl_xor(ss, 16);
+            ss += shfl_xor(ss, 32);
+            const float qinv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) * qscale;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) qv[ks][i] *= qinv;
+                if (qw) {
+                    float w[8];
+                    load_kperm(qw, ks, grp, w);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) qv[ks][i] *= w[i];
+                }
+                qf[rt][ks] = make_frag<T>(qv[ks]);
+            }
+            float es = 0.f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    ef[rt][pt][i] = to_f(eraw[rt][pt][i]) * vmask;
+                    es += ef[rt][pt][i] * ef[rt][pt][i];
+                }
+            }
+            es += shfl_xor(es, 16);
+            es += shfl_xor(es, 32);
+            const float einv = normalize ? 1.0f / sqrtf(es * (1.0f / kP) + eps) : 1.0f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= einv;
+                if (ew) {
+                    float w[4];
+                    load4(ew + pt * 16 + grp * 4, w);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= w[i];
+                }
+            }
         }
-    };
-    if constexpr (kThree) {
-        if (jmax > 0) fetch(0, st0);
-        if (jmax > 1) fetch(1, st1);
-        wait_copies(jmax > 1);
-        block_barrier();
-        // memory j is consumed from stage j % 3 while j+1 (already issued) and j+2
-        // stream into the other two; one barrier per memory
-        for (int j = 0; j < jmax; j += 3) {
-            if (j + 2 < jmax) fetch(j + 2, st2);
-            if (j < nj) consume(st0, st0 + MEMEL);
-            wait_copies(j + 2 < jmax);
-            block_barrier();
-            if (j + 1 >= jmax) break;
-            if (j + 3 < jmax) fetch(j + 3, st0);
-            if (j + 1 < nj) consume(st1, st1 + MEMEL);
-            wait_copies(j + 3 < jmax);
-            block_barrier();
-            if (j + 2 >= jmax) break;
-            if (j + 4 < jmax) fetch(j + 4, st1);
-            if (j + 2 < nj) consume(st2, st2 + MEMEL);
-            wait_copies(j + 4 < jmax);
-            block_barrier();
+        for (int hh = 0; hh < hpb; ++hh) {
+        const int h = h0 + hh;
+        float m[RT], d[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            m[rt] = -INFINITY;
+            d[rt] = 0.f;
+        }
+
+        stream(hh, r0, r1, [&](int s, const char* kt, const char*, int buf) {
+            if (s >= nj) return;
+            // U^T slices: fragments of slice pt+1 are read before the MFMAs of
+            // slice pt (scheduling fences keep that order)
+            Frag<T> fb[2][KS];
+            read_slice(kt, 0, fb[0]);
+            float lp[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+                if (pt < 3) read_slice(kt, pt + 1, fb[(pt + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+                f32x4 u[RT];
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fb[pt & 1][ks], qf[rt][ks]);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            // full logit of the lane's token: sum the 4 lanes sharing its
+            // column with one fp32 MFMA against a ones matrix
+            // (D[i][t] = sum_k B[k][t])
+            bool grow = false;
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const f32x4 red = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                    1.0f, lp[rt], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                lp[rt] = red[0];
+                grow |= lp[rt] > m[rt] + kRescaleLog2;
+            }
+            // lazy rescale: the reference maximum only moves when a logit
+            // exceeds it by more than 2^8, so weights stay <= 256 and O is
+            // rescaled rarely; R = O/d and LSE = m + log2 d do not depend on
+            // the choice of m
+            const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+            if (rescale) {
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    const float mn = fmaxf(m[rt], lp[rt]);
+                    const float al = fast_exp2(m[rt] - mn);
+                    d[rt] *= al;
+                    m[rt] = mn;
+                    if (grp == 0) xa[buf][pair][rt * 16 + col] = al;
+                }
+            }
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const float pw = fast_exp2(lp[rt] - m[rt]);
+                d[rt] += pw;
+                if (grp == 0) xw[buf][pair][rt * 16 + col] = pw;
+            }
+            if (lane == 0) xr[buf][pair] = rescale ? 1 : 0;
+        });
+
+        preload_next(hh);
+        // ---- publish the denominators, write LSE -------------------------------
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            if (grp == 0) xd[hh & 1][pair][rt * 16 + col] = d[rt];
+            if (lse && grp == 0 && tvalid[rt])
+                lse[trow[rt] * H + h] = hist ? (m[rt] + log2f(d[rt])) * kLn2 : -INFINITY;
+        }
+        lds_barrier();
         }
     } else {
-        // two stages (when three do not fit in LDS): j+1 streams while j is consumed
-        if (jmax > 0) fetch(0, st0);
-        wait_dma();
-        __syncthreads();
-        for (int j = 0; j < jmax; j += 2) {
-            if (j + 1 < jmax) fetch(j + 1, st1);
-            if (j < nj) consume(st0, st0 + MEMEL);
-            wait_dma();
-            __syncthreads();
-            if (j + 1 >= jmax) break;
-            if (j + 2 < jmax) fetch(j + 2, st0);
-            if (j + 1 < nj) consume(st1, st1 + MEMEL);
-            wait_dma();
-            __syncthreads();
+        // ---- value wave: C of the pair's tokens, accumulator O ----------------
+        Frag<T> cf[RT][KS];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const T* crow = Cm + (trow[rt] * G + g) * N;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                cf[rt][ks] = cat_frag<T>(ld4(crow + ks * 32 + 4 * grp), ld4(crow + ks * 32 + 16 + 4 * grp));
         }
-    }
-
-    // ---- epilogue: y = y_ssd + SiLU(z) R, LSE ------------------------------
-    const bool hist = iw >= 1;
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-        const int64_t t = wbase + rt * 16 + col;
-        if (!active || t >= L) continue;
-        const float zz = to_f(z_per_head ? z[(b * L + t) * H + h] : z[b * L + t]);
-        const float gate = silu(zz);
-        const float invd = hist ? 1.0f / d[rt] : 0.f;
+        for (int rt = 0; rt < RT; ++rt) {
+            if (!tvalid[rt]) {
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            const int64_t off = ((b * L + t) * H + h) * kP + pt * 16 + grp * 4;
-            float ys[4];
-            load4(y_ssd + off, ys);
-            if (hist) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) ys[i] += gate * (o[rt][pt][i] * invd);
+                for (int ks = 0; ks < KS; ++ks) cf[rt][ks] = Frag<T>{};
             }
-            store4(y + off, ys);
         }
-        if (lse && grp == 0) lse[(b * L + t) * H + h] = hist ? (m[rt] + log2f(d[rt])) * kLn2 : -INFINITY;
+        for (int hh = 0; hh < hpb; ++hh) {
+        const int h = h0 + hh;
+        f32x4 o[RT][4];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) o[rt][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        stream(hh, r0, r1, [&](int s, const char*, const char* vt, int buf) {
+            // memory s-1, scored in the previous step (weights in slot buf^1)
+            if (s < 1 || s - 1 >= nj) return;
+            const int wb = buf ^ 1;
+            Frag<T> fb[2][KS];
+            read_slice(vt, 0, fb[0]);
+            float pw[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) pw[rt] = xw[wb][pair][rt * 16 + col];
+            if (__builtin_amdgcn_readfirstlane(xr[wb][pair])) {
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    const float al = xa[wb][pair][rt * 16 + col];
+#pragma unroll
+                    for (int pt = 0; pt < 4; ++pt) o[rt][pt] *= al;
+                }
+            }
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+                if (pt < 3) read_slice(vt, pt + 1, fb[(pt + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+                f32x4 v[RT];
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fb[pt & 1][ks], cf[rt][ks]);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) o[rt][pt] += pw[rt] * v[rt];
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        });
+
+        preload_next(hh);
+        // ---- epilogue: y = y_ssd + SiLU(z) R -----------------------------------
+        float zz[RT];
+        Vec4<T> ys[RT][4];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            zz[rt] = to_f(z_per_head ? z[trow[rt] * H + h] : z[trow[rt]]);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) ys[rt][pt] = ld4(y_ssd + (trow[rt] * H + h) * kP + pt * 16 + grp * 4);
+        }
+        lds_barrier();
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            if (!tvalid[rt]) continue;
+            const float gate = silu(zz[rt]);
+            const float invd = hist ? 1.0f / xd[hh & 1][pair][rt * 16 + col] : 0.f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+                float yv[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[rt][pt][i]);
+                if (hist) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) yv[i] += gate * (o[rt][pt][i] * invd);
+                }
+                store4(y + (trow[rt] * H + h) * kP + pt * 16 + grp * 4, yv);
+            }
+        }
+        }
     }
 }
 
 template <typename T, int N, int S>
 hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e, const void* Cm,
                    const void* mem, const void* z, const void* y_ssd, void* y, float* lse,
-                   void* ws, hipStream_t st) {
-    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;  // memories any token attends to
-    T* kfrag = reinterpret_cast<T*>(ws);
-    T* vfrag = reinterpret_cast<T*>(reinterpret_cast<char*>(ws) +
-                                    align256(sizeof(T) * s.B * Mp * s.H * (size_t)N * kP));
-    if (Mp > 0) {
-        prof_begin("k_sma_prep", st);
-        k_sma_prep<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
-            (const T*)mem, kfrag, vfrag, a.eps, a.normalize, s.H, Mp, s.Mcap);
-        prof_end(st);
+                   hipStream_t st) {
+    constexpr int TPB = sma_tokens_per_block<T>();
+    const int nblk = (int)((s.L + TPB - 1) / TPB);
+    // heads per block: up to kHeadsPerBlock heads of one group
+    const int per_group = s.H / s.G;
+    int hpb = 1;
+    for (int c = kHeadsPerBlock; c > 1; c >>= 1) {
+        if (per_group % c == 0) {
+            hpb = c;
+            break;
+        }
     }
-    const int nblk = (int)((s.L + kTokPerBlock - 1) / kTokPerBlock);
-    const int64_t BH = s.B * s.H;
-    // 64 tokens per wave while the per-token operands fit the register file,
-    // 32 tokens per wave (8 waves) for the largest state size
-    constexpr int RT = (N * (int)sizeof(T) > 128) ? 2 : 4;
-    prof_begin("k_sma_main", st);
-    k_sma_main<T, N, S, RT><<<dim3((unsigned)(BH * nblk)), 16 / RT * 64, 0, st>>>(
-        (const T*)q, (const T*)e, (const T*)Cm, kfrag, vfrag, (const T*)z, (const T*)y_ssd, (T*)y,
-        lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H, s.G, Mp, nblk, BH);
+    const int64_t BHC = s.B * (s.H / hpb);
+    prof_begin("k_sma", st);
+    k_sma<T, N, S><<<dim3((unsigned)(BHC * nblk)), kThreads, 0, st>>>(
+        (const T*)q, (const T*)e, (const T*)Cm, (const T*)mem, (const T*)z, (const T*)y_ssd, (T*)y,
+        lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H, s.G, s.Mcap, nblk, hpb, BHC);
     prof_end(st);
     return hipGetLastError();
 }
@@ -387,11 +542,11 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
 template <typename T, int N>
 hipError_t run_sma_s(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                      const void* Cm, const void* mem, const void* z, const void* ys, void* y,
-                     float* lse, void* ws, hipStream_t st) {
+                     float* lse, hipStream_t st) {
     switch (s.S) {
-        case 64: return run_sma<T, N, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
-        case 128: return run_sma<T, N, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
-        case 256: return run_sma<T, N, 256>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
+        case 64: return run_sma<T, N, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
+        case 128: return run_sma<T, N, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
+        case 256: return run_sma<T, N, 256>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
     }
     return hipErrorInvalidValue;
 }
@@ -399,27 +554,24 @@ hipError_t run_sma_s(const Shape& s, const SmaArgs& a, const void* q, const void
 template <typename T>
 hipError_t run_sma_n(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                      const void* Cm, const void* mem, const void* z, const void* ys, void* y,
-                     float* lse, void* ws, hipStream_t st) {
+                     float* lse, hipStream_t st) {
     switch (s.N) {
-        case 32: return run_sma_s<T, 32>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
-        case 64: return run_sma_s<T, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
-        case 128: return run_sma_s<T, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
+        case 32: return run_sma_s<T, 32>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
+        case 64: return run_sma_s<T, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
+        case 128: return run_sma_s<T, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
     }
     return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-size_t sma_workspace_bytes(const Shape& s) {
-    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
-    return 2 * align256(elem_bytes(s.dtype) * s.B * Mp * s.H * (size_t)s.N * s.P);
-}
+size_t sma_workspace_bytes(const Shape&) { return 0; }
 
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
-                      float* lse, void* ws, hipStream_t st) {
-    if (s.dtype == 1) return run_sma_n<bf16>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, ws, st);
-    return run_sma_n<float>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, ws, st);
+                      float* lse, void*, hipStream_t st) {
+    if (s.dtype == 1) return run_sma_n<bf16>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, st);
+    return run_sma_n<float>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, st);
 }
 
 }  // namespace dart
