@@ -132,6 +132,23 @@ __device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
 // ---- wave-level helpers ---------------------------------------------------
 __device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
 
+// Sum over aligned groups of G = 8 or 16 consecutive lanes with DPP lane moves
+// (no LDS round trip): swap within pairs, then within quads, then mirror
+// within 8 (and 16) lanes; every lane of a group ends with the group sum.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+template <int G>
+__device__ __forceinline__ float dpp_group_sum(float v) {
+    static_assert(G == 8 || G == 16, "group of 8 or 16 lanes");
+    v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp_mov<0x141>(v);  // row_half_mirror (lane i <-> 7-i within 8)
+    if constexpr (G == 16) v += dpp_mov<0x140>(v);  // row_mirror (lane i <-> 15-i within 16)
+    return v;
+}
+
 __device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }

@@ -180,12 +180,16 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         loff[i] = (uint32_t)(tid + i * kThreads) * 16u;
         asm volatile("" : "+v"(loff[i]));
     }
-    // indices past the last memory re-read the last one, so loads are issued
-    // on every path and the compiler waits only for the set being written
-    auto load_regs = [&](int hh, int j) {
+    // The block streams nmem = hpb * jmax memories: index J is memory
+    // J % jmax of head h0 + J / jmax.  Indices past the last re-read the last
+    // one, so loads are issued on every path and the compiler waits only for
+    // the register set being written.
+    const int nmem = hpb * jmax;
+    auto load_regs = [&](int J) {
         Regs r;
-        const int jj = j < jmax ? j : jmax - 1;
-        const char* src = mbase0 + (int64_t)hh * MEMB + (int64_t)jj * jstride;
+        const int jj = J < nmem ? J : nmem - 1;
+        const int hh = jj / jmax;
+        const char* src = mbase0 + (int64_t)hh * MEMB + (int64_t)(jj - hh * jmax) * jstride;
 #pragma unroll
         for (int i = 0; i < PPT; ++i) {
             if (copier) r.p[i] = *reinterpret_cast<const uint4*>(src + loff[i]);
@@ -200,9 +204,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         for (int i = 0; i < PPT; ++i) {
             const int pc = tid + i * kThreads;
             const int row = pc / RPC, c = pc % RPC;
-            float ss = piece_sumsq(r.p[i], T());
-#pragma unroll
-            for (int msk = 1; msk < RPC; msk <<= 1) ss += shfl_xor(ss, msk);
+            const float ss = dpp_group_sum<RPC>(piece_sumsq(r.p[i], T()));
             const float rn = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
             *reinterpret_cast<uint4*>(kt + Tl::off(row, c * 16)) = piece_scale(r.p[i], rn, T());
         }
@@ -222,29 +224,28 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             f[ks] = frag_km<T, RB>(tile, ks * 32 + 4 * grp, ks * 32 + 16 + 4 * grp, pt * 16, lane);
     };
 
-    // The step loop, shared by both kinds of wave: step s runs `work(s)`, then
-    // writes key tile s+1 and value tile s and loads memory s+2.  Steps run
-    // for s = 0..jmax; register set s%2 holds memory s once its key tile is
-    // written (memories 0 and 1 are loaded before the token operands, so
-    // their latency overlaps the prologue).  Every wave executes the same
-    // barriers.
-    auto stream = [&](int hh, Regs& r0, Regs& r1, auto&& work) {
-        if (jmax == 0) return;
+    // The step loop, shared by both kinds of wave, runs steps s = 0..nmem:
+    // step s scores memory s and accumulates the values of memory s-1, then
+    // writes key tile s+1 and value tile s and loads memory s+2.  Register set
+    // s%2 holds memory s once its key tile is written (memories 0 and 1 are
+    // loaded before the token operands, so their latency overlaps the
+    // prologue).  Every wave executes the same barriers.
+    auto stream = [&](Regs& r0, Regs& r1, auto&& work) {
         store_key(r0, kts);
         lds_barrier();
         for (int s = 0;; s += 2) {
             work(s, kts, vts + MEMB, 0);
             store_value(r0, vts);
             store_key(r1, kts + MEMB);
-            r0 = load_regs(hh, s + 2);
+            r0 = load_regs(s + 2);
             lds_barrier();
-            if (s + 1 > jmax) break;
+            if (s + 1 > nmem) break;
             work(s + 1, kts + MEMB, vts, 1);
             store_value(r1, vts + MEMB);
             store_key(r0, kts);
-            r1 = load_regs(hh, s + 3);
+            r1 = load_regs(s + 3);
             lds_barrier();
-            if (s + 2 > jmax) break;
+            if (s + 2 > nmem) break;
         }
     };
 
@@ -260,17 +261,10 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         trow[rt] = b * L + (t < L ? t : L - 1);
     }
     Regs r0, r1;
-    if (jmax > 0) {
-        r0 = load_regs(0, 0);
-        r1 = load_regs(0, 1);
+    if (nmem > 0) {
+        r0 = load_regs(0);
+        r1 = load_regs(1);
     }
-    // after a head's last step: its successor's first two memories
-    auto preload_next = [&](int hh) {
-        if (jmax > 0 && hh + 1 < hpb) {
-            r0 = load_regs(hh + 1, 0);
-            r1 = load_regs(hh + 1, 1);
-        }
-    };
     const bool hist = ip >= 1;
 
     if (scorer) {
@@ -344,86 +338,94 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 }
             }
         }
-        for (int hh = 0; hh < hpb; ++hh) {
-        const int h = h0 + hh;
         float m[RT], d[RT];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            m[rt] = -INFINITY;
-            d[rt] = 0.f;
-        }
-
-        stream(hh, r0, r1, [&](int s, const char* kt, const char*, int buf) {
-            if (s >= nj) return;
-            // U^T slices: fragments of slice pt+1 are read before the MFMAs of
-            // slice pt (scheduling fences keep that order)
-            Frag<T> fb[2][KS];
-            read_slice(kt, 0, fb[0]);
-            float lp[RT];
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                if (pt < 3) read_slice(kt, pt + 1, fb[(pt + 1) & 1]);
-                __builtin_amdgcn_sched_barrier(0);
-                f32x4 u[RT];
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fb[pt & 1][ks], qf[rt][ks]);
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            // full logit of the lane's token: sum the 4 lanes sharing its
-            // column with one fp32 MFMA against a ones matrix
-            // (D[i][t] = sum_k B[k][t])
-            bool grow = false;
+        // LSE of one head, and its denominators for the value wave
+        auto finish_head = [&](int hh) __attribute__((always_inline)) {
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                const f32x4 red = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                    1.0f, lp[rt], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-                lp[rt] = red[0];
-                grow |= lp[rt] > m[rt] + kRescaleLog2;
+                if (grp == 0) xd[hh & 1][pair][rt * 16 + col] = d[rt];
+                if (lse && grp == 0 && tvalid[rt])
+                    lse[trow[rt] * H + h0 + hh] = hist ? (m[rt] + log2f(d[rt])) * kLn2 : -INFINITY;
             }
-            // lazy rescale: the reference maximum only moves when a logit
-            // exceeds it by more than 2^8, so weights stay <= 256 and O is
-            // rescaled rarely; R = O/d and LSE = m + log2 d do not depend on
-            // the choice of m
-            const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
-            if (rescale) {
+        };
+        if (nmem == 0) {
+            // no history in this block: LSE = -inf for every head
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) d[rt] = 0.f;
+            for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
+            return;
+        }
+        stream(r0, r1, [&](int s, const char* kt, const char*, int buf) {
+            if (s >= nmem) return;
+            const int hh = s / jmax, j = s - hh * jmax;
+            if (j == 0) {
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
-                    const float mn = fmaxf(m[rt], lp[rt]);
-                    const float al = fast_exp2(m[rt] - mn);
-                    d[rt] *= al;
-                    m[rt] = mn;
-                    if (grp == 0) xa[buf][pair][rt * 16 + col] = al;
+                    m[rt] = -INFINITY;
+                    d[rt] = 0.f;
                 }
             }
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                const float pw = fast_exp2(lp[rt] - m[rt]);
-                d[rt] += pw;
-                if (grp == 0) xw[buf][pair][rt * 16 + col] = pw;
+            if (j < nj) {
+                // U^T slices: fragments of slice pt+1 are read before the MFMAs of
+                // slice pt (scheduling fences keep that order)
+                Frag<T> fb[2][KS];
+                read_slice(kt, 0, fb[0]);
+                float lp[RT];
+    #pragma unroll
+                for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
+    #pragma unroll
+                for (int pt = 0; pt < 4; ++pt) {
+                    if (pt < 3) read_slice(kt, pt + 1, fb[(pt + 1) & 1]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    f32x4 u[RT];
+    #pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                    for (int ks = 0; ks < KS; ++ks)
+    #pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fb[pt & 1][ks], qf[rt][ks]);
+    #pragma unroll
+                    for (int rt = 0; rt < RT; ++rt)
+    #pragma unroll
+                        for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+                // full logit of the lane's token: sum the 4 lanes sharing its
+                // column with one fp32 MFMA against a ones matrix
+                // (D[i][t] = sum_k B[k][t])
+                bool grow = false;
+    #pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    const f32x4 red = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        1.0f, lp[rt], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                    lp[rt] = red[0];
+                    grow |= lp[rt] > m[rt] + kRescaleLog2;
+                }
+                // lazy rescale: the reference maximum only moves when a logit
+                // exceeds it by more than 2^8, so weights stay <= 256 and O is
+                // rescaled rarely; R = O/d and LSE = m + log2 d do not depend on
+                // the choice of m
+                const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+                if (rescale) {
+    #pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) {
+                        const float mn = fmaxf(m[rt], lp[rt]);
+                        const float al = fast_exp2(m[rt] - mn);
+                        d[rt] *= al;
+                        m[rt] = mn;
+                        if (grp == 0) xa[buf][pair][rt * 16 + col] = al;
+                    }
+                }
+    #pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    const float pw = fast_exp2(lp[rt] - m[rt]);
+                    d[rt] += pw;
+                    if (grp == 0) xw[buf][pair][rt * 16 + col] = pw;
+                }
+                if (lane == 0) xr[buf][pair] = rescale ? 1 : 0;
             }
-            if (lane == 0) xr[buf][pair] = rescale ? 1 : 0;
+            if (j == jmax - 1) finish_head(hh);
         });
-
-        preload_next(hh);
-        // ---- publish the denominators, write LSE -------------------------------
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            if (grp == 0) xd[hh & 1][pair][rt * 16 + col] = d[rt];
-            if (lse && grp == 0 && tvalid[rt])
-                lse[trow[rt] * H + h] = hist ? (m[rt] + log2f(d[rt])) * kLn2 : -INFINITY;
-        }
-        lds_barrier();
-        }
     } else {
         // ---- value wave: C of the pair's tokens, accumulator O ----------------
         Frag<T> cf[RT][KS];
@@ -441,77 +443,86 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 for (int ks = 0; ks < KS; ++ks) cf[rt][ks] = Frag<T>{};
             }
         }
-        for (int hh = 0; hh < hpb; ++hh) {
-        const int h = h0 + hh;
         f32x4 o[RT][4];
+        // y = y_ssd + SiLU(z) R of one head
+        auto finish_head = [&](int hh) __attribute__((always_inline)) {
+            const int h = h0 + hh;
+            float zz[RT];
+            Vec4<T> ys[RT][4];
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+            for (int rt = 0; rt < RT; ++rt) {
+                zz[rt] = to_f(z_per_head ? z[trow[rt] * H + h] : z[trow[rt]]);
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt) o[rt][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-        stream(hh, r0, r1, [&](int s, const char*, const char* vt, int buf) {
+                for (int pt = 0; pt < 4; ++pt) ys[rt][pt] = ld4(y_ssd + (trow[rt] * H + h) * kP + pt * 16 + grp * 4);
+            }
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                if (!tvalid[rt]) continue;
+                const float gate = silu(zz[rt]);
+                const float invd = hist ? 1.0f / xd[hh & 1][pair][rt * 16 + col] : 0.f;
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) {
+                    float yv[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[rt][pt][i]);
+                    if (hist) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) yv[i] += gate * (o[rt][pt][i] * invd);
+                    }
+                    store4(y + (trow[rt] * H + h) * kP + pt * 16 + grp * 4, yv);
+                }
+            }
+        };
+        if (nmem == 0) {
+            // no history in this block: y = y_ssd for every head
+            for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
+            return;
+        }
+        stream(r0, r1, [&](int s, const char*, const char* vt, int buf) {
             // memory s-1, scored in the previous step (weights in slot buf^1)
-            if (s < 1 || s - 1 >= nj) return;
-            const int wb = buf ^ 1;
-            Frag<T> fb[2][KS];
-            read_slice(vt, 0, fb[0]);
-            float pw[RT];
+            if (s < 1) return;
+            const int hh = (s - 1) / jmax, j = (s - 1) - hh * jmax;
+            if (j == 0) {
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) pw[rt] = xw[wb][pair][rt * 16 + col];
-            if (__builtin_amdgcn_readfirstlane(xr[wb][pair])) {
+                for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                for (int rt = 0; rt < RT; ++rt) {
-                    const float al = xa[wb][pair][rt * 16 + col];
-#pragma unroll
-                    for (int pt = 0; pt < 4; ++pt) o[rt][pt] *= al;
+                    for (int pt = 0; pt < 4; ++pt) o[rt][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+            if (j < nj) {
+                const int wb = buf ^ 1;
+                Frag<T> fb[2][KS];
+                read_slice(vt, 0, fb[0]);
+                float pw[RT];
+    #pragma unroll
+                for (int rt = 0; rt < RT; ++rt) pw[rt] = xw[wb][pair][rt * 16 + col];
+                if (__builtin_amdgcn_readfirstlane(xr[wb][pair])) {
+    #pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) {
+                        const float al = xa[wb][pair][rt * 16 + col];
+    #pragma unroll
+                        for (int pt = 0; pt < 4; ++pt) o[rt][pt] *= al;
+                    }
+                }
+    #pragma unroll
+                for (int pt = 0; pt < 4; ++pt) {
+                    if (pt < 3) read_slice(vt, pt + 1, fb[(pt + 1) & 1]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    f32x4 v[RT];
+    #pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+                    for (int ks = 0; ks < KS; ++ks)
+    #pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fb[pt & 1][ks], cf[rt][ks]);
+    #pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) o[rt][pt] += pw[rt] * v[rt];
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                if (pt < 3) read_slice(vt, pt + 1, fb[(pt + 1) & 1]);
-                __builtin_amdgcn_sched_barrier(0);
-                f32x4 v[RT];
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fb[pt & 1][ks], cf[rt][ks]);
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) o[rt][pt] += pw[rt] * v[rt];
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            // the head's last memory is in: its denominators were published
+            // in the previous step
+            if (j == jmax - 1) finish_head(hh);
         });
-
-        preload_next(hh);
-        // ---- epilogue: y = y_ssd + SiLU(z) R -----------------------------------
-        float zz[RT];
-        Vec4<T> ys[RT][4];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            zz[rt] = to_f(z_per_head ? z[trow[rt] * H + h] : z[trow[rt]]);
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) ys[rt][pt] = ld4(y_ssd + (trow[rt] * H + h) * kP + pt * 16 + grp * 4);
-        }
-        lds_barrier();
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            if (!tvalid[rt]) continue;
-            const float gate = silu(zz[rt]);
-            const float invd = hist ? 1.0f / xd[hh & 1][pair][rt * 16 + col] : 0.f;
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                float yv[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[rt][pt][i]);
-                if (hist) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) yv[i] += gate * (o[rt][pt][i] * invd);
-                }
-                store4(y + (trow[rt] * H + h) * kP + pt * 16 + grp * 4, yv);
-            }
-        }
-        }
     }
 }
 
