@@ -110,8 +110,9 @@ dart_status dart_ssd_chunk_scan(const dart_dims* dims, const void* x, const floa
                                 void* y_ssd, void* mem, float* h_last, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
-/* Bytes of workspace dart_sma_fwd needs for `dims`.  This build streams the
- * memories straight from `mem` and needs none (0; workspace may be NULL). */
+/* Bytes of workspace dart_sma_fwd needs for `dims`: the key side
+ * r_j (.) dH_j of memories 0..M-2 in the cache layout (storage dtype); 0 when
+ * M = 1 (workspace may then be NULL). */
 size_t dart_sma_workspace_bytes(const dart_dims* dims);
 
 /*

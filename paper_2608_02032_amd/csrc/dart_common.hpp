@@ -162,6 +162,25 @@ __device__ __forceinline__ void lds_dma16(const void* gsrc, void* lds_wave_base)
                                      16, 0, 0);
 }
 __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0); }
+// The same copy issued from inline assembly, invisible to the compiler's
+// wait-count tracking: the caller must wait for it (s_waitcnt vmcnt) before
+// the LDS bytes are read.  Used where the compiler cannot tell a copy in
+// flight from the tiles being read and would otherwise drain every copy
+// before each LDS read.  M0 (the LDS base) is saved and restored.
+__device__ __forceinline__ void lds_dma16_untracked(const void* gsrc, void* lds_wave_base) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_wave_base);
+    uint32_t save;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(save)
+        : "v"(gsrc), "s"(m0)
+        : "memory");
+}
 // s_waitcnt immediate that waits until at most k vector-memory operations of
 // the wave are outstanding (expcnt and lgkmcnt left unconstrained; gfx9
 // encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
@@ -194,7 +213,9 @@ struct SwzTile {
 // Copy `rows` rows of RB bytes (global row stride gstride bytes) into a
 // swizzled LDS tile.  Rows >= rows_valid read the last valid row instead
 // (never out of bounds); callers mask their contribution.  rows_valid >= 1.
-template <int RB>
+// Wave w issues copies q0 = 64 w, 64 (w + nwaves), ... of the rows * RB / 1024
+// one-KiB pieces.  UNTRACKED selects lds_dma16_untracked.
+template <int RB, bool UNTRACKED = false>
 __device__ __forceinline__ void dma_tile(char* lds, const char* g, int64_t gstride, int rows,
                                          int rows_valid, int wave, int nwaves, int lane) {
     using Tl = SwzTile<RB>;
@@ -205,7 +226,11 @@ __device__ __forceinline__ void dma_tile(char* lds, const char* g, int64_t gstri
             const int r = q / Tl::CPR, cs = q % Tl::CPR;
             const int c = cs ^ (r & Tl::MASK);
             const int rr = r < rows_valid ? r : rows_valid - 1;
-            lds_dma16(g + rr * gstride + c * 16, lds + q0 * 16);
+            if constexpr (UNTRACKED) {
+                lds_dma16_untracked(g + rr * gstride + c * 16, lds + q0 * 16);
+            } else {
+                lds_dma16(g + rr * gstride + c * 16, lds + q0 * 16);
+            }
         }
     }
 }

@@ -16,8 +16,10 @@ struct Shape {
     int dtype;     // 0 fp32, 1 bf16
 };
 
-// Workspace carve-up of the scan: per-chunk log decay [B][H][M] (float) and the
-// chunk-entry states [B][M][H][N][P] (storage dtype).
+// Workspace of the scan: per-chunk log decay [B][H][M] (float), the
+// chunk-entry states [B][M][H][N][P] (storage dtype), the within-chunk
+// cumulative log decay [B][H][M][S] and the causal Gram tiles of every chunk
+// and group (float).
 size_t scan_workspace_bytes(const Shape& s);
 hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const float* A,
                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
@@ -31,7 +33,8 @@ struct SmaArgs {
     int z_per_head;
 };
 
-// Workspace of the SMA forward: none (the kernel reads the memories as stored).
+// Workspace of the SMA forward: the key side r (.) dH of memories 0..M-2,
+// [B][M-1][H][N][P] in the storage dtype.
 size_t sma_workspace_bytes(const Shape& s);
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,

@@ -6,19 +6,24 @@
 // Y = Y_intra + Y_inter; block form Y_[c] = C<-_[c] H_[c-1] + L_[c] X_[c]).
 // Discretisation: a_t = exp(dt_t A_h), input dt_t B_t^T x_t.
 //
-// Three kernels, one stream:
+// Four kernels, one stream:
 //   k_chunk_state  per (b, chunk, head): within-chunk cumulative log decay
-//                  cs, then dH = B^T diag(exp(cs_e - cs_s) dt_s) X on MFMA
-//                  (B and X staged transposed through LDS), written to `mem`;
-//                  the chunk's total log decay cs_e goes to the workspace.
+//                  cs (kept in the workspace, log2 units, for k_chunk_out),
+//                  then dH = B^T diag(exp(cs_e - cs_s) dt_s) X on MFMA (B and X
+//                  staged through LDS), written to `mem`; the chunk's total log
+//                  decay cs_e goes to the workspace.
+//   k_chunk_gram   per (b, chunk, group, 4 row tiles): the causal part of the
+//                  chunk's Gram matrix G^T = B C^T (it depends on the group,
+//                  not the head, so it is formed once for all heads of a
+//                  group), stored in the MFMA accumulator layout that
+//                  k_chunk_out consumes as its A operand.
 //   k_state_pass   per (b, head, element block): sequential over chunks,
 //                  H_[c] = exp(cs_e(c)) H_[c-1] + dH_[c]; stores the state
 //                  entering every chunk (workspace) and h_last.
-//   k_chunk_out    per (b, chunk, head): y = (L o C B^T)(dt X) + (C o e^{cs}) H_[c-1]
-//                  on MFMA.  The Gram tile G^T = B C^T comes out of the MFMA
-//                  in exactly the register layout the next MFMA wants for its
-//                  A operand (rows t, 8 s-values per lane), so the masked and
-//                  decayed scores never leave registers.
+//   k_chunk_out    per (b, chunk, head): y = (L o G)(dt X) + (C o e^{cs}) H_[c-1]
+//                  on MFMA: the Gram tiles are read straight into registers,
+//                  masked and decayed there, and multiplied with X (staged
+//                  through LDS).
 // Decays are always exponentiated as differences cs_t - cs_s <= 0 (no
 // overflow; underflow to 0 is the correct limit).
 #include "dart_common.hpp"
@@ -58,8 +63,8 @@ __device__ float block_inclusive_scan(float v, float* sred) {
 template <typename T, int N, int S>
 __global__ __launch_bounds__(kThreads) void k_chunk_state(
     const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
-    const T* __restrict__ Bm, T* __restrict__ mem, float* __restrict__ chunk_lda, int64_t L, int H,
-    int G, int64_t M, int64_t Mcap) {
+    const T* __restrict__ Bm, T* __restrict__ mem, float* __restrict__ chunk_lda,
+    float* __restrict__ cs2, int64_t L, int H, int G, int64_t M, int64_t Mcap) {
     constexpr int XRB = kP * (int)sizeof(T);   // bytes per x row
     constexpr int BRB = N * (int)sizeof(T);    // bytes per B row
     constexpr int XT = kSB * XRB, BT = kSB * BRB;
@@ -97,7 +102,10 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
     if (tid == S - 1) s_cse = cs;
     __syncthreads();
     const float cse = s_cse;
-    if (tid < S) s_w[tid] = (tid < len) ? __expf(cse - cs) * dts : 0.f;
+    if (tid < S) {
+        s_w[tid] = (tid < len) ? __expf(cse - cs) * dts : 0.f;
+        cs2[((b * H + h) * M + c) * S + tid] = cs * kLog2e;
+    }
     if (tid == 0) chunk_lda[(b * H + h) * M + c] = cse;
 
     f32x4 acc[N / 16];
@@ -178,61 +186,111 @@ __global__ __launch_bounds__(kThreads) void k_state_pass(
 }
 
 // ---------------------------------------------------------------------------
-// Chunk output: y_t = sum_{s<=t} (C_t.B_s) exp(cs_t - cs_s) dt_s x_s
+// Causal Gram tiles.  Row tile r (tokens t in [16r, 16r+16)) meets the 32-token
+// s blocks sk = 0..r/2; pair (r, sk) holds G^T[s][t] = B_s . C_t for
+// s = 32 sk + 16u + 4 (lane/16) + i, t = 16 r + lane%16 as 8 floats per lane
+// (u, i), which is the accumulator layout of the MFMA below and the A-operand
+// layout k_chunk_out wants (any consistent k order is valid).
+// ---------------------------------------------------------------------------
+__host__ __device__ constexpr int gram_pairs(int S) { return (S / 32) * (S / 32 + 1); }
+__device__ __forceinline__ int gram_pair(int r, int sk) {
+    const int m = r >> 1;
+    return ((r & 1) ? (m + 1) * (m + 1) : m * (m + 1)) + sk;
+}
+
+template <typename T, int N, int S>
+__global__ __launch_bounds__(kThreads) void k_chunk_gram(const T* __restrict__ Bm,
+                                                         const T* __restrict__ Cm,
+                                                         float* __restrict__ gram, int64_t L,
+                                                         int G, int64_t M) {
+    constexpr int KS = N / 32;
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t c = blockIdx.y;
+    const int64_t bg = blockIdx.z;  // b * G + g
+    const int64_t b = bg / G;
+    const int g = (int)(bg % G);
+    const int lane = threadIdx.x & 63, col = lane & 15, grp = lane >> 4;
+    const int64_t t0 = c * S;
+    const int len = (int)(L - t0 < S ? L - t0 : S);
+    // rows past the end of a partial chunk read the last row (finite values;
+    // k_chunk_out gives them zero weight)
+    auto row = [&](const T* base, int t) {
+        const int tc = t < len ? t : len - 1;
+        return base + ((b * L + t0 + tc) * G + g) * N;
+    };
+    Frag<T> cf[KS];
+    const T* crow = row(Cm, r * 16 + col);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) cf[ks] = load_frag(crow + ks * 32 + grp * 8);
+    float* out = gram + (bg * M + c) * (int64_t)gram_pairs(S) * 512;
+    for (int sk = 0; sk <= (r >> 1); ++sk) {
+        f32x4 gacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const T* brow = row(Bm, sk * 32 + u * 16 + col);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) gacc[u] = mma16(gacc[u], load_frag(brow + ks * 32 + grp * 8), cf[ks]);
+        }
+        f32x4* dst = reinterpret_cast<f32x4*>(out + ((int64_t)gram_pair(r, sk) * 64 + lane) * 8);
+        dst[0] = gacc[0];
+        dst[1] = gacc[1];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Chunk output: y_t = sum_{s<=t} G_ts exp(cs_t - cs_s) dt_s x_s
 //                     + exp(cs_t) C_t H_[c-1].
-// Wave w owns the 16-row tiles rt = w, w+4, ... (interleaved for balance).
-// H_[c-1], B_c and x_c are DMA-staged in natural layout (B and x in two
-// 64-token stages held in distinct LDS objects); C rows stay in registers.
+// Wave w owns the 16-row tiles r = w, w+4, ... (interleaved for balance).
+// H_[c-1] and the chunk's x rows are DMA-staged in natural layout; C rows (for
+// the inter-chunk term) and the Gram tiles go straight to registers.
 // ---------------------------------------------------------------------------
 template <typename T, int N, int S>
-__global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_chunk_out(
-    const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
-    const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ states,
-    T* __restrict__ y, int64_t L, int H, int G, int64_t M) {
+__global__ __launch_bounds__(kThreads) void k_chunk_out(
+    const T* __restrict__ x, const float* __restrict__ dt, const T* __restrict__ Cm,
+    const T* __restrict__ states, const float* __restrict__ cs2, const float* __restrict__ gram,
+    T* __restrict__ y, int64_t L, int H, int G, int64_t M, int64_t BM) {
     constexpr int KS = N / 32;     // 32-deep k steps over the state dim
     constexpr int NQ = S / 64;     // row tiles per wave
     constexpr int XRB = kP * (int)sizeof(T);
-    constexpr int BRB = N * (int)sizeof(T);
-    constexpr int XT = kSB * XRB, BT = kSB * BRB;
+    constexpr int XT = S * XRB;    // the chunk's x rows
     constexpr int HT = N * XRB;    // H_[c-1] tile, rows n of P values
-    const int c = blockIdx.x, h = blockIdx.y;
-    const int64_t b = blockIdx.z;
+    // Block order: workgroups are dealt to the 8 XCDs round-robin by block
+    // index.  When B*M is a multiple of 8, XCD x runs the heads of chunks
+    // (b, c) = x, x+8, ... one after another, so all heads reading one
+    // chunk's Gram tiles share one L2.
+    const int64_t bid = blockIdx.x;
+    int64_t bc;
+    int h;
+    if (BM % 8 == 0) {
+        const int64_t slot = bid >> 3;
+        bc = (slot / H) * 8 + (bid & 7);
+        h = (int)(slot % H);
+    } else {
+        bc = bid / H;
+        h = (int)(bid % H);
+    }
+    const int64_t b = bc / M;
+    const int64_t c = bc % M;
     const int g = (int)((int64_t)h * G / H);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    const int64_t t0 = (int64_t)c * S;
+    const int64_t t0 = c * S;
     const int len = (int)(L - t0 < S ? L - t0 : S);
-    const int nsb = (len + kSB - 1) / kSB;
 
     __shared__ float s_cs[S];  // within-chunk cumulative log decay, log2 units
     __shared__ float s_dt[S];
-    __shared__ float s_red[4];
     __shared__ __attribute__((aligned(16))) char ht[HT];
-    __shared__ __attribute__((aligned(16))) char xs0[XT];
-    __shared__ __attribute__((aligned(16))) char bs0[BT];
-    __shared__ __attribute__((aligned(16))) char xs1[XT];
-    __shared__ __attribute__((aligned(16))) char bs1[BT];
+    __shared__ __attribute__((aligned(16))) char xs[XT];
     __shared__ __attribute__((aligned(16))) T so[4][16 * kP];  // per-wave output tile
 
-    const char* xg = reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP);
-    const char* bg = reinterpret_cast<const char*>(Bm + ((b * L + t0) * G + g) * N);
-    const int64_t xstride = (int64_t)H * XRB, bstride = (int64_t)G * BRB;
-    auto stage = [&](int sb, char* xd, char* bd) {
-        const int rv = len - sb * kSB;
-        dma_tile<XRB>(xd, xg + sb * kSB * xstride, xstride, kSB, rv, wave, 4, lane);
-        dma_tile<BRB>(bd, bg + sb * kSB * bstride, bstride, kSB, rv, wave, 4, lane);
-    };
     dma_tile<XRB>(ht, reinterpret_cast<const char*>(states + ((b * M + c) * H + h) * (int64_t)N * kP),
                   XRB, N, N, wave, 4, lane);
-    stage(0, xs0, bs0);
-
-    const float dts = (tid < len) ? dt[(b * L + t0 + tid) * H + h] : 0.f;
-    const float cs = block_inclusive_scan(tid < S ? dts * A[h] : 0.f, s_red);
-    if (tid < S) {
-        s_cs[tid] = cs * kLog2e;
-        s_dt[tid] = dts;
+    dma_tile<XRB>(xs, reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP),
+                  (int64_t)H * XRB, S, len, wave, 4, lane);
+    for (int i = tid; i < S; i += kThreads) {
+        s_cs[i] = cs2[((b * H + h) * M + c) * S + i];
+        s_dt[i] = (i < len) ? dt[(b * L + t0 + i) * H + h] : 0.f;
     }
-
     // C rows of this wave's tiles, in fragment layout (row t = lane%16)
     Frag<T> cf[NQ][KS];
     f32x4 yacc[NQ][4];
@@ -269,59 +327,68 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_chunk_out(
         }
     }
 
-    auto consume = [&](int sb, const char* xt, const char* bt) {
-        const int s0 = sb * kSB;
+    // intra-chunk term, one 32-token s block at a time for all of the wave's
+    // row tiles: Gram values (loaded one block ahead) times the causal mask,
+    // the decay and dt_s, then times x on MFMA (x fragments shared by the
+    // tiles).  A tile that does not reach the s block uses zeros.
+    const float* gbase = gram + ((b * G + g) * M + c) * (int64_t)gram_pairs(S) * 512 + lane * 8;
+    const int last_sk = ((wave + 4 * (NQ - 1)) * 16 + 15) / 32;  // last block any tile reaches
+    auto load_gram = [&](int sk, f32x4 (&gv)[NQ][2]) {
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            const int tlo = (wave + 4 * q) * 16;
-#pragma unroll
-            for (int ss = 0; ss < 2; ++ss) {
-                const int sbase = s0 + ss * 32;
-                if (sbase > tlo + 15) continue;  // wave-uniform: fully above the diagonal
-                // Gram tiles G^T[s][t] for s in [sbase, sbase+32), t in the row tile
-                f32x4 gacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        const Frag<T> fb = frag_rowmajor<T, BRB>(bt, ss * 32 + u * 16 + col, ks * 32 + grp * 8);
-                        gacc[u] = mma16(gacc[u], fb, cf[q][ks]);
-                    }
-                }
-                // causal mask, decay and dt_s: lane holds t = tlo + col and
-                // s = sbase + 16u + 4 grp + i
-                const int t = tlo + col;
-                const float cst = s_cs[t];
-                float mv[8];
-#pragma unroll
-                for (int u = 0; u < 2; ++u)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int s = sbase + 16 * u + 4 * grp + i;
-                        mv[4 * u + i] = (s <= t) ? gacc[u][i] * fast_exp2(cst - s_cs[s]) * s_dt[s] : 0.f;
-                    }
-                const Frag<T> fm = make_frag<T>(mv);
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt) {
-                    // x operand rows s = sbase + {4 grp + 0..3, 16 + 4 grp + 0..3}, column p
-                    const Frag<T> fx = frag_km<T, XRB>(xt, ss * 32 + 4 * grp, ss * 32 + 16 + 4 * grp,
-                                                       pt * 16, lane);
-                    yacc[q][pt] = mma16(yacc[q][pt], fm, fx);
-                }
+            const int r = wave + 4 * q;
+            if (2 * sk <= r) {
+                const f32x4* src = reinterpret_cast<const f32x4*>(gbase + (int64_t)gram_pair(r, sk) * 512);
+                gv[q][0] = src[0];
+                gv[q][1] = src[1];
+            } else {
+                gv[q][0] = gv[q][1] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
         }
     };
-    for (int sb = 0; sb < nsb; sb += 2) {
-        if (sb + 1 < nsb) stage(sb + 1, xs1, bs1);
-        consume(sb, xs0, bs0);
-        wait_dma();
-        __syncthreads();
-        if (sb + 1 >= nsb) break;
-        if (sb + 2 < nsb) stage(sb + 2, xs0, bs0);
-        consume(sb + 1, xs1, bs1);
-        wait_dma();
-        __syncthreads();
+    f32x4 gcur[NQ][2], gnext[NQ][2];
+    load_gram(0, gcur);
+    for (int sk = 0; sk <= last_sk; ++sk) {
+        if (sk < last_sk) load_gram(sk + 1, gnext);
+        const int sbase = sk * 32;
+        float css[8], dts8[8];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                css[4 * u + i] = s_cs[sbase + 16 * u + 4 * grp + i];
+                dts8[4 * u + i] = s_dt[sbase + 16 * u + 4 * grp + i];
+            }
+        Frag<T> fm[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int t = (wave + 4 * q) * 16 + col;
+            const float cst = s_cs[t];
+            float mv[8];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int k = 4 * u + i;
+                    const int s = sbase + 16 * u + 4 * grp + i;
+                    mv[k] = (s <= t) ? gcur[q][u][i] * fast_exp2(cst - css[k]) * dts8[k] : 0.f;
+                }
+            fm[q] = make_frag<T>(mv);
+        }
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) {
+            // x operand rows s = sbase + {4 grp + 0..3, 16 + 4 grp + 0..3}, column p
+            const Frag<T> fx = frag_km<T, XRB>(xs, sbase + 4 * grp, sbase + 16 + 4 * grp, pt * 16, lane);
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) yacc[q][pt] = mma16(yacc[q][pt], fm[q], fx);
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            gcur[q][0] = gnext[q][0];
+            gcur[q][1] = gnext[q][1];
+        }
     }
+
     // yacc[q][pt][i] = y[t = 16 (wave + 4q) + 4 grp + i][p = 16 pt + col]:
     // each 16-row tile goes through the wave's LDS scratch and leaves as
     // 16-byte stores of whole rows
@@ -345,27 +412,56 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_chunk_out(
     }
 }
 
+// Workspace carve-up of the scan: per-chunk log decay [B][H][M], chunk-entry
+// states [B][M][H][N][P] (storage dtype), within-chunk cumulative log decay
+// [B][H][M][S] and the causal Gram tiles [B][G][M][pairs][64][8] (float).
+struct ScanWs {
+    float* lda;
+    char* states;
+    float* cs2;
+    float* gram;
+    size_t total;
+};
+ScanWs scan_ws(const Shape& s, void* ws) {
+    char* p = reinterpret_cast<char*>(ws);
+    ScanWs w;
+    size_t off = 0;
+    w.lda = reinterpret_cast<float*>(p + off);
+    off += align256(sizeof(float) * s.B * s.H * s.M);
+    w.states = p + off;
+    off += align256(elem_bytes(s.dtype) * s.B * s.M * s.H * (size_t)s.N * s.P);
+    w.cs2 = reinterpret_cast<float*>(p + off);
+    off += align256(sizeof(float) * s.B * s.H * s.M * (size_t)s.S);
+    w.gram = reinterpret_cast<float*>(p + off);
+    off += align256(sizeof(float) * s.B * s.G * s.M * (size_t)gram_pairs(s.S) * 512);
+    w.total = off;
+    return w;
+}
+
 template <typename T, int N, int S>
 hipError_t run_scan(const Shape& s, const void* x, const float* dt, const float* A, const void* Bm,
                     const void* Cm, const float* h0, void* y_ssd, void* mem, float* h_last,
                     void* ws, hipStream_t st) {
-    float* lda = reinterpret_cast<float*>(ws);
-    T* states = reinterpret_cast<T*>(reinterpret_cast<char*>(ws) +
-                                     align256(sizeof(float) * s.B * s.H * s.M));
+    const ScanWs w = scan_ws(s, ws);
+    T* states = reinterpret_cast<T*>(w.states);
     const dim3 grid((unsigned)s.M, (unsigned)s.H, (unsigned)s.B);
     prof_begin("k_chunk_state", st);
     k_chunk_state<T, N, S><<<grid, kThreads, 0, st>>>(
-        (const T*)x, dt, A, (const T*)Bm, (T*)mem, lda, s.L, s.H, s.G, s.M, s.Mcap);
+        (const T*)x, dt, A, (const T*)Bm, (T*)mem, w.lda, w.cs2, s.L, s.H, s.G, s.M, s.Mcap);
+    prof_end(st);
+    prof_begin("k_chunk_gram", st);
+    k_chunk_gram<T, N, S><<<dim3((unsigned)(S / 64), (unsigned)s.M, (unsigned)(s.B * s.G)), kThreads,
+                            0, st>>>((const T*)Bm, (const T*)Cm, w.gram, s.L, s.G, s.M);
     prof_end(st);
     const int NP = N * kP;
     prof_begin("k_state_pass", st);
     k_state_pass<T><<<dim3((unsigned)(NP / (kThreads * 4)), (unsigned)s.H, (unsigned)s.B), kThreads,
-                      0, st>>>((const T*)mem, lda, h0, states, h_last, s.H, NP, s.M, s.Mcap);
+                      0, st>>>((const T*)mem, w.lda, h0, states, h_last, s.H, NP, s.M, s.Mcap);
     prof_end(st);
     prof_begin("k_chunk_out", st);
-    k_chunk_out<T, N, S><<<grid, kThreads, 0, st>>>((const T*)x, dt, A, (const T*)Bm,
-                                                    (const T*)Cm, states, (T*)y_ssd, s.L, s.H,
-                                                    s.G, s.M);
+    k_chunk_out<T, N, S><<<dim3((unsigned)(s.B * s.M * s.H)), kThreads, 0, st>>>(
+        (const T*)x, dt, (const T*)Cm, states, w.cs2, w.gram, (T*)y_ssd, s.L, s.H, s.G, s.M,
+        s.B * s.M);
     prof_end(st);
     return hipGetLastError();
 }
@@ -396,10 +492,7 @@ hipError_t run_scan_n(const Shape& s, const void* x, const float* dt, const floa
 
 }  // namespace
 
-size_t scan_workspace_bytes(const Shape& s) {
-    return align256(sizeof(float) * s.B * s.H * s.M) +
-           align256(elem_bytes(s.dtype) * s.B * s.M * s.H * (size_t)s.N * s.P);
-}
+size_t scan_workspace_bytes(const Shape& s) { return scan_ws(s, nullptr).total; }
 
 hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const float* A,
                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,

@@ -15,18 +15,21 @@
 // per-token operands and every operand fragment it reads from LDS feeds RT
 // independent MFMA chains.
 //
-// The memories dH_j (j < the block's last chunk) stream from the memory cache
-// as stored ([N][P] rows, 16-byte loads into registers ahead of use).  When a
-// loaded memory is written to LDS, the lanes holding one row reduce its inverse
-// RMS r_j[n]; two swizzled [N][P] tiles are written, the key side
-// r_j (.) dH_j and the value side dH_j.  Step s of the streaming loop:
+// A first kernel, k_sma_keys, writes the key side of every attended memory,
+// r_j (.) dH_j with r_j[n] = (mean_p dH_j[n,p]^2 + eps)^-1/2 reduced from the
+// stored values, to the workspace (same [N][P] layout as the cache).  The
+// main kernel streams key tiles from there and value tiles dH_j straight from
+// the memory cache into swizzled [N][P] LDS tiles: by DMA two steps ahead into
+// a four-stage ring (global_load_lds, no registers), or, when four stages do
+// not fit in LDS (fp32, N = 128), through registers one step ahead into two
+// stages.  Step s of the streaming loop:
 //   score waves   U^T = (r_s (.) dH_s)^T Qbar^T (P x tokens, MFMA), logits
 //                 l_t = sum_p U^T[p,t] Ebar[t,p] (the lane's registers plus one
 //                 MFMA against a ones matrix for the 4 lanes of a column),
 //                 online softmax in base 2; the weights of memory s (and a
 //                 rescale factor when the running maximum moved) go to LDS;
 //   value waves   V^T = dH_{s-1}^T C^T (MFMA), O = alpha O + w_{s-1} V;
-//   all threads   write key tile s+1 and value tile s, load memory s+2.
+//   all threads   copy the tiles of a later memory.
 // One barrier per step.  Epilogue: the score wave publishes its softmax
 // denominators and writes LSE = (m + log2 d) ln 2; the value wave writes
 // y = y_ssd + SiLU(z) O/d.  Operand fragments are read with transposing LDS
@@ -99,13 +102,41 @@ __device__ __forceinline__ uint4 piece_scale(uint4 v, float r, float) {
     return __builtin_bit_cast(uint4, f);
 }
 
+// Key side of one memory: kmem = r (.) dH, r[n] the inverse RMS of row n of
+// the stored values.  The RPC lanes holding one row's 16-byte pieces reduce
+// its sum of squares with DPP moves.
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* __restrict__ kmem,
+                                                  float eps, int normalize, int H, int64_t Mp,
+                                                  int64_t Mcap) {
+    constexpr int RB = kP * (int)sizeof(T);
+    constexpr int PIECES = N * RB / 16;
+    constexpr int RPC = RB / 16;
+    static_assert(PIECES % 256 == 0, "pieces must tile the block");
+    const int64_t j = blockIdx.x;
+    const int h = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const uint4* src = reinterpret_cast<const uint4*>(mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP);
+    uint4* dst = reinterpret_cast<uint4*>(kmem + ((b * Mp + j) * H + h) * (int64_t)N * kP);
+    uint4 v[PIECES / 256];
+#pragma unroll
+    for (int i = 0; i < PIECES / 256; ++i) v[i] = src[threadIdx.x + i * 256];
+#pragma unroll
+    for (int i = 0; i < PIECES / 256; ++i) {
+        const float ss = dpp_group_sum<RPC>(piece_sumsq(v[i], T()));
+        const float rn = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
+        dst[threadIdx.x + i * 256] = piece_scale(v[i], rn, T());
+    }
+}
+
 template <typename T, int N, int S>
 __global__ __launch_bounds__(kThreads) void k_sma(
     const T* __restrict__ q, const T* __restrict__ e, const T* __restrict__ Cm,
-    const T* __restrict__ mem, const T* __restrict__ z, const T* y_ssd, T* y,
+    const T* __restrict__ mem, const T* __restrict__ kmem, const T* __restrict__ z,
+    const T* y_ssd, T* y,
     float* __restrict__ lse, const float* __restrict__ qw, const float* __restrict__ ew, float eps,
-    int normalize, int z_per_head, int64_t L, int H, int G, int64_t Mcap, int nblk, int hpb,
-    int64_t BHC) {
+    int normalize, int z_per_head, int64_t L, int H, int G, int64_t Mcap, int64_t Mp, int nblk,
+    int hpb, int64_t BHC) {
     constexpr int KS = N / 32;
     constexpr int RT = sma_rt<T>();
     constexpr int PT = 16 * RT;                  // tokens per pair
@@ -156,66 +187,33 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     const int ip = (int)(pbase / S);                         // the pair's chunk
     const int nj = active ? ip : 0;                          // memories the pair attends
 
-    // LDS: two key tiles and two value tiles (swizzled [N][P]), the softmax
-    // weights (and rescale factors) of the last scored memory per pair, and
-    // the final denominators (by head parity).
-    __shared__ __attribute__((aligned(16))) char kts[2 * MEMB];
-    __shared__ __attribute__((aligned(16))) char vts[2 * MEMB];
+    // LDS: the streamed tiles (see below), the softmax weights (and rescale
+    // factors) of the last scored memory per pair, and the final
+    // denominators (by head parity).
+    constexpr bool kDma = 8 * MEMB + 8192 <= 160 * 1024;  // four (key, value) stages fit
+    __shared__ __attribute__((aligned(16))) char st0[2 * MEMB];
+    __shared__ __attribute__((aligned(16))) char st1[2 * MEMB];
+    __shared__ __attribute__((aligned(16))) char st2[kDma ? 2 * MEMB : 16];
+    __shared__ __attribute__((aligned(16))) char st3[kDma ? 2 * MEMB : 16];
     __shared__ float xw[2][4][PT];
     __shared__ float xa[2][4][PT];
     __shared__ int xr[2][4];
     __shared__ float xd[2][4][PT];
 
     // ---- streaming helpers ---------------------------------------------------
-    // Memory j of head h starts at a wave-uniform address; each lane adds a
-    // fixed 32-bit byte offset (kept in its own register so every load is a
-    // scalar base plus a lane offset).
-    const char* mbase0 = reinterpret_cast<const char*>(mem) + (b * Mcap * H + h0) * (int64_t)MEMB;
-    const int64_t jstride = (int64_t)H * MEMB;
-    const bool copier = PIECES >= kThreads || tid < PIECES;
-    struct Regs { uint4 p[PPT]; };
-    uint32_t loff[PPT];
-#pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-        loff[i] = (uint32_t)(tid + i * kThreads) * 16u;
-        asm volatile("" : "+v"(loff[i]));
-    }
     // The block streams nmem = hpb * jmax memories: index J is memory
     // J % jmax of head h0 + J / jmax.  Indices past the last re-read the last
-    // one, so loads are issued on every path and the compiler waits only for
-    // the register set being written.
+    // one, so copies are issued on every path and the per-wave count of
+    // copies in flight is the same at every wait.  A stage holds the key tile
+    // (bytes [0, MEMB)) and the value tile (bytes [MEMB, 2 MEMB)).
     const int nmem = hpb * jmax;
-    auto load_regs = [&](int J) {
-        Regs r;
+    const char* kbase0 = reinterpret_cast<const char*>(kmem) + (b * Mp * H + h0) * (int64_t)MEMB;
+    const char* vbase0 = reinterpret_cast<const char*>(mem) + (b * Mcap * H + h0) * (int64_t)MEMB;
+    const int64_t jstride = (int64_t)H * MEMB;
+    auto mem_off = [&](int J) {
         const int jj = J < nmem ? J : nmem - 1;
         const int hh = jj / jmax;
-        const char* src = mbase0 + (int64_t)hh * MEMB + (int64_t)(jj - hh * jmax) * jstride;
-#pragma unroll
-        for (int i = 0; i < PPT; ++i) {
-            if (copier) r.p[i] = *reinterpret_cast<const uint4*>(src + loff[i]);
-        }
-        return r;
-    };
-    // key tile: the RPC lanes holding one row reduce its sum of squares to
-    // r_j[n] and write the pieces times r_j[n]
-    auto store_key = [&](const Regs& r, char* kt) {
-        if (!copier) return;
-#pragma unroll
-        for (int i = 0; i < PPT; ++i) {
-            const int pc = tid + i * kThreads;
-            const int row = pc / RPC, c = pc % RPC;
-            const float ss = dpp_group_sum<RPC>(piece_sumsq(r.p[i], T()));
-            const float rn = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
-            *reinterpret_cast<uint4*>(kt + Tl::off(row, c * 16)) = piece_scale(r.p[i], rn, T());
-        }
-    };
-    auto store_value = [&](const Regs& r, char* vt) {
-        if (!copier) return;
-#pragma unroll
-        for (int i = 0; i < PPT; ++i) {
-            const int pc = tid + i * kThreads;
-            *reinterpret_cast<uint4*>(vt + Tl::off(pc / RPC, (pc % RPC) * 16)) = r.p[i];
-        }
+        return (int64_t)hh * MEMB + (int64_t)(jj - hh * jmax) * jstride;
     };
     // operand fragments of one 16-column slice (P index pt) of a tile
     auto read_slice = [&](const char* tile, int pt, Frag<T> (&f)[KS]) {
@@ -224,28 +222,129 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             f[ks] = frag_km<T, RB>(tile, ks * 32 + 4 * grp, ks * 32 + 16 + 4 * grp, pt * 16, lane);
     };
 
-    // The step loop, shared by both kinds of wave, runs steps s = 0..nmem:
-    // step s scores memory s and accumulates the values of memory s-1, then
-    // writes key tile s+1 and value tile s and loads memory s+2.  Register set
-    // s%2 holds memory s once its key tile is written (memories 0 and 1 are
-    // loaded before the token operands, so their latency overlaps the
-    // prologue).  Every wave executes the same barriers.
-    auto stream = [&](Regs& r0, Regs& r1, auto&& work) {
-        store_key(r0, kts);
+    // DMA streaming: step s scores memory s from stage s%4 and accumulates the
+    // values of memory s-1 from stage (s-1)%4, while memory s+2 is copied into
+    // stage (s+2)%4 (last read in step s-1).  The copies are issued untracked
+    // (the compiler would otherwise drain them before every LDS read), and
+    // each wave waits for its own copies of memory s+1 before the barrier:
+    // vector-memory operations complete in order, so allowing the latest
+    // dcnt operations to be outstanding leaves every older copy complete.
+    constexpr int NI = MEMB / 1024;                              // wave copies per tile
+    const int dcnt = 2 * (NI >= kWaves ? NI / kWaves : (wave < NI ? 1 : 0));  // per memory
+    auto fetch = [&](int J, char* st) __attribute__((always_inline)) {
+        const int64_t off = mem_off(J);
+        dma_tile<RB, true>(st, kbase0 + off, RB, N, N, wave, kWaves, lane);
+        dma_tile<RB, true>(st + MEMB, vbase0 + off, RB, N, N, wave, kWaves, lane);
+    };
+    auto wait_older = [&]() __attribute__((always_inline)) {
+        if (dcnt >= 8) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));
+        } else if (dcnt >= 4) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(4));
+        } else if (dcnt >= 2) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(2));
+        }
+    };
+    static_assert(NI < kWaves || (NI % kWaves == 0 && 2 * NI / kWaves <= 8 &&
+                                  (2 * NI / kWaves) % 2 == 0 && (2 * NI / kWaves) != 6),
+                  "per-wave copy count must be 2, 4 or 8");
+    auto stream_dma = [&](auto&& work) {
+        wait_older();
+        lds_barrier();
+        for (int s = 0;; s += 4) {
+            fetch(s + 2, st2);
+            work(s, st0, st3 + MEMB, 0);
+            wait_older();
+            lds_barrier();
+            if (s + 1 > nmem) break;
+            fetch(s + 3, st3);
+            work(s + 1, st1, st0 + MEMB, 1);
+            wait_older();
+            lds_barrier();
+            if (s + 2 > nmem) break;
+            fetch(s + 4, st0);
+            work(s + 2, st2, st1 + MEMB, 0);
+            wait_older();
+            lds_barrier();
+            if (s + 3 > nmem) break;
+            fetch(s + 5, st1);
+            work(s + 3, st3, st2 + MEMB, 1);
+            wait_older();
+            lds_barrier();
+            if (s + 4 > nmem) break;
+        }
+    };
+
+    // Register streaming (two stages): memory s+1 is loaded into registers
+    // during step s-1 and written to stage (s+1)%2 after step s's work.  Its
+    // key tile is needed in step s+1 and its value tile in step s+2, so the
+    // value copy of memory s is written one step later than its key copy.
+    const bool copier = PIECES >= kThreads || tid < PIECES;
+    struct Regs { uint4 k[PPT], v[PPT]; };
+    uint32_t loff[PPT];
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+        loff[i] = (uint32_t)(tid + i * kThreads) * 16u;
+        // each offset in its own register: every load is a scalar base plus a
+        // lane offset
+        asm volatile("" : "+v"(loff[i]));
+    }
+    auto load_regs = [&](int J) {
+        Regs r;
+        const int64_t off = mem_off(J);
+#pragma unroll
+        for (int i = 0; i < PPT; ++i) {
+            if (copier) {
+                r.k[i] = *reinterpret_cast<const uint4*>(kbase0 + off + loff[i]);
+                r.v[i] = *reinterpret_cast<const uint4*>(vbase0 + off + loff[i]);
+            }
+        }
+        return r;
+    };
+    auto put = [&](const uint4 (&src)[PPT], char* tile) {
+        if (!copier) return;
+#pragma unroll
+        for (int i = 0; i < PPT; ++i) {
+            const int pc = tid + i * kThreads;
+            *reinterpret_cast<uint4*>(tile + Tl::off(pc / RPC, (pc % RPC) * 16)) = src[i];
+        }
+    };
+    Regs r0, r1;
+    auto stream_regs = [&](auto&& work) {
+        put(r0.k, st0);
         lds_barrier();
         for (int s = 0;; s += 2) {
-            work(s, kts, vts + MEMB, 0);
-            store_value(r0, vts);
-            store_key(r1, kts + MEMB);
+            work(s, st0, st1 + MEMB, 0);
+            put(r0.v, st0 + MEMB);
+            put(r1.k, st1);
             r0 = load_regs(s + 2);
             lds_barrier();
             if (s + 1 > nmem) break;
-            work(s + 1, kts + MEMB, vts, 1);
-            store_value(r1, vts + MEMB);
-            store_key(r0, kts);
+            work(s + 1, st1, st0 + MEMB, 1);
+            put(r1.v, st1 + MEMB);
+            put(r0.k, st0);
             r1 = load_regs(s + 3);
             lds_barrier();
             if (s + 2 > nmem) break;
+        }
+    };
+    // The first two memories are requested before the token operands, so
+    // their latency overlaps the prologue.
+    if (nmem > 0) {
+        if constexpr (kDma) {
+            fetch(0, st0);
+            fetch(1, st1);
+        } else {
+            r0 = load_regs(0);
+            r1 = load_regs(1);
+        }
+    }
+    // Both kinds of wave run steps s = 0..nmem and execute the same barriers.
+    auto stream = [&](auto&& work) {
+        if constexpr (kDma) {
+            stream_dma(work);
+        } else {
+            stream_regs(work);
         }
     };
 
@@ -259,11 +358,6 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         const int64_t t = pbase + rt * 16 + col;
         tvalid[rt] = t < L;
         trow[rt] = b * L + (t < L ? t : L - 1);
-    }
-    Regs r0, r1;
-    if (nmem > 0) {
-        r0 = load_regs(0);
-        r1 = load_regs(1);
     }
     const bool hist = ip >= 1;
 
@@ -355,7 +449,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
             return;
         }
-        stream(r0, r1, [&](int s, const char* kt, const char*, int buf) {
+        stream([&](int s, const char* kt, const char*, int buf) {
             if (s >= nmem) return;
             const int hh = s / jmax, j = s - hh * jmax;
             if (j == 0) {
@@ -366,35 +460,33 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 }
             }
             if (j < nj) {
-                // U^T slices: fragments of slice pt+1 are read before the MFMAs of
-                // slice pt (scheduling fences keep that order)
+                // U^T slices: fragments of slice pt+1 are requested before the
+                // MFMAs of slice pt
                 Frag<T> fb[2][KS];
                 read_slice(kt, 0, fb[0]);
                 float lp[RT];
-    #pragma unroll
+#pragma unroll
                 for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
-    #pragma unroll
+#pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
                     if (pt < 3) read_slice(kt, pt + 1, fb[(pt + 1) & 1]);
-                    __builtin_amdgcn_sched_barrier(0);
-                    f32x4 u[RT];
-    #pragma unroll
+                        f32x4 u[RT];
+#pragma unroll
                     for (int rt = 0; rt < RT; ++rt) u[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    #pragma unroll
+#pragma unroll
                     for (int ks = 0; ks < KS; ++ks)
-    #pragma unroll
+#pragma unroll
                         for (int rt = 0; rt < RT; ++rt) u[rt] = mma16(u[rt], fb[pt & 1][ks], qf[rt][ks]);
-    #pragma unroll
+#pragma unroll
                     for (int rt = 0; rt < RT; ++rt)
-    #pragma unroll
+#pragma unroll
                         for (int i = 0; i < 4; ++i) lp[rt] += u[rt][i] * ef[rt][pt][i];
-                    __builtin_amdgcn_sched_barrier(0);
-                }
+                    }
                 // full logit of the lane's token: sum the 4 lanes sharing its
                 // column with one fp32 MFMA against a ones matrix
                 // (D[i][t] = sum_k B[k][t])
                 bool grow = false;
-    #pragma unroll
+#pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
                     const f32x4 red = __builtin_amdgcn_mfma_f32_16x16x4f32(
                         1.0f, lp[rt], f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
@@ -407,7 +499,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 // the choice of m
                 const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
                 if (rescale) {
-    #pragma unroll
+#pragma unroll
                     for (int rt = 0; rt < RT; ++rt) {
                         const float mn = fmaxf(m[rt], lp[rt]);
                         const float al = fast_exp2(m[rt] - mn);
@@ -416,7 +508,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                         if (grp == 0) xa[buf][pair][rt * 16 + col] = al;
                     }
                 }
-    #pragma unroll
+#pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
                     const float pw = fast_exp2(lp[rt] - m[rt]);
                     d[rt] += pw;
@@ -478,7 +570,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
             return;
         }
-        stream(r0, r1, [&](int s, const char*, const char* vt, int buf) {
+        stream([&](int s, const char*, const char* vt, int buf) {
             // memory s-1, scored in the previous step (weights in slot buf^1)
             if (s < 1) return;
             const int hh = (s - 1) / jmax, j = (s - 1) - hh * jmax;
@@ -490,34 +582,35 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             }
             if (j < nj) {
                 const int wb = buf ^ 1;
+                // flag and weights first: LDS reads return in order, so the
+                // flag test does not wait for the fragment reads
+                const int rescale = __builtin_amdgcn_readfirstlane(xr[wb][pair]);
+                float pw[RT];
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) pw[rt] = xw[wb][pair][rt * 16 + col];
                 Frag<T> fb[2][KS];
                 read_slice(vt, 0, fb[0]);
-                float pw[RT];
-    #pragma unroll
-                for (int rt = 0; rt < RT; ++rt) pw[rt] = xw[wb][pair][rt * 16 + col];
-                if (__builtin_amdgcn_readfirstlane(xr[wb][pair])) {
-    #pragma unroll
+                if (rescale) {
+#pragma unroll
                     for (int rt = 0; rt < RT; ++rt) {
                         const float al = xa[wb][pair][rt * 16 + col];
-    #pragma unroll
+#pragma unroll
                         for (int pt = 0; pt < 4; ++pt) o[rt][pt] *= al;
                     }
                 }
-    #pragma unroll
+#pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
                     if (pt < 3) read_slice(vt, pt + 1, fb[(pt + 1) & 1]);
-                    __builtin_amdgcn_sched_barrier(0);
-                    f32x4 v[RT];
-    #pragma unroll
+                        f32x4 v[RT];
+#pragma unroll
                     for (int rt = 0; rt < RT; ++rt) v[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    #pragma unroll
+#pragma unroll
                     for (int ks = 0; ks < KS; ++ks)
-    #pragma unroll
+#pragma unroll
                         for (int rt = 0; rt < RT; ++rt) v[rt] = mma16(v[rt], fb[pt & 1][ks], cf[rt][ks]);
-    #pragma unroll
+#pragma unroll
                     for (int rt = 0; rt < RT; ++rt) o[rt][pt] += pw[rt] * v[rt];
-                    __builtin_amdgcn_sched_barrier(0);
-                }
+                    }
             }
             // the head's last memory is in: its denominators were published
             // in the previous step
@@ -529,7 +622,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
 template <typename T, int N, int S>
 hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e, const void* Cm,
                    const void* mem, const void* z, const void* y_ssd, void* y, float* lse,
-                   hipStream_t st) {
+                   void* ws, hipStream_t st) {
     constexpr int TPB = sma_tokens_per_block<T>();
     const int nblk = (int)((s.L + TPB - 1) / TPB);
     // heads per block: up to kHeadsPerBlock heads of one group
@@ -542,10 +635,19 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
         }
     }
     const int64_t BHC = s.B * (s.H / hpb);
+    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;  // memories any token attends to
+    T* kmem = reinterpret_cast<T*>(ws);
+    if (Mp > 0) {
+        prof_begin("k_sma_keys", st);
+        k_sma_keys<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
+            (const T*)mem, kmem, a.eps, a.normalize, s.H, Mp, s.Mcap);
+        prof_end(st);
+    }
     prof_begin("k_sma", st);
     k_sma<T, N, S><<<dim3((unsigned)(BHC * nblk)), kThreads, 0, st>>>(
-        (const T*)q, (const T*)e, (const T*)Cm, (const T*)mem, (const T*)z, (const T*)y_ssd, (T*)y,
-        lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H, s.G, s.Mcap, nblk, hpb, BHC);
+        (const T*)q, (const T*)e, (const T*)Cm, (const T*)mem, kmem, (const T*)z, (const T*)y_ssd,
+        (T*)y, lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H, s.G, s.Mcap, Mp, nblk,
+        hpb, BHC);
     prof_end(st);
     return hipGetLastError();
 }
@@ -553,11 +655,11 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
 template <typename T, int N>
 hipError_t run_sma_s(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                      const void* Cm, const void* mem, const void* z, const void* ys, void* y,
-                     float* lse, hipStream_t st) {
+                     float* lse, void* ws, hipStream_t st) {
     switch (s.S) {
-        case 64: return run_sma<T, N, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
-        case 128: return run_sma<T, N, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
-        case 256: return run_sma<T, N, 256>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
+        case 64: return run_sma<T, N, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
+        case 128: return run_sma<T, N, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
+        case 256: return run_sma<T, N, 256>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
     }
     return hipErrorInvalidValue;
 }
@@ -565,24 +667,27 @@ hipError_t run_sma_s(const Shape& s, const SmaArgs& a, const void* q, const void
 template <typename T>
 hipError_t run_sma_n(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                      const void* Cm, const void* mem, const void* z, const void* ys, void* y,
-                     float* lse, hipStream_t st) {
+                     float* lse, void* ws, hipStream_t st) {
     switch (s.N) {
-        case 32: return run_sma_s<T, 32>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
-        case 64: return run_sma_s<T, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
-        case 128: return run_sma_s<T, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, st);
+        case 32: return run_sma_s<T, 32>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
+        case 64: return run_sma_s<T, 64>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
+        case 128: return run_sma_s<T, 128>(s, a, q, e, Cm, mem, z, ys, y, lse, ws, st);
     }
     return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-size_t sma_workspace_bytes(const Shape&) { return 0; }
+size_t sma_workspace_bytes(const Shape& s) {
+    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
+    return elem_bytes(s.dtype) * s.B * Mp * s.H * (size_t)s.N * s.P;
+}
 
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
-                      float* lse, void*, hipStream_t st) {
-    if (s.dtype == 1) return run_sma_n<bf16>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, st);
-    return run_sma_n<float>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, st);
+                      float* lse, void* ws, hipStream_t st) {
+    if (s.dtype == 1) return run_sma_n<bf16>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, ws, st);
+    return run_sma_n<float>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, ws, st);
 }
 
 }  // namespace dart

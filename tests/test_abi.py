@@ -63,10 +63,15 @@ def test_workspace_sizes(lib):
     d = dims()
     M = 512 // 64
     ws = lib.dart_scan_workspace_bytes(ctypes.byref(d))
-    # chunk log-decays (float) + chunk-entry states (storage dtype)
-    assert ws >= 4 * 2 * 4 * M + 2 * 2 * M * 4 * 64 * 64
-    # the SMA forward streams the memories from the cache as stored
-    assert lib.dart_sma_workspace_bytes(ctypes.byref(d)) == 0
+    # chunk log-decays, chunk-entry states (storage dtype), within-chunk log
+    # decays and the causal Gram tiles (float; one set per group)
+    pairs = (64 // 32) * (64 // 32 + 1)
+    assert ws >= 4 * 2 * 4 * M + 2 * 2 * M * 4 * 64 * 64 + 4 * 2 * 4 * M * 64 + 4 * 2 * 1 * M * pairs * 512
+    # the SMA forward keeps the key side r (.) dH of every attended memory
+    sma = lib.dart_sma_workspace_bytes(ctypes.byref(d))
+    assert sma >= 2 * 2 * (M - 1) * 4 * 64 * 64
+    d1 = dims(seqlen=64)  # one chunk: no memory is ever attended
+    assert lib.dart_sma_workspace_bytes(ctypes.byref(d1)) == 0
     dd = dims(seqlen=0, mem_capacity=40)
     # at least one partial (O[64], m, d) per (b, h) plus the SSM readout y_ssd
     assert lib.dart_decode_workspace_bytes(ctypes.byref(dd)) >= 4 * 2 * 4 * (66 + 64)
