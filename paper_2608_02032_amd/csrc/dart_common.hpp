@@ -168,8 +168,8 @@ __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt(0); }
 // flight from the tiles being read and would otherwise drain every copy
 // before each LDS read.  M0 (the LDS base) is saved and restored.
 __device__ __forceinline__ void lds_dma16_untracked(const void* gsrc, void* lds_wave_base) {
-    const uint32_t m0 = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_wave_base);
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_wave_base);
     uint32_t save;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"

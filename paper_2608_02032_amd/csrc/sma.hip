@@ -129,6 +129,64 @@ __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* 
     }
 }
 
+// Copy of one swizzled [N][P] tile (MEMB bytes) from global memory into LDS by
+// DMA, issued from inline assembly with a scalar tile base and per-lane byte
+// offsets fixed at set-up, so the streaming loop does no vector address work.
+// Wave w copies the 1 KiB pieces w, w + 8, ... (or piece w alone when a tile
+// has fewer than 8); lane i of a piece lands at piece base + 16 i, which holds
+// global chunk (pos ^ (row & 7)) of its row (the tile swizzle is an XOR, its
+// own inverse).  Completion is tracked by the wave's vmcnt.
+template <int RB, int MEMB>
+struct TileDma {
+    static constexpr int CPR = RB / 16;
+    static constexpr int MASK = (CPR < 8 ? CPR : 8) - 1;
+    static constexpr int NI = MEMB / 1024;                      // pieces per tile
+    static constexpr int KPW = NI >= kWaves ? NI / kWaves : 1;  // pieces per wave
+    static_assert(NI >= kWaves ? NI % kWaves == 0 : true, "pieces must tile the waves");
+    uint32_t goff[KPW];
+    bool active;
+    int wave;
+    __device__ void init(int w, int lane) {
+        wave = __builtin_amdgcn_readfirstlane(w);
+        active = NI >= kWaves || w < NI;
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const int q = (w + k * kWaves) * 64 + lane;
+            const int row = q / CPR, pos = q % CPR;
+            goff[k] = (uint32_t)(row * RB + ((pos ^ (row & MASK)) << 4));
+            asm volatile("" : "+v"(goff[k]));
+        }
+    }
+    // copies issued by this wave per tile
+    __device__ int count() const { return active ? KPW : 0; }
+    __device__ __forceinline__ void issue(const char* gtile, char* ltile) const {
+        if (!active) return;
+        // readfirstlane returns a signed int: widen through uint32_t so the low
+        // half is zero-extended
+        const uint64_t gb = (uint64_t)(uintptr_t)gtile;
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(gb >> 32));
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)gb);
+        const uint64_t base = ((uint64_t)hi << 32) | (uint64_t)lo;
+        const uint32_t l0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+            (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)ltile);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const uint32_t m0 =
+                (uint32_t)__builtin_amdgcn_readfirstlane((int)(l0 + (uint32_t)((wave + k * kWaves) * 1024)));
+            uint32_t save;
+            asm volatile(
+                "s_mov_b32 %0, m0\n\t"
+                "s_mov_b32 m0, %3\n\t"
+                "s_nop 0\n\t"
+                "global_load_lds_dwordx4 %1, %2\n\t"
+                "s_mov_b32 m0, %0"
+                : "=&s"(save)
+                : "v"(goff[k]), "s"(base), "s"(m0)
+                : "memory");
+        }
+    }
+};
+
 template <typename T, int N, int S>
 __global__ __launch_bounds__(kThreads) void k_sma(
     const T* __restrict__ q, const T* __restrict__ e, const T* __restrict__ Cm,
@@ -229,12 +287,13 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     // each wave waits for its own copies of memory s+1 before the barrier:
     // vector-memory operations complete in order, so allowing the latest
     // dcnt operations to be outstanding leaves every older copy complete.
-    constexpr int NI = MEMB / 1024;                              // wave copies per tile
-    const int dcnt = 2 * (NI >= kWaves ? NI / kWaves : (wave < NI ? 1 : 0));  // per memory
+    TileDma<RB, MEMB> tdma;
+    tdma.init(wave, lane);
+    const int dcnt = 2 * tdma.count();  // copies per memory issued by this wave
     auto fetch = [&](int J, char* st) __attribute__((always_inline)) {
         const int64_t off = mem_off(J);
-        dma_tile<RB, true>(st, kbase0 + off, RB, N, N, wave, kWaves, lane);
-        dma_tile<RB, true>(st + MEMB, vbase0 + off, RB, N, N, wave, kWaves, lane);
+        tdma.issue(kbase0 + off, st);
+        tdma.issue(vbase0 + off, st + MEMB);
     };
     auto wait_older = [&]() __attribute__((always_inline)) {
         if (dcnt >= 8) {
@@ -245,8 +304,8 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(2));
         }
     };
-    static_assert(NI < kWaves || (NI % kWaves == 0 && 2 * NI / kWaves <= 8 &&
-                                  (2 * NI / kWaves) % 2 == 0 && (2 * NI / kWaves) != 6),
+    static_assert(2 * TileDma<RB, MEMB>::KPW == 2 || 2 * TileDma<RB, MEMB>::KPW == 4 ||
+                      2 * TileDma<RB, MEMB>::KPW == 8,
                   "per-wave copy count must be 2, 4 or 8");
     auto stream_dma = [&](auto&& work) {
         wait_older();
@@ -340,7 +399,11 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         }
     }
     // Both kinds of wave run steps s = 0..nmem and execute the same barriers.
+    // The prologue's loads are complete on entry (an explicit wait), so the
+    // compiler has no earlier load to wait for inside the loop, where such a
+    // wait would also drain the copies in flight.
     auto stream = [&](auto&& work) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         if constexpr (kDma) {
             stream_dma(work);
         } else {
