@@ -129,6 +129,84 @@ __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* 
     }
 }
 
+// The epilogue inputs of one head, for each of a lane's RT tokens: its gate
+// pre-activation z and its 4 x 4 y_ssd values (columns 16 pt + 4 (lane/16) ..
+// +3).  They are loaded inside one assembly block that also waits for them, so
+// the compiler tracks no load of these registers: loads it tracked here, in
+// the streaming loop, made it drain the tile copies in flight at later
+// register reuses in every step.  Called once per head, where the drain is
+// cheap.
+template <typename T, int RT>
+__device__ __forceinline__ void load_epilogue_inputs(const T* const (&zp)[RT],
+                                                     const T* const (&yp)[RT], float (&zz)[RT],
+                                                     Vec4<T> (&ys)[RT][4]);
+template <>
+__device__ __forceinline__ void load_epilogue_inputs<bf16, 4>(const bf16* const (&zp)[4],
+                                                              const bf16* const (&yp)[4],
+                                                              float (&zz)[4],
+                                                              Vec4<bf16> (&ys)[4][4]) {
+    uint32_t zr[4];
+    uint64_t yr[4][4];
+    asm volatile(
+        "global_load_ushort %0, %20, off\n\t"
+        "global_load_ushort %1, %21, off\n\t"
+        "global_load_ushort %2, %22, off\n\t"
+        "global_load_ushort %3, %23, off\n\t"
+        "global_load_dwordx2 %4, %24, off\n\t"
+        "global_load_dwordx2 %5, %24, off offset:32\n\t"
+        "global_load_dwordx2 %6, %24, off offset:64\n\t"
+        "global_load_dwordx2 %7, %24, off offset:96\n\t"
+        "global_load_dwordx2 %8, %25, off\n\t"
+        "global_load_dwordx2 %9, %25, off offset:32\n\t"
+        "global_load_dwordx2 %10, %25, off offset:64\n\t"
+        "global_load_dwordx2 %11, %25, off offset:96\n\t"
+        "global_load_dwordx2 %12, %26, off\n\t"
+        "global_load_dwordx2 %13, %26, off offset:32\n\t"
+        "global_load_dwordx2 %14, %26, off offset:64\n\t"
+        "global_load_dwordx2 %15, %26, off offset:96\n\t"
+        "global_load_dwordx2 %16, %27, off\n\t"
+        "global_load_dwordx2 %17, %27, off offset:32\n\t"
+        "global_load_dwordx2 %18, %27, off offset:64\n\t"
+        "global_load_dwordx2 %19, %27, off offset:96\n\t"
+        "s_waitcnt vmcnt(0)"
+        : "=&v"(zr[0]), "=&v"(zr[1]), "=&v"(zr[2]), "=&v"(zr[3]),
+          "=&v"(yr[0][0]), "=&v"(yr[0][1]), "=&v"(yr[0][2]), "=&v"(yr[0][3]),
+          "=&v"(yr[1][0]), "=&v"(yr[1][1]), "=&v"(yr[1][2]), "=&v"(yr[1][3]),
+          "=&v"(yr[2][0]), "=&v"(yr[2][1]), "=&v"(yr[2][2]), "=&v"(yr[2][3]),
+          "=&v"(yr[3][0]), "=&v"(yr[3][1]), "=&v"(yr[3][2]), "=&v"(yr[3][3])
+        : "v"(zp[0]), "v"(zp[1]), "v"(zp[2]), "v"(zp[3]), "v"(yp[0]), "v"(yp[1]), "v"(yp[2]),
+          "v"(yp[3])
+        : "memory");
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+        zz[rt] = __builtin_bit_cast(float, zr[rt] << 16);
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) ys[rt][pt] = __builtin_bit_cast(Vec4<bf16>, yr[rt][pt]);
+    }
+}
+template <>
+__device__ __forceinline__ void load_epilogue_inputs<float, 2>(const float* const (&zp)[2],
+                                                               const float* const (&yp)[2],
+                                                               float (&zz)[2],
+                                                               Vec4<float> (&ys)[2][4]) {
+    asm volatile(
+        "global_load_dword %0, %10, off\n\t"
+        "global_load_dword %1, %11, off\n\t"
+        "global_load_dwordx4 %2, %12, off\n\t"
+        "global_load_dwordx4 %3, %12, off offset:64\n\t"
+        "global_load_dwordx4 %4, %12, off offset:128\n\t"
+        "global_load_dwordx4 %5, %12, off offset:192\n\t"
+        "global_load_dwordx4 %6, %13, off\n\t"
+        "global_load_dwordx4 %7, %13, off offset:64\n\t"
+        "global_load_dwordx4 %8, %13, off offset:128\n\t"
+        "global_load_dwordx4 %9, %13, off offset:192\n\t"
+        "s_waitcnt vmcnt(0)"
+        : "=&v"(zz[0]), "=&v"(zz[1]), "=&v"(ys[0][0]), "=&v"(ys[0][1]), "=&v"(ys[0][2]),
+          "=&v"(ys[0][3]), "=&v"(ys[1][0]), "=&v"(ys[1][1]), "=&v"(ys[1][2]), "=&v"(ys[1][3])
+        : "v"(zp[0]), "v"(zp[1]), "v"(yp[0]), "v"(yp[1])
+        : "memory");
+}
+
 // Copy of one swizzled [N][P] tile (MEMB bytes) from global memory into LDS by
 // DMA, issued from inline assembly with a scalar tile base and per-lane byte
 // offsets fixed at set-up, so the streaming loop does no vector address work.
@@ -602,14 +680,16 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         // y = y_ssd + SiLU(z) R of one head
         auto finish_head = [&](int hh) __attribute__((always_inline)) {
             const int h = h0 + hh;
-            float zz[RT];
-            Vec4<T> ys[RT][4];
+            const T* zp[RT];
+            const T* yp[RT];
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                zz[rt] = to_f(z_per_head ? z[trow[rt] * H + h] : z[trow[rt]]);
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt) ys[rt][pt] = ld4(y_ssd + (trow[rt] * H + h) * kP + pt * 16 + grp * 4);
+                zp[rt] = z_per_head ? z + trow[rt] * H + h : z + trow[rt];
+                yp[rt] = y_ssd + (trow[rt] * H + h) * kP + grp * 4;
             }
+            float zz[RT];
+            Vec4<T> ys[RT][4];
+            load_epilogue_inputs<T, RT>(zp, yp, zz, ys);
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
                 if (!tvalid[rt]) continue;
