@@ -4,7 +4,7 @@
 One step = the whole hot path over one batch of seeded synthetic inputs that
 are already resident in HBM:
   forward   chunked SSD scan (k_chunk_state, k_chunk_gram, k_state_pass, k_chunk_out)
-            -> state-memory attention + gated residual (k_sma_keys, k_sma)
+            -> state-memory attention + gated residual (k_sma_prep, k_sma)
             on the L = 8192 workload (batch 4, 32 heads, P = 64, N = 128, S = 256);
   decode    one token (k_decode_partial, k_decode_state_merge) for batch 64, 32 heads,
             N = 128, S = 256 over a 65536-token context (256 cached memories).
@@ -222,7 +222,7 @@ def main():
     mflops, mbytes = sma_flops(w), sma_bytes(w)
     scan_ms = sum(avg.get(k, 0.0) for k in ("k_chunk_state", "k_chunk_gram", "k_state_pass",
                                              "k_chunk_out"))
-    sma_ms = sum(avg.get(k, 0.0) for k in ("k_sma_keys", "k_sma"))
+    sma_ms = sum(avg.get(k, 0.0) for k in ("k_sma_prep", "k_sma_keys", "k_sma"))
     main_ms = avg["k_sma"]
     main_tflops = mflops / (main_ms * 1e-3) / 1e12
     roofline = {"kernel": "k_sma", "bound": "mfma",

@@ -266,7 +266,7 @@ struct TileDma {
 };
 
 template <typename T, int N, int S>
-__global__ __launch_bounds__(kThreads) void k_sma(
+__global__ __launch_bounds__(kThreads) void k_sma_regs(
     const T* __restrict__ q, const T* __restrict__ e, const T* __restrict__ Cm,
     const T* __restrict__ mem, const T* __restrict__ kmem, const T* __restrict__ z,
     const T* y_ssd, T* y,
@@ -762,6 +762,625 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 streaming kernel.
+//
+// Same work split as above (8 waves = 4 (score, value) pairs of 64 tokens, four
+// heads of one group per block, one continuous stream of memories), with the
+// value wave two steps behind the score wave:
+//   step s  score waves  MFMAs of memory s (key tile), and before them the
+//                        softmax tail of memory s-1: the last P-slice of its
+//                        logit sums, the reduction over the four lanes of a
+//                        column (gfx950 row-swap moves), the online-softmax
+//                        update and the weights of s-1 written to LDS;
+//           value waves  memory s-2: V^T = dH^T C^T on MFMA, O = alpha O + w V;
+//                        before the barrier they already read the first
+//                        operand fragments of memory s-1;
+//           all waves    DMA of memory s+2 (key tile into a 3-stage ring,
+//                        value tile into a 5-stage ring).
+// So the softmax tail runs while the score wave's first fragment reads are in
+// flight and the value waves have MFMA work ready when the barrier opens.
+// Operand fragments are read PD fragments ahead of their MFMAs; scheduling
+// barriers keep the compiler from sinking the reads next to their use.
+// ---------------------------------------------------------------------------
+
+// Reduce-scatter over the four lanes l, l^16, l^32, l^48 that hold one column
+// of a 16x16 MFMA accumulator: v0..v3 are the lane's partial sums for column
+// tiles 0..3, and the result in 16-lane row g of the wave is the full sum for
+// tile g.  v_permlane32_swap exchanges lanes 32..63 of its first operand with
+// lanes 0..31 of its second, so after swapping (v0, v2) the sum v0 + v2 holds
+// tile 0 over lanes {l, l^32} in the lower half and tile 2 in the upper half
+// (likewise v1 + v3 for tiles 1 and 3); v_permlane16_swap then exchanges the
+// odd 16-lane rows of its first operand with the even rows of its second, and
+// one more sum completes each row's tile.  Issued from assembly: the builtins
+// return the second operand unchanged in this compiler.
+__device__ __forceinline__ float col_reduce_scatter4(float v0, float v1, float v2, float v3) {
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(v0), "+v"(v2));
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(v1), "+v"(v3));
+    float sa = v0 + v2, sb = v1 + v3;
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(sa), "+v"(sb));
+    return sa + sb;
+}
+
+// s_waitcnt vmcnt(k) for the per-wave copy counts that occur (0, 2, 4 or 8).
+__device__ __forceinline__ void wait_vm(int k) {
+    if (k >= 8) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));
+    } else if (k >= 4) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(4));
+    } else if (k >= 2) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(2));
+    } else {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    }
+}
+
+// Key and value sides of every attended memory for the bf16 kernel, both
+// transposed to [P][N]: kT[p][n] = r[n] dH[n][p] (rounded to bf16) and
+// vT[p][n] = dH[n][p], with r[n] = (mean_p dH[n,p]^2 + eps)^-1/2 reduced from
+// the stored values.  Rows of N consecutive n put the contraction index of
+// both SMA products in consecutive bytes, so k_sma reads every MFMA operand
+// fragment with one 16-byte LDS load.  The tile is staged in LDS in the
+// swizzled row layout; two transposing reads then hand each lane 8
+// consecutive n of one p (one 16-byte piece of an output row).  The RPC lanes
+// holding one source row reduce its sum of squares with DPP moves.
+template <int N>
+__global__ __launch_bounds__(256) void k_sma_prep(const bf16* __restrict__ mem,
+                                                  bf16* __restrict__ kT, bf16* __restrict__ vT,
+                                                  float eps, int normalize, int H, int64_t Mp,
+                                                  int64_t Mcap) {
+    constexpr int RB = kP * 2;            // bytes of one source row (fixed n)
+    constexpr int RPC = RB / 16;          // 16-byte pieces per source row
+    constexpr int PIECES = N * RPC;       // 16-byte pieces of one memory
+    constexpr int NG = N / 32;            // 32-row bands of the output pieces
+    static_assert(PIECES % 256 == 0 || 256 % PIECES == 0, "pieces must tile the block");
+    using Tl = SwzTile<RB>;
+    const int64_t j = blockIdx.x;
+    const int h = blockIdx.y;
+    const int64_t b = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ __attribute__((aligned(16))) char t[N * RB];
+    __shared__ float rs[N];
+    const uint4* src = reinterpret_cast<const uint4*>(mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP);
+    for (int q = tid; q < PIECES; q += 256) {
+        const uint4 v = src[q];
+        const int n = q / RPC, pc = q % RPC;
+        const float ss = dpp_group_sum<RPC>(piece_sumsq(v, bf16()));
+        if (pc == 0) rs[n] = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
+        *reinterpret_cast<uint4*>(t + Tl::off(n, pc * 16)) = v;
+    }
+    __syncthreads();
+    // piece w of the 4 NG pieces per wave: columns p = 16 (w % 4) + (lane % 16),
+    // rows n = 32 (w / 4) + 8 (lane / 16) .. +7
+    const int64_t obase = ((b * Mp + j) * H + h) * (int64_t)N * kP;
+    const int g = lane >> 4, c = lane & 15;
+    for (int w = wave; w < 4 * NG; w += 4) {
+        const int pbase = 16 * (w & 3), nb = 32 * (w >> 2) + 8 * g;
+        const bf16x8 v = frag_kmajor_bf16<RB>(t, nb, nb + 4, pbase, lane);
+        bf16x8 k;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) k[i] = (bf16)((float)v[i] * rs[nb + i]);
+        const int64_t o = obase + (int64_t)(pbase + c) * N + nb;
+        *reinterpret_cast<bf16x8*>(vT + o) = v;
+        *reinterpret_cast<bf16x8*>(kT + o) = k;
+    }
+}
+
+// DMA of one [P][N] bf16 tile (P = 64 rows of RB = 2N bytes) into an LDS tile
+// whose 16-byte chunks are XOR-swizzled by row: chunk c of row p sits at
+// c ^ key(p), key(p) = (p RB / 256) mod (RB / 16).  The 16 lanes of one
+// 16-byte fragment read (rows 16 pt + 0..15, one logical chunk) then cover
+// all 64 banks.  Issued from inline assembly with a scalar tile base and
+// per-lane offsets fixed at set-up, as TileDma.
+template <int N, int NW>
+struct TileDmaPN {
+    static constexpr int RB = 2 * N;
+    static constexpr int CPR = RB / 16;
+    static constexpr int MEMB = kP * RB;
+    static constexpr int NI = MEMB / 1024;                      // 1 KiB pieces per tile
+    static constexpr int KPW = NI >= NW ? NI / NW : 1;  // pieces per issuing wave
+    static_assert(NI >= NW ? NI % NW == 0 : true, "pieces must tile the waves");
+    __host__ __device__ static constexpr int key(int row) { return (row * RB / 256) & (CPR - 1); }
+    uint32_t goff[KPW];
+    bool active;
+    int wave;
+    __device__ void init(int w, int lane) {
+        wave = __builtin_amdgcn_readfirstlane(w);
+        active = w < NW && (NI >= NW || w < NI);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const int q = (w + k * NW) * 64 + lane;
+            const int row = q / CPR, pos = q % CPR;
+            goff[k] = (uint32_t)(row * RB + ((pos ^ key(row)) << 4));
+            asm volatile("" : "+v"(goff[k]));
+        }
+    }
+    __device__ int count() const { return active ? KPW : 0; }
+    __device__ __forceinline__ void issue(const char* gtile, char* ltile) const {
+        if (!active) return;
+        const uint64_t gb = (uint64_t)(uintptr_t)gtile;
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(gb >> 32));
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)gb);
+        const uint64_t base = ((uint64_t)hi << 32) | (uint64_t)lo;
+        const uint32_t l0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+            (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)ltile);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const uint32_t m0 =
+                (uint32_t)__builtin_amdgcn_readfirstlane((int)(l0 + (uint32_t)((wave + k * NW) * 1024)));
+            uint32_t save;
+            asm volatile(
+                "s_mov_b32 %0, m0\n\t"
+                "s_mov_b32 m0, %3\n\t"
+                "s_nop 0\n\t"
+                "global_load_lds_dwordx4 %1, %2\n\t"
+                "s_mov_b32 m0, %0"
+                : "=&s"(save)
+                : "v"(goff[k]), "s"(base), "s"(m0)
+                : "memory");
+        }
+    }
+};
+
+template <int N, int S>
+__global__ __launch_bounds__(kThreads) void k_sma(
+    const bf16* __restrict__ q, const bf16* __restrict__ e, const bf16* __restrict__ Cm,
+    const bf16* __restrict__ vT, const bf16* __restrict__ kT, const bf16* __restrict__ z,
+    const bf16* y_ssd, bf16* y, float* __restrict__ lse, const float* __restrict__ qw,
+    const float* __restrict__ ew, float eps, int normalize, int z_per_head, int64_t L, int H, int G,
+    int64_t Mp, int nblk, int hpb, int64_t BHC) {
+    using T = bf16;
+    constexpr int KS = N / 32;
+    constexpr int RT = 4;                    // 16-token column tiles per pair
+    constexpr int PT = 16 * RT;              // tokens per pair
+    constexpr int TPB = 4 * PT;              // tokens per block
+    constexpr int RB = 2 * N;                // bytes of one [P][N] tile row (fixed p)
+    constexpr int MEMB = kP * RB;            // bytes of one memory
+    constexpr int NF = 4 * KS;               // operand fragments per tile (4 P-slices)
+    constexpr int PD = 3;                    // fragments read ahead
+    constexpr int KST = 3, VST = 5;          // key and value ring stages
+    constexpr int FK = KS > 1 ? 1 : 0;       // group that applies the previous slice
+    static_assert(S >= PT, "a pair's tokens must lie in one chunk");
+    static_assert(NF >= 4, "at least one fragment per slice");
+    using Dma = TileDmaPN<N, 4>;  // the score waves issue all copies
+
+    // block order: as in k_sma_regs (XCD-aware, heaviest token block first)
+    const int64_t bid = blockIdx.x;
+    int blk;
+    int64_t bhc;
+    if (BHC % 8 == 0) {
+        const int64_t slot = bid >> 3;
+        blk = nblk - 1 - (int)(slot % nblk);
+        bhc = (slot / nblk) * 8 + (bid & 7);
+    } else {
+        blk = nblk - 1 - (int)(bid / BHC);
+        bhc = bid % BHC;
+    }
+    const int hgroups = H / hpb;
+    const int64_t b = bhc / hgroups;
+    const int h0 = (int)(bhc % hgroups) * hpb;
+    const int g = (int)((int64_t)h0 * G / H);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const bool scorer = wave < 4;
+    const int pair = wave & 3;
+
+    const int64_t blk0 = (int64_t)blk * TPB;
+    const int64_t pbase = blk0 + pair * PT;
+    const int64_t blk_end = (blk0 + TPB < L) ? blk0 + TPB : L;
+    const int jmax = (int)((blk_end - 1) / S);
+    const bool active = pbase < L;
+    const int ip = (int)(pbase / S);
+    const int nj = active ? ip : 0;
+    const bool hist = ip >= 1;
+    const int nmem = hpb * jmax;
+
+    __shared__ __attribute__((aligned(16))) char kring[KST * MEMB];
+    __shared__ __attribute__((aligned(16))) char vring[VST * MEMB];
+    __shared__ float xw[2][4][PT];
+    __shared__ float xa[2][4][PT];
+    __shared__ int xr[2][4];
+    __shared__ float xd[2][4][PT];
+
+    // ---- memory stream: DMA of whole tiles, each wave its fixed pieces -------
+    const char* kbase0 = reinterpret_cast<const char*>(kT) + (b * Mp * H + h0) * (int64_t)MEMB;
+    const char* vbase0 = reinterpret_cast<const char*>(vT) + (b * Mp * H + h0) * (int64_t)MEMB;
+    const int64_t jstride = (int64_t)H * MEMB;
+    Dma tdma;
+    tdma.init(wave, lane);
+    const int dcnt = 2 * tdma.count();  // copies per memory issued by this wave
+    int fh = 0, fj = 0;                 // next memory to copy (head, index)
+    auto fetch_next = [&](int kst, int vst) __attribute__((always_inline)) {
+        const int64_t off = (int64_t)fh * MEMB + (int64_t)fj * jstride;
+        tdma.issue(kbase0 + off, kring + kst * MEMB);
+        tdma.issue(vbase0 + off, vring + vst * MEMB);
+        if (++fj == jmax) {
+            fj = 0;
+            ++fh;
+        }
+    };
+    if (nmem > 0) fetch_next(0, 0);
+    if (nmem > 1) fetch_next(1, 1);
+
+    // Operand fragment (slice pt, k step ks) of a [P][N] tile: lane (grp, col)
+    // takes row p = 16 pt + col, n = 32 ks + 8 grp .. +7, one 16-byte read.
+    // Its byte offset is 16 pt RB + koff[ks], koff[ks] = col RB + (chunk ^ key) 16
+    // with chunk 4 ks + grp (key(16 pt + col) does not depend on pt).
+    uint32_t koff[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+        koff[ks] = (uint32_t)(col * RB + (((4 * ks + grp) ^ Dma::key(col)) << 4));
+    auto frag = [&](const char* tile, int f) __attribute__((always_inline)) {
+        return *reinterpret_cast<const bf16x8*>(tile + (f / KS) * 16 * RB + koff[f % KS]);
+    };
+
+    // token rows of the pair; rows past the end re-read the last token
+    int64_t trow[RT];
+    bool tvalid[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        const int64_t t = pbase + rt * 16 + col;
+        tvalid[rt] = t < L;
+        trow[rt] = b * L + (t < L ? t : L - 1);
+    }
+
+    // One P-slice pt of a tile product: for each k step, the operand fragment
+    // PD ahead is requested, then four MFMAs (one per 16-token column tile)
+    // accumulate into acc; fma(rt) (four VALU ops on the previous slice's
+    // results) is applied for the column tiles assigned to the k step.  The
+    // scheduling groups interleave the MFMAs with that VALU work.  The VALU
+    // work starts at the second k step, so the MFMAs that produced its inputs
+    // were issued at least seven MFMAs earlier and have completed.
+    auto fma_lo = [](int ks) { return KS == 1 ? 0 : KS == 2 ? (ks == 1 ? 0 : RT) : ks == 1 ? 0 : ks == 2 ? RT / 2 : RT; };
+    auto fma_hi = [](int ks) { return KS == 1 ? RT : KS == 2 ? (ks == 1 ? RT : 0) : ks == 1 ? RT / 2 : ks == 2 ? RT : 0; };
+    auto slice_region = [&](Frag<T> (&fr)[4], const char* tile, int pt, f32x4 (&acc)[RT],
+                            const Frag<T> (&bop)[RT][KS], auto&& fma) __attribute__((always_inline)) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (KS > 1 && ks == 1) __builtin_amdgcn_sched_barrier(0);
+            const int f = pt * KS + ks;
+            if (f + PD < NF) fr[(f + PD) & 3] = frag(tile, f + PD);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+                acc[rt] = mma16(ks == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[rt], fr[f & 3], bop[rt][ks]);
+#pragma unroll
+            for (int r = fma_lo(ks); r < fma_hi(ks); ++r) fma(r);
+        }
+        // interleave pattern of the region that holds the VALU work
+        if constexpr (KS == 1) {
+#pragma unroll
+            for (int m = 0; m < RT; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+            }
+        } else {
+#pragma unroll
+            for (int ks = 1; ks < KS; ++ks) {
+                if (pt * KS + ks + PD < NF) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+                for (int m = 0; m < RT; ++m) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    if (KS == 2) {
+                        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+                    } else if (ks <= 2) {
+                        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                    }
+                }
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // One step of the stream for every wave: copy memory s+2, the wave's work,
+    // wait for this wave's copies of memory s+1, barrier.  Score waves (they
+    // write the softmax weights to LDS) make their LDS writes complete before
+    // the barrier; value waves write no LDS and cross it with their reads of
+    // the next step's first fragments still in flight (a compiler-level
+    // barrier keeps every LDS access on its side of it).
+    auto run_stream = [&](auto&& work) __attribute__((always_inline)) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // prologue loads and memories 0, 1
+        lds_barrier();
+        int kc = 0, vc = 0;                        // s % KST, s % VST
+        for (int s = 0; s < nmem + 2; ++s) {
+            const bool copy = s + 2 < nmem;
+            if (copy) fetch_next(kc == 0 ? 2 : kc - 1, vc >= 3 ? vc - 3 : vc + 2);
+            work(s, kc, vc);
+            if (copy) {
+                wait_vm(dcnt);
+            } else {
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+            }
+            if (scorer) {
+                lds_barrier();
+            } else {
+                asm volatile("s_barrier" ::: "memory");
+            }
+            kc = kc == KST - 1 ? 0 : kc + 1;
+            vc = vc == VST - 1 ? 0 : vc + 1;
+        }
+    };
+
+    if (scorer) {
+        // ---- score wave: Qbar and Ebar of the pair's tokens -------------------
+        Frag<T> qraw[RT][KS];
+        Vec4<T> eraw[RT][4];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const T* qrow = q + (trow[rt] * G + g) * N;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) qraw[rt][ks] = load_frag(qrow + ks * 32 + 8 * grp);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) eraw[rt][pt] = ld4(e + (trow[rt] * G + g) * kP + pt * 16 + grp * 4);
+        }
+        Frag<T> qf[RT][KS];
+        float ef[RT][4][4];
+        const float qscale = kLog2e / sqrtf((float)N);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const float vmask = tvalid[rt] ? 1.0f : 0.0f;
+            float qv[KS][8];
+            float ss = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) qv[ks][i] = to_f(qraw[rt][ks][i]) * vmask;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) ss += qv[ks][i] * qv[ks][i];
+            }
+            ss += shfl_xor(ss, 16);
+            ss += shfl_xor(ss, 32);
+            const float qinv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) * qscale;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) qv[ks][i] *= qinv;
+                if (qw) {
+                    float w[8];
+                    load8(qw + ks * 32 + 8 * grp, w);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) qv[ks][i] *= w[i];
+                }
+                qf[rt][ks] = make_frag<T>(qv[ks]);
+            }
+            float es = 0.f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    ef[rt][pt][i] = to_f(eraw[rt][pt][i]) * vmask;
+                    es += ef[rt][pt][i] * ef[rt][pt][i];
+                }
+            }
+            es += shfl_xor(es, 16);
+            es += shfl_xor(es, 32);
+            const float einv = normalize ? 1.0f / sqrtf(es * (1.0f / kP) + eps) : 1.0f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= einv;
+                if (ew) {
+                    float w[4];
+                    load4(ew + pt * 16 + grp * 4, w);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) ef[rt][pt][i] *= w[i];
+                }
+            }
+        }
+        // After the reduction, lane (grp, col) owns token 16 grp + col of the
+        // pair (column tile grp): its running maximum and denominator.
+        const int64_t t_own = pbase + grp * 16 + col;
+        const bool own_valid = t_own < L;
+        const int64_t own_row = b * L + (own_valid ? t_own : L - 1);
+        float m_own = -INFINITY, d_own = 0.f;
+        // LSE of one head, and its denominators for the value wave
+        auto finish_head = [&](int hh) __attribute__((always_inline)) {
+            xd[hh & 1][pair][lane] = d_own;
+            if (lse && own_valid)
+                lse[own_row * H + h0 + hh] = hist ? (m_own + log2f(d_own)) * kLn2 : -INFINITY;
+        };
+        if (nmem == 0) {
+            for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
+            return;
+        }
+        f32x4 u[2][RT];           // U^T slice accumulators (slice parity)
+        float lp[RT];             // logit partial sums of the memory being scored
+        Frag<T> fr[4];            // fragment ring
+        int jm = 0;               // index within its head of memory s
+        int hm = 0;               // head of memory s
+        bool tail_pending = false;  // memory s-1 was scored by this wave
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) u[1][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // partial logit sums of slice pt (in u[pt & 1]) for column tile rt
+        auto lp_fma = [&](int pt, int rt) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) lp[rt] += u[pt & 1][rt][i] * ef[rt][pt][i];
+        };
+        run_stream([&](int s, int kc, int) __attribute__((always_inline)) {
+            const bool mm = s < nmem && jm < nj;
+            const char* kt = kring + kc * MEMB;
+            // slice 0 of memory s, with the last slice's logit sums of memory s-1
+            if (mm) {
+#pragma unroll
+                for (int f = 0; f < PD; ++f) fr[f] = frag(kt, f);
+                slice_region(fr, kt, 0, u[0], qf, [&](int rt) { lp_fma(3, rt); });
+            } else if (tail_pending) {
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) lp_fma(3, rt);
+            }
+            // ---- softmax tail of memory s-1 --------------------------------------
+            if (tail_pending) {
+                const float l = col_reduce_scatter4(lp[0], lp[1], lp[2], lp[3]);
+                // lazy rescale: the reference maximum moves only when a logit
+                // exceeds it by more than 2^8; R = O/d and LSE = m + log2 d do
+                // not depend on that choice
+                const bool rescale = __builtin_amdgcn_ballot_w64(l > m_own + kRescaleLog2) != 0;
+                const float mn = rescale ? fmaxf(m_own, l) : m_own;
+                const float al = fast_exp2(m_own - mn);
+                const float pw = fast_exp2(l - mn);
+                d_own = d_own * al + pw;
+                m_own = mn;
+                const int slot = (s - 1) & 1;
+                xw[slot][pair][lane] = pw;
+                xa[slot][pair][lane] = al;
+                if (lane == 0) xr[slot][pair] = rescale ? 1 : 0;
+            }
+            // the head of memory s-1 is complete
+            if (s >= 1 && s <= nmem && jm == 0) {
+                finish_head(hm - 1);
+                m_own = -INFINITY;
+                d_own = 0.f;
+            }
+            tail_pending = mm;
+            if (mm) {
+                // ---- U^T = (r (.) dH_s)^T Qbar^T, slices 1..3; each slice's
+                // MFMAs are interleaved with the logit sums of the slice before
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
+#pragma unroll
+                for (int pt = 1; pt < 4; ++pt)
+                    slice_region(fr, kt, pt, u[pt & 1], qf, [&](int rt) { lp_fma(pt - 1, rt); });
+            }
+            if (++jm == jmax) {
+                jm = 0;
+                ++hm;
+            }
+        });
+    } else {
+        // ---- value wave: C of the pair's tokens, accumulator O ----------------
+        Frag<T> cf[RT][KS];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const T* crow = Cm + (trow[rt] * G + g) * N;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                cf[rt][ks] = load_frag(crow + ks * 32 + 8 * grp);
+        }
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            if (!tvalid[rt]) {
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) cf[rt][ks] = Frag<T>{};
+            }
+        }
+        f32x4 o[RT][4];
+        // token rows are recomputed here rather than kept live through the
+        // stream (the empty asm keeps the compiler from hoisting them out of it)
+        auto finish_head = [&](int hh) __attribute__((always_inline)) {
+            const int h = h0 + hh;
+            const T* zp[RT];
+            const T* yp[RT];
+            int64_t row[RT];
+            int c = col;
+            asm volatile("" : "+v"(c));
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const int64_t t = pbase + rt * 16 + c;
+                row[rt] = b * L + (t < L ? t : L - 1);
+                zp[rt] = z_per_head ? z + row[rt] * H + h : z + row[rt];
+                yp[rt] = y_ssd + (row[rt] * H + h) * kP + grp * 4;
+            }
+            float zz[RT];
+            Vec4<T> ys[RT][4];
+            load_epilogue_inputs<T, RT>(zp, yp, zz, ys);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                if (pbase + rt * 16 + col >= L) continue;
+                const float gate = silu(zz[rt]);
+                const float invd = hist ? 1.0f / xd[hh & 1][pair][rt * 16 + col] : 0.f;
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) {
+                    float yv[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[rt][pt][i]);
+                    if (hist) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) yv[i] += gate * (o[rt][pt][i] * invd);
+                    }
+                    store4(y + (row[rt] * H + h) * kP + pt * 16 + grp * 4, yv);
+                }
+            }
+        };
+        if (nmem == 0) {
+            for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
+            return;
+        }
+        Frag<T> fr[4];             // fragment ring; the first PD of the next step's
+                                   // memory are read before the barrier
+        int jv = 0, hv = 0;        // (index, head) of memory s-2
+        f32x4 v[2][RT];            // V^T slice accumulators (slice parity)
+        float pwp[RT];             // weights of the memory whose last slice is pending
+        bool pend = false;         // o[.][3] += pwp v[1] is still to be applied
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            v[1][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            pwp[rt] = 0.f;
+        }
+        // memory J's value tile sits in stage J % VST; at step s, J = s-2 is in
+        // stage (vc + 3) % 5 and the next step's memory s-1 in (vc + 4) % 5
+        run_stream([&](int s, int, int vc) __attribute__((always_inline)) {
+            const int J = s - 2;
+            if (J >= 0) {
+                const bool act = jv < nj;
+                const char* vt = vring + (vc >= 2 ? vc - 2 : vc + 3) * MEMB;
+                if (act) {
+                    const int slot = J & 1;
+                    float pw[RT];
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) pw[rt] = xw[slot][pair][rt * 16 + col];
+                    const int rescale_v = xr[slot][pair];
+                    // slice 0, with the previous memory's last slice (weight 0
+                    // when nothing is pending; v[1] is always finite)
+                    if (!pend) {
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) pwp[rt] = 0.f;
+                    }
+                    slice_region(fr, vt, 0, v[0], cf, [&](int rt) { o[rt][3] += pwp[rt] * v[1][rt]; });
+                    // start of a head, or the running maximum moved: O (which
+                    // already holds every earlier memory) is reset or rescaled
+                    if (jv == 0) {
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                            for (int pt = 0; pt < 4; ++pt) o[rt][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    } else if (__builtin_amdgcn_readfirstlane(rescale_v)) {
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const float al = xa[slot][pair][rt * 16 + col];
+#pragma unroll
+                            for (int pt = 0; pt < 4; ++pt) o[rt][pt] *= al;
+                        }
+                    }
+#pragma unroll
+                    for (int pt = 1; pt < 4; ++pt)
+                        slice_region(fr, vt, pt, v[pt & 1], cf,
+                                     [&](int rt) { o[rt][pt - 1] += pw[rt] * v[(pt - 1) & 1][rt]; });
+                    // the last slice waits for the next memory of the head, if it
+                    // is attended; otherwise it completes O now
+                    pend = jv + 1 < nj;
+                    if (pend) {
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) pwp[rt] = pw[rt];
+                    } else {
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) o[rt][3] += pw[rt] * v[1][rt];
+                    }
+                }
+                if (jv == jmax - 1) finish_head(hv);
+                if (++jv == jmax) {
+                    jv = 0;
+                    ++hv;
+                }
+            }
+            // first fragments of the next step's memory (s-1), if attended
+            if (s >= 1 && s - 1 < nmem && jv < nj) {
+                const char* vn = vring + (vc >= 1 ? vc - 1 : vc + 4) * MEMB;
+#pragma unroll
+                for (int f = 0; f < PD; ++f) fr[f] = frag(vn, f);
+            }
+        });
+    }
+}
+
 template <typename T, int N, int S>
 hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e, const void* Cm,
                    const void* mem, const void* z, const void* y_ssd, void* y, float* lse,
@@ -780,6 +1399,23 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
     const int64_t BHC = s.B * (s.H / hpb);
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;  // memories any token attends to
     T* kmem = reinterpret_cast<T*>(ws);
+    if constexpr (sizeof(T) == 2) {
+        // bf16: transposed key and value sides ([P][N]) of memories 0..M-2
+        T* vT = kmem + (size_t)s.B * Mp * s.H * N * kP;
+        if (Mp > 0) {
+            prof_begin("k_sma_prep", st);
+            k_sma_prep<N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
+                (const T*)mem, kmem, vT, a.eps, a.normalize, s.H, Mp, s.Mcap);
+            prof_end(st);
+        }
+        prof_begin("k_sma", st);
+        k_sma<N, S><<<dim3((unsigned)(BHC * nblk)), kThreads, 0, st>>>(
+            (const T*)q, (const T*)e, (const T*)Cm, vT, kmem, (const T*)z, (const T*)y_ssd,
+            (T*)y, lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H, s.G, Mp, nblk,
+            hpb, BHC);
+        prof_end(st);
+        return hipGetLastError();
+    }
     if (Mp > 0) {
         prof_begin("k_sma_keys", st);
         k_sma_keys<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
@@ -787,10 +1423,12 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
         prof_end(st);
     }
     prof_begin("k_sma", st);
-    k_sma<T, N, S><<<dim3((unsigned)(BHC * nblk)), kThreads, 0, st>>>(
-        (const T*)q, (const T*)e, (const T*)Cm, (const T*)mem, kmem, (const T*)z, (const T*)y_ssd,
-        (T*)y, lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H, s.G, s.Mcap, Mp, nblk,
-        hpb, BHC);
+    {
+        k_sma_regs<T, N, S><<<dim3((unsigned)(BHC * nblk)), kThreads, 0, st>>>(
+            (const T*)q, (const T*)e, (const T*)Cm, (const T*)mem, kmem, (const T*)z,
+            (const T*)y_ssd, (T*)y, lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H,
+            s.G, s.Mcap, Mp, nblk, hpb, BHC);
+    }
     prof_end(st);
     return hipGetLastError();
 }
@@ -823,7 +1461,8 @@ hipError_t run_sma_n(const Shape& s, const SmaArgs& a, const void* q, const void
 
 size_t sma_workspace_bytes(const Shape& s) {
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
-    return elem_bytes(s.dtype) * s.B * Mp * s.H * (size_t)s.N * s.P;
+    // bf16: key and value sides; fp32: key side only
+    return (s.dtype == 1 ? 2 : 1) * elem_bytes(s.dtype) * s.B * Mp * s.H * (size_t)s.N * s.P;
 }
 
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,

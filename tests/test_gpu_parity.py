@@ -104,6 +104,9 @@ SMA_CASES = [
     synth.Workload("bf16_L700_N64_S64", 1, 700, 2, 64, 64, 64, "bf16"),
     synth.Workload("bf16_L1024_N128_S128", 1, 1024, 2, 64, 128, 128, "bf16"),
     synth.Workload("bf16_L1100_N32_S64_G2", 1, 1100, 4, 64, 32, 64, "bf16", ngroups=2),
+    # many memories per head, two blocks of four heads per token block
+    synth.Workload("bf16_L4096_N128_S256_H8", 1, 4096, 8, 64, 128, 256, "bf16"),
+    synth.Workload("bf16_L2304_N64_S64_H4", 1, 2304, 4, 64, 64, 64, "bf16"),
 ]
 
 
