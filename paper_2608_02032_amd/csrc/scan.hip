@@ -35,7 +35,6 @@ namespace {
 constexpr int kP = 64;        // head dim
 constexpr int kThreads = 256; // 4 waves
 constexpr int kSB = 64;       // tokens per LDS-staged s-block
-constexpr int kPad = 8;       // LDS row padding (elements)
 
 // Inclusive prefix sum over the block (thread order).  All threads call it.
 __device__ float block_inclusive_scan(float v, float* sred) {
@@ -240,17 +239,32 @@ __global__ __launch_bounds__(kThreads) void k_chunk_gram(const T* __restrict__ B
 // ---------------------------------------------------------------------------
 // Chunk output: y_t = sum_{s<=t} G_ts exp(cs_t - cs_s) dt_s x_s
 //                     + exp(cs_t) C_t H_[c-1].
-// Wave w owns the 16-row tiles r = w, w+4, ... (interleaved for balance).
-// H_[c-1] and the chunk's x rows are DMA-staged in natural layout; C rows (for
-// the inter-chunk term) and the Gram tiles go straight to registers.
+// NW waves (8 for S >= 128); wave w owns the 16-row tiles tile_row(w, q): w,
+// then 2 NW - 1 - w, ... (a light and a heavy tile of the causal triangle,
+// so every wave has about the same number of causal pairs).  H_[c-1]
+// and the chunk's x rows are DMA-staged in natural layout; C rows (for the
+// inter-chunk term) and the Gram tiles go straight to registers.
+// The intra-chunk term runs over the causal (row tile r, 32-token s block sk)
+// pairs only.  For sk < r/2 every s precedes every t, and with e = 32 sk + 31
+// the decay factors as exp2(cs_t - cs_e) exp2(cs_e - cs_s), both <= 1: the
+// per-token factor b_s = exp2(cs_e - cs_s) dt_s is formed once per block and
+// each lane's row factor exp2(cs_t - cs_e) once per pair.  The diagonal pair
+// sk = r/2 applies the causal mask and the exact per-element decay.
 // ---------------------------------------------------------------------------
+template <int S> constexpr int out_waves() { return S / 16 >= 8 ? 8 : S / 16; }
+__device__ __forceinline__ int tile_row(int w, int q, int nw) {
+    return (q & 1) ? nw * (q + 1) - 1 - w : nw * q + w;
+}
+
 template <typename T, int N, int S>
-__global__ __launch_bounds__(kThreads) void k_chunk_out(
+__global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
     const T* __restrict__ x, const float* __restrict__ dt, const T* __restrict__ Cm,
     const T* __restrict__ states, const float* __restrict__ cs2, const float* __restrict__ gram,
     T* __restrict__ y, int64_t L, int H, int G, int64_t M, int64_t BM) {
+    constexpr int NW = out_waves<S>();
+    constexpr int NT = 64 * NW;
     constexpr int KS = N / 32;     // 32-deep k steps over the state dim
-    constexpr int NQ = S / 64;     // row tiles per wave
+    constexpr int NQ = S / 16 / NW; // row tiles per wave
     constexpr int XRB = kP * (int)sizeof(T);
     constexpr int XT = S * XRB;    // the chunk's x rows
     constexpr int HT = N * XRB;    // H_[c-1] tile, rows n of P values
@@ -279,127 +293,119 @@ __global__ __launch_bounds__(kThreads) void k_chunk_out(
 
     __shared__ float s_cs[S];  // within-chunk cumulative log decay, log2 units
     __shared__ float s_dt[S];
+    __shared__ float s_b[S];   // exp2(cs_e - cs_s) dt_s, e = end of the s block
     __shared__ __attribute__((aligned(16))) char ht[HT];
     __shared__ __attribute__((aligned(16))) char xs[XT];
-    __shared__ __attribute__((aligned(16))) T so[4][16 * kP];  // per-wave output tile
 
     dma_tile<XRB>(ht, reinterpret_cast<const char*>(states + ((b * M + c) * H + h) * (int64_t)N * kP),
-                  XRB, N, N, wave, 4, lane);
+                  XRB, N, N, wave, NW, lane);
     dma_tile<XRB>(xs, reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP),
-                  (int64_t)H * XRB, S, len, wave, 4, lane);
-    for (int i = tid; i < S; i += kThreads) {
-        s_cs[i] = cs2[((b * H + h) * M + c) * S + i];
-        s_dt[i] = (i < len) ? dt[(b * L + t0 + i) * H + h] : 0.f;
+                  (int64_t)H * XRB, S, len, wave, NW, lane);
+    const float* csc = cs2 + ((b * H + h) * M + c) * S;
+    for (int i = tid; i < S; i += NT) {
+        const float csi = csc[i];
+        const float cse = csc[i | 31];
+        const float dti = (i < len) ? dt[(b * L + t0 + i) * H + h] : 0.f;
+        s_cs[i] = csi;
+        s_dt[i] = dti;
+        s_b[i] = fast_exp2(cse - csi) * dti;
     }
-    // C rows of this wave's tiles, in fragment layout (row t = lane%16)
-    Frag<T> cf[NQ][KS];
     f32x4 yacc[NQ][4];
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-        const int t = (wave + 4 * q) * 16 + col;
-        const int tc = t < len ? t : len - 1;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-            cf[q][ks] = load_frag(Cm + ((b * L + t0 + tc) * G + g) * N + ks * 32 + grp * 8);
+    for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
     wait_dma();
     __syncthreads();
 
-    // inter-chunk term: (C_t exp(cs_t)) H_[c-1]; H read k-major (k = n)
+    // One row tile at a time (few live registers, so several blocks share a
+    // CU; the H and x fragments are re-read from LDS per tile).  The C rows of
+    // the next tile and the Gram pair of the next s block are requested one
+    // step ahead.
+    const float* gbase = gram + ((b * G + g) * M + c) * (int64_t)gram_pairs(S) * 512 + lane * 8;
+    auto load_c = [&](int q, Frag<T> (&cr)[KS]) {
+        const int t = tile_row(wave, q, NW) * 16 + col;
+        const int tc = t < len ? t : len - 1;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) cr[ks] = load_frag(Cm + ((b * L + t0 + tc) * G + g) * N + ks * 32 + grp * 8);
+    };
+    Frag<T> craw[KS];
+    load_c(0, craw);
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-        const int t = (wave + 4 * q) * 16 + col;
-        const float sc = fast_exp2(s_cs[t]);
+        const int r = tile_row(wave, q, NW);
+        const int t = r * 16 + col;
+        const float cst = s_cs[t];
+        const f32x4* gsrc = reinterpret_cast<const f32x4*>(gbase + (int64_t)gram_pair(r, 0) * 512);
+        f32x4 g0 = gsrc[0], g1 = gsrc[1];
+        // inter-chunk term: (C_t exp(cs_t)) H_[c-1]; C rows in fragment layout
+        // (row t = lane%16), H read k-major (k = n)
+        {
+            const float sc = fast_exp2(cst);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            float v[8];
+            for (int ks = 0; ks < KS; ++ks) {
+                float v[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) v[i] = to_f(cf[q][ks][i]) * sc;
-            const Frag<T> fa = make_frag<T>(v);
+                for (int i = 0; i < 8; ++i) v[i] = to_f(craw[ks][i]) * sc;
+                const Frag<T> fa = make_frag<T>(v);
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                const Frag<T> fh = frag_km<T, XRB>(ht, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4,
-                                                   pt * 16, lane);
-                yacc[q][pt] = mma16(yacc[q][pt], fa, fh);
+                for (int pt = 0; pt < 4; ++pt) {
+                    const Frag<T> fh = frag_km<T, XRB>(ht, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, pt * 16, lane);
+                    yacc[q][pt] = mma16(yacc[q][pt], fa, fh);
+                }
             }
         }
-    }
-
-    // intra-chunk term, one 32-token s block at a time for all of the wave's
-    // row tiles: Gram values (loaded one block ahead) times the causal mask,
-    // the decay and dt_s, then times x on MFMA (x fragments shared by the
-    // tiles).  A tile that does not reach the s block uses zeros.
-    const float* gbase = gram + ((b * G + g) * M + c) * (int64_t)gram_pairs(S) * 512 + lane * 8;
-    const int last_sk = ((wave + 4 * (NQ - 1)) * 16 + 15) / 32;  // last block any tile reaches
-    auto load_gram = [&](int sk, f32x4 (&gv)[NQ][2]) {
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int r = wave + 4 * q;
-            if (2 * sk <= r) {
-                const f32x4* src = reinterpret_cast<const f32x4*>(gbase + (int64_t)gram_pair(r, sk) * 512);
-                gv[q][0] = src[0];
-                gv[q][1] = src[1];
-            } else {
-                gv[q][0] = gv[q][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (q + 1 < NQ) load_c(q + 1, craw);
+        // intra-chunk term over the causal s blocks sk <= r/2
+        for (int sk = 0; sk <= (r >> 1); ++sk) {
+            const int sbase = sk * 32;
+            const f32x4 c0 = g0, c1 = g1;
+            if (sk < (r >> 1)) {
+                gsrc = reinterpret_cast<const f32x4*>(gbase + (int64_t)gram_pair(r, sk + 1) * 512);
+                g0 = gsrc[0];
+                g1 = gsrc[1];
             }
-        }
-    };
-    f32x4 gcur[NQ][2], gnext[NQ][2];
-    load_gram(0, gcur);
-    for (int sk = 0; sk <= last_sk; ++sk) {
-        if (sk < last_sk) load_gram(sk + 1, gnext);
-        const int sbase = sk * 32;
-        float css[8], dts8[8];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                css[4 * u + i] = s_cs[sbase + 16 * u + 4 * grp + i];
-                dts8[4 * u + i] = s_dt[sbase + 16 * u + 4 * grp + i];
-            }
-        Frag<T> fm[NQ];
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int t = (wave + 4 * q) * 16 + col;
-            const float cst = s_cs[t];
+            // k order of the A operand: s = sbase + 16 u + 4 grp + i, element 4 u + i
             float mv[8];
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
+            if (sk < (r >> 1)) {
+                const float a = fast_exp2(cst - s_cs[sbase + 31]);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int k = 4 * u + i;
-                    const int s = sbase + 16 * u + 4 * grp + i;
-                    mv[k] = (s <= t) ? gcur[q][u][i] * fast_exp2(cst - css[k]) * dts8[k] : 0.f;
+                    mv[i] = c0[i] * a * s_b[sbase + 4 * grp + i];
+                    mv[4 + i] = c1[i] * a * s_b[sbase + 16 + 4 * grp + i];
                 }
-            fm[q] = make_frag<T>(mv);
-        }
+            } else {
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            // x operand rows s = sbase + {4 grp + 0..3, 16 + 4 grp + 0..3}, column p
-            const Frag<T> fx = frag_km<T, XRB>(xs, sbase + 4 * grp, sbase + 16 + 4 * grp, pt * 16, lane);
+                for (int u = 0; u < 2; ++u)
 #pragma unroll
-            for (int q = 0; q < NQ; ++q) yacc[q][pt] = mma16(yacc[q][pt], fm[q], fx);
-        }
+                    for (int i = 0; i < 4; ++i) {
+                        const int s = sbase + 16 * u + 4 * grp + i;
+                        const float gval = u ? c1[i] : c0[i];
+                        mv[4 * u + i] = (s <= t) ? gval * fast_exp2(cst - s_cs[s]) * s_dt[s] : 0.f;
+                    }
+            }
+            const Frag<T> fm = make_frag<T>(mv);
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            gcur[q][0] = gnext[q][0];
-            gcur[q][1] = gnext[q][1];
+            for (int pt = 0; pt < 4; ++pt) {
+                const Frag<T> fx = frag_km<T, XRB>(xs, sbase + 4 * grp, sbase + 16 + 4 * grp, pt * 16, lane);
+                yacc[q][pt] = mma16(yacc[q][pt], fm, fx);
+            }
         }
     }
 
-    // yacc[q][pt][i] = y[t = 16 (wave + 4q) + 4 grp + i][p = 16 pt + col]:
-    // each 16-row tile goes through the wave's LDS scratch and leaves as
-    // 16-byte stores of whole rows
-    T* st = so[wave];
+    // yacc[q][pt][i] = y[t = 16 tile_row(wave, q) + 4 grp + i][p = 16 pt + col]:
+    // each 16-row tile goes through the wave's LDS scratch (the x rows, no
+    // longer read once every wave is done) and leaves as 16-byte stores of
+    // whole rows
+    __syncthreads();
+    T* st = reinterpret_cast<T*>(xs) + wave * 16 * kP;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) st[(4 * grp + i) * kP + pt * 16 + col] = from_f<T>(yacc[q][pt][i]);
-        const int tbase = (wave + 4 * q) * 16;
+        const int tbase = tile_row(wave, q, NW) * 16;
 #pragma unroll
         for (int e8 = lane; e8 < 16 * (kP / 8); e8 += 64) {
             const int r = e8 / (kP / 8), k8 = e8 % (kP / 8);
@@ -459,7 +465,7 @@ hipError_t run_scan(const Shape& s, const void* x, const float* dt, const float*
                       0, st>>>((const T*)mem, w.lda, h0, states, h_last, s.H, NP, s.M, s.Mcap);
     prof_end(st);
     prof_begin("k_chunk_out", st);
-    k_chunk_out<T, N, S><<<dim3((unsigned)(s.B * s.M * s.H)), kThreads, 0, st>>>(
+    k_chunk_out<T, N, S><<<dim3((unsigned)(s.B * s.M * s.H)), 64 * out_waves<S>(), 0, st>>>(
         (const T*)x, dt, (const T*)Cm, states, w.cs2, w.gram, (T*)y_ssd, s.L, s.H, s.G, s.M,
         s.B * s.M);
     prof_end(st);
