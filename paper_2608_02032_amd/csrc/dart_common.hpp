@@ -281,6 +281,33 @@ __device__ __forceinline__ Frag<T> frag_km(const char* tile, int krow0, int krow
     }
 }
 
+// The two transposing reads of frag_kmajor_bf16 with their per-lane byte
+// offsets computed once: rows ra and rb (per lane, + lane/4 within each
+// 16-lane group), columns cbase + 4 (lane % 4).  The row swizzle of SwzTile
+// depends on the row only modulo 8, so the fragment of rows shifted by a
+// multiple of 8 is read at the same offsets plus `add` = rows * RB bytes
+// (an immediate when known at compile time), with no address arithmetic.
+template <int RB>
+struct KmOffBf16 {
+    uint32_t o0, o1;
+    __device__ __forceinline__ void init(int ra, int rb, int cbase, int lane) {
+        using Tl = SwzTile<RB>;
+        const int j = lane & 15;
+        const int col_b = (cbase + 4 * (j & 3)) * 2;
+        o0 = (uint32_t)Tl::off(ra + (j >> 2), col_b);
+        o1 = (uint32_t)Tl::off(rb + (j >> 2), col_b);
+    }
+    __device__ __forceinline__ bf16x8 read(const char* tile, int add) const {
+        const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(tile + add + o0));
+        const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(tile + add + o1));
+        const bf16x4 b0 = __builtin_bit_cast(bf16x4, v0);
+        const bf16x4 b1 = __builtin_bit_cast(bf16x4, v1);
+        return bf16x8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+    }
+};
+
 // Fragment from a row-major swizzled tile (rows = the operand's m or n index,
 // 8 consecutive k per lane): one 16-byte read (two for fp32).
 template <typename T, int RB>

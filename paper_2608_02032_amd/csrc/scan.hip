@@ -34,7 +34,6 @@ namespace {
 
 constexpr int kP = 64;        // head dim
 constexpr int kThreads = 256; // 4 waves
-constexpr int kSB = 64;       // tokens per LDS-staged s-block
 
 // Inclusive prefix sum over the block (thread order).  All threads call it.
 __device__ float block_inclusive_scan(float v, float* sred) {
@@ -54,11 +53,51 @@ __device__ float block_inclusive_scan(float v, float* sred) {
 
 // ---------------------------------------------------------------------------
 // Chunk-state contraction: dH_[c] = sum_s exp(cs_e - cs_s) dt_s B_s^T x_s.
-// B_c and x_c stream through LDS in 64-token blocks (DMA, two stages held in
-// distinct LDS objects so the next block's copy overlaps this block's MFMAs);
-// both MFMA operands are read k-major with transpose loads.  Wave w owns
-// p-tile w and all n-tiles of the N x P result.
+// B_c and x_c stream through LDS in 32-token blocks by DMA into a four-stage
+// ring, three blocks ahead of the MFMAs that consume them; both MFMA operands
+// are read k-major with transpose loads.  Wave w owns p-tile w and all
+// n-tiles of the N x P result.  The copies are issued untracked (the compiler
+// cannot tell the stage being read from those being filled and would drain
+// every copy before each read); each wave waits for its own copies of a stage
+// before the barrier that opens it (vector memory operations complete in
+// order).
 // ---------------------------------------------------------------------------
+constexpr int kSB = 32;       // tokens per LDS-staged s block
+constexpr int kStages = 4;    // ring stages (kStages - 1 blocks in flight)
+
+// 4-byte global -> LDS copy by DMA (global_load_lds_dword), untracked like
+// lds_dma16_untracked: lane i's 4 bytes land at lds_wave_base + 4 i.
+__device__ __forceinline__ void lds_dma4_untracked(const void* gsrc, void* lds_wave_base) {
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_wave_base);
+    uint32_t save;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dword %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(save)
+        : "v"(gsrc), "s"(m0)
+        : "memory");
+}
+// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 15].
+__device__ __forceinline__ void wait_vm_upto(int n) {
+    switch (n) {
+#define DART_VMC(k) case k: __builtin_amdgcn_s_waitcnt(vmcnt_imm(k)); break;
+        DART_VMC(1) DART_VMC(2) DART_VMC(3) DART_VMC(4) DART_VMC(5) DART_VMC(6) DART_VMC(7)
+        DART_VMC(8) DART_VMC(9) DART_VMC(10) DART_VMC(11) DART_VMC(12) DART_VMC(13) DART_VMC(14)
+        DART_VMC(15)
+#undef DART_VMC
+        default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;
+    }
+}
+// 1 KiB copies that dma_tile issues from wave w of 4 for a tile of `pieces`
+// 16-byte pieces.
+__device__ __forceinline__ int dma_copies(int pieces, int w) {
+    return pieces > 64 * w ? (pieces - 64 * w + 255) / 256 : 0;
+}
+
 template <typename T, int N, int S>
 __global__ __launch_bounds__(kThreads) void k_chunk_state(
     const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
@@ -67,6 +106,10 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
     constexpr int XRB = kP * (int)sizeof(T);   // bytes per x row
     constexpr int BRB = N * (int)sizeof(T);    // bytes per B row
     constexpr int XT = kSB * XRB, BT = kSB * BRB;
+    constexpr int STB = XT + BT;               // bytes of one ring stage
+    constexpr int OUTB = 4 * N * 16 * (int)sizeof(T);  // output strips (reuse the ring)
+    constexpr int RINGB = kStages * STB > OUTB ? kStages * STB : OUTB;
+    static_assert(S <= kThreads, "one thread per token of the chunk");
     const int c = blockIdx.x, h = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int g = (int)((int64_t)h * G / H);
@@ -76,74 +119,107 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
     const int len = (int)(L - t0 < S ? L - t0 : S);
     const int nsb = (len + kSB - 1) / kSB;
 
+    __shared__ float s_dt[S];
     __shared__ float s_w[S];
     __shared__ float s_red[4];
     __shared__ float s_cse;
-    __shared__ __attribute__((aligned(16))) char xs0[XT];
-    __shared__ __attribute__((aligned(16))) char bs0[BT];
-    __shared__ __attribute__((aligned(16))) char xs1[XT];
-    __shared__ __attribute__((aligned(16))) char bs1[BT];
-    __shared__ __attribute__((aligned(16))) T so[4][N * 16];  // per-wave output strip
+    __shared__ __attribute__((aligned(16))) char ring[RINGB];
 
+    // copies: the chunk's dt (with block 0), then the x and B rows of each
+    // s block into its ring stage; rows past the end re-read the last row
+    // (their weights are zero), blocks past the end are not copied
+    if (tid < S) {
+        const int tok = tid < len ? tid : len - 1;
+        lds_dma4_untracked(dt + (b * L + t0 + tok) * H + h, s_dt + wave * 64);
+    }
     const char* xg = reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP);
     const char* bg = reinterpret_cast<const char*>(Bm + ((b * L + t0) * G + g) * N);
     const int64_t xstride = (int64_t)H * XRB, bstride = (int64_t)G * BRB;
-    auto stage = [&](int sb, char* xd, char* bd) {
+    auto stage = [&](int sb) {
+        if (sb >= nsb) return;
+        char* st = ring + (sb % kStages) * STB;
         const int rv = len - sb * kSB;
-        dma_tile<XRB>(xd, xg + sb * kSB * xstride, xstride, kSB, rv, wave, 4, lane);
-        dma_tile<BRB>(bd, bg + sb * kSB * bstride, bstride, kSB, rv, wave, 4, lane);
+        dma_tile<XRB, true>(st, xg + sb * kSB * xstride, xstride, kSB, rv, wave, 4, lane);
+        dma_tile<BRB, true>(st + XT, bg + sb * kSB * bstride, bstride, kSB, rv, wave, 4, lane);
     };
-    stage(0, xs0, bs0);
+    // this wave's copies per s block
+    const int cpw = dma_copies(XT / 16, wave) + dma_copies(BT / 16, wave);
+    // wait until this wave's copies of block sb are complete: the copies of
+    // the (at most kStages - 2) later blocks may still be in flight
+    auto wait_block = [&](int sb) {
+        const int later = (nsb - 1 - sb) < (kStages - 2) ? (nsb - 1 - sb) : (kStages - 2);
+        wait_vm_upto(later * cpw);
+    };
+#pragma unroll
+    for (int sb = 0; sb < kStages - 1; ++sb) stage(sb);
 
-    // cumulative log decay within the chunk (tokens past L contribute 0)
-    const float dts = (tid < len) ? dt[(b * L + t0 + tid) * H + h] : 0.f;
+    // block 0 and dt are in: cumulative log decay within the chunk (tokens
+    // past L contribute 0) and the weights exp(cs_e - cs_s) dt_s
+    wait_block(0);
+    __syncthreads();
+    const float dts = (tid < len) ? s_dt[tid] : 0.f;
     const float cs = block_inclusive_scan(tid < S ? dts * A[h] : 0.f, s_red);
     if (tid == S - 1) s_cse = cs;
     __syncthreads();
     const float cse = s_cse;
-    if (tid < S) {
-        s_w[tid] = (tid < len) ? __expf(cse - cs) * dts : 0.f;
-        cs2[((b * H + h) * M + c) * S + tid] = cs * kLog2e;
-    }
-    if (tid == 0) chunk_lda[(b * H + h) * M + c] = cse;
+    if (tid < S) s_w[tid] = (tid < len) ? __expf(cse - cs) * dts : 0.f;
 
     f32x4 acc[N / 16];
 #pragma unroll
     for (int nt = 0; nt < N / 16; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto consume = [&](int sb, const char* xt, const char* bt) {
+    // one s block: x operand (k = s, column p) scaled by w_s, then the B
+    // operand of every n tile; bf16 reads use offsets fixed here
+    KmOffBf16<XRB> xo;
+    KmOffBf16<BRB> bo[N / 16];
+    if constexpr (sizeof(T) == 2) {
+        xo.init(8 * grp, 8 * grp + 4, wave * 16, lane);
 #pragma unroll
-        for (int ks = 0; ks < kSB / 32; ++ks) {
-            // x operand (k = s, column p), scaled by w_s
-            Frag<T> fx = frag_km<T, XRB>(xt, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, wave * 16, lane);
-            float xv[8];
+        for (int nt = 0; nt < N / 16; ++nt) bo[nt].init(8 * grp, 8 * grp + 4, nt * 16, lane);
+    }
+    auto consume = [&](int sb, int u) __attribute__((always_inline)) {
+        const char* xt = ring + u * STB;
+        const char* bt = xt + XT;
+        Frag<T> fx;
+        if constexpr (sizeof(T) == 2) {
+            fx = xo.read(ring, u * STB);
+        } else {
+            fx = frag_km<T, XRB>(xt, 8 * grp, 8 * grp + 4, wave * 16, lane);
+        }
+        float xv[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) xv[i] = to_f(fx[i]) * s_w[sb * kSB + ks * 32 + 8 * grp + i];
-            fx = make_frag<T>(xv);
+        for (int i = 0; i < 8; ++i) xv[i] = to_f(fx[i]) * s_w[sb * kSB + 8 * grp + i];
+        fx = make_frag<T>(xv);
 #pragma unroll
-            for (int nt = 0; nt < N / 16; ++nt) {
-                const Frag<T> fb = frag_km<T, BRB>(bt, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, nt * 16, lane);
-                acc[nt] = mma16(acc[nt], fb, fx);
+        for (int nt = 0; nt < N / 16; ++nt) {
+            Frag<T> fb;
+            if constexpr (sizeof(T) == 2) {
+                fb = bo[nt].read(ring, u * STB + XT);
+            } else {
+                fb = frag_km<T, BRB>(bt, 8 * grp, 8 * grp + 4, nt * 16, lane);
             }
+            acc[nt] = mma16(acc[nt], fb, fx);
         }
     };
-    wait_dma();
-    __syncthreads();
-    for (int sb = 0; sb < nsb; sb += 2) {
-        if (sb + 1 < nsb) stage(sb + 1, xs1, bs1);
-        consume(sb, xs0, bs0);
-        wait_dma();
-        __syncthreads();
-        if (sb + 1 >= nsb) break;
-        if (sb + 2 < nsb) stage(sb + 2, xs0, bs0);
-        consume(sb + 1, xs1, bs1);
-        wait_dma();
-        __syncthreads();
+    // the loop is unrolled over the ring so every stage offset is an immediate
+    for (int sb0 = 0; sb0 < nsb; sb0 += kStages) {
+#pragma unroll
+        for (int u = 0; u < kStages; ++u) {
+            const int sb = sb0 + u;
+            if (sb >= nsb) break;
+            if (sb > 0) wait_block(sb);
+            lds_barrier();   // block sb (and s_w) are in; every wave is done with block sb - 1
+            stage(sb + kStages - 1);
+            consume(sb, u);
+        }
     }
-    // acc[nt][i] = dH[n = 16 nt + 4 (lane/16) + i][p = 16 wave + lane%16]:
-    // the wave's N x 16 strip goes through its own LDS scratch, then each row's
-    // 16 values leave as 16-byte stores
-    T* st = so[wave];
+    // outputs: the within-chunk cumulative decays (log2 units, for the output
+    // kernel), the chunk's total log decay, and dH: acc[nt][i] = dH[n = 16 nt +
+    // 4 (lane/16) + i][p = 16 wave + lane%16], each wave's N x 16 strip through
+    // LDS (the ring) and out as 16-byte row stores
+    if (tid < S) cs2[((b * H + h) * M + c) * S + tid] = cs * kLog2e;
+    if (tid == 0) chunk_lda[(b * H + h) * M + c] = cse;
+    __syncthreads();
+    T* st = reinterpret_cast<T*>(ring) + wave * N * 16;
 #pragma unroll
     for (int nt = 0; nt < N / 16; ++nt)
 #pragma unroll
@@ -293,7 +369,7 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
 
     __shared__ float s_cs[S];  // within-chunk cumulative log decay, log2 units
     __shared__ float s_dt[S];
-    __shared__ float s_b[S];   // exp2(cs_e - cs_s) dt_s, e = end of the s block
+    __shared__ __attribute__((aligned(16))) float s_b[S];   // exp2(cs_e - cs_s) dt_s, e = end of the s block
     __shared__ __attribute__((aligned(16))) char ht[HT];
     __shared__ __attribute__((aligned(16))) char xs[XT];
 
@@ -331,6 +407,30 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
     };
     Frag<T> craw[KS];
     load_c(0, craw);
+    // bf16 fragment reads at offsets fixed here: H rows 32 ks + 8 grp (+4),
+    // x rows 32 sk + 4 grp (+16), column tile pt
+    KmOffBf16<XRB> ho[4], xo[4];
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) {
+            ho[pt].init(8 * grp, 8 * grp + 4, pt * 16, lane);
+            xo[pt].init(4 * grp, 16 + 4 * grp, pt * 16, lane);
+        }
+    }
+    auto frag_h = [&](int ks, int pt) __attribute__((always_inline)) {
+        if constexpr (sizeof(T) == 2) {
+            return ho[pt].read(ht, ks * 32 * XRB);
+        } else {
+            return frag_km<T, XRB>(ht, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, pt * 16, lane);
+        }
+    };
+    auto frag_x = [&](int sk, int pt) __attribute__((always_inline)) {
+        if constexpr (sizeof(T) == 2) {
+            return xo[pt].read(xs, sk * 32 * XRB);
+        } else {
+            return frag_km<T, XRB>(xs, sk * 32 + 4 * grp, sk * 32 + 16 + 4 * grp, pt * 16, lane);
+        }
+    };
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
         const int r = tile_row(wave, q, NW);
@@ -349,15 +449,15 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
                 for (int i = 0; i < 8; ++i) v[i] = to_f(craw[ks][i]) * sc;
                 const Frag<T> fa = make_frag<T>(v);
 #pragma unroll
-                for (int pt = 0; pt < 4; ++pt) {
-                    const Frag<T> fh = frag_km<T, XRB>(ht, ks * 32 + 8 * grp, ks * 32 + 8 * grp + 4, pt * 16, lane);
-                    yacc[q][pt] = mma16(yacc[q][pt], fa, fh);
-                }
+                for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = mma16(yacc[q][pt], fa, frag_h(ks, pt));
             }
         }
         if (q + 1 < NQ) load_c(q + 1, craw);
-        // intra-chunk term over the causal s blocks sk <= r/2
-        for (int sk = 0; sk <= (r >> 1); ++sk) {
+        // intra-chunk term over the causal s blocks sk <= r/2 (unrolled, so
+        // the x fragment offsets are immediates)
+#pragma unroll
+        for (int sk = 0; sk < S / 32; ++sk) {
+            if (sk > (r >> 1)) break;
             const int sbase = sk * 32;
             const f32x4 c0 = g0, c1 = g1;
             if (sk < (r >> 1)) {
@@ -369,10 +469,12 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
             float mv[8];
             if (sk < (r >> 1)) {
                 const float a = fast_exp2(cst - s_cs[sbase + 31]);
+                const f32x4 b0 = *reinterpret_cast<const f32x4*>(&s_b[sbase + 4 * grp]);
+                const f32x4 b1 = *reinterpret_cast<const f32x4*>(&s_b[sbase + 16 + 4 * grp]);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    mv[i] = c0[i] * a * s_b[sbase + 4 * grp + i];
-                    mv[4 + i] = c1[i] * a * s_b[sbase + 16 + 4 * grp + i];
+                    mv[i] = c0[i] * (a * b0[i]);
+                    mv[4 + i] = c1[i] * (a * b1[i]);
                 }
             } else {
 #pragma unroll
@@ -386,10 +488,7 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
             }
             const Frag<T> fm = make_frag<T>(mv);
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                const Frag<T> fx = frag_km<T, XRB>(xs, sbase + 4 * grp, sbase + 16 + 4 * grp, pt * 16, lane);
-                yacc[q][pt] = mma16(yacc[q][pt], fm, fx);
-            }
+            for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = mma16(yacc[q][pt], fm, frag_x(sk, pt));
         }
     }
 

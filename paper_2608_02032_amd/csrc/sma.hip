@@ -939,7 +939,6 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     constexpr int NF = 4 * KS;               // operand fragments per tile (4 P-slices)
     constexpr int PD = 3;                    // fragments read ahead
     constexpr int KST = 3, VST = 5;          // key and value ring stages
-    constexpr int FK = KS > 1 ? 1 : 0;       // group that applies the previous slice
     static_assert(S >= PT, "a pair's tokens must lie in one chunk");
     static_assert(NF >= 4, "at least one fragment per slice");
     using Dma = TileDmaPN<N, 4>;  // the score waves issue all copies
