@@ -48,6 +48,11 @@ def parse():
                          "(reference kernel for scaling HBM byte counters)")
     ap.add_argument("--extra-out", default=None,
                     help="also write per-kernel detail as JSON to this file")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line: time the forward (scan and SMA "
+                         "separately) on every bf16 forward workload and print one JSON line each")
+    ap.add_argument("--sweep-out", default=None,
+                    help="with --sweep: also write the results as a markdown table to this file")
     return ap.parse_args()
 
 
@@ -118,6 +123,84 @@ def cpu_baseline(w, nbatch):
                       % (nbatch, w.batch, w.name, w.nheads, w.seqlen, sec)}
 
 
+def sweep(args):
+    """Scan and SMA time and utilisation on every bf16 forward workload (the
+    chunk/state sweep at L = 8192, the Mamba-2-130M-shaped layer and the
+    L = 65536 long context)."""
+    import torch
+    from paper_2608_02032_amd import dart, synth
+    dev = torch.device("cuda:0")
+    names = [n for n, w in synth.WORKLOADS.items() if w.dtype == "bf16"]
+    rows = []
+    for name in names:
+        w = synth.WORKLOADS[name]
+        d = synth.forward_inputs(w, seed=0)
+        T = {k: torch.from_numpy(v).to(dev) for k, v in d.items()}
+        for k in ("x", "Bm", "Cm", "q", "e", "z"):
+            T[k] = T[k].to(torch.bfloat16)
+        B, L, H, P, N, S = w.batch, w.seqlen, w.nheads, w.headdim, w.dstate, w.chunk
+        y_ssd = torch.empty((B, L, H, P), dtype=torch.bfloat16, device=dev)
+        mem = torch.empty((B, w.nchunks, H, N, P), dtype=torch.bfloat16, device=dev)
+        h_last = torch.empty((B, H, N, P), dtype=torch.float32, device=dev)
+        y = torch.empty_like(y_ssd)
+        lse = torch.empty((B, L, H), dtype=torch.float32, device=dev)
+        dims = dart.make_dims(B, L, H, P, N, S, w.dtype, w.ngroups)
+        ws_scan = torch.empty(dart.workspace_bytes("scan", dims), dtype=torch.uint8, device=dev)
+        ws_sma = torch.empty(max(1, dart.workspace_bytes("sma", dims)), dtype=torch.uint8, device=dev)
+        stream = torch.cuda.current_stream()
+
+        def forward():
+            dart.ssd_chunk_scan(T["x"], T["dt"], T["A"], T["Bm"], T["Cm"], S, mem=mem, y_ssd=y_ssd,
+                                h_last=h_last, workspace=ws_scan, stream=stream)
+            dart.sma_fwd(T["q"], T["e"], T["Cm"], mem, T["z"], y_ssd, S, y=y, lse=lse,
+                         workspace=ws_sma, stream=stream)
+        for _ in range(args.warmup):
+            forward()
+        torch.cuda.synchronize()
+        dart.profile_reset()
+        dart.profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            forward()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dart.profile_enable(False)
+        kern = dart.profile_read(reset=True)
+        avg = {k: v[0] / max(v[1], 1) for k, v in kern.items()}
+        fwd_ms = e0.elapsed_time(e1) / args.steps
+        scan_ms = sum(avg.get(k, 0.0) for k in ("k_chunk_state", "k_chunk_gram", "k_state_pass",
+                                                 "k_chunk_out"))
+        sma_ms = sum(avg.get(k, 0.0) for k in ("k_sma_prep", "k_sma_keys", "k_sma"))
+        sflops, sbytes, mflops = scan_flops(w), scan_bytes(w), sma_flops(w)
+        r = {"workload": name, "batch": B, "seq_len": L, "heads": H, "dstate": N, "chunk": S,
+             "fwd_ms": round(fwd_ms, 4), "tokens_per_s": round(B * L / (fwd_ms * 1e-3), 1),
+             "scan_us": round(scan_ms * 1e3, 2), "sma_us": round(sma_ms * 1e3, 2),
+             "k_sma_us": round(avg.get("k_sma", 0.0) * 1e3, 2),
+             "scan_hbm_frac": round(sbytes / (scan_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+             "scan_mfma_util": round(sflops / (scan_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+             "sma_mfma_util": round(mflops / (sma_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+             "k_sma_mfma_util": round(mflops / (avg["k_sma"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+             if avg.get("k_sma") else None}
+        rows.append(r)
+        print(json.dumps(r), flush=True)
+        del T, y_ssd, mem, h_last, y, lse, ws_scan, ws_sma
+        torch.cuda.empty_cache()
+    if args.sweep_out:
+        hdr = ["workload", "fwd_ms", "tokens_per_s", "scan_us", "scan_hbm_frac", "scan_mfma_util",
+               "sma_us", "k_sma_us", "sma_mfma_util", "k_sma_mfma_util"]
+        lines = ["# Forward sweep (bf16 workloads)", "", "Command:", "", "```",
+                 "python3 bench.py --sweep --steps %d --warmup %d --sweep-out <this file>"
+                 % (args.steps, args.warmup), "```", "",
+                 "Times from the library's HIP events; utilisation against 8 TB/s and "
+                 "2.5 PFLOP/s (algorithmic bytes and flops).", "",
+                 "| " + " | ".join(hdr) + " |", "|" + "---|" * len(hdr)]
+        for r in rows:
+            lines.append("| " + " | ".join(str(r[k]) for k in hdr) + " |")
+        with open(args.sweep_out, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -136,6 +219,9 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.sweep:
+        sweep(args)
+        return
     w = synth.WORKLOADS[args.workload]
     dw = synth.DECODE_WORKLOADS[args.decode_workload]
     bf = torch.bfloat16 if w.dtype == "bf16" else torch.float32
