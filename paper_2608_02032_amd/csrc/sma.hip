@@ -44,7 +44,7 @@ constexpr int kP = 64;
 constexpr int kWaves = 8;                  // 4 (score, value) pairs
 constexpr int kThreads = kWaves * 64;
 constexpr float kRescaleLog2 = 8.0f;       // lazy-rescale threshold (log2 units)
-constexpr int kHeadsPerBlock = 4;          // heads of one group served by a block (power of 2)
+constexpr int kHeadsPerBlock = 8;          // heads of one group served by a block (power of 2)
 
 // 16-token column tiles per pair: 4 for bf16 (64 tokens), 2 for fp32 (its
 // operand fragments take twice the registers).
