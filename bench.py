@@ -35,8 +35,8 @@ PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="sweep_L8192_S256_N128")
     ap.add_argument("--decode-workload", default="decode_B64_ctx65536")
     ap.add_argument("--no-decode", action="store_true", help="time the forward only")

@@ -8,32 +8,35 @@
 // query tile fixed, historical memories streamed, online softmax, only R and
 // the log-sum-exp leave the chip).
 //
-// One kernel, k_sma: one workgroup per (b, head, token block).  The block's 8
-// waves form 4 pairs; each pair owns 16*RT consecutive tokens inside one
-// chunk.  In a pair, the score wave holds Qbar and Ebar and the value wave
-// holds C and the output accumulator O, so each wave keeps only half of the
-// per-token operands and every operand fragment it reads from LDS feeds RT
-// independent MFMA chains.
-//
-// A first kernel, k_sma_keys, writes the key side of every attended memory,
-// r_j (.) dH_j with r_j[n] = (mean_p dH_j[n,p]^2 + eps)^-1/2 reduced from the
-// stored values, to the workspace (same [N][P] layout as the cache).  The
-// main kernel streams key tiles from there and value tiles dH_j straight from
-// the memory cache into swizzled [N][P] LDS tiles: by DMA two steps ahead into
-// a four-stage ring (global_load_lds, no registers), or, when four stages do
-// not fit in LDS (fp32, N = 128), through registers one step ahead into two
-// stages.  Step s of the streaming loop:
+// Both precisions run one workgroup per (b, group of heads, token block).
+// The block's 8 waves form 4 pairs; each pair owns 16*RT consecutive tokens
+// inside one chunk.  In a pair, the score wave holds Qbar and Ebar and the
+// value wave holds C and the output accumulator O, so each wave keeps only
+// half of the per-token operands and every operand fragment it reads from LDS
+// feeds RT independent MFMA chains.  The block streams the memories of its
+// heads, head by head; per step:
 //   score waves   U^T = (r_s (.) dH_s)^T Qbar^T (P x tokens, MFMA), logits
-//                 l_t = sum_p U^T[p,t] Ebar[t,p] (the lane's registers plus one
-//                 MFMA against a ones matrix for the 4 lanes of a column),
-//                 online softmax in base 2; the weights of memory s (and a
-//                 rescale factor when the running maximum moved) go to LDS;
-//   value waves   V^T = dH_{s-1}^T C^T (MFMA), O = alpha O + w_{s-1} V;
-//   all threads   copy the tiles of a later memory.
-// One barrier per step.  Epilogue: the score wave publishes its softmax
-// denominators and writes LSE = (m + log2 d) ln 2; the value wave writes
-// y = y_ssd + SiLU(z) O/d.  Operand fragments are read with transposing LDS
-// loads (ds_read_b64_tr_b16 for bf16).
+//                 l_t = sum_p U^T[p,t] Ebar[t,p], online softmax in base 2;
+//                 the weights of memory s (and a rescale factor when the
+//                 running maximum moved) go to LDS;
+//   value waves   V^T = dH^T C^T of an earlier memory (MFMA), O = alpha O + w V;
+// with one barrier per step.  Epilogue of each head: the score wave publishes
+// its softmax denominators and writes LSE = (m + log2 d) ln 2; the value wave
+// writes y = y_ssd + SiLU(z) O/d.
+//
+// bf16 (k_sma_prep, k_sma): a first kernel writes both sides of every attended
+// memory transposed to [P][N] (key side r (.) dH rounded to bf16, value side
+// dH), so every MFMA operand fragment is one 16-byte LDS read.  k_sma copies
+// the tiles by DMA (global_load_lds, no registers) into XOR-swizzled LDS
+// rings, key tiles two steps and value tiles one step ahead; the value waves
+// lag the score waves by two memories so neither waits on the other within a
+// step, and they copy each head's y_ssd rows and gates into LDS a step before
+// the head ends.
+//
+// fp32 (k_sma_keys, k_sma_regs): a first kernel writes the key side in the
+// cache's [N][P] layout; value tiles come straight from the cache, through
+// registers one step ahead when four LDS stages do not fit.  Operand fragments
+// are read with transposing LDS loads.
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
 
@@ -140,50 +143,6 @@ template <typename T, int RT>
 __device__ __forceinline__ void load_epilogue_inputs(const T* const (&zp)[RT],
                                                      const T* const (&yp)[RT], float (&zz)[RT],
                                                      Vec4<T> (&ys)[RT][4]);
-template <>
-__device__ __forceinline__ void load_epilogue_inputs<bf16, 4>(const bf16* const (&zp)[4],
-                                                              const bf16* const (&yp)[4],
-                                                              float (&zz)[4],
-                                                              Vec4<bf16> (&ys)[4][4]) {
-    uint32_t zr[4];
-    uint64_t yr[4][4];
-    asm volatile(
-        "global_load_ushort %0, %20, off\n\t"
-        "global_load_ushort %1, %21, off\n\t"
-        "global_load_ushort %2, %22, off\n\t"
-        "global_load_ushort %3, %23, off\n\t"
-        "global_load_dwordx2 %4, %24, off\n\t"
-        "global_load_dwordx2 %5, %24, off offset:32\n\t"
-        "global_load_dwordx2 %6, %24, off offset:64\n\t"
-        "global_load_dwordx2 %7, %24, off offset:96\n\t"
-        "global_load_dwordx2 %8, %25, off\n\t"
-        "global_load_dwordx2 %9, %25, off offset:32\n\t"
-        "global_load_dwordx2 %10, %25, off offset:64\n\t"
-        "global_load_dwordx2 %11, %25, off offset:96\n\t"
-        "global_load_dwordx2 %12, %26, off\n\t"
-        "global_load_dwordx2 %13, %26, off offset:32\n\t"
-        "global_load_dwordx2 %14, %26, off offset:64\n\t"
-        "global_load_dwordx2 %15, %26, off offset:96\n\t"
-        "global_load_dwordx2 %16, %27, off\n\t"
-        "global_load_dwordx2 %17, %27, off offset:32\n\t"
-        "global_load_dwordx2 %18, %27, off offset:64\n\t"
-        "global_load_dwordx2 %19, %27, off offset:96\n\t"
-        "s_waitcnt vmcnt(0)"
-        : "=&v"(zr[0]), "=&v"(zr[1]), "=&v"(zr[2]), "=&v"(zr[3]),
-          "=&v"(yr[0][0]), "=&v"(yr[0][1]), "=&v"(yr[0][2]), "=&v"(yr[0][3]),
-          "=&v"(yr[1][0]), "=&v"(yr[1][1]), "=&v"(yr[1][2]), "=&v"(yr[1][3]),
-          "=&v"(yr[2][0]), "=&v"(yr[2][1]), "=&v"(yr[2][2]), "=&v"(yr[2][3]),
-          "=&v"(yr[3][0]), "=&v"(yr[3][1]), "=&v"(yr[3][2]), "=&v"(yr[3][3])
-        : "v"(zp[0]), "v"(zp[1]), "v"(zp[2]), "v"(zp[3]), "v"(yp[0]), "v"(yp[1]), "v"(yp[2]),
-          "v"(yp[3])
-        : "memory");
-#pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
-        zz[rt] = __builtin_bit_cast(float, zr[rt] << 16);
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) ys[rt][pt] = __builtin_bit_cast(Vec4<bf16>, yr[rt][pt]);
-    }
-}
 template <>
 __device__ __forceinline__ void load_epilogue_inputs<float, 2>(const float* const (&zp)[2],
                                                                const float* const (&yp)[2],
@@ -938,7 +897,8 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     constexpr int MEMB = kP * RB;            // bytes of one memory
     constexpr int NF = 4 * KS;               // operand fragments per tile (4 P-slices)
     constexpr int PD = 3;                    // fragments read ahead
-    constexpr int KST = 3, VST = 5;          // key and value ring stages
+    constexpr int KST = 3, VST = 4;          // key and value ring stages
+    constexpr int YB = PT * kP * 2;          // bytes of a pair's y_ssd tile (bf16)
     static_assert(S >= PT, "a pair's tokens must lie in one chunk");
     static_assert(NF >= 4, "at least one fragment per slice");
     using Dma = TileDmaPN<N, 4>;  // the score waves issue all copies
@@ -980,6 +940,8 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     __shared__ float xa[2][4][PT];
     __shared__ int xr[2][4];
     __shared__ float xd[2][4][PT];
+    __shared__ __attribute__((aligned(16))) char ybuf[4 * YB];  // epilogue y_ssd, per pair
+    __shared__ uint32_t zbuf[4][PT];                            // epilogue z, per pair
 
     // ---- memory stream: DMA of whole tiles, each wave its fixed pieces -------
     const char* kbase0 = reinterpret_cast<const char*>(kT) + (b * Mp * H + h0) * (int64_t)MEMB;
@@ -987,19 +949,28 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     const int64_t jstride = (int64_t)H * MEMB;
     Dma tdma;
     tdma.init(wave, lane);
-    const int dcnt = 2 * tdma.count();  // copies per memory issued by this wave
-    int fh = 0, fj = 0;                 // next memory to copy (head, index)
-    auto fetch_next = [&](int kst, int vst) __attribute__((always_inline)) {
-        const int64_t off = (int64_t)fh * MEMB + (int64_t)fj * jstride;
-        tdma.issue(kbase0 + off, kring + kst * MEMB);
-        tdma.issue(vbase0 + off, vring + vst * MEMB);
-        if (++fj == jmax) {
-            fj = 0;
-            ++fh;
+    const int tcnt = tdma.count();      // copies per tile issued by this wave
+    // next key and value tiles to copy, as (head, index) in memory order
+    int kh = 0, kj = 0, vh = 0, vj = 0;
+    auto advance = [&](int& h, int& j) __attribute__((always_inline)) {
+        if (++j == jmax) {
+            j = 0;
+            ++h;
         }
     };
-    if (nmem > 0) fetch_next(0, 0);
-    if (nmem > 1) fetch_next(1, 1);
+    auto fetch_k = [&](int st) __attribute__((always_inline)) {
+        tdma.issue(kbase0 + (int64_t)kh * MEMB + (int64_t)kj * jstride, kring + st * MEMB);
+        advance(kh, kj);
+    };
+    auto fetch_v = [&](int st) __attribute__((always_inline)) {
+        tdma.issue(vbase0 + (int64_t)vh * MEMB + (int64_t)vj * jstride, vring + st * MEMB);
+        advance(vh, vj);
+    };
+    if (nmem > 0) {
+        fetch_k(0);
+        fetch_v(0);
+    }
+    if (nmem > 1) fetch_k(1);
 
     // Operand fragment (slice pt, k step ks) of a [P][N] tile: lane (grp, col)
     // takes row p = 16 pt + col, n = 32 ks + 8 grp .. +7, one 16-byte read.
@@ -1070,26 +1041,34 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // One step of the stream for every wave: copy memory s+2, the wave's work,
-    // wait for this wave's copies of memory s+1, barrier.  Score waves (they
-    // write the softmax weights to LDS) make their LDS writes complete before
-    // the barrier; value waves write no LDS and cross it with their reads of
-    // the next step's first fragments still in flight (a compiler-level
-    // barrier keeps every LDS access on its side of it).
+    // One step of the stream for every wave: copy the key tile of memory s+2
+    // and the value tile of memory s+1 (the score waves issue all copies), the
+    // wave's work, barrier.  Memory s is scored at step s and its value tile
+    // consumed at step s+2 (first fragments read at the end of step s+1), so
+    // three key stages and four value stages suffice.  Score waves wait for
+    // every copy but this step's and make their LDS writes (the softmax
+    // weights) complete before the barrier; value waves write LDS only
+    // through their own epilogue copies, which they wait for themselves, and
+    // cross the barrier with their reads of the next step's first fragments
+    // still in flight (a compiler-level barrier keeps every LDS access on its
+    // side of it).
     auto run_stream = [&](auto&& work) __attribute__((always_inline)) {
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // prologue loads and memories 0, 1
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // prologue loads and first tiles
         lds_barrier();
         int kc = 0, vc = 0;                        // s % KST, s % VST
         for (int s = 0; s < nmem + 2; ++s) {
-            const bool copy = s + 2 < nmem;
-            if (copy) fetch_next(kc == 0 ? 2 : kc - 1, vc >= 3 ? vc - 3 : vc + 2);
+            const bool kcopy = s + 2 < nmem, vcopy = s + 1 < nmem;
+            if (kcopy) fetch_k(kc == 0 ? 2 : kc - 1);
+            if (vcopy) fetch_v(vc == VST - 1 ? 0 : vc + 1);
             work(s, kc, vc);
-            if (copy) {
-                wait_vm(dcnt);
-            } else {
-                __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-            }
             if (scorer) {
+                if (kcopy) {
+                    wait_vm(2 * tcnt);
+                } else if (vcopy) {
+                    wait_vm(tcnt);
+                } else {
+                    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+                }
                 lds_barrier();
             } else {
                 asm volatile("s_barrier" ::: "memory");
@@ -1262,47 +1241,103 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             }
         }
         f32x4 o[RT][4];
-        // token rows are recomputed here rather than kept live through the
-        // stream (the empty asm keeps the compiler from hoisting them out of it)
+        // Epilogue inputs of head hh (the pair's y_ssd rows and gates) are
+        // copied into the pair's LDS buffers a step before the head's last
+        // memory is consumed, so their latency hides behind that step.  y_ssd
+        // row r (64 bf16, eight 16-byte chunks) goes to ybuf row r with chunk c
+        // in slot c ^ (r & 7): copy k moves rows 8k .. 8k+7, lane l taking row
+        // 8k + l/8 and slot l % 8.  The gate of token r is one 16-bit copy into
+        // the 4-byte slot r of zbuf.  Rows past the end re-read the last token.
+        char* const yb = ybuf + pair * YB;
+        const int lastr = (int)((L - 1 - pbase < PT - 1) ? L - 1 - pbase : PT - 1);
+        const int64_t zstride = z_per_head ? H : 1;
+        auto prefetch_epilogue = [&](int hh) __attribute__((always_inline)) {
+            if (!active) return;  // no token of the pair exists
+            const int h = h0 + hh;
+            const uint64_t yg = (uint64_t)(uintptr_t)(y_ssd + ((b * L + pbase) * H + h) * kP);
+            const uint64_t zg = (uint64_t)(uintptr_t)(z + (b * L + pbase) * zstride + (z_per_head ? h : 0));
+            const uint64_t ybase = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(yg >> 32)) << 32) |
+                                   (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)yg);
+            const uint64_t zbase = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(zg >> 32)) << 32) |
+                                   (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)zg);
+            const uint32_t lb = (uint32_t)__builtin_amdgcn_readfirstlane(
+                (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)yb);
+            const uint32_t lz = (uint32_t)__builtin_amdgcn_readfirstlane(
+                (int)(uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)&zbuf[pair][0]);
+            // per-lane offsets are recomputed at each use (the empty asm keeps
+            // the compiler from hoisting them out of the stream)
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            const uint32_t rowb = (uint32_t)(H * kP * 2);
+            const uint32_t slot = (uint32_t)(((ln & 7) ^ (ln >> 3)) << 4);
+#pragma unroll
+            for (int k = 0; k < PT / 8; ++k) {
+                const int r = 8 * k + (ln >> 3);
+                const uint32_t off = (uint32_t)(r < lastr ? r : lastr) * rowb + slot;
+                const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lb + (uint32_t)(k * 1024)));
+                uint32_t save;
+                asm volatile(
+                    "s_mov_b32 %0, m0\n\t"
+                    "s_mov_b32 m0, %3\n\t"
+                    "s_nop 0\n\t"
+                    "global_load_lds_dwordx4 %1, %2\n\t"
+                    "s_mov_b32 m0, %0"
+                    : "=&s"(save)
+                    : "v"(off), "s"(ybase), "s"(m0)
+                    : "memory");
+            }
+            {
+                const uint32_t off = (uint32_t)((ln < lastr ? ln : lastr) * zstride * 2);
+                uint32_t save;
+                asm volatile(
+                    "s_mov_b32 %0, m0\n\t"
+                    "s_mov_b32 m0, %3\n\t"
+                    "s_nop 0\n\t"
+                    "global_load_lds_ushort %1, %2\n\t"
+                    "s_mov_b32 m0, %0"
+                    : "=&s"(save)
+                    : "v"(off), "s"(zbase), "s"(lz)
+                    : "memory");
+            }
+        };
+        // y = y_ssd + silu(z) R for head hh, R = O / d, once its copies landed
         auto finish_head = [&](int hh) __attribute__((always_inline)) {
             const int h = h0 + hh;
-            const T* zp[RT];
-            const T* yp[RT];
-            int64_t row[RT];
-            int c = col;
-            asm volatile("" : "+v"(c));
+            int c = col, gq = grp;
+            asm volatile("" : "+v"(c), "+v"(gq));
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
-                const int64_t t = pbase + rt * 16 + c;
-                row[rt] = b * L + (t < L ? t : L - 1);
-                zp[rt] = z_per_head ? z + row[rt] * H + h : z + row[rt];
-                yp[rt] = y_ssd + (row[rt] * H + h) * kP + grp * 4;
-            }
-            float zz[RT];
-            Vec4<T> ys[RT][4];
-            load_epilogue_inputs<T, RT>(zp, yp, zz, ys);
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                if (pbase + rt * 16 + col >= L) continue;
-                const float gate = silu(zz[rt]);
-                const float invd = hist ? 1.0f / xd[hh & 1][pair][rt * 16 + col] : 0.f;
+                const int r = rt * 16 + c;
+                const int64_t t = pbase + r;
+                if (t >= L) continue;
+                const float gate = silu(__builtin_bit_cast(float, zbuf[pair][r] << 16));
+                const float invd = hist ? 1.0f / xd[hh & 1][pair][r] : 0.f;
+                bf16* yrow = y + ((b * L + t) * H + h) * kP + gq * 4;
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
+                    const Vec4<T> ys = *reinterpret_cast<const Vec4<T>*>(
+                        yb + r * (kP * 2) + ((((2 * pt + (gq >> 1)) ^ (c & 7))) << 4) + (gq & 1) * 8);
                     float yv[4];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[rt][pt][i]);
+                    for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[i]);
                     if (hist) {
 #pragma unroll
                         for (int i = 0; i < 4; ++i) yv[i] += gate * (o[rt][pt][i] * invd);
                     }
-                    store4(y + (row[rt] * H + h) * kP + pt * 16 + grp * 4, yv);
+                    store4(yrow + pt * 16, yv);
                 }
             }
         };
         if (nmem == 0) {
-            for (int hh = 0; hh < hpb; ++hh) finish_head(hh);
+            for (int hh = 0; hh < hpb; ++hh) {
+                prefetch_epilogue(hh);
+                finish_head(hh);
+            }
             return;
         }
+        // index of the memory at whose step a head's epilogue copies start
+        const int jpf = jmax >= 2 ? jmax - 2 : 0;
         Frag<T> fr[4];             // fragment ring; the first PD of the next step's
                                    // memory are read before the barrier
         int jv = 0, hv = 0;        // (index, head) of memory s-2
@@ -1315,12 +1350,13 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             pwp[rt] = 0.f;
         }
         // memory J's value tile sits in stage J % VST; at step s, J = s-2 is in
-        // stage (vc + 3) % 5 and the next step's memory s-1 in (vc + 4) % 5
+        // stage (vc + 2) % 4 and the next step's memory s-1 in (vc + 3) % 4
         run_stream([&](int s, int, int vc) __attribute__((always_inline)) {
             const int J = s - 2;
             if (J >= 0) {
                 const bool act = jv < nj;
-                const char* vt = vring + (vc >= 2 ? vc - 2 : vc + 3) * MEMB;
+                const char* vt = vring + (vc >= 2 ? vc - 2 : vc + 2) * MEMB;
+                if (jv == jpf) prefetch_epilogue(hv);
                 if (act) {
                     const int slot = J & 1;
                     float pw[RT];
@@ -1372,7 +1408,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             }
             // first fragments of the next step's memory (s-1), if attended
             if (s >= 1 && s - 1 < nmem && jv < nj) {
-                const char* vn = vring + (vc >= 1 ? vc - 1 : vc + 4) * MEMB;
+                const char* vn = vring + (vc >= 1 ? vc - 1 : vc + 3) * MEMB;
 #pragma unroll
                 for (int f = 0; f < PD; ++f) fr[f] = frag(vn, f);
             }
@@ -1414,22 +1450,21 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
             hpb, BHC);
         prof_end(st);
         return hipGetLastError();
-    }
-    if (Mp > 0) {
-        prof_begin("k_sma_keys", st);
-        k_sma_keys<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
-            (const T*)mem, kmem, a.eps, a.normalize, s.H, Mp, s.Mcap);
-        prof_end(st);
-    }
-    prof_begin("k_sma", st);
-    {
+    } else {
+        if (Mp > 0) {
+            prof_begin("k_sma_keys", st);
+            k_sma_keys<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
+                (const T*)mem, kmem, a.eps, a.normalize, s.H, Mp, s.Mcap);
+            prof_end(st);
+        }
+        prof_begin("k_sma", st);
         k_sma_regs<T, N, S><<<dim3((unsigned)(BHC * nblk)), kThreads, 0, st>>>(
             (const T*)q, (const T*)e, (const T*)Cm, (const T*)mem, kmem, (const T*)z,
             (const T*)y_ssd, (T*)y, lse, a.qw, a.ew, a.eps, a.normalize, a.z_per_head, s.L, s.H,
             s.G, s.Mcap, Mp, nblk, hpb, BHC);
+        prof_end(st);
+        return hipGetLastError();
     }
-    prof_end(st);
-    return hipGetLastError();
 }
 
 template <typename T, int N>
