@@ -181,6 +181,26 @@ __device__ __forceinline__ void lds_dma16_untracked(const void* gsrc, void* lds_
         : "v"(gsrc), "s"(m0)
         : "memory");
 }
+// The same copy with the LDS destination given as an LDS byte address (the
+// wave's base; lane i lands 16 i bytes further).
+__device__ __forceinline__ void lds_dma16_untracked_at(const void* gsrc, uint32_t lds_wave_base) {
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_wave_base);
+    uint32_t save;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(save)
+        : "v"(gsrc), "s"(m0)
+        : "memory");
+}
+// LDS byte address of a __shared__ object.
+template <typename V>
+__device__ __forceinline__ uint32_t lds_addr(V* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)p;
+}
 // s_waitcnt immediate that waits until at most k vector-memory operations of
 // the wave are outstanding (expcnt and lgkmcnt left unconstrained; gfx9
 // encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).

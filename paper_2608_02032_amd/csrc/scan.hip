@@ -29,6 +29,8 @@
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
 
+#include <type_traits>
+
 namespace dart {
 namespace {
 
@@ -102,7 +104,7 @@ template <typename T, int N, int S>
 __global__ __launch_bounds__(kThreads) void k_chunk_state(
     const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const T* __restrict__ Bm, T* __restrict__ mem, float* __restrict__ chunk_lda,
-    float* __restrict__ cs2, int64_t L, int H, int G, int64_t M, int64_t Mcap) {
+    float* __restrict__ aux, int64_t L, int H, int G, int64_t M, int64_t Mcap) {
     constexpr int XRB = kP * (int)sizeof(T);   // bytes per x row
     constexpr int BRB = N * (int)sizeof(T);    // bytes per B row
     constexpr int XT = kSB * XRB, BT = kSB * BRB;
@@ -212,11 +214,22 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
             consume(sb, u);
         }
     }
-    // outputs: the within-chunk cumulative decays (log2 units, for the output
-    // kernel), the chunk's total log decay, and dH: acc[nt][i] = dH[n = 16 nt +
+    // outputs: the chunk's per-token record for the output kernel (cumulative
+    // log decay cs in log2 units, dt (0 past the end), and the weight
+    // exp2(cs_e - cs_s) dt_s with e the last token of the s's 32-token block),
+    // the chunk's total log decay, and dH: acc[nt][i] = dH[n = 16 nt +
     // 4 (lane/16) + i][p = 16 wave + lane%16], each wave's N x 16 strip through
     // LDS (the ring) and out as 16-byte row stores
-    if (tid < S) cs2[((b * H + h) * M + c) * S + tid] = cs * kLog2e;
+    {
+        const float cs2 = cs * kLog2e;
+        const float cse2 = __shfl(cs2, lane | 31);
+        if (tid < S) {
+            float* rec = aux + ((b * H + h) * M + c) * 3 * S;
+            rec[tid] = cs2;
+            rec[S + tid] = dts;
+            rec[2 * S + tid] = fast_exp2(cse2 - cs2) * dts;
+        }
+    }
     if (tid == 0) chunk_lda[(b * H + h) * M + c] = cse;
     __syncthreads();
     T* st = reinterpret_cast<T*>(ring) + wave * N * 16;
@@ -335,7 +348,7 @@ __device__ __forceinline__ int tile_row(int w, int q, int nw) {
 template <typename T, int N, int S>
 __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
     const T* __restrict__ x, const float* __restrict__ dt, const T* __restrict__ Cm,
-    const T* __restrict__ states, const float* __restrict__ cs2, const float* __restrict__ gram,
+    const T* __restrict__ states, const float* __restrict__ aux, const float* __restrict__ gram,
     T* __restrict__ y, int64_t L, int H, int G, int64_t M, int64_t BM) {
     constexpr int NW = out_waves<S>();
     constexpr int NT = 64 * NW;
@@ -377,7 +390,7 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
                   XRB, N, N, wave, NW, lane);
     dma_tile<XRB>(xs, reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP),
                   (int64_t)H * XRB, S, len, wave, NW, lane);
-    const float* csc = cs2 + ((b * H + h) * M + c) * S;
+    const float* csc = aux + ((b * H + h) * M + c) * 3 * S;
     for (int i = tid; i < S; i += NT) {
         const float csi = csc[i];
         const float cse = csc[i | 31];
@@ -517,16 +530,305 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Chunk output for bf16, one workgroup per (b, chunk, group, slice of hpb
+// heads of the group).  The chunk's causal Gram pairs G^T[s][t] = B_s . C_t
+// depend on the group only: each wave forms those of its row tiles once (bf16
+// registers; the same nine pairs per wave for S = 256, the row tiles being
+// paired light with heavy as in k_chunk_out) and keeps them, with its C rows,
+// for every head of the slice.  Each head's inputs (x rows, H_[c-1] and the
+// chunk's per-token record cs, dt, exp2(cs_e - cs_s) dt_s) arrive by DMA in
+// one of two buffers, the next head's copy running under the current head's
+// MFMAs.  Per head:
+//   y = diag(exp2(cs_t)) (C H_[c-1])            inter-chunk term, the decay
+//                                               applied to the accumulator rows
+//     + sum over causal s blocks of (G o decay) (x)   intra-chunk term
+// with the decay factored over s blocks before the row tile as in k_chunk_out
+// and exact on the diagonal block.  A wave's two row tiles share every H and x
+// fragment they both use (one LDS read, two MFMAs), and the x fragments of
+// the next s block are read while the current one is multiplied.  The k
+// order of all operands is s (or n) = 16 u + 4 (lane/16) + i for element
+// 4 u + i, which makes the transposing reads of the H and x tiles
+// conflict-free.  Outputs go through a wave-private LDS strip (rows padded to
+// 144 bytes, so the 16-bit accumulator writes do not conflict) and leave as
+// 16-byte row stores.
+// ---------------------------------------------------------------------------
+template <int N, int S>
+__global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
+    const bf16* __restrict__ x, const bf16* __restrict__ Bm, const bf16* __restrict__ Cm,
+    const bf16* __restrict__ states, const float* __restrict__ aux, bf16* __restrict__ y,
+    int64_t L, int H, int G, int64_t M, int hpb, int64_t nbcg) {
+    using T = bf16;
+    constexpr int NW = out_waves<S>();
+    constexpr int NT = 64 * NW;
+    constexpr int KS = N / 32;
+    constexpr int NQ = S / 16 / NW;
+    constexpr int XRB = kP * 2;                   // bytes of an x, H or y row
+    constexpr int XT = S * XRB;                   // x rows of the chunk
+    constexpr int HT = N * XRB;                   // H_[c-1]
+    constexpr int AT = 3 * S * 4;                 // per-token record
+    constexpr int UB = XT + HT + AT;              // one head's inputs
+    constexpr int YRB = 144;                      // padded staging row
+    constexpr int MSK0 = ((NW - 1) >> 1) + 1;     // s blocks of row tile q = 0 (at most)
+    constexpr int MSK1 = ((2 * NW - 1) >> 1) + 1; // of row tile q = 1
+    constexpr int MSKL = NQ == 2 ? MSK1 : MSK0;   // s blocks of the wave (at most)
+    static_assert(NQ == 1 || NQ == 2, "one or two row tiles per wave");
+
+    // block -> (b, c, g, head slice); the slices of one (b, c, g) share an XCD
+    const int nhs = (H / G) / hpb;
+    const int64_t bid = blockIdx.x;
+    int64_t bcg;
+    int hs;
+    if (nbcg % 8 == 0) {
+        const int64_t slot = bid >> 3;
+        bcg = (slot / nhs) * 8 + (bid & 7);
+        hs = (int)(slot % nhs);
+    } else {
+        bcg = bid / nhs;
+        hs = (int)(bid % nhs);
+    }
+    const int g = (int)(bcg % G);
+    const int64_t bc = bcg / G;
+    const int64_t b = bc / M, c = bc % M;
+    const int hbase = g * (H / G) + hs * hpb;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t t0 = c * S;
+    const int len = (int)(L - t0 < S ? L - t0 : S);
+
+    __shared__ __attribute__((aligned(16))) char units[2 * UB];
+    __shared__ __attribute__((aligned(16))) char ystage[NW * NQ * 16 * YRB];
+
+    // Copies of one head's inputs into buffer u (LDS destinations as byte
+    // addresses): x and H_[c-1] into swizzled row tiles (rows past the end of
+    // a partial chunk re-read the last row), the record linearly.
+    const uint32_t units_lds = lds_addr(units);
+    auto issue_unit = [&](int hh, int u) __attribute__((always_inline)) {
+        const int h = hbase + hh;
+        const uint32_t ub = units_lds + (uint32_t)(u * UB);
+        auto tile = [&](uint32_t dst, const char* src, int64_t gstride, int rows, int rows_valid) {
+            using Tl = SwzTile<XRB>;
+            for (int q0 = wave * 64; q0 < rows * Tl::CPR; q0 += NT) {
+                const int q = q0 + lane;
+                if (q < rows * Tl::CPR) {
+                    const int r = q / Tl::CPR, ch = (q % Tl::CPR) ^ (r & Tl::MASK);
+                    const int rr = r < rows_valid ? r : rows_valid - 1;
+                    lds_dma16_untracked_at(src + rr * gstride + ch * 16, dst + (uint32_t)(q0 * 16));
+                }
+            }
+        };
+        tile(ub, reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP), (int64_t)H * XRB, S, len);
+        tile(ub + XT, reinterpret_cast<const char*>(states + ((b * M + c) * H + h) * (int64_t)N * kP),
+             XRB, N, N);
+        const char* ag = reinterpret_cast<const char*>(aux + ((b * H + h) * M + c) * 3 * S);
+        for (int q0 = wave * 64; q0 < AT / 16; q0 += NT) {
+            const int q = q0 + lane;
+            if (q < AT / 16) lds_dma16_untracked_at(ag + q * 16, ub + (uint32_t)(XT + HT + q0 * 16));
+        }
+    };
+    issue_unit(0, 0);
+
+    // the wave's row tiles and their C rows, in the k order above (rows past
+    // the end of a partial chunk read the last row: finite values, zero weight)
+    int rq[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) rq[q] = tile_row(wave, q, NW);
+    auto kfrag = [&](const bf16* row, int ks) __attribute__((always_inline)) {
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 4 * grp);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 16 + 4 * grp);
+        return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    };
+    bf16x8 craw[NQ][KS];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int t = rq[q] * 16 + col;
+        const bf16* crow = Cm + ((b * L + t0 + (t < len ? t : len - 1)) * G + g) * N;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) craw[q][ks] = kfrag(crow, ks);
+    }
+    // Gram pairs of the wave's row tiles: element 4 u + i of pair (q, sk) is
+    // G^T[s = 32 sk + 16 u + 4 grp + i][t = 16 r_q + col]
+    bf16x8 gq0[MSK0], gq1[MSK1];
+    auto gram_pair = [&](int q, int sk) __attribute__((always_inline)) {
+        f32x4 acc[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int sr = sk * 32 + u * 16 + col;
+            const bf16* brow = Bm + ((b * L + t0 + (sr < len ? sr : len - 1)) * G + g) * N;
+            acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) acc[u] = mma16(acc[u], kfrag(brow, ks), craw[q][ks]);
+        }
+        const float v[8] = {acc[0][0], acc[0][1], acc[0][2], acc[0][3],
+                            acc[1][0], acc[1][1], acc[1][2], acc[1][3]};
+        return make_frag<T>(v);
+    };
+#pragma unroll
+    for (int sk = 0; sk < MSK0; ++sk)
+        if (sk <= (rq[0] >> 1)) gq0[sk] = gram_pair(0, sk);
+    if constexpr (NQ == 2) {
+#pragma unroll
+        for (int sk = 0; sk < MSK1; ++sk)
+            if (sk <= (rq[NQ - 1] >> 1)) gq1[sk] = gram_pair(NQ - 1, sk);
+    }
+
+    // transposing fragment reads at offsets fixed here: rows (k) 4 grp + i and
+    // 16 + 4 grp + i of a 32-row block, column tile pt
+    KmOffBf16<XRB> ko[4];
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) ko[pt].init(4 * grp, 16 + 4 * grp, pt * 16, lane);
+
+    auto head = [&](int h, const char* ub) __attribute__((always_inline)) {
+        // per-lane indices are recomputed for every head (the empty asm keeps
+        // the compiler from hoisting the diagonal masks and offsets derived
+        // from them out of the head loop, where they would not fit)
+        int lc = col, lg = grp;
+        asm volatile("" : "+v"(lc), "+v"(lg));
+        const char* xt = ub;
+        const char* ht = ub + XT;
+        const float* rc = reinterpret_cast<const float*>(ub + XT + HT);  // cs | dt | weight
+        f32x4 yacc[NQ][4];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // inter-chunk term, each H fragment shared by the row tiles
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) {
+                const bf16x8 hf = ko[pt].read(ht, ks * 32 * XRB);
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) yacc[q][pt] = mma16(yacc[q][pt], craw[q][ks], hf);
+            }
+        // accumulator rows t = 16 r + 4 grp + i take exp2(cs_t)
+        float cst[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const f32x4 csr = *reinterpret_cast<const f32x4*>(rc + rq[q] * 16 + 4 * lg);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float e = fast_exp2(csr[i]);
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) yacc[q][pt][i] *= e;
+            }
+            cst[q] = rc[rq[q] * 16 + lc];
+        }
+        // intra-chunk term over the s blocks of the heavier row tile
+        const int skmax = rq[NQ - 1] >> 1;
+        bf16x8 xf[2][4];
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) xf[0][pt] = ko[pt].read(xt, 0);
+#pragma unroll
+        for (int sk = 0; sk < MSKL; ++sk) {
+            if (sk > skmax) break;
+            const int cur = sk & 1;
+            const int sbase = sk * 32;
+            if (sk + 1 <= skmax) {
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) xf[cur ^ 1][pt] = ko[pt].read(xt, (sbase + 32) * XRB);
+            }
+            const f32x4 b0 = *reinterpret_cast<const f32x4*>(rc + 2 * S + sbase + 4 * lg);
+            const f32x4 b1 = *reinterpret_cast<const f32x4*>(rc + 2 * S + sbase + 16 + 4 * lg);
+            const float cse = rc[sbase + 31];
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const int rs = rq[q] >> 1;
+                if (sk > rs) continue;
+                // (q, sk) are constants once the loops are unrolled; q = 0
+                // never reaches sk >= MSK0
+                bf16x8 gv = q == 0 ? gq0[sk < MSK0 ? sk : MSK0 - 1] : gq1[sk < MSK1 ? sk : MSK1 - 1];
+                asm volatile("" : "+v"(gv));  // widened per head, not kept widened
+                float mv[8];
+                if (sk < rs) {
+                    const float a = fast_exp2(cst[q] - cse);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        mv[i] = to_f(gv[i]) * (a * b0[i]);
+                        mv[4 + i] = to_f(gv[4 + i]) * (a * b1[i]);
+                    }
+                } else {
+                    const int t = rq[q] * 16 + lc;
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const f32x4 css = *reinterpret_cast<const f32x4*>(rc + sbase + 16 * u + 4 * lg);
+                        const f32x4 dts = *reinterpret_cast<const f32x4*>(rc + S + sbase + 16 * u + 4 * lg);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int sidx = sbase + 16 * u + 4 * lg + i;
+                            mv[4 * u + i] = (sidx <= t) ? to_f(gv[4 * u + i]) * fast_exp2(cst[q] - css[i]) * dts[i]
+                                                        : 0.f;
+                        }
+                    }
+                }
+                const bf16x8 fm = make_frag<T>(mv);
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = mma16(yacc[q][pt], fm, xf[cur][pt]);
+            }
+        }
+        // yacc[q][pt][i] = y[t = 16 r_q + 4 grp + i][p = 16 pt + col] -> staging strip
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int r = rq[q];
+            char* st = ystage + (wave * NQ + q) * 16 * YRB;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt)
+                    *reinterpret_cast<T*>(st + (4 * lg + i) * YRB + (pt * 16 + lc) * 2) = from_f<T>(yacc[q][pt][i]);
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int e = lane + 64 * k;
+                const int row = e >> 3, ch = e & 7;
+                const uint4 v = *reinterpret_cast<const uint4*>(st + row * YRB + ch * 16);
+                if (r * 16 + row < len)
+                    *reinterpret_cast<uint4*>(y + ((b * L + t0 + r * 16 + row) * H + h) * kP + ch * 8) = v;
+            }
+        }
+    };
+
+    for (int hh = 0; hh < hpb; ++hh) {
+        // this wave's copies of head hh are in: only the y stores of head
+        // hh - 1 were issued after them (vector memory operations complete in
+        // order); a partial chunk, whose stores are predicated, waits for all
+        if (hh == 0 || len < S) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        } else {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NQ));
+        }
+        lds_barrier();  // every wave's copies are in; head hh - 1 is done with its buffer
+        if (hh + 1 < hpb) issue_unit(hh + 1, (hh + 1) & 1);
+        head(hbase + hh, units + (hh & 1) * UB);
+    }
+}
+
 // Workspace carve-up of the scan: per-chunk log decay [B][H][M], chunk-entry
-// states [B][M][H][N][P] (storage dtype), within-chunk cumulative log decay
-// [B][H][M][S] and the causal Gram tiles [B][G][M][pairs][64][8] (float).
+// states [B][M][H][N][P] (storage dtype), the per-token record (cs, dt,
+// weight) [B][H][M][3][S] and, for fp32 only, the causal Gram tiles
+// [B][G][M][pairs][64][8] (float).
 struct ScanWs {
     float* lda;
     char* states;
-    float* cs2;
+    float* aux;
     float* gram;
     size_t total;
 };
+
+// Heads per workgroup of k_chunk_out_heads: the largest divisor of the heads
+// of a group that still gives every compute unit a workgroup.
+int out_heads_per_block(int64_t nbcg, int hg) {
+    static int cus = [] {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        return n;
+    }();
+    for (int hpb = hg; hpb > 1; --hpb)
+        if (hg % hpb == 0 && nbcg * (hg / hpb) >= cus) return hpb;
+    return 1;
+}
 ScanWs scan_ws(const Shape& s, void* ws) {
     char* p = reinterpret_cast<char*>(ws);
     ScanWs w;
@@ -535,10 +837,10 @@ ScanWs scan_ws(const Shape& s, void* ws) {
     off += align256(sizeof(float) * s.B * s.H * s.M);
     w.states = p + off;
     off += align256(elem_bytes(s.dtype) * s.B * s.M * s.H * (size_t)s.N * s.P);
-    w.cs2 = reinterpret_cast<float*>(p + off);
-    off += align256(sizeof(float) * s.B * s.H * s.M * (size_t)s.S);
+    w.aux = reinterpret_cast<float*>(p + off);
+    off += align256(sizeof(float) * s.B * s.H * s.M * 3 * (size_t)s.S);
     w.gram = reinterpret_cast<float*>(p + off);
-    off += align256(sizeof(float) * s.B * s.G * s.M * (size_t)gram_pairs(s.S) * 512);
+    if (s.dtype != 1) off += align256(sizeof(float) * s.B * s.G * s.M * (size_t)gram_pairs(s.S) * 512);
     w.total = off;
     return w;
 }
@@ -552,21 +854,31 @@ hipError_t run_scan(const Shape& s, const void* x, const float* dt, const float*
     const dim3 grid((unsigned)s.M, (unsigned)s.H, (unsigned)s.B);
     prof_begin("k_chunk_state", st);
     k_chunk_state<T, N, S><<<grid, kThreads, 0, st>>>(
-        (const T*)x, dt, A, (const T*)Bm, (T*)mem, w.lda, w.cs2, s.L, s.H, s.G, s.M, s.Mcap);
+        (const T*)x, dt, A, (const T*)Bm, (T*)mem, w.lda, w.aux, s.L, s.H, s.G, s.M, s.Mcap);
     prof_end(st);
-    prof_begin("k_chunk_gram", st);
-    k_chunk_gram<T, N, S><<<dim3((unsigned)(S / 64), (unsigned)s.M, (unsigned)(s.B * s.G)), kThreads,
-                            0, st>>>((const T*)Bm, (const T*)Cm, w.gram, s.L, s.G, s.M);
-    prof_end(st);
+    if constexpr (sizeof(T) == 4) {
+        prof_begin("k_chunk_gram", st);
+        k_chunk_gram<T, N, S><<<dim3((unsigned)(S / 64), (unsigned)s.M, (unsigned)(s.B * s.G)),
+                                kThreads, 0, st>>>((const T*)Bm, (const T*)Cm, w.gram, s.L, s.G, s.M);
+        prof_end(st);
+    }
     const int NP = N * kP;
     prof_begin("k_state_pass", st);
     k_state_pass<T><<<dim3((unsigned)(NP / (kThreads * 4)), (unsigned)s.H, (unsigned)s.B), kThreads,
                       0, st>>>((const T*)mem, w.lda, h0, states, h_last, s.H, NP, s.M, s.Mcap);
     prof_end(st);
     prof_begin("k_chunk_out", st);
-    k_chunk_out<T, N, S><<<dim3((unsigned)(s.B * s.M * s.H)), 64 * out_waves<S>(), 0, st>>>(
-        (const T*)x, dt, (const T*)Cm, states, w.cs2, w.gram, (T*)y_ssd, s.L, s.H, s.G, s.M,
-        s.B * s.M);
+    if constexpr (sizeof(T) == 2) {
+        const int64_t nbcg = s.B * s.M * s.G;
+        const int hpb = out_heads_per_block(nbcg, s.H / s.G);
+        k_chunk_out_heads<N, S><<<dim3((unsigned)(nbcg * (s.H / s.G / hpb))), 64 * out_waves<S>(), 0,
+                                  st>>>((const bf16*)x, (const bf16*)Bm, (const bf16*)Cm, states,
+                                        w.aux, (bf16*)y_ssd, s.L, s.H, s.G, s.M, hpb, nbcg);
+    } else {
+        k_chunk_out<T, N, S><<<dim3((unsigned)(s.B * s.M * s.H)), 64 * out_waves<S>(), 0, st>>>(
+            (const T*)x, dt, (const T*)Cm, states, w.aux, w.gram, (T*)y_ssd, s.L, s.H, s.G, s.M,
+            s.B * s.M);
+    }
     prof_end(st);
     return hipGetLastError();
 }

@@ -63,10 +63,14 @@ def test_workspace_sizes(lib):
     d = dims()
     M = 512 // 64
     ws = lib.dart_scan_workspace_bytes(ctypes.byref(d))
-    # chunk log-decays, chunk-entry states (storage dtype), within-chunk log
-    # decays and the causal Gram tiles (float; one set per group)
+    # chunk log-decays, chunk-entry states (storage dtype) and the per-token
+    # record (cumulative log decay, dt, weight); fp32 adds the causal Gram
+    # tiles (float; one set per group)
+    assert ws >= 4 * 2 * 4 * M + 2 * 2 * M * 4 * 64 * 64 + 4 * 2 * 4 * M * 3 * 64
     pairs = (64 // 32) * (64 // 32 + 1)
-    assert ws >= 4 * 2 * 4 * M + 2 * 2 * M * 4 * 64 * 64 + 4 * 2 * 4 * M * 64 + 4 * 2 * 1 * M * pairs * 512
+    ws32 = lib.dart_scan_workspace_bytes(ctypes.byref(dims(dtype="fp32")))
+    assert ws32 >= (4 * 2 * 4 * M + 4 * 2 * M * 4 * 64 * 64 + 4 * 2 * 4 * M * 3 * 64
+                    + 4 * 2 * 1 * M * pairs * 512)
     # the SMA forward keeps the key side r (.) dH of every attended memory
     sma = lib.dart_sma_workspace_bytes(ctypes.byref(d))
     assert sma >= 2 * 2 * (M - 1) * 4 * 64 * 64

@@ -35,6 +35,10 @@ SCAN_CASES = [
     synth.Workload("bf16_L1024_N128_S256", 2, 1024, 4, 64, 128, 256, "bf16"),
     synth.Workload("bf16_L600_N64_S128", 1, 600, 3, 64, 64, 128, "bf16"),
     synth.Workload("bf16_L320_N32_S64", 2, 320, 2, 64, 32, 64, "bf16"),
+    # several heads per output workgroup (two-buffer head loop), full and ragged
+    synth.Workload("bf16_L4096_H32_N128_S256", 1, 4096, 32, 64, 128, 256, "bf16"),
+    synth.Workload("bf16_L4000_H32_N128_S256", 1, 4000, 32, 64, 128, 256, "bf16"),
+    synth.Workload("bf16_L600_H8_G2_N128_S128", 1, 600, 8, 64, 128, 128, "bf16", ngroups=2),
 ]
 
 
@@ -189,6 +193,49 @@ def test_scan_and_sma_are_deterministic():
         outs.append([t.cpu() for t in (y_ssd, mem, hl, y, lse)])
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+def test_full_size_forward_sampled():
+    """The benchmark workload (batch 4, L 8192, 32 heads, N 128, S 256, bf16) in
+    the launch configuration the benchmark times: the scan outputs of sampled
+    (b, h) slices against the oracle run on those slices, and SMA rows sampled
+    across the sequence against the SMA definition on the GPU's own memories."""
+    import torch
+    w = synth.WORKLOADS["sweep_L8192_S256_N128"]
+    announce("full size sampled %s" % (w,))
+    d = synth.forward_inputs(w, seed=21)
+    y_ssd, mem, hl = run_scan(w, d)
+    q, e, Cm, z = (to_dev(d[k], w.dtype) for k in ("q", "e", "Cm", "z"))
+    y, lse = dart.sma_fwd(q, e, Cm, mem, z, y_ssd, w.chunk)
+    torch.cuda.synchronize()
+    tol = TOL[w.dtype]
+    S, L = w.chunk, w.seqlen
+    rng = np.random.default_rng(22)
+    for b, h in [(0, 0), (1, 13), (3, 31)]:
+        xs = d["x"][b:b + 1, :, h:h + 1]
+        dts = d["dt"][b:b + 1, :, h:h + 1]
+        As = d["A"][h:h + 1]
+        Bs, Cs = d["Bm"][b:b + 1], d["Cm"][b:b + 1]
+        y_ref, hl_ref = oracle.ssd_recurrence(xs, dts, As, Bs, Cs)
+        mem_ref = oracle.chunk_memories(xs, dts, As, Bs, S)
+        what = "(b=%d, h=%d)" % (b, h)
+        assert_close_slices(to_np(y_ssd[b:b + 1, :, h:h + 1]), y_ref, tol, what="y_ssd " + what)
+        assert_close_slices(to_np(mem[b:b + 1, :, h:h + 1]), mem_ref, tol, axes_keep=(0, 1, 2),
+                            what="mem " + what)
+        assert_close_slices(to_np(hl[b:b + 1, h:h + 1]), hl_ref, tol, axes_keep=(0, 1),
+                            what="h_last " + what)
+        # SMA rows: first and last token of some chunks and random tokens
+        ts = np.unique(np.concatenate([[0, S - 1, S, 2 * S - 1, L - S, L - 1],
+                                       rng.integers(0, L, 10)]))
+        rows = np.stack([np.zeros_like(ts), ts, np.zeros_like(ts)], axis=1)
+        yr, lr = oracle.sma_rows(d["q"][b:b + 1], d["e"][b:b + 1], d["Cm"][b:b + 1],
+                                 to_np(mem[b:b + 1, :, h:h + 1]), d["z"][b:b + 1, :, h:h + 1],
+                                 to_np(y_ssd[b:b + 1, :, h:h + 1]), S, rows)
+        ti = torch.as_tensor(ts, device=y.device)
+        got_y = to_np(y[b, :, h][ti])
+        got_l = to_np(lse[b, :, h][ti])
+        assert_close_slices(got_y[None], yr[None], tol, axes_keep=(0,), what="y rows " + what)
+        assert_lse_close(got_l[None], lr[None], tol, what="lse rows " + what, axes_keep=(0,))
 
 
 # --------------------------------------------------------------------------- #
