@@ -247,6 +247,225 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
 }
 
 // ---------------------------------------------------------------------------
+// Chunk-state contraction for bf16, one workgroup per (b, chunk, group, slice
+// of hpb heads of the group): the chunk's B rows depend on the group only, so
+// each wave reads its B^T operand fragments once (staged through LDS) and
+// keeps them in registers for every head of the slice.  The prologue also
+// copies the dt of every head of the slice and forms all their within-chunk
+// decays at once (wave w takes heads w, w + 8, ...; a wave-level scan of dt A):
+// the contraction weights exp(cs_e - cs_s) dt_s stay in LDS (over the B rows,
+// no longer needed), the per-token record and the total log decay go to the
+// workspace.  Per head, the x rows arrive by DMA in one of two buffers while
+// the previous head computes.  Wave w owns n tiles NTW (w % NG) .. and p tiles
+// PTW (w / NG) .. of the N x P result; each x fragment is scaled by the
+// weights of its tokens before the MFMAs.  The result leaves through a
+// wave-private LDS strip (rows padded to PTW 32 + 16 bytes) as 16-byte pieces.
+// ---------------------------------------------------------------------------
+template <int N, int S>
+__global__ __launch_bounds__(512) void k_chunk_state_heads(
+    const bf16* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
+    const bf16* __restrict__ Bm, bf16* __restrict__ mem, float* __restrict__ chunk_lda,
+    float* __restrict__ aux, int64_t L, int H, int G, int64_t M, int64_t Mcap, int hpb,
+    int64_t nbcg) {
+    using T = bf16;
+    constexpr int NW = 8, NT = 64 * NW;
+    constexpr int XRB = kP * 2;                 // bytes per x row
+    constexpr int BRB = N * 2;                  // bytes per B row
+    constexpr int XT = S * XRB, BT = S * BRB;
+    constexpr int KST = S / 32;                 // 32-token k steps
+    constexpr int NTW = N >= 128 ? N / 64 : 1;  // n tiles per wave
+    constexpr int PTW = (N / 32) / NTW;         // p tiles per wave
+    constexpr int NG = (N / 16) / NTW;          // n-tile groups
+    static_assert(NG * (4 / PTW) == NW, "tiles cover the waves");
+    constexpr int SRB = PTW * 32 + 16;          // padded staging row (bytes)
+    constexpr int SROWS = NTW * 16;
+    constexpr int TPL = S / 64;                 // tokens per lane in a decay scan
+    constexpr int LPB = 32 / TPL;               // lanes per 32-token block
+
+    const int nhs = (H / G) / hpb;
+    const int64_t bid = blockIdx.x;
+    int64_t bcg;
+    int hs;
+    if (nbcg % 8 == 0) {
+        const int64_t slot = bid >> 3;
+        bcg = (slot / nhs) * 8 + (bid & 7);
+        hs = (int)(slot % nhs);
+    } else {
+        bcg = bid / nhs;
+        hs = (int)(bid % nhs);
+    }
+    const int g = (int)(bcg % G);
+    const int64_t bc = bcg / G;
+    const int64_t b = bc / M, c = bc % M;
+    const int hbase = g * (H / G) + hs * hpb;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = lane >> 4, col = lane & 15;
+    const int64_t t0 = c * S;
+    const int len = (int)(L - t0 < S ? L - t0 : S);
+    const int ng = wave % NG, pg = wave / NG;
+
+    // bt: the B rows, then (after the fragments are read) the weights of
+    // every head [hpb][S] fp32; xbuf[1] holds the heads' dt until the first
+    // head loop copy
+    __shared__ __attribute__((aligned(16))) char bt[BT];
+    __shared__ __attribute__((aligned(16))) char xbuf[2][XT];
+    __shared__ __attribute__((aligned(16))) char ystage[NW * SROWS * SRB];
+    float* const wall = reinterpret_cast<float*>(bt);
+    const float* const dtall = reinterpret_cast<const float*>(&xbuf[1][0]);
+    const uint32_t bt_lds = lds_addr(bt), x_lds = lds_addr(xbuf);
+
+    // copies into swizzled row tiles (rows past the end re-read the last row)
+    auto tile = [&](uint32_t dst, const char* src, int64_t gstride, int rows, int rows_valid, auto rbc)
+        __attribute__((always_inline)) {
+        constexpr int RB = decltype(rbc)::value;
+        using Tl = SwzTile<RB>;
+        for (int q0 = wave * 64; q0 < rows * Tl::CPR; q0 += NT) {
+            const int q = q0 + lane;
+            if (q < rows * Tl::CPR) {
+                const int r = q / Tl::CPR, ch = (q % Tl::CPR) ^ (r & Tl::MASK);
+                const int rr = r < rows_valid ? r : rows_valid - 1;
+                lds_dma16_untracked_at(src + rr * gstride + ch * 16, dst + (uint32_t)(q0 * 16));
+            }
+        }
+    };
+    auto issue_x = [&](int hh, int u) __attribute__((always_inline)) {
+        tile(x_lds + (uint32_t)(u * XT), reinterpret_cast<const char*>(x + ((b * L + t0) * H + hbase + hh) * kP),
+             (int64_t)H * XRB, S, len, std::integral_constant<int, XRB>{});
+    };
+
+    // prologue copies: B rows, head 0's x rows, every head's dt (one 4-byte
+    // copy per token; head hd by wave hd % 8)
+    tile(bt_lds, reinterpret_cast<const char*>(Bm + ((b * L + t0) * G + g) * N), (int64_t)G * BRB, S, len,
+         std::integral_constant<int, BRB>{});
+    issue_x(0, 0);
+    for (int hd = wave; hd < hpb; hd += NW) {
+#pragma unroll
+        for (int k = 0; k < TPL; ++k) {
+            const int tok = k * 64 + lane;
+            const int tc = tok < len ? tok : len - 1;
+            const uint32_t m0 = x_lds + (uint32_t)(XT + (hd * S + k * 64) * 4);
+            const float* src = dt + (b * L + t0 + tc) * H + hbase + hd;
+            uint32_t save;
+            asm volatile(
+                "s_mov_b32 %0, m0\n\t"
+                "s_mov_b32 m0, %2\n\t"
+                "s_nop 0\n\t"
+                "global_load_lds_dword %1, off\n\t"
+                "s_mov_b32 m0, %0"
+                : "=&s"(save)
+                : "v"(src), "s"((uint32_t)__builtin_amdgcn_readfirstlane((int)m0))
+                : "memory");
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
+    bf16x8 bfr[NTW][KST];
+    {
+        KmOffBf16<BRB> bo;
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+            bo.init(8 * grp, 8 * grp + 4, (ng * NTW + j) * 16, lane);
+#pragma unroll
+            for (int ks = 0; ks < KST; ++ks) bfr[j][ks] = bo.read(bt, ks * 32 * BRB);
+        }
+    }
+    lds_barrier();  // every wave holds its B^T fragments: bt takes the weights
+    // decays of head hd, lane l holding tokens TPL l .. TPL l + TPL - 1
+    for (int hd = wave; hd < hpb; hd += NW) {
+        const int h = hbase + hd;
+        const float a = A[h];
+        float dv[TPL], cs[TPL];
+        float run = 0.f;
+#pragma unroll
+        for (int k = 0; k < TPL; ++k) {
+            const int tok = TPL * lane + k;
+            dv[k] = tok < len ? dtall[hd * S + tok] : 0.f;
+            run += dv[k] * a;
+            cs[k] = run;
+        }
+        float incl = run;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const float t = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += t;
+        }
+        const float excl = incl - run;
+#pragma unroll
+        for (int k = 0; k < TPL; ++k) cs[k] += excl;
+        const float cse = __shfl(cs[TPL - 1], 63, 64);                // chunk end
+        const float cbe = __shfl(cs[TPL - 1], lane | (LPB - 1), 64);  // 32-token block end
+        float* rec = aux + ((b * H + h) * M + c) * 3 * S;
+#pragma unroll
+        for (int k = 0; k < TPL; ++k) {
+            const float cs2 = cs[k] * kLog2e;
+            wall[hd * S + TPL * lane + k] = __expf(cse - cs[k]) * dv[k];
+            rec[TPL * lane + k] = cs2;
+            rec[S + TPL * lane + k] = dv[k];
+            rec[2 * S + TPL * lane + k] = fast_exp2(cbe * kLog2e - cs2) * dv[k];
+        }
+        if (lane == 0) chunk_lda[(b * H + h) * M + c] = cse;
+    }
+    KmOffBf16<XRB> xo[PTW];
+#pragma unroll
+    for (int j = 0; j < PTW; ++j) xo[j].init(8 * grp, 8 * grp + 4, (pg * PTW + j) * 16, lane);
+    constexpr int CPRW = PTW * 2;                               // 16-byte pieces per staged row
+    constexpr int NSTW = (SROWS * CPRW + 63) / 64;              // 16-byte stores per wave and head
+
+    for (int hh = 0; hh < hpb; ++hh) {
+        const int u = hh & 1;
+        // this wave's copies of head hh are in: only its dH stores of head
+        // hh - 1 came after them (head 0's were waited for in the prologue)
+        if (hh > 0) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NSTW));
+        lds_barrier();  // copies of head hh and all weights visible; buffer u ^ 1 is free
+        if (hh + 1 < hpb) issue_x(hh + 1, u ^ 1);
+        const float* wv = wall + hh * S;
+        f32x4 acc[NTW][PTW];
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+            for (int k = 0; k < PTW; ++k) acc[j][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KST; ++ks) {
+            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp);
+            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp + 4);
+#pragma unroll
+            for (int k = 0; k < PTW; ++k) {
+                const bf16x8 xr = xo[k].read(&xbuf[u][0], ks * 32 * XRB);
+                float v[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    v[i] = to_f(xr[i]) * w0[i];
+                    v[4 + i] = to_f(xr[4 + i]) * w1[i];
+                }
+                const bf16x8 xf = make_frag<T>(v);
+#pragma unroll
+                for (int j = 0; j < NTW; ++j) acc[j][k] = mma16(acc[j][k], bfr[j][ks], xf);
+            }
+        }
+        // acc[j][k][i] = dH[n = 16 (ng NTW + j) + 4 grp + i][p = 16 (pg PTW + k) + col]
+        char* st = ystage + wave * SROWS * SRB;
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+            for (int k = 0; k < PTW; ++k)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    *reinterpret_cast<T*>(st + (16 * j + 4 * grp + i) * SRB + (16 * k + col) * 2) = from_f<T>(acc[j][k][i]);
+        T* dst = mem + ((b * Mcap + c) * H + hbase + hh) * (int64_t)N * kP + (ng * NTW * 16) * kP + pg * PTW * 16;
+#pragma unroll
+        for (int e0 = 0; e0 < SROWS * CPRW; e0 += 64) {
+            const int e = e0 + lane;
+            if (e < SROWS * CPRW) {
+                const int row = e / CPRW, ch = e % CPRW;
+                const uint4 v = *reinterpret_cast<const uint4*>(st + row * SRB + ch * 16);
+                *reinterpret_cast<uint4*>(dst + row * kP + ch * 8) = v;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Inter-chunk state passing: H_[c] = exp(cs_e(c)) H_[c-1] + dH_[c].
 // states[b][c][h] receives the state entering chunk c (H_[c-1]; h0 for c=0).
 // ---------------------------------------------------------------------------
@@ -815,9 +1034,10 @@ struct ScanWs {
     size_t total;
 };
 
-// Heads per workgroup of k_chunk_out_heads: the largest divisor of the heads
-// of a group that still gives every compute unit a workgroup.
-int out_heads_per_block(int64_t nbcg, int hg) {
+// Heads per workgroup of the bf16 scan kernels: the largest divisor of the
+// heads of a group, at most hmax, that still gives every compute unit a
+// workgroup.
+int out_heads_per_block(int64_t nbcg, int hg, int hmax) {
     static int cus = [] {
         int dev = 0, n = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
@@ -825,7 +1045,7 @@ int out_heads_per_block(int64_t nbcg, int hg) {
             n = 256;
         return n;
     }();
-    for (int hpb = hg; hpb > 1; --hpb)
+    for (int hpb = hg < hmax ? hg : hmax; hpb > 1; --hpb)
         if (hg % hpb == 0 && nbcg * (hg / hpb) >= cus) return hpb;
     return 1;
 }
@@ -851,10 +1071,19 @@ hipError_t run_scan(const Shape& s, const void* x, const float* dt, const float*
                     void* ws, hipStream_t st) {
     const ScanWs w = scan_ws(s, ws);
     T* states = reinterpret_cast<T*>(w.states);
-    const dim3 grid((unsigned)s.M, (unsigned)s.H, (unsigned)s.B);
+    const int64_t nbcg = s.B * s.M * s.G;
+    // the chunk-state workgroup keeps every head's dt (S floats) in one x
+    // buffer and every head's weights in the B tile: at most 32 and N / 2 heads
+    const int hpb = out_heads_per_block(nbcg, s.H / s.G, N / 2 < 32 ? N / 2 : 32);
     prof_begin("k_chunk_state", st);
-    k_chunk_state<T, N, S><<<grid, kThreads, 0, st>>>(
-        (const T*)x, dt, A, (const T*)Bm, (T*)mem, w.lda, w.aux, s.L, s.H, s.G, s.M, s.Mcap);
+    if constexpr (sizeof(T) == 2) {
+        k_chunk_state_heads<N, S><<<dim3((unsigned)(nbcg * (s.H / s.G / hpb))), 512, 0, st>>>(
+            (const bf16*)x, dt, A, (const bf16*)Bm, (bf16*)mem, w.lda, w.aux, s.L, s.H, s.G, s.M,
+            s.Mcap, hpb, nbcg);
+    } else {
+        k_chunk_state<T, N, S><<<dim3((unsigned)s.M, (unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
+            (const T*)x, dt, A, (const T*)Bm, (T*)mem, w.lda, w.aux, s.L, s.H, s.G, s.M, s.Mcap);
+    }
     prof_end(st);
     if constexpr (sizeof(T) == 4) {
         prof_begin("k_chunk_gram", st);
@@ -869,8 +1098,6 @@ hipError_t run_scan(const Shape& s, const void* x, const float* dt, const float*
     prof_end(st);
     prof_begin("k_chunk_out", st);
     if constexpr (sizeof(T) == 2) {
-        const int64_t nbcg = s.B * s.M * s.G;
-        const int hpb = out_heads_per_block(nbcg, s.H / s.G);
         k_chunk_out_heads<N, S><<<dim3((unsigned)(nbcg * (s.H / s.G / hpb))), 64 * out_waves<S>(), 0,
                                   st>>>((const bf16*)x, (const bf16*)Bm, (const bf16*)Cm, states,
                                         w.aux, (bf16*)y_ssd, s.L, s.H, s.G, s.M, hpb, nbcg);
