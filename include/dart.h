@@ -183,6 +183,50 @@ dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, i
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The decode step for a ragged batch: row b of the batch is at its own
+ * 0-based position pos[b] and runs steps 1-6 of dart_decode_step at that
+ * position (reset, append and the number m_b = floor(pos[b]/S) of memories it
+ * attends all follow pos[b]).  Sec. 4 ("Inference Cache") keeps one cache per
+ * sequence; a batch of sequences of different lengths shares these buffers.
+ *
+ *   pos      [B] int64, device, in: the rows' positions
+ *   pos_max  host: an upper bound of pos[] that sizes the launch; rows with
+ *            pos[b] < 0 or pos[b] > pos_max take no part in the step (their
+ *            state, cache and y are left as they are)
+ *   other arguments, layouts and the workspace as in dart_decode_step.
+ * Errors: DART_ERR_INVALID_ARG if pos_max < 0 or pos_max >= S * Mcap (some
+ * row could then need a memory slot the cache does not have).
+ */
+dart_status dart_decode_step_ragged(const dart_dims* dims, const dart_sma_opts* opts,
+                                    const int64_t* pos, int64_t pos_max, const void* x,
+                                    const float* dt, const float* A, const void* Bm,
+                                    const void* Cm, const void* q, const void* e, const void* z,
+                                    float* h_state, float* chunk_acc, void* mem_cache, void* y,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Prefill -> decode handoff.  After dart_ssd_chunk_scan over a batch padded to
+ * a common length with dt = 0 on each row's padding (decay 1 and no input, so
+ * the state, h_last and every memory equal those of the row's own prefix),
+ * the decode state of row b for its next position L_b = lengths[b]:
+ *   h_state[b]   = h_last[b];
+ *   chunk_acc[b] = mem[b][floor(L_b/S)] (the running contribution of the
+ *                  partial chunk, as stored) if L_b % S != 0, else 0.
+ * mem is the scan's memory output written with capacity dims->mem_capacity,
+ * which then serves as the decode cache as is (slots below floor(L_b/S) hold
+ * the row's completed chunks).  Rows with lengths[b] < 0 are left untouched.
+ * The caller keeps ceil(L_b/S) <= mem_capacity.
+ *
+ *   lengths  [B] int64, device, in
+ *   mem      [B][Mcap][H][N][P] storage dtype, in
+ *   h_last   [B][H][N][P] float, in
+ *   h_state, chunk_acc [B][H][N][P] float, out
+ */
+dart_status dart_decode_handoff(const dart_dims* dims, const int64_t* lengths, const void* mem,
+                                const float* h_last, float* h_state, float* chunk_acc,
+                                void* stream);
+
+/*
  * Element count of the length-dependent decode cache for a context of
  * `context` tokens: B * ceil(context/S) * H * N * P chunk-memory elements
  * (Sec. 4 "Inference Cache": O(M N P) per head).  The matched token-attention

@@ -202,9 +202,67 @@ dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, i
     if (workspace_bytes < need)
         return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
     dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
-    return hip_status(dart::launch_decode(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc,
-                                          mem_cache, y, workspace, (hipStream_t)stream),
+    return hip_status(dart::launch_decode(s, a, pos, nullptr, x, dt, A, Bm, Cm, q, e, z, h_state,
+                                          chunk_acc, mem_cache, y, workspace, (hipStream_t)stream),
                       "dart_decode_step launch");
+}
+
+dart_status dart_decode_step_ragged(const dart_dims* dims, const dart_sma_opts* opts,
+                                    const int64_t* pos, int64_t pos_max, const void* x,
+                                    const float* dt, const float* A, const void* Bm,
+                                    const void* Cm, const void* q, const void* e, const void* z,
+                                    float* h_state, float* chunk_acc, void* mem_cache, void* y,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, false, s);
+    if (st != DART_OK) return st;
+    st = check_opts(opts);
+    if (st != DART_OK) return st;
+    if (s.Mcap < 1) return fail(DART_ERR_INVALID_ARG, "decode needs mem_capacity >= 1");
+    if (pos_max < 0)
+        return fail(DART_ERR_INVALID_ARG, "pos_max must be >= 0 (got %lld)", (long long)pos_max);
+    if (pos_max >= s.Mcap * s.S)
+        return fail(DART_ERR_INVALID_ARG,
+                    "pos_max %lld needs more than the %lld memories the cache holds",
+                    (long long)pos_max, (long long)s.Mcap);
+    REQUIRE_PTR(pos);
+    REQUIRE_PTR(x);
+    REQUIRE_PTR(dt);
+    REQUIRE_PTR(A);
+    REQUIRE_PTR(Bm);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(q);
+    REQUIRE_PTR(e);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(h_state);
+    REQUIRE_PTR(chunk_acc);
+    REQUIRE_PTR(mem_cache);
+    REQUIRE_PTR(y);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::decode_workspace_bytes(s);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
+    return hip_status(dart::launch_decode(s, a, pos_max, pos, x, dt, A, Bm, Cm, q, e, z, h_state,
+                                          chunk_acc, mem_cache, y, workspace, (hipStream_t)stream),
+                      "dart_decode_step_ragged launch");
+}
+
+dart_status dart_decode_handoff(const dart_dims* dims, const int64_t* lengths, const void* mem,
+                                const float* h_last, float* h_state, float* chunk_acc,
+                                void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, false, s);
+    if (st != DART_OK) return st;
+    if (s.Mcap < 1) return fail(DART_ERR_INVALID_ARG, "handoff needs mem_capacity >= 1");
+    REQUIRE_PTR(lengths);
+    REQUIRE_PTR(mem);
+    REQUIRE_PTR(h_last);
+    REQUIRE_PTR(h_state);
+    REQUIRE_PTR(chunk_acc);
+    return hip_status(dart::launch_decode_handoff(s, mem, h_last, lengths, h_state, chunk_acc,
+                                                  (hipStream_t)stream),
+                      "dart_decode_handoff launch");
 }
 
 int64_t dart_decode_cache_elems(const dart_dims* dims, int64_t context) {

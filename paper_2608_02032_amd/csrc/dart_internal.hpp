@@ -44,10 +44,16 @@ hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const voi
 // SSM readout y_ssd [B][H][P] (float).
 constexpr int kDecodeMinMemPerSplit = 8;  // smallest split size the workspace allows
 size_t decode_workspace_bytes(const Shape& s);
-hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
-                         const float* dt, const float* A, const void* Bm, const void* Cm,
-                         const void* q, const void* e, const void* z, float* h_state,
-                         float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st);
+// pos_rows (device, [B]) == nullptr: every row at `pos`; otherwise row b at
+// pos_rows[b], rows outside [0, pos] skipped, the grid sized for `pos`.
+hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const int64_t* pos_rows,
+                         const void* x, const float* dt, const float* A, const void* Bm,
+                         const void* Cm, const void* q, const void* e, const void* z,
+                         float* h_state, float* chunk_acc, void* mem, void* y, void* ws,
+                         hipStream_t st);
+hipError_t launch_decode_handoff(const Shape& s, const void* mem, const float* h_last,
+                                 const int64_t* lengths, float* h_state, float* chunk_acc,
+                                 hipStream_t st);
 
 // Optional per-kernel timing (see dart_profile_* in dart.h).  Launchers
 // bracket each kernel launch with prof_begin/prof_end; both are no-ops unless

@@ -141,12 +141,19 @@ template <typename T, int N>
 __global__ __launch_bounds__(kThreads) void k_decode_partial(
     const T* __restrict__ mem_rd, const T* __restrict__ q, const T* __restrict__ e,
     const T* __restrict__ Cm, const float* __restrict__ qw, const float* __restrict__ ew,
-    float* __restrict__ part, float eps, int normalize, int H, int G, int64_t Mcap, int64_t m,
-    int nsplit, int mps) {
+    float* __restrict__ part, float eps, int normalize, int H, int G, int S, int64_t Mcap,
+    int64_t m, const int64_t* __restrict__ pos_rows, int64_t pos_lim, int nsplit, int mps) {
     constexpr int R = N / 8;  // rows per lane (row n = rg + 8 k)
     const int s = blockIdx.x, h = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int g = (int)((int64_t)h * G / H);
+    if (pos_rows) {
+        // ragged batch: this row's own position; rows outside [0, pos_lim]
+        // take no part in the step
+        const int64_t pb = pos_rows[b];
+        if (pb < 0 || pb > pos_lim) return;
+        m = pb / S;
+    }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int po = lane & 7, rg = lane >> 3;
 
@@ -320,10 +327,16 @@ __global__ __launch_bounds__(kThreads) void k_decode_state_merge(
     const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ z,
     float* __restrict__ h_state, float* __restrict__ chunk_acc, T* __restrict__ mem,
     T* __restrict__ y, const float* __restrict__ part, float* __restrict__ yssd, int H, int G,
-    int S, int64_t Mcap, int64_t pos, int64_t m, int nsplit, int z_per_head, int mps) {
+    int S, int64_t Mcap, int64_t pos, int64_t m, const int64_t* __restrict__ pos_rows,
+    int64_t pos_lim, int nsplit, int z_per_head, int mps) {
     const int h = blockIdx.x;
     const int64_t b = blockIdx.y;
     const int g = (int)((int64_t)h * G / H);
+    if (pos_rows) {
+        pos = pos_rows[b];
+        if (pos < 0 || pos > pos_lim) return;  // the row takes no part in the step
+        m = pos / S;
+    }
     __shared__ float s_x[kP], s_B[N], s_C[N];
     __shared__ float s_y[16][kP];
     state_update<T, N>(x, dt, A, Bm, Cm, h_state, chunk_acc, mem, yssd, H, G, S, Mcap, pos, m, b,
@@ -349,10 +362,11 @@ __global__ __launch_bounds__(kThreads) void k_decode_state_merge(
 }
 
 template <typename T, int N>
-hipError_t run_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
-                      const float* dt, const float* A, const void* Bm, const void* Cm,
-                      const void* q, const void* e, const void* z, float* h_state,
+hipError_t run_decode(const Shape& s, const SmaArgs& a, int64_t pos, const int64_t* pos_rows,
+                      const void* x, const float* dt, const float* A, const void* Bm,
+                      const void* Cm, const void* q, const void* e, const void* z, float* h_state,
                       float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st) {
+    // ragged batches size the grid for the largest position (pos = pos_lim)
     const int64_t m = pos / s.S;
     const int mps = decode_mps(s.B * s.H, m);
     const int nsplit_cap = (int)((s.Mcap + kMinMPS - 1) / kMinMPS);
@@ -363,28 +377,78 @@ hipError_t run_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void*
         prof_begin("k_decode_partial", st);
         k_decode_partial<T, N><<<dim3((unsigned)ns, (unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
             (const T*)mem, (const T*)q, (const T*)e, (const T*)Cm, a.qw, a.ew, part, a.eps,
-            a.normalize, s.H, s.G, s.Mcap, m, nsplit_cap, mps);
+            a.normalize, s.H, s.G, s.S, s.Mcap, m, pos_rows, pos, nsplit_cap, mps);
         prof_end(st);
     }
     prof_begin("k_decode_state_merge", st);
     k_decode_state_merge<T, N><<<dim3((unsigned)s.H, (unsigned)s.B), kThreads, 0, st>>>(
         (const T*)x, dt, A, (const T*)Bm, (const T*)Cm, (const T*)z, h_state, chunk_acc, (T*)mem,
-        (T*)y, part, yssd, s.H, s.G, s.S, s.Mcap, pos, m, nsplit_cap, a.z_per_head, mps);
+        (T*)y, part, yssd, s.H, s.G, s.S, s.Mcap, pos, m, pos_rows, pos, nsplit_cap, a.z_per_head,
+        mps);
     prof_end(st);
     return hipGetLastError();
 }
 
 template <typename T>
-hipError_t run_decode_n(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
-                        const float* dt, const float* A, const void* Bm, const void* Cm,
-                        const void* q, const void* e, const void* z, float* hs, float* ca,
-                        void* mem, void* y, void* ws, hipStream_t st) {
+hipError_t run_decode_n(const Shape& s, const SmaArgs& a, int64_t pos, const int64_t* pr,
+                        const void* x, const float* dt, const float* A, const void* Bm,
+                        const void* Cm, const void* q, const void* e, const void* z, float* hs,
+                        float* ca, void* mem, void* y, void* ws, hipStream_t st) {
     switch (s.N) {
-        case 32: return run_decode<T, 32>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
-        case 64: return run_decode<T, 64>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
-        case 128: return run_decode<T, 128>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+        case 32: return run_decode<T, 32>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+        case 64: return run_decode<T, 64>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+        case 128: return run_decode<T, 128>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
     }
     return hipErrorInvalidValue;
+}
+
+// Prefill -> decode handoff for row b of length L_b (lengths[b]; rows with
+// L_b < 0 are left untouched): h_state = h_last and chunk_acc = the running
+// contribution of the partial chunk floor(L_b/S), which the forward scan left
+// in mem slot floor(L_b/S) (0 when L_b is a multiple of S: the next token
+// opens a chunk).
+template <typename T, int N>
+__global__ __launch_bounds__(kThreads) void k_decode_handoff(const T* __restrict__ mem,
+                                                             const float* __restrict__ h_last,
+                                                             const int64_t* __restrict__ lengths,
+                                                             float* __restrict__ h_state,
+                                                             float* __restrict__ chunk_acc, int H,
+                                                             int S, int64_t Mcap) {
+    const int h = blockIdx.x;
+    const int64_t b = blockIdx.y;
+    const int64_t len = lengths[b];
+    if (len < 0) return;
+    const int64_t mi = len / S;
+    const bool partial = (len % S) != 0 && mi < Mcap;
+    const int64_t base = (b * H + h) * (int64_t)N * kP;
+    const T* src = mem + ((b * Mcap + (partial ? mi : 0)) * H + h) * (int64_t)N * kP;
+    for (int e0 = threadIdx.x * 4; e0 < N * kP; e0 += kThreads * 4) {
+        float v[4];
+        load4(h_last + base + e0, v);
+        store4(h_state + base + e0, v);
+        if (partial) {
+            load4(src + e0, v);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = 0.f;
+        }
+        store4(chunk_acc + base + e0, v);
+    }
+}
+
+template <typename T>
+hipError_t run_handoff_n(const Shape& s, const void* mem, const float* h_last,
+                         const int64_t* lengths, float* h_state, float* chunk_acc, hipStream_t st) {
+    const dim3 grid((unsigned)s.H, (unsigned)s.B);
+    prof_begin("k_decode_handoff", st);
+    switch (s.N) {
+        case 32: k_decode_handoff<T, 32><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;
+        case 64: k_decode_handoff<T, 64><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;
+        case 128: k_decode_handoff<T, 128><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;
+        default: prof_end(st); return hipErrorInvalidValue;
+    }
+    prof_end(st);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -395,13 +459,23 @@ size_t decode_workspace_bytes(const Shape& s) {
                                      (size_t)s.B * s.H * s.P));
 }
 
-hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
-                         const float* dt, const float* A, const void* Bm, const void* Cm,
-                         const void* q, const void* e, const void* z, float* h_state,
-                         float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st) {
+hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const int64_t* pos_rows,
+                         const void* x, const float* dt, const float* A, const void* Bm,
+                         const void* Cm, const void* q, const void* e, const void* z,
+                         float* h_state, float* chunk_acc, void* mem, void* y, void* ws,
+                         hipStream_t st) {
     if (s.dtype == 1)
-        return run_decode_n<bf16>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem, y, ws, st);
-    return run_decode_n<float>(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem, y, ws, st);
+        return run_decode_n<bf16>(s, a, pos, pos_rows, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc,
+                                  mem, y, ws, st);
+    return run_decode_n<float>(s, a, pos, pos_rows, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem,
+                               y, ws, st);
+}
+
+hipError_t launch_decode_handoff(const Shape& s, const void* mem, const float* h_last,
+                                 const int64_t* lengths, float* h_state, float* chunk_acc,
+                                 hipStream_t st) {
+    if (s.dtype == 1) return run_handoff_n<bf16>(s, mem, h_last, lengths, h_state, chunk_acc, st);
+    return run_handoff_n<float>(s, mem, h_last, lengths, h_state, chunk_acc, st);
 }
 
 }  // namespace dart

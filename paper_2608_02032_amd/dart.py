@@ -45,7 +45,7 @@ class SmaOpts(ctypes.Structure):
 
 EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspace_bytes",
            "dart_sma_fwd", "dart_decode_workspace_bytes", "dart_decode_step",
-           "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
+           "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
            "dart_profile_enable", "dart_profile_flush", "dart_profile_count",
            "dart_profile_name", "dart_profile_total_ms", "dart_profile_launches",
            "dart_profile_reset")
@@ -79,6 +79,11 @@ def load_library(path: str = LIB_PATH):
         lib.dart_decode_workspace_bytes.restype = sz
         lib.dart_decode_step.argtypes = [D, O, i64, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
         lib.dart_decode_step.restype = st
+        lib.dart_decode_step_ragged.argtypes = [D, O, P, i64, P, P, P, P, P, P, P, P, P, P, P, P,
+                                                P, sz, P]
+        lib.dart_decode_step_ragged.restype = st
+        lib.dart_decode_handoff.argtypes = [D, P, P, P, P, P, P]
+        lib.dart_decode_handoff.restype = st
         lib.dart_decode_cache_elems.argtypes = [D, i64]
         lib.dart_decode_cache_elems.restype = i64
         lib.dart_status_string.argtypes = [st]
@@ -249,6 +254,57 @@ def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache, c
                                _ptr(h_state), _ptr(chunk_acc), _ptr(mem_cache), _ptr(y),
                                _ptr(workspace), workspace.numel(), _stream(stream)))
     return y
+
+
+def decode_step_ragged(pos, pos_max, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache,
+                       chunk, eps=DEFAULT_EPS, normalize=True, q_norm_w=None, e_norm_w=None,
+                       y=None, workspace=None, stream=None):
+    """One decode step of a ragged batch (dart_decode_step_ragged): row b at
+    position pos[b] (int64 device tensor [B]); pos_max bounds pos (host int).
+    Updates h_state, chunk_acc and mem_cache in place; returns y [B][H][P]."""
+    torch = _torch()
+    lib = load_library()
+    B_, H, P = x.shape
+    G, N = Bm.shape[1], Bm.shape[2]
+    dtype = _dtype_code(x)
+    for t, nm in ((dt, "dt"), (A, "A"), (h_state, "h_state"), (chunk_acc, "chunk_acc")):
+        _check_f32(t, nm)
+    if pos.dtype != torch.int64 or not pos.is_cuda or pos.numel() != B_:
+        raise ValueError("pos must be an int64 device tensor of %d entries" % B_)
+    z_per_head = 1 if z.dim() == 2 else 0
+    dims = make_dims(B_, 0, H, P, N, chunk, dtype, G, mem_cache.shape[1])
+    opts = SmaOpts(float(eps), _ptr(q_norm_w), _ptr(e_norm_w), int(bool(normalize)), z_per_head)
+    if y is None:
+        y = torch.empty_like(x)
+    need = lib.dart_decode_workspace_bytes(ctypes.byref(dims))
+    if workspace is None:
+        workspace = _workspace(need, x.device)
+    check(lib.dart_decode_step_ragged(ctypes.byref(dims), ctypes.byref(opts), _ptr(pos), int(pos_max),
+                                      _ptr(x), _ptr(dt), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(q),
+                                      _ptr(e), _ptr(z), _ptr(h_state), _ptr(chunk_acc),
+                                      _ptr(mem_cache), _ptr(y), _ptr(workspace), workspace.numel(),
+                                      _stream(stream)))
+    return y
+
+
+def decode_handoff(lengths, mem, h_last, chunk, h_state=None, chunk_acc=None, stream=None):
+    """Decode state after a (dt = 0 padded) prefill (dart_decode_handoff):
+    returns (h_state, chunk_acc) for the rows' next positions lengths[b]."""
+    torch = _torch()
+    lib = load_library()
+    B_, Mcap, H, N, P = mem.shape
+    dtype = _dtype_code(mem)
+    _check_f32(h_last, "h_last")
+    if lengths.dtype != torch.int64 or not lengths.is_cuda or lengths.numel() != B_:
+        raise ValueError("lengths must be an int64 device tensor of %d entries" % B_)
+    dims = make_dims(B_, 0, H, P, N, chunk, dtype, 1, Mcap)
+    if h_state is None:
+        h_state = torch.empty_like(h_last)
+    if chunk_acc is None:
+        chunk_acc = torch.empty_like(h_last)
+    check(lib.dart_decode_handoff(ctypes.byref(dims), _ptr(lengths), _ptr(mem), _ptr(h_last),
+                                  _ptr(h_state), _ptr(chunk_acc), _stream(stream)))
+    return h_state, chunk_acc
 
 
 def workspace_bytes(kind: str, dims: Dims) -> int:

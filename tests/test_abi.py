@@ -162,6 +162,26 @@ def test_decode_rejects_cache_overflow_and_bad_pos(lib):
     assert call_decode(lib, dd, 10, nbytes=need - 1) == dart.DART_ERR_INVALID_ARG
 
 
+def test_ragged_decode_and_handoff_reject_bad_arguments(lib):
+    o = dart.SmaOpts(1e-6, None, None, 1, 1)
+    d = dims(seqlen=0, chunk=64, mem_capacity=4)
+
+    def ragged(pos_max, pos_ptr=1, nbytes=1 << 40, dd=d):
+        return lib.dart_decode_step_ragged(ctypes.byref(dd), ctypes.byref(o), pos_ptr, pos_max, 1, 1,
+                                           1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, nbytes, None)
+    assert ragged(-1) == dart.DART_ERR_INVALID_ARG
+    # positions up to 255 fit four memories; 256 could need slot 4
+    assert ragged(256) == dart.DART_ERR_INVALID_ARG
+    assert b"pos_max" in lib.dart_last_error()
+    assert ragged(10, pos_ptr=None) == dart.DART_ERR_INVALID_ARG
+    need = lib.dart_decode_workspace_bytes(ctypes.byref(d))
+    assert ragged(10, nbytes=need - 1) == dart.DART_ERR_INVALID_ARG
+    assert ragged(10, dd=dims(seqlen=0, mem_capacity=0)) == dart.DART_ERR_INVALID_ARG
+    assert lib.dart_decode_handoff(ctypes.byref(d), None, 1, 1, 1, 1, None) == dart.DART_ERR_INVALID_ARG
+    assert lib.dart_decode_handoff(ctypes.byref(dims(seqlen=0, mem_capacity=0)), 1, 1, 1, 1, 1,
+                                   None) == dart.DART_ERR_INVALID_ARG
+
+
 def test_cache_ratio_closed_form_matches_paper(lib):
     """Pin C-P12: element count of the length-dependent decode cache over the
     matched KV cache (2 L P per head) is N/(2S); the paper prints 25% at

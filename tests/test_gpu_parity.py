@@ -275,6 +275,58 @@ def test_decode_token_by_token_reproduces_forward(dtype, S, N, L, z_per_head):
     assert_close_slices(to_np(h_state), ref["h_last"], tol, axes_keep=(0, 1), what="h_state")
 
 
+@pytest.mark.parametrize("dtype,S,N,lengths,steps", [("fp32", 64, 64, (70, 128, 5), 70),
+                                                      ("bf16", 128, 128, (300, 256, 129, 0), 140)])
+def test_ragged_prefill_handoff_and_decode(dtype, S, N, lengths, steps):
+    """Rows of different prompt lengths: one scan over the batch padded with
+    dt = 0, the handoff, then decode steps at each row's own position; every
+    row's outputs against the oracle forward over that row's own sequence."""
+    import torch
+    B_ = len(lengths)
+    T = max(lengths) + steps
+    w = synth.Workload("ragged_%s" % dtype, B_, T, 2, 64, N, S, dtype)
+    announce("ragged prefill/handoff/decode %s lengths %s" % (w, lengths))
+    d = synth.forward_inputs(w, seed=31)
+    H, P = w.nheads, w.headdim
+    Lp = max(lengths)
+    Mcap = -(-T // S) + 1
+    dt_pad = d["dt"][:, :Lp].copy()
+    for b, lb in enumerate(lengths):
+        dt_pad[b, lb:] = 0.0
+    dev = {k: to_dev(d[k], dtype) for k in ("x", "Bm", "Cm", "q", "e", "z")}
+    dt_all, A = f32_dev(d["dt"]), f32_dev(d["A"])
+    h_last = None
+    if Lp > 0:
+        _, mem, h_last = dart.ssd_chunk_scan(dev["x"][:, :Lp].contiguous(), f32_dev(dt_pad), A,
+                                             dev["Bm"][:, :Lp].contiguous(),
+                                             dev["Cm"][:, :Lp].contiguous(), S, mem_capacity=Mcap)
+    lens = torch.tensor(lengths, dtype=torch.int64, device="cuda")
+    h_state, chunk_acc = dart.decode_handoff(lens, mem, h_last, S)
+    rows = torch.arange(B_, device="cuda")
+    ys = []
+    for k in range(steps):
+        pos = lens + k
+        take = lambda t: t[rows, pos].contiguous()
+        y = dart.decode_step_ragged(pos, max(lengths) + k, take(dev["x"]), take(dt_all), A,
+                                    take(dev["Bm"]), take(dev["Cm"]), take(dev["q"]), take(dev["e"]),
+                                    take(dev["z"]), h_state, chunk_acc, mem, S)
+        ys.append(to_np(y))
+    torch.cuda.synchronize()
+    tol = TOL[dtype]
+    for b, lb in enumerate(lengths):
+        tb = lb + steps
+        sl = lambda a: a[b:b + 1, :tb]
+        ref = oracle.forward(sl(d["x"]), sl(d["dt"]), d["A"], sl(d["Bm"]), sl(d["Cm"]), sl(d["q"]),
+                             sl(d["e"]), sl(d["z"]), S)
+        got = np.stack([ys[k][b] for k in range(steps)], axis=0)[None]
+        assert_close_slices(got, ref["y"][:, lb:tb], tol, what="decode y row %d (L=%d)" % (b, lb))
+        assert_close_slices(to_np(h_state[b:b + 1]), ref["h_last"], tol, axes_keep=(0, 1),
+                            what="h_state row %d" % b)
+        full = tb // S
+        assert_close_slices(to_np(mem[b:b + 1, :full]), ref["mem"][:, :full], tol, axes_keep=(0, 1, 2),
+                            what="cache row %d" % b)
+
+
 @pytest.mark.parametrize("dtype,N,S,m,offset", [("bf16", 128, 256, 40, 17), ("bf16", 128, 256, 19, 255),
                                                 ("fp32", 64, 64, 33, 0), ("bf16", 32, 128, 1, 5)])
 def test_decode_single_step_on_synthetic_cache(dtype, N, S, m, offset):

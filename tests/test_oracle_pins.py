@@ -462,3 +462,24 @@ def test_synth_recipe_ranges_and_bf16_rounding():
     d2 = synth.forward_inputs(w, seed=0)
     for k in d:
         np.testing.assert_array_equal(d[k], d2[k])
+
+
+def test_zero_dt_padding_leaves_prefix_state_and_memories():
+    """Right-padding with dt = 0 (decay exp(0) = 1, input term 0) leaves the
+    prefix's outputs, final state and chunk memories unchanged, exactly: the
+    reading the prefill -> decode handoff of a ragged batch relies on.  The
+    padded chunk's memory decays through the padding by factors of one."""
+    w = synth.Workload("pad", 1, 150, 2, 64, 32, 64, "fp32")
+    d = synth.forward_inputs(w, seed=5)
+    L, S = 100, 64
+    cut = lambda a: a[:, :L]
+    y1, h1 = oracle.ssd_recurrence(cut(d["x"]), cut(d["dt"]), d["A"], cut(d["Bm"]), cut(d["Cm"]))
+    dtp = d["dt"].copy()
+    dtp[:, L:] = 0.0
+    y2, h2 = oracle.ssd_recurrence(d["x"], dtp, d["A"], d["Bm"], d["Cm"])
+    np.testing.assert_array_equal(h1, h2)
+    np.testing.assert_array_equal(y1, y2[:, :L])
+    m1 = oracle.chunk_memories(cut(d["x"]), cut(d["dt"]), d["A"], cut(d["Bm"]), S)
+    m2 = oracle.chunk_memories(d["x"], dtp, d["A"], d["Bm"], S)
+    np.testing.assert_array_equal(m1, m2[:, :2])
+    assert not np.any(m2[:, 2])
