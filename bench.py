@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--workload", default="sweep_L8192_S256_N128")
     ap.add_argument("--decode-workload", default="decode_B64_ctx65536")
     ap.add_argument("--no-decode", action="store_true", help="time the forward only")
+    ap.add_argument("--no-ragged", action="store_true",
+                    help="skip the separately timed ragged-batch decode steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=4,
                     help="batches of the workload the CPU oracle is timed on")
@@ -338,6 +340,40 @@ def main():
             "algorithmic_bytes": dbytes,
             "k_decode_partial_gbps": round(cache_bytes / (part_ms * 1e-3) / 1e9, 1),
             "k_decode_partial_traffic": traffic_for("k_decode_partial")}
+
+    if not args.no_decode and not args.no_ragged:
+        # ragged batch (row b at its own position, spread evenly over the
+        # context), timed on its own after the steps above
+        R = 10
+        pos_list = [dw.chunk + (b * (dw.context - dw.chunk)) // max(dw.batch - 1, 1)
+                    for b in range(dw.batch)]
+        pos_r = torch.tensor(pos_list, dtype=torch.int64, device=dev)
+        pmax = max(pos_list)
+
+        def decode_ragged():
+            dart.decode_step_ragged(pos_r, pmax, D["x"], D["dt"], D["A"], D["Bm"], D["Cm"], D["q"],
+                                    D["e"], D["z"], h_state, chunk_acc, cache, dw.chunk, y=y_dec,
+                                    workspace=ws_dec, stream=stream)
+        for _ in range(3):
+            decode_ragged()
+        er = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        er[0].record(stream)
+        for _ in range(R):
+            decode_ragged()
+        er[1].record(stream)
+        torch.cuda.synchronize()
+        rag_ms = er[0].elapsed_time(er[1]) / R
+        esz = 2
+        rbytes = (sum(p // dw.chunk for p in pos_list) * dw.nheads * dw.dstate * dw.headdim * esz
+                  + 4 * dw.batch * dw.nheads * dw.dstate * dw.headdim * 4
+                  + dw.batch * dw.nheads * dw.headdim * esz * 2
+                  + dw.batch * dw.ngroups * (3 * dw.dstate + dw.headdim) * esz + dw.batch * dw.nheads * 8)
+        extra["decode_ragged"] = {
+            "positions": "row b at %d + b (%d - %d) / %d" % (dw.chunk, dw.context, dw.chunk, dw.batch - 1),
+            "us_per_step": round(rag_ms * 1e3, 2), "algorithmic_bytes": rbytes,
+            "hbm_gbps": round(rbytes / (rag_ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(rbytes / (rag_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
 
     tokens = B * L
     line = {
