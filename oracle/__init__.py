@@ -75,6 +75,11 @@ def _load():
                                                 _D, _D, _D, _D, _D, _D, _D, _D, _D, _D,
                                                 _D, _D, _D, _D]
         lib.dart_oracle_decode_step.restype = ctypes.c_int
+        lib.dart_oracle_sma_bwd.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
+                                            ctypes.c_double, _INT, _INT,
+                                            _D, _D, _D, _D, _D, _D, _D, _D,
+                                            _D, _D, _D, _D, _D]
+        lib.dart_oracle_sma_bwd.restype = None
         _lib = lib
         return lib
 
@@ -171,6 +176,31 @@ def sma_rows(q, e, Cm, mem, z, y_ssd, S, rows, eps=1e-6, normalize=True, q_norm_
                                  rows.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                                  _ptr(yr), _ptr(lr))
     return yr, lr
+
+
+def sma_bwd(q, e, Cm, mem, z, dy, S, eps=1e-6, normalize=True, q_norm_w=None, e_norm_w=None):
+    """Gradients of the SMA + gate forward for the loss sum(dy * y), by
+    recomputing every row (App. C) and the chain rule through Sec. 3 and
+    App. B.1 (the norm weights are constants).  Shapes as in sma(); dy like
+    y_ssd.  Returns {"dq", "de", "dC", "dmem", "dz", "dy_ssd"}: q, e, C
+    gradients summed over the heads of their group, dmem in the cache layout
+    (slots never attended are zero), dz like z, dy_ssd = dy."""
+    q, e, Cm, mem, z, dy = map(_f64, (q, e, Cm, mem, z, dy))
+    B_, L, H, P = dy.shape
+    G, N = q.shape[2], q.shape[3]
+    Mcap = mem.shape[1]
+    assert Mcap >= -(-L // S)
+    z_per_head = 1 if z.ndim == 3 else 0
+    qw = None if q_norm_w is None else _f64(q_norm_w)
+    ew = None if e_norm_w is None else _f64(e_norm_w)
+    out = {"dq": np.empty_like(q), "de": np.empty_like(e), "dC": np.empty_like(Cm),
+           "dmem": np.empty_like(mem), "dz": np.empty_like(z)}
+    _load().dart_oracle_sma_bwd(B_, L, H, G, P, N, int(S), Mcap, float(eps), int(bool(normalize)),
+                                z_per_head, _ptr(q), _ptr(e), _ptr(Cm), _ptr(qw), _ptr(ew),
+                                _ptr(mem), _ptr(z), _ptr(dy), _ptr(out["dq"]), _ptr(out["de"]),
+                                _ptr(out["dC"]), _ptr(out["dmem"]), _ptr(out["dz"]))
+    out["dy_ssd"] = dy.copy()
+    return out
 
 
 def forward(x, dt, A, Bm, Cm, q, e, z, S, eps=1e-6, normalize=True, q_norm_w=None,

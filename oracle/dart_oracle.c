@@ -31,6 +31,9 @@
  *                                token an explicit two-pass softmax over the
  *                                strictly earlier chunks, then
  *                                Y_t = C_t H_t + SiLU(z_t) R_t.
+ *   dart_oracle_sma_bwd          gradients of dart_oracle_sma (loss sum dy . y)
+ *                                by recomputing every row (App. C) and the chain
+ *                                rule through Sec. 3 and App. B.1, written out.
  *   dart_oracle_decode_step      one autoregressive token (the paper gives no
  *                                algorithm; the order used is: update the
  *                                recurrent state and the running chunk
@@ -313,6 +316,186 @@ void dart_oracle_sma_rows(int64_t B, int64_t L, int H, int G, int P, int N, int 
         free(Rrow);
         free(rr);
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Backward of the SMA forward above (the loss is sum_t dy_t . y_t), by       */
+/* recomputing each row's logits and recovering the softmax weights exactly  */
+/* (App. C: scores recomputed, probabilities exp(l - LSE); here the exact    */
+/* softmax).  Differentiating the definitions of Sec. 3 and App. B.1:        */
+/*   y = y_ssd + SiLU(z) R:   dR = SiLU(z) dy,  dz = SiLU'(z) (R . dy),      */
+/*   R = sum_j w_j V_j:       dw_j = dR . V_j,  dl_j = w_j (dw_j - dR . R),  */
+/*                            dV_j = w_j dR                                  */
+/*   V_j = C dH_j:            dC += dH_j dV_j,  ddH_j += C (x) dV_j          */
+/*   l_j = Qbar . K_j / sqrt(N), K_j = r_j (.) (dH_j Ebar):                  */
+/*     dQbar += dl_j K_j / sqrt(N),  dA_j = dl_j Qbar (.) r_j / sqrt(N),     */
+/*     ddH_j += dA_j (x) Ebar,  dEbar += dH_j^T dA_j,                        */
+/*     dr_j += dl_j Qbar (.) (dH_j Ebar) / sqrt(N)                           */
+/*   r_j[n] = (P^-1 sum_p dH_j[n,p]^2 + eps)^-1/2:                           */
+/*     ddH_j[n,p] -= dr_j[n] r_j[n]^3 dH_j[n,p] / P                          */
+/*   Qbar = RMSNorm(q) w:  dq = inv u - q inv^3 (u . q) / N, u = dQbar (.) w */
+/*   (and Ebar likewise).  The norm weights are constants here.             */
+/* q, e, C gradients sum over the heads of their group; dz sums over heads   */
+/* when one gate serves every head of a token.  Outputs are overwritten.     */
+/* ------------------------------------------------------------------------ */
+static double silu_grad(double z) {
+    const double s = 1.0 / (1.0 + exp(-z));
+    return s * (1.0 + z * (1.0 - s));
+}
+
+static void rms_normalise_bwd(const double* v, int D, double eps, const double* w,
+                              const double* dout, double* dv) {
+    double ss = 0.0;
+    for (int k = 0; k < D; ++k) ss += v[k] * v[k];
+    const double inv = 1.0 / sqrt(ss / D + eps);
+    double uv = 0.0;
+    for (int k = 0; k < D; ++k) uv += dout[k] * (w ? w[k] : 1.0) * v[k];
+    for (int k = 0; k < D; ++k)
+        dv[k] += dout[k] * (w ? w[k] : 1.0) * inv - v[k] * inv * inv * inv * uv / D;
+}
+
+void dart_oracle_sma_bwd(int64_t B, int64_t L, int H, int G, int P, int N, int S, int64_t Mcap,
+                         double eps, int normalize, int z_per_head, const double* q,
+                         const double* e, const double* Cm, const double* qw, const double* ew,
+                         const double* mem, const double* z, const double* dy, double* dq,
+                         double* de, double* dC, double* dmem, double* dz) {
+    const int64_t M = (L + S - 1) / S;
+    const double isn = 1.0 / sqrt((double)N);
+    double* rr = all_inv_rms(B, H, P, N, Mcap, M, eps, normalize, mem);
+    for (size_t k = 0; k < (size_t)B * L * G * N; ++k) dq[k] = 0.0, dC[k] = 0.0;
+    for (size_t k = 0; k < (size_t)B * L * G * P; ++k) de[k] = 0.0;
+    for (size_t k = 0; k < (size_t)B * Mcap * H * N * P; ++k) dmem[k] = 0.0;
+    for (size_t k = 0; k < (size_t)B * L * (z_per_head ? H : 1); ++k) dz[k] = 0.0;
+    /* rows of one batch entry touch only that entry's outputs */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        double* drr = (double*)calloc((size_t)H * (M > 0 ? M : 1) * N, sizeof(double));
+        double* qbar = (double*)malloc(sizeof(double) * N);
+        double* ebar = (double*)malloc(sizeof(double) * P);
+        double* ell = (double*)malloc(sizeof(double) * (M + 1));
+        double* w = (double*)malloc(sizeof(double) * (M + 1));
+        double* Vj = (double*)malloc(sizeof(double) * (size_t)(M + 1) * P);
+        double* Aj = (double*)malloc(sizeof(double) * (size_t)(M + 1) * N);
+        double* R = (double*)malloc(sizeof(double) * P);
+        double* dR = (double*)malloc(sizeof(double) * P);
+        double* dqbar = (double*)malloc(sizeof(double) * N);
+        double* debar = (double*)malloc(sizeof(double) * P);
+        for (int h = 0; h < H; ++h) {
+            const int g = group_of(h, H, G);
+            const double* rbh = rr + ((size_t)b * H + h) * M * N;
+            for (int64_t t = 0; t < L; ++t) {
+                const int64_t i = t / S;
+                if (i == 0) continue; /* no history: y = y_ssd, nothing flows back */
+                const double* qt = q + ((size_t)b * L + t) * G * N + (size_t)g * N;
+                const double* et = e + ((size_t)b * L + t) * G * P + (size_t)g * P;
+                const double* ct = Cm + ((size_t)b * L + t) * G * N + (size_t)g * N;
+                if (normalize) {
+                    rms_normalise(qt, N, eps, qw, qbar);
+                    rms_normalise(et, P, eps, ew, ebar);
+                } else {
+                    for (int n = 0; n < N; ++n) qbar[n] = qt[n];
+                    for (int p = 0; p < P; ++p) ebar[p] = et[p];
+                }
+                /* recompute logits and values */
+                for (int64_t j = 0; j < i; ++j) {
+                    const double* dH = mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+                    const double* r = rbh + (size_t)j * N;
+                    double l = 0.0;
+                    for (int n = 0; n < N; ++n) {
+                        double a = 0.0;
+                        for (int p = 0; p < P; ++p) a += dH[(size_t)n * P + p] * ebar[p];
+                        Aj[(size_t)j * N + n] = a;
+                        l += qbar[n] * r[n] * a;
+                    }
+                    ell[j] = l * isn;
+                    for (int p = 0; p < P; ++p) {
+                        double v = 0.0;
+                        for (int n = 0; n < N; ++n) v += ct[n] * dH[(size_t)n * P + p];
+                        Vj[(size_t)j * P + p] = v;
+                    }
+                }
+                double m = -INFINITY;
+                for (int64_t j = 0; j < i; ++j) m = ell[j] > m ? ell[j] : m;
+                double d = 0.0;
+                for (int64_t j = 0; j < i; ++j) d += exp(ell[j] - m);
+                for (int p = 0; p < P; ++p) R[p] = 0.0;
+                for (int64_t j = 0; j < i; ++j) {
+                    w[j] = exp(ell[j] - m) / d;
+                    for (int p = 0; p < P; ++p) R[p] += w[j] * Vj[(size_t)j * P + p];
+                }
+                /* gate */
+                const double* dyt = dy + (((size_t)b * L + t) * H + h) * P;
+                const size_t zi = z_per_head ? ((size_t)b * L + t) * H + h : (size_t)b * L + t;
+                const double gate = silu(z[zi]);
+                double rdy = 0.0, D = 0.0;
+                for (int p = 0; p < P; ++p) {
+                    rdy += R[p] * dyt[p];
+                    dR[p] = gate * dyt[p];
+                    D += dR[p] * R[p];
+                }
+                dz[zi] += silu_grad(z[zi]) * rdy;
+                for (int n = 0; n < N; ++n) dqbar[n] = 0.0;
+                for (int p = 0; p < P; ++p) debar[p] = 0.0;
+                double* dct = dC + ((size_t)b * L + t) * G * N + (size_t)g * N;
+                for (int64_t j = 0; j < i; ++j) {
+                    const double* dH = mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+                    double* ddH = dmem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+                    const double* r = rbh + (size_t)j * N;
+                    double* dr = drr + ((size_t)h * M + j) * N;
+                    double dw = 0.0;
+                    for (int p = 0; p < P; ++p) dw += dR[p] * Vj[(size_t)j * P + p];
+                    const double dl = w[j] * (dw - D);
+                    for (int n = 0; n < N; ++n) {
+                        const double a = Aj[(size_t)j * N + n];
+                        dqbar[n] += dl * r[n] * a * isn;
+                        dr[n] += dl * qbar[n] * a * isn;
+                        const double dA = dl * qbar[n] * r[n] * isn;
+                        double dc = 0.0;
+                        for (int p = 0; p < P; ++p) {
+                            const double dV = w[j] * dR[p];
+                            dc += dV * dH[(size_t)n * P + p];
+                            ddH[(size_t)n * P + p] += ct[n] * dV + dA * ebar[p];
+                            debar[p] += dA * dH[(size_t)n * P + p];
+                        }
+                        dct[n] += dc;
+                    }
+                }
+                double* dqt = dq + ((size_t)b * L + t) * G * N + (size_t)g * N;
+                double* det = de + ((size_t)b * L + t) * G * P + (size_t)g * P;
+                if (normalize) {
+                    rms_normalise_bwd(qt, N, eps, qw, dqbar, dqt);
+                    rms_normalise_bwd(et, P, eps, ew, debar, det);
+                } else {
+                    for (int n = 0; n < N; ++n) dqt[n] += dqbar[n];
+                    for (int p = 0; p < P; ++p) det[p] += debar[p];
+                }
+            }
+            /* through r_j = (mean_p dH_j^2 + eps)^-1/2 */
+            if (normalize)
+                for (int64_t j = 0; j < M; ++j) {
+                    const double* dH = mem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+                    double* ddH = dmem + (((size_t)b * Mcap + j) * H + h) * (size_t)N * P;
+                    const double* r = rbh + (size_t)j * N;
+                    const double* dr = drr + ((size_t)h * M + j) * N;
+                    for (int n = 0; n < N; ++n) {
+                        const double c = dr[n] * r[n] * r[n] * r[n] / P;
+                        for (int p = 0; p < P; ++p) ddH[(size_t)n * P + p] -= c * dH[(size_t)n * P + p];
+                    }
+                }
+        }
+        free(drr);
+        free(qbar);
+        free(ebar);
+        free(ell);
+        free(w);
+        free(Vj);
+        free(Aj);
+        free(R);
+        free(dR);
+        free(dqbar);
+        free(debar);
+    }
+    free(rr);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -483,3 +483,45 @@ def test_zero_dt_padding_leaves_prefix_state_and_memories():
     m2 = oracle.chunk_memories(d["x"], dtp, d["A"], d["Bm"], S)
     np.testing.assert_array_equal(m1, m2[:, :2])
     assert not np.any(m2[:, 2])
+
+
+@pytest.mark.parametrize("normalize,z_per_head,G,weights", [(True, True, 1, False), (True, False, 2, True),
+                                                             (False, True, 1, False)])
+def test_sma_backward_matches_finite_differences(normalize, z_per_head, G, weights):
+    """The oracle's SMA backward against central differences of the oracle's
+    forward (loss sum dy . y) at sampled entries of every input: the two share
+    no arithmetic beyond the forward definition, so a dropped term, a wrong
+    sign or a transposed index in the backward fails here."""
+    rng = np.random.default_rng(7 + G)
+    B_, L, H, P, N, S = 1, 40, 4, 8, 6, 8
+    q = rng.standard_normal((B_, L, G, N))
+    e = rng.standard_normal((B_, L, G, P))
+    C = rng.standard_normal((B_, L, G, N)) * 0.5
+    M = -(-L // S)
+    mem = rng.standard_normal((B_, M, H, N, P)) * 0.3
+    z = rng.standard_normal((B_, L, H) if z_per_head else (B_, L))
+    ys = rng.standard_normal((B_, L, H, P))
+    dy = rng.standard_normal((B_, L, H, P))
+    qw = rng.uniform(0.5, 1.5, N) if weights else None
+    ew = rng.uniform(0.5, 1.5, P) if weights else None
+    kw = dict(normalize=normalize, q_norm_w=qw, e_norm_w=ew)
+
+    def loss(v):
+        y, _ = oracle.sma(v["q"], v["e"], v["C"], v["mem"], v["z"], ys, S, **kw)
+        return float((y * dy).sum())
+
+    g = oracle.sma_bwd(q, e, C, mem, z, dy, S, **kw)
+    base = {"q": q, "e": e, "C": C, "mem": mem, "z": z}
+    step = 1e-6
+    for name, key in (("q", "dq"), ("e", "de"), ("C", "dC"), ("mem", "dmem"), ("z", "dz")):
+        arr = base[name]
+        for _ in range(8):
+            idx = tuple(int(rng.integers(0, n)) for n in arr.shape)
+            lo, hi = arr.copy(), arr.copy()
+            lo[idx] -= step
+            hi[idx] += step
+            fd = (loss(dict(base, **{name: hi})) - loss(dict(base, **{name: lo}))) / (2 * step)
+            assert abs(fd - g[key][idx]) <= 1e-6 + 1e-5 * abs(fd), (name, idx, fd, g[key][idx])
+    # the first chunk has no history and the last memory is never attended
+    assert not np.any(g["dq"][:, :S]) and not np.any(g["dmem"][:, M - 1])
+    np.testing.assert_array_equal(g["dy_ssd"], dy)
