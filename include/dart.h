@@ -72,8 +72,10 @@ typedef struct {
                                row inverse-RMS r; the paper leaves it open; > 0
                                required when normalize = 1 (1e-6 is the default of
                                the Python binding) */
-    const float* q_norm_w;  /* device [N] RMSNorm weight of Q, or NULL for ones */
-    const float* e_norm_w;  /* device [P] RMSNorm weight of E, or NULL for ones */
+    const float* q_norm_w;  /* device [N] RMSNorm weight of Q, or NULL for ones;
+                               unused when normalize = 0 */
+    const float* e_norm_w;  /* device [P] RMSNorm weight of E, or NULL for ones;
+                               unused when normalize = 0 */
     int32_t normalize;      /* 1: normalised score branch of App. B.1;
                                0: Alg. 1 as printed (raw Q, E and r = 1) */
     int32_t z_per_head;     /* 1: z is [B][L][H] (one gate per head);
@@ -144,6 +146,47 @@ dart_status dart_sma_fwd(const dart_dims* dims, const dart_sma_opts* opts, const
                          const void* e, const void* Cm, const void* mem, const void* z,
                          const void* y_ssd, void* y, float* lse, void* workspace,
                          size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace dart_sma_bwd needs for `dims`: the key side of
+ * memories 0..M-2 (as dart_sma_workspace_bytes for fp32), the normalised
+ * query and E rows, two floats per (b, head, memory 0..M-2, token), the
+ * per-head-block partial token gradients and one float per (b, token, head). */
+size_t dart_sma_bwd_workspace_bytes(const dart_dims* dims);
+
+/*
+ * Backward of dart_sma_fwd for the loss sum_t dy_t . y_t (App. C: the scores
+ * are recomputed and the softmax weights recovered as exp(l_j - LSE_t) from
+ * the forward's log-sum-exp; the chain rule through the definitions of Sec. 3
+ * and App. B.1, with the RMSNorm weights held constant).  With
+ * g = SiLU(z_t), p_j the softmax weights and Dy = R_t . dy_t:
+ *     dl_j = g p_j (dy_t . V_j - Dy),      dz_t = SiLU'(z_t) Dy,
+ *     dC_t = sum_j g p_j dH_j dy_t,        dQbar = sum_j dl_j K_j / sqrt(N),
+ *     dEbar = sum_j dH_j^T (r_j (.) Qbar) dl_j / sqrt(N),
+ *     ddH_j = sum_t [g p_j C_t^T dy_t + r_j (.) (dl_j Qbar^T Ebar) / sqrt(N)]
+ *             - (r_j^3 / P) (.) rowsum(dH_j (.) that second sum) (.) dH_j,
+ * then dq and de through RMSNorm.  This is the attention branch only: the
+ * gradient of y with respect to y_ssd is dy itself, and the scan's own
+ * backward is not part of this call.
+ *
+ *   q, e, Cm, mem, z  as in dart_sma_fwd (storage dtype, in)
+ *   lse    [B][L][H]        float, in: the forward's log-sum-exp
+ *   dy     [B][L][H][P]     storage dtype, in: gradient of y
+ *   dq     [B][L][G][N]     float, out (summed over the heads of a group)
+ *   de     [B][L][G][P]     float, out (summed over the heads of a group)
+ *   dC     [B][L][G][N]     float, out: the attention branch's part of the
+ *                           gradient of C (summed over the heads of a group)
+ *   dmem   [B][Mcap][H][N][P] float, out: every slot written (slots M-1 and
+ *                           above, which no token attends, are zero)
+ *   dz     like z           float, out
+ *   workspace               device buffer of >= dart_sma_bwd_workspace_bytes()
+ * Tokens of the first chunk get zero q, e, C and z gradients.  Deterministic:
+ * no atomics, every sum has a fixed order.
+ */
+dart_status dart_sma_bwd(const dart_dims* dims, const dart_sma_opts* opts, const void* q,
+                         const void* e, const void* Cm, const void* mem, const void* z,
+                         const float* lse, const void* dy, float* dq, float* de, float* dC,
+                         float* dmem, float* dz, void* workspace, size_t workspace_bytes,
+                         void* stream);
 
 /* Bytes of workspace dart_decode_step needs (dims->seqlen is ignored; the
  * worst case over positions that fit dims->mem_capacity is returned). */

@@ -78,6 +78,12 @@ dart_status check_opts(const dart_sma_opts* o) {
     return DART_OK;
 }
 
+// The norm weights belong to RMSNorm: without normalisation they are unused.
+dart::SmaArgs sma_args(const dart_sma_opts* o) {
+    return dart::SmaArgs{o->eps, o->normalize ? o->q_norm_w : nullptr,
+                         o->normalize ? o->e_norm_w : nullptr, o->normalize, o->z_per_head};
+}
+
 dart_status hip_status(hipError_t e, const char* what) {
     if (e != hipSuccess) return fail(DART_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
     return ok();
@@ -153,10 +159,47 @@ dart_status dart_sma_fwd(const dart_dims* dims, const dart_sma_opts* opts, const
         if (a0 < b0 + bytes && b0 < a0 + bytes)
             return fail(DART_ERR_INVALID_ARG, "y partially overlaps y_ssd (only exact aliasing is allowed)");
     }
-    dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
+    const dart::SmaArgs a = sma_args(opts);
     return hip_status(dart::launch_sma(s, a, q, e, Cm, mem, z, y_ssd, y, lse, workspace,
                                        (hipStream_t)stream),
                       "dart_sma_fwd launch");
+}
+
+size_t dart_sma_bwd_workspace_bytes(const dart_dims* dims) {
+    dart::Shape s;
+    if (make_shape(dims, true, s) != DART_OK) return 0;
+    return dart::sma_bwd_workspace_bytes(s);
+}
+
+dart_status dart_sma_bwd(const dart_dims* dims, const dart_sma_opts* opts, const void* q,
+                         const void* e, const void* Cm, const void* mem, const void* z,
+                         const float* lse, const void* dy, float* dq, float* de, float* dC,
+                         float* dmem, float* dz, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, true, s);
+    if (st != DART_OK) return st;
+    st = check_opts(opts);
+    if (st != DART_OK) return st;
+    REQUIRE_PTR(q);
+    REQUIRE_PTR(e);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(mem);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(lse);
+    REQUIRE_PTR(dy);
+    REQUIRE_PTR(dq);
+    REQUIRE_PTR(de);
+    REQUIRE_PTR(dC);
+    REQUIRE_PTR(dmem);
+    REQUIRE_PTR(dz);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::sma_bwd_workspace_bytes(s);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return hip_status(dart::launch_sma_bwd(s, sma_args(opts), q, e, Cm, mem, z, lse, dy, dq, de, dC,
+                                           dmem, dz, workspace, (hipStream_t)stream),
+                      "dart_sma_bwd launch");
 }
 
 size_t dart_decode_workspace_bytes(const dart_dims* dims) {
@@ -201,7 +244,7 @@ dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, i
     const size_t need = dart::decode_workspace_bytes(s);
     if (workspace_bytes < need)
         return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
-    dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
+    const dart::SmaArgs a = sma_args(opts);
     return hip_status(dart::launch_decode(s, a, pos, nullptr, x, dt, A, Bm, Cm, q, e, z, h_state,
                                           chunk_acc, mem_cache, y, workspace, (hipStream_t)stream),
                       "dart_decode_step launch");
@@ -242,7 +285,7 @@ dart_status dart_decode_step_ragged(const dart_dims* dims, const dart_sma_opts* 
     const size_t need = dart::decode_workspace_bytes(s);
     if (workspace_bytes < need)
         return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
-    dart::SmaArgs a{opts->eps, opts->q_norm_w, opts->e_norm_w, opts->normalize, opts->z_per_head};
+    const dart::SmaArgs a = sma_args(opts);
     return hip_status(dart::launch_decode(s, a, pos_max, pos, x, dt, A, Bm, Cm, q, e, z, h_state,
                                           chunk_acc, mem_cache, y, workspace, (hipStream_t)stream),
                       "dart_decode_step_ragged launch");

@@ -40,6 +40,19 @@ hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const voi
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
                       float* lse, void* ws, hipStream_t st);
 
+// Key side r (.) dH of memories 0..M-2 in the cache layout [B][M-1][H][N][P]
+// (storage dtype), as the fp32 forward stages it.
+hipError_t launch_sma_keys(const Shape& s, const SmaArgs& a, const void* mem, void* kmem,
+                           hipStream_t st);
+
+// SMA backward: key side, Qbar/Ebar, per-(head, memory, token) softmax
+// scalars, per-head-block partial token gradients and R . dy.
+size_t sma_bwd_workspace_bytes(const Shape& s);
+hipError_t launch_sma_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                          const void* Cm, const void* mem, const void* z, const float* lse,
+                          const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
+                          void* ws, hipStream_t st);
+
 // Decode: per-split partial softmax statistics [B][H][nsplit][P+2] and the
 // SSM readout y_ssd [B][H][P] (float).
 constexpr int kDecodeMinMemPerSplit = 8;  // smallest split size the workspace allows

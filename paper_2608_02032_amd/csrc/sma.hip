@@ -1493,6 +1493,29 @@ hipError_t run_sma_n(const Shape& s, const SmaArgs& a, const void* q, const void
 
 }  // namespace
 
+hipError_t launch_sma_keys(const Shape& s, const SmaArgs& a, const void* mem, void* kmem,
+                           hipStream_t st) {
+    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
+    if (Mp == 0) return hipSuccess;
+    const dim3 grid((unsigned)Mp, (unsigned)s.H, (unsigned)s.B);
+    prof_begin("k_sma_keys", st);
+    if (s.dtype == 1) {
+        switch (s.N) {
+            case 32: k_sma_keys<bf16, 32><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 64: k_sma_keys<bf16, 64><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 128: k_sma_keys<bf16, 128><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+        }
+    } else {
+        switch (s.N) {
+            case 32: k_sma_keys<float, 32><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 64: k_sma_keys<float, 64><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 128: k_sma_keys<float, 128><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+        }
+    }
+    prof_end(st);
+    return hipGetLastError();
+}
+
 size_t sma_workspace_bytes(const Shape& s) {
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
     // bf16: key and value sides; fp32: key side only

@@ -1,0 +1,735 @@
+// sma_bwd.hip -- backward of the state-memory attention with the gated residual.
+//
+// Paper: Sec. 3 ("State-Memory Attention", "Gated Residual Integration"),
+// App. B.1 (normalised scores) and App. C (the backward recomputes the scores
+// from the stored log-sum-exp instead of keeping the attention weights).
+//
+// For the loss sum_t dy_t . y_t, token t of chunk i, memory j < i, with
+// p_j = exp(l_j - LSE_t) (the forward's weights, recovered exactly), gate
+// g = SiLU(z_t), s = 1/sqrt(N) and the key side Kh_j = r_j (.) dH_j:
+//   dwy_j = dy_t . V_j = C_t . (dH_j dy_t)     Dy = sum_j p_j dwy_j = R_t . dy_t
+//   dl_j  = g p_j (dwy_j - Dy)                 (softmax backward, dR = g dy)
+//   dC_t  += g p_j dH_j dy_t                   (V_j = C_t dH_j)
+//   dQbar += s dl_j Kh_j Ebar_t                (l_j = s Qbar . Kh_j Ebar)
+//   dEbar += s dl_j Kh_j^T Qbar_t
+//   dz_t   = SiLU'(z_t) Dy                     (summed over heads for one gate)
+// and, per memory j, over the later tokens t:
+//   M1 = sum_t g p_j[t] C_t^T dy_t,   M2 = sum_t s dl_j[t] Qbar_t^T Ebar_t
+//   ddH_j = M1 + r_j (.) M2 - (r_j^3 / P) (.) rowsum(dH_j (.) M2) (.) dH_j
+// (the last term through r_j = (mean_p dH_j^2 + eps)^-1/2 of the stored
+// values; r = 1 and no such term without normalisation).  q and e gradients
+// follow through RMSNorm with the weights held constant.
+//
+// Kernels, in launch order:
+//   k_sma_keys          key side Kh_j, shared with the forward (cache layout)
+//   k_bwd_prep          Qbar (scaled by log2(e)/sqrt(N), storage dtype, the
+//                       forward's operand exactly) and Ebar (float) per token
+//   k_bwd_tokens        one workgroup per (64 tokens of one chunk, block of
+//                       heads of one group); per head two passes over the
+//                       memories, tiles copied into LDS by DMA one step ahead:
+//                         pass 1: W' = Kh^T Qbar' -> logits -> p;
+//                                 X = dH dy^T -> dwy, dC += g p X;
+//                         pass 2: W' again -> dEbar; Z = Kh Ebar^T -> dQbar,
+//                       with tokens on the MFMA column side so every per-token
+//                       scalar is per lane.  It writes g p_j[t] and s' dl_j[t]
+//                       per (b, h, j, t) for the memory kernel, R . dy per
+//                       (b, t, h) and per-head-block partial sums of dQbar,
+//                       dEbar, dC.
+//   k_bwd_mem           one workgroup per (b, h, j): M1 and M2 over the later
+//                       tokens in 32-token steps (scaled operands staged in
+//                       LDS from registers loaded one step ahead), then the
+//                       epilogue above.  Heavy memories (small j) go first.
+//   k_bwd_finish        one wave per (b, t, group): sums the partials over the
+//                       group's head blocks, RMSNorm backward, dz.
+#include "dart_common.hpp"
+#include "dart_internal.hpp"
+
+namespace dart {
+namespace {
+
+constexpr int kP = 64;
+constexpr int kTokWaves = 4;
+constexpr int kTokBlock = 16 * kTokWaves;  // tokens per k_bwd_tokens workgroup
+constexpr int kMemTB = 32;                 // tokens per k_bwd_mem step
+constexpr int kHeadsPerBlock = 8;
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+    return v;
+}
+
+// An empty use of every register of a fragment: the compiler waits for its
+// loads here (16-byte pieces, so the asm operands stay 128-bit wide).
+__device__ __forceinline__ void keep(const bf16x8& f) { asm volatile("" ::"v"(f)); }
+__device__ __forceinline__ void keep(const f32x8& f) {
+    const f32x4 a{f[0], f[1], f[2], f[3]}, b{f[4], f[5], f[6], f[7]};
+    asm volatile("" ::"v"(a), "v"(b));
+}
+
+__device__ __forceinline__ float silu_grad(float z) {
+    const float sg = 1.0f / (1.0f + __expf(-z));
+    return sg * (1.0f + z * (1.0f - sg));
+}
+
+// 4-byte global -> LDS copy by DMA, invisible to the compiler's wait-count
+// tracking (lane i lands at lds_base + 4 i); the caller waits with vmcnt.
+__device__ __forceinline__ void lds_dma4_at(const void* gsrc, uint32_t lds_base) {
+    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_base);
+    uint32_t save;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dword %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(save)
+        : "v"(gsrc), "s"(m0)
+        : "memory");
+}
+
+// ---- Qbar' and Ebar per (b, t, g) row: one wave per row ---------------------
+// Qbar' = RMSNorm(q) w * log2(e)/sqrt(N) rounded to the storage dtype (the
+// forward's score operand); Ebar = RMSNorm(e) w in float.  Without
+// normalisation the raw vectors (times log2(e)/sqrt(N) for q).
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const T* __restrict__ e,
+                                                  const float* __restrict__ qw,
+                                                  const float* __restrict__ ew, T* __restrict__ qb,
+                                                  float* __restrict__ eb, float eps, int normalize,
+                                                  int64_t rows) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    constexpr int QE = (N + 63) / 64;
+    float qv[QE];
+    float ss = 0.f;
+#pragma unroll
+    for (int k = 0; k < QE; ++k) {
+        const int n = lane + 64 * k;
+        qv[k] = n < N ? to_f(q[row * N + n]) : 0.f;
+        ss += qv[k] * qv[k];
+    }
+    ss = wave_sum(ss);
+    const float qscale = kLog2e / sqrtf((float)N);
+    const float qinv = (normalize ? 1.0f / sqrtf(ss * (1.0f / N) + eps) : 1.0f) * qscale;
+#pragma unroll
+    for (int k = 0; k < QE; ++k) {
+        const int n = lane + 64 * k;
+        if (n < N) {
+            float v = qv[k] * qinv;
+            if (qw) v *= qw[n];
+            qb[row * N + n] = from_f<T>(v);
+        }
+    }
+    const float ev = to_f(e[row * kP + lane]);
+    const float es = wave_sum(ev * ev);
+    const float einv = normalize ? 1.0f / sqrtf(es * (1.0f / kP) + eps) : 1.0f;
+    float v = ev * einv;
+    if (ew) v *= ew[lane];
+    eb[row * kP + lane] = v;
+}
+
+// ---- token-side gradients ------------------------------------------------------
+// Workgroup: 64 consecutive tokens of chunk i >= 1 (all in one chunk because
+// S is a multiple of 64) and hpb heads of one group.  Wave w owns tokens
+// 16 w .. 16 w + 15; in every MFMA product the memory tile is the A operand
+// (rows n or p) and the tokens are the 16 columns, so lane l works on token
+// l % 16 and its rows 4 (l / 16) + 0..3 of each 16-row tile.
+//
+// Steps k = 0 .. hpb * 2 i - 1 run (head, pass, memory) in order; the tiles of
+// step k + 1 (Kh_j, and dH_j in pass 1) are copied into the other LDS buffer
+// while step k computes.  Pass 2 reads back the g p_j and dwy_j this wave
+// wrote in pass 1 through a 4-byte DMA into LDS, issued after the step's
+// stores.
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_bwd_tokens(
+    const T* __restrict__ qb, const float* __restrict__ eb, const T* __restrict__ Cm,
+    const T* __restrict__ mem, const T* __restrict__ kmem, const T* __restrict__ z,
+    const float* __restrict__ lse, const T* __restrict__ dy, float* __restrict__ gpw,
+    float* __restrict__ gdw, float* __restrict__ part, float* __restrict__ rdy, int z_per_head,
+    int64_t L, int H, int G, int S, int64_t Mcap, int64_t Mp, int hpb, int blk0) {
+    constexpr int RB = kP * (int)sizeof(T);  // bytes of one tile row (fixed n)
+    constexpr int TILE = N * RB;
+    constexpr int NT = N / 16;
+    constexpr int KQ = N / 32;
+    __shared__ __attribute__((aligned(16))) char khl[2][TILE];
+    __shared__ __attribute__((aligned(16))) char dhl[2][TILE];
+    __shared__ float scl[2][kTokWaves][32];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t b = blockIdx.z;
+    const int hb = blockIdx.y;
+    const int64_t t0 = (int64_t)(blk0 + (int64_t)blockIdx.x) * kTokBlock;
+    const int nj = (int)(t0 / S);  // memories every token of the block attends
+    const int64_t t = t0 + wave * 16 + col;
+    const bool valid = t < L;
+    const int64_t tc = valid ? t : L - 1;
+    const int h0 = hb * hpb;
+    const int g = h0 / (H / G);
+    const int64_t bt = b * L + tc;
+    const float isn = 1.0f / sqrtf((float)N);
+
+    // group-shared token operands
+    Frag<T> qf[KQ];
+    {
+        const T* qrow = qb + (bt * G + g) * N;
+#pragma unroll
+        for (int ks = 0; ks < KQ; ++ks) {
+            float a[4], c[4], v[8];
+            load4(qrow + ks * 32 + 4 * grp, a);
+            load4(qrow + ks * 32 + 16 + 4 * grp, c);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[i] = a[i];
+                v[4 + i] = c[i];
+            }
+            qf[ks] = make_frag<T>(v);
+        }
+    }
+    const float* erow = eb + (bt * G + g) * kP;
+    Frag<T> ef[2];
+    float ea[4][4];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        float v[8];
+        load8(erow + ks * 32 + 8 * grp, v);
+        ef[ks] = make_frag<T>(v);
+    }
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) load4(erow + 16 * pt + 4 * grp, ea[pt]);
+    float ca[NT][4];
+    {
+        const T* crow = Cm + (bt * G + g) * N;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) load4(crow + 16 * nt + 4 * grp, ca[nt]);
+    }
+
+    f32x4 dQ[NT], dC[NT], dE[4];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) dQ[nt] = dC[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) dE[pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nsteps = hpb * 2 * nj;
+    auto decode = [&](int k, int& hh, int& pass, int& j) {
+        hh = k / (2 * nj);
+        const int rem = k - hh * 2 * nj;
+        pass = rem >= nj ? 1 : 0;
+        j = rem - pass * nj;
+    };
+    auto issue_tiles = [&](int k) {
+        int hh, pass, j;
+        decode(k, hh, pass, j);
+        const int64_t hj = ((b * Mp + j) * H + h0 + hh) * (int64_t)N * kP;
+        dma_tile<RB, true>(khl[k & 1], reinterpret_cast<const char*>(kmem + hj), RB, N, N, wave,
+                           kTokWaves, lane);
+        if (!pass) {
+            const int64_t mj = ((b * Mcap + j) * H + h0 + hh) * (int64_t)N * kP;
+            dma_tile<RB, true>(dhl[k & 1], reinterpret_cast<const char*>(mem + mj), RB, N, N,
+                               wave, kTokWaves, lane);
+        }
+    };
+    // per (head, memory) scalar slot of this lane's token
+    auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * L + tc; };
+
+    issue_tiles(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
+
+    Frag<T> dyf[2];
+    float lse2 = 0.f, gate = 0.f, Dy = 0.f;
+    for (int k = 0; k < nsteps; ++k) {
+        int hh, pass, j;
+        decode(k, hh, pass, j);
+        const int h = h0 + hh;
+        if (pass == 0 && j == 0) {
+            // this head's per-token operands, waited for before the next copies
+            const T* dyrow = dy + (bt * H + h) * kP;
+            dyf[0] = load_frag(dyrow + 8 * grp);
+            dyf[1] = load_frag(dyrow + 32 + 8 * grp);
+            lse2 = lse[bt * H + h] * kLog2e;
+            gate = silu(to_f(z[z_per_head ? bt * H + h : bt]));
+            Dy = 0.f;
+            keep(dyf[0]);
+            keep(dyf[1]);
+            asm volatile("" ::"v"(lse2), "v"(gate));
+        }
+        if (k + 1 < nsteps) issue_tiles(k + 1);
+        const char* kt = khl[k & 1];
+        // W'^T = Kh^T Qbar'^T: rows p, token columns (log2-scaled scores)
+        f32x4 w[4];
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) w[pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KQ; ++ks) {
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt)
+                w[pt] = mma16(w[pt], frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp,
+                                                   16 * pt, lane),
+                              qf[ks]);
+        }
+        if (pass == 0) {
+            float l2 = 0.f;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) l2 += ea[pt][i] * w[pt][i];
+            l2 += shfl_xor(l2, 16);
+            l2 += shfl_xor(l2, 32);
+            const float p = fast_exp2(l2 - lse2);
+            // X^T = dH dy^T: rows n, token columns
+            const char* dt = dhl[k & 1];
+            f32x4 x[NT];
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                x[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+                    x[nt] = mma16(x[nt], frag_rowmajor<T, RB>(dt, 16 * nt + col, 32 * ks + 8 * grp),
+                                  dyf[ks]);
+            }
+            float dw = 0.f;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) dw += ca[nt][i] * x[nt][i];
+            dw += shfl_xor(dw, 16);
+            dw += shfl_xor(dw, 32);
+            Dy += p * dw;
+            const float gp = gate * p;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) dC[nt] += gp * x[nt];
+            if (lane < 16 && valid) {
+                gpw[sidx(h, j)] = gp;
+                gdw[sidx(h, j)] = dw;
+                if (j == nj - 1) rdy[bt * H + h] = Dy;
+            }
+        } else {
+            const float gp = scl[k & 1][wave][col];
+            const float dw = scl[k & 1][wave][16 + col];
+            const float dl = gp * (dw - Dy);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) dE[pt] += (dl * kLn2) * w[pt];
+            // Z^T = Kh Ebar^T: rows n, token columns
+            f32x4 zz[NT];
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                zz[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+                    zz[nt] = mma16(zz[nt], frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp),
+                                   ef[ks]);
+            }
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) dQ[nt] += (dl * isn) * zz[nt];
+            if (lane < 16 && valid) gdw[sidx(h, j)] = dl * kLn2;
+        }
+        // scalars of the next step when it is a pass-2 step (written by this
+        // wave in pass 1; with a single memory, by this very step)
+        if (k + 1 < nsteps) {
+            int hn, pn, jn;
+            decode(k + 1, hn, pn, jn);
+            if (pn == 1) {
+                if (nj == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+                if (lane < 32) {
+                    const float* src = (lane < 16 ? gpw : gdw) + sidx(h0 + hn, jn);
+                    lds_dma4_at(src, lds_addr(&scl[(k + 1) & 1][wave][0]));
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        lds_barrier();
+    }
+
+    if (!valid) return;
+    // per-head-block partial sums: dQbar [N], dEbar [P], dC [N]
+    float* pr = part + (bt * gridDim.y + hb) * (2 * N + kP);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[nt];
+        *reinterpret_cast<f32x4*>(pr + N + kP + 16 * nt + 4 * grp) = dC[nt];
+    }
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) *reinterpret_cast<f32x4*>(pr + N + 16 * pt + 4 * grp) = dE[pt];
+}
+
+// ---- memory-side gradients -------------------------------------------------------
+// Workgroup (b, h, j): M1 = sum_t (g p_j[t] C_t)^T dy_t and
+// M2 = sum_t (s' dl_j[t] Qbar'_t)^T Ebar_t over tokens t >= (j+1) S, 32 per
+// step.  The four token-major tiles of a step (scaled C, scaled Qbar', dy,
+// Ebar) are staged in LDS in the storage dtype; wave w owns the output
+// columns p = 16 w .. 16 w + 15 of every n tile.  Slots j >= M-1 (attended
+// by no token) are written as zeros.
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_bwd_mem(const T* __restrict__ qb,
+                                                 const float* __restrict__ eb,
+                                                 const T* __restrict__ Cm, const T* __restrict__ dy,
+                                                 const T* __restrict__ mem,
+                                                 const float* __restrict__ gpw,
+                                                 const float* __restrict__ gdw,
+                                                 float* __restrict__ dmem, float eps, int normalize,
+                                                 int64_t L, int H, int G, int S, int64_t Mcap,
+                                                 int64_t Mp, int64_t BH) {
+    constexpr int ES = (int)sizeof(T);
+    constexpr int RBN = N * ES, RBP = kP * ES;
+    constexpr int CT = kMemTB * RBN, DT = kMemTB * RBP;
+    constexpr int BUF = 2 * CT + 2 * DT;
+    constexpr int NT = N / 16;
+    constexpr int PCN = kMemTB * N / 8;   // 8-element pieces of an N-wide tile
+    constexpr int PCP = kMemTB * kP / 8;  // ... of a P-wide tile
+    constexpr int TOT = 2 * PCN + 2 * PCP;
+    constexpr int PPT = (TOT + 255) / 256;
+    __shared__ __attribute__((aligned(16))) char buf[2][BUF];
+    __shared__ float red[2][4][N];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t j = (int64_t)blockIdx.x / BH;
+    const int64_t bh = (int64_t)blockIdx.x - j * BH;
+    const int64_t b = bh / H;
+    const int h = (int)(bh - b * H);
+    const int g = h / (H / G);
+    float* out = dmem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
+    if (j >= Mp) {
+        for (int q = tid; q < N * kP / 4; q += 256)
+            reinterpret_cast<f32x4*>(out)[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        return;
+    }
+    const int64_t tbeg = (j + 1) * S;
+    const int nblk = (int)((L - tbeg + kMemTB - 1) / kMemTB);
+    const float* gpr = gpw + ((b * H + h) * Mp + j) * L;
+    const float* gdr = gdw + ((b * H + h) * Mp + j) * L;
+
+    float rv[PPT][8];
+    float rs[PPT];
+    auto load_block = [&](int blk) {
+#pragma unroll
+        for (int k = 0; k < PPT; ++k) {
+            const int q = tid + 256 * k;
+            rs[k] = 0.f;
+            if (q >= TOT) continue;
+            int r, c;
+            if (q < 2 * PCN) {
+                const int qq = q < PCN ? q : q - PCN;
+                r = qq / (N / 8);
+                c = qq % (N / 8);
+            } else {
+                const int qq = q < 2 * PCN + PCP ? q - 2 * PCN : q - 2 * PCN - PCP;
+                r = qq / (kP / 8);
+                c = qq % (kP / 8);
+            }
+            const int64_t tt = tbeg + (int64_t)blk * kMemTB + r;
+            const bool ok = tt < L;
+            const int64_t tk = ok ? tt : L - 1;
+            const int64_t btk = b * L + tk;
+            if (q < PCN) {
+                load8(Cm + (btk * G + g) * N + 8 * c, rv[k]);
+                rs[k] = ok ? gpr[tk] : 0.f;
+            } else if (q < 2 * PCN) {
+                load8(qb + (btk * G + g) * N + 8 * c, rv[k]);
+                rs[k] = ok ? gdr[tk] : 0.f;
+            } else if (q < 2 * PCN + PCP) {
+                load8(dy + (btk * H + h) * kP + 8 * c, rv[k]);
+                rs[k] = 1.f;
+            } else {
+                load8(eb + (btk * G + g) * kP + 8 * c, rv[k]);
+                rs[k] = 1.f;
+            }
+        }
+    };
+    auto store_block = [&](char* dst) {
+#pragma unroll
+        for (int k = 0; k < PPT; ++k) {
+            const int q = tid + 256 * k;
+            if (q >= TOT) continue;
+            char* tile;
+            int r, c, rb;
+            if (q < 2 * PCN) {
+                const int qq = q < PCN ? q : q - PCN;
+                tile = dst + (q < PCN ? 0 : CT);
+                r = qq / (N / 8);
+                c = qq % (N / 8);
+                rb = RBN;
+            } else {
+                const bool isdy = q < 2 * PCN + PCP;
+                const int qq = isdy ? q - 2 * PCN : q - 2 * PCN - PCP;
+                tile = dst + 2 * CT + (isdy ? 0 : DT);
+                r = qq / (kP / 8);
+                c = qq % (kP / 8);
+                rb = RBP;
+            }
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = rv[k][i] * rs[k];
+            // 8 elements = 16 bytes (bf16) or two 16-byte chunks (fp32)
+#pragma unroll
+            for (int hf = 0; hf < ES / 2; ++hf) {
+                const int byte = 8 * c * ES + 16 * hf;
+                const int cpr = rb / 16;
+                const int mask = (cpr < 8 ? cpr : 8) - 1;
+                const int o = r * rb + ((((byte >> 4) ^ (r & mask)) << 4));
+                if constexpr (ES == 2) {
+                    *reinterpret_cast<bf16x8*>(tile + o) = make_frag<bf16>(v);
+                } else {
+                    *reinterpret_cast<f32x4*>(tile + o) =
+                        f32x4{v[4 * hf], v[4 * hf + 1], v[4 * hf + 2], v[4 * hf + 3]};
+                }
+            }
+        }
+    };
+
+    f32x4 m1[NT], m2[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) m1[nt] = m2[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    load_block(0);
+    store_block(buf[0]);
+    __syncthreads();
+    for (int blk = 0; blk < nblk; ++blk) {
+        if (blk + 1 < nblk) load_block(blk + 1);
+        const char* cs = buf[blk & 1];
+        const char* qs = cs + CT;
+        const char* dyt = cs + 2 * CT;
+        const char* et = dyt + DT;
+        const Frag<T> b1 = frag_km<T, RBP>(dyt, 4 * grp, 16 + 4 * grp, 16 * wave, lane);
+        const Frag<T> b2 = frag_km<T, RBP>(et, 4 * grp, 16 + 4 * grp, 16 * wave, lane);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            m1[nt] = mma16(m1[nt], frag_km<T, RBN>(cs, 4 * grp, 16 + 4 * grp, 16 * nt, lane), b1);
+            m2[nt] = mma16(m2[nt], frag_km<T, RBN>(qs, 4 * grp, 16 + 4 * grp, 16 * nt, lane), b2);
+        }
+        if (blk + 1 < nblk) store_block(buf[(blk + 1) & 1]);
+        __syncthreads();
+    }
+
+    // epilogue: r[n] and dr[n] = sum_p dH[n,p] M2[n,p] reduced over the four
+    // waves' column tiles, then ddH
+    const T* hsrc = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
+    const int p = 16 * wave + col;
+    float hv[NT][4];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hv[nt][i] = to_f(hsrc[(16 * nt + 4 * grp + i) * kP + p]);
+    if (normalize) {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float s2 = dpp_group_sum<16>(hv[nt][i] * hv[nt][i]);
+                const float d2 = dpp_group_sum<16>(hv[nt][i] * m2[nt][i]);
+                if (col == 0) {
+                    red[0][wave][16 * nt + 4 * grp + i] = s2;
+                    red[1][wave][16 * nt + 4 * grp + i] = d2;
+                }
+            }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int n = 16 * nt + 4 * grp + i;
+            float o = m1[nt][i];
+            if (normalize) {
+                const float ss = red[0][0][n] + red[0][1][n] + red[0][2][n] + red[0][3][n];
+                const float dr = red[1][0][n] + red[1][1][n] + red[1][2][n] + red[1][3][n];
+                const float r = __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps);
+                o += r * m2[nt][i] - (r * r * r * (1.0f / kP)) * dr * hv[nt][i];
+            } else {
+                o += m2[nt][i];
+            }
+            out[n * kP + p] = o;
+        }
+}
+
+// ---- finishing: per (b, t, g) -------------------------------------------------------
+template <typename T, int N>
+__global__ __launch_bounds__(256) void k_bwd_finish(
+    const T* __restrict__ q, const T* __restrict__ e, const T* __restrict__ z,
+    const float* __restrict__ qw, const float* __restrict__ ew, const float* __restrict__ part,
+    const float* __restrict__ rdy, float* __restrict__ dq, float* __restrict__ de,
+    float* __restrict__ dC, float* __restrict__ dz, float eps, int normalize, int z_per_head,
+    int64_t L, int H, int G, int S, int hpb, int64_t rows) {
+    constexpr int QE = (N + 63) / 64;
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int g = (int)(row % G);
+    const int64_t bt = row / G;
+    const int64_t t = bt % L;
+    const bool hist = t >= S;  // tokens of the first chunk get no gradient
+    const int hpg = H / G;
+    const int nhb = H / hpb;
+    const int hb0 = g * hpg / hpb, hb1 = (g + 1) * hpg / hpb;
+    float sq[QE], sc[QE], se = 0.f;
+#pragma unroll
+    for (int k = 0; k < QE; ++k) sq[k] = sc[k] = 0.f;
+    if (hist) {
+        for (int hb = hb0; hb < hb1; ++hb) {
+            const float* pr = part + (bt * nhb + hb) * (2 * N + kP);
+#pragma unroll
+            for (int k = 0; k < QE; ++k) {
+                const int n = lane + 64 * k;
+                if (n < N) {
+                    sq[k] += pr[n];
+                    sc[k] += pr[N + kP + n];
+                }
+            }
+            se += pr[N + lane];
+        }
+    }
+    // q: dq = inv u - q inv^3 (u . q) / N with u = dQbar (.) w
+    float qv[QE], u[QE];
+    float ss = 0.f, uq = 0.f;
+#pragma unroll
+    for (int k = 0; k < QE; ++k) {
+        const int n = lane + 64 * k;
+        qv[k] = n < N ? to_f(q[row * N + n]) : 0.f;
+        u[k] = n < N ? sq[k] * (normalize && qw ? qw[n] : 1.0f) : 0.f;
+        ss += qv[k] * qv[k];
+        uq += u[k] * qv[k];
+    }
+    ss = wave_sum(ss);
+    uq = wave_sum(uq);
+    const float qi = 1.0f / sqrtf(ss * (1.0f / N) + eps);
+#pragma unroll
+    for (int k = 0; k < QE; ++k) {
+        const int n = lane + 64 * k;
+        if (n < N) {
+            dq[row * N + n] = normalize ? u[k] * qi - qv[k] * qi * qi * qi * uq * (1.0f / N) : sq[k];
+            dC[row * N + n] = sc[k];
+        }
+    }
+    const float ev = to_f(e[row * kP + lane]);
+    const float ue = se * (normalize && ew ? ew[lane] : 1.0f);
+    const float es = wave_sum(ev * ev);
+    const float ueu = wave_sum(ue * ev);
+    const float ei = 1.0f / sqrtf(es * (1.0f / kP) + eps);
+    de[row * kP + lane] = normalize ? ue * ei - ev * ei * ei * ei * ueu * (1.0f / kP) : se;
+    // gate
+    if (z_per_head) {
+        for (int k = lane; k < hpg; k += 64) {
+            const int h = g * hpg + k;
+            dz[bt * H + h] = hist ? silu_grad(to_f(z[bt * H + h])) * rdy[bt * H + h] : 0.f;
+        }
+    } else if (g == 0) {
+        float s = 0.f;
+        if (hist)
+            for (int h = lane; h < H; h += 64) s += rdy[bt * H + h];
+        s = wave_sum(s);
+        if (lane == 0) dz[bt] = hist ? silu_grad(to_f(z[bt])) * s : 0.f;
+    }
+}
+
+int bwd_heads_per_block(const Shape& s) {
+    const int per_group = s.H / s.G;
+    for (int c = kHeadsPerBlock; c > 1; c >>= 1)
+        if (per_group % c == 0) return c;
+    return 1;
+}
+
+struct BwdWs {
+    void* kmem;
+    void* qb;
+    float* eb;
+    float* gp;
+    float* gd;
+    float* part;
+    float* rdy;
+    size_t bytes;
+};
+
+BwdWs bwd_layout(const Shape& s, void* base) {
+    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
+    const size_t es = elem_bytes(s.dtype);
+    const int nhb = s.H / bwd_heads_per_block(s);
+    size_t o = 0;
+    BwdWs w;
+    char* p = reinterpret_cast<char*>(base);
+    auto take = [&](size_t bytes) {
+        void* r = p ? p + o : nullptr;
+        o += align256(bytes);
+        return r;
+    };
+    w.kmem = take(es * s.B * Mp * s.H * (size_t)s.N * s.P);
+    w.qb = take(es * s.B * s.L * s.G * (size_t)s.N);
+    w.eb = (float*)take(4 * s.B * s.L * s.G * (size_t)s.P);
+    w.gp = (float*)take(4 * s.B * s.H * Mp * (size_t)s.L);
+    w.gd = (float*)take(4 * s.B * s.H * Mp * (size_t)s.L);
+    w.part = (float*)take(4 * s.B * s.L * nhb * (size_t)(2 * s.N + s.P));
+    w.rdy = (float*)take(4 * s.B * s.L * (size_t)s.H);
+    w.bytes = o;
+    return w;
+}
+
+template <typename T, int N>
+hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* e, const void* Cm,
+                   const void* mem, const void* z, const float* lse, const void* dy, float* dq,
+                   float* de, float* dC, float* dmem, float* dz, void* ws, hipStream_t st) {
+    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
+    const BwdWs w = bwd_layout(s, ws);
+    const int hpb = bwd_heads_per_block(s);
+    hipError_t err;
+    if (Mp > 0) {
+        err = launch_sma_keys(s, a, mem, w.kmem, st);
+        if (err != hipSuccess) return err;
+    }
+    const int64_t rows = s.B * s.L * s.G;
+    const unsigned rblocks = (unsigned)((rows + 3) / 4);
+    prof_begin("k_bwd_prep", st);
+    k_bwd_prep<T, N><<<rblocks, 256, 0, st>>>((const T*)q, (const T*)e, a.qw, a.ew, (T*)w.qb, w.eb,
+                                              a.eps, a.normalize, rows);
+    prof_end(st);
+    const int blk0 = s.S / kTokBlock;
+    const int64_t nblk = (s.L + kTokBlock - 1) / kTokBlock - blk0;
+    if (Mp > 0 && nblk > 0) {
+        prof_begin("k_bwd_tokens", st);
+        k_bwd_tokens<T, N><<<dim3((unsigned)nblk, (unsigned)(s.H / hpb), (unsigned)s.B), 256, 0, st>>>(
+            (const T*)w.qb, w.eb, (const T*)Cm, (const T*)mem, (const T*)w.kmem, (const T*)z, lse,
+            (const T*)dy, w.gp, w.gd, w.part, w.rdy, a.z_per_head, s.L, s.H, s.G, s.S, s.Mcap, Mp,
+            hpb, blk0);
+        prof_end(st);
+    }
+    const int64_t BH = s.B * s.H;
+    prof_begin("k_bwd_mem", st);
+    k_bwd_mem<T, N><<<(unsigned)(BH * s.Mcap), 256, 0, st>>>(
+        (const T*)w.qb, w.eb, (const T*)Cm, (const T*)dy, (const T*)mem, w.gp, w.gd, dmem, a.eps,
+        a.normalize, s.L, s.H, s.G, s.S, s.Mcap, Mp, BH);
+    prof_end(st);
+    prof_begin("k_bwd_finish", st);
+    k_bwd_finish<T, N><<<rblocks, 256, 0, st>>>((const T*)q, (const T*)e, (const T*)z, a.qw, a.ew,
+                                                w.part, w.rdy, dq, de, dC, dz, a.eps, a.normalize,
+                                                a.z_per_head, s.L, s.H, s.G, s.S, hpb, rows);
+    prof_end(st);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t run_bwd_n(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                     const void* Cm, const void* mem, const void* z, const float* lse,
+                     const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
+                     void* ws, hipStream_t st) {
+    switch (s.N) {
+        case 32: return run_bwd<T, 32>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+        case 64: return run_bwd<T, 64>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+        case 128: return run_bwd<T, 128>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+size_t sma_bwd_workspace_bytes(const Shape& s) { return bwd_layout(s, nullptr).bytes; }
+
+hipError_t launch_sma_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                          const void* Cm, const void* mem, const void* z, const float* lse,
+                          const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
+                          void* ws, hipStream_t st) {
+    if (s.dtype == 1) return run_bwd_n<bf16>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+    return run_bwd_n<float>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+}
+
+}  // namespace dart

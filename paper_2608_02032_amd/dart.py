@@ -44,7 +44,8 @@ class SmaOpts(ctypes.Structure):
 
 
 EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspace_bytes",
-           "dart_sma_fwd", "dart_decode_workspace_bytes", "dart_decode_step",
+           "dart_sma_fwd", "dart_sma_bwd_workspace_bytes", "dart_sma_bwd",
+           "dart_decode_workspace_bytes", "dart_decode_step",
            "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
            "dart_profile_enable", "dart_profile_flush", "dart_profile_count",
            "dart_profile_name", "dart_profile_total_ms", "dart_profile_launches",
@@ -75,6 +76,10 @@ def load_library(path: str = LIB_PATH):
         lib.dart_sma_workspace_bytes.restype = sz
         lib.dart_sma_fwd.argtypes = [D, O, P, P, P, P, P, P, P, P, P, sz, P]
         lib.dart_sma_fwd.restype = st
+        lib.dart_sma_bwd_workspace_bytes.argtypes = [D]
+        lib.dart_sma_bwd_workspace_bytes.restype = sz
+        lib.dart_sma_bwd.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
+        lib.dart_sma_bwd.restype = st
         lib.dart_decode_workspace_bytes.argtypes = [D]
         lib.dart_decode_workspace_bytes.restype = sz
         lib.dart_decode_step.argtypes = [D, O, i64, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
@@ -227,6 +232,40 @@ def sma_fwd(q, e, Cm, mem, z, y_ssd, chunk, eps=DEFAULT_EPS, normalize=True, q_n
                            _ptr(mem), _ptr(z), _ptr(y_ssd), _ptr(y), _ptr(lse_t), _ptr(workspace),
                            workspace.numel(), _stream(stream)))
     return y, lse_t
+
+
+def sma_bwd(q, e, Cm, mem, z, lse, dy, chunk, eps=DEFAULT_EPS, normalize=True, q_norm_w=None,
+            e_norm_w=None, workspace=None, stream=None):
+    """Backward of sma_fwd for the loss sum(dy * y) (dart_sma_bwd).
+
+    lse [B][L][H] f32 is the forward's output; dy like y_ssd.  Returns a dict
+    of float32 tensors: dq, de, dC ([B][L][G][.], summed over each group's
+    heads), dmem (like mem) and dz (like z).  The gradient with respect to
+    y_ssd is dy itself.
+    """
+    torch = _torch()
+    lib = load_library()
+    B_, L, H, P = dy.shape
+    G, N = q.shape[2], q.shape[3]
+    dtype = _dtype_code(dy)
+    _check_f32(q_norm_w, "q_norm_w")
+    _check_f32(e_norm_w, "e_norm_w")
+    _check_f32(lse, "lse")
+    z_per_head = 1 if z.dim() == 3 else 0
+    dims = make_dims(B_, L, H, P, N, chunk, dtype, G, mem.shape[1])
+    opts = SmaOpts(float(eps), _ptr(q_norm_w), _ptr(e_norm_w), int(bool(normalize)), z_per_head)
+    f32 = dict(dtype=torch.float32, device=dy.device)
+    out = {"dq": torch.empty(q.shape, **f32), "de": torch.empty(e.shape, **f32),
+           "dC": torch.empty(Cm.shape, **f32), "dmem": torch.empty(mem.shape, **f32),
+           "dz": torch.empty(z.shape, **f32)}
+    need = lib.dart_sma_bwd_workspace_bytes(ctypes.byref(dims))
+    if workspace is None:
+        workspace = _workspace(need, dy.device)
+    check(lib.dart_sma_bwd(ctypes.byref(dims), ctypes.byref(opts), _ptr(q), _ptr(e), _ptr(Cm),
+                           _ptr(mem), _ptr(z), _ptr(lse), _ptr(dy), _ptr(out["dq"]),
+                           _ptr(out["de"]), _ptr(out["dC"]), _ptr(out["dmem"]), _ptr(out["dz"]),
+                           _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
 
 
 def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache, chunk,

@@ -198,3 +198,27 @@ def test_cache_ratio_closed_form_matches_paper(lib):
     for S, N, r in [(64, 128, 1.0), (16, 16, 0.5), (128, 64, 0.25)]:
         d = dart.make_dims(1, 0, 1, 64, N, S, "bf16")
         assert lib.dart_decode_cache_elems(ctypes.byref(d), 4096) / (2 * 4096 * 64) == r
+
+
+def test_sma_bwd_workspace_and_bad_arguments(lib):
+    d = dims()
+    M = 512 // 64
+    ws = lib.dart_sma_bwd_workspace_bytes(ctypes.byref(d))
+    # key side (storage dtype), normalised q (storage) and e (float), two floats
+    # per (b, h, attended memory, token), partials per head block, R . dy
+    assert ws >= (2 * 2 * (M - 1) * 4 * 64 * 64 + 2 * 2 * 512 * 64 + 4 * 2 * 512 * 64
+                  + 2 * 4 * 2 * 4 * (M - 1) * 512 + 4 * 2 * 512 * 4)
+    assert lib.dart_sma_bwd_workspace_bytes(ctypes.byref(dims(headdim=48))) == 0
+    o = dart.SmaOpts(1e-6, None, None, 1, 1)
+
+    def bwd(ptr_over=None, nbytes=1 << 40, opts=o):
+        p = [1] * 13
+        if ptr_over is not None:
+            p[ptr_over] = None
+        return lib.dart_sma_bwd(ctypes.byref(d), ctypes.byref(opts), *p, nbytes, None)
+    for k in range(13):
+        assert bwd(k) == dart.DART_ERR_INVALID_ARG
+        assert b"required pointer" in lib.dart_last_error()
+    assert bwd(nbytes=ws - 1) == dart.DART_ERR_INVALID_ARG
+    assert b"workspace too small" in lib.dart_last_error()
+    assert bwd(opts=dart.SmaOpts(0.0, None, None, 1, 1)) == dart.DART_ERR_INVALID_ARG

@@ -1,0 +1,159 @@
+"""GPU parity of the SMA backward (dart_sma_bwd) against the fp64 oracle
+backward (itself pinned by central differences of the oracle forward) on the
+same seeded inputs.  The GPU recomputes the softmax weights from the LSE its
+own forward returned.  Metric as the forward parity tests: per slice
+max|gpu - ref| / max|ref|.
+
+fp32 storage: against the exact oracle, 1e-4.
+bf16 storage: the bf16 path forms its logits from two bf16 operands (Qbar
+scaled by log2(e)/sqrt(N), and r (.) dH), exactly as its forward does.  With
+logits of rms about sqrt(P) = 8 that rounding moves each softmax weight by
+about 1 %, and the gradients, which are linear in the weights and in their
+differences, by up to a few %.  So bf16 is checked (a) per slice at 2e-2
+against the oracle evaluated with those two operands rounded to bf16
+(round_scores), which isolates the kernels' own error, and (b) against the
+exact oracle over each whole tensor at BF16_EXACT_TOL."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_02032_amd import dart, synth
+from tests.helpers import TOL, assert_close_slices, f32_dev, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+BF16_EXACT_TOL = 5e-2
+
+
+def announce(msg):
+    print("\n[gpu-case] " + msg, flush=True)
+
+
+def bwd_case(w, seed):
+    d = synth.forward_inputs(w, seed=seed)
+    rng = np.random.default_rng(seed + 200)
+    mem = synth.synthetic_memories(rng, w.batch, max(w.nchunks, w.mem_capacity), w.nheads,
+                                   w.dstate, w.headdim, w.dtype)
+    y_ssd = synth.to_storage(rng.standard_normal((w.batch, w.seqlen, w.nheads, w.headdim))
+                             .astype(np.float32) * 0.05, w.dtype)
+    dy = synth.to_storage(rng.standard_normal((w.batch, w.seqlen, w.nheads, w.headdim))
+                          .astype(np.float32), w.dtype)
+    return d, mem, y_ssd, dy
+
+
+def run_gpu(w, d, mem, y_ssd, dy, **kw):
+    import torch
+    q, e, Cm = (to_dev(d[k], w.dtype) for k in ("q", "e", "Cm"))
+    z = to_dev(d["z"], w.dtype)
+    mem_t = to_dev(mem, w.dtype)
+    _, lse = dart.sma_fwd(q, e, Cm, mem_t, z, to_dev(y_ssd, w.dtype), w.chunk, **kw)
+    g = dart.sma_bwd(q, e, Cm, mem_t, z, lse, to_dev(dy, w.dtype), w.chunk, **kw)
+    torch.cuda.synchronize()
+    return {k: to_np(v) for k, v in g.items()}
+
+
+def compare(w, got, ref, tol, tag="", whole=False):
+    M = w.nchunks
+    keep = lambda k: () if whole else k
+    for k in ("dq", "de", "dC"):
+        assert_close_slices(got[k], ref[k], tol, axes_keep=keep((0, 2)), what=k + tag)
+    zkeep = (0, 2) if got["dz"].ndim == 3 else (0,)
+    assert_close_slices(got["dz"], ref["dz"], tol, axes_keep=keep(zkeep), what="dz" + tag)
+    if M > 1:
+        assert_close_slices(got["dmem"][:, :M - 1], ref["dmem"][:, :M - 1], tol,
+                            axes_keep=keep((0, 1, 2)), what="dmem" + tag)
+    # memories no token attends get exactly zero
+    assert np.all(got["dmem"][:, M - 1:] == 0.0)
+    # tokens of the first chunk have no history: exactly zero
+    S = w.chunk
+    for k in ("dq", "de", "dC", "dz"):
+        assert np.all(got[k][:, :S] == 0.0), k
+
+
+BWD_CASES = [
+    synth.WORKLOADS["tiny_fp32_L512"],
+    synth.Workload("fp32_L700_N64_S128", 1, 700, 2, 64, 64, 128, "fp32"),
+    synth.Workload("fp32_L768_N128_S256_H3", 1, 768, 3, 64, 128, 256, "fp32"),
+    synth.Workload("bf16_L1280_N128_S256_H3", 2, 1280, 3, 64, 128, 256, "bf16"),
+    synth.Workload("bf16_L700_N64_S64", 1, 700, 2, 64, 64, 64, "bf16"),
+    synth.Workload("bf16_L1100_N32_S64_G2", 1, 1100, 4, 64, 32, 64, "bf16", ngroups=2),
+    # two blocks of eight heads, many memories, ragged tail
+    synth.Workload("bf16_L1000_N128_S128_H16", 1, 1000, 16, 64, 128, 128, "bf16"),
+    # one gate per token shared by every head
+    synth.Workload("bf16_L640_N64_S64_sharedz", 2, 640, 4, 64, 64, 64, "bf16", z_per_head=False),
+    # more memory slots than chunks: the extra slots get zero
+    synth.Workload("fp32_L300_N64_S64_cap8", 1, 300, 2, 64, 64, 64, "fp32", mem_capacity=8),
+]
+
+
+def check(w, got, d, mem, dy, tag="", **kw):
+    ref = oracle.sma_bwd(d["q"], d["e"], d["Cm"], mem, d["z"], dy, w.chunk, **kw)
+    if w.dtype == "fp32":
+        compare(w, got, ref, TOL["fp32"], tag)
+        return
+    compare(w, got, ref, BF16_EXACT_TOL, tag + " (exact, whole)", whole=True)
+    ref = oracle.sma_bwd(d["q"], d["e"], d["Cm"], mem, d["z"], dy, w.chunk, round_scores=True, **kw)
+    compare(w, got, ref, TOL["bf16"], tag + " (bf16 scores)")
+
+
+@pytest.mark.parametrize("w", BWD_CASES, ids=lambda w: w.name)
+def test_sma_bwd_matches_oracle(w):
+    announce("sma bwd %s" % (w,))
+    d, mem, y_ssd, dy = bwd_case(w, seed=11)
+    got = run_gpu(w, d, mem, y_ssd, dy)
+    check(w, got, d, mem, dy)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_sma_bwd_unnormalised_and_weighted(dtype):
+    w = synth.Workload("opts_%s_L640_N64_S128" % dtype, 1, 640, 4, 64, 64, 128, dtype)
+    announce("sma bwd options %s" % (w,))
+    d, mem, y_ssd, dy = bwd_case(w, seed=12)
+    # Alg. 1 as printed: raw Q, E, r = 1 (norm weights are ignored there)
+    rng = np.random.default_rng(3)
+    qw = (1.0 + 0.2 * rng.standard_normal(w.dstate)).astype(np.float32)
+    ew = (1.0 + 0.2 * rng.standard_normal(w.headdim)).astype(np.float32)
+    got = run_gpu(w, d, mem, y_ssd, dy, normalize=False, q_norm_w=f32_dev(qw),
+                  e_norm_w=f32_dev(ew))
+    check(w, got, d, mem, dy, " normalize=0", normalize=False)
+    # normalised with RMSNorm weights
+    got = run_gpu(w, d, mem, y_ssd, dy, q_norm_w=f32_dev(qw), e_norm_w=f32_dev(ew))
+    check(w, got, d, mem, dy, " weights", q_norm_w=qw, e_norm_w=ew)
+
+
+def test_sma_bwd_single_chunk_is_zero():
+    w = synth.Workload("one_chunk_bf16_L200_S256", 2, 200, 2, 64, 128, 256, "bf16")
+    announce("sma bwd one chunk %s" % (w,))
+    d, mem, y_ssd, dy = bwd_case(w, seed=13)
+    got = run_gpu(w, d, mem, y_ssd, dy)
+    for k, v in got.items():
+        assert np.all(v == 0.0), k
+
+
+def test_sma_bwd_full_size_sampled():
+    """At the L = 8192, 32-head, N = 128, S = 256 shape: the token gradients of
+    the first 1024 tokens equal those of the problem cut to L = 1024 (a
+    token's gradients involve only its own chunk's predecessors), checked
+    against the oracle there; the memory gradients of two sampled heads are
+    checked against a one-head oracle over the whole sequence."""
+    w = synth.WORKLOADS["sweep_L8192_S256_N128"]
+    w = synth.Workload(w.name + "_B1", 1, w.seqlen, w.nheads, w.headdim, w.dstate, w.chunk, w.dtype)
+    announce("sma bwd full size %s" % (w,))
+    d, mem, y_ssd, dy = bwd_case(w, seed=14)
+    got = run_gpu(w, d, mem, y_ssd, dy)
+    tol = TOL[w.dtype]
+    Lc = 1024
+    cut = {k: d[k][:, :Lc] for k in ("q", "e", "Cm", "z")}
+    ref = oracle.sma_bwd(cut["q"], cut["e"], cut["Cm"], mem, cut["z"], dy[:, :Lc], w.chunk,
+                         round_scores=True)
+    for k in ("dq", "de", "dC", "dz"):
+        assert_close_slices(got[k][:, :Lc], ref[k], tol, axes_keep=(0, 2),
+                            what=k + " (first 1024, bf16 scores)")
+    M = w.nchunks
+    for h in (5, 30):
+        r1 = oracle.sma_bwd(d["q"], d["e"], d["Cm"], mem[:, :, h:h + 1], d["z"][:, :, h:h + 1],
+                            dy[:, :, h:h + 1], w.chunk, round_scores=True)
+        assert_close_slices(got["dmem"][:, :M - 1, h:h + 1], r1["dmem"][:, :M - 1], tol,
+                            axes_keep=(0, 1, 2), what="dmem head %d (bf16 scores)" % h)
+        assert_close_slices(got["dz"][:, :, h:h + 1], r1["dz"], tol, axes_keep=(0, 2),
+                            what="dz head %d (bf16 scores)" % h)

@@ -525,3 +525,33 @@ def test_sma_backward_matches_finite_differences(normalize, z_per_head, G, weigh
     # the first chunk has no history and the last memory is never attended
     assert not np.any(g["dq"][:, :S]) and not np.any(g["dmem"][:, M - 1])
     np.testing.assert_array_equal(g["dy_ssd"], dy)
+
+
+def test_sma_backward_rounded_scores_reduce_to_exact_on_bf16_operands():
+    """round_scores = 1 (the logits from the bf16 path's two score operands,
+    Qbar log2(e)/sqrt(N) and r (.) dH, rounded to bf16) equals the exact
+    backward when both operands are already bf16 values: without normalisation
+    r = 1, so memories drawn as bf16 values and q = (bf16 value) sqrt(N)/log2(e)
+    leave nothing to round.  A wrong base conversion or scale in that branch
+    fails the first check; the second shows the option does round."""
+    rng = np.random.default_rng(21)
+    B_, L, H, G, P, N, S = 1, 48, 2, 1, 8, 16, 8
+    M = -(-L // S)
+    qr = synth.round_bf16(rng.standard_normal((B_, L, G, N)).astype(np.float32)).astype(np.float64)
+    q = qr * math.sqrt(N) / math.log2(math.e)
+    e = rng.standard_normal((B_, L, G, P))
+    C = rng.standard_normal((B_, L, G, N))
+    mem = synth.round_bf16(rng.standard_normal((B_, M, H, N, P)).astype(np.float32) * 0.3)
+    mem = mem.astype(np.float64)
+    z = rng.standard_normal((B_, L, H))
+    dy = rng.standard_normal((B_, L, H, P))
+    exact = oracle.sma_bwd(q, e, C, mem, z, dy, S, normalize=False)
+    rounded = oracle.sma_bwd(q, e, C, mem, z, dy, S, normalize=False, round_scores=True)
+    for k in ("dq", "de", "dC", "dmem", "dz"):
+        np.testing.assert_allclose(rounded[k], exact[k], rtol=1e-9, atol=1e-12, err_msg=k)
+    # generic operands: the rounding moves the gradients, by about bf16's step
+    q2 = rng.standard_normal((B_, L, G, N))
+    a = oracle.sma_bwd(q2, e, C, mem, z, dy, S)
+    b = oracle.sma_bwd(q2, e, C, mem, z, dy, S, round_scores=True)
+    rel = np.abs(a["dq"] - b["dq"]).max() / np.abs(a["dq"]).max()
+    assert 1e-5 < rel < 0.2
