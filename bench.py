@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--no-decode", action="store_true", help="time the forward only")
     ap.add_argument("--no-ragged", action="store_true",
                     help="skip the separately timed ragged-batch decode steps")
+    ap.add_argument("--no-bwd", action="store_true",
+                    help="skip the separately timed SMA backward on the same workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=4,
                     help="batches of the workload the CPU oracle is timed on")
@@ -93,6 +95,12 @@ def sma_bytes(w, esize=2):
             + zsz * esize                       # read z
             + B * L * H * P * esize * 2         # read y_ssd, write y
             + B * L * H * 4)                    # write lse
+
+
+def sma_bwd_flops(w):
+    """Backward per (token, earlier memory) pair: logits again, dy . V via
+    dH dy, dQbar via Kh Ebar (token side) and the two memory-side products."""
+    return w.batch * w.nheads * 10 * w.dstate * w.headdim * sma_pairs(w)
 
 
 def decode_bytes(d, esize=2):
@@ -374,6 +382,45 @@ def main():
             "us_per_step": round(rag_ms * 1e3, 2), "algorithmic_bytes": rbytes,
             "hbm_gbps": round(rbytes / (rag_ms * 1e-3) / 1e9, 1),
             "hbm_frac": round(rbytes / (rag_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+
+    if not args.no_bwd:
+        # SMA backward on the same workload (loss sum dy . y), timed on its own
+        # after the steps above, with the forward's LSE and memories
+        g = torch.Generator(device=dev)
+        g.manual_seed(4)
+        dy = torch.randn((B, L, H, P), generator=g, device=dev).to(bf)
+        f32 = dict(dtype=torch.float32, device=dev)
+        grads = {"dq": torch.empty(T["q"].shape, **f32), "de": torch.empty(T["e"].shape, **f32),
+                 "dC": torch.empty(T["Cm"].shape, **f32), "dmem": torch.empty(mem.shape, **f32),
+                 "dz": torch.empty(T["z"].shape, **f32)}
+        ws_bwd = torch.empty(dart.workspace_bytes("sma_bwd", dims), dtype=torch.uint8, device=dev)
+
+        def backward():
+            dart.sma_bwd(T["q"], T["e"], T["Cm"], mem, T["z"], lse, dy, S, out=grads,
+                         workspace=ws_bwd, stream=stream)
+        for _ in range(3):
+            backward()
+        R = 10
+        eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        dart.profile_reset()
+        dart.profile_enable(True)
+        eb[0].record(stream)
+        for _ in range(R):
+            backward()
+        eb[1].record(stream)
+        torch.cuda.synchronize()
+        dart.profile_enable(False)
+        bk = dart.profile_read(reset=True)
+        bavg = {k: v[0] / max(v[1], 1) for k, v in bk.items()}
+        bwd_ms = eb[0].elapsed_time(eb[1]) / R
+        bflops = sma_bwd_flops(w)
+        extra["sma_bwd"] = {
+            "us": round(bwd_ms * 1e3, 2), "algorithmic_flops": bflops,
+            "mfma_util": round(bflops / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "tokens_per_s": round(B * L / (bwd_ms * 1e-3), 1),
+            "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(bavg.items())}}
+        del ws_bwd, grads
 
     tokens = B * L
     line = {

@@ -25,18 +25,20 @@
 //   k_bwd_prep          Qbar (scaled by log2(e)/sqrt(N), storage dtype, the
 //                       forward's operand exactly) and Ebar (float) per token
 //   k_bwd_tokens        one workgroup per (64 tokens of one chunk, block of
-//                       heads of one group); per head two passes over the
-//                       memories, tiles copied into LDS by DMA one step ahead:
-//                         pass 1: W' = Kh^T Qbar' -> logits -> p;
-//                                 X = dH dy^T -> dwy, dC += g p X;
-//                         pass 2: W' again -> dEbar; Z = Kh Ebar^T -> dQbar,
-//                       with tokens on the MFMA column side so every per-token
-//                       scalar is per lane.  It writes g p_j[t] and s' dl_j[t]
-//                       per (b, h, j, t) for the memory kernel, R . dy per
-//                       (b, t, h) and per-head-block partial sums of dQbar,
-//                       dEbar, dC.
+//                       heads of one group); one pass over (head, memory),
+//                       tiles streamed through an LDS ring by DMA:
+//                         W' = Kh^T Qbar' -> logits -> p;
+//                         X = dH dy^T -> dwy, dC += g p X;
+//                         Z = Kh Ebar^T, with dQbar and dEbar formed from
+//                         running sums at the head's end (Dy is known then),
+//                       tokens on the MFMA column side so every per-token
+//                       scalar is per lane.  It writes g p_j[t] and dwy_j[t]
+//                       per (b, h, j, t) for the memory kernel, Dy = R . dy
+//                       per (b, t, h) and per-head-block partial sums of
+//                       dQbar, dEbar, dC.
 //   k_bwd_mem           one workgroup per (b, h, j): M1 and M2 over the later
-//                       tokens in 32-token steps (scaled operands staged in
+//                       tokens in 32-token steps, dl_j[t] formed from the
+//                       stored g p_j, dwy_j and Dy (scaled operands staged in
 //                       LDS from registers loaded one step ahead), then the
 //                       epilogue above.  Heavy memories (small j) go first.
 //   k_bwd_finish        one wave per (b, t, group): sums the partials over the
@@ -70,22 +72,6 @@ __device__ __forceinline__ void keep(const f32x8& f) {
 __device__ __forceinline__ float silu_grad(float z) {
     const float sg = 1.0f / (1.0f + __expf(-z));
     return sg * (1.0f + z * (1.0f - sg));
-}
-
-// 4-byte global -> LDS copy by DMA, invisible to the compiler's wait-count
-// tracking (lane i lands at lds_base + 4 i); the caller waits with vmcnt.
-__device__ __forceinline__ void lds_dma4_at(const void* gsrc, uint32_t lds_base) {
-    const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_base);
-    uint32_t save;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %2\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dword %1, off\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(save)
-        : "v"(gsrc), "s"(m0)
-        : "memory");
 }
 
 // ---- Qbar' and Ebar per (b, t, g) row: one wave per row ---------------------
@@ -137,31 +123,58 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
 // (rows n or p) and the tokens are the 16 columns, so lane l works on token
 // l % 16 and its rows 4 (l / 16) + 0..3 of each 16-row tile.
 //
-// Steps k = 0 .. hpb * 2 i - 1 run (head, pass, memory) in order; the tiles of
-// step k + 1 (Kh_j, and dH_j in pass 1) are copied into the other LDS buffer
-// while step k computes.  Pass 2 reads back the g p_j and dwy_j this wave
-// wrote in pass 1 through a 4-byte DMA into LDS, issued after the step's
-// stores.
+// One pass over (head, memory j) steps.  Per step: W' = Kh^T Qbar'^T (logits,
+// p_j), X = dH dy^T (dwy_j, dC += g p_j X) and Z = Kh Ebar^T.  dl_j needs
+// Dy = sum_j p_j dwy_j, known only after the head's last memory, so the head
+// accumulates S1 = sum_j p_j dwy_j Z_j, S2 = sum_j p_j Z_j (and T1, T2 with
+// W'), and adds g s (S1 - Dy S2) to dQbar and g ln2 (T1 - Dy T2) to dEbar at
+// its end (W' and Qbar' carry log2(e)/sqrt(N); ln2 takes it back to s).
+// Tiles (Kh_j, dH_j) stream through an NS-stage LDS ring by DMA, NS - 1 steps
+// ahead; each wave waits only for its own copies of the current step and one
+// barrier per step orders the stages.
+template <typename T, int N>
+constexpr int tok_stages() {
+    return (N * kP * (int)sizeof(T) * 2 * 4 <= 131072) ? 4 : 2;
+}
+
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_bwd_tokens(
     const T* __restrict__ qb, const float* __restrict__ eb, const T* __restrict__ Cm,
     const T* __restrict__ mem, const T* __restrict__ kmem, const T* __restrict__ z,
     const float* __restrict__ lse, const T* __restrict__ dy, float* __restrict__ gpw,
     float* __restrict__ gdw, float* __restrict__ part, float* __restrict__ rdy, int z_per_head,
-    int64_t L, int H, int G, int S, int64_t Mcap, int64_t Mp, int hpb, int blk0) {
+    int64_t L, int H, int G, int S, int64_t Mcap, int64_t Mp, int hpb, int blk0, int nblk,
+    int64_t BHC) {
     constexpr int RB = kP * (int)sizeof(T);  // bytes of one tile row (fixed n)
     constexpr int TILE = N * RB;
     constexpr int NT = N / 16;
     constexpr int KQ = N / 32;
-    __shared__ __attribute__((aligned(16))) char khl[2][TILE];
-    __shared__ __attribute__((aligned(16))) char dhl[2][TILE];
-    __shared__ float scl[2][kTokWaves][32];
+    constexpr int NS = tok_stages<T, N>();
+    constexpr int CPS = 2 * N * (RB / 16) / (64 * kTokWaves);  // DMA copies per wave per step
+    __shared__ __attribute__((aligned(16))) char ring[NS][2][TILE];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    const int64_t b = blockIdx.z;
-    const int hb = blockIdx.y;
-    const int64_t t0 = (int64_t)(blk0 + (int64_t)blockIdx.x) * kTokBlock;
+    // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
+    // index and each XCD has its own L2.  When the number of (b, head block)
+    // pairs is a multiple of 8, XCD x runs the token blocks of pairs x, x+8,
+    // ... one pair after another, heaviest first: the blocks running together
+    // on an XCD stream the same memory tiles in the same order.
+    const int64_t bid = blockIdx.x;
+    int blk;
+    int64_t bhc;
+    if (BHC % 8 == 0) {
+        const int64_t slot = bid >> 3;
+        blk = nblk - 1 - (int)(slot % nblk);
+        bhc = (slot / nblk) * 8 + (bid & 7);
+    } else {
+        blk = nblk - 1 - (int)(bid / BHC);
+        bhc = bid % BHC;
+    }
+    const int nhb = H / hpb;
+    const int64_t b = bhc / nhb;
+    const int hb = (int)(bhc % nhb);
+    const int64_t t0 = (int64_t)(blk0 + blk) * kTokBlock;
     const int nj = (int)(t0 / S);  // memories every token of the block attends
     const int64_t t = t0 + wave * 16 + col;
     const bool valid = t < L;
@@ -206,46 +219,48 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
         for (int nt = 0; nt < NT; ++nt) load4(crow + 16 * nt + 4 * grp, ca[nt]);
     }
 
-    f32x4 dQ[NT], dC[NT], dE[4];
+    const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
+    f32x4 dQ[NT], dC[NT], dE[4], s1[NT], s2[NT], u1[4], u2[4];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) dQ[nt] = dC[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nt = 0; nt < NT; ++nt) dQ[nt] = dC[nt] = zero4;
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) dE[pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int pt = 0; pt < 4; ++pt) dE[pt] = zero4;
 
-    const int nsteps = hpb * 2 * nj;
-    auto decode = [&](int k, int& hh, int& pass, int& j) {
-        hh = k / (2 * nj);
-        const int rem = k - hh * 2 * nj;
-        pass = rem >= nj ? 1 : 0;
-        j = rem - pass * nj;
-    };
+    const int nsteps = hpb * nj;
     auto issue_tiles = [&](int k) {
-        int hh, pass, j;
-        decode(k, hh, pass, j);
+        const int hh = k / nj, j = k - hh * nj;
         const int64_t hj = ((b * Mp + j) * H + h0 + hh) * (int64_t)N * kP;
-        dma_tile<RB, true>(khl[k & 1], reinterpret_cast<const char*>(kmem + hj), RB, N, N, wave,
-                           kTokWaves, lane);
-        if (!pass) {
-            const int64_t mj = ((b * Mcap + j) * H + h0 + hh) * (int64_t)N * kP;
-            dma_tile<RB, true>(dhl[k & 1], reinterpret_cast<const char*>(mem + mj), RB, N, N,
-                               wave, kTokWaves, lane);
-        }
+        const int64_t mj = ((b * Mcap + j) * H + h0 + hh) * (int64_t)N * kP;
+        dma_tile<RB, true>(ring[k % NS][0], reinterpret_cast<const char*>(kmem + hj), RB, N, N,
+                           wave, kTokWaves, lane);
+        dma_tile<RB, true>(ring[k % NS][1], reinterpret_cast<const char*>(mem + mj), RB, N, N,
+                           wave, kTokWaves, lane);
     };
     // per (head, memory) scalar slot of this lane's token
     auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * L + tc; };
 
-    issue_tiles(0);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    lds_barrier();
+#pragma unroll
+    for (int k = 0; k < NS - 1; ++k)
+        if (k < nsteps) issue_tiles(k);
 
     Frag<T> dyf[2];
     float lse2 = 0.f, gate = 0.f, Dy = 0.f;
     for (int k = 0; k < nsteps; ++k) {
-        int hh, pass, j;
-        decode(k, hh, pass, j);
+        const int hh = k / nj, j = k - hh * nj;
         const int h = h0 + hh;
-        if (pass == 0 && j == 0) {
-            // this head's per-token operands, waited for before the next copies
+        // this step's copies (the ones of the later steps in flight may stay)
+        const int ahead = nsteps - 1 - k < NS - 2 ? nsteps - 1 - k : NS - 2;
+        if (ahead >= 2) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * CPS));
+        } else if (ahead == 1) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPS));
+        } else {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        }
+        lds_barrier();
+        if (j == 0) {
+            // this head's per-token operands (waited for here, before the
+            // next copies are issued)
             const T* dyrow = dy + (bt * H + h) * kP;
             dyf[0] = load_frag(dyrow + 8 * grp);
             dyf[1] = load_frag(dyrow + 32 + 8 * grp);
@@ -255,13 +270,18 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
             keep(dyf[0]);
             keep(dyf[1]);
             asm volatile("" ::"v"(lse2), "v"(gate));
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) s1[nt] = s2[nt] = zero4;
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) u1[pt] = u2[pt] = zero4;
         }
-        if (k + 1 < nsteps) issue_tiles(k + 1);
-        const char* kt = khl[k & 1];
+        if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
+        const char* kt = ring[k % NS][0];
+        const char* dt = ring[k % NS][1];
         // W'^T = Kh^T Qbar'^T: rows p, token columns (log2-scaled scores)
         f32x4 w[4];
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt) w[pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int pt = 0; pt < 4; ++pt) w[pt] = zero4;
 #pragma unroll
         for (int ks = 0; ks < KQ; ++ks) {
 #pragma unroll
@@ -270,82 +290,65 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
                                                    16 * pt, lane),
                               qf[ks]);
         }
-        if (pass == 0) {
-            float l2 = 0.f;
+        float l2 = 0.f;
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt)
+        for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) l2 += ea[pt][i] * w[pt][i];
-            l2 += shfl_xor(l2, 16);
-            l2 += shfl_xor(l2, 32);
-            const float p = fast_exp2(l2 - lse2);
-            // X^T = dH dy^T: rows n, token columns
-            const char* dt = dhl[k & 1];
-            f32x4 x[NT];
+            for (int i = 0; i < 4; ++i) l2 += ea[pt][i] * w[pt][i];
+        l2 += shfl_xor(l2, 16);
+        l2 += shfl_xor(l2, 32);
+        const float p = fast_exp2(l2 - lse2);
+        // X^T = dH dy^T and Z^T = Kh Ebar^T: rows n, token columns
+        f32x4 x[NT], zz[NT];
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                x[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int nt = 0; nt < NT; ++nt) {
+            x[nt] = zz[nt] = zero4;
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
-                    x[nt] = mma16(x[nt], frag_rowmajor<T, RB>(dt, 16 * nt + col, 32 * ks + 8 * grp),
-                                  dyf[ks]);
-            }
-            float dw = 0.f;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) dw += ca[nt][i] * x[nt][i];
-            dw += shfl_xor(dw, 16);
-            dw += shfl_xor(dw, 32);
-            Dy += p * dw;
-            const float gp = gate * p;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) dC[nt] += gp * x[nt];
-            if (lane < 16 && valid) {
-                gpw[sidx(h, j)] = gp;
-                gdw[sidx(h, j)] = dw;
-                if (j == nj - 1) rdy[bt * H + h] = Dy;
-            }
-        } else {
-            const float gp = scl[k & 1][wave][col];
-            const float dw = scl[k & 1][wave][16 + col];
-            const float dl = gp * (dw - Dy);
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) dE[pt] += (dl * kLn2) * w[pt];
-            // Z^T = Kh Ebar^T: rows n, token columns
-            f32x4 zz[NT];
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                zz[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
-                    zz[nt] = mma16(zz[nt], frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp),
-                                   ef[ks]);
-            }
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) dQ[nt] += (dl * isn) * zz[nt];
-            if (lane < 16 && valid) gdw[sidx(h, j)] = dl * kLn2;
-        }
-        // scalars of the next step when it is a pass-2 step (written by this
-        // wave in pass 1; with a single memory, by this very step)
-        if (k + 1 < nsteps) {
-            int hn, pn, jn;
-            decode(k + 1, hn, pn, jn);
-            if (pn == 1) {
-                if (nj == 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-                if (lane < 32) {
-                    const float* src = (lane < 16 ? gpw : gdw) + sidx(h0 + hn, jn);
-                    lds_dma4_at(src, lds_addr(&scl[(k + 1) & 1][wave][0]));
-                }
+            for (int ks = 0; ks < 2; ++ks) {
+                x[nt] = mma16(x[nt], frag_rowmajor<T, RB>(dt, 16 * nt + col, 32 * ks + 8 * grp),
+                              dyf[ks]);
+                zz[nt] = mma16(zz[nt], frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp),
+                               ef[ks]);
             }
         }
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-        lds_barrier();
+        float dw = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dw += ca[nt][i] * x[nt][i];
+        dw += shfl_xor(dw, 16);
+        dw += shfl_xor(dw, 32);
+        Dy += p * dw;
+        const float gp = gate * p, pd = p * dw;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            dC[nt] += gp * x[nt];
+            s1[nt] += pd * zz[nt];
+            s2[nt] += p * zz[nt];
+        }
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) {
+            u1[pt] += pd * w[pt];
+            u2[pt] += p * w[pt];
+        }
+        if (lane < 16 && valid) {
+            gpw[sidx(h, j)] = gp;
+            gdw[sidx(h, j)] = dw;
+        }
+        if (j == nj - 1) {
+            // the head's dl_j = g p_j (dwy_j - Dy), summed against Z and W'
+            const float cq = gate * isn, ce = gate * kLn2;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) dQ[nt] += cq * (s1[nt] - Dy * s2[nt]);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) dE[pt] += ce * (u1[pt] - Dy * u2[pt]);
+            if (lane < 16 && valid) rdy[bt * H + h] = Dy;
+        }
     }
 
     if (!valid) return;
     // per-head-block partial sums: dQbar [N], dEbar [P], dC [N]
-    float* pr = part + (bt * gridDim.y + hb) * (2 * N + kP);
+    float* pr = part + (bt * nhb + hb) * (2 * N + kP);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
         *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[nt];
@@ -357,7 +360,7 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
 
 // ---- memory-side gradients -------------------------------------------------------
 // Workgroup (b, h, j): M1 = sum_t (g p_j[t] C_t)^T dy_t and
-// M2 = sum_t (s' dl_j[t] Qbar'_t)^T Ebar_t over tokens t >= (j+1) S, 32 per
+// M2 = sum_t (ln2 dl_j[t] Qbar'_t)^T Ebar_t over tokens t >= (j+1) S, 32 per
 // step.  The four token-major tiles of a step (scaled C, scaled Qbar', dy,
 // Ebar) are staged in LDS in the storage dtype; wave w owns the output
 // columns p = 16 w .. 16 w + 15 of every n tile.  Slots j >= M-1 (attended
@@ -369,6 +372,7 @@ __global__ __launch_bounds__(256) void k_bwd_mem(const T* __restrict__ qb,
                                                  const T* __restrict__ mem,
                                                  const float* __restrict__ gpw,
                                                  const float* __restrict__ gdw,
+                                                 const float* __restrict__ rdy,
                                                  float* __restrict__ dmem, float eps, int normalize,
                                                  int64_t L, int H, int G, int S, int64_t Mcap,
                                                  int64_t Mp, int64_t BH) {
@@ -429,7 +433,8 @@ __global__ __launch_bounds__(256) void k_bwd_mem(const T* __restrict__ qb,
                 rs[k] = ok ? gpr[tk] : 0.f;
             } else if (q < 2 * PCN) {
                 load8(qb + (btk * G + g) * N + 8 * c, rv[k]);
-                rs[k] = ok ? gdr[tk] : 0.f;
+                // ln2 dl_j = ln2 g p_j (dwy_j - Dy): Qbar' carries log2(e)/sqrt(N)
+                rs[k] = ok ? kLn2 * gpr[tk] * (gdr[tk] - rdy[btk * H + h]) : 0.f;
             } else if (q < 2 * PCN + PCP) {
                 load8(dy + (btk * H + h) * kP + 8 * c, rv[k]);
                 rs[k] = 1.f;
@@ -687,16 +692,17 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     const int64_t nblk = (s.L + kTokBlock - 1) / kTokBlock - blk0;
     if (Mp > 0 && nblk > 0) {
         prof_begin("k_bwd_tokens", st);
-        k_bwd_tokens<T, N><<<dim3((unsigned)nblk, (unsigned)(s.H / hpb), (unsigned)s.B), 256, 0, st>>>(
+        const int64_t BHC = s.B * (s.H / hpb);
+        k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 256, 0, st>>>(
             (const T*)w.qb, w.eb, (const T*)Cm, (const T*)mem, (const T*)w.kmem, (const T*)z, lse,
             (const T*)dy, w.gp, w.gd, w.part, w.rdy, a.z_per_head, s.L, s.H, s.G, s.S, s.Mcap, Mp,
-            hpb, blk0);
+            hpb, blk0, (int)nblk, BHC);
         prof_end(st);
     }
     const int64_t BH = s.B * s.H;
     prof_begin("k_bwd_mem", st);
     k_bwd_mem<T, N><<<(unsigned)(BH * s.Mcap), 256, 0, st>>>(
-        (const T*)w.qb, w.eb, (const T*)Cm, (const T*)dy, (const T*)mem, w.gp, w.gd, dmem, a.eps,
+        (const T*)w.qb, w.eb, (const T*)Cm, (const T*)dy, (const T*)mem, w.gp, w.gd, w.rdy, dmem, a.eps,
         a.normalize, s.L, s.H, s.G, s.S, s.Mcap, Mp, BH);
     prof_end(st);
     prof_begin("k_bwd_finish", st);

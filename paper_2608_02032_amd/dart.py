@@ -235,13 +235,13 @@ def sma_fwd(q, e, Cm, mem, z, y_ssd, chunk, eps=DEFAULT_EPS, normalize=True, q_n
 
 
 def sma_bwd(q, e, Cm, mem, z, lse, dy, chunk, eps=DEFAULT_EPS, normalize=True, q_norm_w=None,
-            e_norm_w=None, workspace=None, stream=None):
+            e_norm_w=None, out=None, workspace=None, stream=None):
     """Backward of sma_fwd for the loss sum(dy * y) (dart_sma_bwd).
 
     lse [B][L][H] f32 is the forward's output; dy like y_ssd.  Returns a dict
     of float32 tensors: dq, de, dC ([B][L][G][.], summed over each group's
     heads), dmem (like mem) and dz (like z).  The gradient with respect to
-    y_ssd is dy itself.
+    y_ssd is dy itself.  `out` may hold preallocated tensors under those keys.
     """
     torch = _torch()
     lib = load_library()
@@ -255,9 +255,15 @@ def sma_bwd(q, e, Cm, mem, z, lse, dy, chunk, eps=DEFAULT_EPS, normalize=True, q
     dims = make_dims(B_, L, H, P, N, chunk, dtype, G, mem.shape[1])
     opts = SmaOpts(float(eps), _ptr(q_norm_w), _ptr(e_norm_w), int(bool(normalize)), z_per_head)
     f32 = dict(dtype=torch.float32, device=dy.device)
-    out = {"dq": torch.empty(q.shape, **f32), "de": torch.empty(e.shape, **f32),
-           "dC": torch.empty(Cm.shape, **f32), "dmem": torch.empty(mem.shape, **f32),
-           "dz": torch.empty(z.shape, **f32)}
+    want = {"dq": q.shape, "de": e.shape, "dC": Cm.shape, "dmem": mem.shape, "dz": z.shape}
+    out = dict(out or {})
+    for k, shape in want.items():
+        if k not in out:
+            out[k] = torch.empty(shape, **f32)
+        elif tuple(out[k].shape) != tuple(shape) or out[k].dtype != torch.float32 \
+                or not out[k].is_contiguous():
+            raise ValueError("out[%r] must be a contiguous float32 tensor of shape %s"
+                             % (k, tuple(shape)))
     need = lib.dart_sma_bwd_workspace_bytes(ctypes.byref(dims))
     if workspace is None:
         workspace = _workspace(need, dy.device)
@@ -349,6 +355,7 @@ def decode_handoff(lengths, mem, h_last, chunk, h_state=None, chunk_acc=None, st
 def workspace_bytes(kind: str, dims: Dims) -> int:
     lib = load_library()
     fn = {"scan": lib.dart_scan_workspace_bytes, "sma": lib.dart_sma_workspace_bytes,
+          "sma_bwd": lib.dart_sma_bwd_workspace_bytes,
           "decode": lib.dart_decode_workspace_bytes}[kind]
     return int(fn(ctypes.byref(dims)))
 
