@@ -36,10 +36,11 @@
 //                       per (b, h, j, t) for the memory kernel, Dy = R . dy
 //                       per (b, t, h) and per-head-block partial sums of
 //                       dQbar, dEbar, dC.
-//   k_bwd_mem           one workgroup per (b, h, j): M1 and M2 over the later
-//                       tokens in 32-token steps, dl_j[t] formed from the
-//                       stored g p_j, dwy_j and Dy (scaled operands staged in
-//                       LDS from registers loaded one step ahead), then the
+//   k_bwd_mem           one workgroup per (b, h, 4 memories): M1 and M2 over
+//                       the later tokens, the token stream copied into LDS by
+//                       DMA once for the four memories, dl_j[t] formed from
+//                       the stored g p_j, dwy_j and Dy and applied to the
+//                       MFMA operand fragments in registers; then the
 //                       epilogue above.  Heavy memories (small j) go first.
 //   k_bwd_finish        one wave per (b, t, group): sums the partials over the
 //                       group's head blocks, RMSNorm backward, dz.
@@ -52,7 +53,7 @@ namespace {
 constexpr int kP = 64;
 constexpr int kTokWaves = 4;
 constexpr int kTokBlock = 16 * kTokWaves;  // tokens per k_bwd_tokens workgroup
-constexpr int kMemTB = 32;                 // tokens per k_bwd_mem step
+constexpr int kMemJ = 4;                   // memories per k_bwd_mem workgroup
 constexpr int kHeadsPerBlock = 8;
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -76,14 +77,15 @@ __device__ __forceinline__ float silu_grad(float z) {
 
 // ---- Qbar' and Ebar per (b, t, g) row: one wave per row ---------------------
 // Qbar' = RMSNorm(q) w * log2(e)/sqrt(N) rounded to the storage dtype (the
-// forward's score operand); Ebar = RMSNorm(e) w in float.  Without
+// forward's score operand); Ebar = RMSNorm(e) w in float, and (ebt != NULL)
+// also in the storage dtype for the memory kernel's MFMA operand.  Without
 // normalisation the raw vectors (times log2(e)/sqrt(N) for q).
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const T* __restrict__ e,
                                                   const float* __restrict__ qw,
                                                   const float* __restrict__ ew, T* __restrict__ qb,
-                                                  float* __restrict__ eb, float eps, int normalize,
-                                                  int64_t rows) {
+                                                  float* __restrict__ eb, T* __restrict__ ebt,
+                                                  float eps, int normalize, int64_t rows) {
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -114,6 +116,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
     float v = ev * einv;
     if (ew) v *= ew[lane];
     eb[row * kP + lane] = v;
+    if (ebt) ebt[row * kP + lane] = from_f<T>(v);
 }
 
 // ---- token-side gradients ------------------------------------------------------
@@ -359,15 +362,32 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
 }
 
 // ---- memory-side gradients -------------------------------------------------------
-// Workgroup (b, h, j): M1 = sum_t (g p_j[t] C_t)^T dy_t and
-// M2 = sum_t (ln2 dl_j[t] Qbar'_t)^T Ebar_t over tokens t >= (j+1) S, 32 per
-// step.  The four token-major tiles of a step (scaled C, scaled Qbar', dy,
-// Ebar) are staged in LDS in the storage dtype; wave w owns the output
-// columns p = 16 w .. 16 w + 15 of every n tile.  Slots j >= M-1 (attended
-// by no token) are written as zeros.
+// Workgroup (b, h, block of kMemJ memories j0 .. j0 + kMemJ - 1), 8 waves:
+//   M1_j = sum_t C_t^T (g p_j[t] dy_t),   M2_j = sum_t Qbar'_t^T (ln2 dl_j[t] Ebar_t)
+// over the tokens t >= (j + 1) S.  The token stream (C, Qbar', dy, Ebar in the
+// storage dtype, unscaled) is read once for all the block's memories: TB
+// tokens per step are copied into LDS by DMA one step ahead, and the
+// per-(memory, token) factors g p_j and ln2 dl_j (zero where memory j is not
+// attended) scale the dy and Ebar fragments in registers.  Wave w owns the
+// output columns p = 16 (w % 4) .. + 15 and half of the n tiles.  Memories
+// j >= M - 1 (attended by no token) are written as zeros.
+template <typename T>
+constexpr int mem_tb() { return sizeof(T) == 2 ? 64 : 32; }
+
+template <typename T>
+__device__ __forceinline__ Frag<T> scale_frag(Frag<T> f, const f32x4& s0, const f32x4& s1) {
+    Frag<T> r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        r[i] = from_f<T>(to_f(f[i]) * s0[i]);
+        r[4 + i] = from_f<T>(to_f(f[4 + i]) * s1[i]);
+    }
+    return r;
+}
+
 template <typename T, int N>
-__global__ __launch_bounds__(256) void k_bwd_mem(const T* __restrict__ qb,
-                                                 const float* __restrict__ eb,
+__global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
+                                                 const T* __restrict__ ebt,
                                                  const T* __restrict__ Cm, const T* __restrict__ dy,
                                                  const T* __restrict__ mem,
                                                  const float* __restrict__ gpw,
@@ -376,178 +396,184 @@ __global__ __launch_bounds__(256) void k_bwd_mem(const T* __restrict__ qb,
                                                  float* __restrict__ dmem, float eps, int normalize,
                                                  int64_t L, int H, int G, int S, int64_t Mcap,
                                                  int64_t Mp, int64_t BH) {
+    constexpr int J = kMemJ;
     constexpr int ES = (int)sizeof(T);
+    constexpr int TB = mem_tb<T>();
     constexpr int RBN = N * ES, RBP = kP * ES;
-    constexpr int CT = kMemTB * RBN, DT = kMemTB * RBP;
-    constexpr int BUF = 2 * CT + 2 * DT;
+    constexpr int CT = TB * RBN, DT = TB * RBP;
+    constexpr int STAGE = 2 * CT + 2 * DT;
     constexpr int NT = N / 16;
-    constexpr int PCN = kMemTB * N / 8;   // 8-element pieces of an N-wide tile
-    constexpr int PCP = kMemTB * kP / 8;  // ... of a P-wide tile
-    constexpr int TOT = 2 * PCN + 2 * PCP;
-    constexpr int PPT = (TOT + 255) / 256;
-    __shared__ __attribute__((aligned(16))) char buf[2][BUF];
-    __shared__ float red[2][4][N];
+    constexpr int NH = NT / 2;  // n tiles per wave
+    static_assert(NH >= 1, "at least two n tiles");
+    __shared__ __attribute__((aligned(16))) char buf[2][STAGE];
+    __shared__ __attribute__((aligned(16))) float sc[2][J][2][TB];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    const int64_t j = (int64_t)blockIdx.x / BH;
-    const int64_t bh = (int64_t)blockIdx.x - j * BH;
+    const int pt = wave & 3, nh = wave >> 2;
+    const int64_t jb = (int64_t)blockIdx.x / BH;
+    const int64_t bh = (int64_t)blockIdx.x - jb * BH;
     const int64_t b = bh / H;
     const int h = (int)(bh - b * H);
     const int g = h / (H / G);
-    float* out = dmem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
-    if (j >= Mp) {
-        for (int q = tid; q < N * kP / 4; q += 256)
-            reinterpret_cast<f32x4*>(out)[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int64_t j0 = jb * J;
+    const int p = 16 * pt + col;
+    auto out_of = [&](int jl) { return dmem + ((b * Mcap + j0 + jl) * H + h) * (int64_t)N * kP; };
+    if (j0 >= Mp) {
+        // no memory of the block is attended: zeros (slots up to Mcap)
+        for (int jl = 0; jl < J; ++jl) {
+            if (j0 + jl >= Mcap) break;
+            float* out = out_of(jl);
+            for (int q = tid; q < N * kP / 4; q += 512)
+                reinterpret_cast<f32x4*>(out)[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
         return;
     }
-    const int64_t tbeg = (j + 1) * S;
-    const int nblk = (int)((L - tbeg + kMemTB - 1) / kMemTB);
-    const float* gpr = gpw + ((b * H + h) * Mp + j) * L;
-    const float* gdr = gdw + ((b * H + h) * Mp + j) * L;
+    const int64_t tbeg = (j0 + 1) * S;
+    const int nstep = (int)((L - tbeg + TB - 1) / TB);
+    const int64_t grow = (b * L) * G + g;  // row of token 0 in the [B][L][G] layout
 
-    float rv[PPT][8];
-    float rs[PPT];
-    auto load_block = [&](int blk) {
-#pragma unroll
-        for (int k = 0; k < PPT; ++k) {
-            const int q = tid + 256 * k;
-            rs[k] = 0.f;
-            if (q >= TOT) continue;
-            int r, c;
-            if (q < 2 * PCN) {
-                const int qq = q < PCN ? q : q - PCN;
-                r = qq / (N / 8);
-                c = qq % (N / 8);
-            } else {
-                const int qq = q < 2 * PCN + PCP ? q - 2 * PCN : q - 2 * PCN - PCP;
-                r = qq / (kP / 8);
-                c = qq % (kP / 8);
-            }
-            const int64_t tt = tbeg + (int64_t)blk * kMemTB + r;
-            const bool ok = tt < L;
-            const int64_t tk = ok ? tt : L - 1;
-            const int64_t btk = b * L + tk;
-            if (q < PCN) {
-                load8(Cm + (btk * G + g) * N + 8 * c, rv[k]);
-                rs[k] = ok ? gpr[tk] : 0.f;
-            } else if (q < 2 * PCN) {
-                load8(qb + (btk * G + g) * N + 8 * c, rv[k]);
-                // ln2 dl_j = ln2 g p_j (dwy_j - Dy): Qbar' carries log2(e)/sqrt(N)
-                rs[k] = ok ? kLn2 * gpr[tk] * (gdr[tk] - rdy[btk * H + h]) : 0.f;
-            } else if (q < 2 * PCN + PCP) {
-                load8(dy + (btk * H + h) * kP + 8 * c, rv[k]);
-                rs[k] = 1.f;
-            } else {
-                load8(eb + (btk * G + g) * kP + 8 * c, rv[k]);
-                rs[k] = 1.f;
+    auto issue = [&](int st) {
+        const int64_t t0 = tbeg + (int64_t)st * TB;
+        const int rv = (int)(L - t0 < TB ? L - t0 : TB);
+        char* d = buf[st & 1];
+        dma_tile<RBN, true>(d, reinterpret_cast<const char*>(Cm + (grow + t0 * G) * N),
+                            (int64_t)G * RBN, TB, rv, wave, 8, lane);
+        dma_tile<RBN, true>(d + CT, reinterpret_cast<const char*>(qb + (grow + t0 * G) * N),
+                            (int64_t)G * RBN, TB, rv, wave, 8, lane);
+        dma_tile<RBP, true>(d + 2 * CT,
+                            reinterpret_cast<const char*>(dy + ((b * L + t0) * H + h) * kP),
+                            (int64_t)H * RBP, TB, rv, wave, 8, lane);
+        dma_tile<RBP, true>(d + 2 * CT + DT,
+                            reinterpret_cast<const char*>(ebt + (grow + t0 * G) * kP),
+                            (int64_t)G * RBP, TB, rv, wave, 8, lane);
+    };
+    // factors of step st: g p_j[t] and ln2 dl_j[t] = ln2 g p_j (dwy_j - Dy)
+    float fg = 0.f, fd = 0.f;
+    auto load_factors = [&](int st) {
+        fg = fd = 0.f;
+        if (tid < J * TB) {
+            const int jl = tid / TB, tk = tid % TB;
+            const int64_t j = j0 + jl, t = tbeg + (int64_t)st * TB + tk;
+            if (j < Mp && t < L && t >= (j + 1) * S) {
+                const int64_t si = ((b * H + h) * Mp + j) * L + t;
+                const float gp = gpw[si];
+                fg = gp;
+                fd = kLn2 * gp * (gdw[si] - rdy[(b * L + t) * H + h]);
             }
         }
     };
-    auto store_block = [&](char* dst) {
-#pragma unroll
-        for (int k = 0; k < PPT; ++k) {
-            const int q = tid + 256 * k;
-            if (q >= TOT) continue;
-            char* tile;
-            int r, c, rb;
-            if (q < 2 * PCN) {
-                const int qq = q < PCN ? q : q - PCN;
-                tile = dst + (q < PCN ? 0 : CT);
-                r = qq / (N / 8);
-                c = qq % (N / 8);
-                rb = RBN;
-            } else {
-                const bool isdy = q < 2 * PCN + PCP;
-                const int qq = isdy ? q - 2 * PCN : q - 2 * PCN - PCP;
-                tile = dst + 2 * CT + (isdy ? 0 : DT);
-                r = qq / (kP / 8);
-                c = qq % (kP / 8);
-                rb = RBP;
-            }
-            float v[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) v[i] = rv[k][i] * rs[k];
-            // 8 elements = 16 bytes (bf16) or two 16-byte chunks (fp32)
-#pragma unroll
-            for (int hf = 0; hf < ES / 2; ++hf) {
-                const int byte = 8 * c * ES + 16 * hf;
-                const int cpr = rb / 16;
-                const int mask = (cpr < 8 ? cpr : 8) - 1;
-                const int o = r * rb + ((((byte >> 4) ^ (r & mask)) << 4));
-                if constexpr (ES == 2) {
-                    *reinterpret_cast<bf16x8*>(tile + o) = make_frag<bf16>(v);
-                } else {
-                    *reinterpret_cast<f32x4*>(tile + o) =
-                        f32x4{v[4 * hf], v[4 * hf + 1], v[4 * hf + 2], v[4 * hf + 3]};
-                }
-            }
+    auto store_factors = [&](int st) {
+        if (tid < J * TB) {
+            const int jl = tid / TB, tk = tid % TB;
+            sc[st & 1][jl][0][tk] = fg;
+            sc[st & 1][jl][1][tk] = fd;
         }
     };
 
-    f32x4 m1[NT], m2[NT];
+    f32x4 m1[J][NH], m2[J][NH];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) m1[nt] = m2[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int jl = 0; jl < J; ++jl)
+#pragma unroll
+        for (int k = 0; k < NH; ++k) m1[jl][k] = m2[jl][k] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    load_block(0);
-    store_block(buf[0]);
-    __syncthreads();
-    for (int blk = 0; blk < nblk; ++blk) {
-        if (blk + 1 < nblk) load_block(blk + 1);
-        const char* cs = buf[blk & 1];
+    issue(0);
+    load_factors(0);
+    store_factors(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
+    for (int st = 0; st < nstep; ++st) {
+        if (st + 1 < nstep) {
+            issue(st + 1);
+            load_factors(st + 1);
+        }
+        const char* cs = buf[st & 1];
         const char* qs = cs + CT;
         const char* dyt = cs + 2 * CT;
         const char* et = dyt + DT;
-        const Frag<T> b1 = frag_km<T, RBP>(dyt, 4 * grp, 16 + 4 * grp, 16 * wave, lane);
-        const Frag<T> b2 = frag_km<T, RBP>(et, 4 * grp, 16 + 4 * grp, 16 * wave, lane);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            m1[nt] = mma16(m1[nt], frag_km<T, RBN>(cs, 4 * grp, 16 + 4 * grp, 16 * nt, lane), b1);
-            m2[nt] = mma16(m2[nt], frag_km<T, RBN>(qs, 4 * grp, 16 + 4 * grp, 16 * nt, lane), b2);
-        }
-        if (blk + 1 < nblk) store_block(buf[(blk + 1) & 1]);
-        __syncthreads();
-    }
-
-    // epilogue: r[n] and dr[n] = sum_p dH[n,p] M2[n,p] reduced over the four
-    // waves' column tiles, then ddH
-    const T* hsrc = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
-    const int p = 16 * wave + col;
-    float hv[NT][4];
+        for (int ks = 0; ks < TB / 32; ++ks) {
+            const int r0 = 32 * ks + 4 * grp, r1 = r0 + 16;
+            const Frag<T> bd = frag_km<T, RBP>(dyt, r0, r1, 16 * pt, lane);
+            const Frag<T> be = frag_km<T, RBP>(et, r0, r1, 16 * pt, lane);
+            Frag<T> ac[NH], aq[NH];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+            for (int k = 0; k < NH; ++k) {
+                ac[k] = frag_km<T, RBN>(cs, r0, r1, 16 * (nh * NH + k), lane);
+                aq[k] = frag_km<T, RBN>(qs, r0, r1, 16 * (nh * NH + k), lane);
+            }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) hv[nt][i] = to_f(hsrc[(16 * nt + 4 * grp + i) * kP + p]);
-    if (normalize) {
+            for (int jl = 0; jl < J; ++jl) {
+                const f32x4 g0 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][0][r0]);
+                const f32x4 g1 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][0][r1]);
+                const f32x4 d0 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][1][r0]);
+                const f32x4 d1 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][1][r1]);
+                const Frag<T> bdj = scale_frag<T>(bd, g0, g1);
+                const Frag<T> bej = scale_frag<T>(be, d0, d1);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float s2 = dpp_group_sum<16>(hv[nt][i] * hv[nt][i]);
-                const float d2 = dpp_group_sum<16>(hv[nt][i] * m2[nt][i]);
-                if (col == 0) {
-                    red[0][wave][16 * nt + 4 * grp + i] = s2;
-                    red[1][wave][16 * nt + 4 * grp + i] = d2;
+                for (int k = 0; k < NH; ++k) {
+                    m1[jl][k] = mma16(m1[jl][k], ac[k], bdj);
+                    m2[jl][k] = mma16(m2[jl][k], aq[k], bej);
                 }
             }
-        __syncthreads();
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int n = 16 * nt + 4 * grp + i;
-            float o = m1[nt][i];
-            if (normalize) {
-                const float ss = red[0][0][n] + red[0][1][n] + red[0][2][n] + red[0][3][n];
-                const float dr = red[1][0][n] + red[1][1][n] + red[1][2][n] + red[1][3][n];
-                const float r = __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps);
-                o += r * m2[nt][i] - (r * r * r * (1.0f / kP)) * dr * hv[nt][i];
-            } else {
-                o += m2[nt][i];
-            }
-            out[n * kP + p] = o;
         }
+        if (st + 1 < nstep) store_factors(st + 1);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        lds_barrier();
+    }
+
+    // epilogue per memory: r[n] and dr[n] = sum_p dH[n,p] M2[n,p] reduced over
+    // the four column waves through LDS (the stage buffers are free now)
+    float* red = reinterpret_cast<float*>(&buf[0][0]);  // [J][2][4][N]
+#pragma unroll
+    for (int jl = 0; jl < J; ++jl) {
+        const int64_t j = j0 + jl;
+        if (j >= Mp) continue;
+        const T* hsrc = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
+#pragma unroll
+        for (int k = 0; k < NH; ++k)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = 16 * (nh * NH + k) + 4 * grp + i;
+                const float hv = to_f(hsrc[n * kP + p]);
+                const float s2 = dpp_group_sum<16>(hv * hv);
+                const float d2 = dpp_group_sum<16>(hv * m2[jl][k][i]);
+                if (col == 0) {
+                    red[((jl * 2 + 0) * 4 + pt) * N + n] = s2;
+                    red[((jl * 2 + 1) * 4 + pt) * N + n] = d2;
+                }
+            }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int jl = 0; jl < J; ++jl) {
+        const int64_t j = j0 + jl;
+        if (j >= Mcap) break;
+        float* out = out_of(jl);
+        const T* hsrc = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
+#pragma unroll
+        for (int k = 0; k < NH; ++k)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = 16 * (nh * NH + k) + 4 * grp + i;
+                float o = 0.f;
+                if (j < Mp) {
+                    o = m1[jl][k][i];
+                    if (normalize) {
+                        const float* r0 = red + (jl * 2 + 0) * 4 * N + n;
+                        const float* r1 = red + (jl * 2 + 1) * 4 * N + n;
+                        const float ss = r0[0] + r0[N] + r0[2 * N] + r0[3 * N];
+                        const float dr = r1[0] + r1[N] + r1[2 * N] + r1[3 * N];
+                        const float r = __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps);
+                        const float hv = to_f(hsrc[n * kP + p]);
+                        o += r * m2[jl][k][i] - (r * r * r * (1.0f / kP)) * dr * hv;
+                    } else {
+                        o += m2[jl][k][i];
+                    }
+                }
+                out[n * kP + p] = o;
+            }
+    }
 }
 
 // ---- finishing: per (b, t, g) -------------------------------------------------------
@@ -640,6 +666,7 @@ struct BwdWs {
     void* kmem;
     void* qb;
     float* eb;
+    void* ebt;  // Ebar in the storage dtype (eb itself for fp32)
     float* gp;
     float* gd;
     float* part;
@@ -662,6 +689,7 @@ BwdWs bwd_layout(const Shape& s, void* base) {
     w.kmem = take(es * s.B * Mp * s.H * (size_t)s.N * s.P);
     w.qb = take(es * s.B * s.L * s.G * (size_t)s.N);
     w.eb = (float*)take(4 * s.B * s.L * s.G * (size_t)s.P);
+    w.ebt = s.dtype == 1 ? take(es * s.B * s.L * s.G * (size_t)s.P) : (void*)w.eb;
     w.gp = (float*)take(4 * s.B * s.H * Mp * (size_t)s.L);
     w.gd = (float*)take(4 * s.B * s.H * Mp * (size_t)s.L);
     w.part = (float*)take(4 * s.B * s.L * nhb * (size_t)(2 * s.N + s.P));
@@ -686,7 +714,8 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     const unsigned rblocks = (unsigned)((rows + 3) / 4);
     prof_begin("k_bwd_prep", st);
     k_bwd_prep<T, N><<<rblocks, 256, 0, st>>>((const T*)q, (const T*)e, a.qw, a.ew, (T*)w.qb, w.eb,
-                                              a.eps, a.normalize, rows);
+                                              sizeof(T) == 2 ? (T*)w.ebt : nullptr, a.eps,
+                                              a.normalize, rows);
     prof_end(st);
     const int blk0 = s.S / kTokBlock;
     const int64_t nblk = (s.L + kTokBlock - 1) / kTokBlock - blk0;
@@ -701,8 +730,9 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     }
     const int64_t BH = s.B * s.H;
     prof_begin("k_bwd_mem", st);
-    k_bwd_mem<T, N><<<(unsigned)(BH * s.Mcap), 256, 0, st>>>(
-        (const T*)w.qb, w.eb, (const T*)Cm, (const T*)dy, (const T*)mem, w.gp, w.gd, w.rdy, dmem, a.eps,
+    const int64_t njb = (s.Mcap + kMemJ - 1) / kMemJ;
+    k_bwd_mem<T, N><<<(unsigned)(BH * njb), 512, 0, st>>>(
+        (const T*)w.qb, (const T*)w.ebt, (const T*)Cm, (const T*)dy, (const T*)mem, w.gp, w.gd, w.rdy, dmem, a.eps,
         a.normalize, s.L, s.H, s.G, s.S, s.Mcap, Mp, BH);
     prof_end(st);
     prof_begin("k_bwd_finish", st);
