@@ -419,7 +419,8 @@ def main():
             "us": round(bwd_ms * 1e3, 2), "algorithmic_flops": bflops,
             "mfma_util": round(bflops / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "tokens_per_s": round(B * L / (bwd_ms * 1e-3), 1),
-            "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(bavg.items())}}
+            "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(bavg.items())},
+            "traffic_bytes": {k: traffic_for(k) for k in ("k_bwd_tokens", "k_bwd_mem")}}
         del ws_bwd, grads
 
     tokens = B * L

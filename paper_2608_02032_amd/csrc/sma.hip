@@ -107,11 +107,12 @@ __device__ __forceinline__ uint4 piece_scale(uint4 v, float r, float) {
 
 // Key side of one memory: kmem = r (.) dH, r[n] the inverse RMS of row n of
 // the stored values.  The RPC lanes holding one row's 16-byte pieces reduce
-// its sum of squares with DPP moves.
+// its sum of squares with DPP moves.  rinv (optional, [B][Mp][H][N]) receives
+// 1 / r[n].
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* __restrict__ kmem,
-                                                  float eps, int normalize, int H, int64_t Mp,
-                                                  int64_t Mcap) {
+                                                  float* __restrict__ rinv, float eps,
+                                                  int normalize, int H, int64_t Mp, int64_t Mcap) {
     constexpr int RB = kP * (int)sizeof(T);
     constexpr int PIECES = N * RB / 16;
     constexpr int RPC = RB / 16;
@@ -129,6 +130,8 @@ __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* 
         const float ss = dpp_group_sum<RPC>(piece_sumsq(v[i], T()));
         const float rn = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
         dst[threadIdx.x + i * 256] = piece_scale(v[i], rn, T());
+        const int q = threadIdx.x + i * 256;
+        if (rinv && q % RPC == 0) rinv[((b * Mp + j) * H + h) * (int64_t)N + q / RPC] = 1.0f / rn;
     }
 }
 
@@ -1454,7 +1457,7 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
         if (Mp > 0) {
             prof_begin("k_sma_keys", st);
             k_sma_keys<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
-                (const T*)mem, kmem, a.eps, a.normalize, s.H, Mp, s.Mcap);
+                (const T*)mem, kmem, nullptr, a.eps, a.normalize, s.H, Mp, s.Mcap);
             prof_end(st);
         }
         prof_begin("k_sma", st);
@@ -1494,22 +1497,22 @@ hipError_t run_sma_n(const Shape& s, const SmaArgs& a, const void* q, const void
 }  // namespace
 
 hipError_t launch_sma_keys(const Shape& s, const SmaArgs& a, const void* mem, void* kmem,
-                           hipStream_t st) {
+                           float* rinv, hipStream_t st) {
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
     if (Mp == 0) return hipSuccess;
     const dim3 grid((unsigned)Mp, (unsigned)s.H, (unsigned)s.B);
     prof_begin("k_sma_keys", st);
     if (s.dtype == 1) {
         switch (s.N) {
-            case 32: k_sma_keys<bf16, 32><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 64: k_sma_keys<bf16, 64><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 128: k_sma_keys<bf16, 128><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 32: k_sma_keys<bf16, 32><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 64: k_sma_keys<bf16, 64><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 128: k_sma_keys<bf16, 128><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
         }
     } else {
         switch (s.N) {
-            case 32: k_sma_keys<float, 32><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 64: k_sma_keys<float, 64><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 128: k_sma_keys<float, 128><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 32: k_sma_keys<float, 32><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 64: k_sma_keys<float, 64><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 128: k_sma_keys<float, 128><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
         }
     }
     prof_end(st);

@@ -21,14 +21,15 @@
 // follow through RMSNorm with the weights held constant.
 //
 // Kernels, in launch order:
-//   k_sma_keys          key side Kh_j, shared with the forward (cache layout)
+//   k_sma_keys          key side Kh_j (cache layout) and 1 / r_j, shared with
+//                       the forward
 //   k_bwd_prep          Qbar (scaled by log2(e)/sqrt(N), storage dtype, the
 //                       forward's operand exactly) and Ebar (float) per token
 //   k_bwd_tokens        one workgroup per (64 tokens of one chunk, block of
 //                       heads of one group); one pass over (head, memory),
 //                       tiles streamed through an LDS ring by DMA:
 //                         W' = Kh^T Qbar' -> logits -> p;
-//                         X = dH dy^T -> dwy, dC += g p X;
+//                         X = dH dy^T = diag(1/r) Kh dy^T -> dwy, dC += g p X;
 //                         Z = Kh Ebar^T, with dQbar and dEbar formed from
 //                         running sums at the head's end (Dy is known then),
 //                       tokens on the MFMA column side so every per-token
@@ -74,6 +75,57 @@ __device__ __forceinline__ float silu_grad(float z) {
     const float sg = 1.0f / (1.0f + __expf(-z));
     return sg * (1.0f + z * (1.0f - sg));
 }
+
+// DMA copy of one XOR-swizzled tile of TILE bytes (rows of RB bytes, chunk c
+// of row r stored at chunk c ^ (r & MASK)) from a contiguous global tile,
+// with the per-lane offsets fixed at set-up and the tile base passed as a
+// scalar, so issuing a copy costs no vector address arithmetic.  Wave w of NW
+// copies the 1 KiB pieces w, w + NW, ...; lane i of a piece lands 16 i bytes
+// into it.  Invisible to the compiler's wait counting: the caller waits with
+// vmcnt (count() copies per call).
+template <int RB, int TILE, int NW>
+struct TileCopy {
+    static constexpr int CPR = RB / 16;
+    static constexpr int MASK = (CPR < 8 ? CPR : 8) - 1;
+    static constexpr int NI = TILE / 1024;  // pieces per tile
+    static constexpr int KPW = NI / NW;     // pieces per wave
+    static_assert(NI % NW == 0 && KPW >= 1, "pieces must tile the waves");
+    uint32_t goff[KPW];
+    int wave;
+    __device__ void init(int w, int lane) {
+        wave = __builtin_amdgcn_readfirstlane(w);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const int q = (w + k * NW) * 64 + lane;
+            const int row = q / CPR, pos = q % CPR;
+            goff[k] = (uint32_t)(row * RB + ((pos ^ (row & MASK)) << 4));
+            asm volatile("" : "+v"(goff[k]));
+        }
+    }
+    static constexpr int count() { return KPW; }
+    __device__ __forceinline__ void issue(const void* gtile, char* ltile) const {
+        const uint64_t gb = (uint64_t)(uintptr_t)gtile;
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(gb >> 32));
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)gb);
+        const uint64_t base = ((uint64_t)hi << 32) | (uint64_t)lo;
+        const uint32_t l0 = lds_addr(ltile);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane(
+                (int)(l0 + (uint32_t)((wave + k * NW) * 1024)));
+            uint32_t save;
+            asm volatile(
+                "s_mov_b32 %0, m0\n\t"
+                "s_mov_b32 m0, %3\n\t"
+                "s_nop 0\n\t"
+                "global_load_lds_dwordx4 %1, %2\n\t"
+                "s_mov_b32 m0, %0"
+                : "=&s"(save)
+                : "v"(goff[k]), "s"(base), "s"(m0)
+                : "memory");
+        }
+    }
+};
 
 // ---- Qbar' and Ebar per (b, t, g) row: one wave per row ---------------------
 // Qbar' = RMSNorm(q) w * log2(e)/sqrt(N) rounded to the storage dtype (the
@@ -127,23 +179,25 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
 // l % 16 and its rows 4 (l / 16) + 0..3 of each 16-row tile.
 //
 // One pass over (head, memory j) steps.  Per step: W' = Kh^T Qbar'^T (logits,
-// p_j), X = dH dy^T (dwy_j, dC += g p_j X) and Z = Kh Ebar^T.  dl_j needs
+// p_j), X = dH dy^T (dwy_j, dC += g p_j X) and Z = Kh Ebar^T, all three from
+// the key-side tile alone (X as diag(1/r) Kh dy^T, so dH is not streamed;
+// in bf16 this reads dH through the key side's rounding).  dl_j needs
 // Dy = sum_j p_j dwy_j, known only after the head's last memory, so the head
 // accumulates S1 = sum_j p_j dwy_j Z_j, S2 = sum_j p_j Z_j (and T1, T2 with
 // W'), and adds g s (S1 - Dy S2) to dQbar and g ln2 (T1 - Dy T2) to dEbar at
 // its end (W' and Qbar' carry log2(e)/sqrt(N); ln2 takes it back to s).
-// Tiles (Kh_j, dH_j) stream through an NS-stage LDS ring by DMA, NS - 1 steps
-// ahead; each wave waits only for its own copies of the current step and one
-// barrier per step orders the stages.
+// Tiles (Kh_j and the row of 1/r_j) stream through an NS-stage LDS ring by
+// DMA, NS - 1 steps ahead; each wave waits only for its own copies of the
+// current step and one barrier per step orders the stages.
 template <typename T, int N>
 constexpr int tok_stages() {
-    return (N * kP * (int)sizeof(T) * 2 * 4 <= 131072) ? 4 : 2;
+    return (N * kP * (int)sizeof(T) * 4 <= 131072) ? 4 : 2;
 }
 
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_bwd_tokens(
     const T* __restrict__ qb, const float* __restrict__ eb, const T* __restrict__ Cm,
-    const T* __restrict__ mem, const T* __restrict__ kmem, const T* __restrict__ z,
+    const float* __restrict__ rinv, const T* __restrict__ kmem, const T* __restrict__ z,
     const float* __restrict__ lse, const T* __restrict__ dy, float* __restrict__ gpw,
     float* __restrict__ gdw, float* __restrict__ part, float* __restrict__ rdy, int z_per_head,
     int64_t L, int H, int G, int S, int64_t Mcap, int64_t Mp, int hpb, int blk0, int nblk,
@@ -153,8 +207,11 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
     constexpr int NT = N / 16;
     constexpr int KQ = N / 32;
     constexpr int NS = tok_stages<T, N>();
-    constexpr int CPS = 2 * N * (RB / 16) / (64 * kTokWaves);  // DMA copies per wave per step
-    __shared__ __attribute__((aligned(16))) char ring[NS][2][TILE];
+    using Copy = TileCopy<RB, TILE, kTokWaves>;
+    constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per wave
+    constexpr int CPS = Copy::count() + 1;  // DMA copies per wave per step
+    __shared__ __attribute__((aligned(16))) char ring[NS][TILE];
+    __shared__ __attribute__((aligned(16))) float rring[NS][N];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -230,14 +287,15 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
     for (int pt = 0; pt < 4; ++pt) dE[pt] = zero4;
 
     const int nsteps = hpb * nj;
+    Copy copy;
+    copy.init(wave, lane);
     auto issue_tiles = [&](int k) {
         const int hh = k / nj, j = k - hh * nj;
-        const int64_t hj = ((b * Mp + j) * H + h0 + hh) * (int64_t)N * kP;
-        const int64_t mj = ((b * Mcap + j) * H + h0 + hh) * (int64_t)N * kP;
-        dma_tile<RB, true>(ring[k % NS][0], reinterpret_cast<const char*>(kmem + hj), RB, N, N,
-                           wave, kTokWaves, lane);
-        dma_tile<RB, true>(ring[k % NS][1], reinterpret_cast<const char*>(mem + mj), RB, N, N,
-                           wave, kTokWaves, lane);
+        const int64_t hj = (b * Mp + j) * H + h0 + hh;
+        copy.issue(kmem + hj * N * kP, ring[k % NS]);
+        if (lane < RPW)
+            lds_dma16_untracked_at(rinv + hj * N + (wave * RPW + lane) * 4,
+                                   lds_addr(&rring[k % NS][0]) + wave * RPW * 16);
     };
     // per (head, memory) scalar slot of this lane's token
     auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * L + tc; };
@@ -279,8 +337,7 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
             for (int pt = 0; pt < 4; ++pt) u1[pt] = u2[pt] = zero4;
         }
         if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
-        const char* kt = ring[k % NS][0];
-        const char* dt = ring[k % NS][1];
+        const char* kt = ring[k % NS];
         // W'^T = Kh^T Qbar'^T: rows p, token columns (log2-scaled scores)
         f32x4 w[4];
 #pragma unroll
@@ -301,18 +358,19 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
         l2 += shfl_xor(l2, 16);
         l2 += shfl_xor(l2, 32);
         const float p = fast_exp2(l2 - lse2);
-        // X^T = dH dy^T and Z^T = Kh Ebar^T: rows n, token columns
+        // X^T = dH dy^T = diag(1/r) Kh dy^T and Z^T = Kh Ebar^T: rows n, token
+        // columns, both from the same key-side fragments
         f32x4 x[NT], zz[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             x[nt] = zz[nt] = zero4;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                x[nt] = mma16(x[nt], frag_rowmajor<T, RB>(dt, 16 * nt + col, 32 * ks + 8 * grp),
-                              dyf[ks]);
-                zz[nt] = mma16(zz[nt], frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp),
-                               ef[ks]);
+                const Frag<T> a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
+                x[nt] = mma16(x[nt], a, dyf[ks]);
+                zz[nt] = mma16(zz[nt], a, ef[ks]);
             }
+            x[nt] *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
         }
         float dw = 0.f;
 #pragma unroll
@@ -667,6 +725,7 @@ struct BwdWs {
     void* qb;
     float* eb;
     void* ebt;  // Ebar in the storage dtype (eb itself for fp32)
+    float* rinv;  // 1 / r of every attended memory row, [B][M-1][H][N]
     float* gp;
     float* gd;
     float* part;
@@ -687,6 +746,7 @@ BwdWs bwd_layout(const Shape& s, void* base) {
         return r;
     };
     w.kmem = take(es * s.B * Mp * s.H * (size_t)s.N * s.P);
+    w.rinv = (float*)take(4 * s.B * Mp * s.H * (size_t)s.N);
     w.qb = take(es * s.B * s.L * s.G * (size_t)s.N);
     w.eb = (float*)take(4 * s.B * s.L * s.G * (size_t)s.P);
     w.ebt = s.dtype == 1 ? take(es * s.B * s.L * s.G * (size_t)s.P) : (void*)w.eb;
@@ -707,7 +767,7 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     const int hpb = bwd_heads_per_block(s);
     hipError_t err;
     if (Mp > 0) {
-        err = launch_sma_keys(s, a, mem, w.kmem, st);
+        err = launch_sma_keys(s, a, mem, w.kmem, w.rinv, st);
         if (err != hipSuccess) return err;
     }
     const int64_t rows = s.B * s.L * s.G;
@@ -723,7 +783,7 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
         prof_begin("k_bwd_tokens", st);
         const int64_t BHC = s.B * (s.H / hpb);
         k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 256, 0, st>>>(
-            (const T*)w.qb, w.eb, (const T*)Cm, (const T*)mem, (const T*)w.kmem, (const T*)z, lse,
+            (const T*)w.qb, w.eb, (const T*)Cm, w.rinv, (const T*)w.kmem, (const T*)z, lse,
             (const T*)dy, w.gp, w.gd, w.part, w.rdy, a.z_per_head, s.L, s.H, s.G, s.S, s.Mcap, Mp,
             hpb, blk0, (int)nblk, BHC);
         prof_end(st);
