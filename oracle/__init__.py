@@ -58,6 +58,10 @@ def _load():
         lib.dart_oracle_ssd_recurrence.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT,
                                                    _D, _D, _D, _D, _D, _D, _D, _D]
         lib.dart_oracle_ssd_recurrence.restype = None
+        lib.dart_oracle_ssd_bwd.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
+                                            _D, _D, _D, _D, _D, _D, _D, _D, _D,
+                                            _D, _D, _D, _D, _D, _D]
+        lib.dart_oracle_ssd_bwd.restype = None
         lib.dart_oracle_chunk_memories.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
                                                    _D, _D, _D, _D, _D]
         lib.dart_oracle_chunk_memories.restype = None
@@ -125,6 +129,29 @@ def chunk_memories(x, dt, A, Bm, S, mem_capacity=None):
     _load().dart_oracle_chunk_memories(B_, L, H, G, P, N, int(S), Mcap, _ptr(x), _ptr(dt),
                                        _ptr(A), _ptr(Bm), _ptr(mem))
     return mem
+
+
+def ssd_bwd(x, dt, A, Bm, Cm, S, dy, dmem=None, dh_last=None, h0=None):
+    """Gradients of sum(dy * y_ssd) + sum(dmem * mem) + sum(dh_last * h_last)
+    for the recurrence of Sec. 2 and the memories of Sec. 3, by running the
+    recurrence backwards.  Shapes as ssd_recurrence / chunk_memories; dmem is
+    [B][Mcap][H][N][P] (Mcap >= ceil(L/S)).  Returns {"dx", "ddt", "dA",
+    "dB", "dC", "dh0"} (B and C gradients summed over each group's heads)."""
+    x, dt, A, Bm, Cm, dy = map(_f64, (x, dt, A, Bm, Cm, dy))
+    B_, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    dmem = None if dmem is None else _f64(dmem)
+    Mcap = dmem.shape[1] if dmem is not None else -(-L // S)
+    assert Mcap >= -(-L // S)
+    dhl = None if dh_last is None else _f64(dh_last)
+    h0 = None if h0 is None else _f64(h0)
+    out = {"dx": np.empty_like(x), "ddt": np.empty_like(dt), "dA": np.empty_like(A),
+           "dB": np.empty_like(Bm), "dC": np.empty_like(Cm), "dh0": np.zeros((B_, H, N, P))}
+    _load().dart_oracle_ssd_bwd(B_, L, H, G, P, N, int(S), Mcap, _ptr(x), _ptr(dt), _ptr(A),
+                                _ptr(Bm), _ptr(Cm), _ptr(h0), _ptr(dy), _ptr(dmem), _ptr(dhl),
+                                _ptr(out["dx"]), _ptr(out["ddt"]), _ptr(out["dA"]),
+                                _ptr(out["dB"]), _ptr(out["dC"]), _ptr(out["dh0"]))
+    return out
 
 
 def sma(q, e, Cm, mem, z, y_ssd, S, eps=1e-6, normalize=True, q_norm_w=None, e_norm_w=None,

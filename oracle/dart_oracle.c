@@ -31,6 +31,9 @@
  *                                token an explicit two-pass softmax over the
  *                                strictly earlier chunks, then
  *                                Y_t = C_t H_t + SiLU(z_t) R_t.
+ *   dart_oracle_ssd_bwd          gradients of the recurrence and the memories
+ *                                (loss sum dy . y_ssd + <dmem, dH> + <dh, H_{L-1}>)
+ *                                by running the recurrence backwards.
  *   dart_oracle_sma_bwd          gradients of dart_oracle_sma (loss sum dy . y)
  *                                by recomputing every row (App. C) and the chain
  *                                rule through Sec. 3 and App. B.1, written out.
@@ -144,6 +147,125 @@ void dart_oracle_chunk_memories(int64_t B, int64_t L, int H, int G, int P, int N
             }
         }
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Backward of the scan and its memories: gradients of                       */
+/*   loss = sum_t dy_t . y_t + sum_c <dmem_c, dH_[c]> + <dh_last, H_{L-1}>    */
+/* with respect to x, dt, A, B, C and h0, by running the recurrence of Sec. 2 */
+/* backwards.  With u_t = dt_t B_t^T x_t and a_t = exp(dt_t A_h):            */
+/*   G_t = C_t^T dy_t + a_{t+1} G_{t+1},  G_{L-1} includes dh_last            */
+/*     (the adjoint of H_t through y and h_last);                             */
+/*   F_t = a_{t+1} F_{t+1} inside chunk c, F_{e(c)} = dmem_c                  */
+/*     (the adjoint of the chunk's running contribution D_t, D reset to 0 at  */
+/*     the chunk's first token, dH_[c] = D_{e(c)});                           */
+/*   dx_t = dt_t B_t (G_t + F_t),  dB_t = dt_t (G_t + F_t) x_t,               */
+/*   dC_t = H_t dy_t,  da_t = <G_t, H_{t-1}> + <F_t, D_{t-1}>,                */
+/*   ddt_t = B_t (G_t + F_t) x_t + da_t a_t A_h,  dA_h = sum_t da_t a_t dt_t, */
+/*   dh0 = a_0 G_0.                                                          */
+/* B and C gradients sum over the heads of their group.  dmem, dh_last and   */
+/* h0 may be NULL (zero).  Memory: the states of one (b, h) are kept for the */
+/* whole sequence (L N P doubles), fine at the sizes the oracle serves.      */
+/* ------------------------------------------------------------------------ */
+void dart_oracle_ssd_bwd(int64_t B, int64_t L, int H, int G, int P, int N, int S, int64_t Mcap,
+                         const double* x, const double* dt, const double* A, const double* Bm,
+                         const double* Cm, const double* h0, const double* dy,
+                         const double* dmem, const double* dhl, double* dx, double* ddt,
+                         double* dA, double* dB, double* dC, double* dh0) {
+    const size_t NP = (size_t)N * P;
+    for (size_t k = 0; k < (size_t)B * L * H * P; ++k) dx[k] = 0.0;
+    for (size_t k = 0; k < (size_t)B * L * H; ++k) ddt[k] = 0.0;
+    for (size_t k = 0; k < (size_t)B * L * G * N; ++k) dB[k] = 0.0, dC[k] = 0.0;
+    double* dAb = (double*)calloc((size_t)B * H, sizeof(double));
+    /* rows of one batch entry touch only that entry's outputs */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < B; ++b) {
+        double* Hs = (double*)malloc(sizeof(double) * (size_t)(L + 1) * NP); /* H_{-1..L-1} */
+        double* Ds = (double*)malloc(sizeof(double) * (size_t)(L + 1) * NP); /* D_{-1..L-1} */
+        double* Gt = (double*)malloc(sizeof(double) * NP);
+        double* Ft = (double*)malloc(sizeof(double) * NP);
+        for (int h = 0; h < H; ++h) {
+            const int g = group_of(h, H, G);
+            /* forward: every state, and every chunk's running contribution */
+            for (size_t k = 0; k < NP; ++k) {
+                Hs[k] = h0 ? h0[((size_t)b * H + h) * NP + k] : 0.0;
+                Ds[k] = 0.0;
+            }
+            for (int64_t t = 0; t < L; ++t) {
+                const double d = DT_AT(b, t, h);
+                const double a = exp(d * A[h]);
+                const int first = (t % S) == 0;
+                const double* Hp = Hs + (size_t)t * NP;
+                const double* Dp = Ds + (size_t)t * NP;
+                double* Hn = Hs + (size_t)(t + 1) * NP;
+                double* Dn = Ds + (size_t)(t + 1) * NP;
+                for (int n = 0; n < N; ++n)
+                    for (int p = 0; p < P; ++p) {
+                        const size_t k = (size_t)n * P + p;
+                        const double u = d * BM_AT(b, t, g, n) * X_AT(b, t, h, p);
+                        Hn[k] = a * Hp[k] + u;
+                        Dn[k] = (first ? 0.0 : a * Dp[k]) + u;
+                    }
+            }
+            /* backward */
+            for (size_t k = 0; k < NP; ++k) {
+                Gt[k] = dhl ? dhl[((size_t)b * H + h) * NP + k] : 0.0;
+                Ft[k] = 0.0;
+            }
+            for (int64_t t = L - 1; t >= 0; --t) {
+                const double d = DT_AT(b, t, h);
+                const double a = exp(d * A[h]);
+                const int64_t c = t / S;
+                const int last = (t == L - 1) || ((t + 1) % S == 0);
+                const int first = (t % S) == 0;
+                /* G_t = C_t^T dy_t + (a_{t+1} G_{t+1}, already in Gt) */
+                for (int n = 0; n < N; ++n)
+                    for (int p = 0; p < P; ++p)
+                        Gt[(size_t)n * P + p] += CM_AT(b, t, g, n) * Y_AT(dy, b, t, h, p);
+                /* F_t: dmem_c at the chunk's last token, carried inside it */
+                if (last)
+                    for (size_t k = 0; k < NP; ++k)
+                        Ft[k] = dmem ? dmem[(((size_t)b * Mcap + c) * H + h) * NP + k] : 0.0;
+                const double* Hp = Hs + (size_t)t * NP;        /* H_{t-1} */
+                const double* Hc = Hs + (size_t)(t + 1) * NP;  /* H_t */
+                const double* Dp = Ds + (size_t)t * NP;        /* D_{t-1} (not read at a chunk start) */
+                double da = 0.0, din = 0.0;
+                for (int n = 0; n < N; ++n) {
+                    double db = 0.0, dc = 0.0;
+                    for (int p = 0; p < P; ++p) {
+                        const size_t k = (size_t)n * P + p;
+                        const double lam = Gt[k] + Ft[k];
+                        Y_AT(dx, b, t, h, p) += d * BM_AT(b, t, g, n) * lam;
+                        db += lam * X_AT(b, t, h, p);
+                        dc += Hc[k] * Y_AT(dy, b, t, h, p);
+                        da += Gt[k] * Hp[k] + (first ? 0.0 : Ft[k] * Dp[k]);
+                    }
+                    dB[(((size_t)b * L + t) * G + g) * N + n] += d * db;
+                    dC[(((size_t)b * L + t) * G + g) * N + n] += dc;
+                    din += BM_AT(b, t, g, n) * db;
+                }
+                ddt[((size_t)b * L + t) * H + h] = din + da * a * A[h];
+                dAb[(size_t)b * H + h] += da * a * d;
+                /* carry to t - 1 */
+                for (size_t k = 0; k < NP; ++k) {
+                    Gt[k] *= a;
+                    Ft[k] *= a;
+                }
+            }
+            if (dh0)
+                for (size_t k = 0; k < NP; ++k) dh0[((size_t)b * H + h) * NP + k] = Gt[k];
+        }
+        free(Hs);
+        free(Ds);
+        free(Gt);
+        free(Ft);
+    }
+    for (int h = 0; h < H; ++h) {
+        double s = 0.0;
+        for (int64_t b = 0; b < B; ++b) s += dAb[(size_t)b * H + h];
+        dA[h] = s;
+    }
+    free(dAb);
 }
 
 /* ------------------------------------------------------------------------ */

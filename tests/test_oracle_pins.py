@@ -555,3 +555,78 @@ def test_sma_backward_rounded_scores_reduce_to_exact_on_bf16_operands():
     b = oracle.sma_bwd(q2, e, C, mem, z, dy, S, round_scores=True)
     rel = np.abs(a["dq"] - b["dq"]).max() / np.abs(a["dq"]).max()
     assert 1e-5 < rel < 0.2
+
+
+@pytest.mark.parametrize("G,with_h0,with_dmem", [(2, True, True), (1, False, True), (1, True, False)])
+def test_scan_backward_matches_finite_differences(G, with_h0, with_dmem):
+    """The oracle's scan backward against central differences of the oracle's
+    recurrence and brute-force memories (loss sum dy . y_ssd + <dmem, dH> +
+    <dh_last, h_last>) at sampled entries of x, dt, A, B, C and h0; a ragged
+    last chunk included.  The two share nothing beyond the forward definition."""
+    rng = np.random.default_rng(31 + G)
+    B_, L, H, P, N, S = 2, 21, 4, 3, 5, 8
+    M = -(-L // S)
+    x = rng.standard_normal((B_, L, H, P))
+    dt = rng.uniform(0.05, 0.5, (B_, L, H))
+    A = -rng.uniform(0.5, 2.0, H)
+    Bm = rng.standard_normal((B_, L, G, N))
+    Cm = rng.standard_normal((B_, L, G, N))
+    h0 = rng.standard_normal((B_, H, N, P)) * 0.3 if with_h0 else None
+    dy = rng.standard_normal((B_, L, H, P))
+    dmem = rng.standard_normal((B_, M, H, N, P)) if with_dmem else None
+    dhl = rng.standard_normal((B_, H, N, P))
+
+    def loss(v):
+        y, hl = oracle.ssd_recurrence(v["x"], v["dt"], v["A"], v["Bm"], v["Cm"], h0=v["h0"])
+        out = float((y * dy).sum() + (hl * dhl).sum())
+        if with_dmem:
+            out += float((oracle.chunk_memories(v["x"], v["dt"], v["A"], v["Bm"], S) * dmem).sum())
+        return out
+
+    g = oracle.ssd_bwd(x, dt, A, Bm, Cm, S, dy, dmem=dmem, dh_last=dhl, h0=h0)
+    base = {"x": x, "dt": dt, "A": A, "Bm": Bm, "Cm": Cm, "h0": h0}
+    step = 1e-6
+    names = [("x", "dx"), ("dt", "ddt"), ("A", "dA"), ("Bm", "dB"), ("Cm", "dC")]
+    if with_h0:
+        names.append(("h0", "dh0"))
+    for name, key in names:
+        arr = base[name]
+        for _ in range(8):
+            idx = tuple(int(rng.integers(0, n)) for n in arr.shape)
+            lo, hi = arr.copy(), arr.copy()
+            lo[idx] -= step
+            hi[idx] += step
+            fd = (loss(dict(base, **{name: hi})) - loss(dict(base, **{name: lo}))) / (2 * step)
+            assert abs(fd - g[key][idx]) <= 1e-6 + 1e-5 * abs(fd), (name, idx, fd, g[key][idx])
+
+
+def test_scan_backward_decay_gradient_is_a_reverse_cumsum():
+    """A property of the scan backward (and the identity a chunked GPU scan
+    backward can use): the decay part of the dt gradient,
+    d(loss)/d(dt_t A_h) = (ddt_t - dx_t . x_t / dt_t) / A_h, equals
+    sum_{s >= t} (y_s . dy_s - dx_s . x_s) + <dh_last, h_last>
+      + sum over chunks c' >= chunk(t) of <dmem_c', dH_c'>,
+    since a_t <G_t, H_{t-1}> = <G_t, H_t> - <G_t, u_t> telescopes."""
+    rng = np.random.default_rng(41)
+    B_, L, H, G, P, N, S = 1, 19, 2, 1, 4, 3, 6
+    M = -(-L // S)
+    x = rng.standard_normal((B_, L, H, P))
+    dt = rng.uniform(0.05, 0.5, (B_, L, H))
+    A = -rng.uniform(0.5, 2.0, H)
+    Bm = rng.standard_normal((B_, L, G, N))
+    Cm = rng.standard_normal((B_, L, G, N))
+    h0 = rng.standard_normal((B_, H, N, P)) * 0.3
+    dy = rng.standard_normal((B_, L, H, P))
+    dmem = rng.standard_normal((B_, M, H, N, P))
+    dhl = rng.standard_normal((B_, H, N, P))
+    g = oracle.ssd_bwd(x, dt, A, Bm, Cm, S, dy, dmem=dmem, dh_last=dhl, h0=h0)
+    y, hl = oracle.ssd_recurrence(x, dt, A, Bm, Cm, h0=h0)
+    mem = oracle.chunk_memories(x, dt, A, Bm, S)
+    for h in range(H):
+        dxx = (g["dx"][0, :, h] * x[0, :, h]).sum(-1)
+        term = (y[0, :, h] * dy[0, :, h]).sum(-1) - dxx
+        memdot = (dmem[0, :, h] * mem[0, :, h]).sum((-1, -2))
+        for t in range(L):
+            lhs = (g["ddt"][0, t, h] - dxx[t] / dt[0, t, h]) / A[h]
+            rhs = term[t:].sum() + (dhl[0, h] * hl[0, h]).sum() + memdot[t // S:].sum()
+            assert abs(lhs - rhs) <= 1e-9 * (1 + abs(rhs)), (h, t, lhs, rhs)
