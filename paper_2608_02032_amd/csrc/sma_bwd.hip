@@ -26,7 +26,8 @@
 //   k_bwd_prep          Qbar (scaled by log2(e)/sqrt(N), storage dtype, the
 //                       forward's operand exactly) and Ebar (float) per token
 //   k_bwd_tokens        one workgroup per (64 tokens of one chunk, block of
-//                       heads of one group); one pass over (head, memory),
+//                       heads of one group), 8 waves, each pair splitting the
+//                       state index; one pass over (head, memory),
 //                       tiles streamed through an LDS ring by DMA:
 //                         W' = Kh^T Qbar' -> logits -> p;
 //                         X = dH dy^T = diag(1/r) Kh dy^T -> dwy, dC += g p X;
@@ -173,48 +174,56 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
 
 // ---- token-side gradients ------------------------------------------------------
 // Workgroup: 64 consecutive tokens of chunk i >= 1 (all in one chunk because
-// S is a multiple of 64) and hpb heads of one group.  Wave w owns tokens
-// 16 w .. 16 w + 15; in every MFMA product the memory tile is the A operand
-// (rows n or p) and the tokens are the 16 columns, so lane l works on token
-// l % 16 and its rows 4 (l / 16) + 0..3 of each 16-row tile.
+// S is a multiple of 64) and hpb heads of one group, 8 waves.  Waves w and
+// w + 4 share tokens 16 w .. 16 w + 15 and split the state index n in two
+// halves: each forms its half of every product and keeps only its half of
+// the per-token state, so a wave holds at most 256 registers and two waves
+// share a SIMD.  In every MFMA product the memory tile is the A operand (rows
+// n or p) and the tokens are the 16 columns, so lane l works on token l % 16
+// and its rows 4 (l / 16) + 0..3 of each 16-row tile.
 //
 // One pass over (head, memory j) steps.  Per step: W' = Kh^T Qbar'^T (logits,
-// p_j), X = dH dy^T (dwy_j, dC += g p_j X) and Z = Kh Ebar^T, all three from
-// the key-side tile alone (X as diag(1/r) Kh dy^T, so dH is not streamed;
-// in bf16 this reads dH through the key side's rounding).  dl_j needs
-// Dy = sum_j p_j dwy_j, known only after the head's last memory, so the head
-// accumulates S1 = sum_j p_j dwy_j Z_j, S2 = sum_j p_j Z_j (and T1, T2 with
-// W'), and adds g s (S1 - Dy S2) to dQbar and g ln2 (T1 - Dy T2) to dEbar at
-// its end (W' and Qbar' carry log2(e)/sqrt(N); ln2 takes it back to s).
+// p_j; the two halves add their partial contractions over n through LDS),
+// X = dH dy^T (dwy_j, likewise; dC += g p_j X) and Z = Kh Ebar^T, all three
+// from the key-side tile alone (X as diag(1/r) Kh dy^T, so dH is not
+// streamed; in bf16 this reads dH through the key side's rounding).  dl_j
+// needs Dy = sum_j p_j dwy_j, known only after the head's last memory, so the
+// head accumulates S1 = sum_j p_j dwy_j Z_j, S2 = sum_j p_j Z_j (and U1, U2
+// with W') and adds g s (S1 - Dy S2) to dQbar and g ln2 (U1 - Dy U2) to dEbar
+// at its end (W' and Qbar' carry log2(e)/sqrt(N); ln2 takes it back to s).
 // Tiles (Kh_j and the row of 1/r_j) stream through an NS-stage LDS ring by
-// DMA, NS - 1 steps ahead; each wave waits only for its own copies of the
-// current step and one barrier per step orders the stages.
+// DMA, NS - 1 steps ahead, copied by waves 0-3; each copying wave waits only
+// for its own copies of the current step and a barrier orders the stages.
 template <typename T, int N>
 constexpr int tok_stages() {
     return (N * kP * (int)sizeof(T) * 4 <= 131072) ? 4 : 2;
 }
 
 template <typename T, int N>
-__global__ __launch_bounds__(256) void k_bwd_tokens(
+__global__ __launch_bounds__(512) void k_bwd_tokens(
     const T* __restrict__ qb, const float* __restrict__ eb, const T* __restrict__ Cm,
     const float* __restrict__ rinv, const T* __restrict__ kmem, const T* __restrict__ z,
     const float* __restrict__ lse, const T* __restrict__ dy, float* __restrict__ gpw,
     float* __restrict__ gdw, float* __restrict__ part, float* __restrict__ rdy, int z_per_head,
-    int64_t L, int H, int G, int S, int64_t Mcap, int64_t Mp, int hpb, int blk0, int nblk,
-    int64_t BHC) {
+    int64_t L, int H, int G, int S, int64_t Mp, int hpb, int blk0, int nblk, int64_t BHC) {
     constexpr int RB = kP * (int)sizeof(T);  // bytes of one tile row (fixed n)
     constexpr int TILE = N * RB;
     constexpr int NT = N / 16;
     constexpr int KQ = N / 32;
+    constexpr int NTH = NT / 2;          // n tiles per wave
+    constexpr int QH = (KQ + 1) / 2;     // 32-deep n steps of W' per wave
     constexpr int NS = tok_stages<T, N>();
     using Copy = TileCopy<RB, TILE, kTokWaves>;
-    constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per wave
-    constexpr int CPS = Copy::count() + 1;  // DMA copies per wave per step
+    constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per copying wave
+    constexpr int CPS = Copy::count() + 1;  // DMA copies per copying wave per step
     __shared__ __attribute__((aligned(16))) char ring[NS][TILE];
     __shared__ __attribute__((aligned(16))) float rring[NS][N];
+    __shared__ float xch[2][2][kTokWaves][16];  // (logit, dwy) partials per half
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
+    const int tg = wave & 3, nh = wave >> 2;  // token group, half of n
+    const bool copier = wave < kTokWaves;
     // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
     // index and each XCD has its own L2.  When the number of (b, head block)
     // pairs is a multiple of 8, XCD x runs the token blocks of pairs x, x+8,
@@ -236,20 +245,22 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
     const int hb = (int)(bhc % nhb);
     const int64_t t0 = (int64_t)(blk0 + blk) * kTokBlock;
     const int nj = (int)(t0 / S);  // memories every token of the block attends
-    const int64_t t = t0 + wave * 16 + col;
+    const int64_t t = t0 + tg * 16 + col;
     const bool valid = t < L;
     const int64_t tc = valid ? t : L - 1;
     const int h0 = hb * hpb;
     const int g = h0 / (H / G);
     const int64_t bt = b * L + tc;
     const float isn = 1.0f / sqrtf((float)N);
+    const int nt0 = nh * NTH;  // first n tile of this wave
 
-    // group-shared token operands
-    Frag<T> qf[KQ];
+    // group-shared token operands (this wave's half of Qbar' and C)
+    Frag<T> qf[QH];
     {
         const T* qrow = qb + (bt * G + g) * N;
 #pragma unroll
-        for (int ks = 0; ks < KQ; ++ks) {
+        for (int k = 0; k < QH; ++k) {
+            const int ks = nh * QH + k < KQ ? nh * QH + k : KQ - 1;
             float a[4], c[4], v[8];
             load4(qrow + ks * 32 + 4 * grp, a);
             load4(qrow + ks * 32 + 16 + 4 * grp, c);
@@ -258,7 +269,7 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
                 v[i] = a[i];
                 v[4 + i] = c[i];
             }
-            qf[ks] = make_frag<T>(v);
+            qf[k] = make_frag<T>(v);
         }
     }
     const float* erow = eb + (bt * G + g) * kP;
@@ -272,30 +283,31 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
     }
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) load4(erow + 16 * pt + 4 * grp, ea[pt]);
-    float ca[NT][4];
+    float ca[NTH][4];
     {
         const T* crow = Cm + (bt * G + g) * N;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) load4(crow + 16 * nt + 4 * grp, ca[nt]);
+        for (int k = 0; k < NTH; ++k) load4(crow + 16 * (nt0 + k) + 4 * grp, ca[k]);
     }
 
     const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
-    f32x4 dQ[NT], dC[NT], dE[4], s1[NT], s2[NT], u1[4], u2[4];
+    f32x4 dQ[NTH], dC[NTH], dE[4], s1[NTH], s2[NTH], u1[4], u2[4];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) dQ[nt] = dC[nt] = zero4;
+    for (int k = 0; k < NTH; ++k) dQ[k] = dC[k] = zero4;
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) dE[pt] = zero4;
 
     const int nsteps = hpb * nj;
     Copy copy;
-    copy.init(wave, lane);
+    copy.init(tg, lane);
     auto issue_tiles = [&](int k) {
+        if (!copier) return;
         const int hh = k / nj, j = k - hh * nj;
         const int64_t hj = (b * Mp + j) * H + h0 + hh;
         copy.issue(kmem + hj * N * kP, ring[k % NS]);
         if (lane < RPW)
-            lds_dma16_untracked_at(rinv + hj * N + (wave * RPW + lane) * 4,
-                                   lds_addr(&rring[k % NS][0]) + wave * RPW * 16);
+            lds_dma16_untracked_at(rinv + hj * N + (tg * RPW + lane) * 4,
+                                   lds_addr(&rring[k % NS][0]) + tg * RPW * 16);
     };
     // per (head, memory) scalar slot of this lane's token
     auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * L + tc; };
@@ -332,67 +344,78 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
             keep(dyf[1]);
             asm volatile("" ::"v"(lse2), "v"(gate));
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) s1[nt] = s2[nt] = zero4;
+            for (int q = 0; q < NTH; ++q) s1[q] = s2[q] = zero4;
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) u1[pt] = u2[pt] = zero4;
         }
         if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
         const char* kt = ring[k % NS];
-        // W'^T = Kh^T Qbar'^T: rows p, token columns (log2-scaled scores)
+        // this half's part of W'^T = Kh^T Qbar'^T: rows p, token columns
         f32x4 w[4];
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) w[pt] = zero4;
 #pragma unroll
-        for (int ks = 0; ks < KQ; ++ks) {
+        for (int q = 0; q < QH; ++q) {
+            const int ks = nh * QH + q;
+            if (ks < KQ) {
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt)
-                w[pt] = mma16(w[pt], frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp,
-                                                   16 * pt, lane),
-                              qf[ks]);
+                for (int pt = 0; pt < 4; ++pt)
+                    w[pt] = mma16(w[pt], frag_km<T, RB>(kt, 32 * ks + 4 * grp,
+                                                       32 * ks + 16 + 4 * grp, 16 * pt, lane),
+                                  qf[q]);
+            }
         }
         float l2 = 0.f;
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) l2 += ea[pt][i] * w[pt][i];
-        l2 += shfl_xor(l2, 16);
-        l2 += shfl_xor(l2, 32);
-        const float p = fast_exp2(l2 - lse2);
-        // X^T = dH dy^T = diag(1/r) Kh dy^T and Z^T = Kh Ebar^T: rows n, token
-        // columns, both from the same key-side fragments
-        f32x4 x[NT], zz[NT];
+        // X^T = diag(1/r) Kh dy^T and Z^T = Kh Ebar^T on this half's n tiles
+        f32x4 x[NTH], zz[NTH];
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            x[nt] = zz[nt] = zero4;
+        for (int q = 0; q < NTH; ++q) {
+            const int nt = nt0 + q;
+            x[q] = zz[q] = zero4;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const Frag<T> a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
-                x[nt] = mma16(x[nt], a, dyf[ks]);
-                zz[nt] = mma16(zz[nt], a, ef[ks]);
+                x[q] = mma16(x[q], a, dyf[ks]);
+                zz[q] = mma16(zz[q], a, ef[ks]);
             }
-            x[nt] *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+            x[q] *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
         }
         float dw = 0.f;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
+        for (int q = 0; q < NTH; ++q)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) dw += ca[nt][i] * x[nt][i];
+            for (int i = 0; i < 4; ++i) dw += ca[q][i] * x[q][i];
+        l2 += shfl_xor(l2, 16);
+        l2 += shfl_xor(l2, 32);
         dw += shfl_xor(dw, 16);
         dw += shfl_xor(dw, 32);
+        // the other half's partial sums
+        if (lane < 16) {
+            xch[0][nh][tg][col] = l2;
+            xch[1][nh][tg][col] = dw;
+        }
+        lds_barrier();
+        l2 += xch[0][nh ^ 1][tg][col];
+        dw += xch[1][nh ^ 1][tg][col];
+        const float p = fast_exp2(l2 - lse2);
         Dy += p * dw;
         const float gp = gate * p, pd = p * dw;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            dC[nt] += gp * x[nt];
-            s1[nt] += pd * zz[nt];
-            s2[nt] += p * zz[nt];
+        for (int q = 0; q < NTH; ++q) {
+            dC[q] += gp * x[q];
+            s1[q] += pd * zz[q];
+            s2[q] += p * zz[q];
         }
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) {
             u1[pt] += pd * w[pt];
             u2[pt] += p * w[pt];
         }
-        if (lane < 16 && valid) {
+        if (nh == 0 && lane < 16 && valid) {
             gpw[sidx(h, j)] = gp;
             gdw[sidx(h, j)] = dw;
         }
@@ -400,23 +423,36 @@ __global__ __launch_bounds__(256) void k_bwd_tokens(
             // the head's dl_j = g p_j (dwy_j - Dy), summed against Z and W'
             const float cq = gate * isn, ce = gate * kLn2;
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) dQ[nt] += cq * (s1[nt] - Dy * s2[nt]);
+            for (int q = 0; q < NTH; ++q) dQ[q] += cq * (s1[q] - Dy * s2[q]);
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) dE[pt] += ce * (u1[pt] - Dy * u2[pt]);
-            if (lane < 16 && valid) rdy[bt * H + h] = Dy;
+            if (nh == 0 && lane < 16 && valid) rdy[bt * H + h] = Dy;
         }
     }
 
+    // the two halves' dEbar partials meet in LDS (the ring is free now)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
+    f32x4* dex = reinterpret_cast<f32x4*>(&ring[0][0]) + (tg * 64 + lane) * 4;
+    if (nh == 1) {
+#pragma unroll
+        for (int pt = 0; pt < 4; ++pt) dex[pt] = dE[pt];
+    }
+    lds_barrier();
     if (!valid) return;
     // per-head-block partial sums: dQbar [N], dEbar [P], dC [N]
     float* pr = part + (bt * nhb + hb) * (2 * N + kP);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-        *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[nt];
-        *reinterpret_cast<f32x4*>(pr + N + kP + 16 * nt + 4 * grp) = dC[nt];
+    for (int q = 0; q < NTH; ++q) {
+        const int nt = nt0 + q;
+        *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[q];
+        *reinterpret_cast<f32x4*>(pr + N + kP + 16 * nt + 4 * grp) = dC[q];
     }
+    if (nh == 0) {
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) *reinterpret_cast<f32x4*>(pr + N + 16 * pt + 4 * grp) = dE[pt];
+        for (int pt = 0; pt < 4; ++pt)
+            *reinterpret_cast<f32x4*>(pr + N + 16 * pt + 4 * grp) = dE[pt] + dex[pt];
+    }
 }
 
 // ---- memory-side gradients -------------------------------------------------------
@@ -782,10 +818,10 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     if (Mp > 0 && nblk > 0) {
         prof_begin("k_bwd_tokens", st);
         const int64_t BHC = s.B * (s.H / hpb);
-        k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 256, 0, st>>>(
+        k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
             (const T*)w.qb, w.eb, (const T*)Cm, w.rinv, (const T*)w.kmem, (const T*)z, lse,
-            (const T*)dy, w.gp, w.gd, w.part, w.rdy, a.z_per_head, s.L, s.H, s.G, s.S, s.Mcap, Mp,
-            hpb, blk0, (int)nblk, BHC);
+            (const T*)dy, w.gp, w.gd, w.part, w.rdy, a.z_per_head, s.L, s.H, s.G, s.S, Mp, hpb,
+            blk0, (int)nblk, BHC);
         prof_end(st);
     }
     const int64_t BH = s.B * s.H;
