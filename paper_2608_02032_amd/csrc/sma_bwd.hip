@@ -175,15 +175,15 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
 // ---- token-side gradients ------------------------------------------------------
 // Workgroup: 64 consecutive tokens of chunk i >= 1 (all in one chunk because
 // S is a multiple of 64) and hpb heads of one group, 8 waves.  Waves w and
-// w + 4 share tokens 16 w .. 16 w + 15 and split the state index n in two
-// halves: each forms its half of every product and keeps only its half of
-// the per-token state, so a wave holds at most 256 registers and two waves
+// w + 4 share tokens 16 w .. 16 w + 15 and split the work in halves: rows p
+// of W' (and dEbar), rows n of X and Z (and dQbar, dC); each keeps only its
+// half of the per-token state, so a wave fits 256 registers and two waves
 // share a SIMD.  In every MFMA product the memory tile is the A operand (rows
 // n or p) and the tokens are the 16 columns, so lane l works on token l % 16
 // and its rows 4 (l / 16) + 0..3 of each 16-row tile.
 //
 // One pass over (head, memory j) steps.  Per step: W' = Kh^T Qbar'^T (logits,
-// p_j; the two halves add their partial contractions over n through LDS),
+// p_j; the two halves add their partial sums over p through LDS),
 // X = dH dy^T (dwy_j, likewise; dC += g p_j X) and Z = Kh Ebar^T, all three
 // from the key-side tile alone (X as diag(1/r) Kh dy^T, so dH is not
 // streamed; in bf16 this reads dH through the key side's rounding).  dl_j
@@ -211,7 +211,6 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     constexpr int NT = N / 16;
     constexpr int KQ = N / 32;
     constexpr int NTH = NT / 2;          // n tiles per wave
-    constexpr int QH = (KQ + 1) / 2;     // 32-deep n steps of W' per wave
     constexpr int NS = tok_stages<T, N>();
     using Copy = TileCopy<RB, TILE, kTokWaves>;
     constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per copying wave
@@ -253,14 +252,14 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     const int64_t bt = b * L + tc;
     const float isn = 1.0f / sqrtf((float)N);
     const int nt0 = nh * NTH;  // first n tile of this wave
+    const int pt0 = nh * 2;    // first p tile of this wave
 
-    // group-shared token operands (this wave's half of Qbar' and C)
-    Frag<T> qf[QH];
+    // group-shared token operands (Qbar' whole; this wave's halves of Ebar, C)
+    Frag<T> qf[KQ];
     {
         const T* qrow = qb + (bt * G + g) * N;
 #pragma unroll
-        for (int k = 0; k < QH; ++k) {
-            const int ks = nh * QH + k < KQ ? nh * QH + k : KQ - 1;
+        for (int ks = 0; ks < KQ; ++ks) {
             float a[4], c[4], v[8];
             load4(qrow + ks * 32 + 4 * grp, a);
             load4(qrow + ks * 32 + 16 + 4 * grp, c);
@@ -269,12 +268,12 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
                 v[i] = a[i];
                 v[4 + i] = c[i];
             }
-            qf[k] = make_frag<T>(v);
+            qf[ks] = make_frag<T>(v);
         }
     }
     const float* erow = eb + (bt * G + g) * kP;
     Frag<T> ef[2];
-    float ea[4][4];
+    float ea[2][4];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
         float v[8];
@@ -282,20 +281,23 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         ef[ks] = make_frag<T>(v);
     }
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) load4(erow + 16 * pt + 4 * grp, ea[pt]);
-    float ca[NTH][4];
+    for (int q = 0; q < 2; ++q) load4(erow + 16 * (pt0 + q) + 4 * grp, ea[q]);
+    // C in the storage dtype (half the registers in bf16), widened where used
+    typedef T T4 __attribute__((ext_vector_type(4)));
+    T4 ca[NTH];
     {
         const T* crow = Cm + (bt * G + g) * N;
 #pragma unroll
-        for (int k = 0; k < NTH; ++k) load4(crow + 16 * (nt0 + k) + 4 * grp, ca[k]);
+        for (int k = 0; k < NTH; ++k)
+            ca[k] = *reinterpret_cast<const T4*>(crow + 16 * (nt0 + k) + 4 * grp);
     }
 
     const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
-    f32x4 dQ[NTH], dC[NTH], dE[4], s1[NTH], s2[NTH], u1[4], u2[4];
+    f32x4 dQ[NTH], dC[NTH], dE[2], s1[NTH], s2[NTH], u1[2], u2[2];
 #pragma unroll
     for (int k = 0; k < NTH; ++k) dQ[k] = dC[k] = zero4;
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) dE[pt] = zero4;
+    for (int q = 0; q < 2; ++q) dE[q] = zero4;
 
     const int nsteps = hpb * nj;
     Copy copy;
@@ -346,30 +348,27 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
 #pragma unroll
             for (int q = 0; q < NTH; ++q) s1[q] = s2[q] = zero4;
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt) u1[pt] = u2[pt] = zero4;
+            for (int q = 0; q < 2; ++q) u1[q] = u2[q] = zero4;
         }
         if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
         const char* kt = ring[k % NS];
-        // this half's part of W'^T = Kh^T Qbar'^T: rows p, token columns
-        f32x4 w[4];
+        // this half's rows p of W'^T = Kh^T Qbar'^T: token columns
+        f32x4 w[2];
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt) w[pt] = zero4;
+        for (int q = 0; q < 2; ++q) w[q] = zero4;
 #pragma unroll
-        for (int q = 0; q < QH; ++q) {
-            const int ks = nh * QH + q;
-            if (ks < KQ) {
+        for (int ks = 0; ks < KQ; ++ks) {
 #pragma unroll
-                for (int pt = 0; pt < 4; ++pt)
-                    w[pt] = mma16(w[pt], frag_km<T, RB>(kt, 32 * ks + 4 * grp,
-                                                       32 * ks + 16 + 4 * grp, 16 * pt, lane),
-                                  qf[q]);
-            }
+            for (int q = 0; q < 2; ++q)
+                w[q] = mma16(w[q], frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp,
+                                                  16 * (pt0 + q), lane),
+                             qf[ks]);
         }
         float l2 = 0.f;
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt)
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) l2 += ea[pt][i] * w[pt][i];
+            for (int i = 0; i < 4; ++i) l2 += ea[q][i] * w[q][i];
         // X^T = diag(1/r) Kh dy^T and Z^T = Kh Ebar^T on this half's n tiles
         f32x4 x[NTH], zz[NTH];
 #pragma unroll
@@ -388,7 +387,7 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
 #pragma unroll
         for (int q = 0; q < NTH; ++q)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) dw += ca[q][i] * x[q][i];
+            for (int i = 0; i < 4; ++i) dw += to_f(ca[q][i]) * x[q][i];
         l2 += shfl_xor(l2, 16);
         l2 += shfl_xor(l2, 32);
         dw += shfl_xor(dw, 16);
@@ -411,9 +410,9 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
             s2[q] += p * zz[q];
         }
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt) {
-            u1[pt] += pd * w[pt];
-            u2[pt] += p * w[pt];
+        for (int q = 0; q < 2; ++q) {
+            u1[q] += pd * w[q];
+            u2[q] += p * w[q];
         }
         if (nh == 0 && lane < 16 && valid) {
             gpw[sidx(h, j)] = gp;
@@ -425,20 +424,11 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
 #pragma unroll
             for (int q = 0; q < NTH; ++q) dQ[q] += cq * (s1[q] - Dy * s2[q]);
 #pragma unroll
-            for (int pt = 0; pt < 4; ++pt) dE[pt] += ce * (u1[pt] - Dy * u2[pt]);
+            for (int q = 0; q < 2; ++q) dE[q] += ce * (u1[q] - Dy * u2[q]);
             if (nh == 0 && lane < 16 && valid) rdy[bt * H + h] = Dy;
         }
     }
 
-    // the two halves' dEbar partials meet in LDS (the ring is free now)
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    lds_barrier();
-    f32x4* dex = reinterpret_cast<f32x4*>(&ring[0][0]) + (tg * 64 + lane) * 4;
-    if (nh == 1) {
-#pragma unroll
-        for (int pt = 0; pt < 4; ++pt) dex[pt] = dE[pt];
-    }
-    lds_barrier();
     if (!valid) return;
     // per-head-block partial sums: dQbar [N], dEbar [P], dC [N]
     float* pr = part + (bt * nhb + hb) * (2 * N + kP);
@@ -448,11 +438,9 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[q];
         *reinterpret_cast<f32x4*>(pr + N + kP + 16 * nt + 4 * grp) = dC[q];
     }
-    if (nh == 0) {
 #pragma unroll
-        for (int pt = 0; pt < 4; ++pt)
-            *reinterpret_cast<f32x4*>(pr + N + 16 * pt + 4 * grp) = dE[pt] + dex[pt];
-    }
+    for (int q = 0; q < 2; ++q)
+        *reinterpret_cast<f32x4*>(pr + N + 16 * (pt0 + q) + 4 * grp) = dE[q];
 }
 
 // ---- memory-side gradients -------------------------------------------------------
