@@ -451,8 +451,12 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
 // tokens per step are copied into LDS by DMA one step ahead, and the
 // per-(memory, token) factors g p_j and ln2 dl_j (zero where memory j is not
 // attended) scale the dy and Ebar fragments in registers.  Wave w owns the
-// output columns p = 16 (w % 4) .. + 15 and half of the n tiles.  Memories
-// j >= M - 1 (attended by no token) are written as zeros.
+// output columns p = 16 (w % 4) .. + 15 and half of the n tiles.  The token
+// tiles stream through a 3-stage LDS ring, two steps ahead: waves 0-3 issue
+// the DMA copies (and wait for their own with exact counts), waves 4-7 load
+// the factors of the step two ahead and write them to LDS at the end of the
+// current one, so the ordinary loads never make a copying wave drain its
+// copies.  Memories j >= M - 1 (attended by no token) are written as zeros.
 template <typename T>
 constexpr int mem_tb() { return sizeof(T) == 2 ? 64 : 32; }
 
@@ -487,8 +491,12 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     constexpr int NT = N / 16;
     constexpr int NH = NT / 2;  // n tiles per wave
     static_assert(NH >= 1, "at least two n tiles");
-    __shared__ __attribute__((aligned(16))) char buf[2][STAGE];
-    __shared__ __attribute__((aligned(16))) float sc[2][J][2][TB];
+    constexpr int NS = 3;
+    // DMA copies per copying wave per step (every tile is a multiple of 256 pieces)
+    constexpr int CPW = (2 * TB * RBN / 16 + 2 * TB * RBP / 16) / 256;
+    static_assert((TB * RBP / 16) % 256 == 0, "tiles must split evenly over four waves");
+    __shared__ __attribute__((aligned(16))) char buf[NS][STAGE];
+    __shared__ __attribute__((aligned(16))) float sc[NS][J][2][TB];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -515,27 +523,32 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     const int nstep = (int)((L - tbeg + TB - 1) / TB);
     const int64_t grow = (b * L) * G + g;  // row of token 0 in the [B][L][G] layout
 
+    const bool copier = wave < 4;
     auto issue = [&](int st) {
+        if (!copier || st >= nstep) return;
         const int64_t t0 = tbeg + (int64_t)st * TB;
         const int rv = (int)(L - t0 < TB ? L - t0 : TB);
-        char* d = buf[st & 1];
+        char* d = buf[st % NS];
         dma_tile<RBN, true>(d, reinterpret_cast<const char*>(Cm + (grow + t0 * G) * N),
-                            (int64_t)G * RBN, TB, rv, wave, 8, lane);
+                            (int64_t)G * RBN, TB, rv, wave, 4, lane);
         dma_tile<RBN, true>(d + CT, reinterpret_cast<const char*>(qb + (grow + t0 * G) * N),
-                            (int64_t)G * RBN, TB, rv, wave, 8, lane);
+                            (int64_t)G * RBN, TB, rv, wave, 4, lane);
         dma_tile<RBP, true>(d + 2 * CT,
                             reinterpret_cast<const char*>(dy + ((b * L + t0) * H + h) * kP),
-                            (int64_t)H * RBP, TB, rv, wave, 8, lane);
+                            (int64_t)H * RBP, TB, rv, wave, 4, lane);
         dma_tile<RBP, true>(d + 2 * CT + DT,
                             reinterpret_cast<const char*>(ebt + (grow + t0 * G) * kP),
-                            (int64_t)G * RBP, TB, rv, wave, 8, lane);
+                            (int64_t)G * RBP, TB, rv, wave, 4, lane);
     };
-    // factors of step st: g p_j[t] and ln2 dl_j[t] = ln2 g p_j (dwy_j - Dy)
+    // factors of step st: g p_j[t] and ln2 dl_j[t] = ln2 g p_j (dwy_j - Dy),
+    // loaded and stored by waves 4-7 (thread ft = tid - 256 of J * TB = 256)
+    static_assert(J * TB <= 256, "one factor per thread of waves 4-7");
+    const int ft = tid - 256;
     float fg = 0.f, fd = 0.f;
     auto load_factors = [&](int st) {
         fg = fd = 0.f;
-        if (tid < J * TB) {
-            const int jl = tid / TB, tk = tid % TB;
+        if (ft >= 0 && ft < J * TB && st < nstep) {
+            const int jl = ft / TB, tk = ft % TB;
             const int64_t j = j0 + jl, t = tbeg + (int64_t)st * TB + tk;
             if (j < Mp && t < L && t >= (j + 1) * S) {
                 const int64_t si = ((b * H + h) * Mp + j) * L + t;
@@ -546,10 +559,10 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
         }
     };
     auto store_factors = [&](int st) {
-        if (tid < J * TB) {
-            const int jl = tid / TB, tk = tid % TB;
-            sc[st & 1][jl][0][tk] = fg;
-            sc[st & 1][jl][1][tk] = fd;
+        if (ft >= 0 && ft < J * TB && st < nstep) {
+            const int jl = ft / TB, tk = ft % TB;
+            sc[st % NS][jl][0][tk] = fg;
+            sc[st % NS][jl][1][tk] = fd;
         }
     };
 
@@ -560,16 +573,22 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
         for (int k = 0; k < NH; ++k) m1[jl][k] = m2[jl][k] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     issue(0);
+    issue(1);
     load_factors(0);
     store_factors(0);
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    lds_barrier();
+    load_factors(1);
+    store_factors(1);
     for (int st = 0; st < nstep; ++st) {
+        // this step's copies landed (the next step's may stay in flight)
         if (st + 1 < nstep) {
-            issue(st + 1);
-            load_factors(st + 1);
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPW));
+        } else {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         }
-        const char* cs = buf[st & 1];
+        lds_barrier();
+        issue(st + 2);
+        load_factors(st + 2);
+        const char* cs = buf[st % NS];
         const char* qs = cs + CT;
         const char* dyt = cs + 2 * CT;
         const char* et = dyt + DT;
@@ -586,10 +605,10 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
             }
 #pragma unroll
             for (int jl = 0; jl < J; ++jl) {
-                const f32x4 g0 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][0][r0]);
-                const f32x4 g1 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][0][r1]);
-                const f32x4 d0 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][1][r0]);
-                const f32x4 d1 = *reinterpret_cast<const f32x4*>(&sc[st & 1][jl][1][r1]);
+                const f32x4 g0 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][0][r0]);
+                const f32x4 g1 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][0][r1]);
+                const f32x4 d0 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][1][r0]);
+                const f32x4 d1 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][1][r1]);
                 const Frag<T> bdj = scale_frag<T>(bd, g0, g1);
                 const Frag<T> bej = scale_frag<T>(be, d0, d1);
 #pragma unroll
@@ -599,10 +618,10 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
                 }
             }
         }
-        if (st + 1 < nstep) store_factors(st + 1);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-        lds_barrier();
+        store_factors(st + 2);
     }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
 
     // epilogue per memory: r[n] and dr[n] = sum_p dH[n,p] M2[n,p] reduced over
     // the four column waves through LDS (the stage buffers are free now)
