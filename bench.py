@@ -44,6 +44,8 @@ def parse():
                     help="skip the separately timed ragged-batch decode steps")
     ap.add_argument("--no-bwd", action="store_true",
                     help="skip the separately timed SMA backward on the same workload")
+    ap.add_argument("--no-block", action="store_true",
+                    help="skip the separately timed block kernels (conv, dt, gated norm)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batches", type=int, default=4,
                     help="batches of the workload the CPU oracle is timed on")
@@ -422,6 +424,56 @@ def main():
             "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(bavg.items())},
             "traffic_bytes": {k: traffic_for(k) for k in ("k_bwd_tokens", "k_bwd_mem")}}
         del ws_bwd, grads
+
+    if not args.no_block:
+        # the block around the path at the same shape, timed on its own: the
+        # width-4 convolution + SiLU over the x, B, C channels of an input
+        # projection row (z, xBC, dt, q, e and gate columns), softplus step
+        # sizes, and the gated RMSNorm over the H*P output channels
+        G_, N_ = w.ngroups, w.dstate
+        D_in = H * P
+        C_conv = D_in + 2 * G_ * N_
+        row = D_in + C_conv + H + G_ * (N_ + P) + H
+        g = torch.Generator(device=dev)
+        g.manual_seed(5)
+        proj = torch.randn((B, L, row), generator=g, device=dev).to(bf)
+        cw = torch.randn((C_conv, 4), generator=g, device=dev) * 0.5
+        cb = torch.randn((C_conv,), generator=g, device=dev) * 0.1
+        st_c = torch.zeros((B, C_conv, 3), dtype=torch.float32, device=dev)
+        conv_out = torch.empty((B, L, C_conv), dtype=bf, device=dev)
+        dtb = torch.randn((H,), generator=g, device=dev)
+        dt_out = torch.empty((B, L, H), dtype=torch.float32, device=dev)
+        ynorm = torch.empty((B, L, D_in), dtype=bf, device=dev)
+        nw = torch.ones((D_in,), dtype=torch.float32, device=dev)
+        yv = y.view(B, L, D_in) if y.is_contiguous() else y.reshape(B, L, D_in)
+        legs = {
+            "conv1d_silu": (lambda: dart.conv1d_silu(proj[:, :, D_in:], cw, cb, state_out=st_c,
+                                                     channels=C_conv, out=conv_out, stream=stream),
+                            2 * B * L * C_conv * 2 + B * C_conv * 12),
+            "dt_softplus": (lambda: dart.dt_softplus(proj[:, :, D_in + C_conv:], dtb, nheads=H,
+                                                     out=dt_out, stream=stream),
+                            B * L * H * (2 + 4)),
+            "gated_rmsnorm": (lambda: dart.gated_rmsnorm(yv, proj[:, :, :D_in], nw, out=ynorm,
+                                                         stream=stream),
+                              3 * B * L * D_in * 2),
+        }
+        blk = {}
+        for name, (fn, nbytes) in legs.items():
+            for _ in range(3):
+                fn()
+            ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            torch.cuda.synchronize()
+            ev2[0].record(stream)
+            for _ in range(10):
+                fn()
+            ev2[1].record(stream)
+            torch.cuda.synchronize()
+            ms = ev2[0].elapsed_time(ev2[1]) / 10
+            blk[name] = {"us": round(ms * 1e3, 2), "algorithmic_bytes": nbytes,
+                         "hbm_gbps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                         "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4)}
+        extra["block"] = blk
+        del proj, conv_out, dt_out, ynorm
 
     tokens = B * L
     line = {

@@ -188,6 +188,56 @@ dart_status dart_sma_bwd(const dart_dims* dims, const dart_sma_opts* opts, const
                          float* dmem, float* dz, void* workspace, size_t workspace_bytes,
                          void* stream);
 
+/*
+ * The steps either side of the path in the DART (Mamba-2) block.  The paper
+ * fixes the convolution width (4) and RMSNorm (App. D.2, with Table 8); the
+ * conventions below are those of the Mamba-2 block it builds on.  All three
+ * are stream-ordered elementwise or row-local kernels; none allocates.
+ *
+ * dart_conv1d_silu: causal depthwise convolution of width 4 over the token
+ * axis with bias and SiLU, on the x, B and C channels of the input
+ * projection:  out[b][t][c] = SiLU(bias[c] + sum_{k=0..3} w[c][k] in[b][t-3+k][c]),
+ * where in[b][s][c] for s < 0 is state_in[b][c][3+s] (zero when state_in is
+ * NULL).  state_out (optional) receives the last three inputs of each
+ * channel, oldest first: the decode cache of the convolution, so a call
+ * over tokens 0..L-1 followed by one over L.. with that state equals one call
+ * over both (a decode step is seqlen = 1).
+ *   in         [B][L][row_stride] storage dtype, channel c at element c of
+ *              the row (pass a pointer to the first x channel of the
+ *              projection output)
+ *   weight     [C][4] float (weight[c][3] multiplies the current token)
+ *   bias       [C] float, or NULL
+ *   state_in   [B][C][3] float, or NULL;  state_out [B][C][3] float, or NULL
+ *              (state_out may equal state_in when seqlen <= 32)
+ *   out        [B][L][C] storage dtype
+ */
+dart_status dart_conv1d_silu(int64_t batch, int64_t seqlen, int32_t channels, int64_t row_stride,
+                             int32_t dtype, const void* in, const float* weight, const float* bias,
+                             const float* state_in, float* state_out, void* out, void* stream);
+
+/*
+ * Step sizes from the projection: dt[r][h] = softplus(raw[r][h] + bias[h])
+ * = log(1 + exp(.)), in float (the scan takes dt already positive).
+ *   raw  [rows][row_stride] storage dtype (head h at element h of the row)
+ *   bias [H] float, or NULL;  dt [rows][H] float
+ */
+dart_status dart_dt_softplus(int64_t rows, int32_t nheads, int64_t row_stride, int32_t dtype,
+                             const void* raw, const float* bias, float* dt, void* stream);
+
+/*
+ * Gated RMSNorm ahead of the output projection: with u = y (.) SiLU(z),
+ *   out = u / sqrt(mean over its group of u^2 + eps) (.) weight,
+ * over consecutive groups of `group` channels of each row (group = dim for
+ * one group).
+ *   y, out [rows][dim] storage dtype;  z [rows][z_row_stride] storage dtype
+ *   (the gate channels of the projection output);  weight [dim] float or NULL
+ * Requirements: group divides dim, group and z_row_stride multiples of 8,
+ * y, z, out and weight 16-byte aligned, eps > 0.
+ */
+dart_status dart_gated_rmsnorm(int64_t rows, int32_t dim, int32_t group, int32_t dtype,
+                               const void* y, const void* z, int64_t z_row_stride,
+                               const float* weight, float eps, void* out, void* stream);
+
 /* Bytes of workspace dart_decode_step needs (dims->seqlen is ignored; the
  * worst case over positions that fit dims->mem_capacity is returned). */
 size_t dart_decode_workspace_bytes(const dart_dims* dims);

@@ -62,6 +62,12 @@ def _load():
                                             _D, _D, _D, _D, _D, _D, _D, _D, _D,
                                             _D, _D, _D, _D, _D, _D]
         lib.dart_oracle_ssd_bwd.restype = None
+        lib.dart_oracle_conv1d_silu.argtypes = [_I64, _I64, _INT, _I64, _D, _D, _D, _D, _D, _D]
+        lib.dart_oracle_conv1d_silu.restype = None
+        lib.dart_oracle_dt_softplus.argtypes = [_I64, _INT, _D, _D, _D]
+        lib.dart_oracle_dt_softplus.restype = None
+        lib.dart_oracle_gated_rmsnorm.argtypes = [_I64, _INT, _INT, ctypes.c_double, _D, _D, _D, _D]
+        lib.dart_oracle_gated_rmsnorm.restype = None
         lib.dart_oracle_chunk_memories.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
                                                    _D, _D, _D, _D, _D]
         lib.dart_oracle_chunk_memories.restype = None
@@ -272,3 +278,44 @@ def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem, S, eps=
     if rc != 0:
         raise ValueError("decode position %d does not fit a cache of %d memories" % (pos, Mcap))
     return y
+
+
+def conv1d_silu(inp, w, bias=None, state=None, channels=None):
+    """Causal width-4 depthwise convolution + bias + SiLU over the token axis.
+    inp [B][L][R] (the first `channels` of each row's R elements are the
+    channels, default all), w [C][4] (w[c][3] multiplies the current token),
+    bias [C], state [B][C][3] (the three inputs before token 0, oldest first)
+    or None.  Returns (out [B][L][C], state_out [B][C][3])."""
+    inp, w = _f64(inp), _f64(w)
+    B_, L, R = inp.shape
+    C = R if channels is None else int(channels)
+    bias = None if bias is None else _f64(bias)
+    state = None if state is None else _f64(state)
+    out = np.empty((B_, L, C))
+    st = np.empty((B_, C, 3))
+    _load().dart_oracle_conv1d_silu(B_, L, C, R, _ptr(inp), _ptr(w), _ptr(bias), _ptr(state),
+                                    _ptr(out), _ptr(st))
+    return out, st
+
+
+def dt_softplus(raw, bias=None):
+    """dt = softplus(raw + bias[h]); raw [..][H]."""
+    raw = _f64(raw)
+    H = raw.shape[-1]
+    bias = None if bias is None else _f64(bias)
+    out = np.empty_like(raw)
+    _load().dart_oracle_dt_softplus(raw.size // H, H, _ptr(raw), _ptr(bias), _ptr(out))
+    return out
+
+
+def gated_rmsnorm(y, z, w=None, group=None, eps=1e-6):
+    """u = y * SiLU(z); u / sqrt(mean over each group of `group` channels of
+    u^2 + eps) * w.  y, z [..][D]; w [D] or None."""
+    y, z = _f64(y), _f64(z)
+    D = y.shape[-1]
+    group = D if group is None else int(group)
+    w = None if w is None else _f64(w)
+    out = np.empty_like(y)
+    _load().dart_oracle_gated_rmsnorm(y.size // D, D, group, float(eps), _ptr(y), _ptr(z), _ptr(w),
+                                      _ptr(out))
+    return out

@@ -37,6 +37,11 @@
  *   dart_oracle_sma_bwd          gradients of dart_oracle_sma (loss sum dy . y)
  *                                by recomputing every row (App. C) and the chain
  *                                rule through Sec. 3 and App. B.1, written out.
+ *   dart_oracle_conv1d_silu,     the block around the path: causal width-4
+ *   dart_oracle_dt_softplus,     convolution + SiLU with its carried state,
+ *   dart_oracle_gated_rmsnorm    softplus step sizes, gated RMSNorm (the
+ *                                conventions of the Mamba-2 block; "parity
+ *                                unpinned" beyond the definitions).
  *   dart_oracle_decode_step      one autoregressive token (the paper gives no
  *                                algorithm; the order used is: update the
  *                                recurrent state and the running chunk
@@ -745,4 +750,81 @@ int dart_oracle_decode_step(int64_t B, int H, int G, int P, int N, int S, int64_
         }
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The block around the path (Table 8 context: convolution width 4 and      */
+/* RMSNorm; the remaining conventions are those of the Mamba-2 block DART   */
+/* builds on).                                                              */
+/*                                                                          */
+/* Causal depthwise convolution of width 4 over the token axis with bias    */
+/* and SiLU: out[t][c] = SiLU(bias[c] + sum_{k=0..3} w[c][k] in[t-3+k][c]),  */
+/* where in[t] for t < 0 is the carried state (st_in[c][3 + t], zeros when  */
+/* absent).  st_out receives the last three inputs in token order (the     */
+/* decode cache of the convolution).  in rows have `stride` elements, the   */
+/* channels the first C of them.                                           */
+/* ------------------------------------------------------------------------ */
+void dart_oracle_conv1d_silu(int64_t B, int64_t L, int C, int64_t stride, const double* in,
+                             const double* w, const double* bias, const double* st_in,
+                             double* out, double* st_out) {
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t b = 0; b < B; ++b) {
+        for (int c = 0; c < C; ++c) {
+            for (int64_t t = 0; t < L; ++t) {
+                double acc = bias ? bias[c] : 0.0;
+                for (int k = 0; k < 4; ++k) {
+                    const int64_t s = t - 3 + k;
+                    double v;
+                    if (s >= 0)
+                        v = in[((size_t)b * L + s) * stride + c];
+                    else
+                        v = st_in ? st_in[((size_t)b * C + c) * 3 + (3 + s)] : 0.0;
+                    acc += w[(size_t)c * 4 + k] * v;
+                }
+                out[((size_t)b * L + t) * C + c] = silu(acc);
+            }
+            if (st_out)
+                for (int i = 0; i < 3; ++i) {
+                    const int64_t s = L - 3 + i;
+                    double v;
+                    if (s >= 0)
+                        v = in[((size_t)b * L + s) * stride + c];
+                    else
+                        v = st_in ? st_in[((size_t)b * C + c) * 3 + (3 + s)] : 0.0;
+                    st_out[((size_t)b * C + c) * 3 + i] = v;
+                }
+        }
+    }
+}
+
+/* Step size from the projection: dt = softplus(raw + bias[h]) (log1p(exp)). */
+void dart_oracle_dt_softplus(int64_t rows, int H, const double* raw, const double* bias,
+                             double* dt) {
+    for (int64_t r = 0; r < rows; ++r)
+        for (int h = 0; h < H; ++h) {
+            const double v = raw[(size_t)r * H + h] + (bias ? bias[h] : 0.0);
+            dt[(size_t)r * H + h] = v > 30.0 ? v + log1p(exp(-v)) : log1p(exp(v));
+        }
+}
+
+/* Gated RMSNorm ahead of the output projection: with u = y (.) SiLU(z),     */
+/* out = u / sqrt(mean_{group}(u^2) + eps) * w over consecutive groups of   */
+/* `group` channels of each row (D channels, D % group == 0).              */
+void dart_oracle_gated_rmsnorm(int64_t rows, int D, int group, double eps, const double* y,
+                               const double* z, const double* w, double* out) {
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        for (int g0 = 0; g0 < D; g0 += group) {
+            double ss = 0.0;
+            for (int k = g0; k < g0 + group; ++k) {
+                const double u = y[(size_t)r * D + k] * silu(z[(size_t)r * D + k]);
+                ss += u * u;
+            }
+            const double inv = 1.0 / sqrt(ss / group + eps);
+            for (int k = g0; k < g0 + group; ++k) {
+                const double u = y[(size_t)r * D + k] * silu(z[(size_t)r * D + k]);
+                out[(size_t)r * D + k] = u * inv * (w ? w[k] : 1.0);
+            }
+        }
+    }
 }

@@ -8,6 +8,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <cstdint>
 #include <cstring>
 
 #include "dart_internal.hpp"
@@ -200,6 +201,64 @@ dart_status dart_sma_bwd(const dart_dims* dims, const dart_sma_opts* opts, const
     return hip_status(dart::launch_sma_bwd(s, sma_args(opts), q, e, Cm, mem, z, lse, dy, dq, de, dC,
                                            dmem, dz, workspace, (hipStream_t)stream),
                       "dart_sma_bwd launch");
+}
+
+dart_status dart_conv1d_silu(int64_t batch, int64_t seqlen, int32_t channels, int64_t row_stride,
+                             int32_t dtype, const void* in, const float* weight, const float* bias,
+                             const float* state_in, float* state_out, void* out, void* stream) {
+    if (batch < 1 || seqlen < 1 || channels < 1)
+        return fail(DART_ERR_INVALID_ARG, "batch, seqlen and channels must be >= 1");
+    if (batch > 65535 || (seqlen + 31) / 32 > 65535)
+        return fail(DART_ERR_UNSUPPORTED, "batch <= 65535 and seqlen <= 32 * 65535");
+    if (row_stride < channels)
+        return fail(DART_ERR_INVALID_ARG, "row_stride (%lld) < channels (%d)", (long long)row_stride, channels);
+    if (dtype != DART_FP32 && dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", dtype);
+    REQUIRE_PTR(in);
+    REQUIRE_PTR(weight);
+    REQUIRE_PTR(out);
+    if (state_out && state_out == state_in && seqlen > 32)
+        return fail(DART_ERR_INVALID_ARG, "state_out may alias state_in only for seqlen <= 32");
+    return hip_status(dart::launch_conv1d_silu(dtype, batch, seqlen, channels, row_stride, in, weight,
+                                               bias, state_in, state_out, out, (hipStream_t)stream),
+                      "dart_conv1d_silu launch");
+}
+
+dart_status dart_dt_softplus(int64_t rows, int32_t nheads, int64_t row_stride, int32_t dtype,
+                             const void* raw, const float* bias, float* dt, void* stream) {
+    if (rows < 1 || nheads < 1) return fail(DART_ERR_INVALID_ARG, "rows and nheads must be >= 1");
+    if (row_stride < nheads)
+        return fail(DART_ERR_INVALID_ARG, "row_stride (%lld) < nheads (%d)", (long long)row_stride, nheads);
+    if (dtype != DART_FP32 && dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", dtype);
+    if ((rows * nheads + 255) / 256 > 2147483647LL) return fail(DART_ERR_UNSUPPORTED, "too many rows");
+    REQUIRE_PTR(raw);
+    REQUIRE_PTR(dt);
+    return hip_status(dart::launch_dt_softplus(dtype, rows, nheads, raw, row_stride, bias, dt,
+                                               (hipStream_t)stream),
+                      "dart_dt_softplus launch");
+}
+
+dart_status dart_gated_rmsnorm(int64_t rows, int32_t dim, int32_t group, int32_t dtype,
+                               const void* y, const void* z, int64_t z_row_stride,
+                               const float* weight, float eps, void* out, void* stream) {
+    if (rows < 1 || dim < 1 || group < 1) return fail(DART_ERR_INVALID_ARG, "rows, dim and group must be >= 1");
+    if (dim % group != 0 || group % 8 != 0)
+        return fail(DART_ERR_INVALID_ARG, "group must divide dim and be a multiple of 8 (dim %d, group %d)", dim, group);
+    if (z_row_stride < dim || z_row_stride % 8 != 0)
+        return fail(DART_ERR_INVALID_ARG, "z_row_stride must be >= dim and a multiple of 8");
+    if (dtype != DART_FP32 && dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", dtype);
+    if (!(eps > 0.0f)) return fail(DART_ERR_INVALID_ARG, "eps must be > 0");
+    REQUIRE_PTR(y);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(out);
+    if (((uintptr_t)y | (uintptr_t)z | (uintptr_t)out | (uintptr_t)weight) % 16 != 0)
+        return fail(DART_ERR_INVALID_ARG, "y, z, out and weight must be 16-byte aligned");
+    if ((rows * (dim / group) + 3) / 4 > 2147483647LL) return fail(DART_ERR_UNSUPPORTED, "too many rows");
+    return hip_status(dart::launch_gated_rmsnorm(dtype, rows, dim, group, y, z, z_row_stride, weight,
+                                                 eps, out, (hipStream_t)stream),
+                      "dart_gated_rmsnorm launch");
 }
 
 size_t dart_decode_workspace_bytes(const dart_dims* dims) {

@@ -54,6 +54,16 @@ hipError_t launch_sma_bwd(const Shape& s, const SmaArgs& a, const void* q, const
                           const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
                           void* ws, hipStream_t st);
 
+// The block around the path (block.hip).
+hipError_t launch_conv1d_silu(int dtype, int64_t B, int64_t L, int C, int64_t stride,
+                              const void* in, const float* w, const float* bias,
+                              const float* st_in, float* st_out, void* out, hipStream_t st);
+hipError_t launch_dt_softplus(int dtype, int64_t rows, int H, const void* raw, int64_t stride,
+                              const float* bias, float* dt, hipStream_t st);
+hipError_t launch_gated_rmsnorm(int dtype, int64_t rows, int D, int group, const void* y,
+                                const void* z, int64_t zstride, const float* w, float eps,
+                                void* out, hipStream_t st);
+
 // Decode: per-split partial softmax statistics [B][H][nsplit][P+2] and the
 // SSM readout y_ssd [B][H][P] (float).
 constexpr int kDecodeMinMemPerSplit = 8;  // smallest split size the workspace allows

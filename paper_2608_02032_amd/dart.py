@@ -45,6 +45,7 @@ class SmaOpts(ctypes.Structure):
 
 EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspace_bytes",
            "dart_sma_fwd", "dart_sma_bwd_workspace_bytes", "dart_sma_bwd",
+           "dart_conv1d_silu", "dart_dt_softplus", "dart_gated_rmsnorm",
            "dart_decode_workspace_bytes", "dart_decode_step",
            "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
            "dart_profile_enable", "dart_profile_flush", "dart_profile_count",
@@ -80,6 +81,14 @@ def load_library(path: str = LIB_PATH):
         lib.dart_sma_bwd_workspace_bytes.restype = sz
         lib.dart_sma_bwd.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
         lib.dart_sma_bwd.restype = st
+        lib.dart_conv1d_silu.argtypes = [i64, i64, ctypes.c_int32, i64, ctypes.c_int32, P, P, P, P,
+                                         P, P, P]
+        lib.dart_conv1d_silu.restype = st
+        lib.dart_dt_softplus.argtypes = [i64, ctypes.c_int32, i64, ctypes.c_int32, P, P, P, P]
+        lib.dart_dt_softplus.restype = st
+        lib.dart_gated_rmsnorm.argtypes = [i64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P, P,
+                                           i64, P, ctypes.c_float, P, P]
+        lib.dart_gated_rmsnorm.restype = st
         lib.dart_decode_workspace_bytes.argtypes = [D]
         lib.dart_decode_workspace_bytes.restype = sz
         lib.dart_decode_step.argtypes = [D, O, i64, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
@@ -133,6 +142,10 @@ def _torch():
     return torch
 
 
+def _dtype_num(t):
+    return {"fp32": DART_FP32, "bf16": DART_BF16}[_dtype_code(t)]
+
+
 def _dtype_code(t):
     torch = _torch()
     if t.dtype == torch.bfloat16:
@@ -149,6 +162,16 @@ def _ptr(t) -> Optional[int]:
         raise ValueError("tensor must live on the GPU")
     if not t.is_contiguous():
         raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _ptr_rows(t) -> int:
+    """Pointer of a view whose rows are contiguous (innermost stride 1) at a
+    common row stride, e.g. a channel slice of a projection output."""
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if t.stride(-1) != 1:
+        raise ValueError("tensor rows must be contiguous")
     return t.data_ptr()
 
 
@@ -271,6 +294,71 @@ def sma_bwd(q, e, Cm, mem, z, lse, dy, chunk, eps=DEFAULT_EPS, normalize=True, q
                            _ptr(mem), _ptr(z), _ptr(lse), _ptr(dy), _ptr(out["dq"]),
                            _ptr(out["de"]), _ptr(out["dC"]), _ptr(out["dmem"]), _ptr(out["dz"]),
                            _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
+
+
+def conv1d_silu(inp, weight, bias=None, state_in=None, state_out=None, channels=None, out=None,
+                stream=None):
+    """Causal width-4 depthwise convolution + bias + SiLU (dart_conv1d_silu).
+
+    inp [B][L][R] (channels = the first `channels` of each row, default R;
+    pass a view starting at the first x channel), weight [C][4] f32, bias [C]
+    f32, state_in/state_out [B][C][3] f32 (state_out=True allocates one).
+    Returns (out [B][L][C], state_out or None)."""
+    torch = _torch()
+    lib = load_library()
+    B_, L, R = inp.shape
+    C = R if channels is None else int(channels)
+    if inp.stride(2) != 1 or inp.stride(0) != L * inp.stride(1):
+        raise ValueError("inp rows must be contiguous with a common row stride")
+    for t, nm in ((weight, "weight"), (bias, "bias"), (state_in, "state_in")):
+        _check_f32(t, nm)
+    if state_out is True:
+        state_out = torch.empty((B_, C, 3), dtype=torch.float32, device=inp.device)
+    if out is None:
+        out = torch.empty((B_, L, C), dtype=inp.dtype, device=inp.device)
+    check(lib.dart_conv1d_silu(B_, L, C, inp.stride(1), _dtype_num(inp), _ptr_rows(inp), _ptr(weight),
+                               _ptr(bias), _ptr(state_in), _ptr(state_out), _ptr(out),
+                               _stream(stream)))
+    return out, state_out
+
+
+def dt_softplus(raw, bias=None, nheads=None, out=None, stream=None):
+    """dt = softplus(raw + bias) in float (dart_dt_softplus); raw [..][R] with
+    the heads the first `nheads` (default R) elements of each row."""
+    torch = _torch()
+    lib = load_library()
+    R = raw.shape[-1]
+    H = R if nheads is None else int(nheads)
+    rows = raw.numel() // R
+    if raw.stride(-1) != 1:
+        raise ValueError("raw rows must be contiguous")
+    _check_f32(bias, "bias")
+    if out is None:
+        out = torch.empty(tuple(raw.shape[:-1]) + (H,), dtype=torch.float32, device=raw.device)
+    stride = raw.stride(-2) if raw.dim() > 1 else R
+    check(lib.dart_dt_softplus(rows, H, stride, _dtype_num(raw), _ptr_rows(raw), _ptr(bias), _ptr(out),
+                               _stream(stream)))
+    return out
+
+
+def gated_rmsnorm(y, z, weight=None, group=None, eps=DEFAULT_EPS, out=None, stream=None):
+    """u = y * SiLU(z); u / sqrt(mean over each group of u^2 + eps) * weight
+    (dart_gated_rmsnorm).  y [..][D] contiguous; z [..][D] rows of a common
+    stride (e.g. the gate slice of the projection output)."""
+    torch = _torch()
+    lib = load_library()
+    D = y.shape[-1]
+    rows = y.numel() // D
+    group = D if group is None else int(group)
+    if not y.is_contiguous() or z.stride(-1) != 1:
+        raise ValueError("y must be contiguous and z rows contiguous")
+    _check_f32(weight, "weight")
+    if out is None:
+        out = torch.empty_like(y)
+    zs = z.stride(-2) if z.dim() > 1 else D
+    check(lib.dart_gated_rmsnorm(rows, D, group, _dtype_num(y), _ptr(y), _ptr_rows(z), zs,
+                                 _ptr(weight), float(eps), _ptr(out), _stream(stream)))
     return out
 
 

@@ -222,3 +222,24 @@ def test_sma_bwd_workspace_and_bad_arguments(lib):
     assert bwd(nbytes=ws - 1) == dart.DART_ERR_INVALID_ARG
     assert b"workspace too small" in lib.dart_last_error()
     assert bwd(opts=dart.SmaOpts(0.0, None, None, 1, 1)) == dart.DART_ERR_INVALID_ARG
+
+
+def test_block_entry_points_reject_bad_arguments(lib):
+    E = dart.DART_ERR_INVALID_ARG
+    # conv: sizes, stride, dtype, pointers, aliasing of the state over a long sequence
+    assert lib.dart_conv1d_silu(0, 8, 4, 4, 1, 1, 1, None, None, None, 1, None) == E
+    assert lib.dart_conv1d_silu(1, 8, 4, 3, 1, 1, 1, None, None, None, 1, None) == E
+    assert lib.dart_conv1d_silu(1, 8, 4, 4, 7, 1, 1, None, None, None, 1, None) == E
+    assert lib.dart_conv1d_silu(1, 8, 4, 4, 1, None, 1, None, None, None, 1, None) == E
+    assert lib.dart_conv1d_silu(1, 33, 4, 4, 1, 1, 1, None, 8, 8, 1, None) == E
+    assert b"alias" in lib.dart_last_error()
+    # dt
+    assert lib.dart_dt_softplus(4, 3, 2, 1, 1, None, 1, None) == E
+    assert lib.dart_dt_softplus(4, 3, 3, 1, None, None, 1, None) == E
+    # gated norm: group must divide dim and be a multiple of 8; z stride; alignment; eps
+    assert lib.dart_gated_rmsnorm(2, 64, 24, 1, 16, 16, 64, None, 1e-6, 16, None) == E
+    assert lib.dart_gated_rmsnorm(2, 64, 12, 1, 16, 16, 64, None, 1e-6, 16, None) == E
+    assert lib.dart_gated_rmsnorm(2, 64, 64, 1, 16, 16, 60, None, 1e-6, 16, None) == E
+    assert lib.dart_gated_rmsnorm(2, 64, 64, 1, 8, 16, 64, None, 1e-6, 16, None) == E
+    assert b"aligned" in lib.dart_last_error()
+    assert lib.dart_gated_rmsnorm(2, 64, 64, 1, 16, 16, 64, None, 0.0, 16, None) == E

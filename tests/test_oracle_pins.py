@@ -630,3 +630,50 @@ def test_scan_backward_decay_gradient_is_a_reverse_cumsum():
             lhs = (g["ddt"][0, t, h] - dxx[t] / dt[0, t, h]) / A[h]
             rhs = term[t:].sum() + (dhl[0, h] * hl[0, h]).sum() + memdot[t // S:].sum()
             assert abs(lhs - rhs) <= 1e-9 * (1 + abs(rhs)), (h, t, lhs, rhs)
+
+
+def test_block_conv_reduces_to_library_convolution_and_chains():
+    """The causal width-4 convolution: with no carried state it is numpy's
+    full convolution of each channel with its weights (kernel reversed: w[3]
+    multiplies the current token), truncated to the first L outputs, then
+    SiLU; and splitting the sequence, carrying the state, reproduces one
+    pass (the decode cache of the convolution)."""
+    rng = np.random.default_rng(51)
+    B_, L, R, C = 2, 23, 7, 5
+    x = rng.standard_normal((B_, L, R))
+    w = rng.standard_normal((C, 4))
+    bias = rng.standard_normal(C)
+    out, st = oracle.conv1d_silu(x, w, bias, channels=C)
+    for b in range(B_):
+        for c in range(C):
+            a = np.convolve(x[b, :, c], w[c][::-1])[:L] + bias[c]
+            np.testing.assert_allclose(out[b, :, c], a / (1 + np.exp(-a)), rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(st, np.transpose(x[:, L - 3:, :C], (0, 2, 1)))
+    for cut in (1, 2, 3, 10):
+        o1, s1 = oracle.conv1d_silu(x[:, :cut], w, bias, channels=C)
+        o2, s2 = oracle.conv1d_silu(x[:, cut:], w, bias, state=s1, channels=C)
+        np.testing.assert_allclose(np.concatenate([o1, o2], axis=1), out, rtol=1e-12, atol=1e-12)
+        np.testing.assert_array_equal(s2, st)
+
+
+def test_block_dt_softplus_and_gated_rmsnorm_closed_forms():
+    """softplus against numpy's logaddexp(0, v), ln 2 at 0; gated RMSNorm:
+    every group of the output has unit RMS (eps -> 0, unit weights), is
+    unchanged by scaling y, and with z large positive (SiLU(z) ~ z) equals
+    the RMSNorm of y * z."""
+    rng = np.random.default_rng(52)
+    raw = rng.standard_normal((6, 4)) * 10
+    bias = rng.standard_normal(4)
+    np.testing.assert_allclose(oracle.dt_softplus(raw, bias), np.logaddexp(0.0, raw + bias),
+                               rtol=1e-13, atol=1e-300)
+    assert oracle.dt_softplus(np.zeros((1, 1)))[0, 0] == pytest.approx(math.log(2.0), rel=1e-15)
+    y = rng.standard_normal((5, 32))
+    z = rng.standard_normal((5, 32))
+    o = oracle.gated_rmsnorm(y, z, group=8, eps=1e-30)
+    rms = np.sqrt((o.reshape(5, 4, 8) ** 2).mean(-1))
+    np.testing.assert_allclose(rms, 1.0, rtol=1e-12)
+    np.testing.assert_allclose(oracle.gated_rmsnorm(3.5 * y, z, group=8, eps=1e-30), o, rtol=1e-12)
+    zl = np.full_like(y, 40.0)
+    u = y * 40.0
+    ref = u / np.sqrt((u.reshape(5, 4, 8) ** 2).mean(-1, keepdims=True)).repeat(8, -1).reshape(5, 32)
+    np.testing.assert_allclose(oracle.gated_rmsnorm(y, zl, group=8, eps=1e-30), ref, rtol=1e-12)
