@@ -27,7 +27,7 @@
  *    NULL = the null stream) and runs asynchronously.
  *  - Errors: every argument check runs on the host before any launch.  A
  *    failing check returns DART_ERR_INVALID_ARG (malformed arguments) or
- *    DART_ERR_UNSUPPORTED (well-formed shapes this build has no kernel for)
+ *    DART_ERR_UNSUPPORTED (well-formed shapes the library has no kernel for)
  *    and enqueues nothing; a failed launch returns DART_ERR_HIP.
  *    dart_last_error() gives a message for the last non-OK status of the
  *    calling thread.  Numeric contracts (dt > 0, A < 0) are the caller's.

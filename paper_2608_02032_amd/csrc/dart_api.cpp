@@ -46,7 +46,7 @@ dart_status make_shape(const dart_dims* d, bool need_seqlen, dart::Shape& s) {
         return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", d->dtype);
     if (d->mem_capacity < 0) return fail(DART_ERR_INVALID_ARG, "mem_capacity must be >= 0");
     if (d->headdim != 64)
-        return fail(DART_ERR_UNSUPPORTED, "headdim %d not supported (this build has kernels for 64)", d->headdim);
+        return fail(DART_ERR_UNSUPPORTED, "headdim %d not supported (the library has kernels for 64)", d->headdim);
     if (d->dstate != 32 && d->dstate != 64 && d->dstate != 128)
         return fail(DART_ERR_UNSUPPORTED, "dstate %d not supported (32, 64 or 128)", d->dstate);
     if (d->chunk != 64 && d->chunk != 128 && d->chunk != 256)

@@ -26,8 +26,9 @@
 //   k_bwd_prep          Qbar (scaled by log2(e)/sqrt(N), storage dtype, the
 //                       forward's operand exactly) and Ebar (float) per token
 //   k_bwd_tokens        one workgroup per (64 tokens of one chunk, block of
-//                       heads of one group), 8 waves, each pair splitting the
-//                       state index; one pass over (head, memory),
+//                       heads of one group), 8 waves, a pair per 16 tokens
+//                       splitting the rows of each product; one pass over
+//                       (head, memory),
 //                       tiles streamed through an LDS ring by DMA:
 //                         W' = Kh^T Qbar' -> logits -> p;
 //                         X = dH dy^T = diag(1/r) Kh dy^T -> dwy, dC += g p X;
@@ -53,7 +54,8 @@ namespace dart {
 namespace {
 
 constexpr int kP = 64;
-constexpr int kTokWaves = 4;
+constexpr int kTokWaves = 4;               // 16-token groups (and copying waves) per
+                                           // k_bwd_tokens workgroup; two waves a group
 constexpr int kTokBlock = 16 * kTokWaves;  // tokens per k_bwd_tokens workgroup
 constexpr int kMemJ = 4;                   // memories per k_bwd_mem workgroup
 constexpr int kHeadsPerBlock = 8;
@@ -64,8 +66,8 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-// An empty use of every register of a fragment: the compiler waits for its
-// loads here (16-byte pieces, so the asm operands stay 128-bit wide).
+// An empty use of every register of a fragment, so the compiler waits for its
+// loads at this point (operands of at most 128 bits each).
 __device__ __forceinline__ void keep(const bf16x8& f) { asm volatile("" ::"v"(f)); }
 __device__ __forceinline__ void keep(const f32x8& f) {
     const f32x4 a{f[0], f[1], f[2], f[3]}, b{f[4], f[5], f[6], f[7]};

@@ -49,7 +49,7 @@ class Workload:
         return replace(self, **kw)
 
 
-# The workloads measured or checked by this build, named by what they are.
+# The workloads measured or checked, named by what they are.
 WORKLOADS: Dict[str, Workload] = {
     "tiny_fp32_L512": Workload("tiny_fp32_L512", 1, 512, 2, 64, 32, 64, "fp32"),
     "mamba2_130m_L4096": Workload("mamba2_130m_L4096", 8, 4096, 24, 64, 128, 256, "bf16"),
