@@ -40,7 +40,7 @@ def source_hash() -> str:
 def kernel_short(name: str):
     if "dart" not in name:
         return None
-    m = re.search(r"(k_[a-z_]+)", name)
+    m = re.search(r"(k_[a-z0-9_]+)", name)
     return m.group(1) if m else None
 
 
