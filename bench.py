@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--no-ragged", action="store_true",
                     help="skip the separately timed ragged-batch decode steps")
     ap.add_argument("--no-bwd", action="store_true",
-                    help="skip the separately timed SMA backward on the same workload")
+                    help="skip the separately timed backward (SMA and scan) on the same workload")
     ap.add_argument("--no-block", action="store_true",
                     help="skip the separately timed block kernels (conv, dt, gated norm)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -97,6 +97,16 @@ def sma_bytes(w, esize=2):
             + zsz * esize                       # read z
             + B * L * H * P * esize * 2         # read y_ssd, write y
             + B * L * H * 4)                    # write lse
+
+
+def ssd_bwd_bytes(w):
+    """Bytes the scan backward must move at the least: x, dy (storage dtype),
+    dt, B, C and the memory gradient (float) in; dx, ddt, dB, dC (float) and
+    dA out."""
+    B, L, H, P, N, G, M = w.batch, w.seqlen, w.nheads, w.headdim, w.dstate, w.ngroups, w.nchunks
+    es = 2 if w.dtype == "bf16" else 4
+    return (2 * B * L * H * P * es + 4 * B * L * H + 2 * B * L * G * N * es + 4 * B * M * H * N * P
+            + 4 * B * L * H * P + 4 * B * L * H + 2 * 4 * B * L * G * N + 4 * H)
 
 
 def sma_bwd_flops(w):
@@ -423,7 +433,41 @@ def main():
             "tokens_per_s": round(B * L / (bwd_ms * 1e-3), 1),
             "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(bavg.items())},
             "traffic_bytes": {k: traffic_for(k) for k in ("k_bwd_tokens", "k_bwd_mem")}}
-        del ws_bwd, grads
+        del ws_bwd
+
+        # scan backward on the same workload, chained as a layer's backward
+        # runs: the y_ssd gradient is dy itself (the residual) and the memory
+        # gradient is what the SMA backward just produced
+        ws_sb = torch.empty(dart.workspace_bytes("ssd_bwd", dims), dtype=torch.uint8, device=dev)
+        sgrads = {"dx": torch.empty((B, L, H, P), **f32), "ddt": torch.empty((B, L, H), **f32),
+                  "dA": torch.empty((H,), **f32), "dB": torch.empty(T["Bm"].shape, **f32),
+                  "dC": torch.empty(T["Cm"].shape, **f32),
+                  "dh0": torch.empty((B, H, w.dstate, P), **f32)}
+
+        def scan_backward():
+            dart.ssd_bwd(T["x"], T["dt"], T["A"], T["Bm"], T["Cm"], S, dy, dmem=grads["dmem"],
+                         out=sgrads, workspace=ws_sb, stream=stream)
+        for _ in range(3):
+            scan_backward()
+        torch.cuda.synchronize()
+        dart.profile_reset()
+        dart.profile_enable(True)
+        eb[0].record(stream)
+        for _ in range(R):
+            scan_backward()
+        eb[1].record(stream)
+        torch.cuda.synchronize()
+        dart.profile_enable(False)
+        sk = dart.profile_read(reset=True)
+        savg = {k: v[0] / max(v[1], 1) for k, v in sk.items()}
+        sb_ms = eb[0].elapsed_time(eb[1]) / R
+        sbb = ssd_bwd_bytes(w)
+        extra["ssd_bwd"] = {
+            "us": round(sb_ms * 1e3, 2), "tokens_per_s": round(B * L / (sb_ms * 1e-3), 1),
+            "algorithmic_bytes": sbb, "hbm_gbps": round(sbb / (sb_ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(sbb / (sb_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+            "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(savg.items())}}
+        del ws_sb, sgrads, grads
 
     if not args.no_block:
         # the block around the path at the same shape, timed on its own: the

@@ -112,6 +112,42 @@ dart_status dart_ssd_chunk_scan(const dart_dims* dims, const void* x, const floa
                                 void* y_ssd, void* mem, float* h_last, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
+/* Bytes of workspace dart_ssd_bwd needs for `dims`: a forward scan's own
+ * workspace and outputs, plus chunk adjoints, per-token decay pieces and
+ * per-head-block dB / dC partials (all float). */
+size_t dart_ssd_bwd_workspace_bytes(const dart_dims* dims);
+
+/*
+ * Backward of dart_ssd_chunk_scan (Sec. 2 recurrence, Sec. 3 / App. A chunk
+ * memories): the gradients of
+ *     sum dy . y_ssd + sum_c <dmem_c, dH_[c]> + <dh_last, H_{L-1}>
+ * with respect to x, dt, A, Bm, Cm and h0, for the same inputs the forward
+ * took.  The forward is recomputed inside (its chunk-entry states seed the
+ * token sweeps), so nothing of a previous forward call is needed.  The
+ * decay gradient is formed by the exact reverse-cumulative-sum identity
+ *     d loss / d log a_t = sum_{s >= t} (y_s . dy_s - dx_s . x_s)
+ *                          + <dh_last, H_{L-1}> + sum_{c' >= c(t)} <dmem_c', dH_[c']>,
+ * then ddt_t = dx_t . x_t / dt_t + A_h (that), dA_h = sum_{b,t} dt_t (that).
+ *
+ *   x, dt, A, Bm, Cm, h0    as dart_ssd_chunk_scan (h0 may be NULL: zero)
+ *   dy      [B][L][H][P]    storage dtype, in
+ *   dmem    [B][Mcap][H][N][P] float, in, or NULL (slots 0..M-1 read)
+ *   dh_last [B][H][N][P]    float, in, or NULL
+ *   dx      [B][L][H][P]    float, out
+ *   ddt     [B][L][H]       float, out
+ *   dA      [H]             float, out (summed over the batch)
+ *   dB, dC  [B][L][G][N]    float, out (summed over each group's heads)
+ *   dh0     [B][H][N][P]    float, out, or NULL
+ *   workspace               device buffer of >= dart_ssd_bwd_workspace_bytes()
+ * Every output element is written (no accumulation into the caller's
+ * buffers).  Deterministic: no atomics.
+ */
+dart_status dart_ssd_bwd(const dart_dims* dims, const void* x, const float* dt, const float* A,
+                         const void* Bm, const void* Cm, const float* h0, const void* dy,
+                         const float* dmem, const float* dh_last, float* dx, float* ddt, float* dA,
+                         float* dB, float* dC, float* dh0, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
 /* Bytes of workspace dart_sma_fwd needs for `dims`: the key side
  * r_j (.) dH_j of memories 0..M-2 in the cache layout (storage dtype); 0 when
  * M = 1 (workspace may then be NULL). */

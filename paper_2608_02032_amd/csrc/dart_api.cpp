@@ -126,6 +126,40 @@ dart_status dart_ssd_chunk_scan(const dart_dims* dims, const void* x, const floa
                       "dart_ssd_chunk_scan launch");
 }
 
+size_t dart_ssd_bwd_workspace_bytes(const dart_dims* dims) {
+    dart::Shape s;
+    if (make_shape(dims, true, s) != DART_OK) return 0;
+    return dart::ssd_bwd_workspace_bytes(s);
+}
+
+dart_status dart_ssd_bwd(const dart_dims* dims, const void* x, const float* dt, const float* A,
+                         const void* Bm, const void* Cm, const float* h0, const void* dy,
+                         const float* dmem, const float* dh_last, float* dx, float* ddt, float* dA,
+                         float* dB, float* dC, float* dh0, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, true, s);
+    if (st != DART_OK) return st;
+    REQUIRE_PTR(x);
+    REQUIRE_PTR(dt);
+    REQUIRE_PTR(A);
+    REQUIRE_PTR(Bm);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(dy);
+    REQUIRE_PTR(dx);
+    REQUIRE_PTR(ddt);
+    REQUIRE_PTR(dA);
+    REQUIRE_PTR(dB);
+    REQUIRE_PTR(dC);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::ssd_bwd_workspace_bytes(s);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return hip_status(dart::launch_ssd_bwd(s, x, dt, A, Bm, Cm, h0, dy, dmem, dh_last, dx, ddt, dA,
+                                           dB, dC, dh0, workspace, (hipStream_t)stream),
+                      "dart_ssd_bwd launch");
+}
+
 size_t dart_sma_workspace_bytes(const dart_dims* dims) {
     dart::Shape s;
     if (make_shape(dims, true, s) != DART_OK) return 0;

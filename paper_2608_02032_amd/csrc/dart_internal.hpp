@@ -25,6 +25,17 @@ hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const flo
                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
                        float* h_last, void* ws, hipStream_t st);
 
+// The chunk-entry states H_[c-1] a scan left in its workspace,
+// [B][M][H][N][P] in the storage dtype (H_[-1] = h0 or 0).
+const void* scan_entry_states(const Shape& s, const void* ws);
+
+// Backward of the scan and its memories (scan_bwd.hip).
+size_t ssd_bwd_workspace_bytes(const Shape& s);
+hipError_t launch_ssd_bwd(const Shape& s, const void* x, const float* dt, const float* A,
+                          const void* Bm, const void* Cm, const float* h0, const void* dy,
+                          const float* dmem, const float* dh_last, float* dx, float* ddt, float* dA,
+                          float* dB, float* dC, float* dh0, void* ws, hipStream_t st);
+
 struct SmaArgs {
     float eps;
     const float* qw;

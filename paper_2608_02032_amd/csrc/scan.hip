@@ -1138,6 +1138,10 @@ hipError_t run_scan_n(const Shape& s, const void* x, const float* dt, const floa
 
 size_t scan_workspace_bytes(const Shape& s) { return scan_ws(s, nullptr).total; }
 
+const void* scan_entry_states(const Shape& s, const void* ws) {
+    return scan_ws(s, const_cast<void*>(ws)).states;
+}
+
 hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const float* A,
                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
                        float* h_last, void* ws, hipStream_t st) {

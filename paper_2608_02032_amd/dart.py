@@ -45,6 +45,7 @@ class SmaOpts(ctypes.Structure):
 
 EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspace_bytes",
            "dart_sma_fwd", "dart_sma_bwd_workspace_bytes", "dart_sma_bwd",
+           "dart_ssd_bwd_workspace_bytes", "dart_ssd_bwd",
            "dart_conv1d_silu", "dart_dt_softplus", "dart_gated_rmsnorm",
            "dart_decode_workspace_bytes", "dart_decode_step",
            "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
@@ -81,6 +82,10 @@ def load_library(path: str = LIB_PATH):
         lib.dart_sma_bwd_workspace_bytes.restype = sz
         lib.dart_sma_bwd.argtypes = [D, O, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
         lib.dart_sma_bwd.restype = st
+        lib.dart_ssd_bwd_workspace_bytes.argtypes = [D]
+        lib.dart_ssd_bwd_workspace_bytes.restype = sz
+        lib.dart_ssd_bwd.argtypes = [D] + [P] * 16 + [sz, P]
+        lib.dart_ssd_bwd.restype = st
         lib.dart_conv1d_silu.argtypes = [i64, i64, ctypes.c_int32, i64, ctypes.c_int32, P, P, P, P,
                                          P, P, P]
         lib.dart_conv1d_silu.restype = st
@@ -297,6 +302,46 @@ def sma_bwd(q, e, Cm, mem, z, lse, dy, chunk, eps=DEFAULT_EPS, normalize=True, q
     return out
 
 
+def ssd_bwd(x, dt, A, Bm, Cm, chunk, dy, dmem=None, dh_last=None, h0=None, out=None,
+            workspace=None, stream=None):
+    """Backward of ssd_chunk_scan (dart_ssd_bwd) for the loss
+    sum(dy * y_ssd) + sum(dmem * mem) + sum(dh_last * h_last).
+
+    dy like x (storage dtype); dmem [B][Mcap][H][N][P] f32 or None; dh_last
+    and h0 [B][H][N][P] f32 or None.  Returns a dict of float32 tensors dx,
+    ddt, dA, dB, dC (summed over each group's heads) and dh0.  `out` may hold
+    preallocated tensors under those keys.
+    """
+    torch = _torch()
+    lib = load_library()
+    B_, L, H, P = x.shape
+    G, N = Bm.shape[2], Bm.shape[3]
+    dtype = _dtype_code(x)
+    for t, nm in ((dt, "dt"), (A, "A"), (dmem, "dmem"), (dh_last, "dh_last"), (h0, "h0")):
+        _check_f32(t, nm)
+    mcap = dmem.shape[1] if dmem is not None else 0
+    dims = make_dims(B_, L, H, P, N, chunk, dtype, G, mcap)
+    f32 = dict(dtype=torch.float32, device=x.device)
+    want = {"dx": x.shape, "ddt": dt.shape, "dA": A.shape, "dB": Bm.shape, "dC": Cm.shape,
+            "dh0": (B_, H, N, P)}
+    out = dict(out or {})
+    for k, shape in want.items():
+        if k not in out:
+            out[k] = torch.empty(shape, **f32)
+        elif tuple(out[k].shape) != tuple(shape) or out[k].dtype != torch.float32 \
+                or not out[k].is_contiguous():
+            raise ValueError("out[%r] must be a contiguous float32 tensor of shape %s"
+                             % (k, tuple(shape)))
+    need = lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(dims))
+    if workspace is None:
+        workspace = _workspace(need, x.device)
+    check(lib.dart_ssd_bwd(ctypes.byref(dims), _ptr(x), _ptr(dt), _ptr(A), _ptr(Bm), _ptr(Cm),
+                           _ptr(h0), _ptr(dy), _ptr(dmem), _ptr(dh_last), _ptr(out["dx"]),
+                           _ptr(out["ddt"]), _ptr(out["dA"]), _ptr(out["dB"]), _ptr(out["dC"]),
+                           _ptr(out["dh0"]), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
+
+
 def conv1d_silu(inp, weight, bias=None, state_in=None, state_out=None, channels=None, out=None,
                 stream=None):
     """Causal width-4 depthwise convolution + bias + SiLU (dart_conv1d_silu).
@@ -444,6 +489,7 @@ def workspace_bytes(kind: str, dims: Dims) -> int:
     lib = load_library()
     fn = {"scan": lib.dart_scan_workspace_bytes, "sma": lib.dart_sma_workspace_bytes,
           "sma_bwd": lib.dart_sma_bwd_workspace_bytes,
+          "ssd_bwd": lib.dart_ssd_bwd_workspace_bytes,
           "decode": lib.dart_decode_workspace_bytes}[kind]
     return int(fn(ctypes.byref(dims)))
 

@@ -224,6 +224,27 @@ def test_sma_bwd_workspace_and_bad_arguments(lib):
     assert bwd(opts=dart.SmaOpts(0.0, None, None, 1, 1)) == dart.DART_ERR_INVALID_ARG
 
 
+def test_ssd_bwd_workspace_and_bad_arguments(lib):
+    d = dims()
+    ws = lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(d))
+    # at least the forward scan's workspace plus R and dR (float, per chunk)
+    assert ws >= lib.dart_scan_workspace_bytes(ctypes.byref(d)) + 2 * 4 * (d.batch * (512 // 64)
+                                                                          * d.nheads * 64 * 64)
+    assert lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(dims(headdim=48))) == 0
+    required = (0, 1, 2, 3, 4, 6, 9, 10, 11, 12, 13, 15)  # h0, dmem, dh_last, dh0 optional
+
+    def bwd(ptr_over=None, nbytes=1 << 40):
+        p = [1] * 16
+        if ptr_over is not None:
+            p[ptr_over] = None
+        return lib.dart_ssd_bwd(ctypes.byref(d), *p, nbytes, None)
+    for k in required:
+        assert bwd(k) == dart.DART_ERR_INVALID_ARG
+        assert b"required pointer" in lib.dart_last_error()
+    assert bwd(nbytes=ws - 1) == dart.DART_ERR_INVALID_ARG
+    assert b"workspace too small" in lib.dart_last_error()
+
+
 def test_block_entry_points_reject_bad_arguments(lib):
     E = dart.DART_ERR_INVALID_ARG
     # conv: sizes, stride, dtype, pointers, aliasing of the state over a long sequence
