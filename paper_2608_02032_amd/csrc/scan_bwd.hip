@@ -208,11 +208,20 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
             const float a = __expf(d * Ah);
             const float xd = d * to_f(x[th * kP + p]);
             const float dyv = to_f(dy[th * kP + p]);
+            // the wave's R entries of B_t as 16-byte vector loads (n0 is a multiple of 8)
+            float bv[R];
             const T* brow = Bm + ((b * L + t) * G + g) * N + n0;
+#pragma unroll
+            for (int i = 0; i < R; i += 8) {
+                float t8[8];
+                load8(brow + i, t8);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) bv[i + k] = t8[k];
+            }
             float v[R];
 #pragma unroll
             for (int i = 0; i < R; ++i) {
-                const float u = to_f(brow[i]) * xd;
+                const float u = bv[i] * xd;
                 st[i] = a * st[i] + u;
                 dh[i] = a * dh[i] + u;
                 v[i] = st[i] * dyv;
@@ -258,11 +267,23 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
             const float xv = to_f(x[th * kP + p]);
             const T* crow = Cm + ((b * L + t) * G + g) * N + n0;
             const T* brow = Bm + ((b * L + t) * G + g) * N + n0;
+            float bv[R], cv[R];
+#pragma unroll
+            for (int i = 0; i < R; i += 8) {
+                float t8[8], u8[8];
+                load8(brow + i, t8);
+                load8(crow + i, u8);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    bv[i + k] = t8[k];
+                    cv[i + k] = u8[k];
+                }
+            }
             float px = 0.f, v[R];
 #pragma unroll
             for (int i = 0; i < R; ++i) {
-                lam[i] += to_f(crow[i]) * dyv;
-                px += to_f(brow[i]) * lam[i];
+                lam[i] += cv[i] * dyv;
+                px += bv[i] * lam[i];
                 v[i] = lam[i] * xv;
             }
             const float sb = lane_sums<R>(v, lane);
