@@ -28,9 +28,10 @@
 //   k_sbwd_tokens  per (b, c, block of heads of one group): for each head a
 //                  forward sweep over the chunk's tokens (H_t from the entry
 //                  state, dC) and a reverse one (Lam_t, dx, dB).  Each of the
-//                  4 waves holds N/4 rows of the N x P state, lane = p, so the
-//                  sums over p are in-wave butterflies and the sum over n of
-//                  dx meets in LDS once per 16 tokens.  The same sweeps give
+//                  4 waves holds N/4 rows of the N x P state, each lane N/16
+//                  rows by 4 columns, so the sums over p are short in-lane
+//                  sums plus a reduce-scatter over 16 lanes, and the sum over
+//                  n of dx meets in LDS once per 16 tokens.  The same sweeps give
 //                  the pieces of the decay gradient (y.dy, (B Lam).x and the
 //                  memory terms) on one consistent trajectory;
 //   k_sbwd_decay   per (b, h): the reverse cumulative sum -> ddt, dA partials;
@@ -149,16 +150,58 @@ __device__ __forceinline__ void rs_step(float (&cur)[R], int lane) {
     }
 }
 
-template <int R>
+// Sum of each of the R values of every lane over the groups of LANES lanes that
+// differ in their low log2(LANES) bits; afterwards lane l holds the group sum of
+// value (l % LANES) / (LANES / R).
+template <int R, int LANES>
 __device__ __forceinline__ float lane_sums(float (&v)[R], int lane) {
-    rs_step<R, R, 32>(v, lane);
+    rs_step<R, R, LANES / 2>(v, lane);
     float s = v[0];
 #pragma unroll
-    for (int m = (64 / R) / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+    for (int m = (LANES / R) / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
     return s;
 }
 
+template <int K>
+__device__ __forceinline__ void load_k(const bf16* p, float (&v)[K]) {
+    if constexpr (K % 8 == 0) {
+#pragma unroll
+        for (int i = 0; i < K; i += 8) {
+            float t[8];
+            load8(p + i, t);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[i + k] = t[k];
+        }
+    } else if constexpr (K == 4) {
+        load4(p, v);
+    } else {
+#pragma unroll
+        for (int i = 0; i < K; ++i) v[i] = (float)p[i];
+    }
+}
+template <int K>
+__device__ __forceinline__ void load_k(const float* p, float (&v)[K]) {
+    if constexpr (K % 4 == 0) {
+#pragma unroll
+        for (int i = 0; i < K; i += 4) {
+            float t[4];
+            load4(p + i, t);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[i + k] = t[k];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < K; ++i) v[i] = p[i];
+    }
+}
+
 // ---- per (b, c, head block): the two sweeps ----------------------------------------
+// Wave w holds state rows n0 = w N/4 .. n0 + N/4 - 1; inside the wave lane
+// (ng, pg) = (lane / 16, lane % 16) holds the RL = N/16 rows n0 + ng RL + i and
+// the 4 columns 4 pg + c.  Sums over p (dC, dB) are then 4-term in-lane sums
+// followed by a reduce-scatter over the 16 pg lanes; the sum over n of dx is an
+// in-lane sum over RL rows, a reduce-scatter over the 4 ng lanes and an LDS
+// exchange between the waves once per 16 tokens.
 // Besides dx, dB and dC this records, per wave, the pieces of the decay
 // gradient that the same recomputed trajectory gives: y_t . dy_t
 // (= C_t . dC_t), (B_t Lam_t) . x_t, and <dmem_c, dH_[c]> (+ <dh_last, H_{L-1}>
@@ -171,23 +214,24 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
     const float* __restrict__ dhl, float* __restrict__ dx, float* __restrict__ bxl,
     float* __restrict__ ydyp, float* __restrict__ mdp, float* __restrict__ dBp,
     float* __restrict__ dCp, int64_t L, int H, int G, int S, int64_t M, int64_t Mcap, int hpb) {
-    constexpr int R = N / 4;     // rows of the state per wave
-    constexpr int TB = 16;       // tokens per dx reduction
-    constexpr int GRP = 64 / R;  // lanes that share one row sum
+    constexpr int RL = N / 16;       // rows per lane
+    constexpr int GRP = 16 / RL;     // pg lanes that share one row sum
+    constexpr int TB = 16;           // tokens per dx exchange
     __shared__ float xpart[2][TB][4][kP];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int ng = lane >> 4, pg = lane & 15;
     const int64_t c = blockIdx.x;
     const int hb = blockIdx.y;
     const int64_t b = blockIdx.z;
     const int nhb = H / hpb;
     const int h0 = hb * hpb;
     const int g = h0 / (H / G);
-    const int n0 = wave * R;
-    const int p = lane;
+    const int nl = wave * (N / 4) + ng * RL;  // first row of this lane
+    const int pl = pg * 4;                    // first column of this lane
     const int64_t a0 = c * S;
     const int64_t e = (c + 1) * S < L ? (c + 1) * S - 1 : L - 1;
-    const int krow = lane / GRP;  // the row whose sum this lane holds
-    const bool writer = lane % GRP == 0;
+    const int nsum = wave * (N / 4) + ng * RL + pg / GRP;  // row of this lane's sum
+    const bool writer = pg % GRP == 0;
 
     for (int hh = 0; hh < hpb; ++hh) {
         const int h = h0 + hh;
@@ -196,117 +240,133 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
         const int64_t sm = ((b * Mcap + c) * H + h) * (int64_t)N * kP;
         // forward sweep: H_t from the entry state; dC_t = H_t dy_t; the
         // chunk's own contribution dH accumulates beside it
-        float st[R], dh[R];
+        float st[RL][4], dh[RL][4];
 #pragma unroll
-        for (int i = 0; i < R; ++i) {
-            st[i] = to_f(states[ch * (int64_t)N * kP + (n0 + i) * kP + p]);
-            dh[i] = 0.f;
+        for (int i = 0; i < RL; ++i) {
+            float t4[4];
+            load4(states + ch * (int64_t)N * kP + (nl + i) * kP + pl, t4);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                st[i][k] = t4[k];
+                dh[i][k] = 0.f;
+            }
         }
         for (int64_t t = a0; t <= e; ++t) {
             const int64_t th = (b * L + t) * H + h;
             const float d = dt[th];
             const float a = __expf(d * Ah);
-            const float xd = d * to_f(x[th * kP + p]);
-            const float dyv = to_f(dy[th * kP + p]);
-            // the wave's R entries of B_t as 16-byte vector loads (n0 is a multiple of 8)
-            float bv[R];
-            const T* brow = Bm + ((b * L + t) * G + g) * N + n0;
+            float xv[4], dyv[4], bv[RL];
+            load4(x + th * kP + pl, xv);
+            load4(dy + th * kP + pl, dyv);
+            load_k<RL>(Bm + ((b * L + t) * G + g) * N + nl, bv);
 #pragma unroll
-            for (int i = 0; i < R; i += 8) {
-                float t8[8];
-                load8(brow + i, t8);
+            for (int k = 0; k < 4; ++k) xv[k] *= d;
+            float v[RL];
 #pragma unroll
-                for (int k = 0; k < 8; ++k) bv[i + k] = t8[k];
+            for (int i = 0; i < RL; ++i) {
+                float acc = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float u = bv[i] * xv[k];
+                    st[i][k] = a * st[i][k] + u;
+                    dh[i][k] = a * dh[i][k] + u;
+                    acc += st[i][k] * dyv[k];
+                }
+                v[i] = acc;
             }
-            float v[R];
-#pragma unroll
-            for (int i = 0; i < R; ++i) {
-                const float u = bv[i] * xd;
-                st[i] = a * st[i] + u;
-                dh[i] = a * dh[i] + u;
-                v[i] = st[i] * dyv;
-            }
-            const float sc = lane_sums<R>(v, lane);
+            const float sc = lane_sums<RL, 16>(v, lane);
             if (writer) {
-                float* o = dCp + ((b * L + t) * nhb + hb) * (int64_t)N + n0 + krow;
+                float* o = dCp + ((b * L + t) * nhb + hb) * (int64_t)N + nsum;
                 *o = hh == 0 ? sc : *o + sc;
             }
-            // y_t . dy_t over this wave's rows: C_n dC_n summed over the row groups
-            float yd = to_f(Cm[((b * L + t) * G + g) * N + n0 + krow]) * sc;
+            // y_t . dy_t over this wave's rows: C_n dC_n summed over the rows
+            float yd = writer ? to_f(Cm[((b * L + t) * G + g) * N + nsum]) * sc : 0.f;
 #pragma unroll
-            for (int m = GRP; m < 64; m <<= 1) yd += __shfl_xor(yd, m, 64);
+            for (int m = 32; m >= 1; m >>= 1) yd += __shfl_xor(yd, m, 64);
             if (lane == 0) ydyp[th * 4 + wave] = yd;
         }
         float md = 0.f;
         if (dmem) {
 #pragma unroll
-            for (int i = 0; i < R; ++i) md += dmem[sm + (n0 + i) * kP + p] * dh[i];
+            for (int i = 0; i < RL; ++i) {
+                float t4[4];
+                load4(dmem + sm + (nl + i) * kP + pl, t4);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) md += t4[k] * dh[i][k];
+            }
         }
         if (dhl && c == M - 1) {
             const float* hr = dhl + (b * H + h) * (int64_t)N * kP;
 #pragma unroll
-            for (int i = 0; i < R; ++i) md += hr[(n0 + i) * kP + p] * st[i];
+            for (int i = 0; i < RL; ++i) {
+                float t4[4];
+                load4(hr + (nl + i) * kP + pl, t4);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) md += t4[k] * st[i][k];
+            }
         }
 #pragma unroll
         for (int m = 32; m >= 1; m >>= 1) md += __shfl_xor(md, m, 64);
         if (lane == 0) mdp[((b * H + h) * M + c) * 4 + wave] = md;
 
         // reverse sweep: Lam from W_c = R_c + dmem_c; dx, dB
-        float lam[R];
+        float lam[RL][4];
 #pragma unroll
-        for (int i = 0; i < R; ++i) {
-            const int64_t o = (n0 + i) * kP + p;
-            lam[i] = Rs[ch * (int64_t)N * kP + o] + (dmem ? dmem[sm + o] : 0.f);
+        for (int i = 0; i < RL; ++i) {
+            const int64_t o = (nl + i) * kP + pl;
+            float r4[4], m4[4] = {0.f, 0.f, 0.f, 0.f};
+            load4(Rs + ch * (int64_t)N * kP + o, r4);
+            if (dmem) load4(dmem + sm + o, m4);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) lam[i][k] = r4[k] + m4[k];
         }
         const int ntok = (int)(e - a0 + 1);
         for (int k = 0; k < ntok; ++k) {
             const int64_t t = e - k;
             const int64_t th = (b * L + t) * H + h;
             const float d = dt[th];
-            const float dyv = to_f(dy[th * kP + p]);
-            const float xv = to_f(x[th * kP + p]);
-            const T* crow = Cm + ((b * L + t) * G + g) * N + n0;
-            const T* brow = Bm + ((b * L + t) * G + g) * N + n0;
-            float bv[R], cv[R];
+            float xv[4], dyv[4], bv[RL], cv[RL];
+            load4(x + th * kP + pl, xv);
+            load4(dy + th * kP + pl, dyv);
+            load_k<RL>(Bm + ((b * L + t) * G + g) * N + nl, bv);
+            load_k<RL>(Cm + ((b * L + t) * G + g) * N + nl, cv);
+            float px[4] = {0.f, 0.f, 0.f, 0.f}, v[RL];
 #pragma unroll
-            for (int i = 0; i < R; i += 8) {
-                float t8[8], u8[8];
-                load8(brow + i, t8);
-                load8(crow + i, u8);
+            for (int i = 0; i < RL; ++i) {
+                float acc = 0.f;
 #pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    bv[i + k] = t8[k];
-                    cv[i + k] = u8[k];
+                for (int q = 0; q < 4; ++q) {
+                    lam[i][q] += cv[i] * dyv[q];
+                    px[q] += bv[i] * lam[i][q];
+                    acc += lam[i][q] * xv[q];
                 }
+                v[i] = acc;
             }
-            float px = 0.f, v[R];
-#pragma unroll
-            for (int i = 0; i < R; ++i) {
-                lam[i] += cv[i] * dyv;
-                px += bv[i] * lam[i];
-                v[i] = lam[i] * xv;
-            }
-            const float sb = lane_sums<R>(v, lane);
+            const float sb = lane_sums<RL, 16>(v, lane);
             if (writer) {
-                float* o = dBp + ((b * L + t) * nhb + hb) * (int64_t)N + n0 + krow;
+                float* o = dBp + ((b * L + t) * nhb + hb) * (int64_t)N + nsum;
                 *o = hh == 0 ? d * sb : *o + d * sb;
             }
+            // sum of px over the 4 ng lanes: lane (ng, pg) keeps column 4 pg + ng
+            rs_step<4, 4, 32>(px, lane);
             const int slot = k % TB, buf = (k / TB) & 1;
-            xpart[buf][slot][wave][p] = px;
+            xpart[buf][slot][wave][pl + ng] = px[0];
             // carry to t - 1: Lam_{t-1} = C_{t-1}^T dy_{t-1} + a_t Lam_t
             const float a = __expf(d * Ah);
 #pragma unroll
-            for (int i = 0; i < R; ++i) lam[i] *= a;
+            for (int i = 0; i < RL; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) lam[i][q] *= a;
             if (slot == TB - 1 || k == ntok - 1) {
                 __syncthreads();
                 // wave w finishes tokens w, w + 4, ... of this batch
                 const int kb = k - slot;
                 for (int q = wave; q <= slot; q += 4) {
                     const int64_t tq = (b * L + (e - (kb + q))) * H + h;
-                    const float s4 = xpart[buf][q][0][p] + xpart[buf][q][1][p] +
-                                     xpart[buf][q][2][p] + xpart[buf][q][3][p];
-                    dx[tq * kP + p] = dt[tq] * s4;
-                    float pr = s4 * to_f(x[tq * kP + p]);
+                    const float s4 = xpart[buf][q][0][lane] + xpart[buf][q][1][lane] +
+                                     xpart[buf][q][2][lane] + xpart[buf][q][3][lane];
+                    dx[tq * kP + lane] = dt[tq] * s4;
+                    float pr = s4 * to_f(x[tq * kP + lane]);
 #pragma unroll
                     for (int o = 32; o >= 1; o >>= 1) pr += __shfl_xor(pr, o, 64);
                     if (lane == 0) bxl[tq] = pr;
