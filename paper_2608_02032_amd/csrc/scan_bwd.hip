@@ -195,6 +195,17 @@ __device__ __forceinline__ void load_k(const float* p, float (&v)[K]) {
     }
 }
 
+// K storage elements kept raw in registers (converted where used), so that a
+// load issued one token ahead is not waited for at once.
+template <typename T, int K>
+struct alignas(sizeof(T) * K >= 16 ? 16 : sizeof(T) * K) RawVec {
+    T v[K];
+};
+template <typename T, int K>
+__device__ __forceinline__ RawVec<T, K> raw_load(const T* p) {
+    return *reinterpret_cast<const RawVec<T, K>*>(p);
+}
+
 // ---- per (b, c, head block): the two sweeps ----------------------------------------
 // Wave w holds state rows n0 = w N/4 .. n0 + N/4 - 1; inside the wave lane
 // (ng, pg) = (lane / 16, lane % 16) holds the RL = N/16 rows n0 + ng RL + i and
@@ -251,14 +262,33 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
                 dh[i][k] = 0.f;
             }
         }
+        // the next token's rows are loaded while this one is swept
+        RawVec<T, 4> xr, yr;
+        RawVec<T, RL> br;
+        float dn;
+        auto fetch_f = [&](int64_t t) {
+            const int64_t th = (b * L + t) * H + h;
+            dn = dt[th];
+            xr = raw_load<T, 4>(x + th * kP + pl);
+            yr = raw_load<T, 4>(dy + th * kP + pl);
+            br = raw_load<T, RL>(Bm + ((b * L + t) * G + g) * N + nl);
+        };
+        fetch_f(a0);
         for (int64_t t = a0; t <= e; ++t) {
             const int64_t th = (b * L + t) * H + h;
-            const float d = dt[th];
+            const float d = dn;
+            const RawVec<T, 4> xc = xr, yc = yr;
+            const RawVec<T, RL> bc = br;
+            if (t < e) fetch_f(t + 1);
             const float a = __expf(d * Ah);
             float xv[4], dyv[4], bv[RL];
-            load4(x + th * kP + pl, xv);
-            load4(dy + th * kP + pl, dyv);
-            load_k<RL>(Bm + ((b * L + t) * G + g) * N + nl, bv);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                xv[k] = to_f(xc.v[k]);
+                dyv[k] = to_f(yc.v[k]);
+            }
+#pragma unroll
+            for (int i = 0; i < RL; ++i) bv[i] = to_f(bc.v[i]);
 #pragma unroll
             for (int k = 0; k < 4; ++k) xv[k] *= d;
             float v[RL];
@@ -321,15 +351,34 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
             for (int k = 0; k < 4; ++k) lam[i][k] = r4[k] + m4[k];
         }
         const int ntok = (int)(e - a0 + 1);
+        RawVec<T, RL> cr;
+        auto fetch_r = [&](int64_t t) {
+            const int64_t th = (b * L + t) * H + h;
+            dn = dt[th];
+            xr = raw_load<T, 4>(x + th * kP + pl);
+            yr = raw_load<T, 4>(dy + th * kP + pl);
+            br = raw_load<T, RL>(Bm + ((b * L + t) * G + g) * N + nl);
+            cr = raw_load<T, RL>(Cm + ((b * L + t) * G + g) * N + nl);
+        };
+        fetch_r(e);
         for (int k = 0; k < ntok; ++k) {
             const int64_t t = e - k;
             const int64_t th = (b * L + t) * H + h;
-            const float d = dt[th];
+            const float d = dn;
+            const RawVec<T, 4> xc = xr, yc = yr;
+            const RawVec<T, RL> bc = br, cc = cr;
+            if (k + 1 < ntok) fetch_r(t - 1);
             float xv[4], dyv[4], bv[RL], cv[RL];
-            load4(x + th * kP + pl, xv);
-            load4(dy + th * kP + pl, dyv);
-            load_k<RL>(Bm + ((b * L + t) * G + g) * N + nl, bv);
-            load_k<RL>(Cm + ((b * L + t) * G + g) * N + nl, cv);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                xv[q] = to_f(xc.v[q]);
+                dyv[q] = to_f(yc.v[q]);
+            }
+#pragma unroll
+            for (int i = 0; i < RL; ++i) {
+                bv[i] = to_f(bc.v[i]);
+                cv[i] = to_f(cc.v[i]);
+            }
             float px[4] = {0.f, 0.f, 0.f, 0.f}, v[RL];
 #pragma unroll
             for (int i = 0; i < RL; ++i) {
