@@ -265,10 +265,12 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
         // the next token's rows are loaded while this one is swept
         RawVec<T, 4> xr, yr;
         RawVec<T, RL> br;
-        float dn;
+        float dn, on = 0.f;  // on: the previous heads' partial of the row sum
+        const bool rmw = hh > 0 && writer;
         auto fetch_f = [&](int64_t t) {
             const int64_t th = (b * L + t) * H + h;
             dn = dt[th];
+            if (rmw) on = dCp[((b * L + t) * nhb + hb) * (int64_t)N + nsum];
             xr = raw_load<T, 4>(x + th * kP + pl);
             yr = raw_load<T, 4>(dy + th * kP + pl);
             br = raw_load<T, RL>(Bm + ((b * L + t) * G + g) * N + nl);
@@ -276,7 +278,7 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
         fetch_f(a0);
         for (int64_t t = a0; t <= e; ++t) {
             const int64_t th = (b * L + t) * H + h;
-            const float d = dn;
+            const float d = dn, oc = on;
             const RawVec<T, 4> xc = xr, yc = yr;
             const RawVec<T, RL> bc = br;
             if (t < e) fetch_f(t + 1);
@@ -305,10 +307,7 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
                 v[i] = acc;
             }
             const float sc = lane_sums<RL, 16>(v, lane);
-            if (writer) {
-                float* o = dCp + ((b * L + t) * nhb + hb) * (int64_t)N + nsum;
-                *o = hh == 0 ? sc : *o + sc;
-            }
+            if (writer) dCp[((b * L + t) * nhb + hb) * (int64_t)N + nsum] = oc + sc;
             // y_t . dy_t over this wave's rows: C_n dC_n summed over the rows
             float yd = writer ? to_f(Cm[((b * L + t) * G + g) * N + nsum]) * sc : 0.f;
 #pragma unroll
@@ -355,6 +354,7 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
         auto fetch_r = [&](int64_t t) {
             const int64_t th = (b * L + t) * H + h;
             dn = dt[th];
+            if (rmw) on = dBp[((b * L + t) * nhb + hb) * (int64_t)N + nsum];
             xr = raw_load<T, 4>(x + th * kP + pl);
             yr = raw_load<T, 4>(dy + th * kP + pl);
             br = raw_load<T, RL>(Bm + ((b * L + t) * G + g) * N + nl);
@@ -364,7 +364,7 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
         for (int k = 0; k < ntok; ++k) {
             const int64_t t = e - k;
             const int64_t th = (b * L + t) * H + h;
-            const float d = dn;
+            const float d = dn, ob = on;
             const RawVec<T, 4> xc = xr, yc = yr;
             const RawVec<T, RL> bc = br, cc = cr;
             if (k + 1 < ntok) fetch_r(t - 1);
@@ -392,10 +392,7 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
                 v[i] = acc;
             }
             const float sb = lane_sums<RL, 16>(v, lane);
-            if (writer) {
-                float* o = dBp + ((b * L + t) * nhb + hb) * (int64_t)N + nsum;
-                *o = hh == 0 ? d * sb : *o + d * sb;
-            }
+            if (writer) dBp[((b * L + t) * nhb + hb) * (int64_t)N + nsum] = ob + d * sb;
             // sum of px over the 4 ng lanes: lane (ng, pg) keeps column 4 pg + ng
             rs_step<4, 4, 32>(px, lane);
             const int slot = k % TB, buf = (k / TB) & 1;
