@@ -1,6 +1,6 @@
-"""The library under HIP graph capture: the forward (scan, then SMA + gate) and
-a ragged decode step (positions on the device, so one captured graph serves
-every step) are captured once and replayed several times, with the
+"""The library under HIP graph capture: the forward (scan, then SMA + gate), the
+scan backward, and a ragged decode step (positions on the device, so one
+captured graph serves every step) are captured once and replayed several times, with the
 program's own eager work and synchronisations between replays (new inputs,
 an eager run into separate buffers).  Every replay must equal the eager
 result bit for bit (the kernels are deterministic and the library issues no
@@ -121,3 +121,52 @@ def test_ragged_decode_step_replays_in_a_graph():
         assert torch.equal(cache, cc_e), k
         pos.add_(1)  # every row moves on one token (device-side, outside the graph)
         print("  replay %d equals the eager step" % k, flush=True)
+
+
+def test_scan_backward_replays_in_a_graph():
+    import torch
+    w = synth.Workload("graph_bwd_bf16_L600_N64_S128", 2, 600, 4, 64, 64, 128, "bf16")
+    announce("graph scan backward %s" % (w,))
+    B, L, H, P, N, S, M = w.batch, w.seqlen, w.nheads, w.headdim, w.dstate, w.chunk, w.nchunks
+    d = synth.forward_inputs(w, seed=91)
+    inp = {k: to_dev(d[k], w.dtype) for k in ("x", "Bm", "Cm")}
+    inp["dt"], inp["A"] = f32_dev(d["dt"]), f32_dev(d["A"])
+    rng = np.random.default_rng(92)
+    dy = to_dev(synth.to_storage(rng.standard_normal((B, L, H, P)).astype(np.float32), "bf16"), "bf16")
+    dmem = f32_dev(rng.standard_normal((B, M, H, N, P)).astype(np.float32))
+    dims = dart.make_dims(B, L, H, P, N, S, w.dtype, 1, M)
+    ws = torch.empty(dart.workspace_bytes("ssd_bwd", dims), dtype=torch.uint8, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+
+    def buffers():
+        return {"dx": torch.empty((B, L, H, P), **f32), "ddt": torch.empty((B, L, H), **f32),
+                "dA": torch.empty((H,), **f32), "dB": torch.empty((B, L, 1, N), **f32),
+                "dC": torch.empty((B, L, 1, N), **f32), "dh0": torch.empty((B, H, N, P), **f32)}
+
+    def bwd(o):
+        dart.ssd_bwd(inp["x"], inp["dt"], inp["A"], inp["Bm"], inp["Cm"], S, dy, dmem=dmem, out=o,
+                     workspace=ws)
+
+    out = buffers()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        bwd(out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        bwd(out)
+    for rep in range(3):
+        d2 = synth.forward_inputs(w, seed=93 + rep)
+        for k in ("x", "Bm", "Cm"):
+            inp[k].copy_(to_dev(d2[k], w.dtype))
+        inp["dt"].copy_(f32_dev(d2["dt"]))
+        ref = buffers()
+        bwd(ref)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in out:
+            assert torch.equal(out[k], ref[k]), (rep, k)
+        print("  replay %d equals the eager backward" % rep, flush=True)
