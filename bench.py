@@ -10,7 +10,8 @@ are already resident in HBM:
             N = 128, S = 256 over a 65536-token context (256 cached memories).
 `value` is forward tokens/s (batch * L / forward time).  Per-kernel times come
 from HIP events the library records around every launch on the launch stream
-(dart_profile_*), averaged over the timed steps.
+(dart_profile_*): in the timed steps only around k_sma (the roofline kernel),
+then around every launch in a separate pass for the breakdown.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1]
 """
@@ -234,7 +235,7 @@ def main():
     import numpy as np
     import torch
     from paper_2608_02032_amd import dart, synth
-    from paper_2608_02032_amd.profiling import traffic_for
+    from paper_2608_02032_amd.profiling import mfma_for, traffic_for
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -295,6 +296,17 @@ def main():
                          h_state, chunk_acc, cache, dw.chunk, y=y_dec, workspace=ws_dec,
                          stream=stream)
 
+    def profiled(fn, reps):
+        """Per-kernel times of `reps` further calls, every launch bracketed by
+        library events (kept out of the timed calls)."""
+        dart.profile_reset()
+        dart.profile_enable(True)
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        dart.profile_enable(False)
+        return dart.profile_read(reset=True)
+
     for _ in range(args.warmup):
         forward()
         if not args.no_decode:
@@ -302,7 +314,11 @@ def main():
     torch.cuda.synchronize()
 
     # ---- timed region --------------------------------------------------------
+    # The headline steps run with library events around k_sma only (its
+    # average launch time gives the roofline); every other kernel runs back to
+    # back with nothing recorded between launches.
     dart.profile_reset()
+    dart.profile_filter("k_sma")
     dart.profile_enable(True)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -317,12 +333,23 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     dart.profile_enable(False)
-    kernels = dart.profile_read(reset=True)
+    kmain = dart.profile_read(reset=True)
     fwd_ms = [e[0].elapsed_time(e[1]) for e in ev]
     dec_ms = [e[1].elapsed_time(e[2]) for e in ev]
     step_ms = [e[0].elapsed_time(e[2]) for e in ev]
     fwd_mean = sum(fwd_ms) / len(fwd_ms)
     ms_per_step = sum(step_ms) / len(step_ms)
+
+    # ---- per-kernel breakdown: a separate pass with every launch bracketed --
+    nprof = min(args.steps, 20)
+    dart.profile_enable(True)
+    for _ in range(nprof):
+        forward()
+        if not args.no_decode:
+            decode()
+    torch.cuda.synchronize()
+    dart.profile_enable(False)
+    kernels = dart.profile_read(reset=True)
     avg = {k: v[0] / max(v[1], 1) for k, v in kernels.items()}  # ms per launch
 
     # ---- rooflines -----------------------------------------------------------
@@ -331,14 +358,15 @@ def main():
     scan_ms = sum(avg.get(k, 0.0) for k in ("k_chunk_state", "k_chunk_gram", "k_state_pass",
                                              "k_chunk_out"))
     sma_ms = sum(avg.get(k, 0.0) for k in ("k_sma_prep", "k_sma_keys", "k_sma"))
-    main_ms = avg["k_sma"]
+    main_ms = kmain["k_sma"][0] / max(kmain["k_sma"][1], 1)
     main_tflops = mflops / (main_ms * 1e-3) / 1e12
     roofline = {"kernel": "k_sma", "bound": "mfma",
                 "achieved": round(main_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(main_tflops / PEAK_BF16_TFLOPS, 4),
                 "traffic": traffic_for("k_sma"),
                 "avg_us": round(main_ms * 1e3, 2),
-                "algorithmic_flops_per_launch": mflops}
+                "algorithmic_flops_per_launch": mflops,
+                "timed": "k_sma launches of the timed steps (library HIP events on its stream)"}
     extra = {
         "mfma_util": {"scan": round(sflops / (scan_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                       "sma": round(mflops / (sma_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
@@ -347,6 +375,9 @@ def main():
                  "algorithmic_bytes": sbytes, "algorithmic_flops": sflops},
         "sma": {"us": round(sma_ms * 1e3, 2), "algorithmic_flops": mflops, "algorithmic_bytes": mbytes},
         "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(avg.items())},
+        "kernels_pass": "%d further steps with library events around every launch" % nprof,
+        "mfma_busy": {k: mfma_for(k) for k in ("k_sma", "k_chunk_out_heads", "k_chunk_state_heads",
+                                               "k_bwd_tokens", "k_bwd_mem")},
     }
     if not args.no_decode:
         dbytes = decode_bytes(dw)
@@ -415,15 +446,12 @@ def main():
         R = 10
         eb = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         torch.cuda.synchronize()
-        dart.profile_reset()
-        dart.profile_enable(True)
         eb[0].record(stream)
         for _ in range(R):
             backward()
         eb[1].record(stream)
         torch.cuda.synchronize()
-        dart.profile_enable(False)
-        bk = dart.profile_read(reset=True)
+        bk = profiled(backward, R)
         bavg = {k: v[0] / max(v[1], 1) for k, v in bk.items()}
         bwd_ms = eb[0].elapsed_time(eb[1]) / R
         bflops = sma_bwd_flops(w)
@@ -450,15 +478,12 @@ def main():
         for _ in range(3):
             scan_backward()
         torch.cuda.synchronize()
-        dart.profile_reset()
-        dart.profile_enable(True)
         eb[0].record(stream)
         for _ in range(R):
             scan_backward()
         eb[1].record(stream)
         torch.cuda.synchronize()
-        dart.profile_enable(False)
-        sk = dart.profile_read(reset=True)
+        sk = profiled(scan_backward, R)
         savg = {k: v[0] / max(v[1], 1) for k, v in sk.items()}
         sb_ms = eb[0].elapsed_time(eb[1]) / R
         sbb = ssd_bwd_bytes(w)

@@ -369,16 +369,21 @@ const char* dart_last_error(void);
 
 /*
  * Optional kernel timing (a tracing aid, off by default).  While enabled,
- * every kernel the library launches is bracketed by two HIP events recorded
- * on the stream it is launched on.  dart_profile_flush() waits for the
- * pending events and adds each kernel's elapsed time to a per-kernel total;
- * the totals are read by index (0 .. dart_profile_count()-1) and cleared by
- * dart_profile_reset().  Events are created on first use and kept for reuse
- * until dart_profile_reset(); this is the only state the library keeps, and
- * these functions are not thread-safe.  dart_profile_flush() returns
+ * every kernel the library launches -- or, after dart_profile_filter(name),
+ * only the kernel of that name (e.g. "k_sma") -- is bracketed by two HIP
+ * events recorded on the stream it is launched on.  dart_profile_flush()
+ * waits for the pending events and adds each kernel's elapsed time to a
+ * per-kernel total; the totals are read by index (0 .. dart_profile_count()-1)
+ * and cleared, with the filter, by dart_profile_reset().  Events are created
+ * on first use and kept for reuse until dart_profile_reset(); this is the only
+ * state the library keeps.  The totals are shared by all threads under one
+ * lock and every launching thread pairs its own events, so the functions may
+ * be called from several threads; a reset while another thread launches
+ * drops that thread's open interval.  dart_profile_flush() returns
  * DART_ERR_HIP if an event query fails.
  */
 dart_status dart_profile_enable(int enable);
+dart_status dart_profile_filter(const char* kernel);  /* NULL or "": every kernel */
 dart_status dart_profile_flush(void);
 int dart_profile_count(void);
 const char* dart_profile_name(int index);     /* kernel name, or NULL */

@@ -86,7 +86,7 @@ def _load():
                                                 _D, _D, _D, _D]
         lib.dart_oracle_decode_step.restype = ctypes.c_int
         lib.dart_oracle_sma_bwd.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
-                                            ctypes.c_double, _INT, _INT, _INT,
+                                            ctypes.c_double, _INT, _INT,
                                             _D, _D, _D, _D, _D, _D, _D, _D,
                                             _D, _D, _D, _D, _D]
         lib.dart_oracle_sma_bwd.restype = None
@@ -211,18 +211,13 @@ def sma_rows(q, e, Cm, mem, z, y_ssd, S, rows, eps=1e-6, normalize=True, q_norm_
     return yr, lr
 
 
-def sma_bwd(q, e, Cm, mem, z, dy, S, eps=1e-6, normalize=True, q_norm_w=None, e_norm_w=None,
-            round_scores=False):
+def sma_bwd(q, e, Cm, mem, z, dy, S, eps=1e-6, normalize=True, q_norm_w=None, e_norm_w=None):
     """Gradients of the SMA + gate forward for the loss sum(dy * y), by
     recomputing every row (App. C) and the chain rule through Sec. 3 and
     App. B.1 (the norm weights are constants).  Shapes as in sma(); dy like
     y_ssd.  Returns {"dq", "de", "dC", "dmem", "dz", "dy_ssd"}: q, e, C
     gradients summed over the heads of their group, dmem in the cache layout
-    (slots never attended are zero), dz like z, dy_ssd = dy.
-
-    round_scores=True forms the logits from the two score operands rounded
-    to bf16 as the bf16 path stores them (Qbar log2(e)/sqrt(N) and r (.) dH);
-    everything else stays exact."""
+    (slots never attended are zero), dz like z, dy_ssd = dy."""
     q, e, Cm, mem, z, dy = map(_f64, (q, e, Cm, mem, z, dy))
     B_, L, H, P = dy.shape
     G, N = q.shape[2], q.shape[3]
@@ -234,7 +229,7 @@ def sma_bwd(q, e, Cm, mem, z, dy, S, eps=1e-6, normalize=True, q_norm_w=None, e_
     out = {"dq": np.empty_like(q), "de": np.empty_like(e), "dC": np.empty_like(Cm),
            "dmem": np.empty_like(mem), "dz": np.empty_like(z)}
     _load().dart_oracle_sma_bwd(B_, L, H, G, P, N, int(S), Mcap, float(eps), int(bool(normalize)),
-                                z_per_head, int(bool(round_scores)), _ptr(q), _ptr(e), _ptr(Cm), _ptr(qw), _ptr(ew),
+                                z_per_head, _ptr(q), _ptr(e), _ptr(Cm), _ptr(qw), _ptr(ew),
                                 _ptr(mem), _ptr(z), _ptr(dy), _ptr(out["dq"]), _ptr(out["de"]),
                                 _ptr(out["dC"]), _ptr(out["dmem"]), _ptr(out["dz"]))
     out["dy_ssd"] = dy.copy()

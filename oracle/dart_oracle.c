@@ -465,18 +465,6 @@ void dart_oracle_sma_rows(int64_t B, int64_t L, int H, int G, int P, int N, int 
 /* q, e, C gradients sum over the heads of their group; dz sums over heads   */
 /* when one gate serves every head of a token.  Outputs are overwritten.     */
 /* ------------------------------------------------------------------------ */
-/* Round to the nearest bfloat16 (8 significant bits, ties to even) through
- * float: the storage format of the bf16 path's score operands. */
-#define LOG2E 1.4426950408889634
-#define LN2 0.6931471805599453
-static double round_bf16(double v) {
-    union { float f; uint32_t u; } c;
-    c.f = (float)v;
-    if ((c.u & 0x7f800000u) == 0x7f800000u) return (double)c.f; /* inf, nan */
-    c.u = (c.u + 0x7fffu + ((c.u >> 16) & 1u)) & 0xffff0000u;
-    return (double)c.f;
-}
-
 static double silu_grad(double z) {
     const double s = 1.0 / (1.0 + exp(-z));
     return s * (1.0 + z * (1.0 - s));
@@ -494,7 +482,7 @@ static void rms_normalise_bwd(const double* v, int D, double eps, const double* 
 }
 
 void dart_oracle_sma_bwd(int64_t B, int64_t L, int H, int G, int P, int N, int S, int64_t Mcap,
-                         double eps, int normalize, int z_per_head, int round_scores,
+                         double eps, int normalize, int z_per_head,
                          const double* q, const double* e, const double* Cm, const double* qw,
                          const double* ew, const double* mem, const double* z, const double* dy,
                          double* dq, double* de, double* dC, double* dmem, double* dz) {
@@ -544,18 +532,9 @@ void dart_oracle_sma_bwd(int64_t B, int64_t L, int H, int G, int P, int N, int S
                         double a = 0.0;
                         for (int p = 0; p < P; ++p) a += dH[(size_t)n * P + p] * ebar[p];
                         Aj[(size_t)j * N + n] = a;
-                        if (round_scores) {
-                            /* the score from bf16 operands: Qbar / sqrt(N) in
-                               base-2 units and the key side r (.) dH */
-                            double ar = 0.0;
-                            for (int p = 0; p < P; ++p)
-                                ar += round_bf16(r[n] * dH[(size_t)n * P + p]) * ebar[p];
-                            l += round_bf16(qbar[n] * isn * LOG2E) * ar;
-                        } else {
-                            l += qbar[n] * r[n] * a;
-                        }
+                        l += qbar[n] * r[n] * a;
                     }
-                    ell[j] = round_scores ? l * LN2 : l * isn;
+                    ell[j] = l * isn;
                     for (int p = 0; p < P; ++p) {
                         double v = 0.0;
                         for (int n = 0; n < N; ++n) v += ct[n] * dH[(size_t)n * P + p];

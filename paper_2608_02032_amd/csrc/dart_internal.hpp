@@ -52,10 +52,11 @@ hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const voi
                       float* lse, void* ws, hipStream_t st);
 
 // Key side r (.) dH of memories 0..M-2 in the cache layout [B][M-1][H][N][P]
-// (storage dtype), as the fp32 forward stages it; rinv (optional,
+// (storage dtype), as the fp32 forward stages it; klo (optional, bf16 only,
+// same layout) receives its rounding residual; rinv (optional,
 // [B][M-1][H][N] float) receives 1 / r.
 hipError_t launch_sma_keys(const Shape& s, const SmaArgs& a, const void* mem, void* kmem,
-                           float* rinv, hipStream_t st);
+                           void* klo, float* rinv, hipStream_t st);
 
 // SMA backward: key side, Qbar/Ebar, per-(head, memory, token) softmax
 // scalars, per-head-block partial token gradients and R . dy.

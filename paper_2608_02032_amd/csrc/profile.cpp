@@ -1,8 +1,13 @@
 // profile.cpp -- optional kernel timing with HIP events (dart_profile_* in
-// dart.h).  Off by default; when on, every launch is bracketed by two events
-// recorded on the launch stream, and flush() turns them into per-kernel totals.
+// dart.h).  Off by default; when on, every launch (or only the launches of the
+// kernel named by the filter) is bracketed by two events recorded on the
+// launch stream, and flush() turns them into per-kernel totals.  The totals
+// are shared by all threads under one mutex; the event opened by prof_begin
+// belongs to the launching thread, so concurrent launches from several
+// threads pair their own events.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -23,12 +28,13 @@ struct Pending {
 };
 
 std::mutex g_mu;
-bool g_on = false;
+std::atomic<bool> g_on{false};
+std::string g_filter;  // empty: every kernel
 std::vector<Entry> g_entries;
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_free;
-int g_open_entry = -1;
-hipEvent_t g_open_start = nullptr;
+thread_local int g_open_entry = -1;
+thread_local hipEvent_t g_open_start = nullptr;
 
 hipEvent_t take_event() {
     if (!g_free.empty()) {
@@ -53,8 +59,9 @@ int entry_for(const char* name) {
 namespace dart {
 
 void prof_begin(const char* kernel, hipStream_t st) {
-    if (!g_on) return;
+    if (!g_on.load(std::memory_order_relaxed)) return;
     std::lock_guard<std::mutex> lk(g_mu);
+    if (!g_filter.empty() && g_filter != kernel) return;
     hipEvent_t e = take_event();
     if (!e) return;
     (void)hipEventRecord(e, st);
@@ -63,7 +70,7 @@ void prof_begin(const char* kernel, hipStream_t st) {
 }
 
 void prof_end(hipStream_t st) {
-    if (!g_on) return;
+    if (!g_on.load(std::memory_order_relaxed)) return;
     std::lock_guard<std::mutex> lk(g_mu);
     if (!g_open_start) return;
     hipEvent_t e = take_event();
@@ -80,7 +87,13 @@ extern "C" {
 
 dart_status dart_profile_enable(int enable) {
     std::lock_guard<std::mutex> lk(g_mu);
-    g_on = enable != 0;
+    g_on.store(enable != 0);
+    return DART_OK;
+}
+
+dart_status dart_profile_filter(const char* kernel) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_filter = kernel ? kernel : "";
     return DART_OK;
 }
 
@@ -137,8 +150,7 @@ void dart_profile_reset(void) {
     for (hipEvent_t e : g_free) (void)hipEventDestroy(e);
     g_free.clear();
     g_entries.clear();
-    g_open_start = nullptr;
-    g_open_entry = -1;
+    g_filter.clear();
 }
 
 }  // extern "C"

@@ -105,14 +105,29 @@ __device__ __forceinline__ uint4 piece_scale(uint4 v, float r, float) {
     return __builtin_bit_cast(uint4, f);
 }
 
+// The rounding residual of a scaled bf16 piece: lo = bf16(v r - bf16(v r)), so
+// that hi + lo carries v r to about 16 significant bits.
+__device__ __forceinline__ uint4 piece_scale_lo(uint4 v, float r) {
+    const bf16x8 h = __builtin_bit_cast(bf16x8, v);
+    bf16x8 o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float x = (float)h[i] * r;
+        o[i] = (bf16)(x - (float)(bf16)x);
+    }
+    return __builtin_bit_cast(uint4, o);
+}
+
 // Key side of one memory: kmem = r (.) dH, r[n] the inverse RMS of row n of
 // the stored values.  The RPC lanes holding one row's 16-byte pieces reduce
 // its sum of squares with DPP moves.  rinv (optional, [B][Mp][H][N]) receives
-// 1 / r[n].
+// 1 / r[n]; klo (optional, bf16 only) the rounding residual of the bf16 key
+// side, so kmem + klo is r (.) dH to about 16 bits.
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* __restrict__ kmem,
-                                                  float* __restrict__ rinv, float eps,
-                                                  int normalize, int H, int64_t Mp, int64_t Mcap) {
+                                                  T* __restrict__ klo, float* __restrict__ rinv,
+                                                  float eps, int normalize, int H, int64_t Mp,
+                                                  int64_t Mcap) {
     constexpr int RB = kP * (int)sizeof(T);
     constexpr int PIECES = N * RB / 16;
     constexpr int RPC = RB / 16;
@@ -121,7 +136,8 @@ __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* 
     const int h = blockIdx.y;
     const int64_t b = blockIdx.z;
     const uint4* src = reinterpret_cast<const uint4*>(mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP);
-    uint4* dst = reinterpret_cast<uint4*>(kmem + ((b * Mp + j) * H + h) * (int64_t)N * kP);
+    const int64_t obase = ((b * Mp + j) * H + h) * (int64_t)N * kP;
+    uint4* dst = reinterpret_cast<uint4*>(kmem + obase);
     uint4 v[PIECES / 256];
 #pragma unroll
     for (int i = 0; i < PIECES / 256; ++i) v[i] = src[threadIdx.x + i * 256];
@@ -130,6 +146,9 @@ __global__ __launch_bounds__(256) void k_sma_keys(const T* __restrict__ mem, T* 
         const float ss = dpp_group_sum<RPC>(piece_sumsq(v[i], T()));
         const float rn = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
         dst[threadIdx.x + i * 256] = piece_scale(v[i], rn, T());
+        if constexpr (sizeof(T) == 2) {
+            if (klo) reinterpret_cast<uint4*>(klo + obase)[threadIdx.x + i * 256] = piece_scale_lo(v[i], rn);
+        }
         const int q = threadIdx.x + i * 256;
         if (rinv && q % RPC == 0) rinv[((b * Mp + j) * H + h) * (int64_t)N + q / RPC] = 1.0f / rn;
     }
@@ -1457,7 +1476,7 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
         if (Mp > 0) {
             prof_begin("k_sma_keys", st);
             k_sma_keys<T, N><<<dim3((unsigned)Mp, (unsigned)s.H, (unsigned)s.B), 256, 0, st>>>(
-                (const T*)mem, kmem, nullptr, a.eps, a.normalize, s.H, Mp, s.Mcap);
+                (const T*)mem, kmem, nullptr, nullptr, a.eps, a.normalize, s.H, Mp, s.Mcap);
             prof_end(st);
         }
         prof_begin("k_sma", st);
@@ -1497,24 +1516,28 @@ hipError_t run_sma_n(const Shape& s, const SmaArgs& a, const void* q, const void
 }  // namespace
 
 hipError_t launch_sma_keys(const Shape& s, const SmaArgs& a, const void* mem, void* kmem,
-                           float* rinv, hipStream_t st) {
+                           void* klo, float* rinv, hipStream_t st) {
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
     if (Mp == 0) return hipSuccess;
     const dim3 grid((unsigned)Mp, (unsigned)s.H, (unsigned)s.B);
     prof_begin("k_sma_keys", st);
+#define DART_KEYS(T, NN)                                                                      \
+    k_sma_keys<T, NN><<<grid, 256, 0, st>>>((const T*)mem, (T*)kmem, (T*)klo, rinv, a.eps, \
+                                            a.normalize, s.H, Mp, s.Mcap)
     if (s.dtype == 1) {
         switch (s.N) {
-            case 32: k_sma_keys<bf16, 32><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 64: k_sma_keys<bf16, 64><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 128: k_sma_keys<bf16, 128><<<grid, 256, 0, st>>>((const bf16*)mem, (bf16*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 32: DART_KEYS(bf16, 32); break;
+            case 64: DART_KEYS(bf16, 64); break;
+            case 128: DART_KEYS(bf16, 128); break;
         }
     } else {
         switch (s.N) {
-            case 32: k_sma_keys<float, 32><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 64: k_sma_keys<float, 64><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
-            case 128: k_sma_keys<float, 128><<<grid, 256, 0, st>>>((const float*)mem, (float*)kmem, rinv, a.eps, a.normalize, s.H, Mp, s.Mcap); break;
+            case 32: DART_KEYS(float, 32); break;
+            case 64: DART_KEYS(float, 64); break;
+            case 128: DART_KEYS(float, 128); break;
         }
     }
+#undef DART_KEYS
     prof_end(st);
     return hipGetLastError();
 }

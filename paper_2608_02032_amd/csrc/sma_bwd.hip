@@ -130,17 +130,22 @@ struct TileCopy {
     }
 };
 
-// ---- Qbar' and Ebar per (b, t, g) row: one wave per row ---------------------
-// Qbar' = RMSNorm(q) w * log2(e)/sqrt(N) rounded to the storage dtype (the
-// forward's score operand); Ebar = RMSNorm(e) w in float, and (ebt != NULL)
-// also in the storage dtype for the memory kernel's MFMA operand.  Without
-// normalisation the raw vectors (times log2(e)/sqrt(N) for q).
+// ---- per (b, t, g) row: one wave per row -----------------------------------
+// qb = Qbar' = RMSNorm(q) w * log2(e)/sqrt(N) in the storage dtype (the
+// operand of the gradient products); the score operand of the logits is kept
+// exact instead: qh = q (.) w (the storage value itself when w = NULL), in
+// bf16 also its rounding residual ql, and the per-row scale qsc with
+// Qbar' = (q (.) w) qsc.  Ebar = RMSNorm(e) w in float, and (ebt != NULL)
+// also in the storage dtype.  Without normalisation: raw q and e, qsc =
+// log2(e)/sqrt(N).
 template <typename T, int N>
 __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const T* __restrict__ e,
                                                   const float* __restrict__ qw,
                                                   const float* __restrict__ ew, T* __restrict__ qb,
-                                                  float* __restrict__ eb, T* __restrict__ ebt,
-                                                  float eps, int normalize, int64_t rows) {
+                                                  T* __restrict__ qh, bf16* __restrict__ ql,
+                                                  float* __restrict__ qsc, float* __restrict__ eb,
+                                                  T* __restrict__ ebt, float eps, int normalize,
+                                                  int64_t rows) {
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= rows) return;
@@ -160,11 +165,14 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
     for (int k = 0; k < QE; ++k) {
         const int n = lane + 64 * k;
         if (n < N) {
-            float v = qv[k] * qinv;
-            if (qw) v *= qw[n];
-            qb[row * N + n] = from_f<T>(v);
+            const float qwv = qw ? qv[k] * qw[n] : qv[k];
+            qb[row * N + n] = from_f<T>(qwv * qinv);
+            const T hi = from_f<T>(qwv);
+            qh[row * N + n] = hi;
+            if (ql) ql[row * N + n] = (bf16)(qwv - to_f(hi));
         }
     }
+    if (lane == 0) qsc[row] = qinv;
     const float ev = to_f(e[row * kP + lane]);
     const float es = wave_sum(ev * ev);
     const float einv = normalize ? 1.0f / sqrtf(es * (1.0f / kP) + eps) : 1.0f;
@@ -174,65 +182,14 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
     if (ebt) ebt[row * kP + lane] = from_f<T>(v);
 }
 
-// ---- token-side gradients ------------------------------------------------------
-// Workgroup: 64 consecutive tokens of chunk i >= 1 (all in one chunk because
-// S is a multiple of 64) and hpb heads of one group, 8 waves.  Waves w and
-// w + 4 share tokens 16 w .. 16 w + 15 and split the work in halves: rows p
-// of W' (and dEbar), rows n of X and Z (and dQbar, dC); each keeps only its
-// half of the per-token state, so a wave fits 256 registers and two waves
-// share a SIMD.  In every MFMA product the memory tile is the A operand (rows
-// n or p) and the tokens are the 16 columns, so lane l works on token l % 16
-// and its rows 4 (l / 16) + 0..3 of each 16-row tile.
-//
-// One pass over (head, memory j) steps.  Per step: W' = Kh^T Qbar'^T (logits,
-// p_j; the two halves add their partial sums over p through LDS),
-// X = dH dy^T (dwy_j, likewise; dC += g p_j X) and Z = Kh Ebar^T, all three
-// from the key-side tile alone (X as diag(1/r) Kh dy^T, so dH is not
-// streamed; in bf16 this reads dH through the key side's rounding).  dl_j
-// needs Dy = sum_j p_j dwy_j, known only after the head's last memory, so the
-// head accumulates S1 = sum_j p_j dwy_j Z_j, S2 = sum_j p_j Z_j (and U1, U2
-// with W') and adds g s (S1 - Dy S2) to dQbar and g ln2 (U1 - Dy U2) to dEbar
-// at its end (W' and Qbar' carry log2(e)/sqrt(N); ln2 takes it back to s).
-// Tiles (Kh_j and the row of 1/r_j) stream through an NS-stage LDS ring by
-// DMA, NS - 1 steps ahead, copied by waves 0-3; each copying wave waits only
-// for its own copies of the current step and a barrier orders the stages.
-template <typename T, int N>
-constexpr int tok_stages() {
-    return (N * kP * (int)sizeof(T) * 4 <= 131072) ? 4 : 2;
-}
-
-template <typename T, int N>
-__global__ __launch_bounds__(512) void k_bwd_tokens(
-    const T* __restrict__ qb, const float* __restrict__ eb, const T* __restrict__ Cm,
-    const float* __restrict__ rinv, const T* __restrict__ kmem, const T* __restrict__ z,
-    const float* __restrict__ lse, const T* __restrict__ dy, float* __restrict__ gpw,
-    float* __restrict__ gdw, float* __restrict__ part, float* __restrict__ rdy, int z_per_head,
-    int64_t L, int H, int G, int S, int64_t Mp, int hpb, int blk0, int nblk, int64_t BHC) {
-    constexpr int RB = kP * (int)sizeof(T);  // bytes of one tile row (fixed n)
-    constexpr int TILE = N * RB;
-    constexpr int NT = N / 16;
-    constexpr int KQ = N / 32;
-    constexpr int NTH = NT / 2;          // n tiles per wave
-    constexpr int NS = tok_stages<T, N>();
-    using Copy = TileCopy<RB, TILE, kTokWaves>;
-    constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per copying wave
-    constexpr int CPS = Copy::count() + 1;  // DMA copies per copying wave per step
-    __shared__ __attribute__((aligned(16))) char ring[NS][TILE];
-    __shared__ __attribute__((aligned(16))) float rring[NS][N];
-    __shared__ float xch[2][2][kTokWaves][16];  // (logit, dwy) partials per half
-
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int col = lane & 15, grp = lane >> 4;
-    const int tg = wave & 3, nh = wave >> 2;  // token group, half of n
-    const bool copier = wave < kTokWaves;
-    // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
-    // index and each XCD has its own L2.  When the number of (b, head block)
-    // pairs is a multiple of 8, XCD x runs the token blocks of pairs x, x+8,
-    // ... one pair after another, heaviest first: the blocks running together
-    // on an XCD stream the same memory tiles in the same order.
-    const int64_t bid = blockIdx.x;
-    int blk;
-    int64_t bhc;
+// Block order shared by the two token kernels.  Workgroups are dealt to the
+// 8 XCDs round-robin by block index and each XCD has its own L2.  When the
+// number of (b, head block) pairs is a multiple of 8, XCD x runs the token
+// blocks of pairs x, x+8, ... one pair after another, heaviest first: the
+// blocks running together on an XCD stream the same memory tiles in the
+// same order.
+__device__ __forceinline__ void tok_block(int64_t bid, int nblk, int64_t BHC, int& blk,
+                                          int64_t& bhc) {
     if (BHC % 8 == 0) {
         const int64_t slot = bid >> 3;
         blk = nblk - 1 - (int)(slot % nblk);
@@ -241,6 +198,279 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         blk = nblk - 1 - (int)(bid / BHC);
         bhc = bid % BHC;
     }
+}
+
+// LDS ring stages of the token kernels: four when NTILES tiles of a stage fit
+// 32 KiB, else two.
+template <typename T, int N, int NTILES>
+constexpr int tok_stages() {
+    return (NTILES * N * kP * (int)sizeof(T) * 4 <= 131072) ? 4 : 2;
+}
+
+// The k-permuted fragments of one token's row of N values (a B operand with
+// the contraction over n): k step ks holds n = 32 ks + 4 (lane/16) + 0..3 and
+// + 16.
+template <typename T, typename S, int N>
+__device__ __forceinline__ void load_row_frags(const S* row, int grp, Frag<T> (&f)[N / 32]) {
+#pragma unroll
+    for (int ks = 0; ks < N / 32; ++ks) {
+        float a[4], c[4], v[8];
+        load4(row + ks * 32 + 4 * grp, a);
+        load4(row + ks * 32 + 16 + 4 * grp, c);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[i] = a[i];
+            v[4 + i] = c[i];
+        }
+        f[ks] = make_frag<T>(v);
+    }
+}
+
+// ---- scores: exact logits and dy . V per (head, memory, token) ---------------
+// Workgroup: 64 consecutive tokens of chunk i >= 1 and hpb heads of one group,
+// 8 waves; waves w and w + 4 share tokens 16 w .. 16 w + 15 and split the
+// rows: rows p of W'^T = Kh^T (q (.) w) (this half's part of every logit)
+// and rows n of X^T = diag(1/r) Kh dy^T (its part of dy . V = C . X).  The
+// two partial sums meet in LDS once per step.
+//
+// The logits are formed to about 16 bits although the operands are stored in
+// bf16: the key side streams as hi + lo (the lo tile holds the rounding
+// residual of r (.) dH), the query operand is q (.) w, exact when w = NULL
+// (then q is the stored bf16 value) and otherwise hi + lo as well, and the
+// row scale of RMSNorm multiplies the finished sum.  So W' = Kh_hi^T q_hi +
+// Kh_lo^T q_hi (+ Kh_hi^T q_lo).  The softmax backward differences the
+// weights (dl_j = g p_j (dy . V_j - Dy)) and its sums over memories cancel,
+// so bf16-rounded logits (an absolute error of about 1e-2 at logits of rms
+// sqrt(P)) would move the gradients by several per cent; with these logits
+// they move by about 1e-5.
+//
+// Per (head, memory) it writes the logit l2 (log2 units) and dwy; at the
+// head's last memory, with d = sum_j exp2(l2_j - lse2) over the forward's
+// log-sum-exp lse2 (log2 units), the exact log-sum-exp of these logits
+// lse2 + log2(d) and Dy = sum_j p_j dwy_j with p_j = exp2(l2_j - lse2) / d:
+// the weights the gradient kernels use are the softmax of the exact logits,
+// whatever rounding the forward's log-sum-exp carries.  Tiles stream through
+// an NS-stage LDS ring by DMA, NS - 1 steps ahead, copied by waves 0-3.
+template <typename T, int N>
+__global__ __launch_bounds__(512) void k_bwd_scores(
+    const T* __restrict__ qh, const bf16* __restrict__ ql, const float* __restrict__ qsc,
+    const float* __restrict__ eb, const T* __restrict__ Cm, const float* __restrict__ rinv,
+    const T* __restrict__ kmem, const T* __restrict__ klo, const float* __restrict__ lse,
+    const T* __restrict__ dy, float* __restrict__ lw, float* __restrict__ dwv,
+    float* __restrict__ lsep, float* __restrict__ rdy, int use_ql, int64_t L, int64_t Ls, int H,
+    int G, int S, int64_t Mp, int hpb, int blk0, int nblk, int64_t BHC) {
+    constexpr bool LO = sizeof(T) == 2;
+    constexpr int NTL = LO ? 2 : 1;  // tiles per stage: key side (and its residual)
+    constexpr int RB = kP * (int)sizeof(T);
+    constexpr int TILE = N * RB;
+    constexpr int NT = N / 16;
+    constexpr int KQ = N / 32;
+    constexpr int NTH = NT / 2;
+    constexpr int NS = tok_stages<T, N, NTL>();
+    using Copy = TileCopy<RB, TILE, kTokWaves>;
+    constexpr int RPW = N / 16;
+    constexpr int CPS = NTL * Copy::count() + 1;
+    __shared__ __attribute__((aligned(16))) char ring[NS][NTL][TILE];
+    __shared__ __attribute__((aligned(16))) float rring[NS][N];
+    __shared__ float xch[2][2][kTokWaves][16];
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int tg = wave & 3, nh = wave >> 2;
+    const bool copier = wave < kTokWaves;
+    int blk;
+    int64_t bhc;
+    tok_block(blockIdx.x, nblk, BHC, blk, bhc);
+    const int nhb = H / hpb;
+    const int64_t b = bhc / nhb;
+    const int hb = (int)(bhc % nhb);
+    const int64_t t0 = (int64_t)(blk0 + blk) * kTokBlock;
+    const int nj = (int)(t0 / S);
+    const int64_t t = t0 + tg * 16 + col;
+    const bool valid = t < L;
+    const int64_t tc = valid ? t : L - 1;
+    const int h0 = hb * hpb;
+    const int g = h0 / (H / G);
+    const int64_t bt = b * L + tc;
+    const int nt0 = nh * NTH;
+    const int pt0 = nh * 2;
+
+    Frag<T> qf[KQ];
+    load_row_frags<T, T, N>(qh + (bt * G + g) * N, grp, qf);
+    Frag<bf16> qlf[LO ? KQ : 1];
+    if constexpr (LO) {
+        if (use_ql) {
+            load_row_frags<bf16, bf16, N>(ql + (bt * G + g) * N, grp, qlf);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < KQ; ++ks) qlf[ks] = bf16x8{};
+        }
+    }
+    const float qs = qsc[bt * G + g];
+    const float* erow = eb + (bt * G + g) * kP;
+    float ea[2][4];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) load4(erow + 16 * (pt0 + q) + 4 * grp, ea[q]);
+    typedef T T4 __attribute__((ext_vector_type(4)));
+    T4 ca[NTH];
+    {
+        const T* crow = Cm + (bt * G + g) * N;
+#pragma unroll
+        for (int k = 0; k < NTH; ++k)
+            ca[k] = *reinterpret_cast<const T4*>(crow + 16 * (nt0 + k) + 4 * grp);
+    }
+    const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
+    const int nsteps = hpb * nj;
+    Copy copy;
+    copy.init(tg, lane);
+    auto issue_tiles = [&](int k) {
+        if (!copier) return;
+        const int hh = k / nj, j = k - hh * nj;
+        const int64_t hj = (b * Mp + j) * H + h0 + hh;
+        copy.issue(kmem + hj * N * kP, ring[k % NS][0]);
+        if constexpr (LO) copy.issue(klo + hj * N * kP, ring[k % NS][NTL - 1]);
+        if (lane < RPW)
+            lds_dma16_untracked_at(rinv + hj * N + (tg * RPW + lane) * 4,
+                                   lds_addr(&rring[k % NS][0]) + tg * RPW * 16);
+    };
+    auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * Ls + tc; };
+
+#pragma unroll
+    for (int k = 0; k < NS - 1; ++k)
+        if (k < nsteps) issue_tiles(k);
+
+    Frag<T> dyf[2];
+    float lse2 = 0.f, dsum = 0.f, dyacc = 0.f;
+    for (int k = 0; k < nsteps; ++k) {
+        const int hh = k / nj, j = k - hh * nj;
+        const int h = h0 + hh;
+        const int ahead = nsteps - 1 - k < NS - 2 ? nsteps - 1 - k : NS - 2;
+        if (ahead >= 2) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * CPS));
+        } else if (ahead == 1) {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(CPS));
+        } else {
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        }
+        lds_barrier();
+        if (j == 0) {
+            const T* dyrow = dy + (bt * H + h) * kP;
+            dyf[0] = load_frag(dyrow + 8 * grp);
+            dyf[1] = load_frag(dyrow + 32 + 8 * grp);
+            lse2 = lse[bt * H + h] * kLog2e;
+            dsum = dyacc = 0.f;
+            keep(dyf[0]);
+            keep(dyf[1]);
+            asm volatile("" ::"v"(lse2));
+        }
+        if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
+        const char* kt = ring[k % NS][0];
+        // this half's rows p of W'^T
+        f32x4 w[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) w[q] = zero4;
+#pragma unroll
+        for (int ks = 0; ks < KQ; ++ks) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int r0 = 32 * ks + 4 * grp, r1 = r0 + 16, cb = 16 * (pt0 + q);
+                const Frag<T> a = frag_km<T, RB>(kt, r0, r1, cb, lane);
+                w[q] = mma16(w[q], a, qf[ks]);
+                if constexpr (LO) {
+                    const char* kl = ring[k % NS][NTL - 1];
+                    w[q] = mma16(w[q], frag_km<T, RB>(kl, r0, r1, cb, lane), qf[ks]);
+                    if (use_ql) w[q] = mma16(w[q], a, qlf[ks]);
+                }
+            }
+        }
+        float l2 = 0.f;
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) l2 += ea[q][i] * w[q][i];
+        // this half's rows n of X^T = diag(1/r) Kh dy^T, then C . X
+        float dw = 0.f;
+#pragma unroll
+        for (int q = 0; q < NTH; ++q) {
+            const int nt = nt0 + q;
+            f32x4 x = zero4;
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+                x = mma16(x, frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp), dyf[ks]);
+            x *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dw += to_f(ca[q][i]) * x[i];
+        }
+        l2 += shfl_xor(l2, 16);
+        l2 += shfl_xor(l2, 32);
+        dw += shfl_xor(dw, 16);
+        dw += shfl_xor(dw, 32);
+        if (lane < 16) {
+            xch[0][nh][tg][col] = l2;
+            xch[1][nh][tg][col] = dw;
+        }
+        lds_barrier();
+        l2 = (l2 + xch[0][nh ^ 1][tg][col]) * qs;
+        dw += xch[1][nh ^ 1][tg][col];
+        const float p = fast_exp2(l2 - lse2);
+        dsum += p;
+        dyacc += p * dw;
+        if (nh == 0 && lane < 16 && valid) {
+            lw[sidx(h, j)] = l2;
+            dwv[sidx(h, j)] = dw;
+            if (j == nj - 1) {
+                lsep[bt * H + h] = lse2 + __log2f(dsum);
+                rdy[bt * H + h] = dyacc / dsum;
+            }
+        }
+    }
+}
+
+// ---- token-side gradients ------------------------------------------------------
+// Same workgroup and block order as k_bwd_scores.  Waves w and w + 4 share
+// tokens 16 w .. 16 w + 15 and split the rows of each product: rows p of W'
+// (and dEbar), rows n of X and Z (and dQbar, dC).  In every MFMA product the
+// memory tile is the A operand (rows n or p) and the tokens are the 16
+// columns, so lane l works on token l % 16 and its rows 4 (l / 16) + 0..3 of
+// each 16-row tile.
+//
+// The scores kernel has left, per (head, memory, token), the exact logit and
+// dwy, and per (token, head) the exact log-sum-exp and Dy; these rows (64
+// tokens of one head and memory) arrive by DMA with the key tile, so each
+// step knows p_j = exp2(l2_j - lse2') and dl_j = g p_j (dwy_j - Dy) at once:
+//   dQbar += s dl_j Z_j,   Z = Kh Ebar^T;
+//   dEbar += s dl_j Kh_j^T Qbar = ln2 dl_j W'_j,   W' = Kh^T Qbar'^T;
+//   dC    += g p_j X_j,    X = diag(1/r) Kh dy^T = dH dy^T;
+// the three products from the key side alone (bf16 rounding of these
+// operands is not amplified: each sum over memories carries the exact
+// weights).  g p_j replaces the logit in place for the memory kernel.
+template <typename T, int N>
+__global__ __launch_bounds__(512) void k_bwd_tokens(
+    const T* __restrict__ qb, const float* __restrict__ eb, const float* __restrict__ rinv,
+    const T* __restrict__ kmem, const T* __restrict__ z, const float* __restrict__ lsep,
+    const float* __restrict__ rdy, const T* __restrict__ dy, float* __restrict__ gpw,
+    const float* __restrict__ gdw, float* __restrict__ part, int z_per_head, int64_t L, int64_t Ls,
+    int H, int G, int S, int64_t Mp, int hpb, int blk0, int nblk, int64_t BHC) {
+    constexpr int RB = kP * (int)sizeof(T);  // bytes of one tile row (fixed n)
+    constexpr int TILE = N * RB;
+    constexpr int NT = N / 16;
+    constexpr int KQ = N / 32;
+    constexpr int NTH = NT / 2;          // n tiles per wave
+    constexpr int NS = tok_stages<T, N, 1>();
+    using Copy = TileCopy<RB, TILE, kTokWaves>;
+    constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per copying wave
+    constexpr int CPS = Copy::count() + 2;   // DMA copies per copying wave per step
+    __shared__ __attribute__((aligned(16))) char ring[NS][TILE];
+    __shared__ __attribute__((aligned(16))) float rring[NS][N];
+    __shared__ __attribute__((aligned(16))) float lring[NS][kTokWaves][2][16];  // logit, dwy
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int tg = wave & 3, nh = wave >> 2;  // token group, half of n
+    const bool copier = wave < kTokWaves;
+    int blk;
+    int64_t bhc;
+    tok_block(blockIdx.x, nblk, BHC, blk, bhc);
     const int nhb = H / hpb;
     const int64_t b = bhc / nhb;
     const int hb = (int)(bhc % nhb);
@@ -256,46 +486,20 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     const int nt0 = nh * NTH;  // first n tile of this wave
     const int pt0 = nh * 2;    // first p tile of this wave
 
-    // group-shared token operands (Qbar' whole; this wave's halves of Ebar, C)
+    // group-shared token operands (Qbar' whole; Ebar)
     Frag<T> qf[KQ];
-    {
-        const T* qrow = qb + (bt * G + g) * N;
-#pragma unroll
-        for (int ks = 0; ks < KQ; ++ks) {
-            float a[4], c[4], v[8];
-            load4(qrow + ks * 32 + 4 * grp, a);
-            load4(qrow + ks * 32 + 16 + 4 * grp, c);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                v[i] = a[i];
-                v[4 + i] = c[i];
-            }
-            qf[ks] = make_frag<T>(v);
-        }
-    }
+    load_row_frags<T, T, N>(qb + (bt * G + g) * N, grp, qf);
     const float* erow = eb + (bt * G + g) * kP;
     Frag<T> ef[2];
-    float ea[2][4];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
         float v[8];
         load8(erow + ks * 32 + 8 * grp, v);
         ef[ks] = make_frag<T>(v);
     }
-#pragma unroll
-    for (int q = 0; q < 2; ++q) load4(erow + 16 * (pt0 + q) + 4 * grp, ea[q]);
-    // C in the storage dtype (half the registers in bf16), widened where used
-    typedef T T4 __attribute__((ext_vector_type(4)));
-    T4 ca[NTH];
-    {
-        const T* crow = Cm + (bt * G + g) * N;
-#pragma unroll
-        for (int k = 0; k < NTH; ++k)
-            ca[k] = *reinterpret_cast<const T4*>(crow + 16 * (nt0 + k) + 4 * grp);
-    }
 
     const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
-    f32x4 dQ[NTH], dC[NTH], dE[2], s1[NTH], s2[NTH], u1[2], u2[2];
+    f32x4 dQ[NTH], dC[NTH], dE[2];
 #pragma unroll
     for (int k = 0; k < NTH; ++k) dQ[k] = dC[k] = zero4;
 #pragma unroll
@@ -312,9 +516,14 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         if (lane < RPW)
             lds_dma16_untracked_at(rinv + hj * N + (tg * RPW + lane) * 4,
                                    lds_addr(&rring[k % NS][0]) + tg * RPW * 16);
+        // this token group's 16 logits (lanes 0-3) and dwy (lanes 4-7)
+        if (lane < 8) {
+            const int64_t srow = ((b * H + h0 + hh) * Mp + j) * Ls + t0 + 16 * tg + 4 * (lane & 3);
+            lds_dma16_untracked_at(lane < 4 ? (const float*)gpw + srow : gdw + srow,
+                                   lds_addr(&lring[k % NS][tg][0][0]));
+        }
     };
-    // per (head, memory) scalar slot of this lane's token
-    auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * L + tc; };
+    auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * Ls + tc; };
 
 #pragma unroll
     for (int k = 0; k < NS - 1; ++k)
@@ -341,94 +550,47 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
             const T* dyrow = dy + (bt * H + h) * kP;
             dyf[0] = load_frag(dyrow + 8 * grp);
             dyf[1] = load_frag(dyrow + 32 + 8 * grp);
-            lse2 = lse[bt * H + h] * kLog2e;
+            lse2 = lsep[bt * H + h];
+            Dy = rdy[bt * H + h];
             gate = silu(to_f(z[z_per_head ? bt * H + h : bt]));
-            Dy = 0.f;
             keep(dyf[0]);
             keep(dyf[1]);
-            asm volatile("" ::"v"(lse2), "v"(gate));
-#pragma unroll
-            for (int q = 0; q < NTH; ++q) s1[q] = s2[q] = zero4;
-#pragma unroll
-            for (int q = 0; q < 2; ++q) u1[q] = u2[q] = zero4;
+            asm volatile("" ::"v"(lse2), "v"(Dy), "v"(gate));
         }
         if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
         const char* kt = ring[k % NS];
-        // this half's rows p of W'^T = Kh^T Qbar'^T: token columns
-        f32x4 w[2];
+        const float p = fast_exp2(lring[k % NS][tg][0][col] - lse2);
+        const float gp = gate * p;
+        const float dl = gp * (lring[k % NS][tg][1][col] - Dy);
+        // this half's rows p of W'^T = Kh^T Qbar'^T: dEbar += ln2 dl W'
+        const float ce = kLn2 * dl;
 #pragma unroll
-        for (int q = 0; q < 2; ++q) w[q] = zero4;
+        for (int q = 0; q < 2; ++q) {
+            f32x4 w = zero4;
 #pragma unroll
-        for (int ks = 0; ks < KQ; ++ks) {
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-                w[q] = mma16(w[q], frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp,
-                                                  16 * (pt0 + q), lane),
-                             qf[ks]);
+            for (int ks = 0; ks < KQ; ++ks)
+                w = mma16(w, frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp,
+                                            16 * (pt0 + q), lane),
+                          qf[ks]);
+            dE[q] += ce * w;
         }
-        float l2 = 0.f;
-#pragma unroll
-        for (int q = 0; q < 2; ++q)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) l2 += ea[q][i] * w[q][i];
         // X^T = diag(1/r) Kh dy^T and Z^T = Kh Ebar^T on this half's n tiles
-        f32x4 x[NTH], zz[NTH];
+        const float cq = isn * dl;
 #pragma unroll
         for (int q = 0; q < NTH; ++q) {
             const int nt = nt0 + q;
-            x[q] = zz[q] = zero4;
+            f32x4 x = zero4, zz = zero4;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const Frag<T> a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
-                x[q] = mma16(x[q], a, dyf[ks]);
-                zz[q] = mma16(zz[q], a, ef[ks]);
+                x = mma16(x, a, dyf[ks]);
+                zz = mma16(zz, a, ef[ks]);
             }
-            x[q] *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+            x *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+            dC[q] += gp * x;
+            dQ[q] += cq * zz;
         }
-        float dw = 0.f;
-#pragma unroll
-        for (int q = 0; q < NTH; ++q)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) dw += to_f(ca[q][i]) * x[q][i];
-        l2 += shfl_xor(l2, 16);
-        l2 += shfl_xor(l2, 32);
-        dw += shfl_xor(dw, 16);
-        dw += shfl_xor(dw, 32);
-        // the other half's partial sums
-        if (lane < 16) {
-            xch[0][nh][tg][col] = l2;
-            xch[1][nh][tg][col] = dw;
-        }
-        lds_barrier();
-        l2 += xch[0][nh ^ 1][tg][col];
-        dw += xch[1][nh ^ 1][tg][col];
-        const float p = fast_exp2(l2 - lse2);
-        Dy += p * dw;
-        const float gp = gate * p, pd = p * dw;
-#pragma unroll
-        for (int q = 0; q < NTH; ++q) {
-            dC[q] += gp * x[q];
-            s1[q] += pd * zz[q];
-            s2[q] += p * zz[q];
-        }
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            u1[q] += pd * w[q];
-            u2[q] += p * w[q];
-        }
-        if (nh == 0 && lane < 16 && valid) {
-            gpw[sidx(h, j)] = gp;
-            gdw[sidx(h, j)] = dw;
-        }
-        if (j == nj - 1) {
-            // the head's dl_j = g p_j (dwy_j - Dy), summed against Z and W'
-            const float cq = gate * isn, ce = gate * kLn2;
-#pragma unroll
-            for (int q = 0; q < NTH; ++q) dQ[q] += cq * (s1[q] - Dy * s2[q]);
-#pragma unroll
-            for (int q = 0; q < 2; ++q) dE[q] += ce * (u1[q] - Dy * u2[q]);
-            if (nh == 0 && lane < 16 && valid) rdy[bt * H + h] = Dy;
-        }
+        if (nh == 0 && lane < 16 && valid) gpw[sidx(h, j)] = gp;
     }
 
     if (!valid) return;
@@ -482,8 +644,8 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
                                                  const float* __restrict__ gdw,
                                                  const float* __restrict__ rdy,
                                                  float* __restrict__ dmem, float eps, int normalize,
-                                                 int64_t L, int H, int G, int S, int64_t Mcap,
-                                                 int64_t Mp, int64_t BH) {
+                                                 int64_t L, int64_t Ls, int H, int G, int S,
+                                                 int64_t Mcap, int64_t Mp, int64_t BH) {
     constexpr int J = kMemJ;
     constexpr int ES = (int)sizeof(T);
     constexpr int TB = mem_tb<T>();
@@ -553,7 +715,7 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
             const int jl = ft / TB, tk = ft % TB;
             const int64_t j = j0 + jl, t = tbeg + (int64_t)st * TB + tk;
             if (j < Mp && t < L && t >= (j + 1) * S) {
-                const int64_t si = ((b * H + h) * Mp + j) * L + t;
+                const int64_t si = ((b * H + h) * Mp + j) * Ls + t;
                 const float gp = gpw[si];
                 fg = gp;
                 fd = kLn2 * gp * (gdw[si] - rdy[(b * L + t) * H + h]);
@@ -767,21 +929,32 @@ int bwd_heads_per_block(const Shape& s) {
 
 struct BwdWs {
     void* kmem;
-    void* qb;
+    void* klo;    // rounding residual of the bf16 key side (bf16 only)
+    void* qb;     // Qbar' in the storage dtype
+    void* qh;     // q (.) w in the storage dtype
+    void* ql;     // its bf16 rounding residual (bf16 only)
+    float* qsc;   // per-row scale: Qbar' = (q (.) w) qsc
     float* eb;
-    void* ebt;  // Ebar in the storage dtype (eb itself for fp32)
+    void* ebt;    // Ebar in the storage dtype (eb itself for fp32)
     float* rinv;  // 1 / r of every attended memory row, [B][M-1][H][N]
-    float* gp;
-    float* gd;
+    float* gp;    // per (b, h, memory, token): the exact logit, then g p
+    float* gd;    // per (b, h, memory, token): dwy
     float* part;
-    float* rdy;
+    float* rdy;   // Dy per (b, t, h)
+    float* lsep;  // exact log-sum-exp (log2 units) per (b, t, h)
     size_t bytes;
 };
+
+// Row stride of the per-(b, h, memory) token arrays: a multiple of the 64
+// tokens a token-kernel workgroup reads as one row piece.
+inline int64_t bwd_row_stride(const Shape& s) { return (s.L + kTokBlock - 1) / kTokBlock * kTokBlock; }
 
 BwdWs bwd_layout(const Shape& s, void* base) {
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
     const size_t es = elem_bytes(s.dtype);
+    const bool lo = s.dtype == 1;
     const int nhb = s.H / bwd_heads_per_block(s);
+    const size_t Ls = (size_t)bwd_row_stride(s);
     size_t o = 0;
     BwdWs w;
     char* p = reinterpret_cast<char*>(base);
@@ -791,14 +964,19 @@ BwdWs bwd_layout(const Shape& s, void* base) {
         return r;
     };
     w.kmem = take(es * s.B * Mp * s.H * (size_t)s.N * s.P);
+    w.klo = lo ? take(es * s.B * Mp * s.H * (size_t)s.N * s.P) : nullptr;
     w.rinv = (float*)take(4 * s.B * Mp * s.H * (size_t)s.N);
     w.qb = take(es * s.B * s.L * s.G * (size_t)s.N);
+    w.qh = take(es * s.B * s.L * s.G * (size_t)s.N);
+    w.ql = lo ? take(2 * s.B * s.L * s.G * (size_t)s.N) : nullptr;
+    w.qsc = (float*)take(4 * s.B * s.L * (size_t)s.G);
     w.eb = (float*)take(4 * s.B * s.L * s.G * (size_t)s.P);
-    w.ebt = s.dtype == 1 ? take(es * s.B * s.L * s.G * (size_t)s.P) : (void*)w.eb;
-    w.gp = (float*)take(4 * s.B * s.H * Mp * (size_t)s.L);
-    w.gd = (float*)take(4 * s.B * s.H * Mp * (size_t)s.L);
+    w.ebt = lo ? take(es * s.B * s.L * s.G * (size_t)s.P) : (void*)w.eb;
+    w.gp = (float*)take(4 * s.B * s.H * Mp * Ls);
+    w.gd = (float*)take(4 * s.B * s.H * Mp * Ls);
     w.part = (float*)take(4 * s.B * s.L * nhb * (size_t)(2 * s.N + s.P));
     w.rdy = (float*)take(4 * s.B * s.L * (size_t)s.H);
+    w.lsep = (float*)take(4 * s.B * s.L * (size_t)s.H);
     w.bytes = o;
     return w;
 }
@@ -810,27 +988,38 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
     const BwdWs w = bwd_layout(s, ws);
     const int hpb = bwd_heads_per_block(s);
+    const int64_t Ls = bwd_row_stride(s);
+    constexpr bool LO = sizeof(T) == 2;
     hipError_t err;
     if (Mp > 0) {
-        err = launch_sma_keys(s, a, mem, w.kmem, w.rinv, st);
+        err = launch_sma_keys(s, a, mem, w.kmem, w.klo, w.rinv, st);
         if (err != hipSuccess) return err;
     }
     const int64_t rows = s.B * s.L * s.G;
     const unsigned rblocks = (unsigned)((rows + 3) / 4);
     prof_begin("k_bwd_prep", st);
-    k_bwd_prep<T, N><<<rblocks, 256, 0, st>>>((const T*)q, (const T*)e, a.qw, a.ew, (T*)w.qb, w.eb,
-                                              sizeof(T) == 2 ? (T*)w.ebt : nullptr, a.eps,
-                                              a.normalize, rows);
+    k_bwd_prep<T, N><<<rblocks, 256, 0, st>>>((const T*)q, (const T*)e, a.qw, a.ew, (T*)w.qb,
+                                              (T*)w.qh, (bf16*)w.ql, w.qsc, w.eb,
+                                              LO ? (T*)w.ebt : nullptr, a.eps, a.normalize, rows);
     prof_end(st);
     const int blk0 = s.S / kTokBlock;
     const int64_t nblk = (s.L + kTokBlock - 1) / kTokBlock - blk0;
     if (Mp > 0 && nblk > 0) {
-        prof_begin("k_bwd_tokens", st);
         const int64_t BHC = s.B * (s.H / hpb);
+        // the query operand needs its residual only when a norm weight makes
+        // q (.) w inexact in bf16
+        const int use_ql = LO && a.qw != nullptr;
+        prof_begin("k_bwd_scores", st);
+        k_bwd_scores<T, N><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
+            (const T*)w.qh, (const bf16*)w.ql, w.qsc, w.eb, (const T*)Cm, w.rinv, (const T*)w.kmem,
+            (const T*)w.klo, lse, (const T*)dy, w.gp, w.gd, w.lsep, w.rdy, use_ql, s.L, Ls, s.H,
+            s.G, s.S, Mp, hpb, blk0, (int)nblk, BHC);
+        prof_end(st);
+        prof_begin("k_bwd_tokens", st);
         k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
-            (const T*)w.qb, w.eb, (const T*)Cm, w.rinv, (const T*)w.kmem, (const T*)z, lse,
-            (const T*)dy, w.gp, w.gd, w.part, w.rdy, a.z_per_head, s.L, s.H, s.G, s.S, Mp, hpb,
-            blk0, (int)nblk, BHC);
+            (const T*)w.qb, w.eb, w.rinv, (const T*)w.kmem, (const T*)z, w.lsep, w.rdy,
+            (const T*)dy, w.gp, w.gd, w.part, a.z_per_head, s.L, Ls, s.H, s.G, s.S, Mp, hpb, blk0,
+            (int)nblk, BHC);
         prof_end(st);
     }
     const int64_t BH = s.B * s.H;
@@ -838,7 +1027,7 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     const int64_t njb = (s.Mcap + kMemJ - 1) / kMemJ;
     k_bwd_mem<T, N><<<(unsigned)(BH * njb), 512, 0, st>>>(
         (const T*)w.qb, (const T*)w.ebt, (const T*)Cm, (const T*)dy, (const T*)mem, w.gp, w.gd, w.rdy, dmem, a.eps,
-        a.normalize, s.L, s.H, s.G, s.S, s.Mcap, Mp, BH);
+        a.normalize, s.L, Ls, s.H, s.G, s.S, s.Mcap, Mp, BH);
     prof_end(st);
     prof_begin("k_bwd_finish", st);
     k_bwd_finish<T, N><<<rblocks, 256, 0, st>>>((const T*)q, (const T*)e, (const T*)z, a.qw, a.ew,

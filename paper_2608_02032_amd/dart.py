@@ -49,7 +49,7 @@ EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspa
            "dart_conv1d_silu", "dart_dt_softplus", "dart_gated_rmsnorm",
            "dart_decode_workspace_bytes", "dart_decode_step",
            "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
-           "dart_profile_enable", "dart_profile_flush", "dart_profile_count",
+           "dart_profile_enable", "dart_profile_filter", "dart_profile_flush", "dart_profile_count",
            "dart_profile_name", "dart_profile_total_ms", "dart_profile_launches",
            "dart_profile_reset")
 
@@ -111,6 +111,8 @@ def load_library(path: str = LIB_PATH):
         lib.dart_last_error.restype = ctypes.c_char_p
         lib.dart_profile_enable.argtypes = [ctypes.c_int]
         lib.dart_profile_enable.restype = st
+        lib.dart_profile_filter.argtypes = [ctypes.c_char_p]
+        lib.dart_profile_filter.restype = st
         lib.dart_profile_flush.argtypes = []
         lib.dart_profile_flush.restype = st
         lib.dart_profile_count.argtypes = []
@@ -504,6 +506,11 @@ def decode_cache_elems(dims: Dims, context: int) -> int:
 
 def profile_enable(on: bool = True):
     check(load_library().dart_profile_enable(1 if on else 0))
+
+
+def profile_filter(kernel: Optional[str] = None):
+    """Time only the launches of `kernel` (None: every kernel)."""
+    check(load_library().dart_profile_filter(kernel.encode() if kernel else None))
 
 
 def profile_reset():

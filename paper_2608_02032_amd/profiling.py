@@ -4,6 +4,9 @@
     python -m paper_2608_02032_amd.profiling traffic <fetch counter_collection.csv>
            <write counter_collection.csv> <copy bytes> <out.json> <out.md> "<commands>"
 
+    python -m paper_2608_02032_amd.profiling mfma <counter_collection.csv> <kernel_stats.csv>
+           <out.json> <out.md> "<command>"
+
 `traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
 launch of each library kernel.  Each counter is scaled by what it reads for a
 plain device copy of known size run in the same process (the copy kernel moves
@@ -25,6 +28,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+MFMA_JSON = os.path.join(ROOT, "profiles", "mfma_counters.json")
+# MI355X: GRBM_GUI_ACTIVE comes back summed over the 8 XCDs; 1024 SIMDs
+# (256 CUs x 4) each report SQ_VALU_MFMA_BUSY_CYCLES.
+N_XCD = 8
+N_SIMD = 1024
+PEAK_BF16_TFLOPS = 2500.0
 
 
 def source_hash() -> str:
@@ -117,11 +126,73 @@ def traffic_for(kernel: str):
     return None if k is None else k["traffic_bytes"]
 
 
+def mfma_summary(pmc_csv: str, stats_csv: str, out_json: str, out_md: str, command: str) -> dict:
+    """Per kernel: MFMA-busy fraction of every SIMD's cycles while the kernel
+    ran (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024)), the bf16
+    MFMA flops it executed (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512), the shader
+    clock (GRBM_GUI_ACTIVE / 8 over the traced duration) and the executed
+    TFLOP/s."""
+    vals = defaultdict(lambda: defaultdict(list))
+    for r in csv.DictReader(open(pmc_csv)):
+        k = kernel_short(r["Kernel_Name"])
+        if k:
+            vals[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    dur = {}
+    for r in csv.DictReader(open(stats_csv)):
+        k = kernel_short(r["Name"])
+        if k:
+            dur[k] = float(r["AverageNs"]) * 1e-9
+    mean = lambda v: sum(v) / len(v) if v else 0.0
+    out = {"source_hash": source_hash(), "kernels": {}}
+    lines = ["# MFMA counters per launch (rocprofv3 --pmc)", "", "Commands:", "", "```", command, "```",
+             "", "busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d x %d SIMDs); "
+             "executed = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flops per launch; clock = GRBM_GUI_ACTIVE / %d "
+             "over the kernel-trace average duration." % (N_XCD, N_SIMD, N_XCD), "",
+             "| kernel | launches | avg us | MFMA busy | bf16 GFLOP executed | executed TFLOP/s | clock GHz |",
+             "|---|---|---|---|---|---|---|"]
+    for k in sorted(vals):
+        c = vals[k]
+        gui = mean(c.get("GRBM_GUI_ACTIVE", [])) / N_XCD
+        busy = mean(c.get("SQ_VALU_MFMA_BUSY_CYCLES", []))
+        mops = mean(c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", []))
+        frac = busy / (gui * N_SIMD) if gui > 0 else None
+        flops = mops * 512.0
+        d = dur.get(k)
+        tf = flops / d / 1e12 if d else None
+        ghz = gui / d / 1e9 if d else None
+        out["kernels"][k] = {"mfma_busy": frac, "bf16_flops": flops, "avg_s": d,
+                             "executed_tflops": tf, "clock_ghz": ghz}
+        lines.append("| %s | %d | %s | %s | %.1f | %s | %s |" % (
+            k, len(c.get("SQ_VALU_MFMA_BUSY_CYCLES", [])), "%.1f" % (d * 1e6) if d else "-",
+            "%.1f %%" % (100 * frac) if frac is not None else "-", flops / 1e9,
+            "%.0f" % tf if tf else "-", "%.2f" % ghz if ghz else "-"))
+    with open(out_json, "w") as fh:
+        json.dump(out, fh, indent=1)
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    return out
+
+
+def mfma_for(kernel: str):
+    """Counter-measured MFMA-busy fraction of `kernel`, or None when no
+    counters were taken for the current kernel sources."""
+    if not os.path.exists(MFMA_JSON):
+        return None
+    d = json.load(open(MFMA_JSON))
+    if d.get("source_hash") != source_hash():
+        return None
+    k = d["kernels"].get(kernel)
+    return None if k is None or k["mfma_busy"] is None else round(k["mfma_busy"], 4)
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "trace":
         print(trace_summary(sys.argv[2], sys.argv[3], sys.argv[4]))
     elif sys.argv[1] == "traffic":
         print(json.dumps(traffic_summary(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5],
                                          sys.argv[6], sys.argv[7]), indent=1))
+    elif sys.argv[1] == "mfma":
+        print(json.dumps(mfma_summary(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5],
+                                      sys.argv[6]), indent=1))
     else:
         raise SystemExit(__doc__)

@@ -26,19 +26,35 @@ def assert_close_slices(got, ref, tol, axes_keep=(0, 2), what=""):
     return err
 
 
-def assert_lse_close(got, ref, tol, what="lse", axes_keep=(0, 2)):
-    """-inf exactly where the reference has no history; elsewhere the same
-    per-(b, h)-slice metric as the other outputs: max|d| / max|ref| over the
-    slice's finite entries."""
+# Per-entry bound on the log-sum-exp.  fp32: |d| <= 1e-4 (1 + |ref|).  bf16:
+# a logit passes through three bf16 roundings -- the stored memory, the key
+# side r (.) dH and the query operand Qbar log2(e)/sqrt(N) -- each a relative
+# error of at most u = 2^-9 per element, independent across the N P terms of
+# the logit.  Under the normalisation every operand has unit RMS and the
+# 1/sqrt(N) scale cancels the sum over n, so the logit error has a standard
+# deviation of about u sqrt(k P / 3) for k roundings: u sqrt(P) = 0.0156 at
+# P = 64, k = 3.  The LSE, a weighted mean of its logits, inherits it.  The
+# bound is 8 such deviations, |d| <= 8 u sqrt(P) = 0.125 absolute.
+LSE_ATOL = {"fp32": 0.0, "bf16": 8.0 * 2.0 ** -9 * 8.0}
+LSE_RTOL = {"fp32": 1e-4, "bf16": 0.0}
+
+
+def assert_lse_close(got, ref, dtype, what="lse"):
+    """-inf exactly where the reference has no history; elsewhere every entry
+    within |d| <= LSE_ATOL + LSE_RTOL (1 + |ref|)."""
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     ninf = np.isneginf(ref)
     assert np.array_equal(np.isneginf(got), ninf), "%s: -inf pattern differs" % what
     fin = ~ninf
     assert np.all(np.isfinite(got[fin])), "%s: non-finite values" % what
-    g = np.where(fin, got, 0.0)
-    r = np.where(fin, ref, 0.0)
-    return assert_close_slices(g, r, tol, axes_keep, what)
+    d = np.abs(got[fin] - ref[fin])
+    bound = LSE_ATOL[dtype] + LSE_RTOL[dtype] * (1.0 + np.abs(ref[fin]))
+    worst = float((d / bound).max()) if d.size else 0.0
+    print("  %-28s max |d| %.3e, max |d|/bound %.3f" % (what, float(d.max()) if d.size else 0.0, worst),
+          flush=True)
+    assert worst <= 1.0, "%s: |d| exceeds the per-entry bound (worst ratio %.3f)" % (what, worst)
+    return worst
 
 
 def to_dev(a, dtype, device="cuda"):

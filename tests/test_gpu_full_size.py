@@ -11,6 +11,7 @@ import pytest
 import oracle
 from paper_2608_02032_amd import dart, synth
 from tests.helpers import TOL, assert_close_slices, assert_lse_close, f32_dev, to_dev, to_np
+from tests.test_gpu_parity import readout_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -42,6 +43,9 @@ def test_forward_full_size_sampled(name, slices):
     x, Bm, Cm, q, e, z = (to_dev(d[k], w.dtype) for k in ("x", "Bm", "Cm", "q", "e", "z"))
     y_ssd, mem, hl = dart.ssd_chunk_scan(x, f32_dev(d["dt"]), f32_dev(d["A"]), Bm, Cm, w.chunk)
     y, lse = dart.sma_fwd(q, e, Cm, mem, z, y_ssd, w.chunk)
+    # the readout alone: y_ssd = 0 and one gate z = 2 (y = SiLU(2) R)
+    ys0, z2 = readout_inputs(w, d)
+    yR, _ = dart.sma_fwd(q, e, Cm, mem, to_dev(z2, w.dtype), to_dev(ys0, w.dtype), w.chunk)
     torch.cuda.synchronize()
     tol = TOL[w.dtype]
     S, L = w.chunk, w.seqlen
@@ -68,9 +72,13 @@ def test_forward_full_size_sampled(name, slices):
         ti = torch.as_tensor(ts, device=y.device)
         assert_close_slices(to_np(y[b, :, h][ti])[None], yr[None], tol, axes_keep=(0,),
                             what="y rows " + what)
-        assert_lse_close(to_np(lse[b, :, h][ti])[None], lr[None], tol, what="lse rows " + what,
-                         axes_keep=(0,))
-    del x, Bm, Cm, q, e, z, y_ssd, mem, hl, y, lse
+        assert_lse_close(to_np(lse[b, :, h][ti])[None], lr[None], w.dtype, what="lse rows " + what)
+        rr, _ = oracle.sma_rows(d["q"][b:b + 1], d["e"][b:b + 1], d["Cm"][b:b + 1],
+                                to_np(mem[b:b + 1, :, h:h + 1]), z2[b:b + 1, :, h:h + 1],
+                                ys0[b:b + 1, :, h:h + 1], S, rows)
+        assert_close_slices(to_np(yR[b, :, h][ti])[None], rr[None], tol, axes_keep=(0,),
+                            what="R rows " + what)
+    del x, Bm, Cm, q, e, z, y_ssd, mem, hl, y, lse, yR
     torch.cuda.empty_cache()
 
 

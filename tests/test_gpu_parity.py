@@ -1,7 +1,11 @@
 """GPU parity: the HIP path through the C ABI against the fp64 CPU oracle on
 the same seeded inputs.  Tolerance (per (b, h) slice, max|gpu - ref| / max|ref|):
-1e-4 for fp32 storage, 2e-2 for bf16 storage with fp32 accumulation; LSE as
-|d| <= tol (1 + |ref|) on finite entries and -inf exactly where it must be."""
+1e-4 for fp32 storage, 2e-2 for bf16 storage with fp32 accumulation.  The SMA
+readout R is checked on its own: every SMA case runs a second time with
+y_ssd = 0 and one constant gate z = 2, so y = SiLU(2) R and the per-slice
+metric sees R alone.  LSE: every finite entry within the per-entry bound of
+tests.helpers (|d| <= 1e-4 (1 + |ref|) in fp32, |d| <= 0.1 in bf16) and -inf
+exactly where the reference has no history."""
 import math
 
 import numpy as np
@@ -122,10 +126,29 @@ def test_sma_matches_explicit_softmax(w):
     y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, w.chunk)
     tol = TOL[w.dtype]
     assert_close_slices(to_np(y), y_ref, tol, what="y")
-    assert_lse_close(to_np(lse), lse_ref, tol)
+    assert_lse_close(to_np(lse), lse_ref, w.dtype)
     # first chunk: y == y_ssd bitwise, LSE = -inf
     S = w.chunk
     np.testing.assert_array_equal(to_np(y)[:, :S], y_ssd[:, :S].astype(np.float64))
+    check_readout(w, d, mem)
+
+
+def readout_inputs(w, d):
+    """y_ssd = 0 and one gate z = 2 for every token and head: y = SiLU(2) R."""
+    z2 = np.full_like(d["z"], 2.0)
+    return np.zeros((w.batch, w.seqlen, w.nheads, w.headdim), dtype=np.float32), z2
+
+
+def check_readout(w, d, mem, **kw):
+    """The SMA readout R alone, per (b, h) slice (tokens of the first chunk,
+    R = 0, are exact zeros on both sides)."""
+    ys0, z2 = readout_inputs(w, d)
+    y, _ = run_sma(w, d, mem, ys0, z=z2, **kw)
+    okw = {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in kw.items()}
+    y_ref, _ = oracle.sma(d["q"], d["e"], d["Cm"], mem, z2, ys0, w.chunk, **okw)
+    got = to_np(y)
+    assert np.all(got[:, :w.chunk] == 0.0)
+    assert_close_slices(got, y_ref, TOL[w.dtype], what="R (y_ssd = 0, z = 2)")
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
@@ -140,7 +163,8 @@ def test_sma_options(dtype):
     y, lse = run_sma(w, d, mem, y_ssd, normalize=False)
     y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, 64, normalize=False)
     assert_close_slices(to_np(y), y_ref, tol, what="y (normalize=0)")
-    assert_lse_close(to_np(lse), lse_ref, tol)
+    assert_lse_close(to_np(lse), lse_ref, dtype)
+    check_readout(w, d, mem, normalize=False)
     # norm weights + in place
     rng = np.random.default_rng(3)
     qw = rng.uniform(0.5, 1.5, 64).astype(np.float32)
@@ -149,7 +173,8 @@ def test_sma_options(dtype):
     y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, 64, q_norm_w=qw,
                                 e_norm_w=ew)
     assert_close_slices(to_np(y), y_ref, tol, what="y (weights, in place)")
-    assert_lse_close(to_np(lse), lse_ref, tol)
+    assert_lse_close(to_np(lse), lse_ref, dtype)
+    check_readout(w, d, mem, q_norm_w=f32_dev(qw), e_norm_w=f32_dev(ew))
 
 
 def test_sma_gate_zero_returns_ssm_output():
@@ -176,7 +201,7 @@ def test_forward_end_to_end(w):
                          w.chunk)
     tol = TOL[w.dtype]
     assert_close_slices(to_np(y), ref["y"], tol, what="y")
-    assert_lse_close(to_np(lse), ref["lse"], tol)
+    assert_lse_close(to_np(lse), ref["lse"], w.dtype)
 
 
 def test_scan_and_sma_are_deterministic():
@@ -207,6 +232,8 @@ def test_full_size_forward_sampled():
     y_ssd, mem, hl = run_scan(w, d)
     q, e, Cm, z = (to_dev(d[k], w.dtype) for k in ("q", "e", "Cm", "z"))
     y, lse = dart.sma_fwd(q, e, Cm, mem, z, y_ssd, w.chunk)
+    ys0, z2 = readout_inputs(w, d)
+    yR, _ = dart.sma_fwd(q, e, Cm, mem, to_dev(z2, w.dtype), to_dev(ys0, w.dtype), w.chunk)
     torch.cuda.synchronize()
     tol = TOL[w.dtype]
     S, L = w.chunk, w.seqlen
@@ -235,7 +262,13 @@ def test_full_size_forward_sampled():
         got_y = to_np(y[b, :, h][ti])
         got_l = to_np(lse[b, :, h][ti])
         assert_close_slices(got_y[None], yr[None], tol, axes_keep=(0,), what="y rows " + what)
-        assert_lse_close(got_l[None], lr[None], tol, what="lse rows " + what, axes_keep=(0,))
+        assert_lse_close(got_l[None], lr[None], w.dtype, what="lse rows " + what)
+        # the readout alone on the same rows (y_ssd = 0, z = 2)
+        rr, _ = oracle.sma_rows(d["q"][b:b + 1], d["e"][b:b + 1], d["Cm"][b:b + 1],
+                                to_np(mem[b:b + 1, :, h:h + 1]), z2[b:b + 1, :, h:h + 1],
+                                ys0[b:b + 1, :, h:h + 1], S, rows)
+        assert_close_slices(to_np(yR[b, :, h][ti])[None], rr[None], tol, axes_keep=(0,),
+                            what="R rows " + what)
 
 
 # --------------------------------------------------------------------------- #
