@@ -312,6 +312,31 @@ dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, i
                              void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * dart_decode_step for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same step, arguments and errors as dart_decode_step, with
+ * no workspace argument.  Its partial softmax statistics and SSM readout go
+ * to a fixed scratch array the library holds on each device it runs on, of
+ * DART_DECODE_NOALLOC_SCRATCH_BYTES (16 MiB), kept until the process ends;
+ * the step needs B * H * (nsplit * (P + 2) + P) * 4 bytes of it, nsplit the
+ * number of memory splits of the step (at most ceil(m / 8)), e.g. 1.6 MB for
+ * B = 64, H = 32 and 256 cached memories.  A step that needs more returns
+ * DART_ERR_UNSUPPORTED before any launch.  The scratch is that of the device
+ * current on the calling thread, which must be the device of `stream` and of
+ * every buffer.  Every call on a device shares its scratch: calls that
+ * overlap in time on one device (several streams, or threads without
+ * ordering) race, so issue them in one stream order.  Nothing in the scratch
+ * needs clearing: every value a step reads was written by that step.  This
+ * function allocates nothing.
+ */
+#define DART_DECODE_NOALLOC_SCRATCH_BYTES (16u << 20)
+dart_status dart_decode_step_noalloc(const dart_dims* dims, const dart_sma_opts* opts, int64_t pos,
+                                     const void* x, const float* dt, const float* A,
+                                     const void* Bm, const void* Cm, const void* q, const void* e,
+                                     const void* z, float* h_state, float* chunk_acc,
+                                     void* mem_cache, void* y, void* stream);
+
+/*
  * The decode step for a ragged batch: row b of the batch is at its own
  * 0-based position pos[b] and runs steps 1-6 of dart_decode_step at that
  * position (reset, append and the number m_b = floor(pos[b]/S) of memories it

@@ -343,6 +343,49 @@ dart_status dart_decode_step(const dart_dims* dims, const dart_sma_opts* opts, i
                       "dart_decode_step launch");
 }
 
+dart_status dart_decode_step_noalloc(const dart_dims* dims, const dart_sma_opts* opts, int64_t pos,
+                                     const void* x, const float* dt, const float* A,
+                                     const void* Bm, const void* Cm, const void* q, const void* e,
+                                     const void* z, float* h_state, float* chunk_acc,
+                                     void* mem_cache, void* y, void* stream) {
+    dart::Shape s;
+    dart_status st = make_shape(dims, false, s);
+    if (st != DART_OK) return st;
+    st = check_opts(opts);
+    if (st != DART_OK) return st;
+    if (s.Mcap < 1) return fail(DART_ERR_INVALID_ARG, "decode needs mem_capacity >= 1");
+    if (pos < 0) return fail(DART_ERR_INVALID_ARG, "pos must be >= 0 (got %lld)", (long long)pos);
+    const int64_t m = pos / s.S;
+    if (m > s.Mcap)
+        return fail(DART_ERR_INVALID_ARG, "pos %lld needs %lld cached memories > capacity %lld",
+                    (long long)pos, (long long)m, (long long)s.Mcap);
+    if (pos % s.S == s.S - 1 && m >= s.Mcap)
+        return fail(DART_ERR_INVALID_ARG, "pos %lld closes chunk %lld but the cache holds %lld memories",
+                    (long long)pos, (long long)m, (long long)s.Mcap);
+    REQUIRE_PTR(x);
+    REQUIRE_PTR(dt);
+    REQUIRE_PTR(A);
+    REQUIRE_PTR(Bm);
+    REQUIRE_PTR(Cm);
+    REQUIRE_PTR(q);
+    REQUIRE_PTR(e);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(h_state);
+    REQUIRE_PTR(chunk_acc);
+    REQUIRE_PTR(mem_cache);
+    REQUIRE_PTR(y);
+    const size_t need = dart::decode_noalloc_scratch_bytes(s, pos);
+    if (need > (size_t)DART_DECODE_NOALLOC_SCRATCH_BYTES)
+        return fail(DART_ERR_UNSUPPORTED,
+                    "this step needs %zu bytes of scratch; the library's fixed scratch holds %zu "
+                    "(use dart_decode_step with a workspace)",
+                    need, (size_t)DART_DECODE_NOALLOC_SCRATCH_BYTES);
+    const dart::SmaArgs a = sma_args(opts);
+    return hip_status(dart::launch_decode_noalloc(s, a, pos, x, dt, A, Bm, Cm, q, e, z, h_state,
+                                                  chunk_acc, mem_cache, y, (hipStream_t)stream),
+                      "dart_decode_step_noalloc launch");
+}
+
 dart_status dart_decode_step_ragged(const dart_dims* dims, const dart_sma_opts* opts,
                                     const int64_t* pos, int64_t pos_max, const void* x,
                                     const float* dt, const float* A, const void* Bm,

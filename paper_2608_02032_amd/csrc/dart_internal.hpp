@@ -87,6 +87,14 @@ hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const in
                          const void* Cm, const void* q, const void* e, const void* z,
                          float* h_state, float* chunk_acc, void* mem, void* y, void* ws,
                          hipStream_t st);
+// The allocation-free decode step: the same kernels with the library's fixed
+// device scratch (DART_DECODE_NOALLOC_SCRATCH_BYTES per device) as the
+// workspace, laid out for this step's own split count.
+size_t decode_noalloc_scratch_bytes(const Shape& s, int64_t pos);
+hipError_t launch_decode_noalloc(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
+                                 const float* dt, const float* A, const void* Bm, const void* Cm,
+                                 const void* q, const void* e, const void* z, float* h_state,
+                                 float* chunk_acc, void* mem, void* y, hipStream_t st);
 hipError_t launch_decode_handoff(const Shape& s, const void* mem, const float* h_last,
                                  const int64_t* lengths, float* h_state, float* chunk_acc,
                                  hipStream_t st);

@@ -26,6 +26,9 @@
 #include "dart_internal.hpp"
 
 #include <cstdlib>
+#include <mutex>
+
+#include "dart.h"
 
 namespace dart {
 namespace {
@@ -363,15 +366,26 @@ __global__ __launch_bounds__(kThreads) void k_decode_state_merge(
     y[(b * H + h) * kP + p] = from_f<T>(yssd[(b * H + h) * kP + p] + silu(zz) * R);
 }
 
+// Number of splits of a step that attends m memories.
+inline int decode_splits(const Shape& s, int64_t m) {
+    if (m <= 0) return 0;
+    const int mps = decode_mps(s.B * s.H, m);
+    return (int)((m + mps - 1) / mps);
+}
+
+// nsplit_stride: the partials' split stride in the workspace (0: the
+// workspace's worst case over positions that fit the cache).
 template <typename T, int N>
 hipError_t run_decode(const Shape& s, const SmaArgs& a, int64_t pos, const int64_t* pos_rows,
                       const void* x, const float* dt, const float* A, const void* Bm,
                       const void* Cm, const void* q, const void* e, const void* z, float* h_state,
-                      float* chunk_acc, void* mem, void* y, void* ws, hipStream_t st) {
+                      float* chunk_acc, void* mem, void* y, void* ws, int nsplit_stride,
+                      hipStream_t st) {
     // ragged batches size the grid for the largest position (pos = pos_lim)
     const int64_t m = pos / s.S;
     const int mps = decode_mps(s.B * s.H, m);
-    const int nsplit_cap = (int)((s.Mcap + kMinMPS - 1) / kMinMPS);
+    const int nsplit_cap =
+        nsplit_stride > 0 ? nsplit_stride : (int)((s.Mcap + kMinMPS - 1) / kMinMPS);
     float* part = reinterpret_cast<float*>(ws);
     float* yssd = part + decode_part_floats(s.B, s.H, nsplit_cap);
     if (m > 0) {
@@ -395,13 +409,41 @@ template <typename T>
 hipError_t run_decode_n(const Shape& s, const SmaArgs& a, int64_t pos, const int64_t* pr,
                         const void* x, const float* dt, const float* A, const void* Bm,
                         const void* Cm, const void* q, const void* e, const void* z, float* hs,
-                        float* ca, void* mem, void* y, void* ws, hipStream_t st) {
+                        float* ca, void* mem, void* y, void* ws, int nss, hipStream_t st) {
     switch (s.N) {
-        case 32: return run_decode<T, 32>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
-        case 64: return run_decode<T, 64>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
-        case 128: return run_decode<T, 128>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, st);
+        case 32: return run_decode<T, 32>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
+        case 64: return run_decode<T, 64>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
+        case 128: return run_decode<T, 128>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
     }
     return hipErrorInvalidValue;
+}
+
+// Fixed device scratch of the allocation-free decode step: the partials
+// [B][H][nsplit][P+2] of that step's own split count and y_ssd [B][H][P]
+// (float).  Each device holds its own copy; host code reaches it only through
+// the address hipGetSymbolAddress returns on that device.
+static __device__ __align__(256) char scratch[DART_DECODE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address, looked up once per device (with that
+// device current) and kept.
+hipError_t scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 // Prefill -> decode handoff for row b of length L_b (lengths[b]; rows with
@@ -468,9 +510,30 @@ hipError_t launch_decode(const Shape& s, const SmaArgs& a, int64_t pos, const in
                          hipStream_t st) {
     if (s.dtype == 1)
         return run_decode_n<bf16>(s, a, pos, pos_rows, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc,
-                                  mem, y, ws, st);
+                                  mem, y, ws, 0, st);
     return run_decode_n<float>(s, a, pos, pos_rows, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem,
-                               y, ws, st);
+                               y, ws, 0, st);
+}
+
+size_t decode_noalloc_scratch_bytes(const Shape& s, int64_t pos) {
+    const int ns = decode_splits(s, pos / s.S);
+    return sizeof(float) * (decode_part_floats(s.B, s.H, ns > 0 ? ns : 1) + (size_t)s.B * s.H * s.P);
+}
+
+hipError_t launch_decode_noalloc(const Shape& s, const SmaArgs& a, int64_t pos, const void* x,
+                                 const float* dt, const float* A, const void* Bm, const void* Cm,
+                                 const void* q, const void* e, const void* z, float* h_state,
+                                 float* chunk_acc, void* mem, void* y, hipStream_t st) {
+    void* ws = nullptr;
+    const hipError_t err = scratch_address(&ws);
+    if (err != hipSuccess) return err;
+    const int ns = decode_splits(s, pos / s.S);
+    const int nss = ns > 0 ? ns : 1;
+    if (s.dtype == 1)
+        return run_decode_n<bf16>(s, a, pos, nullptr, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc,
+                                  mem, y, ws, nss, st);
+    return run_decode_n<float>(s, a, pos, nullptr, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem,
+                               y, ws, nss, st);
 }
 
 hipError_t launch_decode_handoff(const Shape& s, const void* mem, const float* h_last,

@@ -47,7 +47,7 @@ EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspa
            "dart_sma_fwd", "dart_sma_bwd_workspace_bytes", "dart_sma_bwd",
            "dart_ssd_bwd_workspace_bytes", "dart_ssd_bwd",
            "dart_conv1d_silu", "dart_dt_softplus", "dart_gated_rmsnorm",
-           "dart_decode_workspace_bytes", "dart_decode_step",
+           "dart_decode_workspace_bytes", "dart_decode_step", "dart_decode_step_noalloc",
            "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
            "dart_profile_enable", "dart_profile_filter", "dart_profile_flush", "dart_profile_count",
            "dart_profile_name", "dart_profile_total_ms", "dart_profile_launches",
@@ -98,6 +98,8 @@ def load_library(path: str = LIB_PATH):
         lib.dart_decode_workspace_bytes.restype = sz
         lib.dart_decode_step.argtypes = [D, O, i64, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
         lib.dart_decode_step.restype = st
+        lib.dart_decode_step_noalloc.argtypes = [D, O, i64] + [P] * 13
+        lib.dart_decode_step_noalloc.restype = st
         lib.dart_decode_step_ragged.argtypes = [D, O, P, i64, P, P, P, P, P, P, P, P, P, P, P, P,
                                                 P, sz, P]
         lib.dart_decode_step_ragged.restype = st
@@ -433,6 +435,30 @@ def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache, c
                                _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(q), _ptr(e), _ptr(z),
                                _ptr(h_state), _ptr(chunk_acc), _ptr(mem_cache), _ptr(y),
                                _ptr(workspace), workspace.numel(), _stream(stream)))
+    return y
+
+
+def decode_step_noalloc(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache, chunk,
+                        eps=DEFAULT_EPS, normalize=True, q_norm_w=None, e_norm_w=None, y=None,
+                        stream=None):
+    """dart_decode_step_noalloc: the decode step with the library's fixed
+    device scratch instead of a workspace (y is allocated here unless given)."""
+    torch = _torch()
+    lib = load_library()
+    B_, H, P = x.shape
+    G, N = Bm.shape[1], Bm.shape[2]
+    dtype = _dtype_code(x)
+    for t, nm in ((dt, "dt"), (A, "A"), (h_state, "h_state"), (chunk_acc, "chunk_acc")):
+        _check_f32(t, nm)
+    z_per_head = 1 if z.dim() == 2 else 0
+    dims = make_dims(B_, 0, H, P, N, chunk, dtype, G, mem_cache.shape[1])
+    opts = SmaOpts(float(eps), _ptr(q_norm_w), _ptr(e_norm_w), int(bool(normalize)), z_per_head)
+    if y is None:
+        y = torch.empty_like(x)
+    check(lib.dart_decode_step_noalloc(ctypes.byref(dims), ctypes.byref(opts), int(pos), _ptr(x),
+                                       _ptr(dt), _ptr(A), _ptr(Bm), _ptr(Cm), _ptr(q), _ptr(e),
+                                       _ptr(z), _ptr(h_state), _ptr(chunk_acc), _ptr(mem_cache),
+                                       _ptr(y), _stream(stream)))
     return y
 
 

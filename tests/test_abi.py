@@ -264,3 +264,19 @@ def test_block_entry_points_reject_bad_arguments(lib):
     assert lib.dart_gated_rmsnorm(2, 64, 64, 1, 8, 16, 64, None, 1e-6, 16, None) == E
     assert b"aligned" in lib.dart_last_error()
     assert lib.dart_gated_rmsnorm(2, 64, 64, 1, 16, 16, 64, None, 0.0, 16, None) == E
+
+
+def test_noalloc_decode_rejects_a_step_beyond_its_scratch(lib):
+    """dart_decode_step_noalloc refuses, before any launch, a step whose
+    partials would not fit the fixed scratch: B = 4096, H = 64 needs
+    4096 * 64 * (66 + 64) * 4 bytes > 16 MiB even for one split."""
+    d = dims(batch=4096, nheads=64, seqlen=0, mem_capacity=4)
+    opts = dart.SmaOpts(1e-6, None, None, 1, 1)
+    buf = ctypes.create_string_buffer(64)
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    st = lib.dart_decode_step_noalloc(ctypes.byref(d), ctypes.byref(opts), 64, *([p] * 12), None)
+    assert st == 2, lib.dart_last_error()
+    assert b"scratch" in lib.dart_last_error()
+    # a NULL required pointer is still an argument error, found first
+    st = lib.dart_decode_step_noalloc(ctypes.byref(d), ctypes.byref(opts), 64, None, *([p] * 11), None)
+    assert st == 1
