@@ -31,8 +31,11 @@
  *    and enqueues nothing; a failed launch returns DART_ERR_HIP.
  *    dart_last_error() gives a message for the last non-OK status of the
  *    calling thread.  Numeric contracts (dt > 0, A < 0) are the caller's.
- *  - Supported shapes: P = 64; N in {32, 64, 128}; S in {64, 128, 256};
- *    any L >= 1 (a partial last chunk is allowed); any B, H with H % G == 0.
+ *  - Supported shapes: P = 64; N in {16, 32, 64, 128}; 1 <= S <= 4096; any
+ *    L >= 1 (a partial last chunk is allowed); any B, H <= 65535 with
+ *    H % G == 0.  N in {32, 64, 128} with S in {64, 128, 256} run the tuned
+ *    MFMA kernels; every other shape runs generic fp32 kernels (the paper
+ *    trains at S = 16, N in {16, 64} and evaluates at S = 32 and 64).
  */
 #ifndef DART_H
 #define DART_H
@@ -273,6 +276,52 @@ dart_status dart_dt_softplus(int64_t rows, int32_t nheads, int64_t row_stride, i
 dart_status dart_gated_rmsnorm(int64_t rows, int32_t dim, int32_t group, int32_t dtype,
                                const void* y, const void* z, int64_t z_row_stride,
                                const float* weight, float eps, void* out, void* stream);
+
+/*
+ * Backward of the three block kernels above, for a loss whose gradient with
+ * respect to the kernel's output is `dout` (float).  Gradients are float and
+ * overwrite their outputs; the sums over tokens or rows (weights, biases) are
+ * formed from per-block partials in the workspace in a fixed order
+ * (deterministic).  The forward inputs are passed again (nothing of the
+ * forward call is kept).
+ *
+ * dart_conv1d_silu_bwd: with u = bias + sum_k w_k in[t-3+k] (the forward's
+ * pre-activation) and du = dout SiLU'(u):
+ *   din[t] = sum_k w_k du[t+3-k]   [B][L][din_row_stride] (channel c at c)
+ *   dweight[c][k] = sum_{b,t} du in[t-3+k]   [C][4];   dbias [C] or NULL
+ *   dstate_in [B][C][3] or NULL: the gradient of the carried state
+ *   (in[-3..-1]; zero-state inputs get it too)
+ *   in, weight, bias, state_in, row_stride, dtype as in dart_conv1d_silu.
+ */
+size_t dart_conv1d_silu_bwd_workspace_bytes(int64_t batch, int64_t seqlen, int32_t channels);
+dart_status dart_conv1d_silu_bwd(int64_t batch, int64_t seqlen, int32_t channels,
+                                 int64_t row_stride, int32_t dtype, const void* in,
+                                 const float* weight, const float* bias, const float* state_in,
+                                 const float* dout, float* din, int64_t din_row_stride,
+                                 float* dweight, float* dbias, float* dstate_in, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* dart_dt_softplus_bwd: draw = ddt sigmoid(raw + bias) [rows][draw_row_stride]
+ * (head h at h), dbias [H] = sum over rows, or NULL.  ddt [rows][H] float. */
+size_t dart_dt_softplus_bwd_workspace_bytes(int64_t rows, int32_t nheads);
+dart_status dart_dt_softplus_bwd(int64_t rows, int32_t nheads, int64_t row_stride, int32_t dtype,
+                                 const void* raw, const float* bias, const float* ddt, float* draw,
+                                 int64_t draw_row_stride, float* dbias, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+/* dart_gated_rmsnorm_bwd: with u = y SiLU(z), inv = (mean over the group of
+ * u^2 + eps)^-1/2 and g = dout (.) weight:
+ *   du = inv g - u inv^3 (g . u) / group,  dy = du SiLU(z)  [rows][dim],
+ *   dz = du y SiLU'(z)  [rows][dz_row_stride],
+ *   dweight [dim] = sum over rows of dout u inv, or NULL.
+ * Groups of at most 2048 channels; y, z, dout, dy, dz 32-byte aligned; row
+ * strides multiples of 8. */
+size_t dart_gated_rmsnorm_bwd_workspace_bytes(int64_t rows, int32_t dim);
+dart_status dart_gated_rmsnorm_bwd(int64_t rows, int32_t dim, int32_t group, int32_t dtype,
+                                   const void* y, const void* z, int64_t z_row_stride,
+                                   const float* weight, float eps, const float* dout, float* dy,
+                                   float* dz, int64_t dz_row_stride, float* dweight,
+                                   void* workspace, size_t workspace_bytes, void* stream);
 
 /* Bytes of workspace dart_decode_step needs (dims->seqlen is ignored; the
  * worst case over positions that fit dims->mem_capacity is returned). */

@@ -68,6 +68,12 @@ def _load():
         lib.dart_oracle_dt_softplus.restype = None
         lib.dart_oracle_gated_rmsnorm.argtypes = [_I64, _INT, _INT, ctypes.c_double, _D, _D, _D, _D]
         lib.dart_oracle_gated_rmsnorm.restype = None
+        lib.dart_oracle_conv1d_silu_bwd.argtypes = [_I64, _I64, _INT, _I64] + [_D] * 9
+        lib.dart_oracle_conv1d_silu_bwd.restype = None
+        lib.dart_oracle_dt_softplus_bwd.argtypes = [_I64, _INT] + [_D] * 5
+        lib.dart_oracle_dt_softplus_bwd.restype = None
+        lib.dart_oracle_gated_rmsnorm_bwd.argtypes = [_I64, _INT, _INT, ctypes.c_double] + [_D] * 7
+        lib.dart_oracle_gated_rmsnorm_bwd.restype = None
         lib.dart_oracle_chunk_memories.argtypes = [_I64, _I64, _INT, _INT, _INT, _INT, _INT, _I64,
                                                    _D, _D, _D, _D, _D]
         lib.dart_oracle_chunk_memories.restype = None
@@ -313,4 +319,45 @@ def gated_rmsnorm(y, z, w=None, group=None, eps=1e-6):
     out = np.empty_like(y)
     _load().dart_oracle_gated_rmsnorm(y.size // D, D, group, float(eps), _ptr(y), _ptr(z), _ptr(w),
                                       _ptr(out))
+    return out
+
+
+def conv1d_silu_bwd(inp, w, dout, bias=None, state=None, channels=None):
+    """Gradients of conv1d_silu for a loss with output gradient dout [B][L][C]:
+    returns {"din" [B][L][C], "dw" [C][4], "db" [C], "dstate" [B][C][3]}."""
+    inp, w, dout = _f64(inp), _f64(w), _f64(dout)
+    B_, L, R = inp.shape
+    C = R if channels is None else int(channels)
+    bias = None if bias is None else _f64(bias)
+    state = None if state is None else _f64(state)
+    out = {"din": np.empty((B_, L, C)), "dw": np.empty((C, 4)), "db": np.empty((C,)),
+           "dstate": np.empty((B_, C, 3))}
+    _load().dart_oracle_conv1d_silu_bwd(B_, L, C, R, _ptr(inp), _ptr(w), _ptr(bias), _ptr(state),
+                                        _ptr(dout), _ptr(out["din"]), _ptr(out["dw"]),
+                                        _ptr(out["db"]), _ptr(out["dstate"]))
+    return out
+
+
+def dt_softplus_bwd(raw, ddt, bias=None):
+    """Gradients of dt_softplus: returns (draw like raw, dbias [H])."""
+    raw, ddt = _f64(raw), _f64(ddt)
+    H = raw.shape[-1]
+    bias = None if bias is None else _f64(bias)
+    draw = np.empty_like(raw)
+    dbias = np.empty((H,))
+    _load().dart_oracle_dt_softplus_bwd(raw.size // H, H, _ptr(raw), _ptr(bias), _ptr(ddt),
+                                        _ptr(draw), _ptr(dbias))
+    return draw, dbias
+
+
+def gated_rmsnorm_bwd(y, z, dout, w=None, group=None, eps=1e-6):
+    """Gradients of gated_rmsnorm: returns {"dy", "dz" like y, "dw" [D]}."""
+    y, z, dout = _f64(y), _f64(z), _f64(dout)
+    D = y.shape[-1]
+    group = D if group is None else int(group)
+    w = None if w is None else _f64(w)
+    out = {"dy": np.empty_like(y), "dz": np.empty_like(y), "dw": np.empty((D,))}
+    _load().dart_oracle_gated_rmsnorm_bwd(y.size // D, D, group, float(eps), _ptr(y), _ptr(z),
+                                          _ptr(w), _ptr(dout), _ptr(out["dy"]), _ptr(out["dz"]),
+                                          _ptr(out["dw"]))
     return out

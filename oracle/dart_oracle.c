@@ -807,3 +807,88 @@ void dart_oracle_gated_rmsnorm(int64_t rows, int D, int group, double eps, const
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Backward of the three block definitions above (chain rule, literal loops) */
+/* for a loss whose gradient with respect to the output is dout.             */
+/* ------------------------------------------------------------------------ */
+
+/* Convolution: u[t] = bias + sum_k w[k] in[t-3+k] (in[s<0] from the carried */
+/* state), out = SiLU(u).  du = dout SiLU'(u); every input term of u gets    */
+/* du times its weight; the weights get du times their input.               */
+void dart_oracle_conv1d_silu_bwd(int64_t B, int64_t L, int C, int64_t stride, const double* in,
+                                 const double* w, const double* bias, const double* st_in,
+                                 const double* dout, double* din, double* dw, double* db,
+                                 double* dst) {
+    for (size_t k = 0; k < (size_t)B * L * C; ++k) din[k] = 0.0;
+    for (size_t k = 0; k < (size_t)C * 4; ++k) dw[k] = 0.0;
+    for (int c = 0; c < C; ++c) db[c] = 0.0;
+    for (size_t k = 0; k < (size_t)B * C * 3; ++k) dst[k] = 0.0;
+    for (int64_t b = 0; b < B; ++b)
+        for (int c = 0; c < C; ++c)
+            for (int64_t t = 0; t < L; ++t) {
+                double u = bias ? bias[c] : 0.0;
+                for (int k = 0; k < 4; ++k) {
+                    const int64_t s = t - 3 + k;
+                    const double v = s >= 0 ? in[((size_t)b * L + s) * stride + c]
+                                            : (st_in ? st_in[((size_t)b * C + c) * 3 + (3 + s)] : 0.0);
+                    u += w[(size_t)c * 4 + k] * v;
+                }
+                const double sg = 1.0 / (1.0 + exp(-u));
+                const double du = dout[((size_t)b * L + t) * C + c] * sg * (1.0 + u * (1.0 - sg));
+                db[c] += du;
+                for (int k = 0; k < 4; ++k) {
+                    const int64_t s = t - 3 + k;
+                    const double v = s >= 0 ? in[((size_t)b * L + s) * stride + c]
+                                            : (st_in ? st_in[((size_t)b * C + c) * 3 + (3 + s)] : 0.0);
+                    dw[(size_t)c * 4 + k] += du * v;
+                    if (s >= 0)
+                        din[((size_t)b * L + s) * C + c] += du * w[(size_t)c * 4 + k];
+                    else
+                        dst[((size_t)b * C + c) * 3 + (3 + s)] += du * w[(size_t)c * 4 + k];
+                }
+            }
+}
+
+/* Step sizes: dt = softplus(raw + bias): d raw = ddt sigmoid(raw + bias),   */
+/* d bias = its sum over rows.                                              */
+void dart_oracle_dt_softplus_bwd(int64_t rows, int H, const double* raw, const double* bias,
+                                 const double* ddt, double* draw, double* dbias) {
+    for (int h = 0; h < H; ++h) dbias[h] = 0.0;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int h = 0; h < H; ++h) {
+            const double v = raw[(size_t)r * H + h] + (bias ? bias[h] : 0.0);
+            const double g = ddt[(size_t)r * H + h] / (1.0 + exp(-v));
+            draw[(size_t)r * H + h] = g;
+            dbias[h] += g;
+        }
+}
+
+/* Gated RMSNorm: out_k = u_k inv w_k, u = y SiLU(z), inv = (mean u^2 +     */
+/* eps)^-1/2 over the group.  d u_k = inv w_k dout_k - u_k inv^3 (sum_j     */
+/* w_j dout_j u_j) / group; dy = du SiLU(z); dz = du y SiLU'(z);            */
+/* dw_k = sum over rows of dout_k u_k inv.                                  */
+void dart_oracle_gated_rmsnorm_bwd(int64_t rows, int D, int group, double eps, const double* y,
+                                   const double* z, const double* w, const double* dout,
+                                   double* dy, double* dz, double* dw) {
+    for (int k = 0; k < D; ++k) dw[k] = 0.0;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int g0 = 0; g0 < D; g0 += group) {
+            double ss = 0.0, gu = 0.0;
+            for (int k = g0; k < g0 + group; ++k) {
+                const double u = y[(size_t)r * D + k] * silu(z[(size_t)r * D + k]);
+                ss += u * u;
+                gu += (w ? w[k] : 1.0) * dout[(size_t)r * D + k] * u;
+            }
+            const double inv = 1.0 / sqrt(ss / group + eps);
+            for (int k = g0; k < g0 + group; ++k) {
+                const double zz = z[(size_t)r * D + k];
+                const double u = y[(size_t)r * D + k] * silu(zz);
+                const double du = inv * (w ? w[k] : 1.0) * dout[(size_t)r * D + k] -
+                                  u * inv * inv * inv * gu / group;
+                dy[(size_t)r * D + k] = du * silu(zz);
+                dz[(size_t)r * D + k] = du * y[(size_t)r * D + k] * silu_grad(zz);
+                dw[k] += dout[(size_t)r * D + k] * u * inv;
+            }
+        }
+}

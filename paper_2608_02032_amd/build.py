@@ -21,7 +21,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libdart.so")
 ARCH = "gfx950"
 
-SOURCES = ["scan.hip", "sma.hip", "sma_bwd.hip", "scan_bwd.hip", "decode.hip", "block.hip", "dart_api.cpp", "profile.cpp"]
+SOURCES = ["scan.hip", "sma.hip", "sma_bwd.hip", "scan_bwd.hip", "decode.hip", "block.hip", "generic.hip",
+           "dart_api.cpp", "profile.cpp"]
 
 COMMON_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,

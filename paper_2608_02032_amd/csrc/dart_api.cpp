@@ -47,10 +47,10 @@ dart_status make_shape(const dart_dims* d, bool need_seqlen, dart::Shape& s) {
     if (d->mem_capacity < 0) return fail(DART_ERR_INVALID_ARG, "mem_capacity must be >= 0");
     if (d->headdim != 64)
         return fail(DART_ERR_UNSUPPORTED, "headdim %d not supported (the library has kernels for 64)", d->headdim);
-    if (d->dstate != 32 && d->dstate != 64 && d->dstate != 128)
-        return fail(DART_ERR_UNSUPPORTED, "dstate %d not supported (32, 64 or 128)", d->dstate);
-    if (d->chunk != 64 && d->chunk != 128 && d->chunk != 256)
-        return fail(DART_ERR_UNSUPPORTED, "chunk %d not supported (64, 128 or 256)", d->chunk);
+    if (d->dstate != 16 && d->dstate != 32 && d->dstate != 64 && d->dstate != 128)
+        return fail(DART_ERR_UNSUPPORTED, "dstate %d not supported (16, 32, 64 or 128)", d->dstate);
+    if (d->chunk > 4096)
+        return fail(DART_ERR_UNSUPPORTED, "chunk %d not supported (at most 4096)", d->chunk);
     if (d->batch > 65535 || d->nheads > 65535)
         return fail(DART_ERR_UNSUPPORTED, "batch and nheads must be <= 65535");
     s.B = d->batch;
@@ -293,6 +293,106 @@ dart_status dart_gated_rmsnorm(int64_t rows, int32_t dim, int32_t group, int32_t
     return hip_status(dart::launch_gated_rmsnorm(dtype, rows, dim, group, y, z, z_row_stride, weight,
                                                  eps, out, (hipStream_t)stream),
                       "dart_gated_rmsnorm launch");
+}
+
+size_t dart_conv1d_silu_bwd_workspace_bytes(int64_t batch, int64_t seqlen, int32_t channels) {
+    if (batch < 1 || seqlen < 1 || channels < 1) return 0;
+    return dart::conv1d_silu_bwd_workspace_bytes(batch, seqlen, channels);
+}
+
+dart_status dart_conv1d_silu_bwd(int64_t batch, int64_t seqlen, int32_t channels,
+                                 int64_t row_stride, int32_t dtype, const void* in,
+                                 const float* weight, const float* bias, const float* state_in,
+                                 const float* dout, float* din, int64_t din_row_stride,
+                                 float* dweight, float* dbias, float* dstate_in, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+    if (batch < 1 || seqlen < 1 || channels < 1)
+        return fail(DART_ERR_INVALID_ARG, "batch, seqlen and channels must be >= 1");
+    if (batch > 65535 || (seqlen + 31) / 32 > 65535)
+        return fail(DART_ERR_UNSUPPORTED, "batch <= 65535 and seqlen <= 32 * 65535");
+    if (row_stride < channels || din_row_stride < channels)
+        return fail(DART_ERR_INVALID_ARG, "row strides must be >= channels (%d)", channels);
+    if (dtype != DART_FP32 && dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", dtype);
+    REQUIRE_PTR(in);
+    REQUIRE_PTR(weight);
+    REQUIRE_PTR(dout);
+    REQUIRE_PTR(din);
+    REQUIRE_PTR(dweight);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::conv1d_silu_bwd_workspace_bytes(batch, seqlen, channels);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return hip_status(dart::launch_conv1d_silu_bwd(dtype, batch, seqlen, channels, row_stride, in,
+                                                   weight, bias, state_in, dout, din,
+                                                   din_row_stride, dweight, dbias, dstate_in,
+                                                   workspace, (hipStream_t)stream),
+                      "dart_conv1d_silu_bwd launch");
+}
+
+size_t dart_dt_softplus_bwd_workspace_bytes(int64_t rows, int32_t nheads) {
+    if (rows < 1 || nheads < 1) return 0;
+    return dart::dt_softplus_bwd_workspace_bytes(rows, nheads);
+}
+
+dart_status dart_dt_softplus_bwd(int64_t rows, int32_t nheads, int64_t row_stride, int32_t dtype,
+                                 const void* raw, const float* bias, const float* ddt, float* draw,
+                                 int64_t draw_row_stride, float* dbias, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+    if (rows < 1 || nheads < 1) return fail(DART_ERR_INVALID_ARG, "rows and nheads must be >= 1");
+    if (row_stride < nheads || draw_row_stride < nheads)
+        return fail(DART_ERR_INVALID_ARG, "row strides must be >= nheads (%d)", nheads);
+    if (dtype != DART_FP32 && dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", dtype);
+    if ((rows + 255) / 256 > 65535) return fail(DART_ERR_UNSUPPORTED, "too many rows");
+    REQUIRE_PTR(raw);
+    REQUIRE_PTR(ddt);
+    REQUIRE_PTR(draw);
+    REQUIRE_PTR(workspace);
+    const size_t need = dart::dt_softplus_bwd_workspace_bytes(rows, nheads);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    return hip_status(dart::launch_dt_softplus_bwd(dtype, rows, nheads, raw, row_stride, bias, ddt,
+                                                   draw, draw_row_stride, dbias, workspace,
+                                                   (hipStream_t)stream),
+                      "dart_dt_softplus_bwd launch");
+}
+
+size_t dart_gated_rmsnorm_bwd_workspace_bytes(int64_t rows, int32_t dim) {
+    if (rows < 1 || dim < 1) return 0;
+    return dart::gated_rmsnorm_bwd_workspace_bytes(rows, dim);
+}
+
+dart_status dart_gated_rmsnorm_bwd(int64_t rows, int32_t dim, int32_t group, int32_t dtype,
+                                   const void* y, const void* z, int64_t z_row_stride,
+                                   const float* weight, float eps, const float* dout, float* dy,
+                                   float* dz, int64_t dz_row_stride, float* dweight,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+    if (rows < 1 || dim < 1 || group < 1) return fail(DART_ERR_INVALID_ARG, "rows, dim and group must be >= 1");
+    if (dim % group != 0 || group % 8 != 0)
+        return fail(DART_ERR_INVALID_ARG, "group must divide dim and be a multiple of 8 (dim %d, group %d)", dim, group);
+    if (group > 2048) return fail(DART_ERR_UNSUPPORTED, "the backward supports groups of at most 2048 channels");
+    if (z_row_stride < dim || z_row_stride % 8 != 0 || dz_row_stride < dim || dz_row_stride % 8 != 0)
+        return fail(DART_ERR_INVALID_ARG, "z and dz row strides must be >= dim and multiples of 8");
+    if (dtype != DART_FP32 && dtype != DART_BF16)
+        return fail(DART_ERR_INVALID_ARG, "dtype must be DART_FP32 or DART_BF16 (got %d)", dtype);
+    if (!(eps > 0.0f)) return fail(DART_ERR_INVALID_ARG, "eps must be > 0");
+    REQUIRE_PTR(y);
+    REQUIRE_PTR(z);
+    REQUIRE_PTR(dout);
+    REQUIRE_PTR(dy);
+    REQUIRE_PTR(dz);
+    REQUIRE_PTR(workspace);
+    if (((uintptr_t)y | (uintptr_t)z | (uintptr_t)dout | (uintptr_t)dy | (uintptr_t)dz) % 32 != 0)
+        return fail(DART_ERR_INVALID_ARG, "y, z, dout, dy and dz must be 32-byte aligned");
+    const size_t need = dart::gated_rmsnorm_bwd_workspace_bytes(rows, dim);
+    if (workspace_bytes < need)
+        return fail(DART_ERR_INVALID_ARG, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    if ((rows / 16 + 1) * (dim / group) / 4 + 1 > 2147483647LL) return fail(DART_ERR_UNSUPPORTED, "too many rows");
+    return hip_status(dart::launch_gated_rmsnorm_bwd(dtype, rows, dim, group, y, z, z_row_stride,
+                                                     weight, eps, dout, dy, dz, dz_row_stride,
+                                                     dweight, workspace, (hipStream_t)stream),
+                      "dart_gated_rmsnorm_bwd launch");
 }
 
 size_t dart_decode_workspace_bytes(const dart_dims* dims) {

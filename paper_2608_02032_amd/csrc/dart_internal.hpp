@@ -25,9 +25,36 @@ hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const flo
                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
                        float* h_last, void* ws, hipStream_t st);
 
+// The tuned kernels serve N in {32, 64, 128} with S in {64, 128, 256}; every
+// other supported shape (N in {16, 32, 64, 128}, any S) takes the generic
+// kernels of generic.hip.
+bool tuned_shape(const Shape& s);
+
+// Workspace pieces of the generic scan: per-chunk log decay [B][H][M], the
+// chunk-entry states in the storage dtype (where the tuned scan keeps them),
+// the chunk contributions and the entry states in float, [B][M][H][N][P].
+struct GenScanWs {
+    float* lda;
+    void* states;
+    float* dh32;
+    float* st32;
+};
+hipError_t launch_gscan(const Shape& s, const void* x, const float* dt, const float* A,
+                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
+                        float* h_last, const GenScanWs& w, hipStream_t st);
+
 // The chunk-entry states H_[c-1] a scan left in its workspace,
 // [B][M][H][N][P] in the storage dtype (H_[-1] = h0 or 0).
 const void* scan_entry_states(const Shape& s, const void* ws);
+// Every chunk's entry state in float for a backward pass: the chunk
+// contributions dH32 [B][M][H][N][P] run token by token in float, the chunk
+// log decays lda [B][H][M], and st32 [B][M][H][N][P] = H_[c-1] (h0 or 0 for
+// c = 0), accumulated in float from dH32 -- the trajectory the backward's
+// own token sweeps reproduce, so the decay gradient telescopes across chunk
+// boundaries without a storage-dtype rounding at each.
+hipError_t launch_scan_states_f32(const Shape& s, const void* x, const float* dt, const float* A,
+                                  const void* Bm, const float* h0, float* lda, float* dh32,
+                                  float* st32, hipStream_t st);
 
 // Backward of the scan and its memories (scan_bwd.hip).
 size_t ssd_bwd_workspace_bytes(const Shape& s);
@@ -50,6 +77,28 @@ size_t sma_workspace_bytes(const Shape& s);
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
                       float* lse, void* ws, hipStream_t st);
+
+// Generic SMA forward (no workspace).
+hipError_t launch_gsma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
+                       float* lse, hipStream_t st);
+
+// Workspace of the generic SMA backward: per (b, h, memory 0..M-2, token) the
+// logit (then g p_j) and dy . V_j (then dl_j) with row stride Ls; Dy per
+// (b, t, h); per-head token gradients [B][L][H][2N+P].
+struct GenBwdWs {
+    float* gp;
+    float* dl;
+    float* rdy;
+    float* part;
+    int64_t Ls;
+    size_t bytes;  // total workspace
+};
+// Token and memory sides of the generic SMA backward (the caller finishes
+// q, e, C and z gradients from part and rdy).
+hipError_t launch_gsma_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                           const void* Cm, const void* mem, const void* z, const void* dy,
+                           const GenBwdWs& w, float* dmem, hipStream_t st);
 
 // Key side r (.) dH of memories 0..M-2 in the cache layout [B][M-1][H][N][P]
 // (storage dtype), as the fp32 forward stages it; klo (optional, bf16 only,
@@ -75,6 +124,24 @@ hipError_t launch_dt_softplus(int dtype, int64_t rows, int H, const void* raw, i
 hipError_t launch_gated_rmsnorm(int dtype, int64_t rows, int D, int group, const void* y,
                                 const void* z, int64_t zstride, const float* w, float eps,
                                 void* out, hipStream_t st);
+
+// Backward of the block kernels (block.hip); workspaces hold per-block
+// partial sums of the weight and bias gradients.
+size_t conv1d_silu_bwd_workspace_bytes(int64_t B, int64_t L, int C);
+hipError_t launch_conv1d_silu_bwd(int dtype, int64_t B, int64_t L, int C, int64_t stride,
+                                  const void* in, const float* w, const float* bias,
+                                  const float* st_in, const float* dout, float* din,
+                                  int64_t dstride, float* dw, float* db, float* dst_in, void* ws,
+                                  hipStream_t st);
+size_t dt_softplus_bwd_workspace_bytes(int64_t rows, int H);
+hipError_t launch_dt_softplus_bwd(int dtype, int64_t rows, int H, const void* raw, int64_t stride,
+                                  const float* bias, const float* ddt, float* draw,
+                                  int64_t dstride, float* dbias, void* ws, hipStream_t st);
+size_t gated_rmsnorm_bwd_workspace_bytes(int64_t rows, int D);
+hipError_t launch_gated_rmsnorm_bwd(int dtype, int64_t rows, int D, int group, const void* y,
+                                    const void* z, int64_t zstride, const float* w, float eps,
+                                    const float* dout, float* dy, float* dz, int64_t dzstride,
+                                    float* dw, void* ws, hipStream_t st);
 
 // Decode: per-split partial softmax statistics [B][H][nsplit][P+2] and the
 // SSM readout y_ssd [B][H][P] (float).

@@ -411,6 +411,7 @@ hipError_t run_decode_n(const Shape& s, const SmaArgs& a, int64_t pos, const int
                         const void* Cm, const void* q, const void* e, const void* z, float* hs,
                         float* ca, void* mem, void* y, void* ws, int nss, hipStream_t st) {
     switch (s.N) {
+        case 16: return run_decode<T, 16>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
         case 32: return run_decode<T, 32>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
         case 64: return run_decode<T, 64>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
         case 128: return run_decode<T, 128>(s, a, pos, pr, x, dt, A, Bm, Cm, q, e, z, hs, ca, mem, y, ws, nss, st);
@@ -486,6 +487,7 @@ hipError_t run_handoff_n(const Shape& s, const void* mem, const float* h_last,
     const dim3 grid((unsigned)s.H, (unsigned)s.B);
     prof_begin("k_decode_handoff", st);
     switch (s.N) {
+        case 16: k_decode_handoff<T, 16><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;
         case 32: k_decode_handoff<T, 32><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;
         case 64: k_decode_handoff<T, 64><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;
         case 128: k_decode_handoff<T, 128><<<grid, kThreads, 0, st>>>((const T*)mem, h_last, lengths, h_state, chunk_acc, s.H, s.S, s.Mcap); break;

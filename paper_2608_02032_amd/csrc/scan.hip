@@ -1057,6 +1057,15 @@ ScanWs scan_ws(const Shape& s, void* ws) {
     off += align256(sizeof(float) * s.B * s.H * s.M);
     w.states = p + off;
     off += align256(elem_bytes(s.dtype) * s.B * s.M * s.H * (size_t)s.N * s.P);
+    if (!tuned_shape(s)) {
+        // generic kernels: the chunk contributions and entry states in float
+        w.aux = reinterpret_cast<float*>(p + off);
+        off += align256(sizeof(float) * s.B * s.M * s.H * (size_t)s.N * s.P);
+        w.gram = reinterpret_cast<float*>(p + off);
+        off += align256(sizeof(float) * s.B * s.M * s.H * (size_t)s.N * s.P);
+        w.total = off;
+        return w;
+    }
     w.aux = reinterpret_cast<float*>(p + off);
     off += align256(sizeof(float) * s.B * s.H * s.M * 3 * (size_t)s.S);
     w.gram = reinterpret_cast<float*>(p + off);
@@ -1145,6 +1154,11 @@ const void* scan_entry_states(const Shape& s, const void* ws) {
 hipError_t launch_scan(const Shape& s, const void* x, const float* dt, const float* A,
                        const void* Bm, const void* Cm, const float* h0, void* y_ssd, void* mem,
                        float* h_last, void* ws, hipStream_t st) {
+    if (!tuned_shape(s)) {
+        const ScanWs w = scan_ws(s, ws);
+        const GenScanWs g{w.lda, w.states, w.aux, w.gram};
+        return launch_gscan(s, x, dt, A, Bm, Cm, h0, y_ssd, mem, h_last, g, st);
+    }
     if (s.dtype == 1) return run_scan_n<bf16>(s, x, dt, A, Bm, Cm, h0, y_ssd, mem, h_last, ws, st);
     return run_scan_n<float>(s, x, dt, A, Bm, Cm, h0, y_ssd, mem, h_last, ws, st);
 }

@@ -221,7 +221,7 @@ template <typename T, int N>
 __global__ __launch_bounds__(256) void k_sbwd_tokens(
     const T* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const T* __restrict__ Bm, const T* __restrict__ Cm, const T* __restrict__ dy,
-    const T* __restrict__ states, const float* __restrict__ Rs, const float* __restrict__ dmem,
+    const float* __restrict__ states, const float* __restrict__ Rs, const float* __restrict__ dmem,
     const float* __restrict__ dhl, float* __restrict__ dx, float* __restrict__ bxl,
     float* __restrict__ ydyp, float* __restrict__ mdp, float* __restrict__ dBp,
     float* __restrict__ dCp, int64_t L, int H, int G, int S, int64_t M, int64_t Mcap, int hpb) {
@@ -527,10 +527,9 @@ int sbwd_heads_per_block(const Shape& s) {
 }
 
 struct SbwdWs {
-    char* scan;
-    void* y;
-    void* mem;
-    float* hl;
+    float* lda;
+    float* dh32;
+    float* st32;
     float* dR;
     float* Rs;
     float* dec;
@@ -544,19 +543,16 @@ struct SbwdWs {
     size_t total;
 };
 
-// Workspace: the forward's own workspace and outputs (y_ssd, memories,
-// H_{L-1}), then the backward's: chunk adjoints dR and R, chunk decays,
-// per-wave memory terms [B][H][M][4] and their suffix sums, per-token
-// (B Lam) . x [B][L][H] and per-wave y . dy [B][L][H][4], per-head-block
-// dB / dC partials [B][L][H/hpb][N], per-batch dA partials.
+// Workspace: the chunk log decays, chunk contributions and entry states of
+// the forward recomputed in float, then the backward's: chunk adjoints dR
+// and R, chunk decays, per-wave memory terms [B][H][M][4] and their suffix
+// sums, per-token (B Lam) . x [B][L][H] and per-wave y . dy [B][L][H][4],
+// per-head-block dB / dC partials [B][L][H/hpb][N], per-batch dA partials.
 SbwdWs sbwd_layout(const Shape& s, void* base) {
-    const size_t es = elem_bytes(s.dtype);
     const size_t NP = (size_t)s.N * s.P;
     const size_t BLH = (size_t)s.B * s.L * s.H;
     const size_t BHM = (size_t)s.B * s.H * s.M;
     const int nhb = s.H / sbwd_heads_per_block(s);
-    Shape f = s;
-    f.Mcap = s.M;
     SbwdWs w;
     size_t o = 0;
     char* p = reinterpret_cast<char*>(base);
@@ -565,10 +561,9 @@ SbwdWs sbwd_layout(const Shape& s, void* base) {
         o += align256(bytes);
         return r;
     };
-    w.scan = take(scan_workspace_bytes(f));
-    w.y = take(es * BLH * s.P);
-    w.mem = take(es * BHM * NP);
-    w.hl = (float*)take(4 * (size_t)s.B * s.H * NP);
+    w.lda = (float*)take(4 * BHM);
+    w.dh32 = (float*)take(4 * BHM * NP);
+    w.st32 = (float*)take(4 * BHM * NP);
     w.dR = (float*)take(4 * BHM * NP);
     w.Rs = (float*)take(4 * BHM * NP);
     w.dec = (float*)take(4 * BHM);
@@ -589,12 +584,9 @@ hipError_t run_sbwd(const Shape& s, const void* x, const float* dt, const float*
                     const float* dmem, const float* dhl, float* dx, float* ddt, float* dA,
                     float* dB, float* dC, float* dh0, void* ws, hipStream_t st) {
     const SbwdWs w = sbwd_layout(s, ws);
-    Shape f = s;
-    f.Mcap = s.M;
-    // the forward again, for the chunk-entry states
-    hipError_t err = launch_scan(f, x, dt, A, Bm, Cm, h0, w.y, w.mem, w.hl, w.scan, st);
+    // the forward again, in float, for every chunk's entry state
+    hipError_t err = launch_scan_states_f32(s, x, dt, A, Bm, h0, w.lda, w.dh32, w.st32, st);
     if (err != hipSuccess) return err;
-    const T* states = (const T*)scan_entry_states(f, w.scan);
     const int hpb = sbwd_heads_per_block(s);
     const int NP = s.N * s.P;
     prof_begin("k_sbwd_chunk", st);
@@ -607,7 +599,7 @@ hipError_t run_sbwd(const Shape& s, const void* x, const float* dt, const float*
     prof_end(st);
     prof_begin("k_sbwd_tokens", st);
     k_sbwd_tokens<T, N><<<dim3((unsigned)s.M, (unsigned)(s.H / hpb), (unsigned)s.B), 256, 0, st>>>(
-        (const T*)x, dt, A, (const T*)Bm, (const T*)Cm, (const T*)dy, states, w.Rs, dmem, dhl, dx,
+        (const T*)x, dt, A, (const T*)Bm, (const T*)Cm, (const T*)dy, w.st32, w.Rs, dmem, dhl, dx,
         w.bxl, w.ydyp, w.mdp, w.dBp, w.dCp, s.L, s.H, s.G, s.S, s.M, s.Mcap, hpb);
     prof_end(st);
     prof_begin("k_sbwd_decay", st);
@@ -628,6 +620,7 @@ hipError_t run_sbwd_n(const Shape& s, const void* x, const float* dt, const floa
                       const float* dmem, const float* dhl, float* dx, float* ddt, float* dA,
                       float* dB, float* dC, float* dh0, void* ws, hipStream_t st) {
     switch (s.N) {
+        case 16: return run_sbwd<T, 16>(s, x, dt, A, Bm, Cm, h0, dy, dmem, dhl, dx, ddt, dA, dB, dC, dh0, ws, st);
         case 32: return run_sbwd<T, 32>(s, x, dt, A, Bm, Cm, h0, dy, dmem, dhl, dx, ddt, dA, dB, dC, dh0, ws, st);
         case 64: return run_sbwd<T, 64>(s, x, dt, A, Bm, Cm, h0, dy, dmem, dhl, dx, ddt, dA, dB, dC, dh0, ws, st);
         case 128: return run_sbwd<T, 128>(s, x, dt, A, Bm, Cm, h0, dy, dmem, dhl, dx, ddt, dA, dB, dC, dh0, ws, st);

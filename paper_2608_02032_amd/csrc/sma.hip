@@ -1543,6 +1543,7 @@ hipError_t launch_sma_keys(const Shape& s, const SmaArgs& a, const void* mem, vo
 }
 
 size_t sma_workspace_bytes(const Shape& s) {
+    if (!tuned_shape(s)) return 0;  // the generic kernel stages memories itself
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
     // bf16: key and value sides; fp32: key side only
     return (s.dtype == 1 ? 2 : 1) * elem_bytes(s.dtype) * s.B * Mp * s.H * (size_t)s.N * s.P;
@@ -1551,6 +1552,7 @@ size_t sma_workspace_bytes(const Shape& s) {
 hipError_t launch_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                       const void* Cm, const void* mem, const void* z, const void* y_ssd, void* y,
                       float* lse, void* ws, hipStream_t st) {
+    if (!tuned_shape(s)) return launch_gsma(s, a, q, e, Cm, mem, z, y_ssd, y, lse, st);
     if (s.dtype == 1) return run_sma_n<bf16>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, ws, st);
     return run_sma_n<float>(s, a, q, e, Cm, mem, z, y_ssd, y, lse, ws, st);
 }

@@ -1037,6 +1037,60 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
     return hipGetLastError();
 }
 
+// The generic path: token and memory sides from generic.hip, then the same
+// finishing kernel with one head per partial.
+GenBwdWs gbwd_layout(const Shape& s, void* base) {
+    const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
+    const size_t Ls = (size_t)bwd_row_stride(s);
+    size_t o = 0;
+    char* p = reinterpret_cast<char*>(base);
+    auto take = [&](size_t bytes) {
+        float* r = p ? reinterpret_cast<float*>(p + o) : nullptr;
+        o += align256(bytes);
+        return r;
+    };
+    GenBwdWs w;
+    w.gp = take(4 * s.B * s.H * (Mp > 0 ? Mp : 1) * Ls);
+    w.dl = take(4 * s.B * s.H * (Mp > 0 ? Mp : 1) * Ls);
+    w.rdy = take(4 * s.B * s.L * (size_t)s.H);
+    w.part = take(4 * s.B * s.L * s.H * (size_t)(2 * s.N + s.P));
+    w.Ls = (int64_t)Ls;
+    w.bytes = o;
+    return w;
+}
+
+template <typename T, int N>
+hipError_t run_gbwd(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                    const void* Cm, const void* mem, const void* z, const float* lse,
+                    const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
+                    void* ws, hipStream_t st) {
+    (void)lse;  // the generic backward forms the exact log-sum-exp itself
+    const GenBwdWs w = gbwd_layout(s, ws);
+    hipError_t err = launch_gsma_bwd(s, a, q, e, Cm, mem, z, dy, w, dmem, st);
+    if (err != hipSuccess) return err;
+    const int64_t rows = s.B * s.L * s.G;
+    prof_begin("k_bwd_finish", st);
+    k_bwd_finish<T, N><<<(unsigned)((rows + 3) / 4), 256, 0, st>>>(
+        (const T*)q, (const T*)e, (const T*)z, a.qw, a.ew, w.part, w.rdy, dq, de, dC, dz, a.eps,
+        a.normalize, a.z_per_head, s.L, s.H, s.G, s.S, 1, rows);
+    prof_end(st);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t run_gbwd_n(const Shape& s, const SmaArgs& a, const void* q, const void* e,
+                      const void* Cm, const void* mem, const void* z, const float* lse,
+                      const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
+                      void* ws, hipStream_t st) {
+    switch (s.N) {
+        case 16: return run_gbwd<T, 16>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+        case 32: return run_gbwd<T, 32>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+        case 64: return run_gbwd<T, 64>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+        case 128: return run_gbwd<T, 128>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <typename T>
 hipError_t run_bwd_n(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                      const void* Cm, const void* mem, const void* z, const float* lse,
@@ -1052,12 +1106,19 @@ hipError_t run_bwd_n(const Shape& s, const SmaArgs& a, const void* q, const void
 
 }  // namespace
 
-size_t sma_bwd_workspace_bytes(const Shape& s) { return bwd_layout(s, nullptr).bytes; }
+size_t sma_bwd_workspace_bytes(const Shape& s) {
+    if (!tuned_shape(s)) return gbwd_layout(s, nullptr).bytes;
+    return bwd_layout(s, nullptr).bytes;
+}
 
 hipError_t launch_sma_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* e,
                           const void* Cm, const void* mem, const void* z, const float* lse,
                           const void* dy, float* dq, float* de, float* dC, float* dmem, float* dz,
                           void* ws, hipStream_t st) {
+    if (!tuned_shape(s)) {
+        if (s.dtype == 1) return run_gbwd_n<bf16>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+        return run_gbwd_n<float>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
+    }
     if (s.dtype == 1) return run_bwd_n<bf16>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
     return run_bwd_n<float>(s, a, q, e, Cm, mem, z, lse, dy, dq, de, dC, dmem, dz, ws, st);
 }

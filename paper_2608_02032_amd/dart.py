@@ -47,6 +47,9 @@ EXPORTS = ("dart_scan_workspace_bytes", "dart_ssd_chunk_scan", "dart_sma_workspa
            "dart_sma_fwd", "dart_sma_bwd_workspace_bytes", "dart_sma_bwd",
            "dart_ssd_bwd_workspace_bytes", "dart_ssd_bwd",
            "dart_conv1d_silu", "dart_dt_softplus", "dart_gated_rmsnorm",
+           "dart_conv1d_silu_bwd_workspace_bytes", "dart_conv1d_silu_bwd",
+           "dart_dt_softplus_bwd_workspace_bytes", "dart_dt_softplus_bwd",
+           "dart_gated_rmsnorm_bwd_workspace_bytes", "dart_gated_rmsnorm_bwd",
            "dart_decode_workspace_bytes", "dart_decode_step", "dart_decode_step_noalloc",
            "dart_decode_step_ragged", "dart_decode_handoff", "dart_decode_cache_elems", "dart_status_string", "dart_last_error",
            "dart_profile_enable", "dart_profile_filter", "dart_profile_flush", "dart_profile_count",
@@ -94,6 +97,22 @@ def load_library(path: str = LIB_PATH):
         lib.dart_gated_rmsnorm.argtypes = [i64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, P, P,
                                            i64, P, ctypes.c_float, P, P]
         lib.dart_gated_rmsnorm.restype = st
+        lib.dart_conv1d_silu_bwd_workspace_bytes.argtypes = [i64, i64, ctypes.c_int32]
+        lib.dart_conv1d_silu_bwd_workspace_bytes.restype = sz
+        lib.dart_conv1d_silu_bwd.argtypes = [i64, i64, ctypes.c_int32, i64, ctypes.c_int32, P, P, P,
+                                             P, P, P, i64, P, P, P, P, sz, P]
+        lib.dart_conv1d_silu_bwd.restype = st
+        lib.dart_dt_softplus_bwd_workspace_bytes.argtypes = [i64, ctypes.c_int32]
+        lib.dart_dt_softplus_bwd_workspace_bytes.restype = sz
+        lib.dart_dt_softplus_bwd.argtypes = [i64, ctypes.c_int32, i64, ctypes.c_int32, P, P, P, P,
+                                             i64, P, P, sz, P]
+        lib.dart_dt_softplus_bwd.restype = st
+        lib.dart_gated_rmsnorm_bwd_workspace_bytes.argtypes = [i64, ctypes.c_int32]
+        lib.dart_gated_rmsnorm_bwd_workspace_bytes.restype = sz
+        lib.dart_gated_rmsnorm_bwd.argtypes = [i64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                               P, P, i64, P, ctypes.c_float, P, P, P, i64, P, P, sz,
+                                               P]
+        lib.dart_gated_rmsnorm_bwd.restype = st
         lib.dart_decode_workspace_bytes.argtypes = [D]
         lib.dart_decode_workspace_bytes.restype = sz
         lib.dart_decode_step.argtypes = [D, O, i64, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
@@ -409,6 +428,85 @@ def gated_rmsnorm(y, z, weight=None, group=None, eps=DEFAULT_EPS, out=None, stre
     check(lib.dart_gated_rmsnorm(rows, D, group, _dtype_num(y), _ptr(y), _ptr_rows(z), zs,
                                  _ptr(weight), float(eps), _ptr(out), _stream(stream)))
     return out
+
+
+def conv1d_silu_bwd(inp, weight, dout, bias=None, state_in=None, channels=None, din=None,
+                    want_state=False, stream=None):
+    """Backward of conv1d_silu (dart_conv1d_silu_bwd) for output gradient dout
+    [B][L][C] (float).  din (optional) may be a float view with a common row
+    stride, e.g. the xBC slice of a projection gradient.  Returns
+    {"din", "dweight", "dbias" (None without bias), "dstate" (or None)}."""
+    torch = _torch()
+    lib = load_library()
+    B_, L, R = inp.shape
+    C = R if channels is None else int(channels)
+    if inp.stride(2) != 1 or inp.stride(0) != L * inp.stride(1):
+        raise ValueError("inp rows must be contiguous with a common row stride")
+    for t, nm in ((weight, "weight"), (bias, "bias"), (state_in, "state_in"), (dout, "dout")):
+        _check_f32(t, nm)
+    f32 = dict(dtype=torch.float32, device=inp.device)
+    if din is None:
+        din = torch.empty((B_, L, C), **f32)
+    if din.stride(2) != 1 or din.stride(0) != L * din.stride(1):
+        raise ValueError("din rows must be contiguous with a common row stride")
+    dw = torch.empty((C, 4), **f32)
+    db = torch.empty((C,), **f32) if bias is not None else None
+    dst = torch.empty((B_, C, 3), **f32) if want_state else None
+    ws = _workspace(lib.dart_conv1d_silu_bwd_workspace_bytes(B_, L, C), inp.device)
+    check(lib.dart_conv1d_silu_bwd(B_, L, C, inp.stride(1), _dtype_num(inp), _ptr_rows(inp),
+                                   _ptr(weight), _ptr(bias), _ptr(state_in), _ptr(dout),
+                                   _ptr_rows(din), din.stride(1), _ptr(dw), _ptr(db), _ptr(dst),
+                                   _ptr(ws), ws.numel(), _stream(stream)))
+    return {"din": din, "dweight": dw, "dbias": db, "dstate": dst}
+
+
+def dt_softplus_bwd(raw, ddt, bias=None, nheads=None, draw=None, stream=None):
+    """Backward of dt_softplus (dart_dt_softplus_bwd): returns (draw, dbias)."""
+    torch = _torch()
+    lib = load_library()
+    R = raw.shape[-1]
+    H = R if nheads is None else int(nheads)
+    rows = raw.numel() // R
+    _check_f32(bias, "bias")
+    _check_f32(ddt, "ddt")
+    f32 = dict(dtype=torch.float32, device=raw.device)
+    if draw is None:
+        draw = torch.empty(tuple(raw.shape[:-1]) + (H,), **f32)
+    dbias = torch.empty((H,), **f32) if bias is not None else None
+    stride = raw.stride(-2) if raw.dim() > 1 else R
+    dstride = draw.stride(-2) if draw.dim() > 1 else H
+    ws = _workspace(lib.dart_dt_softplus_bwd_workspace_bytes(rows, H), raw.device)
+    check(lib.dart_dt_softplus_bwd(rows, H, stride, _dtype_num(raw), _ptr_rows(raw), _ptr(bias),
+                                   _ptr(ddt), _ptr_rows(draw), dstride, _ptr(dbias), _ptr(ws),
+                                   ws.numel(), _stream(stream)))
+    return draw, dbias
+
+
+def gated_rmsnorm_bwd(y, z, dout, weight=None, group=None, eps=DEFAULT_EPS, dz=None, stream=None):
+    """Backward of gated_rmsnorm (dart_gated_rmsnorm_bwd): returns
+    {"dy", "dz", "dweight" (None without weight)}; dz (optional) may be a
+    float view with a common row stride."""
+    torch = _torch()
+    lib = load_library()
+    D = y.shape[-1]
+    rows = y.numel() // D
+    group = D if group is None else int(group)
+    if not y.is_contiguous() or z.stride(-1) != 1 or not dout.is_contiguous():
+        raise ValueError("y and dout must be contiguous and z rows contiguous")
+    _check_f32(weight, "weight")
+    _check_f32(dout, "dout")
+    f32 = dict(dtype=torch.float32, device=y.device)
+    dy = torch.empty(y.shape, **f32)
+    if dz is None:
+        dz = torch.empty(y.shape, **f32)
+    dw = torch.empty((D,), **f32) if weight is not None else None
+    zs = z.stride(-2) if z.dim() > 1 else D
+    dzs = dz.stride(-2) if dz.dim() > 1 else D
+    ws = _workspace(lib.dart_gated_rmsnorm_bwd_workspace_bytes(rows, D), y.device)
+    check(lib.dart_gated_rmsnorm_bwd(rows, D, group, _dtype_num(y), _ptr(y), _ptr_rows(z), zs,
+                                     _ptr(weight), float(eps), _ptr(dout), _ptr(dy), _ptr_rows(dz),
+                                     dzs, _ptr(dw), _ptr(ws), ws.numel(), _stream(stream)))
+    return {"dy": dy, "dz": dz, "dweight": dw}
 
 
 def decode_step(pos, x, dt, A, Bm, Cm, q, e, z, h_state, chunk_acc, mem_cache, chunk,

@@ -100,8 +100,8 @@ def call_scan(lib, d, **ptrs):
     ("nheads", 3, dart.DART_ERR_INVALID_ARG),      # not a multiple of ngroups = 2 below
     ("dtype", 7, dart.DART_ERR_INVALID_ARG),
     ("headdim", 128, dart.DART_ERR_UNSUPPORTED),
-    ("dstate", 16, dart.DART_ERR_UNSUPPORTED),
-    ("chunk", 32, dart.DART_ERR_UNSUPPORTED),
+    ("dstate", 48, dart.DART_ERR_UNSUPPORTED),
+    ("chunk", 8192, dart.DART_ERR_UNSUPPORTED),
     ("mem_capacity", 3, dart.DART_ERR_INVALID_ARG),  # < ceil(512/64) = 8
 ])
 def test_scan_rejects_bad_dims(lib, field, value, status):
@@ -280,3 +280,17 @@ def test_noalloc_decode_rejects_a_step_beyond_its_scratch(lib):
     # a NULL required pointer is still an argument error, found first
     st = lib.dart_decode_step_noalloc(ctypes.byref(d), ctypes.byref(opts), 64, None, *([p] * 11), None)
     assert st == 1
+
+
+@pytest.mark.parametrize("N,S", [(16, 16), (16, 256), (64, 32), (128, 48), (32, 1)])
+def test_generic_shapes_are_accepted_and_sized(lib, N, S):
+    """Shapes outside the tuned set (N in {32, 64, 128} with S in {64, 128,
+    256}) run the generic kernels: they size workspaces instead of returning
+    DART_ERR_UNSUPPORTED."""
+    d = dims(dstate=N, chunk=S, seqlen=300)
+    M = -(-300 // S)
+    assert lib.dart_scan_workspace_bytes(ctypes.byref(d)) >= 2 * 2 * M * 4 * N * 64
+    assert lib.dart_sma_bwd_workspace_bytes(ctypes.byref(d)) > 0
+    assert lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(d)) > 0
+    dd = dims(dstate=N, chunk=S, seqlen=0, mem_capacity=M)
+    assert lib.dart_decode_workspace_bytes(ctypes.byref(dd)) > 0

@@ -67,6 +67,10 @@ CASES = [
     ("bf16_L700_N128_S256", 1, 700, 4, 64, 128, 256, "bf16", 1),
     ("fp32_L1_N64_S64", 3, 1, 2, 64, 64, 64, "fp32", 1),
     ("bf16_L64_N32_S64_G4", 2, 64, 4, 64, 32, 64, "bf16", 4),
+    # many chunks (M = 32 and 64): the decay gradient telescopes across every
+    # chunk boundary
+    ("bf16_L8192_N128_S256_M32", 1, 8192, 2, 64, 128, 256, "bf16", 1),
+    ("bf16_L4096_N64_S64_M64", 1, 4096, 2, 64, 64, 64, "bf16", 1),
 ]
 
 

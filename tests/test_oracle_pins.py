@@ -695,3 +695,60 @@ def test_block_dt_softplus_and_gated_rmsnorm_closed_forms():
     u = y * 40.0
     ref = u / np.sqrt((u.reshape(5, 4, 8) ** 2).mean(-1, keepdims=True)).repeat(8, -1).reshape(5, 32)
     np.testing.assert_allclose(oracle.gated_rmsnorm(y, zl, group=8, eps=1e-30), ref, rtol=1e-12)
+
+
+def _central(f, x, idx, h=1e-6):
+    xp = x.copy(); xp[idx] += h
+    xm = x.copy(); xm[idx] -= h
+    return (f(xp) - f(xm)) / (2 * h)
+
+
+def test_block_backward_matches_finite_differences():
+    """The backward of the three block definitions against central
+    differences of the oracle forward (loss sum dout * out) at sampled
+    entries of every input: the convolution's input, weights, bias and carried
+    state; softplus's raw input and bias; the gated norm's y, z and weight."""
+    rng = np.random.default_rng(31)
+    B_, L, C = 2, 9, 5
+    x = rng.standard_normal((B_, L, C))
+    w = rng.standard_normal((C, 4)) * 0.5
+    bias = rng.standard_normal(C) * 0.2
+    st = rng.standard_normal((B_, C, 3))
+    dout = rng.standard_normal((B_, L, C))
+    g = oracle.conv1d_silu_bwd(x, w, dout, bias=bias, state=st)
+    loss = lambda xx=x, ww=w, bb=bias, ss=st: float((oracle.conv1d_silu(xx, ww, bb, ss)[0] * dout).sum())
+    for idx in [(0, 0, 0), (1, 4, 2), (1, 8, 4), (0, 2, 3)]:
+        fd = _central(lambda v: loss(xx=v), x, idx)
+        assert g["din"][idx] == pytest.approx(fd, abs=1e-7, rel=1e-6)
+    for idx in [(0, 0), (2, 3), (4, 1)]:
+        fd = _central(lambda v: loss(ww=v), w, idx)
+        assert g["dw"][idx] == pytest.approx(fd, abs=1e-7, rel=1e-6)
+    for c in (0, 3):
+        fd = _central(lambda v: loss(bb=v), bias, (c,))
+        assert g["db"][c] == pytest.approx(fd, abs=1e-7, rel=1e-6)
+    for idx in [(0, 1, 0), (1, 3, 2), (1, 0, 1)]:
+        fd = _central(lambda v: loss(ss=v), st, idx)
+        assert g["dstate"][idx] == pytest.approx(fd, abs=1e-7, rel=1e-6)
+
+    raw = rng.standard_normal((7, 3)) * 4
+    bh = rng.standard_normal(3)
+    ddt = rng.standard_normal((7, 3))
+    draw, dbias = oracle.dt_softplus_bwd(raw, ddt, bias=bh)
+    lossd = lambda rr=raw, bb=bh: float((oracle.dt_softplus(rr, bb) * ddt).sum())
+    for idx in [(0, 0), (3, 2), (6, 1)]:
+        assert draw[idx] == pytest.approx(_central(lambda v: lossd(rr=v), raw, idx), abs=1e-7, rel=1e-6)
+    for h in range(3):
+        assert dbias[h] == pytest.approx(_central(lambda v: lossd(bb=v), bh, (h,)), abs=1e-7, rel=1e-6)
+
+    rows, D, grp = 4, 16, 8
+    y = rng.standard_normal((rows, D))
+    z = rng.standard_normal((rows, D))
+    wn = 1 + 0.2 * rng.standard_normal(D)
+    do = rng.standard_normal((rows, D))
+    gn = oracle.gated_rmsnorm_bwd(y, z, do, w=wn, group=grp)
+    lossn = lambda yy=y, zz=z, ww=wn: float((oracle.gated_rmsnorm(yy, zz, ww, group=grp) * do).sum())
+    for idx in [(0, 0), (1, 9), (3, 15), (2, 4)]:
+        assert gn["dy"][idx] == pytest.approx(_central(lambda v: lossn(yy=v), y, idx), abs=1e-7, rel=1e-6)
+        assert gn["dz"][idx] == pytest.approx(_central(lambda v: lossn(zz=v), z, idx), abs=1e-7, rel=1e-6)
+    for k in (0, 7, 12):
+        assert gn["dw"][k] == pytest.approx(_central(lambda v: lossn(ww=v), wn, (k,)), abs=1e-7, rel=1e-6)
