@@ -21,7 +21,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libdart.so")
 ARCH = "gfx950"
 
-SOURCES = ["scan.hip", "sma.hip", "sma_bwd.hip", "scan_bwd.hip", "decode.hip", "block.hip", "generic.hip",
+SOURCES = ["scan.hip", "sma.hip", "sma_bwd.hip", "scan_bwd.hip", "scan_bwd_mfma.hip", "decode.hip", "block.hip", "generic.hip",
            "dart_api.cpp", "profile.cpp"]
 
 COMMON_FLAGS = [

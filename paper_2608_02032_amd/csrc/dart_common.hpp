@@ -149,6 +149,39 @@ __device__ __forceinline__ float dpp_group_sum(float v) {
     return v;
 }
 
+// Reduce-scatter over the 64 lanes of the W values of every lane: at step
+// MASK a lane keeps one half of its values (the upper half where bit MASK of
+// its lane id is set) and adds its partner's copy of that half, so after
+// log2(W) steps lane l holds a partial sum of value l / (64 / W); the
+// remaining bits are summed by plain butterflies.  W - 1 + log2(64 / W)
+// exchanges instead of W full reductions.
+template <int R, int W, int MASK>
+__device__ __forceinline__ void rs_step(float (&cur)[R], int lane) {
+    if constexpr (W > 1) {
+        constexpr int half = W / 2;
+        const bool hi = (lane & MASK) != 0;
+#pragma unroll
+        for (int j = 0; j < half; ++j) {
+            const float keep = hi ? cur[j + half] : cur[j];
+            const float give = hi ? cur[j] : cur[j + half];
+            cur[j] = keep + __shfl_xor(give, MASK, 64);
+        }
+        rs_step<R, half, MASK / 2>(cur, lane);
+    }
+}
+
+// Sum of each of the R values of every lane over the groups of LANES lanes that
+// differ in their low log2(LANES) bits; afterwards lane l holds the group sum of
+// value (l % LANES) / (LANES / R).
+template <int R, int LANES>
+__device__ __forceinline__ float lane_sums(float (&v)[R], int lane) {
+    rs_step<R, R, LANES / 2>(v, lane);
+    float s = v[0];
+#pragma unroll
+    for (int m = (LANES / R) / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+    return s;
+}
+
 __device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }

@@ -63,6 +63,15 @@ hipError_t launch_ssd_bwd(const Shape& s, const void* x, const float* dt, const 
                           const float* dmem, const float* dh_last, float* dx, float* ddt, float* dA,
                           float* dB, float* dC, float* dh0, void* ws, hipStream_t st);
 
+// The chunked-matrix scan backward on MFMA (scan_bwd_mfma.hip): bf16 storage
+// and the tuned shapes; launch_ssd_bwd dispatches to it.
+bool sbwd_mfma_shape(const Shape& s);
+size_t sbwd_mfma_workspace_bytes(const Shape& s);
+hipError_t launch_ssd_bwd_mfma(const Shape& s, const void* x, const float* dt, const float* A,
+                               const void* Bm, const void* Cm, const float* h0, const void* dy,
+                               const float* dmem, const float* dh_last, float* dx, float* ddt, float* dA,
+                               float* dB, float* dC, float* dh0, void* ws, hipStream_t st);
+
 struct SmaArgs {
     float eps;
     const float* qw;

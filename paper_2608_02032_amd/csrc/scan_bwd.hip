@@ -129,39 +129,6 @@ __global__ __launch_bounds__(256) void k_sbwd_pass(const float* __restrict__ dR,
     if (dh0) store4(dh0 + (b * H + h) * (int64_t)NP + e0, r);
 }
 
-// Reduce-scatter over the 64 lanes of the W values of every lane: at step
-// MASK a lane keeps one half of its values (the upper half where bit MASK of
-// its lane id is set) and adds its partner's copy of that half, so after
-// log2(W) steps lane l holds a partial sum of value l / (64 / W); the
-// remaining bits are summed by plain butterflies.  W - 1 + log2(64 / W)
-// exchanges instead of W full reductions.
-template <int R, int W, int MASK>
-__device__ __forceinline__ void rs_step(float (&cur)[R], int lane) {
-    if constexpr (W > 1) {
-        constexpr int half = W / 2;
-        const bool hi = (lane & MASK) != 0;
-#pragma unroll
-        for (int j = 0; j < half; ++j) {
-            const float keep = hi ? cur[j + half] : cur[j];
-            const float give = hi ? cur[j] : cur[j + half];
-            cur[j] = keep + __shfl_xor(give, MASK, 64);
-        }
-        rs_step<R, half, MASK / 2>(cur, lane);
-    }
-}
-
-// Sum of each of the R values of every lane over the groups of LANES lanes that
-// differ in their low log2(LANES) bits; afterwards lane l holds the group sum of
-// value (l % LANES) / (LANES / R).
-template <int R, int LANES>
-__device__ __forceinline__ float lane_sums(float (&v)[R], int lane) {
-    rs_step<R, R, LANES / 2>(v, lane);
-    float s = v[0];
-#pragma unroll
-    for (int m = (LANES / R) / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
-    return s;
-}
-
 template <int K>
 __device__ __forceinline__ void load_k(const bf16* p, float (&v)[K]) {
     if constexpr (K % 8 == 0) {
@@ -363,7 +330,6 @@ __global__ __launch_bounds__(256) void k_sbwd_tokens(
         fetch_r(e);
         for (int k = 0; k < ntok; ++k) {
             const int64_t t = e - k;
-            const int64_t th = (b * L + t) * H + h;
             const float d = dn, ob = on;
             const RawVec<T, 4> xc = xr, yc = yr;
             const RawVec<T, RL> bc = br, cc = cr;
@@ -630,12 +596,16 @@ hipError_t run_sbwd_n(const Shape& s, const void* x, const float* dt, const floa
 
 }  // namespace
 
-size_t ssd_bwd_workspace_bytes(const Shape& s) { return sbwd_layout(s, nullptr).total; }
+size_t ssd_bwd_workspace_bytes(const Shape& s) {
+    return sbwd_mfma_shape(s) ? sbwd_mfma_workspace_bytes(s) : sbwd_layout(s, nullptr).total;
+}
 
 hipError_t launch_ssd_bwd(const Shape& s, const void* x, const float* dt, const float* A,
                           const void* Bm, const void* Cm, const float* h0, const void* dy,
                           const float* dmem, const float* dh_last, float* dx, float* ddt, float* dA,
                           float* dB, float* dC, float* dh0, void* ws, hipStream_t st) {
+    if (sbwd_mfma_shape(s))
+        return launch_ssd_bwd_mfma(s, x, dt, A, Bm, Cm, h0, dy, dmem, dh_last, dx, ddt, dA, dB, dC, dh0, ws, st);
     if (s.dtype == 1)
         return run_sbwd_n<bf16>(s, x, dt, A, Bm, Cm, h0, dy, dmem, dh_last, dx, ddt, dA, dB, dC, dh0, ws, st);
     return run_sbwd_n<float>(s, x, dt, A, Bm, Cm, h0, dy, dmem, dh_last, dx, ddt, dA, dB, dC, dh0, ws, st);
