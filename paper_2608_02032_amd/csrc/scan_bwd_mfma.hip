@@ -321,8 +321,9 @@ __global__ __launch_bounds__(256) void k_sbwd_pass2(
 // Per (b, c, g, set of four 16-token tiles), every head of the group:
 //   the rank-P terms dB_t += dt_t e^{cs_e - cs_t} W_c x_t and
 //   dC_s += e^{cs_s} H_[c-1] dy_s ([n][t] tiles: A = W or H rows from LDS,
-//   B = the scaled x or dy rows of the token tile), w_s = e^{cs_s} C_s .
-//   (H_[c-1] dy_s) per head, and
+//   B = the scaled x or dy rows of the token tile), per head
+//   w_s = e^{cs_s} C_s . (H_[c-1] dy_s) and v~_t = e^{cs_e - cs_t} B_t . (W_c x_t),
+//   and
 //   Mbar[s][t] = sum_h dt_t e^{cs_s - cs_t} (dy_s . x_t) for the set's token
 //   columns (t <= s), in fp32 registers across the heads.
 // Set q holds tiles q, NKB - 1 - q, NKB + q and 2 NKB - 1 - q (NKB = S / 32),
@@ -333,11 +334,11 @@ __global__ __launch_bounds__(256) void k_sbwd_pass2(
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(512) void k_sbwd_group(
-    const bf16* __restrict__ x, const float* __restrict__ dt, const bf16* __restrict__ Cm,
-    const bf16* __restrict__ dy, const float* __restrict__ rec, const bf16* __restrict__ Hb,
-    const bf16* __restrict__ Wb, float* __restrict__ dB, float* __restrict__ dC,
-    float* __restrict__ wp, bf16* __restrict__ mbar, int64_t L, int H, int G, int64_t M,
-    int64_t nbcg) {
+    const bf16* __restrict__ x, const float* __restrict__ dt, const bf16* __restrict__ Bm,
+    const bf16* __restrict__ Cm, const bf16* __restrict__ dy, const float* __restrict__ rec,
+    const bf16* __restrict__ Hb, const bf16* __restrict__ Wb, float* __restrict__ dB,
+    float* __restrict__ dC, float* __restrict__ wp, float* __restrict__ vt, bf16* __restrict__ mbar, int64_t L, int H, int G,
+    int64_t M, int64_t nbcg) {
     constexpr int NW = 8, NT = 512;
     constexpr int XRB = kP * 2;
     constexpr int DYT = S * XRB, TT = N * XRB, RECB = 3 * S * 4;
@@ -368,6 +369,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
 
     __shared__ __attribute__((aligned(16))) char ubuf[2][UB];
     __shared__ float wpart[2][2][64];
+    __shared__ float vpart[2][2][64];
 
     auto issue = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = g * hpg + hh;
@@ -376,21 +378,36 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
                             (int64_t)H * XRB, S, len, wave, NW, lane);
         dma_tile<XRB, true>(&ubuf[u][DYT], reinterpret_cast<const char*>(Wb + o), XRB, N, N, wave, NW, lane);
         dma_tile<XRB, true>(&ubuf[u][DYT + TT], reinterpret_cast<const char*>(Hb + o), XRB, N, N, wave, NW, lane);
-        float* r = reinterpret_cast<float*>(&ubuf[u][DYT + 2 * TT]);
-        const float* rc = rec + ((b * H + h) * M + c) * S;
-        for (int i = tid; i < S; i += NT) {
-            const float cs = rc[i];
-            const bool v = i < len;
-            r[i] = cs;
-            r[S + i] = v ? dt[(b * L + t0 + i) * H + h] : 0.f;
-            r[2 * S + i] = v ? fast_exp2(cs - rc[i & ~31]) : 0.f;
+    };
+    // per-token record of head hh (cs, dt, b_s = e^{cs_s - cs at the s block
+    // start}): thread tid < S takes token tid; loaded early, stored to LDS
+    // before the barrier that opens the head
+    float rq[3];
+    auto load_rec = [&](int hh) __attribute__((always_inline)) {
+        const int h = g * hpg + hh;
+        if (tid < S) {
+            const float* rc = rec + ((b * H + h) * M + c) * S;
+            rq[0] = rc[tid];
+            rq[1] = tid < len ? dt[(b * L + t0 + tid) * H + h] : 0.f;
+            rq[2] = rc[tid & ~31];
         }
     };
-    // C_t at the n rows this lane's accumulators hold (16 nt + 4 grp + i)
-    bf16x4 cv[NTH];
+    auto store_rec = [&](int u) __attribute__((always_inline)) {
+        if (tid < S) {
+            float* r = reinterpret_cast<float*>(&ubuf[u][DYT + 2 * TT]);
+            r[tid] = rq[0];
+            r[S + tid] = rq[1];
+            r[2 * S + tid] = tid < len ? fast_exp2(rq[0] - rq[2]) : 0.f;
+        }
+    };
+    // B_t and C_t at the n rows this lane's accumulators hold (16 nt + 4 grp + i)
+    bf16x4 bv[NTH], cv[NTH];
 #pragma unroll
-    for (int j = 0; j < NTH; ++j)
-        cv[j] = *reinterpret_cast<const bf16x4*>(Cm + ((b * L + t0 + tc) * G + g) * N + (nh * NTH + j) * 16 + 4 * grp);
+    for (int j = 0; j < NTH; ++j) {
+        const int64_t o = ((b * L + t0 + tc) * G + g) * N + (nh * NTH + j) * 16 + 4 * grp;
+        bv[j] = *reinterpret_cast<const bf16x4*>(Bm + o);
+        cv[j] = *reinterpret_cast<const bf16x4*>(Cm + o);
+    }
     f32x4 accB[NTH], accC[NTH];
 #pragma unroll
     for (int j = 0; j < NTH; ++j) {
@@ -402,47 +419,74 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
     for (int k = 0; k < MPW; ++k)
 #pragma unroll
         for (int e = 0; e < 8; ++e) mb[k][e] = 0.f;
+    // x_t fragments, one head ahead
+    bf16x8 xn0, xn1;
+    {
+        const bf16* xr = x + ((b * L + t0 + tc) * H + g * hpg) * kP + 8 * grp;
+        xn0 = load_frag(xr);
+        xn1 = load_frag(xr + 32);
+    }
     issue(0, 0);
+    load_rec(0);
+    store_rec(0);
     for (int hh = 0; hh < hpg; ++hh) {
         const int u = hh & 1;
         const int h = g * hpg + hh;
-        const bf16* xr = x + ((b * L + t0 + tc) * H + h) * kP + 8 * grp;
-        const bf16x8 xf0 = load_frag(xr), xf1 = load_frag(xr + 32);
         __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-        lds_barrier();  // head hh's inputs are in; buffer u ^ 1 and wpart[u ^ 1] are free
-        if (hh + 1 < hpg) issue(hh + 1, u ^ 1);
-        if (hh > 0 && nh == 0 && grp == 0 && valid)
-            wp[(b * L + t0 + t) * H + h - 1] = wpart[u ^ 1][0][slot * 16 + col] + wpart[u ^ 1][1][slot * 16 + col];
+        lds_barrier();  // head hh's inputs are in; buffer u ^ 1 and the exchange slots u ^ 1 are free
+        const bf16x8 xf0 = xn0, xf1 = xn1;
+        if (hh + 1 < hpg) {
+            issue(hh + 1, u ^ 1);
+            load_rec(hh + 1);
+            const bf16* xr = x + ((b * L + t0 + tc) * H + h + 1) * kP + 8 * grp;
+            xn0 = load_frag(xr);
+            xn1 = load_frag(xr + 32);
+        }
+        if (hh > 0 && nh == 0 && grp == 0 && valid) {
+            const int tl = slot * 16 + col;
+            const int64_t o = (b * L + t0 + t) * H + h - 1;
+            wp[o] = wpart[u ^ 1][0][tl] + wpart[u ^ 1][1][tl];
+            vt[o] = vpart[u ^ 1][0][tl] + vpart[u ^ 1][1][tl];
+        }
         const char* dyt = &ubuf[u][0];
         const char* wtl = &ubuf[u][DYT];
         const char* htl = &ubuf[u][DYT + TT];
         const float* rcs = reinterpret_cast<const float*>(&ubuf[u][DYT + 2 * TT]);
         const float* rbs = rcs + 2 * S;
         const float cst = rcs[t], dtt = rcs[S + t], cse = rcs[S - 1];
-        const float sx = dtt * fast_exp2(cse - cst);
+        const float sx = valid ? fast_exp2(cse - cst) : 0.f;
         const float sy = valid ? fast_exp2(cst) : 0.f;
         const bf16x8 xs0 = scale_frag(xf0, sx), xs1 = scale_frag(xf1, sx);
         const bf16x8 ys0 = scale_frag(frag_rowmajor<bf16, XRB>(dyt, tc, 8 * grp), sy);
         const bf16x8 ys1 = scale_frag(frag_rowmajor<bf16, XRB>(dyt, tc, 32 + 8 * grp), sy);
-        float wsum = 0.f;
+        // W x^ (x^ = e^{cs_e - cs_t} x_t): dB_t += dt_t W x^, v~_t = B_t . W x^;
+        // H dy^ (dy^ = e^{cs_t} dy_t): dC_t += H dy^, w_t = C_t . H dy^
+        float wsum = 0.f, vsum = 0.f;
 #pragma unroll
         for (int j = 0; j < NTH; ++j) {
             const int nrow = (nh * NTH + j) * 16 + col;
             const bf16x8 w0 = frag_rowmajor<bf16, XRB>(wtl, nrow, 8 * grp);
             const bf16x8 w1 = frag_rowmajor<bf16, XRB>(wtl, nrow, 32 + 8 * grp);
-            accB[j] = mma16(mma16(accB[j], w0, xs0), w1, xs1);
+            const f32x4 tv = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, w0, xs0), w1, xs1);
             const bf16x8 h0f = frag_rowmajor<bf16, XRB>(htl, nrow, 8 * grp);
             const bf16x8 h1f = frag_rowmajor<bf16, XRB>(htl, nrow, 32 + 8 * grp);
             const f32x4 tmp = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, h0f, ys0), h1f, ys1);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
+                vsum += (float)bv[j][i] * tv[i];
+                accB[j][i] += dtt * tv[i];
                 wsum += (float)cv[j][i] * tmp[i];
                 accC[j][i] += tmp[i];
             }
         }
         wsum += __shfl_xor(wsum, 16, 64);
         wsum += __shfl_xor(wsum, 32, 64);
-        if (grp == 0) wpart[u][nh][slot * 16 + col] = wsum;
+        vsum += __shfl_xor(vsum, 16, 64);
+        vsum += __shfl_xor(vsum, 32, 64);
+        if (grp == 0) {
+            wpart[u][nh][slot * 16 + col] = wsum;
+            vpart[u][nh][slot * 16 + col] = vsum;
+        }
         // Mbar pairs (tile T, s block K): A = dy rows in gram_row order, B = x_t
 #pragma unroll
         for (int k = 0; k < MPW; ++k) {
@@ -477,11 +521,15 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
                 }
             }
         }
+        if (hh + 1 < hpg) store_rec(u ^ 1);
     }
     lds_barrier();
     if (nh == 0 && grp == 0 && valid) {
         const int u = (hpg - 1) & 1;
-        wp[(b * L + t0 + t) * H + g * hpg + hpg - 1] = wpart[u][0][slot * 16 + col] + wpart[u][1][slot * 16 + col];
+        const int tl = slot * 16 + col;
+        const int64_t o = (b * L + t0 + t) * H + g * hpg + hpg - 1;
+        wp[o] = wpart[u][0][tl] + wpart[u][1][tl];
+        vt[o] = vpart[u][0][tl] + vpart[u][1][tl];
     }
     if (valid) {
         const int64_t row = ((b * L + t0 + t) * G + g) * N;
@@ -514,17 +562,19 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
 //   the diagonal block;
 //   M1 = bf16(G1 decay) -> dx^T += dy^T M1 (A = dy^T by transposing reads);
 //   D = M1 G2 dt_t -> c~_t (lane sums) and r_s (LDS, per wave).
-// Then dx^T += W^T (e^{cs_e - cs_t} B_t) (A = W^T from LDS), dx = dt acc,
-// (B Lam) . x = x . acc, and the chunk scan of dL/dl (one wave) -> ddt and the
-// chunk's dA partial.
+// Then dx^T += W^T (e^{cs_e - cs_t} B_t) (A = W^T from LDS), dx = dt acc, and
+// the chunk scan of dL/dl (one wave) -> ddt = (B Lam) . x + A_h dL/dl, with
+// (B Lam) . x = c~_t + v~_t (v~ from k_sbwd_group), and the chunk's dA
+// partial.  Each wave finishes one row tile before the next.
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     const bf16* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const bf16* __restrict__ Bm, const bf16* __restrict__ Cm, const bf16* __restrict__ dy,
     const float* __restrict__ rec, const bf16* __restrict__ Wb, const float* __restrict__ Kp,
-    const float* __restrict__ wp, float* __restrict__ dx, float* __restrict__ ddt,
-    float* __restrict__ dAp, int64_t L, int H, int G, int64_t M, int hpb, int64_t nbcg, int nkp) {
+    const float* __restrict__ wp, const float* __restrict__ vt, float* __restrict__ dx,
+    float* __restrict__ ddt, float* __restrict__ dAp, int64_t L, int H, int G, int64_t M, int hpb,
+    int64_t nbcg, int nkp) {
     constexpr int NW = quad_waves<S>();
     constexpr int NT = 64 * NW;
     constexpr int NQ = S / 16 / NW;
@@ -554,7 +604,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
 
     __shared__ __attribute__((aligned(16))) char ubuf[2][UB];
     __shared__ float rpart[NW][S];
-    __shared__ float tok[3][S];
+    __shared__ float tok[1][S];
 
     auto issue = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = hbase + hh;
@@ -562,14 +612,25 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                             (int64_t)H * XRB, S, len, wave, NW, lane);
         dma_tile<XRB, true>(&ubuf[u][DYT], reinterpret_cast<const char*>(Wb + ((b * M + c) * H + h) * (int64_t)N * kP),
                             XRB, N, N, wave, NW, lane);
-        float* r = reinterpret_cast<float*>(&ubuf[u][DYT + WTB]);
-        const float* rc = rec + ((b * H + h) * M + c) * S;
-        for (int i = tid; i < S; i += NT) {
-            const float cs = rc[i];
-            const bool v = i < len;
-            r[i] = cs;
-            r[S + i] = v ? dt[(b * L + t0 + i) * H + h] : 0.f;
-            r[2 * S + i] = v ? fast_exp2(cs - rc[i & ~31]) : 0.f;
+    };
+    // per-token record of head hh (cs, dt, b_s): thread tid < S takes token
+    // tid; loaded early, stored to LDS before the barrier that opens the head
+    float rq[3];
+    auto load_rec = [&](int hh) __attribute__((always_inline)) {
+        const int h = hbase + hh;
+        if (tid < S) {
+            const float* rc = rec + ((b * H + h) * M + c) * S;
+            rq[0] = rc[tid];
+            rq[1] = tid < len ? dt[(b * L + t0 + tid) * H + h] : 0.f;
+            rq[2] = rc[tid & ~31];
+        }
+    };
+    auto store_rec = [&](int u) __attribute__((always_inline)) {
+        if (tid < S) {
+            float* r = reinterpret_cast<float*>(&ubuf[u][DYT + WTB]);
+            r[tid] = rq[0];
+            r[S + tid] = rq[1];
+            r[2 * S + tid] = tid < len ? fast_exp2(rq[0] - rq[2]) : 0.f;
         }
     };
 
@@ -582,6 +643,8 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     const int npw = nk0 + (NQ == 2 ? NKB - kmin1 : 0);
 
     issue(0, 0);
+    load_rec(0);
+    store_rec(0);
     // G1 of every pair, kept as bf16
     bf16x8 g1c[NPW];
 #pragma unroll
@@ -612,151 +675,174 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) ko[pt].init(8 * grp, 8 * grp + 4, 16 * pt, lane);
 
+    // x_t fragments of the wave's tiles (each reloaded for the next head once
+    // its tile's pairs are done)
+    bf16x8 xf[NQ][2];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int t = 16 * (q ? T1 : T0) + col;
+        const bf16* xr = x + ((b * L + t0 + (t < len ? t : len - 1)) * H + hbase) * kP + 8 * grp;
+        xf[q][0] = load_frag(xr);
+        xf[q][1] = load_frag(xr + 32);
+    }
+
     for (int hh = 0; hh < hpb; ++hh) {
         const int u = hh & 1;
         const int h = hbase + hh;
         __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         lds_barrier();  // head hh's inputs are in; buffer u ^ 1 is free
-        if (hh + 1 < hpb) issue(hh + 1, u ^ 1);
+        if (hh + 1 < hpb) {
+            issue(hh + 1, u ^ 1);
+            load_rec(hh + 1);
+        }
+        // the chunk scan's global inputs, read by wave 0 at the end of the head
+        float wq[TPL], kq = 0.f;
+        if (wave == 0) {
+#pragma unroll
+            for (int k = 0; k < TPL; ++k) {
+                const int tt = TPL * lane + k;
+                wq[k] = tt < len ? wp[(b * L + t0 + tt) * H + h] : 0.f;
+            }
+            if (lane < nkp) kq = Kp[((b * H + h) * M + c) * nkp + lane];
+        }
         const char* dyt = &ubuf[u][0];
         const char* wtl = &ubuf[u][DYT];
         const float* rcs = reinterpret_cast<const float*>(&ubuf[u][DYT + WTB]);
         const float* rdt = rcs + S;
         const float* rbs = rcs + 2 * S;
         for (int i = lane; i < S; i += 64) rpart[wave][i] = 0.f;
+        // lane coordinates made opaque per head, so that the per-pair LDS
+        // offsets are recomputed in the loop rather than held live across it
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int grp = ln >> 4, col = ln & 15;
         const float Ah = A[h];
         const float cse = rcs[S - 1];
 
-        f32x4 acc[NQ][4];
-        float ct[NQ], cst[NQ], dtt[NQ];
-        bf16x8 xf[NQ][2];
+        // one row tile at a time: its pairs, then its W_c term and outputs
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            const int t = 16 * (q ? T1 : T0) + col;
-            const int tc = t < len ? t : len - 1;
-            const bf16* xr = x + ((b * L + t0 + tc) * H + h) * kP + 8 * grp;
-            xf[q][0] = load_frag(xr);
-            xf[q][1] = load_frag(xr + 32);
-            cst[q] = rcs[t];
-            dtt[q] = rdt[t];
-            ct[q] = 0.f;
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) acc[q][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-
-        auto pair = [&](auto qc, int j, int K) __attribute__((always_inline)) {
-            constexpr int q = decltype(qc)::value;
             const int T = q ? T1 : T0;
             const int t = 16 * T + col;
-            f32x4 g2[2];
-#pragma unroll
-            for (int uu = 0; uu < 2; ++uu) {
-                const int s = 32 * K + gram_row(uu, col);
-                const bf16x8 a0 = frag_rowmajor<bf16, XRB>(dyt, s, 8 * grp);
-                const bf16x8 a1 = frag_rowmajor<bf16, XRB>(dyt, s, 32 + 8 * grp);
-                g2[uu] = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, a0, xf[q][0]), a1, xf[q][1]);
-            }
-            float f[8];
-            const int sb = 32 * K + 8 * grp;
-            if (K > (T >> 1)) {
-                const float at = fast_exp2(rcs[32 * K] - cst[q]);
-                const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + sb);
-                const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + sb + 4);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    f[i] = b0[i] * at;
-                    f[4 + i] = b1[i] * at;
-                }
-            } else {
-                const f32x4 c0 = *reinterpret_cast<const f32x4*>(rcs + sb);
-                const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + sb + 4);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    f[i] = (sb + i >= t && sb + i < len) ? fast_exp2(c0[i] - cst[q]) : 0.f;
-                    f[4 + i] = (sb + 4 + i >= t && sb + 4 + i < len) ? fast_exp2(c1[i] - cst[q]) : 0.f;
-                }
-            }
-            bf16x8 m1;
-            float rv[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float gv = e < 4 ? g2[0][e] : g2[1][e - 4];
-                m1[e] = (bf16)((float)g1c[j][e] * f[e]);
-                const float d = (float)m1[e] * gv;
-                ct[q] += d;
-                rv[e] = d * dtt[q];
-            }
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) acc[q][pt] = mma16(acc[q][pt], ko[pt].read(dyt, 32 * K * XRB), m1);
-            const float rs = lane_sums<8, 16>(rv, lane);
-            if ((lane & 1) == 0) rpart[wave][sb + ((lane & 15) >> 1)] += rs;
-        };
-#pragma unroll
-        for (int j = 0; j < NPW; ++j)
-            if (j < nk0) pair(std::integral_constant<int, 0>{}, j, kmin0 + j);
-        if constexpr (NQ == 2) {
-#pragma unroll
-            for (int j = 0; j < NPW; ++j)
-                if (j >= nk0 && j < npw) pair(std::integral_constant<int, 1>{}, j, kmin1 + j - nk0);
-        }
-
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int t = 16 * (q ? T1 : T0) + col;
             const bool valid = t < len;
             const int tc = valid ? t : len - 1;
-            // the W_c term: dx^T += W^T (e^{cs_e - cs_t} B_t)
-            const float sB = valid ? fast_exp2(cse - cst[q]) : 0.f;
+            const float cst = rcs[t], dtt = rdt[t];
+            bf16x8 bq[KS];  // B_t, for the W_c term after the pairs
             const bf16* brow = Bm + ((b * L + t0 + tc) * G + g) * N + 8 * grp;
 #pragma unroll
+            for (int ks = 0; ks < KS; ++ks) bq[ks] = load_frag(brow + 32 * ks);
+            f32x4 acc[4];
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt) acc[pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            float ct = 0.f;
+            auto pair = [&](int j, int K) __attribute__((always_inline)) {
+                f32x4 g2[2];
+#pragma unroll
+                for (int uu = 0; uu < 2; ++uu) {
+                    const int s = 32 * K + gram_row(uu, col);
+                    const bf16x8 a0 = frag_rowmajor<bf16, XRB>(dyt, s, 8 * grp);
+                    const bf16x8 a1 = frag_rowmajor<bf16, XRB>(dyt, s, 32 + 8 * grp);
+                    g2[uu] = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, a0, xf[q][0]), a1, xf[q][1]);
+                }
+                float f[8];
+                const int sb = 32 * K + 8 * grp;
+                if (K > (T >> 1)) {
+                    const float at = fast_exp2(rcs[32 * K] - cst);
+                    const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + sb);
+                    const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + sb + 4);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        f[i] = b0[i] * at;
+                        f[4 + i] = b1[i] * at;
+                    }
+                } else {
+                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(rcs + sb);
+                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + sb + 4);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        f[i] = (sb + i >= t && sb + i < len) ? fast_exp2(c0[i] - cst) : 0.f;
+                        f[4 + i] = (sb + 4 + i >= t && sb + 4 + i < len) ? fast_exp2(c1[i] - cst) : 0.f;
+                    }
+                }
+                bf16x8 m1;
+                float rv[8];
+                // opaque copy: keeps the bf16 -> float conversion of the cached
+                // Gram values inside the head loop (hoisted, it would hold 8
+                // floats per pair live across heads)
+                typedef int i32x4 __attribute__((ext_vector_type(4)));
+                i32x4 graw = __builtin_bit_cast(i32x4, g1c[j]);
+                asm volatile("" : "+v"(graw));
+                const bf16x8 gj = __builtin_bit_cast(bf16x8, graw);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float gv = e < 4 ? g2[0][e] : g2[1][e - 4];
+                    m1[e] = (bf16)((float)gj[e] * f[e]);
+                    const float d = (float)m1[e] * gv;
+                    ct += d;
+                    rv[e] = d * dtt;
+                }
+#pragma unroll
+                for (int pt = 0; pt < 4; ++pt) acc[pt] = mma16(acc[pt], ko[pt].read(dyt, 32 * K * XRB), m1);
+                const float rs = lane_sums<8, 16>(rv, lane);
+                if ((lane & 1) == 0) rpart[wave][sb + ((lane & 15) >> 1)] += rs;
+                // keep the scheduler from interleaving pairs (register pressure)
+                __builtin_amdgcn_sched_barrier(0);
+            };
+            if (q == 0) {
+#pragma unroll
+                for (int j = 0; j < NPW; ++j)
+                    if (j < nk0) pair(j, kmin0 + j);
+            } else {
+#pragma unroll
+                for (int j = 0; j < NPW; ++j)
+                    if (j >= nk0 && j < npw) pair(j, kmin1 + j - nk0);
+            }
+            if (hh + 1 < hpb) {  // this tile's x_t of the next head
+                const bf16* xr = x + ((b * L + t0 + tc) * H + h + 1) * kP + 8 * grp;
+                xf[q][0] = load_frag(xr);
+                xf[q][1] = load_frag(xr + 32);
+            }
+            // the W_c term: dx^T += W^T (e^{cs_e - cs_t} B_t)
+            const float sB = valid ? fast_exp2(cse - cst) : 0.f;
+#pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 bfr = scale_frag(load_frag(brow + 32 * ks), sB);
+                const bf16x8 bfr = scale_frag(bq[ks], sB);
 #pragma unroll
-                for (int pt = 0; pt < 4; ++pt) acc[q][pt] = mma16(acc[q][pt], ko[pt].read(wtl, 32 * ks * XRB), bfr);
+                for (int pt = 0; pt < 4; ++pt) acc[pt] = mma16(acc[pt], ko[pt].read(wtl, 32 * ks * XRB), bfr);
             }
-            // acc[q][pt][i] = (B_t Lam_t)[p = 16 pt + 4 grp + i]
-            const bf16* xr = x + ((b * L + t0 + tc) * H + h) * kP + 4 * grp;
-            float dir = 0.f;
-#pragma unroll
-            for (int pt = 0; pt < 4; ++pt) {
-                const bf16x4 xv = *reinterpret_cast<const bf16x4*>(xr + 16 * pt);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) dir += (float)xv[i] * acc[q][pt][i];
-            }
-            dir += __shfl_xor(dir, 16, 64);
-            dir += __shfl_xor(dir, 32, 64);
-            float cq = ct[q];
-            cq += __shfl_xor(cq, 16, 64);
-            cq += __shfl_xor(cq, 32, 64);
+            // acc[pt][i] = (B_t Lam_t)[p = 16 pt + 4 grp + i]
+            ct += __shfl_xor(ct, 16, 64);
+            ct += __shfl_xor(ct, 32, 64);
             if (valid) {
                 float* dxr = dx + ((b * L + t0 + t) * H + h) * kP + 4 * grp;
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
-                    f32x4 v = acc[q][pt];
+                    f32x4 v = acc[pt];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) v[i] *= dtt[q];
+                    for (int i = 0; i < 4; ++i) v[i] *= dtt;
                     *reinterpret_cast<f32x4*>(dxr + 16 * pt) = v;
                 }
             }
-            if (grp == 0) {
-                tok[0][t] = dtt[q] * cq;
-                tok[1][t] = dtt[q] * (dir - cq);
-                tok[2][t] = dir;
-            }
+            if (grp == 0) tok[0][t] = ct;
         }
+        if (hh + 1 < hpb) store_rec(u ^ 1);
         lds_barrier();
         if (wave == 0) {
-            // dL/dl_t = sum_{s>=t} (r_s - c_s + w_s) + sum_{s<t} v_s + K_c
-            float av[TPL], vv[TPL], asum = 0.f, vsum = 0.f;
+            // dL/dl_t = sum_{s>=t} (r_s - c_s + w_s) + sum_{s<t} v_s + K_c with
+            // c_s = dt_s c~_s, v_s = dt_s v~_s; (B Lam) . x = c~ + v~
+            float av[TPL], vv[TPL], dir[TPL], asum = 0.f, vsum = 0.f;
 #pragma unroll
             for (int k = 0; k < TPL; ++k) {
                 const int tt = TPL * lane + k;
                 float r = 0.f;
 #pragma unroll
                 for (int w = 0; w < NW; ++w) r += rpart[w][tt];
-                const float wq = tt < len ? wp[(b * L + t0 + tt) * H + h] : 0.f;
-                av[k] = r - tok[0][tt] + wq;
-                vv[k] = tok[1][tt];
+                const float d = rdt[tt];
+                const float cc = tok[0][tt];
+                const float vtil = tt < len ? vt[(b * L + t0 + tt) * H + h] : 0.f;
+                av[k] = r - d * cc + wq[k];
+                vv[k] = d * vtil;
+                dir[k] = cc + vtil;
                 asum += av[k];
                 vsum += vv[k];
             }
@@ -770,8 +856,9 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 }
             }
             const float atot = __shfl(ai, 63, 64);
-            float kc = 0.f;
-            for (int k = 0; k < nkp; ++k) kc += Kp[((b * H + h) * M + c) * nkp + k];
+            float kc = kq;
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) kc += __shfl_xor(kc, o, 64);
             float suf = atot - (ai - asum);  // sum over s >= first token of this lane
             float pre = vi - vsum;           // sum over s < first token of this lane
             float dA = 0.f;
@@ -780,7 +867,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 const int tt = TPL * lane + k;
                 const float dl = suf + pre + kc;
                 if (tt < len) {
-                    ddt[(b * L + t0 + tt) * H + h] = tok[2][tt] + Ah * dl;
+                    ddt[(b * L + t0 + tt) * H + h] = dir[k] + Ah * dl;
                     dA += rdt[tt] * dl;
                 }
                 suf -= av[k];
@@ -791,7 +878,6 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
             if (lane == 0) dAp[(b * M + c) * H + h] = dA;
         }
     }
-
 }
 
 // ---------------------------------------------------------------------------
@@ -858,13 +944,18 @@ __global__ __launch_bounds__(512) void k_sbwd_bc(const bf16* __restrict__ mbar, 
     }
 }
 
+// one block per head: a fixed-order tree sum over (b, c)
 __global__ __launch_bounds__(256) void k_sbwd_dA(const float* __restrict__ dAp, float* __restrict__ dA,
                                                  int64_t BM, int H) {
-    for (int h = threadIdx.x; h < H; h += 256) {
-        float s = 0.f;
-        for (int64_t k = 0; k < BM; ++k) s += dAp[k * H + h];
-        dA[h] = s;
-    }
+    __shared__ float red[4];
+    const int h = blockIdx.x, tid = threadIdx.x;
+    float s = 0.f;
+    for (int64_t k = tid; k < BM; k += 256) s += dAp[k * H + h];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+    if ((tid & 63) == 0) red[tid >> 6] = s;
+    __syncthreads();
+    if (tid == 0) dA[h] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
 // heads per workgroup of the contraction and quadratic kernels
@@ -886,6 +977,7 @@ struct MfmaWs {
     bf16* Wb;
     float* Kp;    // [B][H][M][nkp]
     float* wp;    // [B][L][H]
+    float* vt;    // [B][L][H]
     float* dAp;   // [B][M][H]
     bf16* mbar;   // [B][M][G][S][S]
     int nkp;
@@ -915,6 +1007,7 @@ MfmaWs mfma_layout(const Shape& s, void* base) {
     w.Wb = (bf16*)take(2 * BHM * NP);
     w.Kp = (float*)take(4 * BHM * w.nkp);
     w.wp = (float*)take(4 * (size_t)s.B * s.L * s.H);
+    w.vt = (float*)take(4 * (size_t)s.B * s.L * s.H);
     w.dAp = (float*)take(4 * BHM);
     w.mbar = (bf16*)take(2 * BMG * (size_t)s.S * s.S);
     w.total = o;
@@ -943,18 +1036,19 @@ hipError_t run_mfma(const Shape& s, const bf16* x, const float* dt, const float*
         w.dH, w.dR, w.lda, h0, dmem, dhl, w.Hb, w.Wb, w.Kp, dh0, s.H, NP, s.M, s.Mcap);
     prof_end(st);
     prof_begin("k_sbwd_group", st);
-    k_sbwd_group<N, S><<<(unsigned)(nbcg * (S / 64)), 512, 0, st>>>(x, dt, Cm, dy, w.rec, w.Hb, w.Wb, dB, dC,
-                                                                    w.wp, w.mbar, s.L, s.H, s.G, s.M, nbcg);
+    k_sbwd_group<N, S><<<(unsigned)(nbcg * (S / 64)), 512, 0, st>>>(x, dt, Bm, Cm, dy, w.rec, w.Hb, w.Wb, dB,
+                                                                    dC, w.wp, w.vt, w.mbar, s.L, s.H, s.G, s.M,
+                                                                    nbcg);
     prof_end(st);
     prof_begin("k_sbwd_quad", st);
-    k_sbwd_quad<N, S><<<grid, 64 * quad_waves<S>(), 0, st>>>(x, dt, A, Bm, Cm, dy, w.rec, w.Wb, w.Kp, w.wp, dx,
+    k_sbwd_quad<N, S><<<grid, 64 * quad_waves<S>(), 0, st>>>(x, dt, A, Bm, Cm, dy, w.rec, w.Wb, w.Kp, w.wp, w.vt, dx,
                                                              ddt, w.dAp, s.L, s.H, s.G, s.M, hpb, nbcg, w.nkp);
     prof_end(st);
     prof_begin("k_sbwd_bc", st);
     k_sbwd_bc<N, S><<<(unsigned)nbcg, 512, 0, st>>>(w.mbar, w.BT, w.CT, dB, dC, s.L, s.G, s.M);
     prof_end(st);
     prof_begin("k_sbwd_dA", st);
-    k_sbwd_dA<<<1, 256, 0, st>>>(w.dAp, dA, s.B * s.M, s.H);
+    k_sbwd_dA<<<(unsigned)s.H, 256, 0, st>>>(w.dAp, dA, s.B * s.M, s.H);
     prof_end(st);
     return hipGetLastError();
 }
