@@ -37,7 +37,7 @@
 //
 // Kernels, in launch order:
 //   k_sbwd_contract<0>  per (b, c, g, head slice): dH_[c] = B^T diag(e^{cs_e - cs} dt) x
-//                       (fp32), the chunk's cumulative log decay, and B^T of
+//                       (bf16), the chunk's cumulative log decay, and B^T of
 //                       the chunk (bf16, [N][S]);
 //   k_sbwd_contract<1>  the same for dR_c = C^T diag(e^{cs}) dy and C^T;
 //   k_sbwd_pass2        per (b, h, 1024 state elements): forward over chunks
@@ -78,6 +78,33 @@ __device__ __forceinline__ bf16x8 scale_frag(bf16x8 v, float s) {
     return r;
 }
 
+// k-major fragment reads (as KmOffBf16) whose 16 columns are spread:
+// column c = 0..15 of the fragment is tile column cbase + 8 (c / 4) + c % 4.
+// With cbase = 32 (pt / 2) + 4 (pt % 2), the accumulator rows 4 g + i of the
+// four p tiles pt are the columns 8 g + j and 32 + 8 g + j (j = 4 (pt % 2) + i),
+// the k order of the row-major x_t fragments, so x_t . acc needs no exchange.
+template <int RB>
+struct KmOffSpread {
+    uint32_t o0, o1;
+    __device__ __forceinline__ void init(int ra, int rb, int cbase, int lane) {
+        using Tl = SwzTile<RB>;
+        const int j = lane & 15;
+        const int col_b = (cbase + 8 * (j & 3)) * 2;
+        o0 = (uint32_t)Tl::off(ra + (j >> 2), col_b);
+        o1 = (uint32_t)Tl::off(rb + (j >> 2), col_b);
+    }
+    __device__ __forceinline__ bf16x8 read(const char* tile, int add) const {
+        const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(tile + add + o0));
+        const s16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(tile + add + o1));
+        const bf16x4 b0 = __builtin_bit_cast(bf16x4, v0);
+        const bf16x4 b1 = __builtin_bit_cast(bf16x4, v1);
+        return bf16x8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+    }
+};
+__device__ __forceinline__ int spread_base(int pt) { return 32 * (pt >> 1) + 4 * (pt & 1); }
+
 // block -> (b c g, head slice); the slices of one (b, c, g) share an XCD
 __device__ __forceinline__ void block_bcg(int64_t nbcg, int nhs, int64_t& bcg, int& hs) {
     const int64_t bid = blockIdx.x;
@@ -92,8 +119,8 @@ __device__ __forceinline__ void block_bcg(int64_t nbcg, int nhs, int64_t& bcg, i
 }
 
 // ---------------------------------------------------------------------------
-// Chunk contraction out[n][p] = sum_s w_s Am[s][n] V[s][p] per head, 512
-// threads.  MODE 0: Am = B, V = x, w_s = e^{cs_e - cs_s} dt_s (the chunk's own
+// Chunk contraction out[n][p] = sum_s w_s Am[s][n] V[s][p] per head (bf16
+// out), 512 threads.  MODE 0: Am = B, V = x, w_s = e^{cs_e - cs_s} dt_s (the chunk's own
 // state contribution dH); also records cs (log2 units) and the chunk's total
 // log decay.  MODE 1: Am = C, V = dy, w_s = e^{cs_s} (the chunk adjoint dR).
 // Am^T fragments are read once (k-major from the LDS tile) and kept for every
@@ -106,7 +133,7 @@ __device__ __forceinline__ void block_bcg(int64_t nbcg, int nhs, int64_t& bcg, i
 template <int N, int S, int MODE>
 __global__ __launch_bounds__(512) void k_sbwd_contract(
     const bf16* __restrict__ Am, const bf16* __restrict__ V, const float* __restrict__ dt,
-    const float* __restrict__ A, float* __restrict__ out, float* __restrict__ rec,
+    const float* __restrict__ A, bf16* __restrict__ out, float* __restrict__ rec,
     float* __restrict__ lda, bf16* __restrict__ AmT, int64_t L, int H, int G, int64_t M, int hpb,
     int64_t nbcg) {
     constexpr int NW = 8, NT = 512;
@@ -245,14 +272,14 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
             }
         }
         // acc[j][k][i] = out[n = 16 (ng NTW + j) + 4 grp + i][p = 16 (pg PTW + k) + col]
-        float* dst = out + ((b * M + c) * H + hbase + hh) * (int64_t)N * kP;
+        bf16* dst = out + ((b * M + c) * H + hbase + hh) * (int64_t)N * kP;
 #pragma unroll
         for (int j = 0; j < NTW; ++j)
 #pragma unroll
             for (int k = 0; k < PTW; ++k)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    dst[(16 * (ng * NTW + j) + 4 * grp + i) * kP + 16 * (pg * PTW + k) + col] = acc[j][k][i];
+                    dst[(16 * (ng * NTW + j) + 4 * grp + i) * kP + 16 * (pg * PTW + k) + col] = (bf16)acc[j][k][i];
     }
 }
 
@@ -263,7 +290,7 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
 // (-> Kp[b][h][c][block]) and R_{c-1} = e^{lda_c} R_c + dR_c; dh0 = R_{-1}.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_sbwd_pass2(
-    const float* __restrict__ dH, const float* __restrict__ dR, const float* __restrict__ lda,
+    const bf16* __restrict__ dH, const bf16* __restrict__ dR, const float* __restrict__ lda,
     const float* __restrict__ h0, const float* __restrict__ dmem, const float* __restrict__ dhl,
     bf16* __restrict__ Hb, bf16* __restrict__ Wb, float* __restrict__ Kp, float* __restrict__ dh0,
     int H, int NP, int64_t M, int64_t Mcap) {
@@ -322,8 +349,7 @@ __global__ __launch_bounds__(256) void k_sbwd_pass2(
 //   the rank-P terms dB_t += dt_t e^{cs_e - cs_t} W_c x_t and
 //   dC_s += e^{cs_s} H_[c-1] dy_s ([n][t] tiles: A = W or H rows from LDS,
 //   B = the scaled x or dy rows of the token tile), per head
-//   w_s = e^{cs_s} C_s . (H_[c-1] dy_s) and v~_t = e^{cs_e - cs_t} B_t . (W_c x_t),
-//   and
+//   w_s = e^{cs_s} C_s . (H_[c-1] dy_s), and
 //   Mbar[s][t] = sum_h dt_t e^{cs_s - cs_t} (dy_s . x_t) for the set's token
 //   columns (t <= s), in fp32 registers across the heads.
 // Set q holds tiles q, NKB - 1 - q, NKB + q and 2 NKB - 1 - q (NKB = S / 32),
@@ -334,11 +360,11 @@ __global__ __launch_bounds__(256) void k_sbwd_pass2(
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(512) void k_sbwd_group(
-    const bf16* __restrict__ x, const float* __restrict__ dt, const bf16* __restrict__ Bm,
-    const bf16* __restrict__ Cm, const bf16* __restrict__ dy, const float* __restrict__ rec,
-    const bf16* __restrict__ Hb, const bf16* __restrict__ Wb, float* __restrict__ dB,
-    float* __restrict__ dC, float* __restrict__ wp, float* __restrict__ vt, bf16* __restrict__ mbar, int64_t L, int H, int G,
-    int64_t M, int64_t nbcg) {
+    const bf16* __restrict__ x, const float* __restrict__ dt, const bf16* __restrict__ Cm,
+    const bf16* __restrict__ dy, const float* __restrict__ rec, const bf16* __restrict__ Hb,
+    const bf16* __restrict__ Wb, float* __restrict__ dB, float* __restrict__ dC,
+    float* __restrict__ wp, bf16* __restrict__ mbar, int64_t L, int H, int G, int64_t M,
+    int64_t nbcg) {
     constexpr int NW = 8, NT = 512;
     constexpr int XRB = kP * 2;
     constexpr int DYT = S * XRB, TT = N * XRB, RECB = 3 * S * 4;
@@ -369,7 +395,6 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
 
     __shared__ __attribute__((aligned(16))) char ubuf[2][UB];
     __shared__ float wpart[2][2][64];
-    __shared__ float vpart[2][2][64];
 
     auto issue = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = g * hpg + hh;
@@ -400,14 +425,11 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
             r[2 * S + tid] = tid < len ? fast_exp2(rq[0] - rq[2]) : 0.f;
         }
     };
-    // B_t and C_t at the n rows this lane's accumulators hold (16 nt + 4 grp + i)
-    bf16x4 bv[NTH], cv[NTH];
+    // C_t at the n rows this lane's accumulators hold (16 nt + 4 grp + i)
+    bf16x4 cv[NTH];
 #pragma unroll
-    for (int j = 0; j < NTH; ++j) {
-        const int64_t o = ((b * L + t0 + tc) * G + g) * N + (nh * NTH + j) * 16 + 4 * grp;
-        bv[j] = *reinterpret_cast<const bf16x4*>(Bm + o);
-        cv[j] = *reinterpret_cast<const bf16x4*>(Cm + o);
-    }
+    for (int j = 0; j < NTH; ++j)
+        cv[j] = *reinterpret_cast<const bf16x4*>(Cm + ((b * L + t0 + tc) * G + g) * N + (nh * NTH + j) * 16 + 4 * grp);
     f32x4 accB[NTH], accC[NTH];
 #pragma unroll
     for (int j = 0; j < NTH; ++j) {
@@ -444,9 +466,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
         }
         if (hh > 0 && nh == 0 && grp == 0 && valid) {
             const int tl = slot * 16 + col;
-            const int64_t o = (b * L + t0 + t) * H + h - 1;
-            wp[o] = wpart[u ^ 1][0][tl] + wpart[u ^ 1][1][tl];
-            vt[o] = vpart[u ^ 1][0][tl] + vpart[u ^ 1][1][tl];
+            wp[(b * L + t0 + t) * H + h - 1] = wpart[u ^ 1][0][tl] + wpart[u ^ 1][1][tl];
         }
         const char* dyt = &ubuf[u][0];
         const char* wtl = &ubuf[u][DYT];
@@ -454,39 +474,32 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
         const float* rcs = reinterpret_cast<const float*>(&ubuf[u][DYT + 2 * TT]);
         const float* rbs = rcs + 2 * S;
         const float cst = rcs[t], dtt = rcs[S + t], cse = rcs[S - 1];
-        const float sx = valid ? fast_exp2(cse - cst) : 0.f;
+        const float sx = valid ? dtt * fast_exp2(cse - cst) : 0.f;
         const float sy = valid ? fast_exp2(cst) : 0.f;
         const bf16x8 xs0 = scale_frag(xf0, sx), xs1 = scale_frag(xf1, sx);
         const bf16x8 ys0 = scale_frag(frag_rowmajor<bf16, XRB>(dyt, tc, 8 * grp), sy);
         const bf16x8 ys1 = scale_frag(frag_rowmajor<bf16, XRB>(dyt, tc, 32 + 8 * grp), sy);
-        // W x^ (x^ = e^{cs_e - cs_t} x_t): dB_t += dt_t W x^, v~_t = B_t . W x^;
-        // H dy^ (dy^ = e^{cs_t} dy_t): dC_t += H dy^, w_t = C_t . H dy^
-        float wsum = 0.f, vsum = 0.f;
+        // dB_t += W (dt_t e^{cs_e - cs_t} x_t); H dy^ (dy^ = e^{cs_t} dy_t):
+        // dC_t += H dy^, w_t = C_t . H dy^
+        float wsum = 0.f;
 #pragma unroll
         for (int j = 0; j < NTH; ++j) {
             const int nrow = (nh * NTH + j) * 16 + col;
             const bf16x8 w0 = frag_rowmajor<bf16, XRB>(wtl, nrow, 8 * grp);
             const bf16x8 w1 = frag_rowmajor<bf16, XRB>(wtl, nrow, 32 + 8 * grp);
-            const f32x4 tv = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, w0, xs0), w1, xs1);
+            accB[j] = mma16(mma16(accB[j], w0, xs0), w1, xs1);
             const bf16x8 h0f = frag_rowmajor<bf16, XRB>(htl, nrow, 8 * grp);
             const bf16x8 h1f = frag_rowmajor<bf16, XRB>(htl, nrow, 32 + 8 * grp);
             const f32x4 tmp = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, h0f, ys0), h1f, ys1);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                vsum += (float)bv[j][i] * tv[i];
-                accB[j][i] += dtt * tv[i];
                 wsum += (float)cv[j][i] * tmp[i];
                 accC[j][i] += tmp[i];
             }
         }
         wsum += __shfl_xor(wsum, 16, 64);
         wsum += __shfl_xor(wsum, 32, 64);
-        vsum += __shfl_xor(vsum, 16, 64);
-        vsum += __shfl_xor(vsum, 32, 64);
-        if (grp == 0) {
-            wpart[u][nh][slot * 16 + col] = wsum;
-            vpart[u][nh][slot * 16 + col] = vsum;
-        }
+        if (grp == 0) wpart[u][nh][slot * 16 + col] = wsum;
         // Mbar pairs (tile T, s block K): A = dy rows in gram_row order, B = x_t
 #pragma unroll
         for (int k = 0; k < MPW; ++k) {
@@ -527,9 +540,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
     if (nh == 0 && grp == 0 && valid) {
         const int u = (hpg - 1) & 1;
         const int tl = slot * 16 + col;
-        const int64_t o = (b * L + t0 + t) * H + g * hpg + hpg - 1;
-        wp[o] = wpart[u][0][tl] + wpart[u][1][tl];
-        vt[o] = vpart[u][0][tl] + vpart[u][1][tl];
+        wp[(b * L + t0 + t) * H + g * hpg + hpg - 1] = wpart[u][0][tl] + wpart[u][1][tl];
     }
     if (valid) {
         const int64_t row = ((b * L + t0 + t) * G + g) * N;
@@ -561,20 +572,22 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
 //   (b_s = e^{cs_s - cs_K} from LDS, one exp per lane), exact and masked on
 //   the diagonal block;
 //   M1 = bf16(G1 decay) -> dx^T += dy^T M1 (A = dy^T by transposing reads);
-//   D = M1 G2 dt_t -> c~_t (lane sums) and r_s (LDS, per wave).
-// Then dx^T += W^T (e^{cs_e - cs_t} B_t) (A = W^T from LDS), dx = dt acc, and
-// the chunk scan of dL/dl (one wave) -> ddt = (B Lam) . x + A_h dL/dl, with
-// (B Lam) . x = c~_t + v~_t (v~ from k_sbwd_group), and the chunk's dA
-// partial.  Each wave finishes one row tile before the next.
+//   D = M1 G2 dt_t -> r_s (lane sums into LDS, per wave).
+// The Gram's B operand is x~_t = bf16(dt_t x_t), so D = M1 (dy_s . x~_t) and
+// c_t = x~_t . acc (acc = sum_s M1[s,t] dy_s) hold the same products.  Then
+// dx^T += W^T (e^{cs_e - cs_t} B_t) (A = W^T from LDS), dx = dt acc,
+// v_t = x~_t . (W term), (B Lam) . x = x_t . acc (the accumulator rows are
+// spread to the k order of the x_t fragments, see KmOffSpread), and the chunk
+// scan of dL/dl (one wave) -> ddt = (B Lam) . x + A_h dL/dl and the chunk's
+// dA partial.  Each wave finishes one row tile before the next.
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     const bf16* __restrict__ x, const float* __restrict__ dt, const float* __restrict__ A,
     const bf16* __restrict__ Bm, const bf16* __restrict__ Cm, const bf16* __restrict__ dy,
     const float* __restrict__ rec, const bf16* __restrict__ Wb, const float* __restrict__ Kp,
-    const float* __restrict__ wp, const float* __restrict__ vt, float* __restrict__ dx,
-    float* __restrict__ ddt, float* __restrict__ dAp, int64_t L, int H, int G, int64_t M, int hpb,
-    int64_t nbcg, int nkp) {
+    const float* __restrict__ wp, float* __restrict__ dx, float* __restrict__ ddt,
+    float* __restrict__ dAp, int64_t L, int H, int G, int64_t M, int hpb, int64_t nbcg, int nkp) {
     constexpr int NW = quad_waves<S>();
     constexpr int NT = 64 * NW;
     constexpr int NQ = S / 16 / NW;
@@ -604,7 +617,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
 
     __shared__ __attribute__((aligned(16))) char ubuf[2][UB];
     __shared__ float rpart[NW][S];
-    __shared__ float tok[1][S];
+    __shared__ float tok[3][S];
 
     auto issue = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = hbase + hh;
@@ -671,9 +684,9 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
             }
         }
     }
-    KmOffBf16<XRB> ko[4];  // transposing reads of dy^T (k = s) and W^T (k = n), p tile pt
+    KmOffSpread<XRB> ko[4];  // transposing reads of dy^T (k = s) and W^T (k = n), p tile pt
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) ko[pt].init(8 * grp, 8 * grp + 4, 16 * pt, lane);
+    for (int pt = 0; pt < 4; ++pt) ko[pt].init(8 * grp, 8 * grp + 4, spread_base(pt), lane);
 
     // x_t fragments of the wave's tiles (each reloaded for the next head once
     // its tile's pairs are done)
@@ -731,10 +744,13 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
             const bf16* brow = Bm + ((b * L + t0 + tc) * G + g) * N + 8 * grp;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) bq[ks] = load_frag(brow + 32 * ks);
+            // x~_t = bf16(dt_t x_t): the Gram B operand, so that r_s (row sums of
+            // D = M1 (dy_s . x~_t)) and c_t = x~_t . (sum_s M1[s,t] dy_s) hold the
+            // same products
+            const bf16x8 xt0 = scale_frag(xf[q][0], dtt), xt1 = scale_frag(xf[q][1], dtt);
             f32x4 acc[4];
 #pragma unroll
             for (int pt = 0; pt < 4; ++pt) acc[pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-            float ct = 0.f;
             auto pair = [&](int j, int K) __attribute__((always_inline)) {
                 f32x4 g2[2];
 #pragma unroll
@@ -742,7 +758,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                     const int s = 32 * K + gram_row(uu, col);
                     const bf16x8 a0 = frag_rowmajor<bf16, XRB>(dyt, s, 8 * grp);
                     const bf16x8 a1 = frag_rowmajor<bf16, XRB>(dyt, s, 32 + 8 * grp);
-                    g2[uu] = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, a0, xf[q][0]), a1, xf[q][1]);
+                    g2[uu] = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, a0, xt0), a1, xt1);
                 }
                 float f[8];
                 const int sb = 32 * K + 8 * grp;
@@ -775,11 +791,8 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 const bf16x8 gj = __builtin_bit_cast(bf16x8, graw);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const float gv = e < 4 ? g2[0][e] : g2[1][e - 4];
                     m1[e] = (bf16)((float)gj[e] * f[e]);
-                    const float d = (float)m1[e] * gv;
-                    ct += d;
-                    rv[e] = d * dtt;
+                    rv[e] = (float)m1[e] * (e < 4 ? g2[0][e] : g2[1][e - 4]);
                 }
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) acc[pt] = mma16(acc[pt], ko[pt].read(dyt, 32 * K * XRB), m1);
@@ -797,11 +810,17 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 for (int j = 0; j < NPW; ++j)
                     if (j >= nk0 && j < npw) pair(j, kmin1 + j - nk0);
             }
-            if (hh + 1 < hpb) {  // this tile's x_t of the next head
-                const bf16* xr = x + ((b * L + t0 + tc) * H + h + 1) * kP + 8 * grp;
-                xf[q][0] = load_frag(xr);
-                xf[q][1] = load_frag(xr + 32);
-            }
+            // x . acc for the fragment x (k order 8 g + j, 32 + 8 g + j)
+            auto xdot = [&](bf16x8 f0, bf16x8 f1) __attribute__((always_inline)) {
+                float d = 0.f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    d += (float)f0[i] * acc[0][i] + (float)f0[4 + i] * acc[1][i] + (float)f1[i] * acc[2][i] +
+                         (float)f1[4 + i] * acc[3][i];
+                d += __shfl_xor(d, 16, 64);
+                return d + __shfl_xor(d, 32, 64);
+            };
+            const float cq = xdot(xt0, xt1);  // c_t = dt_t c~_t
             // the W_c term: dx^T += W^T (e^{cs_e - cs_t} B_t)
             const float sB = valid ? fast_exp2(cse - cst) : 0.f;
 #pragma unroll
@@ -810,39 +829,43 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) acc[pt] = mma16(acc[pt], ko[pt].read(wtl, 32 * ks * XRB), bfr);
             }
-            // acc[pt][i] = (B_t Lam_t)[p = 16 pt + 4 grp + i]
-            ct += __shfl_xor(ct, 16, 64);
-            ct += __shfl_xor(ct, 32, 64);
+            // acc[pt][i] = (B_t Lam_t)[p = spread_base(pt) + 8 grp + i]
+            const float cw = xdot(xt0, xt1);
+            const float dir = xdot(xf[q][0], xf[q][1]);  // (B_t Lam_t) . x_t
+            if (hh + 1 < hpb) {  // this tile's x_t of the next head
+                const bf16* xr = x + ((b * L + t0 + tc) * H + h + 1) * kP + 8 * grp;
+                xf[q][0] = load_frag(xr);
+                xf[q][1] = load_frag(xr + 32);
+            }
             if (valid) {
-                float* dxr = dx + ((b * L + t0 + t) * H + h) * kP + 4 * grp;
+                float* dxr = dx + ((b * L + t0 + t) * H + h) * kP + 8 * grp;
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
                     f32x4 v = acc[pt];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) v[i] *= dtt;
-                    *reinterpret_cast<f32x4*>(dxr + 16 * pt) = v;
+                    *reinterpret_cast<f32x4*>(dxr + spread_base(pt)) = v;
                 }
             }
-            if (grp == 0) tok[0][t] = ct;
+            if (grp == 0) {
+                tok[0][t] = cq;
+                tok[1][t] = cw - cq;  // v_t = dt_t v~_t
+                tok[2][t] = dir;
+            }
         }
         if (hh + 1 < hpb) store_rec(u ^ 1);
         lds_barrier();
         if (wave == 0) {
-            // dL/dl_t = sum_{s>=t} (r_s - c_s + w_s) + sum_{s<t} v_s + K_c with
-            // c_s = dt_s c~_s, v_s = dt_s v~_s; (B Lam) . x = c~ + v~
-            float av[TPL], vv[TPL], dir[TPL], asum = 0.f, vsum = 0.f;
+            // dL/dl_t = sum_{s>=t} (r_s - c_s + w_s) + sum_{s<t} v_s + K_c
+            float av[TPL], vv[TPL], asum = 0.f, vsum = 0.f;
 #pragma unroll
             for (int k = 0; k < TPL; ++k) {
                 const int tt = TPL * lane + k;
                 float r = 0.f;
 #pragma unroll
                 for (int w = 0; w < NW; ++w) r += rpart[w][tt];
-                const float d = rdt[tt];
-                const float cc = tok[0][tt];
-                const float vtil = tt < len ? vt[(b * L + t0 + tt) * H + h] : 0.f;
-                av[k] = r - d * cc + wq[k];
-                vv[k] = d * vtil;
-                dir[k] = cc + vtil;
+                av[k] = r - tok[0][tt] + wq[k];
+                vv[k] = tok[1][tt];
                 asum += av[k];
                 vsum += vv[k];
             }
@@ -867,7 +890,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 const int tt = TPL * lane + k;
                 const float dl = suf + pre + kc;
                 if (tt < len) {
-                    ddt[(b * L + t0 + tt) * H + h] = dir[k] + Ah * dl;
+                    ddt[(b * L + t0 + tt) * H + h] = tok[2][tt] + Ah * dl;
                     dA += rdt[tt] * dl;
                 }
                 suf -= av[k];
@@ -881,7 +904,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
 }
 
 // ---------------------------------------------------------------------------
-// Per (b, c, g): Mbar (causal blocks) into LDS, then dB^T[n][t] += C^T Mbar (k = s >= t; A = C^T rows from
+// Per (b, c, g, half of the n tiles): Mbar (causal blocks) into LDS, then dB^T[n][t] += C^T Mbar (k = s >= t; A = C^T rows from
 // the chunk's C^T, B = Mbar by transposing reads) and dC^T[n][s] += B^T Mbar^T
 // (k = t <= s; B = Mbar rows).
 // ---------------------------------------------------------------------------
@@ -894,7 +917,8 @@ __global__ __launch_bounds__(512) void k_sbwd_bc(const bf16* __restrict__ mbar, 
     constexpr int NKB = S / 32;
     constexpr int NTILE = S / 16, NNT = N / 16;
     __shared__ __attribute__((aligned(16))) char mt[S * RB];
-    const int64_t bcg = blockIdx.x;
+    const int64_t bcg = blockIdx.x >> 1;
+    const int nhalf = blockIdx.x & 1;  // n tiles [nhalf NNT/2, (nhalf + 1) NNT/2)
     const int g = (int)(bcg % G);
     const int64_t bc = bcg / G;
     const int64_t b = bc / M, c = bc % M;
@@ -916,10 +940,11 @@ __global__ __launch_bounds__(512) void k_sbwd_bc(const bf16* __restrict__ mbar, 
     const bf16* bt = BT + bcg * (int64_t)N * S;
     const bf16* ct = CT + bcg * (int64_t)N * S;
     KmOffBf16<RB> mo;
-    for (int tileid = wave; tileid < NTILE * NNT * 2; tileid += NW) {
-        const bool isB = tileid < NTILE * NNT;
-        const int id = isB ? tileid : tileid - NTILE * NNT;
-        const int T = id / NNT, nt = id % NNT;
+    constexpr int NNH = NNT / 2;  // n tiles of this workgroup
+    for (int tileid = wave; tileid < NTILE * NNH * 2; tileid += NW) {
+        const bool isB = tileid < NTILE * NNH;
+        const int id = isB ? tileid : tileid - NTILE * NNH;
+        const int T = id / NNH, nt = nhalf * NNH + id % NNH;
         const int tk = 16 * T + col;  // token of this lane's column
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
         if (isB) {
@@ -969,15 +994,14 @@ int mfma_hpb(const Shape& s) {
 struct MfmaWs {
     float* rec;   // [B][H][M][S] cs (log2)
     float* lda;   // [B][H][M]
-    float* dH;    // [B][M][H][N][P]
-    float* dR;
+    bf16* dH;     // [B][M][H][N][P]
+    bf16* dR;
     bf16* BT;     // [B][M][G][N][S]
     bf16* CT;
     bf16* Hb;     // [B][M][H][N][P]
     bf16* Wb;
     float* Kp;    // [B][H][M][nkp]
     float* wp;    // [B][L][H]
-    float* vt;    // [B][L][H]
     float* dAp;   // [B][M][H]
     bf16* mbar;   // [B][M][G][S][S]
     int nkp;
@@ -999,15 +1023,14 @@ MfmaWs mfma_layout(const Shape& s, void* base) {
     };
     w.rec = (float*)take(4 * BHM * s.S);
     w.lda = (float*)take(4 * BHM);
-    w.dH = (float*)take(4 * BHM * NP);
-    w.dR = (float*)take(4 * BHM * NP);
+    w.dH = (bf16*)take(2 * BHM * NP);
+    w.dR = (bf16*)take(2 * BHM * NP);
     w.BT = (bf16*)take(2 * BMG * s.N * s.S);
     w.CT = (bf16*)take(2 * BMG * s.N * s.S);
     w.Hb = (bf16*)take(2 * BHM * NP);
     w.Wb = (bf16*)take(2 * BHM * NP);
     w.Kp = (float*)take(4 * BHM * w.nkp);
     w.wp = (float*)take(4 * (size_t)s.B * s.L * s.H);
-    w.vt = (float*)take(4 * (size_t)s.B * s.L * s.H);
     w.dAp = (float*)take(4 * BHM);
     w.mbar = (bf16*)take(2 * BMG * (size_t)s.S * s.S);
     w.total = o;
@@ -1036,16 +1059,15 @@ hipError_t run_mfma(const Shape& s, const bf16* x, const float* dt, const float*
         w.dH, w.dR, w.lda, h0, dmem, dhl, w.Hb, w.Wb, w.Kp, dh0, s.H, NP, s.M, s.Mcap);
     prof_end(st);
     prof_begin("k_sbwd_group", st);
-    k_sbwd_group<N, S><<<(unsigned)(nbcg * (S / 64)), 512, 0, st>>>(x, dt, Bm, Cm, dy, w.rec, w.Hb, w.Wb, dB,
-                                                                    dC, w.wp, w.vt, w.mbar, s.L, s.H, s.G, s.M,
-                                                                    nbcg);
+    k_sbwd_group<N, S><<<(unsigned)(nbcg * (S / 64)), 512, 0, st>>>(x, dt, Cm, dy, w.rec, w.Hb, w.Wb, dB, dC,
+                                                                    w.wp, w.mbar, s.L, s.H, s.G, s.M, nbcg);
     prof_end(st);
     prof_begin("k_sbwd_quad", st);
-    k_sbwd_quad<N, S><<<grid, 64 * quad_waves<S>(), 0, st>>>(x, dt, A, Bm, Cm, dy, w.rec, w.Wb, w.Kp, w.wp, w.vt, dx,
+    k_sbwd_quad<N, S><<<grid, 64 * quad_waves<S>(), 0, st>>>(x, dt, A, Bm, Cm, dy, w.rec, w.Wb, w.Kp, w.wp, dx,
                                                              ddt, w.dAp, s.L, s.H, s.G, s.M, hpb, nbcg, w.nkp);
     prof_end(st);
     prof_begin("k_sbwd_bc", st);
-    k_sbwd_bc<N, S><<<(unsigned)nbcg, 512, 0, st>>>(w.mbar, w.BT, w.CT, dB, dC, s.L, s.G, s.M);
+    k_sbwd_bc<N, S><<<(unsigned)(2 * nbcg), 512, 0, st>>>(w.mbar, w.BT, w.CT, dB, dC, s.L, s.G, s.M);
     prof_end(st);
     prof_begin("k_sbwd_dA", st);
     k_sbwd_dA<<<(unsigned)s.H, 256, 0, st>>>(w.dAp, dA, s.B * s.M, s.H);
