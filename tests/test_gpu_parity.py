@@ -308,6 +308,51 @@ def test_decode_token_by_token_reproduces_forward(dtype, S, N, L, z_per_head):
     assert_close_slices(to_np(h_state), ref["h_last"], tol, axes_keep=(0, 1), what="h_state")
 
 
+@pytest.mark.parametrize("dtype,S,N,z_per_head", [("fp32", 64, 32, True), ("bf16", 64, 64, False)])
+def test_decode_state_snapshot_and_restore(dtype, S, N, z_per_head):
+    """The decode state (h_state, chunk_acc, the memory cache) copied to host
+    memory and back continues exactly as the original: a step sequence that
+    crosses a chunk boundary after the snapshot gives bitwise identical outputs
+    and final state from the restored copy as from the live one."""
+    import torch
+    L0, L1 = 100, 60  # snapshot after 100 tokens; the next 60 cross token 128
+    w = synth.Workload("snap_%s" % dtype, 2, L0 + L1, 2, 64, N, S, dtype, z_per_head=z_per_head)
+    announce("decode snapshot/restore %s" % (w,))
+    d = synth.forward_inputs(w, seed=33)
+    B_, H, P = w.batch, w.nheads, w.headdim
+    Mcap = -(-(L0 + L1) // S)
+    dev = {k: to_dev(d[k], dtype) for k in ("x", "Bm", "Cm", "q", "e", "z")}
+    dt, A = f32_dev(d["dt"]), f32_dev(d["A"])
+
+    def step(t, hs, ca, cache):
+        return dart.decode_step(t, dev["x"][:, t].contiguous(), dt[:, t].contiguous(), A,
+                                dev["Bm"][:, t].contiguous(), dev["Cm"][:, t].contiguous(),
+                                dev["q"][:, t].contiguous(), dev["e"][:, t].contiguous(),
+                                dev["z"][:, t].contiguous(), hs, ca, cache, S)
+
+    h_state = torch.zeros((B_, H, N, P), dtype=torch.float32, device="cuda")
+    chunk_acc = torch.zeros_like(h_state)
+    cache = torch.zeros((B_, Mcap, H, N, P), dtype=dev["x"].dtype, device="cuda")
+    for t in range(L0):
+        step(t, h_state, chunk_acc, cache)
+    torch.cuda.synchronize()
+    snap = [a.cpu() for a in (h_state, chunk_acc, cache)]
+
+    live = [step(t, h_state, chunk_acc, cache).cpu() for t in range(L0, L0 + L1)]
+    live_state = [a.cpu() for a in (h_state, chunk_acc, cache)]
+
+    # restore into fresh device buffers that first hold other values
+    hs2, ca2, cache2 = (torch.full_like(a, 7.0, device="cuda") for a in snap)
+    for dst, src in zip((hs2, ca2, cache2), snap):
+        dst.copy_(src.to("cuda"))
+    again = [step(t, hs2, ca2, cache2).cpu() for t in range(L0, L0 + L1)]
+    torch.cuda.synchronize()
+    for t, (a, b) in enumerate(zip(live, again)):
+        assert torch.equal(a, b), "y differs at step %d after the restore" % (L0 + t)
+    for nm, a, b in zip(("h_state", "chunk_acc", "cache"), live_state, (hs2, ca2, cache2)):
+        assert torch.equal(a, b.cpu()), nm + " differs after the restored steps"
+
+
 @pytest.mark.parametrize("dtype,S,N,lengths,steps", [("fp32", 64, 64, (70, 128, 5), 70),
                                                       ("bf16", 128, 128, (300, 256, 129, 0), 140)])
 def test_ragged_prefill_handoff_and_decode(dtype, S, N, lengths, steps):
