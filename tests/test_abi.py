@@ -227,9 +227,14 @@ def test_sma_bwd_workspace_and_bad_arguments(lib):
 def test_ssd_bwd_workspace_and_bad_arguments(lib):
     d = dims()
     ws = lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(d))
-    # at least the forward scan's workspace plus R and dR (float, per chunk)
-    assert ws >= lib.dart_scan_workspace_bytes(ctypes.byref(d)) + 2 * 4 * (d.batch * (512 // 64)
-                                                                          * d.nheads * 64 * 64)
+    per_chunk = d.batch * (512 // 64) * d.nheads * 64 * 64
+    # bf16 (chunked matrix form): the chunk contributions of the state and of
+    # the adjoint, the entry states and the chunk adjoints, bf16 per chunk
+    assert ws >= 4 * 2 * per_chunk
+    # fp32 (token sweeps): the forward scan's workspace plus R and dR, float
+    d32 = dims(dtype="fp32")
+    ws32 = lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(d32))
+    assert ws32 >= lib.dart_scan_workspace_bytes(ctypes.byref(d32)) + 2 * 4 * per_chunk
     assert lib.dart_ssd_bwd_workspace_bytes(ctypes.byref(dims(headdim=48))) == 0
     required = (0, 1, 2, 3, 4, 6, 9, 10, 11, 12, 13, 15)  # h0, dmem, dh_last, dh0 optional
 
