@@ -227,11 +227,13 @@ __device__ __forceinline__ void load_row_frags(const S* row, int grp, Frag<T> (&
 }
 
 // ---- scores: exact logits and dy . V per (head, memory, token) ---------------
-// Workgroup: 64 consecutive tokens of chunk i >= 1 and hpb heads of one group,
-// 8 waves; waves w and w + 4 share tokens 16 w .. 16 w + 15 and split the
-// rows: rows p of W'^T = Kh^T (q (.) w) (this half's part of every logit)
-// and rows n of X^T = diag(1/r) Kh dy^T (its part of dy . V = C . X).  The
-// two partial sums meet in LDS once per step.
+// Workgroup: 64 RT consecutive tokens of chunk i >= 1 and hpb heads of one
+// group, 8 waves; waves w and w + 4 share the RT 16-token column tiles of
+// tokens 16 RT w .. 16 RT w + 16 RT - 1 and split the rows: rows p of
+// W'^T = Kh^T (q (.) w) (this half's part of every logit) and rows n of
+// X^T = diag(1/r) Kh dy^T (its part of dy . V = C . X).  Every memory
+// fragment read from LDS feeds the RT column tiles.  The two partial sums
+// meet in LDS once per step.
 //
 // The logits are formed to about 16 bits although the operands are stored in
 // bf16: the key side streams as hi + lo (the lo tile holds the rounding
@@ -251,7 +253,7 @@ __device__ __forceinline__ void load_row_frags(const S* row, int grp, Frag<T> (&
 // the weights the gradient kernels use are the softmax of the exact logits,
 // whatever rounding the forward's log-sum-exp carries.  Tiles stream through
 // an NS-stage LDS ring by DMA, NS - 1 steps ahead, copied by waves 0-3.
-template <typename T, int N>
+template <typename T, int N, int RT>
 __global__ __launch_bounds__(512) void k_bwd_scores(
     const T* __restrict__ qh, const bf16* __restrict__ ql, const float* __restrict__ qsc,
     const float* __restrict__ eb, const T* __restrict__ Cm, const float* __restrict__ rinv,
@@ -267,12 +269,13 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
     constexpr int KQ = N / 32;
     constexpr int NTH = NT / 2;
     constexpr int NS = tok_stages<T, N, NTL>();
+    constexpr int TB = kTokBlock * RT;  // tokens per workgroup
     using Copy = TileCopy<RB, TILE, kTokWaves>;
     constexpr int RPW = N / 16;
     constexpr int CPS = NTL * Copy::count() + 1;
     __shared__ __attribute__((aligned(16))) char ring[NS][NTL][TILE];
     __shared__ __attribute__((aligned(16))) float rring[NS][N];
-    __shared__ float xch[2][2][kTokWaves][16];
+    __shared__ float xch[2][2][kTokWaves][16 * RT];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -284,40 +287,46 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
     const int nhb = H / hpb;
     const int64_t b = bhc / nhb;
     const int hb = (int)(bhc % nhb);
-    const int64_t t0 = (int64_t)(blk0 + blk) * kTokBlock;
+    const int64_t t0 = (int64_t)(blk0 + blk) * TB;
     const int nj = (int)(t0 / S);
-    const int64_t t = t0 + tg * 16 + col;
-    const bool valid = t < L;
-    const int64_t tc = valid ? t : L - 1;
     const int h0 = hb * hpb;
     const int g = h0 / (H / G);
-    const int64_t bt = b * L + tc;
     const int nt0 = nh * NTH;
     const int pt0 = nh * 2;
-
-    Frag<T> qf[KQ];
-    load_row_frags<T, T, N>(qh + (bt * G + g) * N, grp, qf);
-    Frag<bf16> qlf[LO ? KQ : 1];
-    if constexpr (LO) {
-        if (use_ql) {
-            load_row_frags<bf16, bf16, N>(ql + (bt * G + g) * N, grp, qlf);
-        } else {
+    bool valid[RT];
+    int64_t tc[RT], bt[RT];
 #pragma unroll
-            for (int ks = 0; ks < KQ; ++ks) qlf[ks] = bf16x8{};
-        }
+    for (int rt = 0; rt < RT; ++rt) {
+        const int64_t t = t0 + tg * 16 * RT + rt * 16 + col;
+        valid[rt] = t < L;
+        tc[rt] = valid[rt] ? t : L - 1;
+        bt[rt] = b * L + tc[rt];
     }
-    const float qs = qsc[bt * G + g];
-    const float* erow = eb + (bt * G + g) * kP;
-    float ea[2][4];
-#pragma unroll
-    for (int q = 0; q < 2; ++q) load4(erow + 16 * (pt0 + q) + 4 * grp, ea[q]);
+
+    Frag<T> qf[RT][KQ];
+    Frag<bf16> qlf[RT][LO ? KQ : 1];
+    float qs[RT], ea[RT][2][4];
     typedef T T4 __attribute__((ext_vector_type(4)));
-    T4 ca[NTH];
-    {
-        const T* crow = Cm + (bt * G + g) * N;
+    T4 ca[RT][NTH];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        load_row_frags<T, T, N>(qh + (bt[rt] * G + g) * N, grp, qf[rt]);
+        if constexpr (LO) {
+            if (use_ql) {
+                load_row_frags<bf16, bf16, N>(ql + (bt[rt] * G + g) * N, grp, qlf[rt]);
+            } else {
+#pragma unroll
+                for (int ks = 0; ks < KQ; ++ks) qlf[rt][ks] = bf16x8{};
+            }
+        }
+        qs[rt] = qsc[bt[rt] * G + g];
+        const float* erow = eb + (bt[rt] * G + g) * kP;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) load4(erow + 16 * (pt0 + q) + 4 * grp, ea[rt][q]);
+        const T* crow = Cm + (bt[rt] * G + g) * N;
 #pragma unroll
         for (int k = 0; k < NTH; ++k)
-            ca[k] = *reinterpret_cast<const T4*>(crow + 16 * (nt0 + k) + 4 * grp);
+            ca[rt][k] = *reinterpret_cast<const T4*>(crow + 16 * (nt0 + k) + 4 * grp);
     }
     const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
     const int nsteps = hpb * nj;
@@ -333,14 +342,15 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
             lds_dma16_untracked_at(rinv + hj * N + (tg * RPW + lane) * 4,
                                    lds_addr(&rring[k % NS][0]) + tg * RPW * 16);
     };
-    auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * Ls + tc; };
 
 #pragma unroll
     for (int k = 0; k < NS - 1; ++k)
         if (k < nsteps) issue_tiles(k);
 
-    Frag<T> dyf[2];
-    float lse2 = 0.f, dsum = 0.f, dyacc = 0.f;
+    Frag<T> dyf[RT][2];
+    float lse2[RT], dsum[RT], dyacc[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) lse2[rt] = dsum[rt] = dyacc[rt] = 0.f;
     for (int k = 0; k < nsteps; ++k) {
         const int hh = k / nj, j = k - hh * nj;
         const int h = h0 + hh;
@@ -354,73 +364,101 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
         }
         lds_barrier();
         if (j == 0) {
-            const T* dyrow = dy + (bt * H + h) * kP;
-            dyf[0] = load_frag(dyrow + 8 * grp);
-            dyf[1] = load_frag(dyrow + 32 + 8 * grp);
-            lse2 = lse[bt * H + h] * kLog2e;
-            dsum = dyacc = 0.f;
-            keep(dyf[0]);
-            keep(dyf[1]);
-            asm volatile("" ::"v"(lse2));
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const T* dyrow = dy + (bt[rt] * H + h) * kP;
+                dyf[rt][0] = load_frag(dyrow + 8 * grp);
+                dyf[rt][1] = load_frag(dyrow + 32 + 8 * grp);
+                lse2[rt] = lse[bt[rt] * H + h] * kLog2e;
+                dsum[rt] = dyacc[rt] = 0.f;
+                keep(dyf[rt][0]);
+                keep(dyf[rt][1]);
+                asm volatile("" ::"v"(lse2[rt]));
+            }
         }
         if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
         const char* kt = ring[k % NS][0];
-        // this half's rows p of W'^T
-        f32x4 w[2];
+        // this half's rows p of W'^T, every column tile per fragment read
+        f32x4 w[RT][2];
 #pragma unroll
-        for (int q = 0; q < 2; ++q) w[q] = zero4;
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int q = 0; q < 2; ++q) w[rt][q] = zero4;
 #pragma unroll
         for (int ks = 0; ks < KQ; ++ks) {
 #pragma unroll
             for (int q = 0; q < 2; ++q) {
                 const int r0 = 32 * ks + 4 * grp, r1 = r0 + 16, cb = 16 * (pt0 + q);
                 const Frag<T> a = frag_km<T, RB>(kt, r0, r1, cb, lane);
-                w[q] = mma16(w[q], a, qf[ks]);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) w[rt][q] = mma16(w[rt][q], a, qf[rt][ks]);
                 if constexpr (LO) {
                     const char* kl = ring[k % NS][NTL - 1];
-                    w[q] = mma16(w[q], frag_km<T, RB>(kl, r0, r1, cb, lane), qf[ks]);
-                    if (use_ql) w[q] = mma16(w[q], a, qlf[ks]);
+                    const Frag<T> al = frag_km<T, RB>(kl, r0, r1, cb, lane);
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) {
+                        w[rt][q] = mma16(w[rt][q], al, qf[rt][ks]);
+                        if (use_ql) w[rt][q] = mma16(w[rt][q], a, qlf[rt][ks]);
+                    }
                 }
             }
         }
-        float l2 = 0.f;
+        float l2[RT], dw[RT];
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
+        for (int rt = 0; rt < RT; ++rt) {
+            l2[rt] = 0.f;
+            dw[rt] = 0.f;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) l2 += ea[q][i] * w[q][i];
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) l2[rt] += ea[rt][q][i] * w[rt][q][i];
+        }
         // this half's rows n of X^T = diag(1/r) Kh dy^T, then C . X
-        float dw = 0.f;
 #pragma unroll
         for (int q = 0; q < NTH; ++q) {
             const int nt = nt0 + q;
-            f32x4 x = zero4;
+            f32x4 x[RT];
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-                x = mma16(x, frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp), dyf[ks]);
-            x *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+            for (int rt = 0; rt < RT; ++rt) x[rt] = zero4;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) dw += to_f(ca[q][i]) * x[i];
+            for (int ks = 0; ks < 2; ++ks) {
+                const Frag<T> a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) x[rt] = mma16(x[rt], a, dyf[rt][ks]);
+            }
+            const f32x4 ri = *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) dw[rt] += to_f(ca[rt][q][i]) * (x[rt][i] * ri[i]);
         }
-        l2 += shfl_xor(l2, 16);
-        l2 += shfl_xor(l2, 32);
-        dw += shfl_xor(dw, 16);
-        dw += shfl_xor(dw, 32);
-        if (lane < 16) {
-            xch[0][nh][tg][col] = l2;
-            xch[1][nh][tg][col] = dw;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            l2[rt] += shfl_xor(l2[rt], 16);
+            l2[rt] += shfl_xor(l2[rt], 32);
+            dw[rt] += shfl_xor(dw[rt], 16);
+            dw[rt] += shfl_xor(dw[rt], 32);
+            if (lane < 16) {
+                xch[0][nh][tg][16 * rt + col] = l2[rt];
+                xch[1][nh][tg][16 * rt + col] = dw[rt];
+            }
         }
         lds_barrier();
-        l2 = (l2 + xch[0][nh ^ 1][tg][col]) * qs;
-        dw += xch[1][nh ^ 1][tg][col];
-        const float p = fast_exp2(l2 - lse2);
-        dsum += p;
-        dyacc += p * dw;
-        if (nh == 0 && lane < 16 && valid) {
-            lw[sidx(h, j)] = l2;
-            dwv[sidx(h, j)] = dw;
-            if (j == nj - 1) {
-                lsep[bt * H + h] = lse2 + __log2f(dsum);
-                rdy[bt * H + h] = dyacc / dsum;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const float lv = (l2[rt] + xch[0][nh ^ 1][tg][16 * rt + col]) * qs[rt];
+            const float dv = dw[rt] + xch[1][nh ^ 1][tg][16 * rt + col];
+            const float p = fast_exp2(lv - lse2[rt]);
+            dsum[rt] += p;
+            dyacc[rt] += p * dv;
+            if (nh == 0 && lane < 16 && valid[rt]) {
+                const int64_t si = ((b * H + h) * Mp + j) * Ls + tc[rt];
+                lw[si] = lv;
+                dwv[si] = dv;
+                if (j == nj - 1) {
+                    lsep[bt[rt] * H + h] = lse2[rt] + __log2f(dsum[rt]);
+                    rdy[bt[rt] * H + h] = dyacc[rt] / dsum[rt];
+                }
             }
         }
     }
@@ -1010,10 +1048,27 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
         // q (.) w inexact in bf16
         const int use_ql = LO && a.qw != nullptr;
         prof_begin("k_bwd_scores", st);
-        k_bwd_scores<T, N><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
-            (const T*)w.qh, (const bf16*)w.ql, w.qsc, w.eb, (const T*)Cm, w.rinv, (const T*)w.kmem,
-            (const T*)w.klo, lse, (const T*)dy, w.gp, w.gd, w.lsep, w.rdy, use_ql, s.L, Ls, s.H,
-            s.G, s.S, Mp, hpb, blk0, (int)nblk, BHC);
+        bool two = false;
+        if constexpr (sizeof(T) == 2) {
+            if (s.S >= 128) {
+                // bf16: 128 tokens per workgroup (S is a multiple of 128, so a
+                // block never straddles chunks)
+                constexpr int TB2 = 2 * kTokBlock;
+                const int sb0 = s.S / TB2;
+                const int64_t snblk = (s.L + TB2 - 1) / TB2 - sb0;
+                k_bwd_scores<T, N, 2><<<(unsigned)(BHC * snblk), 512, 0, st>>>(
+                    (const T*)w.qh, (const bf16*)w.ql, w.qsc, w.eb, (const T*)Cm, w.rinv,
+                    (const T*)w.kmem, (const T*)w.klo, lse, (const T*)dy, w.gp, w.gd, w.lsep, w.rdy,
+                    use_ql, s.L, Ls, s.H, s.G, s.S, Mp, hpb, sb0, (int)snblk, BHC);
+                two = true;
+            }
+        }
+        if (!two) {
+            k_bwd_scores<T, N, 1><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
+                (const T*)w.qh, (const bf16*)w.ql, w.qsc, w.eb, (const T*)Cm, w.rinv,
+                (const T*)w.kmem, (const T*)w.klo, lse, (const T*)dy, w.gp, w.gd, w.lsep, w.rdy,
+                use_ql, s.L, Ls, s.H, s.G, s.S, Mp, hpb, blk0, (int)nblk, BHC);
+        }
         prof_end(st);
         prof_begin("k_bwd_tokens", st);
         k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
