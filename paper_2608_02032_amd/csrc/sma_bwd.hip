@@ -466,23 +466,25 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
 
 // ---- token-side gradients ------------------------------------------------------
 // Same workgroup and block order as k_bwd_scores.  Waves w and w + 4 share
-// tokens 16 w .. 16 w + 15 and split the rows of each product: rows p of W'
-// (and dEbar), rows n of X and Z (and dQbar, dC).  In every MFMA product the
-// memory tile is the A operand (rows n or p) and the tokens are the 16
-// columns, so lane l works on token l % 16 and its rows 4 (l / 16) + 0..3 of
-// each 16-row tile.
+// the RT 16-token column tiles of tokens 16 RT w .. 16 RT w + 16 RT - 1 and
+// split the rows of each product: rows p of W' (and dEbar), rows n of X and Z
+// (and dQbar, dC).  In every MFMA product the memory tile is the A operand
+// (rows n or p) and the tokens are the columns, so lane l works on token
+// l % 16 of each column tile and its rows 4 (l / 16) + 0..3 of each 16-row
+// tile; every fragment read from LDS feeds the RT column tiles.
 //
 // The scores kernel has left, per (head, memory, token), the exact logit and
-// dwy, and per (token, head) the exact log-sum-exp and Dy; these rows (64
-// tokens of one head and memory) arrive by DMA with the key tile, so each
-// step knows p_j = exp2(l2_j - lse2') and dl_j = g p_j (dwy_j - Dy) at once:
+// dwy, and per (token, head) the exact log-sum-exp and Dy; these rows (the
+// block's tokens of one head and memory) arrive by DMA with the key tile, so
+// each step knows p_j = exp2(l2_j - lse2') and dl_j = g p_j (dwy_j - Dy) at
+// once:
 //   dQbar += s dl_j Z_j,   Z = Kh Ebar^T;
 //   dEbar += s dl_j Kh_j^T Qbar = ln2 dl_j W'_j,   W' = Kh^T Qbar'^T;
 //   dC    += g p_j X_j,    X = diag(1/r) Kh dy^T = dH dy^T;
 // the three products from the key side alone (bf16 rounding of these
 // operands is not amplified: each sum over memories carries the exact
 // weights).  g p_j replaces the logit in place for the memory kernel.
-template <typename T, int N>
+template <typename T, int N, int RT>
 __global__ __launch_bounds__(512) void k_bwd_tokens(
     const T* __restrict__ qb, const float* __restrict__ eb, const float* __restrict__ rinv,
     const T* __restrict__ kmem, const T* __restrict__ z, const float* __restrict__ lsep,
@@ -494,13 +496,20 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     constexpr int NT = N / 16;
     constexpr int KQ = N / 32;
     constexpr int NTH = NT / 2;          // n tiles per wave
-    constexpr int NS = tok_stages<T, N, 1>();
+    // (three stages with two column tiles: room for the lane slots below)
+    constexpr int NS = RT > 1 && tok_stages<T, N, 1>() > 3 ? 3 : tok_stages<T, N, 1>();
+    constexpr int TB = kTokBlock * RT;   // tokens per workgroup
     using Copy = TileCopy<RB, TILE, kTokWaves>;
     constexpr int RPW = N / 16;              // 16-byte pieces of the 1/r row per copying wave
     constexpr int CPS = Copy::count() + 2;   // DMA copies per copying wave per step
     __shared__ __attribute__((aligned(16))) char ring[NS][TILE];
     __shared__ __attribute__((aligned(16))) float rring[NS][N];
-    __shared__ __attribute__((aligned(16))) float lring[NS][kTokWaves][2][16];  // logit, dwy
+    __shared__ __attribute__((aligned(16))) float lring[NS][kTokWaves][2][16 * RT];  // logit, dwy
+    // with two column tiles, each lane's Qbar' and Ebar fragments live in LDS
+    // (one 16-byte slot per thread and fragment, conflict-free) rather than
+    // in registers
+    constexpr int QL = RT > 1 ? RT * (KQ + 2) : 1;
+    __shared__ __attribute__((aligned(16))) Frag<T> qslot[QL][512];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -512,36 +521,57 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     const int nhb = H / hpb;
     const int64_t b = bhc / nhb;
     const int hb = (int)(bhc % nhb);
-    const int64_t t0 = (int64_t)(blk0 + blk) * kTokBlock;
+    const int64_t t0 = (int64_t)(blk0 + blk) * TB;
     const int nj = (int)(t0 / S);  // memories every token of the block attends
-    const int64_t t = t0 + tg * 16 + col;
-    const bool valid = t < L;
-    const int64_t tc = valid ? t : L - 1;
     const int h0 = hb * hpb;
     const int g = h0 / (H / G);
-    const int64_t bt = b * L + tc;
     const float isn = 1.0f / sqrtf((float)N);
     const int nt0 = nh * NTH;  // first n tile of this wave
     const int pt0 = nh * 2;    // first p tile of this wave
+    bool valid[RT];
+    int64_t tc[RT], bt[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        const int64_t t = t0 + tg * 16 * RT + rt * 16 + col;
+        valid[rt] = t < L;
+        tc[rt] = valid[rt] ? t : L - 1;
+        bt[rt] = b * L + tc[rt];
+    }
 
     // group-shared token operands (Qbar' whole; Ebar)
-    Frag<T> qf[KQ];
-    load_row_frags<T, T, N>(qb + (bt * G + g) * N, grp, qf);
-    const float* erow = eb + (bt * G + g) * kP;
-    Frag<T> ef[2];
+    Frag<T> qf[RT > 1 ? 1 : RT][KQ], ef[RT > 1 ? 1 : RT][2];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-        float v[8];
-        load8(erow + ks * 32 + 8 * grp, v);
-        ef[ks] = make_frag<T>(v);
+    for (int rt = 0; rt < RT; ++rt) {
+        if constexpr (RT > 1) {
+            Frag<T> tmp[KQ];
+            load_row_frags<T, T, N>(qb + (bt[rt] * G + g) * N, grp, tmp);
+#pragma unroll
+            for (int ks = 0; ks < KQ; ++ks) qslot[rt * KQ + ks][threadIdx.x] = tmp[ks];
+        } else {
+            load_row_frags<T, T, N>(qb + (bt[rt] * G + g) * N, grp, qf[rt]);
+        }
+        const float* erow = eb + (bt[rt] * G + g) * kP;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            float v[8];
+            load8(erow + ks * 32 + 8 * grp, v);
+            if constexpr (RT > 1) {
+                qslot[RT * KQ + rt * 2 + ks][threadIdx.x] = make_frag<T>(v);
+            } else {
+                ef[rt][ks] = make_frag<T>(v);
+            }
+        }
     }
 
     const f32x4 zero4{0.f, 0.f, 0.f, 0.f};
-    f32x4 dQ[NTH], dC[NTH], dE[2];
+    f32x4 dQ[RT][NTH], dC[RT][NTH], dE[RT][2];
 #pragma unroll
-    for (int k = 0; k < NTH; ++k) dQ[k] = dC[k] = zero4;
+    for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) dE[q] = zero4;
+        for (int k = 0; k < NTH; ++k) dQ[rt][k] = dC[rt][k] = zero4;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) dE[rt][q] = zero4;
+    }
 
     const int nsteps = hpb * nj;
     Copy copy;
@@ -554,21 +584,22 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         if (lane < RPW)
             lds_dma16_untracked_at(rinv + hj * N + (tg * RPW + lane) * 4,
                                    lds_addr(&rring[k % NS][0]) + tg * RPW * 16);
-        // this token group's 16 logits (lanes 0-3) and dwy (lanes 4-7)
-        if (lane < 8) {
-            const int64_t srow = ((b * H + h0 + hh) * Mp + j) * Ls + t0 + 16 * tg + 4 * (lane & 3);
-            lds_dma16_untracked_at(lane < 4 ? (const float*)gpw + srow : gdw + srow,
+        // this token group's 16 RT logits (lanes 0 .. 4 RT - 1) and dwy (the next 4 RT)
+        if (lane < 8 * RT) {
+            const int64_t srow = ((b * H + h0 + hh) * Mp + j) * Ls + t0 + 16 * RT * tg + 4 * (lane % (4 * RT));
+            lds_dma16_untracked_at(lane < 4 * RT ? (const float*)gpw + srow : gdw + srow,
                                    lds_addr(&lring[k % NS][tg][0][0]));
         }
     };
-    auto sidx = [&](int h, int j) { return ((b * H + h) * Mp + j) * Ls + tc; };
 
 #pragma unroll
     for (int k = 0; k < NS - 1; ++k)
         if (k < nsteps) issue_tiles(k);
 
-    Frag<T> dyf[2];
-    float lse2 = 0.f, gate = 0.f, Dy = 0.f;
+    Frag<T> dyf[RT][2];
+    float lse2[RT], gate[RT], Dy[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) lse2[rt] = gate[rt] = Dy[rt] = 0.f;
     for (int k = 0; k < nsteps; ++k) {
         const int hh = k / nj, j = k - hh * nj;
         const int h = h0 + hh;
@@ -585,64 +616,105 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         if (j == 0) {
             // this head's per-token operands (waited for here, before the
             // next copies are issued)
-            const T* dyrow = dy + (bt * H + h) * kP;
-            dyf[0] = load_frag(dyrow + 8 * grp);
-            dyf[1] = load_frag(dyrow + 32 + 8 * grp);
-            lse2 = lsep[bt * H + h];
-            Dy = rdy[bt * H + h];
-            gate = silu(to_f(z[z_per_head ? bt * H + h : bt]));
-            keep(dyf[0]);
-            keep(dyf[1]);
-            asm volatile("" ::"v"(lse2), "v"(Dy), "v"(gate));
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const T* dyrow = dy + (bt[rt] * H + h) * kP;
+                dyf[rt][0] = load_frag(dyrow + 8 * grp);
+                dyf[rt][1] = load_frag(dyrow + 32 + 8 * grp);
+                lse2[rt] = lsep[bt[rt] * H + h];
+                Dy[rt] = rdy[bt[rt] * H + h];
+                gate[rt] = silu(to_f(z[z_per_head ? bt[rt] * H + h : bt[rt]]));
+                keep(dyf[rt][0]);
+                keep(dyf[rt][1]);
+                asm volatile("" ::"v"(lse2[rt]), "v"(Dy[rt]), "v"(gate[rt]));
+            }
         }
         if (k + NS - 1 < nsteps) issue_tiles(k + NS - 1);
         const char* kt = ring[k % NS];
-        const float p = fast_exp2(lring[k % NS][tg][0][col] - lse2);
-        const float gp = gate * p;
-        const float dl = gp * (lring[k % NS][tg][1][col] - Dy);
+        // lane coordinates made opaque per step, so that the fragment offsets
+        // are recomputed in the loop rather than held live across it
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int col = ln & 15, grp = ln >> 4;
+        float gp[RT], dl[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const float p = fast_exp2(lring[k % NS][tg][0][16 * rt + col] - lse2[rt]);
+            gp[rt] = gate[rt] * p;
+            dl[rt] = gp[rt] * (lring[k % NS][tg][1][16 * rt + col] - Dy[rt]);
+        }
         // this half's rows p of W'^T = Kh^T Qbar'^T: dEbar += ln2 dl W'
-        const float ce = kLn2 * dl;
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-            f32x4 w = zero4;
+            f32x4 w[RT];
 #pragma unroll
-            for (int ks = 0; ks < KQ; ++ks)
-                w = mma16(w, frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp,
-                                            16 * (pt0 + q), lane),
-                          qf[ks]);
-            dE[q] += ce * w;
+            for (int rt = 0; rt < RT; ++rt) w[rt] = zero4;
+#pragma unroll
+            for (int ks = 0; ks < KQ; ++ks) {
+                const Frag<T> a = frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp, 16 * (pt0 + q), ln);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    if constexpr (RT > 1) {
+                        w[rt] = mma16(w[rt], a, qslot[rt * KQ + ks][threadIdx.x]);
+                    } else {
+                        w[rt] = mma16(w[rt], a, qf[rt][ks]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) dE[rt][q] += (kLn2 * dl[rt]) * w[rt];
+            if constexpr (RT > 1) __builtin_amdgcn_sched_barrier(0);
         }
         // X^T = diag(1/r) Kh dy^T and Z^T = Kh Ebar^T on this half's n tiles
-        const float cq = isn * dl;
 #pragma unroll
         for (int q = 0; q < NTH; ++q) {
             const int nt = nt0 + q;
-            f32x4 x = zero4, zz = zero4;
+            f32x4 x[RT], zz[RT];
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) x[rt] = zz[rt] = zero4;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const Frag<T> a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
-                x = mma16(x, a, dyf[ks]);
-                zz = mma16(zz, a, ef[ks]);
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt) {
+                    x[rt] = mma16(x[rt], a, dyf[rt][ks]);
+                    if constexpr (RT > 1) {
+                        zz[rt] = mma16(zz[rt], a, qslot[RT * KQ + rt * 2 + ks][threadIdx.x]);
+                    } else {
+                        zz[rt] = mma16(zz[rt], a, ef[rt][ks]);
+                    }
+                }
             }
-            x *= *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
-            dC[q] += gp * x;
-            dQ[q] += cq * zz;
+            const f32x4 ri = *reinterpret_cast<const f32x4*>(&rring[k % NS][16 * nt + 4 * grp]);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                dC[rt][q] += gp[rt] * (x[rt] * ri);
+                dQ[rt][q] += (isn * dl[rt]) * zz[rt];
+            }
+            if constexpr (RT > 1) __builtin_amdgcn_sched_barrier(0);  // bounds the live fragments
         }
-        if (nh == 0 && lane < 16 && valid) gpw[sidx(h, j)] = gp;
+        if (nh == 0 && lane < 16) {
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+                if (valid[rt]) gpw[((b * H + h) * Mp + j) * Ls + tc[rt]] = gp[rt];
+        }
     }
 
-    if (!valid) return;
     // per-head-block partial sums: dQbar [N], dEbar [P], dC [N]
-    float* pr = part + (bt * nhb + hb) * (2 * N + kP);
 #pragma unroll
-    for (int q = 0; q < NTH; ++q) {
-        const int nt = nt0 + q;
-        *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[q];
-        *reinterpret_cast<f32x4*>(pr + N + kP + 16 * nt + 4 * grp) = dC[q];
+    for (int rt = 0; rt < RT; ++rt) {
+        if (!valid[rt]) continue;
+        float* pr = part + (bt[rt] * nhb + hb) * (2 * N + kP);
+#pragma unroll
+        for (int q = 0; q < NTH; ++q) {
+            const int nt = nt0 + q;
+            *reinterpret_cast<f32x4*>(pr + 16 * nt + 4 * grp) = dQ[rt][q];
+            *reinterpret_cast<f32x4*>(pr + N + kP + 16 * nt + 4 * grp) = dC[rt][q];
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+            *reinterpret_cast<f32x4*>(pr + N + 16 * (pt0 + q) + 4 * grp) = dE[rt][q];
     }
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-        *reinterpret_cast<f32x4*>(pr + N + 16 * (pt0 + q) + 4 * grp) = dE[q];
 }
 
 // ---- memory-side gradients -------------------------------------------------------
@@ -985,7 +1057,11 @@ struct BwdWs {
 
 // Row stride of the per-(b, h, memory) token arrays: a multiple of the 64
 // tokens a token-kernel workgroup reads as one row piece.
-inline int64_t bwd_row_stride(const Shape& s) { return (s.L + kTokBlock - 1) / kTokBlock * kTokBlock; }
+// Row stride of the per-(head, memory) token arrays: a multiple of the
+// largest token block (128), so a block's rows stay inside the array.
+inline int64_t bwd_row_stride(const Shape& s) {
+    return (s.L + 2 * kTokBlock - 1) / (2 * kTokBlock) * (2 * kTokBlock);
+}
 
 BwdWs bwd_layout(const Shape& s, void* base) {
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;
@@ -1071,10 +1147,25 @@ hipError_t run_bwd(const Shape& s, const SmaArgs& a, const void* q, const void* 
         }
         prof_end(st);
         prof_begin("k_bwd_tokens", st);
-        k_bwd_tokens<T, N><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
-            (const T*)w.qb, w.eb, w.rinv, (const T*)w.kmem, (const T*)z, w.lsep, w.rdy,
-            (const T*)dy, w.gp, w.gd, w.part, a.z_per_head, s.L, Ls, s.H, s.G, s.S, Mp, hpb, blk0,
-            (int)nblk, BHC);
+        two = false;
+        if constexpr (sizeof(T) == 2) {
+            if (s.S >= 128) {
+                constexpr int TB2 = 2 * kTokBlock;
+                const int sb0 = s.S / TB2;
+                const int64_t snblk = (s.L + TB2 - 1) / TB2 - sb0;
+                k_bwd_tokens<T, N, 2><<<(unsigned)(BHC * snblk), 512, 0, st>>>(
+                    (const T*)w.qb, w.eb, w.rinv, (const T*)w.kmem, (const T*)z, w.lsep, w.rdy,
+                    (const T*)dy, w.gp, w.gd, w.part, a.z_per_head, s.L, Ls, s.H, s.G, s.S, Mp, hpb,
+                    sb0, (int)snblk, BHC);
+                two = true;
+            }
+        }
+        if (!two) {
+            k_bwd_tokens<T, N, 1><<<(unsigned)(BHC * nblk), 512, 0, st>>>(
+                (const T*)w.qb, w.eb, w.rinv, (const T*)w.kmem, (const T*)z, w.lsep, w.rdy,
+                (const T*)dy, w.gp, w.gd, w.part, a.z_per_head, s.L, Ls, s.H, s.G, s.S, Mp, hpb,
+                blk0, (int)nblk, BHC);
+        }
         prof_end(st);
     }
     const int64_t BH = s.B * s.H;
