@@ -377,7 +377,8 @@ def main():
         "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(avg.items())},
         "kernels_pass": "%d further steps with library events around every launch" % nprof,
         "mfma_busy": {k: mfma_for(k) for k in ("k_sma", "k_chunk_out_heads", "k_chunk_state_heads",
-                                               "k_bwd_tokens", "k_bwd_mem")},
+                                               "k_bwd_scores", "k_bwd_tokens", "k_bwd_mem",
+                                               "k_sbwd_group", "k_sbwd_quad")},
     }
     if not args.no_decode:
         dbytes = decode_bytes(dw)
@@ -460,7 +461,7 @@ def main():
             "mfma_util": round(bflops / (bwd_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "tokens_per_s": round(B * L / (bwd_ms * 1e-3), 1),
             "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(bavg.items())},
-            "traffic_bytes": {k: traffic_for(k) for k in ("k_bwd_tokens", "k_bwd_mem")}}
+            "traffic_bytes": {k: traffic_for(k) for k in ("k_bwd_scores", "k_bwd_tokens", "k_bwd_mem")}}
         del ws_bwd
 
         # scan backward on the same workload, chained as a layer's backward
@@ -487,11 +488,20 @@ def main():
         savg = {k: v[0] / max(v[1], 1) for k, v in sk.items()}
         sb_ms = eb[0].elapsed_time(eb[1]) / R
         sbb = ssd_bwd_bytes(w)
+        # measured HBM bytes of one call (the contraction kernel runs twice: the
+        # state's and the adjoint's chunk contributions)
+        per_call = {k: traffic_for(k) for k in ("k_sbwd_contract", "k_sbwd_pass2", "k_sbwd_group",
+                                                "k_sbwd_quad", "k_sbwd_bc")}
+        total = (None if any(v is None for v in per_call.values())
+                 else 2 * per_call["k_sbwd_contract"] + sum(v for k, v in per_call.items()
+                                                            if k != "k_sbwd_contract"))
         extra["ssd_bwd"] = {
             "us": round(sb_ms * 1e3, 2), "tokens_per_s": round(B * L / (sb_ms * 1e-3), 1),
             "algorithmic_bytes": sbb, "hbm_gbps": round(sbb / (sb_ms * 1e-3) / 1e9, 1),
             "hbm_frac": round(sbb / (sb_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
-            "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(savg.items())}}
+            "kernels_us": {k: round(v * 1e3, 2) for k, v in sorted(savg.items())},
+            "traffic_bytes": per_call,
+            "traffic_vs_algorithmic": None if total is None else round(total / sbb, 3)}
         del ws_sb, sgrads, grads
 
     if not args.no_block:

@@ -47,9 +47,14 @@ def source_hash() -> str:
 
 
 def kernel_short(name: str):
+    """Short kernel name (k_...) from a mangled or demangled library symbol."""
     if "dart" not in name:
         return None
-    m = re.search(r"(k_[a-z0-9_]+)", name)
+    # mangled: a length-prefixed identifier after the namespaces
+    m = re.search(r"(\d+)(k_[A-Za-z0-9_]+)", re.sub(r"\d+_GLOBAL__N_1", "", name))
+    if m and int(m.group(1)) <= len(m.group(2)):
+        return m.group(2)[:int(m.group(1))]
+    m = re.search(r"(k_[A-Za-z0-9_]+)", name)
     return m.group(1) if m else None
 
 
