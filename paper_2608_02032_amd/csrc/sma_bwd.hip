@@ -21,24 +21,24 @@
 // follow through RMSNorm with the weights held constant.
 //
 // Kernels, in launch order:
-//   k_sma_keys          key side Kh_j (cache layout) and 1 / r_j, shared with
-//                       the forward
-//   k_bwd_prep          Qbar (scaled by log2(e)/sqrt(N), storage dtype, the
-//                       forward's operand exactly) and Ebar (float) per token
-//   k_bwd_tokens        one workgroup per (64 tokens of one chunk, block of
-//                       heads of one group), 8 waves, a pair per 16 tokens
-//                       splitting the rows of each product; one pass over
-//                       (head, memory),
-//                       tiles streamed through an LDS ring by DMA:
-//                         W' = Kh^T Qbar' -> logits -> p;
-//                         X = dH dy^T = diag(1/r) Kh dy^T -> dwy, dC += g p X;
-//                         Z = Kh Ebar^T, with dQbar and dEbar formed from
-//                         running sums at the head's end (Dy is known then),
-//                       tokens on the MFMA column side so every per-token
-//                       scalar is per lane.  It writes g p_j[t] and dwy_j[t]
-//                       per (b, h, j, t) for the memory kernel, Dy = R . dy
-//                       per (b, t, h) and per-head-block partial sums of
-//                       dQbar, dEbar, dC.
+//   k_sma_keys          key side Kh_j (cache layout, bf16 as hi + lo) and 1 / r_j
+//   k_bwd_prep          Qbar' = Qbar log2(e)/sqrt(N) (storage dtype, the
+//                       forward's operand exactly), q (.) w as hi + lo and its
+//                       RMSNorm row scale, Ebar (float, and bf16 for the memory
+//                       kernel) per token
+//   k_bwd_scores        one workgroup per (64 or 128 tokens of one chunk, block
+//                       of heads of one group), 8 waves, a pair per token group
+//                       splitting the rows of each product; per (head, memory)
+//                       the logit to about 16 bits (W' = Kh^T (q (.) w) from the
+//                       hi + lo operands, times the row scale) and
+//                       dwy = C . X, X = diag(1/r) Kh dy^T, written per
+//                       (b, h, j, t); at the head's end the exact log-sum-exp of
+//                       these logits and Dy = sum_j p_j dwy_j per (b, t, h)
+//   k_bwd_tokens        same blocks: with p_j and dl_j known at every step,
+//                       dQbar += s dl_j Z_j (Z = Kh Ebar^T), dEbar += ln2 dl_j W'_j,
+//                       dC += g p_j X_j on MFMA; it writes g p_j[t] over the
+//                       logit for the memory kernel and per-head-block partial
+//                       sums of dQbar, dEbar, dC
 //   k_bwd_mem           one workgroup per (b, h, 4 memories): M1 and M2 over
 //                       the later tokens, the token stream copied into LDS by
 //                       DMA once for the four memories, dl_j[t] formed from
