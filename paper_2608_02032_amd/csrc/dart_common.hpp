@@ -288,6 +288,93 @@ __device__ __forceinline__ void dma_tile(char* lds, const char* g, int64_t gstri
     }
 }
 
+// One 16-byte global -> LDS copy per lane: global address = sbase (scalar) +
+// voff (per lane, 32-bit), LDS destination = m0 + 16 lane.  Completion is
+// tracked by the wave's vmcnt only (the compiler does not see the write).
+__device__ __forceinline__ void lds_dma16_sbase(uint32_t voff, uint64_t sbase, uint32_t m0) {
+    uint32_t save;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(save)
+        : "v"(voff), "s"(sbase), "s"(m0)
+        : "memory");
+}
+// A pointer made wave-uniform (scalar registers).
+__device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
+    const uint64_t a = (uint64_t)(uintptr_t)p;
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    return ((uint64_t)hi << 32) | (uint64_t)lo;
+}
+
+// Copies of one swizzled LDS tile (the SwzTile<RB> layout, ROWS rows of RB
+// bytes; rows >= rows_valid re-read the last valid row) issued by NW waves,
+// with the per-lane global byte offsets (row * gstride + chunk * 16, 32-bit)
+// fixed at set-up, so that issuing a copy costs no vector address work.  Wave
+// w copies the 1 KiB pieces w, w + NW, ...; lane l of piece k lands at byte
+// 1024 k + 16 l of the tile.
+template <int RB, int ROWS, int NW>
+struct TilePlan {
+    static constexpr int CPR = RB / 16;
+    static constexpr int MASK = (CPR < 8 ? CPR : 8) - 1;
+    static_assert(ROWS * CPR % 64 == 0, "the tile is whole 1 KiB pieces");
+    static constexpr int PIECES = ROWS * CPR / 64;
+    static constexpr int KPW = (PIECES + NW - 1) / NW;  // pieces per wave (at most)
+    uint32_t goff[KPW];
+    __device__ __forceinline__ void init(int wave, int lane, uint32_t gstride, int rows_valid) {
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const int q = (wave + k * NW) * 64 + lane;
+            const int r = q / CPR, ch = (q % CPR) ^ (r & MASK);
+            const int rr = r < rows_valid ? r : rows_valid - 1;
+            goff[k] = (uint32_t)rr * gstride + (uint32_t)(ch * 16);
+            asm volatile("" : "+v"(goff[k]));
+        }
+    }
+    // wave: this wave's index (wave-uniform); lds_tile: LDS byte address
+    __device__ __forceinline__ void issue(const void* gtile, uint32_t lds_tile, int wave) const {
+        const uint64_t sb = uniform_ptr(gtile);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const int piece = wave + k * NW;
+            if (PIECES % NW != 0 && piece >= PIECES) break;
+            lds_dma16_sbase(goff[k], sb,
+                            (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds_tile + (uint32_t)(piece * 1024))));
+        }
+    }
+    // copies this wave issues per tile
+    __device__ __forceinline__ int count(int wave) const {
+        return PIECES / NW + (wave < PIECES % NW ? 1 : 0);
+    }
+};
+// Copies of BYTES contiguous bytes (a multiple of 16) into LDS at the same
+// offsets, NW waves: wave w copies the 1 KiB pieces w, w + NW, ...; lanes past
+// the end of a partial last piece copy nothing.
+template <int BYTES, int NW>
+struct LinearPlan {
+    static_assert(BYTES % 16 == 0, "whole 16-byte pieces");
+    static constexpr int PIECES = (BYTES + 1023) / 1024;
+    static constexpr int KPW = (PIECES + NW - 1) / NW;
+    __device__ __forceinline__ void issue(const void* g, uint32_t lds, int wave, int lane) const {
+        const uint64_t sb = uniform_ptr(g);
+#pragma unroll
+        for (int k = 0; k < KPW; ++k) {
+            const int piece = wave + k * NW;
+            if (PIECES % NW != 0 && piece >= PIECES) break;
+            const uint32_t off = (uint32_t)(piece * 1024 + lane * 16);
+            const uint32_t m0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds + (uint32_t)(piece * 1024)));
+            if (BYTES % 1024 == 0 || off < (uint32_t)BYTES) lds_dma16_sbase(off, sb, m0);
+        }
+    }
+    __device__ __forceinline__ int count(int wave) const {
+        return PIECES / NW + (wave < PIECES % NW ? 1 : 0);
+    }
+};
+
 // MFMA operand fragment from a k-major swizzled tile (rows = k, columns = the
 // operand's m or n index): lane l = 16 g + j receives, for its column
 // cbase + j, the 8 values of rows krow0(g) + 0..3 and krow1(g) + 0..3.

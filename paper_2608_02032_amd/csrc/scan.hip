@@ -768,9 +768,11 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
 // the next s block are read while the current one is multiplied.  The k
 // order of all operands is s (or n) = 16 u + 4 (lane/16) + i for element
 // 4 u + i, which makes the transposing reads of the H and x tiles
-// conflict-free.  Outputs go through a wave-private LDS strip (rows padded to
-// 144 bytes, so the 16-bit accumulator writes do not conflict) and leave as
-// 16-byte row stores.
+// conflict-free.  The products are formed transposed (A = the H or x
+// fragment, B = the C or Gram fragment), so that a lane's accumulator holds
+// y[t][p .. p + 3] of one token t: the row decay exp2(cs_t) is one factor per
+// lane, and each lane stores its outputs as 8-byte pieces straight from
+// registers.  The copies use per-lane offsets fixed at set-up.
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
@@ -779,7 +781,6 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
     int64_t L, int H, int G, int64_t M, int hpb, int64_t nbcg) {
     using T = bf16;
     constexpr int NW = out_waves<S>();
-    constexpr int NT = 64 * NW;
     constexpr int KS = N / 32;
     constexpr int NQ = S / 16 / NW;
     constexpr int XRB = kP * 2;                   // bytes of an x, H or y row
@@ -787,7 +788,6 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
     constexpr int HT = N * XRB;                   // H_[c-1]
     constexpr int AT = 3 * S * 4;                 // per-token record
     constexpr int UB = XT + HT + AT;              // one head's inputs
-    constexpr int YRB = 144;                      // padded staging row
     constexpr int MSK0 = ((NW - 1) >> 1) + 1;     // s blocks of row tile q = 0 (at most)
     constexpr int MSK1 = ((2 * NW - 1) >> 1) + 1; // of row tile q = 1
     constexpr int MSKL = NQ == 2 ? MSK1 : MSK0;   // s blocks of the wave (at most)
@@ -817,34 +817,22 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
     const int len = (int)(L - t0 < S ? L - t0 : S);
 
     __shared__ __attribute__((aligned(16))) char units[2 * UB];
-    __shared__ __attribute__((aligned(16))) char ystage[NW * NQ * 16 * YRB];
 
-    // Copies of one head's inputs into buffer u (LDS destinations as byte
-    // addresses): x and H_[c-1] into swizzled row tiles (rows past the end of
-    // a partial chunk re-read the last row), the record linearly.
+    // Copies of one head's inputs into buffer u: x and H_[c-1] into swizzled
+    // row tiles (rows past the end of a partial chunk re-read the last row),
+    // the record linearly.
     const uint32_t units_lds = lds_addr(units);
+    TilePlan<XRB, S, NW> xplan;
+    TilePlan<XRB, N, NW> hplan;
+    const LinearPlan<AT, NW> rplan;
+    xplan.init(wave, lane, (uint32_t)(H * XRB), len);
+    hplan.init(wave, lane, (uint32_t)XRB, N);
     auto issue_unit = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = hbase + hh;
         const uint32_t ub = units_lds + (uint32_t)(u * UB);
-        auto tile = [&](uint32_t dst, const char* src, int64_t gstride, int rows, int rows_valid) {
-            using Tl = SwzTile<XRB>;
-            for (int q0 = wave * 64; q0 < rows * Tl::CPR; q0 += NT) {
-                const int q = q0 + lane;
-                if (q < rows * Tl::CPR) {
-                    const int r = q / Tl::CPR, ch = (q % Tl::CPR) ^ (r & Tl::MASK);
-                    const int rr = r < rows_valid ? r : rows_valid - 1;
-                    lds_dma16_untracked_at(src + rr * gstride + ch * 16, dst + (uint32_t)(q0 * 16));
-                }
-            }
-        };
-        tile(ub, reinterpret_cast<const char*>(x + ((b * L + t0) * H + h) * kP), (int64_t)H * XRB, S, len);
-        tile(ub + XT, reinterpret_cast<const char*>(states + ((b * M + c) * H + h) * (int64_t)N * kP),
-             XRB, N, N);
-        const char* ag = reinterpret_cast<const char*>(aux + ((b * H + h) * M + c) * 3 * S);
-        for (int q0 = wave * 64; q0 < AT / 16; q0 += NT) {
-            const int q = q0 + lane;
-            if (q < AT / 16) lds_dma16_untracked_at(ag + q * 16, ub + (uint32_t)(XT + HT + q0 * 16));
-        }
+        xplan.issue(x + ((b * L + t0) * H + h) * kP, ub, wave);
+        hplan.issue(states + ((b * M + c) * H + h) * (int64_t)N * kP, ub + XT, wave);
+        rplan.issue(aux + ((b * H + h) * M + c) * 3 * S, ub + XT + HT, wave, lane);
     };
     issue_unit(0, 0);
 
@@ -919,20 +907,18 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
             for (int pt = 0; pt < 4; ++pt) {
                 const bf16x8 hf = ko[pt].read(ht, ks * 32 * XRB);
 #pragma unroll
-                for (int q = 0; q < NQ; ++q) yacc[q][pt] = mma16(yacc[q][pt], craw[q][ks], hf);
+                for (int q = 0; q < NQ; ++q) yacc[q][pt] = mma16(yacc[q][pt], hf, craw[q][ks]);
             }
-        // accumulator rows t = 16 r + 4 grp + i take exp2(cs_t)
+        // the lane's token t = 16 r + col takes exp2(cs_t)
         float cst[NQ];
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            const f32x4 csr = *reinterpret_cast<const f32x4*>(rc + rq[q] * 16 + 4 * lg);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float e = fast_exp2(csr[i]);
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt) yacc[q][pt][i] *= e;
-            }
             cst[q] = rc[rq[q] * 16 + lc];
+            const float e = fast_exp2(cst[q]);
+#pragma unroll
+            for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) yacc[q][pt][i] *= e;
         }
         // intra-chunk term over the s blocks of the heavier row tile
         const int skmax = rq[NQ - 1] >> 1;
@@ -983,38 +969,34 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
                 }
                 const bf16x8 fm = make_frag<T>(mv);
 #pragma unroll
-                for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = mma16(yacc[q][pt], fm, xf[cur][pt]);
+                for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = mma16(yacc[q][pt], xf[cur][pt], fm);
             }
         }
-        // yacc[q][pt][i] = y[t = 16 r_q + 4 grp + i][p = 16 pt + col] -> staging strip
+        // yacc[q][pt][i] = y[t = 16 r_q + col][p = 16 pt + 4 grp + i]: 8-byte stores
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            const int r = rq[q];
-            char* st = ystage + (wave * NQ + q) * 16 * YRB;
+            const int t = rq[q] * 16 + lc;
+            if (t < len) {
+                bf16* yrow = y + ((b * L + t0 + t) * H + h) * kP + 4 * lg;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int pt = 0; pt < 4; ++pt)
-                    *reinterpret_cast<T*>(st + (4 * lg + i) * YRB + (pt * 16 + lc) * 2) = from_f<T>(yacc[q][pt][i]);
-#pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                const int e = lane + 64 * k;
-                const int row = e >> 3, ch = e & 7;
-                const uint4 v = *reinterpret_cast<const uint4*>(st + row * YRB + ch * 16);
-                if (r * 16 + row < len)
-                    *reinterpret_cast<uint4*>(y + ((b * L + t0 + r * 16 + row) * H + h) * kP + ch * 8) = v;
+                for (int pt = 0; pt < 4; ++pt) {
+                    const bf16x4 v = {(bf16)yacc[q][pt][0], (bf16)yacc[q][pt][1], (bf16)yacc[q][pt][2],
+                                      (bf16)yacc[q][pt][3]};
+                    *reinterpret_cast<bf16x4*>(yrow + 16 * pt) = v;
+                }
             }
         }
     };
 
     for (int hh = 0; hh < hpb; ++hh) {
         // this wave's copies of head hh are in: only the y stores of head
-        // hh - 1 were issued after them (vector memory operations complete in
-        // order); a partial chunk, whose stores are predicated, waits for all
+        // hh - 1 (four per row tile) were issued after them (vector memory
+        // operations complete in order); a partial chunk, whose stores are
+        // predicated, waits for all
         if (hh == 0 || len < S) {
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         } else {
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NQ));
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * NQ));
         }
         lds_barrier();  // every wave's copies are in; head hh - 1 is done with its buffer
         if (hh + 1 < hpb) issue_unit(hh + 1, (hh + 1) & 1);
