@@ -816,7 +816,12 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
     const int64_t t0 = c * S;
     const int len = (int)(L - t0 < S ? L - t0 : S);
 
-    __shared__ __attribute__((aligned(16))) char units[2 * UB];
+    // the two head buffers; before the head loop the same bytes hold the
+    // chunk's B and C rows (swizzled [S][N] tiles) for the Gram pairs
+    constexpr int BRB = N * 2;
+    constexpr int BCT = S * BRB;
+    constexpr int LDSB = 2 * UB > 2 * BCT ? 2 * UB : 2 * BCT;
+    __shared__ __attribute__((aligned(16))) char units[LDSB];
 
     // Copies of one head's inputs into buffer u: x and H_[c-1] into swizzled
     // row tiles (rows past the end of a partial chunk re-read the last row),
@@ -834,25 +839,34 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
         hplan.issue(states + ((b * M + c) * H + h) * (int64_t)N * kP, ub + XT, wave);
         rplan.issue(aux + ((b * H + h) * M + c) * 3 * S, ub + XT + HT, wave, lane);
     };
-    issue_unit(0, 0);
+    // the chunk's B and C rows, one copy burst (rows past the end of a partial
+    // chunk re-read the last row: finite values, zero weight)
+    {
+        TilePlan<BRB, S, NW> bcplan;
+        bcplan.init(wave, lane, (uint32_t)(G * BRB), len);
+        bcplan.issue(Bm + ((b * L + t0) * G + g) * N, units_lds, wave);
+        bcplan.issue(Cm + ((b * L + t0) * G + g) * N, units_lds + BCT, wave);
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
+    const char* const btile = units;
+    const char* const ctile = units + BCT;
 
-    // the wave's row tiles and their C rows, in the k order above (rows past
-    // the end of a partial chunk read the last row: finite values, zero weight)
+    // the wave's row tiles and their C rows, in the k order above
     int rq[NQ];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) rq[q] = tile_row(wave, q, NW);
-    auto kfrag = [&](const bf16* row, int ks) __attribute__((always_inline)) {
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 4 * grp);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(row + ks * 32 + 16 + 4 * grp);
+    auto kfrag = [&](const char* tile, int row, int ks) __attribute__((always_inline)) {
+        using Tl = SwzTile<BRB>;
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(tile + Tl::off(row, (ks * 32 + 4 * grp) * 2));
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(tile + Tl::off(row, (ks * 32 + 16 + 4 * grp) * 2));
         return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     };
     bf16x8 craw[NQ][KS];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-        const int t = rq[q] * 16 + col;
-        const bf16* crow = Cm + ((b * L + t0 + (t < len ? t : len - 1)) * G + g) * N;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) craw[q][ks] = kfrag(crow, ks);
+        for (int ks = 0; ks < KS; ++ks) craw[q][ks] = kfrag(ctile, rq[q] * 16 + col, ks);
     }
     // Gram pairs of the wave's row tiles: element 4 u + i of pair (q, sk) is
     // G^T[s = 32 sk + 16 u + 4 grp + i][t = 16 r_q + col]
@@ -861,11 +875,9 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
         f32x4 acc[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            const int sr = sk * 32 + u * 16 + col;
-            const bf16* brow = Bm + ((b * L + t0 + (sr < len ? sr : len - 1)) * G + g) * N;
             acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) acc[u] = mma16(acc[u], kfrag(brow, ks), craw[q][ks]);
+            for (int ks = 0; ks < KS; ++ks) acc[u] = mma16(acc[u], kfrag(btile, sk * 32 + u * 16 + col, ks), craw[q][ks]);
         }
         const float v[8] = {acc[0][0], acc[0][1], acc[0][2], acc[0][3],
                             acc[1][0], acc[1][1], acc[1][2], acc[1][3]};
@@ -879,6 +891,8 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
         for (int sk = 0; sk < MSK1; ++sk)
             if (sk <= (rq[NQ - 1] >> 1)) gq1[sk] = gram_pair(NQ - 1, sk);
     }
+    lds_barrier();  // the B and C tiles are consumed: the head buffers take over
+    issue_unit(0, 0);
 
     // transposing fragment reads at offsets fixed here: rows (k) 4 grp + i and
     // 16 + 4 grp + i of a 32-row block, column tile pt
