@@ -355,8 +355,10 @@ __global__ __launch_bounds__(256) void k_sbwd_pass2(
 // Set q holds tiles q, NKB - 1 - q, NKB + q and 2 NKB - 1 - q (NKB = S / 32),
 // which gives every set the same number of causal (tile, s block) pairs.
 // Wave w owns tile w % 4 and half w / 4 of the n tiles and of the tile's
-// pairs.  dB and dC receive the rank-P terms (k_sbwd_bc adds the quadratic
-// ones); Mbar goes out as bf16 [S][S] (rows s, columns t, causal blocks).
+// pairs.  The products take the raw x and dy rows; the per-token factors
+// (dt_t e^{cs_e - cs_t}, e^{cs_t}) scale their fp32 results.  dB and dC
+// receive the rank-P terms (k_sbwd_bc adds the quadratic ones); Mbar goes out
+// as bf16 [S][S] (rows s, columns t, causal blocks).
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(512) void k_sbwd_group(
@@ -365,7 +367,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
     const bf16* __restrict__ Wb, float* __restrict__ dB, float* __restrict__ dC,
     float* __restrict__ wp, bf16* __restrict__ mbar, int64_t L, int H, int G, int64_t M,
     int64_t nbcg) {
-    constexpr int NW = 8, NT = 512;
+    constexpr int NW = 8;
     constexpr int XRB = kP * 2;
     constexpr int DYT = S * XRB, TT = N * XRB, RECB = 3 * S * 4;
     constexpr int UB = DYT + 2 * TT + RECB;
@@ -396,13 +398,18 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
     __shared__ __attribute__((aligned(16))) char ubuf[2][UB];
     __shared__ float wpart[2][2][64];
 
+    TilePlan<XRB, S, NW> dyplan;
+    TilePlan<XRB, N, NW> nplan;
+    dyplan.init(wave, lane, (uint32_t)(H * XRB), len);
+    nplan.init(wave, lane, (uint32_t)XRB, N);
+    const uint32_t ubl = lds_addr(ubuf);
     auto issue = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = g * hpg + hh;
         const int64_t o = ((b * M + c) * H + h) * (int64_t)N * kP;
-        dma_tile<XRB, true>(&ubuf[u][0], reinterpret_cast<const char*>(dy + ((b * L + t0) * H + h) * kP),
-                            (int64_t)H * XRB, S, len, wave, NW, lane);
-        dma_tile<XRB, true>(&ubuf[u][DYT], reinterpret_cast<const char*>(Wb + o), XRB, N, N, wave, NW, lane);
-        dma_tile<XRB, true>(&ubuf[u][DYT + TT], reinterpret_cast<const char*>(Hb + o), XRB, N, N, wave, NW, lane);
+        const uint32_t ub = ubl + (uint32_t)(u * UB);
+        dyplan.issue(dy + ((b * L + t0) * H + h) * kP, ub, wave);
+        nplan.issue(Wb + o, ub + DYT, wave);
+        nplan.issue(Hb + o, ub + DYT + TT, wave);
     };
     // per-token record of head hh (cs, dt, b_s = e^{cs_s - cs at the s block
     // start}): thread tid < S takes token tid; loaded early, stored to LDS
@@ -426,10 +433,13 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
         }
     };
     // C_t at the n rows this lane's accumulators hold (16 nt + 4 grp + i)
-    bf16x4 cv[NTH];
+    float cvf[NTH][4];
 #pragma unroll
-    for (int j = 0; j < NTH; ++j)
-        cv[j] = *reinterpret_cast<const bf16x4*>(Cm + ((b * L + t0 + tc) * G + g) * N + (nh * NTH + j) * 16 + 4 * grp);
+    for (int j = 0; j < NTH; ++j) {
+        const bf16x4 cv = *reinterpret_cast<const bf16x4*>(Cm + ((b * L + t0 + tc) * G + g) * N + (nh * NTH + j) * 16 + 4 * grp);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cvf[j][i] = (float)cv[i];
+    }
     f32x4 accB[NTH], accC[NTH];
 #pragma unroll
     for (int j = 0; j < NTH; ++j) {
@@ -473,13 +483,16 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
         const char* htl = &ubuf[u][DYT + TT];
         const float* rcs = reinterpret_cast<const float*>(&ubuf[u][DYT + 2 * TT]);
         const float* rbs = rcs + 2 * S;
-        const float cst = rcs[t], dtt = rcs[S + t], cse = rcs[S - 1];
+        // the lane's token, opaque per head: the diagonal masks derived from
+        // it are formed in the loop rather than held across it
+        int tq = t;
+        asm volatile("" : "+v"(tq));
+        const float cst = rcs[tq], dtt = rcs[S + tq], cse = rcs[S - 1];
         const float sx = valid ? dtt * fast_exp2(cse - cst) : 0.f;
         const float sy = valid ? fast_exp2(cst) : 0.f;
-        const bf16x8 xs0 = scale_frag(xf0, sx), xs1 = scale_frag(xf1, sx);
-        const bf16x8 ys0 = scale_frag(frag_rowmajor<bf16, XRB>(dyt, tc, 8 * grp), sy);
-        const bf16x8 ys1 = scale_frag(frag_rowmajor<bf16, XRB>(dyt, tc, 32 + 8 * grp), sy);
-        // dB_t += W (dt_t e^{cs_e - cs_t} x_t); H dy^ (dy^ = e^{cs_t} dy_t):
+        const bf16x8 y0 = frag_rowmajor<bf16, XRB>(dyt, tc, 8 * grp);
+        const bf16x8 y1 = frag_rowmajor<bf16, XRB>(dyt, tc, 32 + 8 * grp);
+        // dB_t += dt_t e^{cs_e - cs_t} (W x_t); with dy^ = e^{cs_t} dy_t:
         // dC_t += H dy^, w_t = C_t . H dy^
         float wsum = 0.f;
 #pragma unroll
@@ -487,16 +500,18 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
             const int nrow = (nh * NTH + j) * 16 + col;
             const bf16x8 w0 = frag_rowmajor<bf16, XRB>(wtl, nrow, 8 * grp);
             const bf16x8 w1 = frag_rowmajor<bf16, XRB>(wtl, nrow, 32 + 8 * grp);
-            accB[j] = mma16(mma16(accB[j], w0, xs0), w1, xs1);
+            const f32x4 pb = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, w0, xf0), w1, xf1);
             const bf16x8 h0f = frag_rowmajor<bf16, XRB>(htl, nrow, 8 * grp);
             const bf16x8 h1f = frag_rowmajor<bf16, XRB>(htl, nrow, 32 + 8 * grp);
-            const f32x4 tmp = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, h0f, ys0), h1f, ys1);
+            const f32x4 pc = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, h0f, y0), h1f, y1);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                wsum += (float)cv[j][i] * tmp[i];
-                accC[j][i] += tmp[i];
+                accB[j][i] += sx * pb[i];
+                wsum += cvf[j][i] * pc[i];
+                accC[j][i] += sy * pc[i];
             }
         }
+        wsum *= sy;
         wsum += __shfl_xor(wsum, 16, 64);
         wsum += __shfl_xor(wsum, 32, 64);
         if (grp == 0) wpart[u][nh][slot * 16 + col] = wsum;
@@ -516,6 +531,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
                 const int sb = 32 * K + 8 * grp;
                 if (K > (T >> 1)) {
                     const float at = fast_exp2(rcs[32 * K] - cst) * dtt;
+                    // (off the diagonal block every s of the block follows t)
                     const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + sb);
                     const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + sb + 4);
 #pragma unroll
@@ -528,8 +544,8 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
                     const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + sb + 4);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        if (sb + i >= t && sb + i < len) mb[k][i] += g2[0][i] * (fast_exp2(c0[i] - cst) * dtt);
-                        if (sb + 4 + i >= t && sb + 4 + i < len) mb[k][4 + i] += g2[1][i] * (fast_exp2(c1[i] - cst) * dtt);
+                        if (sb + i >= tq && sb + i < len) mb[k][i] += g2[0][i] * (fast_exp2(c0[i] - cst) * dtt);
+                        if (sb + 4 + i >= tq && sb + 4 + i < len) mb[k][4 + i] += g2[1][i] * (fast_exp2(c1[i] - cst) * dtt);
                     }
                 }
             }
@@ -589,7 +605,6 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     const float* __restrict__ wp, float* __restrict__ dx, float* __restrict__ ddt,
     float* __restrict__ dAp, int64_t L, int H, int G, int64_t M, int hpb, int64_t nbcg, int nkp) {
     constexpr int NW = quad_waves<S>();
-    constexpr int NT = 64 * NW;
     constexpr int NQ = S / 16 / NW;
     constexpr int NKB = S / 32;
     constexpr int NPW = NQ == 2 ? NKB + 1 : NKB;  // pairs of a wave (at most)
@@ -599,6 +614,9 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     constexpr int REC = 3 * S * 4;                // cs (log2), dt, b_s
     constexpr int UB = DYT + WTB + REC;
     constexpr int TPL = S / 64;
+    constexpr int BRB = N * 2;                    // bytes of a B or C row
+    constexpr int BCT = S * BRB;
+    constexpr int LDSB = 2 * UB > 2 * BCT ? 2 * UB : 2 * BCT;
     static_assert(NQ == 1 || NQ == 2, "one or two row tiles per wave");
 
     const int nhs = (H / G) / hpb;
@@ -615,16 +633,22 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     const int64_t t0 = c * S;
     const int len = (int)(L - t0 < S ? L - t0 : S);
 
-    __shared__ __attribute__((aligned(16))) char ubuf[2][UB];
+    // the two head buffers; before the head loop the same bytes hold the
+    // chunk's B and C rows (swizzled [S][N] tiles) for the G1 pairs
+    __shared__ __attribute__((aligned(16))) char lbuf[LDSB];
+    char (*const ubuf)[UB] = reinterpret_cast<char (*)[UB]>(lbuf);
     __shared__ float rpart[NW][S];
     __shared__ float tok[3][S];
 
+    TilePlan<XRB, S, NW> dyplan;
+    TilePlan<XRB, N, NW> wplan;
+    dyplan.init(wave, lane, (uint32_t)(H * XRB), len);
+    wplan.init(wave, lane, (uint32_t)XRB, N);
     auto issue = [&](int hh, int u) __attribute__((always_inline)) {
         const int h = hbase + hh;
-        dma_tile<XRB, true>(&ubuf[u][0], reinterpret_cast<const char*>(dy + ((b * L + t0) * H + h) * kP),
-                            (int64_t)H * XRB, S, len, wave, NW, lane);
-        dma_tile<XRB, true>(&ubuf[u][DYT], reinterpret_cast<const char*>(Wb + ((b * M + c) * H + h) * (int64_t)N * kP),
-                            XRB, N, N, wave, NW, lane);
+        const uint32_t ub = lds_addr(lbuf) + (uint32_t)(u * UB);
+        dyplan.issue(dy + ((b * L + t0) * H + h) * kP, ub, wave);
+        wplan.issue(Wb + ((b * M + c) * H + h) * (int64_t)N * kP, ub + DYT, wave);
     };
     // per-token record of head hh (cs, dt, b_s): thread tid < S takes token
     // tid; loaded early, stored to LDS before the barrier that opens the head
@@ -655,9 +679,17 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     const int nk0 = NKB - kmin0;
     const int npw = nk0 + (NQ == 2 ? NKB - kmin1 : 0);
 
-    issue(0, 0);
-    load_rec(0);
-    store_rec(0);
+    // the chunk's B and C rows, one copy burst (rows past the end of a
+    // partial chunk re-read the last row: finite values, zero weight)
+    const uint32_t lb = lds_addr(lbuf);
+    {
+        TilePlan<BRB, S, NW> bcplan;
+        bcplan.init(wave, lane, (uint32_t)(G * BRB), len);
+        bcplan.issue(Bm + ((b * L + t0) * G + g) * N, lb, wave);
+        bcplan.issue(Cm + ((b * L + t0) * G + g) * N, lb + BCT, wave);
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();
     // G1 of every pair, kept as bf16
     bf16x8 g1c[NPW];
 #pragma unroll
@@ -667,15 +699,14 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
             const int T = q ? T1 : T0;
             const int K = q ? kmin1 + j - nk0 : kmin0 + j;
             const int t = 16 * T + col;
-            const bf16* brow = Bm + ((b * L + t0 + (t < len ? t : len - 1)) * G + g) * N + 8 * grp;
             f32x4 gg[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
             for (int uu = 0; uu < 2; ++uu) {
                 const int s = 32 * K + gram_row(uu, col);
-                const bf16* crow = Cm + ((b * L + t0 + (s < len ? s : len - 1)) * G + g) * N + 8 * grp;
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks)
-                    gg[uu] = mma16(gg[uu], load_frag(crow + 32 * ks), load_frag(brow + 32 * ks));
+                    gg[uu] = mma16(gg[uu], frag_rowmajor<bf16, BRB>(lbuf + BCT, s, 32 * ks + 8 * grp),
+                                   frag_rowmajor<bf16, BRB>(lbuf, t, 32 * ks + 8 * grp));
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -684,6 +715,10 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
             }
         }
     }
+    lds_barrier();  // the B and C tiles are consumed: the head buffers take over
+    issue(0, 0);
+    load_rec(0);
+    store_rec(0);
     KmOffSpread<XRB> ko[4];  // transposing reads of dy^T (k = s) and W^T (k = n), p tile pt
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) ko[pt].init(8 * grp, 8 * grp + 4, spread_base(pt), lane);
