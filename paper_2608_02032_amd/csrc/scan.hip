@@ -256,10 +256,10 @@ __global__ __launch_bounds__(kThreads) void k_chunk_state(
 // the contraction weights exp(cs_e - cs_s) dt_s stay in LDS (over the B rows,
 // no longer needed), the per-token record and the total log decay go to the
 // workspace.  Per head, the x rows arrive by DMA in one of two buffers while
-// the previous head computes.  Wave w owns n tiles NTW (w % NG) .. and p tiles
-// PTW (w / NG) .. of the N x P result; each x fragment is scaled by the
-// weights of its tokens before the MFMAs.  The result leaves through a
-// wave-private LDS strip (rows padded to PTW 32 + 16 bytes) as 16-byte pieces.
+// the previous head computes.  Wave w owns n tiles NTW (w % 2) .. of p tile
+// w / 2 of the N x P result (so two waves weight each x fragment, by the
+// weights of its tokens, before the MFMAs); the products are formed
+// transposed, a lane holding dH[n][p .. p + 3], and leave as 8-byte stores.
 // ---------------------------------------------------------------------------
 template <int N, int S>
 __global__ __launch_bounds__(512) void k_chunk_state_heads(
@@ -268,17 +268,14 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
     float* __restrict__ aux, int64_t L, int H, int G, int64_t M, int64_t Mcap, int hpb,
     int64_t nbcg) {
     using T = bf16;
-    constexpr int NW = 8, NT = 64 * NW;
+    constexpr int NW = 8;
     constexpr int XRB = kP * 2;                 // bytes per x row
     constexpr int BRB = N * 2;                  // bytes per B row
     constexpr int XT = S * XRB, BT = S * BRB;
     constexpr int KST = S / 32;                 // 32-token k steps
-    constexpr int NTW = N >= 128 ? N / 64 : 1;  // n tiles per wave
-    constexpr int PTW = (N / 32) / NTW;         // p tiles per wave
-    constexpr int NG = (N / 16) / NTW;          // n-tile groups
-    static_assert(NG * (4 / PTW) == NW, "tiles cover the waves");
-    constexpr int SRB = PTW * 32 + 16;          // padded staging row (bytes)
-    constexpr int SROWS = NTW * 16;
+    constexpr int NTW = N / 32;                 // n tiles per wave
+    constexpr int NG = 2;                       // n-tile groups
+    static_assert(NG * NTW * 16 == N && NG * 4 == NW, "tiles cover the waves");
     constexpr int TPL = S / 64;                 // tokens per lane in a decay scan
     constexpr int LPB = 32 / TPL;               // lanes per 32-token block
 
@@ -310,34 +307,24 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
     // head loop copy
     __shared__ __attribute__((aligned(16))) char bt[BT];
     __shared__ __attribute__((aligned(16))) char xbuf[2][XT];
-    __shared__ __attribute__((aligned(16))) char ystage[NW * SROWS * SRB];
     float* const wall = reinterpret_cast<float*>(bt);
     const float* const dtall = reinterpret_cast<const float*>(&xbuf[1][0]);
     const uint32_t bt_lds = lds_addr(bt), x_lds = lds_addr(xbuf);
 
     // copies into swizzled row tiles (rows past the end re-read the last row)
-    auto tile = [&](uint32_t dst, const char* src, int64_t gstride, int rows, int rows_valid, auto rbc)
-        __attribute__((always_inline)) {
-        constexpr int RB = decltype(rbc)::value;
-        using Tl = SwzTile<RB>;
-        for (int q0 = wave * 64; q0 < rows * Tl::CPR; q0 += NT) {
-            const int q = q0 + lane;
-            if (q < rows * Tl::CPR) {
-                const int r = q / Tl::CPR, ch = (q % Tl::CPR) ^ (r & Tl::MASK);
-                const int rr = r < rows_valid ? r : rows_valid - 1;
-                lds_dma16_untracked_at(src + rr * gstride + ch * 16, dst + (uint32_t)(q0 * 16));
-            }
-        }
-    };
+    TilePlan<XRB, S, NW> xplan;
+    xplan.init(wave, lane, (uint32_t)(H * XRB), len);
     auto issue_x = [&](int hh, int u) __attribute__((always_inline)) {
-        tile(x_lds + (uint32_t)(u * XT), reinterpret_cast<const char*>(x + ((b * L + t0) * H + hbase + hh) * kP),
-             (int64_t)H * XRB, S, len, std::integral_constant<int, XRB>{});
+        xplan.issue(x + ((b * L + t0) * H + hbase + hh) * kP, x_lds + (uint32_t)(u * XT), wave);
     };
 
     // prologue copies: B rows, head 0's x rows, every head's dt (one 4-byte
     // copy per token; head hd by wave hd % 8)
-    tile(bt_lds, reinterpret_cast<const char*>(Bm + ((b * L + t0) * G + g) * N), (int64_t)G * BRB, S, len,
-         std::integral_constant<int, BRB>{});
+    {
+        TilePlan<BRB, S, NW> bplan;
+        bplan.init(wave, lane, (uint32_t)(G * BRB), len);
+        bplan.issue(Bm + ((b * L + t0) * G + g) * N, bt_lds, wave);
+    }
     issue_x(0, 0);
     for (int hd = wave; hd < hpb; hd += NW) {
 #pragma unroll
@@ -406,61 +393,41 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
         }
         if (lane == 0) chunk_lda[(b * H + h) * M + c] = cse;
     }
-    KmOffBf16<XRB> xo[PTW];
-#pragma unroll
-    for (int j = 0; j < PTW; ++j) xo[j].init(8 * grp, 8 * grp + 4, (pg * PTW + j) * 16, lane);
-    constexpr int CPRW = PTW * 2;                               // 16-byte pieces per staged row
-    constexpr int NSTW = (SROWS * CPRW + 63) / 64;              // 16-byte stores per wave and head
+    KmOffBf16<XRB> xo;
+    xo.init(8 * grp, 8 * grp + 4, pg * 16, lane);
 
     for (int hh = 0; hh < hpb; ++hh) {
         const int u = hh & 1;
         // this wave's copies of head hh are in: only its dH stores of head
-        // hh - 1 came after them (head 0's were waited for in the prologue)
-        if (hh > 0) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NSTW));
+        // hh - 1 (NTW) came after them (head 0's were waited for in the prologue)
+        if (hh > 0) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NTW));
         lds_barrier();  // copies of head hh and all weights visible; buffer u ^ 1 is free
         if (hh + 1 < hpb) issue_x(hh + 1, u ^ 1);
         const float* wv = wall + hh * S;
-        f32x4 acc[NTW][PTW];
+        f32x4 acc[NTW];
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
-#pragma unroll
-            for (int k = 0; k < PTW; ++k) acc[j][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < NTW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KST; ++ks) {
             const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp);
             const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp + 4);
+            const bf16x8 xr = xo.read(&xbuf[u][0], ks * 32 * XRB);
+            float v[8];
 #pragma unroll
-            for (int k = 0; k < PTW; ++k) {
-                const bf16x8 xr = xo[k].read(&xbuf[u][0], ks * 32 * XRB);
-                float v[8];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    v[i] = to_f(xr[i]) * w0[i];
-                    v[4 + i] = to_f(xr[4 + i]) * w1[i];
-                }
-                const bf16x8 xf = make_frag<T>(v);
-#pragma unroll
-                for (int j = 0; j < NTW; ++j) acc[j][k] = mma16(acc[j][k], bfr[j][ks], xf);
+            for (int i = 0; i < 4; ++i) {
+                v[i] = to_f(xr[i]) * w0[i];
+                v[4 + i] = to_f(xr[4 + i]) * w1[i];
             }
+            const bf16x8 xf = make_frag<T>(v);
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) acc[j] = mma16(acc[j], xf, bfr[j][ks]);
         }
-        // acc[j][k][i] = dH[n = 16 (ng NTW + j) + 4 grp + i][p = 16 (pg PTW + k) + col]
-        char* st = ystage + wave * SROWS * SRB;
+        // acc[j][i] = dH[n = 16 (ng NTW + j) + col][p = 16 pg + 4 grp + i]
+        T* dst = mem + ((b * Mcap + c) * H + hbase + hh) * (int64_t)N * kP + 16 * pg + 4 * grp;
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
-#pragma unroll
-            for (int k = 0; k < PTW; ++k)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    *reinterpret_cast<T*>(st + (16 * j + 4 * grp + i) * SRB + (16 * k + col) * 2) = from_f<T>(acc[j][k][i]);
-        T* dst = mem + ((b * Mcap + c) * H + hbase + hh) * (int64_t)N * kP + (ng * NTW * 16) * kP + pg * PTW * 16;
-#pragma unroll
-        for (int e0 = 0; e0 < SROWS * CPRW; e0 += 64) {
-            const int e = e0 + lane;
-            if (e < SROWS * CPRW) {
-                const int row = e / CPRW, ch = e % CPRW;
-                const uint4 v = *reinterpret_cast<const uint4*>(st + row * SRB + ch * 16);
-                *reinterpret_cast<uint4*>(dst + row * kP + ch * 8) = v;
-            }
+        for (int j = 0; j < NTW; ++j) {
+            const bf16x4 v4 = {(bf16)acc[j][0], (bf16)acc[j][1], (bf16)acc[j][2], (bf16)acc[j][3]};
+            *reinterpret_cast<bf16x4*>(dst + (16 * (ng * NTW + j) + col) * kP) = v4;
         }
     }
 }

@@ -125,10 +125,12 @@ __device__ __forceinline__ void block_bcg(int64_t nbcg, int nhs, int64_t& bcg, i
 // log decay.  MODE 1: Am = C, V = dy, w_s = e^{cs_s} (the chunk adjoint dR).
 // Am^T fragments are read once (k-major from the LDS tile) and kept for every
 // head of the slice; each head's V rows arrive by DMA in one of two buffers
-// while the previous head computes.  Wave w owns n tiles NTW (w % NG) .. and
-// p tiles PTW (w / NG) .. of the N x P result.  The slice-0 workgroup also
-// writes Am^T of the chunk, [N][S] bf16 (columns past the end repeat the last
-// token; every consumer gives them zero weight).
+// while the previous head computes.  Wave w owns n tiles NTW (w % 2) .. of
+// p tile w / 2 of the N x P result (so two waves weight each V fragment);
+// the products are formed transposed, a lane holding out[n][p .. p + 3],
+// and leave as 8-byte stores.  The slice-0 workgroup also writes Am^T of the
+// chunk, [N][S] bf16 (columns past the end repeat the last token; every
+// consumer gives them zero weight).
 // ---------------------------------------------------------------------------
 template <int N, int S, int MODE>
 __global__ __launch_bounds__(512) void k_sbwd_contract(
@@ -141,12 +143,11 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
     constexpr int ARB = N * 2;
     constexpr int VT = S * VRB, ATB = S * ARB;
     constexpr int KST = S / 32;
-    constexpr int NTW = N >= 128 ? N / 64 : 1;
-    constexpr int PTW = (N / 32) / NTW;
-    constexpr int NG = (N / 16) / NTW;
-    static_assert(NG * (4 / PTW) == NW, "tiles cover the waves");
+    constexpr int NTW = N / 32;         // n tiles per wave
+    constexpr int NG = 2;               // n-tile groups
+    static_assert(NG * NTW * 16 == N && NG * 4 == NW, "tiles cover the waves");
     constexpr int TPL = S / 64;
-    constexpr int NST = NTW * PTW * 4;  // stores per head and wave
+    constexpr int NST = NTW;            // stores per head and wave
 
     const int nhs = (H / G) / hpb;
     int64_t bcg;
@@ -168,12 +169,17 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
     __shared__ __attribute__((aligned(16))) char vbuf[2][VT];
     float* const wall = reinterpret_cast<float*>(atile);
 
+    TilePlan<VRB, S, NW> vplan;
+    vplan.init(wave, lane, (uint32_t)(H * VRB), len);
+    const uint32_t vbl = lds_addr(vbuf);
     auto issue_v = [&](int hh, int u) __attribute__((always_inline)) {
-        dma_tile<VRB, true>(&vbuf[u][0], reinterpret_cast<const char*>(V + ((b * L + t0) * H + hbase + hh) * kP),
-                            (int64_t)H * VRB, S, len, wave, NW, lane);
+        vplan.issue(V + ((b * L + t0) * H + hbase + hh) * kP, vbl + (uint32_t)(u * VT), wave);
     };
-    dma_tile<ARB, true>(atile, reinterpret_cast<const char*>(Am + ((b * L + t0) * G + g) * N), (int64_t)G * ARB, S,
-                        len, wave, NW, lane);
+    {
+        TilePlan<ARB, S, NW> aplan;
+        aplan.init(wave, lane, (uint32_t)(G * ARB), len);
+        aplan.issue(Am + ((b * L + t0) * G + g) * N, lds_addr(atile), wave);
+    }
     issue_v(0, 0);
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     lds_barrier();
@@ -236,9 +242,8 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
             if (lane == 0) lda[(b * H + h) * M + c] = cse;
         }
     }
-    KmOffBf16<VRB> vo[PTW];
-#pragma unroll
-    for (int j = 0; j < PTW; ++j) vo[j].init(8 * grp, 8 * grp + 4, (pg * PTW + j) * 16, lane);
+    KmOffBf16<VRB> vo;
+    vo.init(8 * grp, 8 * grp + 4, pg * 16, lane);
 
     for (int hh = 0; hh < hpb; ++hh) {
         const int u = hh & 1;
@@ -248,38 +253,31 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
         lds_barrier();
         if (hh + 1 < hpb) issue_v(hh + 1, u ^ 1);
         const float* wv = wall + hh * S;
-        f32x4 acc[NTW][PTW];
+        f32x4 acc[NTW];
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
-#pragma unroll
-            for (int k = 0; k < PTW; ++k) acc[j][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < NTW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KST; ++ks) {
             const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp);
             const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp + 4);
+            const bf16x8 vr = vo.read(&vbuf[u][0], ks * 32 * VRB);
+            float v[8];
 #pragma unroll
-            for (int k = 0; k < PTW; ++k) {
-                const bf16x8 vr = vo[k].read(&vbuf[u][0], ks * 32 * VRB);
-                float v[8];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    v[i] = (float)vr[i] * w0[i];
-                    v[4 + i] = (float)vr[4 + i] * w1[i];
-                }
-                const bf16x8 vf = make_frag<bf16>(v);
-#pragma unroll
-                for (int j = 0; j < NTW; ++j) acc[j][k] = mma16(acc[j][k], afr[j][ks], vf);
+            for (int i = 0; i < 4; ++i) {
+                v[i] = (float)vr[i] * w0[i];
+                v[4 + i] = (float)vr[4 + i] * w1[i];
             }
+            const bf16x8 vf = make_frag<bf16>(v);
+#pragma unroll
+            for (int j = 0; j < NTW; ++j) acc[j] = mma16(acc[j], vf, afr[j][ks]);
         }
-        // acc[j][k][i] = out[n = 16 (ng NTW + j) + 4 grp + i][p = 16 (pg PTW + k) + col]
-        bf16* dst = out + ((b * M + c) * H + hbase + hh) * (int64_t)N * kP;
+        // acc[j][i] = out[n = 16 (ng NTW + j) + col][p = 16 pg + 4 grp + i]
+        bf16* dst = out + ((b * M + c) * H + hbase + hh) * (int64_t)N * kP + 16 * pg + 4 * grp;
 #pragma unroll
-        for (int j = 0; j < NTW; ++j)
-#pragma unroll
-            for (int k = 0; k < PTW; ++k)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    dst[(16 * (ng * NTW + j) + 4 * grp + i) * kP + 16 * (pg * PTW + k) + col] = (bf16)acc[j][k][i];
+        for (int j = 0; j < NTW; ++j) {
+            const bf16x4 v4 = {(bf16)acc[j][0], (bf16)acc[j][1], (bf16)acc[j][2], (bf16)acc[j][3]};
+            *reinterpret_cast<bf16x4*>(dst + (16 * (ng * NTW + j) + col) * kP) = v4;
+        }
     }
 }
 
