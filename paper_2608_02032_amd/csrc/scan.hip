@@ -352,7 +352,7 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
         KmOffBf16<BRB> bo;
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
-            bo.init(8 * grp, 8 * grp + 4, (ng * NTW + j) * 16, lane);
+            bo.init(4 * grp, 16 + 4 * grp, (ng * NTW + j) * 16, lane);
 #pragma unroll
             for (int ks = 0; ks < KST; ++ks) bfr[j][ks] = bo.read(bt, ks * 32 * BRB);
         }
@@ -394,7 +394,7 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
         if (lane == 0) chunk_lda[(b * H + h) * M + c] = cse;
     }
     KmOffBf16<XRB> xo;
-    xo.init(8 * grp, 8 * grp + 4, pg * 16, lane);
+    xo.init(4 * grp, 16 + 4 * grp, pg * 16, lane);
 
     for (int hh = 0; hh < hpb; ++hh) {
         const int u = hh & 1;
@@ -409,8 +409,8 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
         for (int j = 0; j < NTW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KST; ++ks) {
-            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp);
-            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp + 4);
+            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 4 * grp);
+            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 16 + 4 * grp);
             const bf16x8 xr = xo.read(&xbuf[u][0], ks * 32 * XRB);
             float v[8];
 #pragma unroll

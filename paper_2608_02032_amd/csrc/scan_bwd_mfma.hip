@@ -65,11 +65,16 @@ template <int S> constexpr int quad_waves() { return S / 16 >= 8 ? 8 : S / 16; }
 __device__ __forceinline__ int quad_tile(int w, int q, int nw) {
     return q == 0 ? w : 2 * nw - 1 - w;
 }
-// Row r of the A operand of the 32-row Gram tile u holds token
-// 8 (r / 4) + 4 u + r % 4 of its s block, so that accumulator element
-// 4 u + i of lane l (row 4 (l / 16) + i) is token 8 (l / 16) + 4 u + i: the
-// eight s values a lane holds are consecutive.
-__device__ __forceinline__ int gram_row(int u, int r) { return 8 * (r >> 2) + 4 * u + (r & 3); }
+// Row r of the A operand of the 32-row Gram tile u holds token 16 u + r of
+// its s block, so that accumulator element 4 u + i of lane l (row
+// 4 (l / 16) + i) is token 16 u + 4 (l / 16) + i: the k order of every
+// operand that meets these values (s, or n for B_t and W^T) is
+// 16 u + 4 (lane / 16) + i, which keeps the transposing reads of
+// KmOffSpread free of bank conflicts.
+__device__ __forceinline__ int gram_row(int u, int r) { return 16 * u + r; }
+// The token (or n) of element e of a lane's 8-value fragment in that order,
+// within its 32-block.
+__device__ __forceinline__ int korder(int e, int grp) { return 16 * (e >> 2) + 4 * grp + (e & 3); }
 
 __device__ __forceinline__ bf16x8 scale_frag(bf16x8 v, float s) {
     bf16x8 r;
@@ -188,7 +193,7 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
         KmOffBf16<ARB> ao;
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
-            ao.init(8 * grp, 8 * grp + 4, (ng * NTW + j) * 16, lane);
+            ao.init(4 * grp, 16 + 4 * grp, (ng * NTW + j) * 16, lane);
 #pragma unroll
             for (int ks = 0; ks < KST; ++ks) afr[j][ks] = ao.read(atile, ks * 32 * ARB);
         }
@@ -243,7 +248,7 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
         }
     }
     KmOffBf16<VRB> vo;
-    vo.init(8 * grp, 8 * grp + 4, pg * 16, lane);
+    vo.init(4 * grp, 16 + 4 * grp, pg * 16, lane);
 
     for (int hh = 0; hh < hpb; ++hh) {
         const int u = hh & 1;
@@ -258,8 +263,8 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
         for (int j = 0; j < NTW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KST; ++ks) {
-            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp);
-            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 8 * grp + 4);
+            const f32x4 w0 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 4 * grp);
+            const f32x4 w1 = *reinterpret_cast<const f32x4*>(wv + ks * 32 + 16 + 4 * grp);
             const bf16x8 vr = vo.read(&vbuf[u][0], ks * 32 * VRB);
             float v[8];
 #pragma unroll
@@ -526,24 +531,24 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
                     const bf16x8 a1 = frag_rowmajor<bf16, XRB>(dyt, s, 32 + 8 * grp);
                     g2[uu] = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, a0, xf0), a1, xf1);
                 }
-                const int sb = 32 * K + 8 * grp;
+                const int s0 = 32 * K + 4 * grp, s1 = s0 + 16;  // tokens of elements 0..3, 4..7
                 if (K > (T >> 1)) {
                     const float at = fast_exp2(rcs[32 * K] - cst) * dtt;
                     // (off the diagonal block every s of the block follows t)
-                    const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + sb);
-                    const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + sb + 4);
+                    const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + s0);
+                    const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + s1);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         mb[k][i] += g2[0][i] * (b0[i] * at);
                         mb[k][4 + i] += g2[1][i] * (b1[i] * at);
                     }
                 } else {
-                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(rcs + sb);
-                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + sb + 4);
+                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(rcs + s0);
+                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + s1);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        if (sb + i >= tq && sb + i < len) mb[k][i] += g2[0][i] * (fast_exp2(c0[i] - cst) * dtt);
-                        if (sb + 4 + i >= tq && sb + 4 + i < len) mb[k][4 + i] += g2[1][i] * (fast_exp2(c1[i] - cst) * dtt);
+                        if (s0 + i >= tq && s0 + i < len) mb[k][i] += g2[0][i] * (fast_exp2(c0[i] - cst) * dtt);
+                        if (s1 + i >= tq && s1 + i < len) mb[k][4 + i] += g2[1][i] * (fast_exp2(c1[i] - cst) * dtt);
                     }
                 }
             }
@@ -571,7 +576,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
         if (k < nk) {
             const int K = kfirst + 2 * k;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) mo[(int64_t)(32 * K + 8 * grp + e) * S + t] = (bf16)mb[k][e];
+            for (int e = 0; e < 8; ++e) mo[(int64_t)(32 * K + korder(e, grp)) * S + t] = (bf16)mb[k][e];
         }
     }
 }
@@ -719,7 +724,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
     store_rec(0);
     KmOffSpread<XRB> ko[4];  // transposing reads of dy^T (k = s) and W^T (k = n), p tile pt
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) ko[pt].init(8 * grp, 8 * grp + 4, spread_base(pt), lane);
+    for (int pt = 0; pt < 4; ++pt) ko[pt].init(4 * grp, 16 + 4 * grp, spread_base(pt), lane);
 
     // x_t fragments of the wave's tiles (each reloaded for the next head once
     // its tile's pairs are done)
@@ -773,10 +778,14 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
             const bool valid = t < len;
             const int tc = valid ? t : len - 1;
             const float cst = rcs[t], dtt = rdt[t];
-            bf16x8 bq[KS];  // B_t, for the W_c term after the pairs
-            const bf16* brow = Bm + ((b * L + t0 + tc) * G + g) * N + 8 * grp;
+            bf16x8 bq[KS];  // B_t (k order korder), for the W_c term after the pairs
+            const bf16* brow = Bm + ((b * L + t0 + tc) * G + g) * N + 4 * grp;
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) bq[ks] = load_frag(brow + 32 * ks);
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x4 lo = *reinterpret_cast<const bf16x4*>(brow + 32 * ks);
+                const bf16x4 hi = *reinterpret_cast<const bf16x4*>(brow + 32 * ks + 16);
+                bq[ks] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            }
             // x~_t = bf16(dt_t x_t): the Gram B operand, so that r_s (row sums of
             // D = M1 (dy_s . x~_t)) and c_t = x~_t . (sum_s M1[s,t] dy_s) hold the
             // same products
@@ -794,23 +803,23 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                     g2[uu] = mma16(mma16(f32x4{0.f, 0.f, 0.f, 0.f}, a0, xt0), a1, xt1);
                 }
                 float f[8];
-                const int sb = 32 * K + 8 * grp;
+                const int s0 = 32 * K + 4 * grp, s1 = s0 + 16;  // tokens of elements 0..3, 4..7
                 if (K > (T >> 1)) {
                     const float at = fast_exp2(rcs[32 * K] - cst);
-                    const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + sb);
-                    const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + sb + 4);
+                    const f32x4 b0 = *reinterpret_cast<const f32x4*>(rbs + s0);
+                    const f32x4 b1 = *reinterpret_cast<const f32x4*>(rbs + s1);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         f[i] = b0[i] * at;
                         f[4 + i] = b1[i] * at;
                     }
                 } else {
-                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(rcs + sb);
-                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + sb + 4);
+                    const f32x4 c0 = *reinterpret_cast<const f32x4*>(rcs + s0);
+                    const f32x4 c1 = *reinterpret_cast<const f32x4*>(rcs + s1);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        f[i] = (sb + i >= t && sb + i < len) ? fast_exp2(c0[i] - cst) : 0.f;
-                        f[4 + i] = (sb + 4 + i >= t && sb + 4 + i < len) ? fast_exp2(c1[i] - cst) : 0.f;
+                        f[i] = (s0 + i >= t && s0 + i < len) ? fast_exp2(c0[i] - cst) : 0.f;
+                        f[4 + i] = (s1 + i >= t && s1 + i < len) ? fast_exp2(c1[i] - cst) : 0.f;
                     }
                 }
                 bf16x8 m1;
@@ -830,7 +839,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) acc[pt] = mma16(acc[pt], ko[pt].read(dyt, 32 * K * XRB), m1);
                 const float rs = lane_sums<8, 16>(rv, lane);
-                if ((lane & 1) == 0) rpart[wave][sb + ((lane & 15) >> 1)] += rs;
+                if ((lane & 1) == 0) rpart[wave][32 * K + korder((lane & 15) >> 1, grp)] += rs;
                 // keep the scheduler from interleaving pairs (register pressure)
                 __builtin_amdgcn_sched_barrier(0);
             };
@@ -980,17 +989,34 @@ __global__ __launch_bounds__(512) void k_sbwd_bc(const bf16* __restrict__ mbar, 
         const int T = id / NNH, nt = nhalf * NNH + id % NNH;
         const int tk = 16 * T + col;  // token of this lane's column
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        // every A fragment of the tile is requested before the first product
+        bf16x8 av[NKB];
         if (isB) {
-            // dB^T[n][t] = sum_{s >= t} C^T[n][s] Mbar[s][t]
-            mo.init(8 * grp, 8 * grp + 4, 16 * T, lane);
-            const bf16* arow = ct + (int64_t)(16 * nt + col) * S + 8 * grp;
-            for (int K = T >> 1; K < NKB; ++K)
-                acc = mma16(acc, load_frag(arow + 32 * K), mo.read(mt, 32 * K * RB));
+            // dB^T[n][t] = sum_{s >= t} C^T[n][s] Mbar[s][t], k order korder
+            // (conflict-free transposing reads of Mbar)
+            mo.init(4 * grp, 16 + 4 * grp, 16 * T, lane);
+            const bf16* arow = ct + (int64_t)(16 * nt + col) * S + 4 * grp;
+#pragma unroll
+            for (int K = 0; K < NKB; ++K) {
+                if (K >= (T >> 1)) {
+                    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(arow + 32 * K);
+                    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(arow + 32 * K + 16);
+                    av[K] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                }
+            }
+#pragma unroll
+            for (int K = 0; K < NKB; ++K)
+                if (K >= (T >> 1)) acc = mma16(acc, av[K], mo.read(mt, 32 * K * RB));
         } else {
             // dC^T[n][s] = sum_{t <= s} B^T[n][t] Mbar[s][t]
             const bf16* arow = bt + (int64_t)(16 * nt + col) * S + 8 * grp;
-            for (int K = 0; K <= (T >> 1); ++K)
-                acc = mma16(acc, load_frag(arow + 32 * K), frag_rowmajor<bf16, RB>(mt, tk, 32 * K + 8 * grp));
+#pragma unroll
+            for (int K = 0; K < NKB; ++K)
+                if (K <= (T >> 1)) av[K] = load_frag(arow + 32 * K);
+#pragma unroll
+            for (int K = 0; K < NKB; ++K)
+                if (K <= (T >> 1))
+                    acc = mma16(acc, av[K], frag_rowmajor<bf16, RB>(mt, tk, 32 * K + 8 * grp));
         }
         if (tk < len) {
             float* dst = (isB ? dB : dC) + ((b * L + t0 + tk) * G + g) * N + 16 * nt + 4 * grp;

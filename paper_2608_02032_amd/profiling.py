@@ -190,12 +190,51 @@ def mfma_for(kernel: str):
     return None if k is None or k["mfma_busy"] is None else round(k["mfma_busy"], 4)
 
 
+def instmix_summary(pass1_csv: str, pass2_csv: str, out_md: str, commands: str) -> str:
+    """Per kernel and wave: instructions issued by class (SQ_INSTS_VALU,
+    SQ_INSTS_MFMA, SQ_INSTS_SALU, SQ_INSTS_LDS), the share
+    of wave lifetime spent in s_waitcnt (SQ_WAIT_ANY) and waiting to issue
+    (SQ_WAIT_INST_ANY), the share of LDS-active cycles lost to bank conflicts,
+    and the mean wave lifetime (SQ_WAVE_CYCLES counts every 4 cycles)."""
+    vals = defaultdict(lambda: defaultdict(list))
+    for path in (pass1_csv, pass2_csv):
+        for r in csv.DictReader(open(path)):
+            k = kernel_short(r["Kernel_Name"])
+            if k:
+                vals[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    mean = lambda v: sum(v) / len(v) if v else float("nan")
+    lines = ["# Instruction mix and stalls per wave (rocprofv3 --pmc, SQ counters)", "", "Commands:", "",
+             "```", commands, "```", "",
+             "Per wave: issued instructions by class (SQ_INSTS_VALU, _MFMA, _SALU, _LDS); wait = s_waitcnt share of "
+             "the wave lifetime (SQ_WAIT_ANY / SQ_WAVE_CYCLES), issue-wait = waiting to issue "
+             "(SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES); bank = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE; "
+             "lifetime = 4 SQ_WAVE_CYCLES / SQ_WAVES.", "",
+             "| kernel | waves | VALU | MFMA | SALU | LDS | wait | issue-wait | LDS bank | lifetime (cycles) |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for k in sorted(vals):
+        c = {n: mean(v) for n, v in vals[k].items()}
+        w = c.get("SQ_WAVES", float("nan"))
+        wc = c.get("SQ_WAVE_CYCLES", float("nan"))
+        per = lambda n: c.get(n, float("nan")) / w
+        lines.append("| %s | %d | %.0f | %.0f | %.0f | %.0f | %.1f %% | %.1f %% | %.1f %% | %.0f |" % (
+            k, w, per("SQ_INSTS_VALU"), per("SQ_INSTS_MFMA"), per("SQ_INSTS_SALU"), per("SQ_INSTS_LDS"),
+            100 * c.get("SQ_WAIT_ANY", float("nan")) / wc, 100 * c.get("SQ_WAIT_INST_ANY", float("nan")) / wc,
+            100 * c.get("SQ_LDS_BANK_CONFLICT", float("nan")) / max(c.get("SQ_LDS_IDX_ACTIVE", 1.0), 1.0),
+            4 * wc / w))
+    text = "\n".join(lines) + "\n"
+    with open(out_md, "w") as fh:
+        fh.write(text)
+    return text
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "trace":
         print(trace_summary(sys.argv[2], sys.argv[3], sys.argv[4]))
     elif sys.argv[1] == "traffic":
         print(json.dumps(traffic_summary(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5],
                                          sys.argv[6], sys.argv[7]), indent=1))
+    elif sys.argv[1] == "instmix":
+        print(instmix_summary(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5]))
     elif sys.argv[1] == "mfma":
         print(json.dumps(mfma_summary(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5],
                                       sys.argv[6]), indent=1))
