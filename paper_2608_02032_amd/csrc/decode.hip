@@ -254,13 +254,10 @@ __global__ __launch_bounds__(kThreads) void k_decode_partial(
                     v[i] += cb[k] * xv[i];
                 }
             }
-            ss += shfl_xor(ss, 1);
-            kv += shfl_xor(kv, 1);
-            ss += shfl_xor(ss, 2);
-            kv += shfl_xor(kv, 2);
-            ss += shfl_xor(ss, 4);
-            kv += shfl_xor(kv, 4);
-            const float r = normalize ? 1.0f / sqrtf(ss * (1.0f / kP) + eps) : 1.0f;
+            // sums over the row's 8 lanes (DPP), then the row's inverse RMS
+            ss = dpp_group_sum<8>(ss);
+            kv = dpp_group_sum<8>(kv);
+            const float r = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
             lsum += qb[k] * r * kv;
         }
         lsum += shfl_xor(lsum, 8);
