@@ -232,12 +232,13 @@ __global__ __launch_bounds__(kThreads) void k_decode_partial(
                 }
                 if (k & 1) {
                     // value side: pair rows k-1 and k so one dot2 covers both
+                    // (v_perm: the low halves of rows k-1, k, then the high halves)
                     const uint32_t u[4] = {xr[k - 1].v.x, xr[k - 1].v.y, xr[k - 1].v.z,
                                            xr[k - 1].v.w};
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const uint32_t lo = (u[i] & 0xffffu) | (w[i] << 16);
-                        const uint32_t hi = (u[i] >> 16) | (w[i] & 0xffff0000u);
+                        const uint32_t lo = __builtin_amdgcn_perm(w[i], u[i], 0x05040100u);
+                        const uint32_t hi = __builtin_amdgcn_perm(w[i], u[i], 0x07060302u);
                         v[2 * i] = dot2(lo, cbp[k >> 1], v[2 * i]);
                         v[2 * i + 1] = dot2(hi, cbp[k >> 1], v[2 * i + 1]);
                     }
@@ -254,12 +255,13 @@ __global__ __launch_bounds__(kThreads) void k_decode_partial(
                     v[i] += cb[k] * xv[i];
                 }
             }
-            // sums over the row's 8 lanes (DPP), then the row's inverse RMS
+            // the row's sum of squares over its 8 lanes (DPP), then its inverse
+            // RMS; the logit partial kv is summed over the lanes once per memory
             ss = dpp_group_sum<8>(ss);
-            kv = dpp_group_sum<8>(kv);
             const float r = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
             lsum += qb[k] * r * kv;
         }
+        lsum = dpp_group_sum<8>(lsum);
         lsum += shfl_xor(lsum, 8);
         lsum += shfl_xor(lsum, 16);
         lsum += shfl_xor(lsum, 32);
