@@ -332,9 +332,16 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
     const int nsteps = hpb * nj;
     Copy copy;
     copy.init(tg, lane);
+    // (head, memory) of the next copy and of the current step, advanced in
+    // order (no division in the stream)
+    int ih = 0, ij = 0;
     auto issue_tiles = [&](int k) {
+        const int hh = ih, j = ij;
+        if (++ij == nj) {
+            ij = 0;
+            ++ih;
+        }
         if (!copier) return;
-        const int hh = k / nj, j = k - hh * nj;
         const int64_t hj = (b * Mp + j) * H + h0 + hh;
         copy.issue(kmem + hj * N * kP, ring[k % NS][0]);
         if constexpr (LO) copy.issue(klo + hj * N * kP, ring[k % NS][NTL - 1]);
@@ -351,8 +358,8 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
     float lse2[RT], dsum[RT], dyacc[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse2[rt] = dsum[rt] = dyacc[rt] = 0.f;
+    int hh = 0, j = 0;
     for (int k = 0; k < nsteps; ++k) {
-        const int hh = k / nj, j = k - hh * nj;
         const int h = h0 + hh;
         const int ahead = nsteps - 1 - k < NS - 2 ? nsteps - 1 - k : NS - 2;
         if (ahead >= 2) {
@@ -460,6 +467,10 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
                     rdy[bt[rt] * H + h] = dyacc[rt] / dsum[rt];
                 }
             }
+        }
+        if (++j == nj) {
+            j = 0;
+            ++hh;
         }
     }
 }
@@ -576,9 +587,16 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     const int nsteps = hpb * nj;
     Copy copy;
     copy.init(tg, lane);
+    // (head, memory) of the next copy and of the current step, advanced in
+    // order (no division in the stream)
+    int ih = 0, ij = 0;
     auto issue_tiles = [&](int k) {
+        const int hh = ih, j = ij;
+        if (++ij == nj) {
+            ij = 0;
+            ++ih;
+        }
         if (!copier) return;
-        const int hh = k / nj, j = k - hh * nj;
         const int64_t hj = (b * Mp + j) * H + h0 + hh;
         copy.issue(kmem + hj * N * kP, ring[k % NS]);
         if (lane < RPW)
@@ -600,8 +618,8 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     float lse2[RT], gate[RT], Dy[RT];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) lse2[rt] = gate[rt] = Dy[rt] = 0.f;
+    int hh = 0, j = 0;
     for (int k = 0; k < nsteps; ++k) {
-        const int hh = k / nj, j = k - hh * nj;
         const int h = h0 + hh;
         // this step's copies (the ones of the later steps in flight may stay)
         const int ahead = nsteps - 1 - k < NS - 2 ? nsteps - 1 - k : NS - 2;
@@ -697,6 +715,10 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt)
                 if (valid[rt]) gpw[((b * H + h) * Mp + j) * Ls + tc[rt]] = gp[rt];
+        }
+        if (++j == nj) {
+            j = 0;
+            ++hh;
         }
     }
 
