@@ -182,6 +182,40 @@ __device__ __forceinline__ float lane_sums(float (&v)[R], int lane) {
     return s;
 }
 
+// lane_sums<8, 16> with DPP moves instead of LDS permutes.  Each step pairs a
+// lane with a partner that differs in the step's mask bit (row rotate by 8,
+// mirror within 8 lanes, then the two quad swaps); the partner keeps the same
+// half of the values at that point, so the keep / give selection by lane bit is
+// the one of rs_step and lane l again ends with the 16-lane sum of value
+// (l % 16) / 2.
+__device__ __forceinline__ float lane_sums8x16_dpp(float (&v)[8], int lane) {
+    {
+        const bool hi = (lane & 8) != 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float keep = hi ? v[j + 4] : v[j];
+            const float give = hi ? v[j] : v[j + 4];
+            v[j] = keep + dpp_mov<0x128>(give);  // row_ror:8 (partner lane ^ 8)
+        }
+    }
+    {
+        const bool hi = (lane & 4) != 0;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const float keep = hi ? v[j + 2] : v[j];
+            const float give = hi ? v[j] : v[j + 2];
+            v[j] = keep + dpp_mov<0x141>(give);  // row_half_mirror (partner lane ^ 7)
+        }
+    }
+    {
+        const bool hi = (lane & 2) != 0;
+        const float keep = hi ? v[1] : v[0];
+        const float give = hi ? v[0] : v[1];
+        v[0] = keep + dpp_mov<0x4E>(give);  // quad_perm [2,3,0,1] (partner lane ^ 2)
+    }
+    return v[0] + dpp_mov<0xB1>(v[0]);  // quad_perm [1,0,3,2] (partner lane ^ 1)
+}
+
 __device__ __forceinline__ float fast_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }

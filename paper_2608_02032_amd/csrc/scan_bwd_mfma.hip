@@ -838,7 +838,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 }
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) acc[pt] = mma16(acc[pt], ko[pt].read(dyt, 32 * K * XRB), m1);
-                const float rs = lane_sums<8, 16>(rv, lane);
+                const float rs = lane_sums8x16_dpp(rv, ln);
                 if ((lane & 1) == 0) rpart[wave][32 * K + korder((lane & 15) >> 1, grp)] += rs;
                 // keep the scheduler from interleaving pairs (register pressure)
                 __builtin_amdgcn_sched_barrier(0);
