@@ -182,6 +182,21 @@ __device__ __forceinline__ float lane_sums(float (&v)[R], int lane) {
     return s;
 }
 
+// Sum over the lanes l, l^16, l^32, l^48 (the four 16-lane rows of the wave),
+// in every lane, without an LDS round trip: v_permlane32_swap exchanges lanes
+// 32..63 of its first operand with lanes 0..31 of its second, so with both
+// operands a copy of x their sum is x[l] + x[l^32]; v_permlane16_swap exchanges
+// the odd rows of its first operand with the even rows of its second, and the
+// same step adds the lane l^16.  Issued from assembly (the builtins return the
+// second operand unchanged in this compiler); call from uniform control flow.
+__device__ __forceinline__ float row4_sum(float x) {
+    float a = x, b = x;
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+    float c = a + b, d = c;
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(c), "+v"(d));
+    return c + d;
+}
+
 // lane_sums<8, 16> with DPP moves instead of LDS permutes.  Each step pairs a
 // lane with a partner that differs in the step's mask bit (row rotate by 8,
 // mirror within 8 lanes, then the two quad swaps); the partner keeps the same

@@ -261,10 +261,8 @@ __global__ __launch_bounds__(kThreads) void k_decode_partial(
             const float r = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
             lsum += qb[k] * r * kv;
         }
-        lsum = dpp_group_sum<8>(lsum);
-        lsum += shfl_xor(lsum, 8);
-        lsum += shfl_xor(lsum, 16);
-        lsum += shfl_xor(lsum, 32);
+        lsum = dpp_group_sum<16>(lsum);
+        lsum = row4_sum(lsum);
         const float mn = fmaxf(mx, lsum);
         const float al = fast_exp2(mx - mn), pw = fast_exp2(lsum - mn);
         den = den * al + pw;

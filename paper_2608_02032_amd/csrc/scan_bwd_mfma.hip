@@ -514,9 +514,7 @@ __global__ __launch_bounds__(512) void k_sbwd_group(
                 accC[j][i] += sy * pc[i];
             }
         }
-        wsum *= sy;
-        wsum += __shfl_xor(wsum, 16, 64);
-        wsum += __shfl_xor(wsum, 32, 64);
+        wsum = row4_sum(wsum * sy);
         if (grp == 0) wpart[u][nh][slot * 16 + col] = wsum;
         // Mbar pairs (tile T, s block K): A = dy rows in gram_row order, B = x_t
 #pragma unroll
@@ -859,8 +857,7 @@ __global__ __launch_bounds__(64 * quad_waves<S>()) void k_sbwd_quad(
                 for (int i = 0; i < 4; ++i)
                     d += (float)f0[i] * acc[0][i] + (float)f0[4 + i] * acc[1][i] + (float)f1[i] * acc[2][i] +
                          (float)f1[4 + i] * acc[3][i];
-                d += __shfl_xor(d, 16, 64);
-                return d + __shfl_xor(d, 32, 64);
+                return row4_sum(d);
             };
             const float cq = xdot(xt0, xt1);  // c_t = dt_t c~_t
             // the W_c term: dx^T += W^T (e^{cs_e - cs_t} B_t)

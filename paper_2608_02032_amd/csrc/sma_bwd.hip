@@ -441,10 +441,8 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
         }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
-            l2[rt] += shfl_xor(l2[rt], 16);
-            l2[rt] += shfl_xor(l2[rt], 32);
-            dw[rt] += shfl_xor(dw[rt], 16);
-            dw[rt] += shfl_xor(dw[rt], 32);
+            l2[rt] = row4_sum(l2[rt]);
+            dw[rt] = row4_sum(dw[rt]);
             if (lane < 16) {
                 xch[0][nh][tg][16 * rt + col] = l2[rt];
                 xch[1][nh][tg][16 * rt + col] = dw[rt];
