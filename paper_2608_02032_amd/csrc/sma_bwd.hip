@@ -60,11 +60,9 @@ constexpr int kTokBlock = 16 * kTokWaves;  // tokens per k_bwd_tokens workgroup
 constexpr int kMemJ = 4;                   // memories per k_bwd_mem workgroup
 constexpr int kHeadsPerBlock = 8;
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-    return v;
-}
+// Sum over the 64 lanes in every lane (DPP within rows, then row swaps); call
+// from wave-uniform control flow.
+__device__ __forceinline__ float wave_sum(float v) { return row4_sum(dpp_group_sum<16>(v)); }
 
 // An empty use of every register of a fragment, so the compiler waits for its
 // loads at this point (operands of at most 128 bits each).
