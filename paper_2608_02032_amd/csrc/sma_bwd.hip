@@ -743,7 +743,11 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
 // tokens per step are copied into LDS by DMA one step ahead, and the
 // per-(memory, token) factors g p_j and ln2 dl_j (zero where memory j is not
 // attended) scale the dy and Ebar fragments in registers.  Wave w owns the
-// output columns p = 16 (w % 4) .. + 15 and half of the n tiles.  The token
+// output columns p = 16 (w % 4) .. + 15; for bf16 it takes two of the four
+// memories (2 (w / 4), + 1) over every n tile, so each scaled fragment feeds
+// N/16 MFMAs of each product and no two waves scale the same fragment; for
+// fp32 (operands twice as wide) it takes every memory over half the n tiles.
+// The token
 // tiles stream through a 3-stage LDS ring, two steps ahead: waves 0-3 issue
 // the DMA copies (and wait for their own with exact counts), waves 4-7 load
 // the factors of the step two ahead and write them to LDS at the end of the
@@ -780,9 +784,10 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     constexpr int RBN = N * ES, RBP = kP * ES;
     constexpr int CT = TB * RBN, DT = TB * RBP;
     constexpr int STAGE = 2 * CT + 2 * DT;
-    constexpr int NT = N / 16;
-    constexpr int NH = NT / 2;  // n tiles per wave
-    static_assert(NH >= 1, "at least two n tiles");
+    constexpr bool MSPLIT = ES == 2;           // waves split the memories (else the n tiles)
+    constexpr int NT = MSPLIT ? N / 16 : N / 32;  // n tiles per wave
+    constexpr int JW = MSPLIT ? J / 2 : J;        // memories per wave
+    static_assert(NT >= 1 && J % 2 == 0, "whole n tiles, memories in two halves");
     constexpr int NS = 3;
     // DMA copies per copying wave per step (every tile is a multiple of 256 pieces)
     constexpr int CPW = (2 * TB * RBN / 16 + 2 * TB * RBP / 16) / 256;
@@ -792,7 +797,9 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    const int pt = wave & 3, nh = wave >> 2;
+    const int pt = wave & 3;                       // p tile of the wave
+    const int jh = MSPLIT ? (wave >> 2) * JW : 0;  // its first memory
+    const int nt0 = MSPLIT ? 0 : (wave >> 2) * NT; // its first n tile
     const int64_t jb = (int64_t)blockIdx.x / BH;
     const int64_t bh = (int64_t)blockIdx.x - jb * BH;
     const int64_t b = bh / H;
@@ -858,11 +865,11 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
         }
     };
 
-    f32x4 m1[J][NH], m2[J][NH];
+    f32x4 m1[JW][NT], m2[JW][NT];
 #pragma unroll
-    for (int jl = 0; jl < J; ++jl)
+    for (int jw = 0; jw < JW; ++jw)
 #pragma unroll
-        for (int k = 0; k < NH; ++k) m1[jl][k] = m2[jl][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < NT; ++k) m1[jw][k] = m2[jw][k] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     issue(0);
     issue(1);
@@ -889,24 +896,25 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
             const int r0 = 32 * ks + 4 * grp, r1 = r0 + 16;
             const Frag<T> bd = frag_km<T, RBP>(dyt, r0, r1, 16 * pt, lane);
             const Frag<T> be = frag_km<T, RBP>(et, r0, r1, 16 * pt, lane);
-            Frag<T> ac[NH], aq[NH];
+            Frag<T> bdj[JW], bej[JW];
 #pragma unroll
-            for (int k = 0; k < NH; ++k) {
-                ac[k] = frag_km<T, RBN>(cs, r0, r1, 16 * (nh * NH + k), lane);
-                aq[k] = frag_km<T, RBN>(qs, r0, r1, 16 * (nh * NH + k), lane);
-            }
-#pragma unroll
-            for (int jl = 0; jl < J; ++jl) {
+            for (int jw = 0; jw < JW; ++jw) {
+                const int jl = jh + jw;
                 const f32x4 g0 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][0][r0]);
                 const f32x4 g1 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][0][r1]);
                 const f32x4 d0 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][1][r0]);
                 const f32x4 d1 = *reinterpret_cast<const f32x4*>(&sc[st % NS][jl][1][r1]);
-                const Frag<T> bdj = scale_frag<T>(bd, g0, g1);
-                const Frag<T> bej = scale_frag<T>(be, d0, d1);
+                bdj[jw] = scale_frag<T>(bd, g0, g1);
+                bej[jw] = scale_frag<T>(be, d0, d1);
+            }
 #pragma unroll
-                for (int k = 0; k < NH; ++k) {
-                    m1[jl][k] = mma16(m1[jl][k], ac[k], bdj);
-                    m2[jl][k] = mma16(m2[jl][k], aq[k], bej);
+            for (int k = 0; k < NT; ++k) {
+                const Frag<T> ac = frag_km<T, RBN>(cs, r0, r1, 16 * (nt0 + k), lane);
+                const Frag<T> aq = frag_km<T, RBN>(qs, r0, r1, 16 * (nt0 + k), lane);
+#pragma unroll
+                for (int jw = 0; jw < JW; ++jw) {
+                    m1[jw][k] = mma16(m1[jw][k], ac, bdj[jw]);
+                    m2[jw][k] = mma16(m2[jw][k], aq, bej[jw]);
                 }
             }
         }
@@ -919,18 +927,19 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     // the four column waves through LDS (the stage buffers are free now)
     float* red = reinterpret_cast<float*>(&buf[0][0]);  // [J][2][4][N]
 #pragma unroll
-    for (int jl = 0; jl < J; ++jl) {
+    for (int jw = 0; jw < JW; ++jw) {
+        const int jl = jh + jw;
         const int64_t j = j0 + jl;
         if (j >= Mp) continue;
         const T* hsrc = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
 #pragma unroll
-        for (int k = 0; k < NH; ++k)
+        for (int k = 0; k < NT; ++k)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int n = 16 * (nh * NH + k) + 4 * grp + i;
+                const int n = 16 * (nt0 + k) + 4 * grp + i;
                 const float hv = to_f(hsrc[n * kP + p]);
                 const float s2 = dpp_group_sum<16>(hv * hv);
-                const float d2 = dpp_group_sum<16>(hv * m2[jl][k][i]);
+                const float d2 = dpp_group_sum<16>(hv * m2[jw][k][i]);
                 if (col == 0) {
                     red[((jl * 2 + 0) * 4 + pt) * N + n] = s2;
                     red[((jl * 2 + 1) * 4 + pt) * N + n] = d2;
@@ -939,19 +948,20 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     }
     __syncthreads();
 #pragma unroll
-    for (int jl = 0; jl < J; ++jl) {
+    for (int jw = 0; jw < JW; ++jw) {
+        const int jl = jh + jw;
         const int64_t j = j0 + jl;
         if (j >= Mcap) break;
         float* out = out_of(jl);
         const T* hsrc = mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP;
 #pragma unroll
-        for (int k = 0; k < NH; ++k)
+        for (int k = 0; k < NT; ++k)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int n = 16 * (nh * NH + k) + 4 * grp + i;
+                const int n = 16 * (nt0 + k) + 4 * grp + i;
                 float o = 0.f;
                 if (j < Mp) {
-                    o = m1[jl][k][i];
+                    o = m1[jw][k][i];
                     if (normalize) {
                         const float* r0 = red + (jl * 2 + 0) * 4 * N + n;
                         const float* r1 = red + (jl * 2 + 1) * 4 * N + n;
@@ -959,9 +969,9 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
                         const float dr = r1[0] + r1[N] + r1[2 * N] + r1[3 * N];
                         const float r = __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps);
                         const float hv = to_f(hsrc[n * kP + p]);
-                        o += r * m2[jl][k][i] - (r * r * r * (1.0f / kP)) * dr * hv;
+                        o += r * m2[jw][k][i] - (r * r * r * (1.0f / kP)) * dr * hv;
                     } else {
-                        o += m2[jl][k][i];
+                        o += m2[jw][k][i];
                     }
                 }
                 out[n * kP + p] = o;
