@@ -307,8 +307,24 @@ template <int RB>
 struct SwzTile {
     static constexpr int CPR = RB / 16;                  // chunks per row
     static constexpr int MASK = (CPR < 8 ? CPR : 8) - 1;
+    __device__ static __forceinline__ int key(int r) { return r & MASK; }
     __device__ static __forceinline__ int off(int r, int byte_in_row) {
-        return r * RB + ((((byte_in_row >> 4) ^ (r & MASK)) << 4) | (byte_in_row & 15));
+        return r * RB + ((((byte_in_row >> 4) ^ key(r)) << 4) | (byte_in_row & 15));
+    }
+};
+
+// The same with chunk c of row r at chunk c ^ 2 (r & 7), for rows of at least
+// 256 bytes: a k-major fragment read takes 32 bytes (an even-aligned chunk
+// pair) from each of eight consecutive rows, and with this key the eight rows
+// put their pairs on sixteen distinct chunk slots of a 256-byte bank window
+// (with c ^ (r & 7) rows r and r ^ 1 share a pair of slots).
+template <int RB>
+struct SwzTilePair {
+    static constexpr int CPR = RB / 16;
+    static_assert(CPR >= 16, "rows of at least 256 bytes");
+    __device__ static __forceinline__ int key(int r) { return 2 * (r & 7); }
+    __device__ static __forceinline__ int off(int r, int byte_in_row) {
+        return r * RB + ((((byte_in_row >> 4) ^ key(r)) << 4) | (byte_in_row & 15));
     }
 };
 
@@ -317,16 +333,15 @@ struct SwzTile {
 // (never out of bounds); callers mask their contribution.  rows_valid >= 1.
 // Wave w issues copies q0 = 64 w, 64 (w + nwaves), ... of the rows * RB / 1024
 // one-KiB pieces.  UNTRACKED selects lds_dma16_untracked.
-template <int RB, bool UNTRACKED = false>
+template <int RB, bool UNTRACKED = false, class Tl = SwzTile<RB>>
 __device__ __forceinline__ void dma_tile(char* lds, const char* g, int64_t gstride, int rows,
                                          int rows_valid, int wave, int nwaves, int lane) {
-    using Tl = SwzTile<RB>;
     const int total = rows * Tl::CPR;
     for (int q0 = wave * 64; q0 < total; q0 += nwaves * 64) {
         const int q = q0 + lane;
         if (q < total) {
             const int r = q / Tl::CPR, cs = q % Tl::CPR;
-            const int c = cs ^ (r & Tl::MASK);
+            const int c = cs ^ Tl::key(r);
             const int rr = r < rows_valid ? r : rows_valid - 1;
             if constexpr (UNTRACKED) {
                 lds_dma16_untracked(g + rr * gstride + c * 16, lds + q0 * 16);
@@ -360,16 +375,15 @@ __device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
     return ((uint64_t)hi << 32) | (uint64_t)lo;
 }
 
-// Copies of one swizzled LDS tile (the SwzTile<RB> layout, ROWS rows of RB
-// bytes; rows >= rows_valid re-read the last valid row) issued by NW waves,
+// Copies of one swizzled LDS tile (the Tl layout, SwzTile<RB> by default, ROWS
+// rows of RB bytes; rows >= rows_valid re-read the last valid row) issued by NW waves,
 // with the per-lane global byte offsets (row * gstride + chunk * 16, 32-bit)
 // fixed at set-up, so that issuing a copy costs no vector address work.  Wave
 // w copies the 1 KiB pieces w, w + NW, ...; lane l of piece k lands at byte
 // 1024 k + 16 l of the tile.
-template <int RB, int ROWS, int NW>
+template <int RB, int ROWS, int NW, class Tl = SwzTile<RB>>
 struct TilePlan {
     static constexpr int CPR = RB / 16;
-    static constexpr int MASK = (CPR < 8 ? CPR : 8) - 1;
     static_assert(ROWS * CPR % 64 == 0, "the tile is whole 1 KiB pieces");
     static constexpr int PIECES = ROWS * CPR / 64;
     static constexpr int KPW = (PIECES + NW - 1) / NW;  // pieces per wave (at most)
@@ -378,7 +392,7 @@ struct TilePlan {
 #pragma unroll
         for (int k = 0; k < KPW; ++k) {
             const int q = (wave + k * NW) * 64 + lane;
-            const int r = q / CPR, ch = (q % CPR) ^ (r & MASK);
+            const int r = q / CPR, ch = (q % CPR) ^ Tl::key(r);
             const int rr = r < rows_valid ? r : rows_valid - 1;
             goff[k] = (uint32_t)rr * gstride + (uint32_t)(ch * 16);
             asm volatile("" : "+v"(goff[k]));
@@ -431,10 +445,9 @@ struct LinearPlan {
 // row r0 + j/4, columns c0 + 4 (j%4); lane i then holds column c0 + i of rows
 // r0..r0+3); fp32 falls back to eight scalar reads.
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-template <int RB>
+template <int RB, class Tl = SwzTile<RB>>
 __device__ __forceinline__ bf16x8 frag_kmajor_bf16(const char* tile, int krow0, int krow1,
                                                    int cbase, int lane) {
-    using Tl = SwzTile<RB>;
     const int j = lane & 15;
     const int col_b = (cbase + 4 * (j & 3)) * 2;
     const char* a0 = tile + Tl::off(krow0 + (j >> 2), col_b);
@@ -447,10 +460,9 @@ __device__ __forceinline__ bf16x8 frag_kmajor_bf16(const char* tile, int krow0, 
     const bf16x4 b1 = __builtin_bit_cast(bf16x4, v1);
     return bf16x8{b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
 }
-template <int RB>
+template <int RB, class Tl = SwzTile<RB>>
 __device__ __forceinline__ f32x8 frag_kmajor_f32(const char* tile, int krow0, int krow1,
                                                  int cbase, int lane) {
-    using Tl = SwzTile<RB>;
     const int col_b = (cbase + (lane & 15)) * 4;
     f32x8 r;
 #pragma unroll
@@ -460,13 +472,13 @@ __device__ __forceinline__ f32x8 frag_kmajor_f32(const char* tile, int krow0, in
     }
     return r;
 }
-template <typename T, int RB>
+template <typename T, int RB, class Tl = SwzTile<RB>>
 __device__ __forceinline__ Frag<T> frag_km(const char* tile, int krow0, int krow1, int cbase,
                                            int lane) {
     if constexpr (sizeof(T) == 2) {
-        return frag_kmajor_bf16<RB>(tile, krow0, krow1, cbase, lane);
+        return frag_kmajor_bf16<RB, Tl>(tile, krow0, krow1, cbase, lane);
     } else {
-        return frag_kmajor_f32<RB>(tile, krow0, krow1, cbase, lane);
+        return frag_kmajor_f32<RB, Tl>(tile, krow0, krow1, cbase, lane);
     }
 }
 

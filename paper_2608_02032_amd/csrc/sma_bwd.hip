@@ -47,6 +47,8 @@
 //                       epilogue above.  Heavy memories (small j) go first.
 //   k_bwd_finish        one wave per (b, t, group): sums the partials over the
 //                       group's head blocks, RMSNorm backward, dz.
+#include <type_traits>
+
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
 
@@ -783,6 +785,8 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     constexpr int TB = mem_tb<T>();
     constexpr int RBN = N * ES, RBP = kP * ES;
     constexpr int CT = TB * RBN, DT = TB * RBP;
+    // C and Qbar' tiles: pair-spread swizzle where their rows span 256 bytes
+    using SwN = std::conditional_t<(ES == 2 && RBN >= 256), SwzTilePair<RBN>, SwzTile<RBN>>;
     constexpr int STAGE = 2 * CT + 2 * DT;
     constexpr bool MSPLIT = ES == 2;           // waves split the memories (else the n tiles)
     constexpr int NT = MSPLIT ? N / 16 : N / 32;  // n tiles per wave
@@ -823,15 +827,33 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     const int64_t grow = (b * L) * G + g;  // row of token 0 in the [B][L][G] layout
 
     const bool copier = wave < 4;
+    // copies of whole steps from per-lane offsets fixed here (C and Qbar' share
+    // a row stride and layout); a ragged last step takes the general path
+    TilePlan<RBN, TB, 4, SwN> pnc;
+    TilePlan<RBP, TB, 4> pdy, pet;
+    if (copier) {
+        pnc.init(wave, lane, (uint32_t)(G * RBN), TB);
+        pdy.init(wave, lane, (uint32_t)(H * RBP), TB);
+        pet.init(wave, lane, (uint32_t)(G * RBP), TB);
+    }
+    const uint32_t buf_lds = lds_addr(&buf[0][0]);
     auto issue = [&](int st) {
         if (!copier || st >= nstep) return;
         const int64_t t0 = tbeg + (int64_t)st * TB;
         const int rv = (int)(L - t0 < TB ? L - t0 : TB);
+        if (rv == TB) {
+            const uint32_t dl = buf_lds + (uint32_t)((st % NS) * STAGE);
+            pnc.issue(Cm + (grow + t0 * G) * N, dl, wave);
+            pnc.issue(qb + (grow + t0 * G) * N, dl + CT, wave);
+            pdy.issue(dy + ((b * L + t0) * H + h) * kP, dl + 2 * CT, wave);
+            pet.issue(ebt + (grow + t0 * G) * kP, dl + 2 * CT + DT, wave);
+            return;
+        }
         char* d = buf[st % NS];
-        dma_tile<RBN, true>(d, reinterpret_cast<const char*>(Cm + (grow + t0 * G) * N),
-                            (int64_t)G * RBN, TB, rv, wave, 4, lane);
-        dma_tile<RBN, true>(d + CT, reinterpret_cast<const char*>(qb + (grow + t0 * G) * N),
-                            (int64_t)G * RBN, TB, rv, wave, 4, lane);
+        dma_tile<RBN, true, SwN>(d, reinterpret_cast<const char*>(Cm + (grow + t0 * G) * N),
+                                 (int64_t)G * RBN, TB, rv, wave, 4, lane);
+        dma_tile<RBN, true, SwN>(d + CT, reinterpret_cast<const char*>(qb + (grow + t0 * G) * N),
+                                 (int64_t)G * RBN, TB, rv, wave, 4, lane);
         dma_tile<RBP, true>(d + 2 * CT,
                             reinterpret_cast<const char*>(dy + ((b * L + t0) * H + h) * kP),
                             (int64_t)H * RBP, TB, rv, wave, 4, lane);
@@ -842,26 +864,28 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     // factors of step st: g p_j[t] and ln2 dl_j[t] = ln2 g p_j (dwy_j - Dy),
     // loaded and stored by waves 4-7 (thread ft = tid - 256 of J * TB = 256)
     static_assert(J * TB <= 256, "one factor per thread of waves 4-7");
+    // The loaded values stay raw until the store at the end of the step, so the
+    // wait for the loads falls behind the step's MFMA work.
     const int ft = tid - 256;
-    float fg = 0.f, fd = 0.f;
+    float fgp = 0.f, fgw = 0.f, fry = 0.f;
     auto load_factors = [&](int st) {
-        fg = fd = 0.f;
+        fgp = fgw = fry = 0.f;
         if (ft >= 0 && ft < J * TB && st < nstep) {
             const int jl = ft / TB, tk = ft % TB;
             const int64_t j = j0 + jl, t = tbeg + (int64_t)st * TB + tk;
             if (j < Mp && t < L && t >= (j + 1) * S) {
                 const int64_t si = ((b * H + h) * Mp + j) * Ls + t;
-                const float gp = gpw[si];
-                fg = gp;
-                fd = kLn2 * gp * (gdw[si] - rdy[(b * L + t) * H + h]);
+                fgp = gpw[si];
+                fgw = gdw[si];
+                fry = rdy[(b * L + t) * H + h];
             }
         }
     };
     auto store_factors = [&](int st) {
         if (ft >= 0 && ft < J * TB && st < nstep) {
             const int jl = ft / TB, tk = ft % TB;
-            sc[st % NS][jl][0][tk] = fg;
-            sc[st % NS][jl][1][tk] = fd;
+            sc[st % NS][jl][0][tk] = fgp;
+            sc[st % NS][jl][1][tk] = kLn2 * fgp * (fgw - fry);
         }
     };
 
@@ -909,8 +933,8 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
             }
 #pragma unroll
             for (int k = 0; k < NT; ++k) {
-                const Frag<T> ac = frag_km<T, RBN>(cs, r0, r1, 16 * (nt0 + k), lane);
-                const Frag<T> aq = frag_km<T, RBN>(qs, r0, r1, 16 * (nt0 + k), lane);
+                const Frag<T> ac = frag_km<T, RBN, SwN>(cs, r0, r1, 16 * (nt0 + k), lane);
+                const Frag<T> aq = frag_km<T, RBN, SwN>(qs, r0, r1, 16 * (nt0 + k), lane);
 #pragma unroll
                 for (int jw = 0; jw < JW; ++jw) {
                     m1[jw][k] = mma16(m1[jw][k], ac, bdj[jw]);
