@@ -70,12 +70,16 @@ template <typename T> struct RowChunk;
 template <> struct RowChunk<bf16> { uint4 v; };
 template <> struct RowChunk<float> { f32x4 a, b; };
 
+// The cache is read once per step: nontemporal loads keep it from displacing
+// anything in the caches (and stream faster than ordinary loads).
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void load_row(const bf16* p, RowChunk<bf16>& r) {
-    r.v = *reinterpret_cast<const uint4*>(p);
+    const u32x4_nt w = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
+    r.v = make_uint4(w.x, w.y, w.z, w.w);
 }
 __device__ __forceinline__ void load_row(const float* p, RowChunk<float>& r) {
-    r.a = *reinterpret_cast<const f32x4*>(p);
-    r.b = *reinterpret_cast<const f32x4*>(p + 4);
+    r.a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    r.b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
 }
 
 // Workspace layout: partials [B][H][nsplit][P+2] (O[P], m, d), then y_ssd
