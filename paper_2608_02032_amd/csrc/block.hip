@@ -163,8 +163,8 @@ __global__ __launch_bounds__(256) void k_gated_rmsnorm(const T* __restrict__ y,
         const int k = lane * 8 + q * 512;
         if (k < group) {
             float yv[8], zv[8];
-            load8(yr + k, yv);
-            load8(zr + k, zv);
+            load8_nt(yr + k, yv);
+            load8_nt(zr + k, zv);
             // the weights of these channels, loaded with the data (vector
             // loads; 8 consecutive floats at a multiple of 8)
             if (w) {
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(256) void k_gated_rmsnorm(const T* __restrict__ y,
             float o[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) o[i] = u[q][i] * inv * wv[q][i];
-            store8(orow + k, o);
+            store8_nt(orow + k, o);
         }
     }
     for (int k = lane * 8 + KEEP * 512; k < group; k += 512) {

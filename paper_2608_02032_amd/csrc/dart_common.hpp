@@ -92,6 +92,39 @@ __device__ __forceinline__ void store8(float* p, const float (&v)[8]) {
     *reinterpret_cast<f32x4*>(p) = a;
     *reinterpret_cast<f32x4*>(p + 4) = b;
 }
+// Streaming variants for data a kernel touches once: nontemporal loads and
+// stores (the cache lines are not kept for reuse).
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void load8_nt(const bf16* p, float (&v)[8]) {
+    const bf16x8 r = __builtin_bit_cast(bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p)));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (float)r[i];
+}
+__device__ __forceinline__ void load8_nt(const float* p, float (&v)[8]) {
+    const f32x4 a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+    const f32x4 b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + 4));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[i] = a[i];
+        v[4 + i] = b[i];
+    }
+}
+__device__ __forceinline__ void store8_nt(bf16* p, const float (&v)[8]) {
+    bf16x8 r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r[i] = (bf16)v[i];
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4_nt, r), reinterpret_cast<u32x4_nt*>(p));
+}
+__device__ __forceinline__ void store8_nt(float* p, const float (&v)[8]) {
+    f32x4 a, b;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        a[i] = v[i];
+        b[i] = v[4 + i];
+    }
+    __builtin_nontemporal_store(a, reinterpret_cast<f32x4*>(p));
+    __builtin_nontemporal_store(b, reinterpret_cast<f32x4*>(p + 4));
+}
 // Raw fragment load (no conversion) from 8 consecutive elements.
 __device__ __forceinline__ bf16x8 load_frag(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 __device__ __forceinline__ f32x8 load_frag(const float* p) {

@@ -72,7 +72,6 @@ template <> struct RowChunk<float> { f32x4 a, b; };
 
 // The cache is read once per step: nontemporal loads keep it from displacing
 // anything in the caches (and stream faster than ordinary loads).
-typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void load_row(const bf16* p, RowChunk<bf16>& r) {
     const u32x4_nt w = __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p));
     r.v = make_uint4(w.x, w.y, w.z, w.w);
