@@ -741,6 +741,9 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out(
 // lane, and each lane stores its outputs as 8-byte pieces straight from
 // registers.  The copies use per-lane offsets fixed at set-up.
 // ---------------------------------------------------------------------------
+// y stores per row tile and head in k_chunk_out_heads (16 bytes per lane)
+constexpr int kYStores = 2;
+
 template <int N, int S>
 __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
     const bf16* __restrict__ x, const bf16* __restrict__ Bm, const bf16* __restrict__ Cm,
@@ -953,17 +956,39 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
                 for (int pt = 0; pt < 4; ++pt) yacc[q][pt] = mma16(yacc[q][pt], xf[cur][pt], fm);
             }
         }
-        // yacc[q][pt][i] = y[t = 16 r_q + col][p = 16 pt + 4 grp + i]: 8-byte stores
+        // yacc[q][pt][i] = y[t = 16 r_q + col][p = 16 pt + 4 grp + i] (the
+        // head loop's wait counts on kYStores stores per row tile).  A row
+        // swap between the slices pt and pt + 1 (even rows keep slice pt, odd
+        // rows slice pt + 1) gives every lane 8 consecutive p of one token:
+        // 16-byte stores, half as many as with 4 p per lane.
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int t = rq[q] * 16 + lc;
-            if (t < len) {
-                bf16* yrow = y + ((b * L + t0 + t) * H + h) * kP + 4 * lg;
+            uint32_t pk[4][2];
 #pragma unroll
-                for (int pt = 0; pt < 4; ++pt) {
-                    const bf16x4 v = {(bf16)yacc[q][pt][0], (bf16)yacc[q][pt][1], (bf16)yacc[q][pt][2],
-                                      (bf16)yacc[q][pt][3]};
-                    *reinterpret_cast<bf16x4*>(yrow + 16 * pt) = v;
+            for (int pt = 0; pt < 4; ++pt) {
+                const bf16x2 lo = {(bf16)yacc[q][pt][0], (bf16)yacc[q][pt][1]};
+                const bf16x2 hi = {(bf16)yacc[q][pt][2], (bf16)yacc[q][pt][3]};
+                pk[pt][0] = __builtin_bit_cast(uint32_t, lo);
+                pk[pt][1] = __builtin_bit_cast(uint32_t, hi);
+            }
+            // v_permlane16_swap: odd rows of the first operand trade places
+            // with even rows of the second (a row is 16 lanes)
+#pragma unroll
+            for (int pp = 0; pp < 4; pp += 2) {
+#pragma unroll
+                for (int k = 0; k < 2; ++k)
+                    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1"
+                                 : "+v"(pk[pp][k]), "+v"(pk[pp + 1][k]));
+            }
+            if (t < len) {
+                bf16* yrow = y + ((b * L + t0 + t) * H + h) * kP;
+                const int odd = lg & 1;
+#pragma unroll
+                for (int pp = 0; pp < 4; pp += 2) {
+                    const int p0 = 16 * (pp + odd) + 4 * (lg - odd);
+                    *reinterpret_cast<uint4*>(yrow + p0) =
+                        make_uint4(pk[pp][0], pk[pp][1], pk[pp + 1][0], pk[pp + 1][1]);
                 }
             }
         }
@@ -971,13 +996,13 @@ __global__ __launch_bounds__(64 * out_waves<S>()) void k_chunk_out_heads(
 
     for (int hh = 0; hh < hpb; ++hh) {
         // this wave's copies of head hh are in: only the y stores of head
-        // hh - 1 (four per row tile) were issued after them (vector memory
+        // hh - 1 (two per row tile) were issued after them (vector memory
         // operations complete in order); a partial chunk, whose stores are
         // predicated, waits for all
         if (hh == 0 || len < S) {
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         } else {
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * NQ));
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(kYStores * NQ));
         }
         lds_barrier();  // every wave's copies are in; head hh - 1 is done with its buffer
         if (hh + 1 < hpb) issue_unit(hh + 1, (hh + 1) & 1);
