@@ -163,6 +163,50 @@ __device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
     *reinterpret_cast<f32x4*>(p) = r;
 }
 
+// Stores of NT MFMA accumulator tiles as bf16: lane (grp, col) of tile j holds
+// out[row0 + 16 j + col][4 grp + i], i < 4, in rows of `pitch` elements from
+// `base`.  With NT even, a row swap between tiles j and j + 1 (even rows keep
+// tile j, odd rows take tile j + 1; v_permlane16_swap trades odd rows of its
+// first operand with even rows of its second) gives every lane 8 consecutive
+// columns of one row: one 16-byte store per tile pair.  Every lane of the
+// wave must take part.  acc_row_stores<NT>() is the number of stores each
+// lane issues (for wait counts).
+template <int NT>
+constexpr int acc_row_stores() { return NT % 2 == 0 ? NT / 2 : NT; }
+template <int NT>
+__device__ __forceinline__ void store_acc_rows_bf16(bf16* base, int64_t pitch, int row0,
+                                                    const f32x4 (&acc)[NT], int grp, int col) {
+    if constexpr (NT % 2 == 0) {
+        uint32_t pk[NT][2];
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const bf16x2 lo = {(bf16)acc[j][0], (bf16)acc[j][1]};
+            const bf16x2 hi = {(bf16)acc[j][2], (bf16)acc[j][3]};
+            pk[j][0] = __builtin_bit_cast(uint32_t, lo);
+            pk[j][1] = __builtin_bit_cast(uint32_t, hi);
+        }
+#pragma unroll
+        for (int j = 0; j < NT; j += 2) {
+#pragma unroll
+            for (int k = 0; k < 2; ++k)
+                asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(pk[j][k]), "+v"(pk[j + 1][k]));
+        }
+        const int odd = grp & 1;
+#pragma unroll
+        for (int j = 0; j < NT; j += 2) {
+            const int64_t r = row0 + 16 * (j + odd) + col;
+            *reinterpret_cast<uint4*>(base + r * pitch + 4 * (grp - odd)) =
+                make_uint4(pk[j][0], pk[j][1], pk[j + 1][0], pk[j + 1][1]);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const bf16x4 v4 = {(bf16)acc[j][0], (bf16)acc[j][1], (bf16)acc[j][2], (bf16)acc[j][3]};
+            *reinterpret_cast<bf16x4*>(base + (int64_t)(row0 + 16 * j + col) * pitch + 4 * grp) = v4;
+        }
+    }
+}
+
 // ---- wave-level helpers ---------------------------------------------------
 __device__ __forceinline__ float shfl_xor(float v, int mask) { return __shfl_xor(v, mask, 64); }
 

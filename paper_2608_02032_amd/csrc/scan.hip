@@ -274,7 +274,7 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
     constexpr int XT = S * XRB, BT = S * BRB;
     constexpr int KST = S / 32;                 // 32-token k steps
     constexpr int NTW = N / 32;                 // n tiles per wave
-    constexpr int DHS = NTW % 2 == 0 ? NTW / 2 : NTW;  // dH stores per wave and head
+    constexpr int DHS = acc_row_stores<NTW>();  // dH stores per wave and head
     constexpr int NG = 2;                       // n-tile groups
     static_assert(NG * NTW * 16 == N && NG * 4 == NW, "tiles cover the waves");
     constexpr int TPL = S / 64;                 // tokens per lane in a decay scan
@@ -424,40 +424,8 @@ __global__ __launch_bounds__(512) void k_chunk_state_heads(
             for (int j = 0; j < NTW; ++j) acc[j] = mma16(acc[j], xf, bfr[j][ks]);
         }
         // acc[j][i] = dH[n = 16 (ng NTW + j) + col][p = 16 pg + 4 grp + i]
-        T* dst = mem + ((b * Mcap + c) * H + hbase + hh) * (int64_t)N * kP + 16 * pg;
-        if constexpr (NTW % 2 == 0) {
-            // a row swap between the n tiles j and j + 1 (even rows keep tile
-            // j, odd rows tile j + 1) gives every lane 8 consecutive p of one
-            // row n: one 16-byte store per tile pair
-            uint32_t pk[NTW][2];
-#pragma unroll
-            for (int j = 0; j < NTW; ++j) {
-                const bf16x2 lo = {(bf16)acc[j][0], (bf16)acc[j][1]};
-                const bf16x2 hi = {(bf16)acc[j][2], (bf16)acc[j][3]};
-                pk[j][0] = __builtin_bit_cast(uint32_t, lo);
-                pk[j][1] = __builtin_bit_cast(uint32_t, hi);
-            }
-#pragma unroll
-            for (int j = 0; j < NTW; j += 2) {
-#pragma unroll
-                for (int k = 0; k < 2; ++k)
-                    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1"
-                                 : "+v"(pk[j][k]), "+v"(pk[j + 1][k]));
-            }
-            const int odd = grp & 1;
-#pragma unroll
-            for (int j = 0; j < NTW; j += 2) {
-                const int n = 16 * (ng * NTW + j + odd) + col;
-                *reinterpret_cast<uint4*>(dst + n * kP + 4 * (grp - odd)) =
-                    make_uint4(pk[j][0], pk[j][1], pk[j + 1][0], pk[j + 1][1]);
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < NTW; ++j) {
-                const bf16x4 v4 = {(bf16)acc[j][0], (bf16)acc[j][1], (bf16)acc[j][2], (bf16)acc[j][3]};
-                *reinterpret_cast<bf16x4*>(dst + (16 * (ng * NTW + j) + col) * kP + 4 * grp) = v4;
-            }
-        }
+        store_acc_rows_bf16<NTW>(mem + ((b * Mcap + c) * H + hbase + hh) * (int64_t)N * kP + 16 * pg,
+                                 kP, 16 * ng * NTW, acc, grp, col);
     }
 }
 

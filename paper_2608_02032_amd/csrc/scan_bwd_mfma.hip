@@ -152,7 +152,7 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
     constexpr int NG = 2;               // n-tile groups
     static_assert(NG * NTW * 16 == N && NG * 4 == NW, "tiles cover the waves");
     constexpr int TPL = S / 64;
-    constexpr int NST = NTW;            // stores per head and wave
+    constexpr int NST = acc_row_stores<NTW>();  // stores per head and wave
 
     const int nhs = (H / G) / hpb;
     int64_t bcg;
@@ -277,12 +277,8 @@ __global__ __launch_bounds__(512) void k_sbwd_contract(
             for (int j = 0; j < NTW; ++j) acc[j] = mma16(acc[j], vf, afr[j][ks]);
         }
         // acc[j][i] = out[n = 16 (ng NTW + j) + col][p = 16 pg + 4 grp + i]
-        bf16* dst = out + ((b * M + c) * H + hbase + hh) * (int64_t)N * kP + 16 * pg + 4 * grp;
-#pragma unroll
-        for (int j = 0; j < NTW; ++j) {
-            const bf16x4 v4 = {(bf16)acc[j][0], (bf16)acc[j][1], (bf16)acc[j][2], (bf16)acc[j][3]};
-            *reinterpret_cast<bf16x4*>(dst + (16 * (ng * NTW + j) + col) * kP) = v4;
-        }
+        store_acc_rows_bf16<NTW>(out + ((b * M + c) * H + hbase + hh) * (int64_t)N * kP + 16 * pg,
+                                 kP, 16 * ng * NTW, acc, grp, col);
     }
 }
 
