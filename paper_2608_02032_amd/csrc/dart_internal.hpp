@@ -182,6 +182,8 @@ void prof_begin(const char* kernel, hipStream_t st);
 void prof_end(hipStream_t st);
 
 inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+// Compute units of the current device (queried once; 256 if the query fails).
+int device_cu_count();
 inline size_t elem_bytes(int dtype) { return dtype == 1 ? 2 : 4; }
 
 }  // namespace dart

@@ -1019,17 +1019,26 @@ struct ScanWs {
     size_t total;
 };
 
-// Heads per workgroup of the bf16 scan kernels: the largest divisor of the
-// heads of a group, at most hmax, that still gives every compute unit a
-// workgroup.
-int out_heads_per_block(int64_t nbcg, int hg, int hmax) {
-    static int cus = [] {
+}  // namespace
+
+int device_cu_count() {
+    static const int cus = [] {
         int dev = 0, n = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
             n = 256;
         return n;
     }();
+    return cus;
+}
+
+namespace {
+
+// Heads per workgroup of the bf16 scan kernels: the largest divisor of the
+// heads of a group, at most hmax, that still gives every compute unit a
+// workgroup.
+int out_heads_per_block(int64_t nbcg, int hg, int hmax) {
+    const int cus = device_cu_count();
     for (int hpb = hg < hmax ? hg : hmax; hpb > 1; --hpb)
         if (hg % hpb == 0 && nbcg * (hg / hpb) >= cus) return hpb;
     return 1;

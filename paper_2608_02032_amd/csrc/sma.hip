@@ -37,6 +37,8 @@
 // cache's [N][P] layout; value tiles come straight from the cache, through
 // registers one step ahead when four LDS stages do not fit.  Operand fragments
 // are read with transposing LDS loads.
+#include <algorithm>
+
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
 
@@ -273,16 +275,17 @@ __global__ __launch_bounds__(kThreads) void k_sma_regs(
     // C, loaded once) for one token block, one head after another.
     // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
     // index, and each XCD has its own L2.  When the number of head groups
-    // B*H/hpb is a multiple of 8, XCD x runs whole head groups x, x+8, ... one
-    // after another, heaviest token block first, so all blocks reading one
-    // head group's memories share one L2.
+    // B*H/hpb is a multiple of 8, XCD x runs only head groups x, x+8, ..., so
+    // all blocks reading one head group's memories share one L2; token blocks
+    // go heaviest first over all head groups, so that the longest blocks
+    // start first and the short ones fill in behind them.
     const int64_t bid = blockIdx.x;
     int blk;
     int64_t bhc;
     if (BHC % 8 == 0) {
-        const int64_t slot = bid >> 3;
-        blk = nblk - 1 - (int)(slot % nblk);
-        bhc = (slot / nblk) * 8 + (bid & 7);
+        const int64_t slot = bid >> 3, ng8 = BHC >> 3;
+        blk = nblk - 1 - (int)(slot / ng8);
+        bhc = (slot % ng8) * 8 + (bid & 7);
     } else {
         blk = nblk - 1 - (int)(bid / BHC);
         bhc = bid % BHC;
@@ -930,9 +933,9 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     int blk;
     int64_t bhc;
     if (BHC % 8 == 0) {
-        const int64_t slot = bid >> 3;
-        blk = nblk - 1 - (int)(slot % nblk);
-        bhc = (slot / nblk) * 8 + (bid & 7);
+        const int64_t slot = bid >> 3, ng8 = BHC >> 3;
+        blk = nblk - 1 - (int)(slot / ng8);
+        bhc = (slot % ng8) * 8 + (bid & 7);
     } else {
         blk = nblk - 1 - (int)(bid / BHC);
         bhc = bid % BHC;
@@ -1438,21 +1441,49 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     }
 }
 
+// Heads per block: the power-of-2 divisor of the group's heads, at most
+// kHeadsPerBlock, with the least estimated makespan.  A block of hpb heads on
+// token block k streams hpb * jmax(k) memories (plus two pipeline steps) after
+// a set-up of about kSmaSetupSteps steps.  Blocks are launched heaviest first
+// and each CU takes the next one when it frees, so the makespan is about the
+// larger of the longest block and the total work over the CUs (the bound of
+// that greedy order).  More heads per block share q, e and C and their set-up;
+// fewer split the longest blocks, so that short sequences and small batches
+// still fill every CU evenly.
+constexpr int kSmaSetupSteps = 3;
+int sma_heads_per_block(const Shape& s, int tpb) {
+    const int per_group = (int)(s.H / s.G);
+    const int64_t nblk = (s.L + tpb - 1) / tpb;
+    const double cus = (double)device_cu_count();
+    int best = 1;
+    double best_t = -1.0;
+    for (int hpb = kHeadsPerBlock; hpb >= 1; hpb >>= 1) {
+        if (per_group % hpb != 0) continue;
+        const double bhc = (double)(s.B * (s.H / hpb));
+        double longest = 0.0, total = 0.0;
+        for (int64_t k = 0; k < nblk; ++k) {
+            const int64_t end = (k + 1) * tpb < s.L ? (k + 1) * tpb : s.L;
+            const int64_t jmax = (end - 1) / s.S;
+            const double cost = kSmaSetupSteps + (double)(hpb * jmax) + (jmax > 0 ? 2 : 0);
+            longest = std::max(longest, cost);
+            total += bhc * cost;
+        }
+        const double t = std::max(longest, total / cus);
+        if (best_t < 0 || t < best_t * 0.97) {  // fewer heads only for a clear gain
+            best = hpb;
+            best_t = t;
+        }
+    }
+    return best;
+}
+
 template <typename T, int N, int S>
 hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e, const void* Cm,
                    const void* mem, const void* z, const void* y_ssd, void* y, float* lse,
                    void* ws, hipStream_t st) {
     constexpr int TPB = sma_tokens_per_block<T>();
     const int nblk = (int)((s.L + TPB - 1) / TPB);
-    // heads per block: up to kHeadsPerBlock heads of one group
-    const int per_group = s.H / s.G;
-    int hpb = 1;
-    for (int c = kHeadsPerBlock; c > 1; c >>= 1) {
-        if (per_group % c == 0) {
-            hpb = c;
-            break;
-        }
-    }
+    const int hpb = sma_heads_per_block(s, TPB);
     const int64_t BHC = s.B * (s.H / hpb);
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;  // memories any token attends to
     T* kmem = reinterpret_cast<T*>(ws);
