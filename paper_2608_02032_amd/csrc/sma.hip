@@ -1441,29 +1441,35 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     }
 }
 
-// Heads per block: the power-of-2 divisor of the group's heads, at most
-// kHeadsPerBlock, with the least estimated makespan.  A block of hpb heads on
-// token block k streams hpb * jmax(k) memories (plus two pipeline steps) after
-// a set-up of about kSmaSetupSteps steps.  Blocks are launched heaviest first
-// and each CU takes the next one when it frees, so the makespan is about the
-// larger of the longest block and the total work over the CUs (the bound of
-// that greedy order).  More heads per block share q, e and C and their set-up;
-// fewer split the longest blocks, so that short sequences and small batches
-// still fill every CU evenly.
+}  // namespace
+
+// Heads per block of the SMA kernels: the power-of-2 divisor of the group's
+// heads, at most hmax, with the least estimated makespan.  A block of hpb
+// heads on token block k (tpb tokens) streams hpb * jmax(k) memories (plus two
+// pipeline steps) after a set-up of about kSmaSetupSteps steps, jmax(k) being
+// the chunk index of its last token; blocks of the first chunk attend no
+// memory and, with no_first_chunk, are not launched at all.  Blocks are
+// launched heaviest first and each CU takes the next one when it frees, so the
+// makespan is about the larger of the longest block and the total work over
+// the CUs (the bound of that greedy order).  More heads per block share the
+// per-token operands and their set-up; fewer split the longest blocks, so that
+// short sequences and small batches still fill every CU evenly.
 constexpr int kSmaSetupSteps = 3;
-int sma_heads_per_block(const Shape& s, int tpb) {
-    const int per_group = (int)(s.H / s.G);
-    const int64_t nblk = (s.L + tpb - 1) / tpb;
+int sma_block_heads(int64_t B, int H, int G, int64_t L, int S, int tpb, int hmax,
+                    bool no_first_chunk) {
+    const int per_group = H / G;
+    const int64_t nblk = (L + tpb - 1) / tpb;
     const double cus = (double)device_cu_count();
     int best = 1;
     double best_t = -1.0;
-    for (int hpb = kHeadsPerBlock; hpb >= 1; hpb >>= 1) {
+    for (int hpb = hmax; hpb >= 1; hpb >>= 1) {
         if (per_group % hpb != 0) continue;
-        const double bhc = (double)(s.B * (s.H / hpb));
+        const double bhc = (double)(B * (H / hpb));
         double longest = 0.0, total = 0.0;
         for (int64_t k = 0; k < nblk; ++k) {
-            const int64_t end = (k + 1) * tpb < s.L ? (k + 1) * tpb : s.L;
-            const int64_t jmax = (end - 1) / s.S;
+            const int64_t end = (k + 1) * tpb < L ? (k + 1) * tpb : L;
+            const int64_t jmax = (end - 1) / S;
+            if (no_first_chunk && jmax == 0) continue;
             const double cost = kSmaSetupSteps + (double)(hpb * jmax) + (jmax > 0 ? 2 : 0);
             longest = std::max(longest, cost);
             total += bhc * cost;
@@ -1477,13 +1483,15 @@ int sma_heads_per_block(const Shape& s, int tpb) {
     return best;
 }
 
+namespace {
+
 template <typename T, int N, int S>
 hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* e, const void* Cm,
                    const void* mem, const void* z, const void* y_ssd, void* y, float* lse,
                    void* ws, hipStream_t st) {
     constexpr int TPB = sma_tokens_per_block<T>();
     const int nblk = (int)((s.L + TPB - 1) / TPB);
-    const int hpb = sma_heads_per_block(s, TPB);
+    const int hpb = sma_block_heads(s.B, s.H, s.G, s.L, s.S, TPB, kHeadsPerBlock, false);
     const int64_t BHC = s.B * (s.H / hpb);
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;  // memories any token attends to
     T* kmem = reinterpret_cast<T*>(ws);

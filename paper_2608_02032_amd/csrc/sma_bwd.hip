@@ -184,16 +184,16 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const T* __restrict__ q, const
 
 // Block order shared by the two token kernels.  Workgroups are dealt to the
 // 8 XCDs round-robin by block index and each XCD has its own L2.  When the
-// number of (b, head block) pairs is a multiple of 8, XCD x runs the token
-// blocks of pairs x, x+8, ... one pair after another, heaviest first: the
-// blocks running together on an XCD stream the same memory tiles in the
-// same order.
+// number of (b, head block) pairs is a multiple of 8, XCD x runs only pairs
+// x, x+8, ..., so the blocks of one pair share an L2; token blocks go
+// heaviest first over all pairs, so that the longest blocks start first and
+// the short ones fill in behind them.
 __device__ __forceinline__ void tok_block(int64_t bid, int nblk, int64_t BHC, int& blk,
                                           int64_t& bhc) {
     if (BHC % 8 == 0) {
-        const int64_t slot = bid >> 3;
-        blk = nblk - 1 - (int)(slot % nblk);
-        bhc = (slot / nblk) * 8 + (bid & 7);
+        const int64_t slot = bid >> 3, ng8 = BHC >> 3;
+        blk = nblk - 1 - (int)(slot / ng8);
+        bhc = (slot % ng8) * 8 + (bid & 7);
     } else {
         blk = nblk - 1 - (int)(bid / BHC);
         bhc = bid % BHC;
@@ -1082,11 +1082,12 @@ __global__ __launch_bounds__(256) void k_bwd_finish(
     }
 }
 
+// Heads per block of the token kernels (and so of the per-token partials the
+// finishing kernel sums): the token blocks are 128 tokens for bf16 at S >= 128,
+// else kTokBlock, and the first chunk's blocks are not launched.
 int bwd_heads_per_block(const Shape& s) {
-    const int per_group = s.H / s.G;
-    for (int c = kHeadsPerBlock; c > 1; c >>= 1)
-        if (per_group % c == 0) return c;
-    return 1;
+    const int tpb = (s.dtype == 1 && s.S >= 128) ? 2 * kTokBlock : kTokBlock;
+    return sma_block_heads(s.B, s.H, s.G, s.L, s.S, tpb, kHeadsPerBlock, true);
 }
 
 struct BwdWs {
