@@ -1453,8 +1453,13 @@ __global__ __launch_bounds__(kThreads) void k_sma(
 // makespan is about the larger of the longest block and the total work over
 // the CUs (the bound of that greedy order).  More heads per block share the
 // per-token operands and their set-up; fewer split the longest blocks, so that
-// short sequences and small batches still fill every CU evenly.
+// short sequences and small batches still fill every CU evenly.  A split whose
+// head-group count B H / hpb is not a multiple of 8 loses the XCD-local block
+// order (each head group's memory tiles in one L2) and counts kSmaUnaligned
+// times slower (measured at B 1, L 65536, 32 heads: 8 heads per block, 4
+// groups, 7.3 ms; 4 heads, 8 groups, 6.7 ms).
 constexpr int kSmaSetupSteps = 3;
+constexpr double kSmaUnaligned = 1.08;
 int sma_block_heads(int64_t B, int H, int G, int64_t L, int S, int tpb, int hmax,
                     bool no_first_chunk) {
     const int per_group = H / G;
@@ -1474,7 +1479,8 @@ int sma_block_heads(int64_t B, int H, int G, int64_t L, int S, int tpb, int hmax
             longest = std::max(longest, cost);
             total += bhc * cost;
         }
-        const double t = std::max(longest, total / cus);
+        const double t = std::max(longest, total / cus) *
+                         ((B * (H / hpb)) % 8 == 0 ? 1.0 : kSmaUnaligned);
         if (best_t < 0 || t < best_t * 0.97) {  // fewer heads only for a clear gain
             best = hpb;
             best_t = t;
