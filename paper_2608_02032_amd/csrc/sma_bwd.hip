@@ -652,6 +652,18 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
         int ln = lane;
         asm volatile("" : "+v"(ln));
         const int col = ln & 15, grp = ln >> 4;
+        // bf16: the step's fragment offsets, once per step: the transposing
+        // reads of W' (column tile pt0 + q; k blocks move by 32 rows, an
+        // immediate) and the row reads of X and Z (k half ks; n tiles move by
+        // 16 rows, an immediate)
+        KmOffBf16<RB> kofs[2];
+        uint32_t xofs[2];
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) kofs[q].init(4 * grp, 16 + 4 * grp, 16 * (pt0 + q), ln);
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) xofs[ks] = (uint32_t)SwzTile<RB>::off(col, (32 * ks + 8 * grp) * 2);
+        }
         float gp[RT], dl[RT];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
@@ -667,7 +679,12 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
             for (int rt = 0; rt < RT; ++rt) w[rt] = zero4;
 #pragma unroll
             for (int ks = 0; ks < KQ; ++ks) {
-                const Frag<T> a = frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp, 16 * (pt0 + q), ln);
+                Frag<T> a;
+                if constexpr (sizeof(T) == 2) {
+                    a = kofs[q].read(kt, ks * 32 * RB);
+                } else {
+                    a = frag_km<T, RB>(kt, 32 * ks + 4 * grp, 32 * ks + 16 + 4 * grp, 16 * (pt0 + q), ln);
+                }
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
                     if constexpr (RT > 1) {
@@ -690,7 +707,12 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
             for (int rt = 0; rt < RT; ++rt) x[rt] = zz[rt] = zero4;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const Frag<T> a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
+                Frag<T> a;
+                if constexpr (sizeof(T) == 2) {
+                    a = *reinterpret_cast<const bf16x8*>(kt + xofs[ks] + 16 * nt * RB);
+                } else {
+                    a = frag_rowmajor<T, RB>(kt, 16 * nt + col, 32 * ks + 8 * grp);
+                }
 #pragma unroll
                 for (int rt = 0; rt < RT; ++rt) {
                     x[rt] = mma16(x[rt], a, dyf[rt][ks]);
