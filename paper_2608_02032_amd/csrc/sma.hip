@@ -944,7 +944,8 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     const int64_t b = bhc / hgroups;
     const int h0 = (int)(bhc % hgroups) * hpb;
     const int g = (int)((int64_t)h0 * G / H);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: role branches are scalar
     const int col = lane & 15, grp = lane >> 4;
     const bool scorer = wave < 4;
     const int pair = wave & 3;

@@ -277,7 +277,8 @@ __global__ __launch_bounds__(512) void k_bwd_scores(
     __shared__ __attribute__((aligned(16))) float rring[NS][N];
     __shared__ float xch[2][2][kTokWaves][16 * RT];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int col = lane & 15, grp = lane >> 4;
     const int tg = wave & 3, nh = wave >> 2;
     const bool copier = wave < kTokWaves;
@@ -520,7 +521,8 @@ __global__ __launch_bounds__(512) void k_bwd_tokens(
     constexpr int QL = RT > 1 ? RT * (KQ + 2) : 1;
     __shared__ __attribute__((aligned(16))) Frag<T> qslot[QL][512];
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int col = lane & 15, grp = lane >> 4;
     const int tg = wave & 3, nh = wave >> 2;  // token group, half of n
     const bool copier = wave < kTokWaves;
@@ -821,7 +823,8 @@ __global__ __launch_bounds__(512) void k_bwd_mem(const T* __restrict__ qb,
     __shared__ __attribute__((aligned(16))) char buf[NS][STAGE];
     __shared__ __attribute__((aligned(16))) float sc[NS][J][2][TB];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     const int col = lane & 15, grp = lane >> 4;
     const int pt = wave & 3;                       // p tile of the wave
     const int jh = MSPLIT ? (wave >> 2) * JW : 0;  // its first memory
