@@ -36,6 +36,13 @@
  *    H % G == 0.  N in {32, 64, 128} with S in {64, 128, 256} run the tuned
  *    MFMA kernels; every other shape runs generic fp32 kernels (the paper
  *    trains at S = 16, N in {16, 64} and evaluates at S = 32 and 64).
+ *  - Tuning variables (results do not depend on them beyond floating-point
+ *    summation order): DART_SMA_HEADS_PER_BLOCK in {1, 2, 4, 8} forces the
+ *    number of heads one SMA workgroup serves (forward and backward; used
+ *    when it divides H/G; read at every call, so it must not change between
+ *    a workspace query and the call it sizes); DART_DECODE_MPS in
+ *    {8, 16, 32, 64, 128} forces the memories per decode split (read once).
+ *    Unset, both are chosen per shape.
  */
 #ifndef DART_H
 #define DART_H

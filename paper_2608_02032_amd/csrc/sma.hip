@@ -38,6 +38,7 @@
 // registers one step ahead when four LDS stages do not fit.  Operand fragments
 // are read with transposing LDS loads.
 #include <algorithm>
+#include <cstdlib>
 
 #include "dart_common.hpp"
 #include "dart_internal.hpp"
@@ -1464,6 +1465,12 @@ constexpr double kSmaUnaligned = 1.08;
 int sma_block_heads(int64_t B, int H, int G, int64_t L, int S, int tpb, int hmax,
                     bool no_first_chunk) {
     const int per_group = H / G;
+    // DART_SMA_HEADS_PER_BLOCK in {1, 2, 4, 8} forces the split when it divides
+    // the group's heads (testing and tuning); read at every call
+    if (const char* ev = getenv("DART_SMA_HEADS_PER_BLOCK")) {
+        const int x = atoi(ev);
+        if ((x == 1 || x == 2 || x == 4 || x == 8) && x <= hmax && per_group % x == 0) return x;
+    }
     const int64_t nblk = (L + tpb - 1) / tpb;
     const double cus = (double)device_cu_count();
     int best = 1;

@@ -133,6 +133,32 @@ def test_sma_matches_explicit_softmax(w):
     check_readout(w, d, mem)
 
 
+# The small shapes above run with one head per workgroup (the chooser's pick
+# for them); these force 2, 4 and 8 heads per workgroup, so the head changes
+# inside a workgroup's memory stream and the per-head epilogues are checked
+# element by element as well.
+FORCED_HPB = [("bf16_L4096_N128_S256_H8", 8), ("bf16_L4096_N128_S256_H8", 4),
+              ("bf16_L2304_N64_S64_H4", 4), ("bf16_L2304_N64_S64_H4", 2),
+              ("bf16_L1100_N32_S64_G2", 2), ("bf16_L1024_N128_S128", 2), ("fp32_L700_N64_S128", 2)]
+
+
+@pytest.mark.parametrize("name,hpb", FORCED_HPB, ids=lambda v: str(v))
+def test_sma_forced_heads_per_block(name, hpb, monkeypatch):
+    w = {c.name: c for c in SMA_CASES}[name]
+    announce("sma %s, %d heads per block" % (w, hpb))
+    monkeypatch.setenv("DART_SMA_HEADS_PER_BLOCK", str(hpb))
+    d, mem, y_ssd = sma_case(w, seed=7)
+    y, lse = run_sma(w, d, mem, y_ssd)
+    y_ref, lse_ref = oracle.sma(d["q"], d["e"], d["Cm"], mem, d["z"], y_ssd, w.chunk)
+    assert_close_slices(to_np(y), y_ref, TOL[w.dtype], what="y")
+    assert_lse_close(to_np(lse), lse_ref, w.dtype)
+    # the head split changes no arithmetic: bitwise equal to the chosen split
+    monkeypatch.delenv("DART_SMA_HEADS_PER_BLOCK")
+    y0, lse0 = run_sma(w, d, mem, y_ssd)
+    np.testing.assert_array_equal(to_np(y), to_np(y0))
+    np.testing.assert_array_equal(to_np(lse), to_np(lse0))
+
+
 def readout_inputs(w, d):
     """y_ssd = 0 and one gate z = 2 for every token and head: y = SiLU(2) R."""
     z2 = np.full_like(d["z"], 2.0)

@@ -87,6 +87,23 @@ def test_sma_bwd_matches_oracle(w):
     check(w, got, d, mem, dy)
 
 
+# The cases above run with one or eight heads per workgroup as the chooser
+# picks; these force other splits of the token kernels (and of the per-token
+# partials the finishing kernel sums).
+FORCED_HPB = [("bf16_L1000_N128_S128_H16", 8), ("bf16_L1000_N128_S128_H16", 4),
+              ("bf16_L640_N64_S64_sharedz", 4), ("bf16_L1100_N32_S64_G2", 2), ("fp32_L700_N64_S128", 2)]
+
+
+@pytest.mark.parametrize("name,hpb", FORCED_HPB, ids=lambda v: str(v))
+def test_sma_bwd_forced_heads_per_block(name, hpb, monkeypatch):
+    w = {c.name: c for c in BWD_CASES}[name]
+    announce("sma bwd %s, %d heads per block" % (w, hpb))
+    monkeypatch.setenv("DART_SMA_HEADS_PER_BLOCK", str(hpb))
+    d, mem, y_ssd, dy = bwd_case(w, seed=11)
+    got = run_gpu(w, d, mem, y_ssd, dy)
+    check(w, got, d, mem, dy, tag=" hpb %d" % hpb)
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_sma_bwd_unnormalised_and_weighted(dtype):
     w = synth.Workload("opts_%s_L640_N64_S128" % dtype, 1, 640, 4, 64, 64, 128, dtype)
