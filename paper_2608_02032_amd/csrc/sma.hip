@@ -277,16 +277,25 @@ __global__ __launch_bounds__(kThreads) void k_sma_regs(
     // Block order.  Workgroups are dealt to the 8 XCDs round-robin by block
     // index, and each XCD has its own L2.  When the number of head groups
     // B*H/hpb is a multiple of 8, XCD x runs only head groups x, x+8, ..., so
-    // all blocks reading one head group's memories share one L2; token blocks
-    // go heaviest first over all head groups, so that the longest blocks
-    // start first and the short ones fill in behind them.
+    // all blocks reading one head group's memories share one L2.  With one or
+    // two groups per XCD they run one group after the other, heaviest first;
+    // with more, token blocks go heaviest first over all groups, so that the
+    // longest blocks start first and the short ones fill in behind them.
     const int64_t bid = blockIdx.x;
     int blk;
     int64_t bhc;
     if (BHC % 8 == 0) {
         const int64_t slot = bid >> 3, ng8 = BHC >> 3;
-        blk = nblk - 1 - (int)(slot / ng8);
-        bhc = (slot % ng8) * 8 + (bid & 7);
+        if (ng8 <= 2) {
+            // one or two head groups per XCD: one group after the other (its
+            // blocks share the L2 while they run; the first group's light
+            // blocks meet the second's heavy ones)
+            blk = nblk - 1 - (int)(slot % nblk);
+            bhc = (slot / nblk) * 8 + (bid & 7);
+        } else {
+            blk = nblk - 1 - (int)(slot / ng8);
+            bhc = (slot % ng8) * 8 + (bid & 7);
+        }
     } else {
         blk = nblk - 1 - (int)(bid / BHC);
         bhc = bid % BHC;
@@ -935,8 +944,16 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     int64_t bhc;
     if (BHC % 8 == 0) {
         const int64_t slot = bid >> 3, ng8 = BHC >> 3;
-        blk = nblk - 1 - (int)(slot / ng8);
-        bhc = (slot % ng8) * 8 + (bid & 7);
+        if (ng8 <= 2) {
+            // one or two head groups per XCD: one group after the other (its
+            // blocks share the L2 while they run; the first group's light
+            // blocks meet the second's heavy ones)
+            blk = nblk - 1 - (int)(slot % nblk);
+            bhc = (slot / nblk) * 8 + (bid & 7);
+        } else {
+            blk = nblk - 1 - (int)(slot / ng8);
+            bhc = (slot % ng8) * 8 + (bid & 7);
+        }
     } else {
         blk = nblk - 1 - (int)(bid / BHC);
         bhc = bid % BHC;
