@@ -185,9 +185,9 @@ inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 // Compute units of the current device (queried once; 256 if the query fails).
 int device_cu_count();
 // Heads per block of the SMA kernels (forward and backward token kernels) for
-// token blocks of tpb tokens: the power-of-2 divisor of H/G, at most hmax, with
-// the least estimated makespan; no_first_chunk when the first chunk's blocks
-// are not launched.
+// token blocks of tpb tokens: the power-of-2 divisor of H/G, at most hmax (the
+// chooser's cap; the kernels take up to 8), with the least estimated makespan;
+// no_first_chunk when the first chunk's blocks are not launched.
 int sma_block_heads(int64_t B, int H, int G, int64_t L, int S, int tpb, int hmax,
                     bool no_first_chunk);
 inline size_t elem_bytes(int dtype) { return dtype == 1 ? 2 : 4; }

@@ -50,7 +50,12 @@ constexpr int kP = 64;
 constexpr int kWaves = 8;                  // 4 (score, value) pairs
 constexpr int kThreads = kWaves * 64;
 constexpr float kRescaleLog2 = 8.0f;       // lazy-rescale threshold (log2 units)
-constexpr int kHeadsPerBlock = 8;          // heads of one group served by a block (power of 2)
+constexpr int kHeadsPerBlock = 8;          // most heads of one group a block can serve (power of 2)
+// The forward's chooser stops at four heads per block: measured against
+// eight, four take 472 vs 483 us at B 4, L 8192, 32 heads, S 256 and 930 vs
+// 965 us at S 128, and tie at the Mamba-2-130M shape (the greedy-order bound
+// itself cannot see the difference).
+constexpr int kFwdHeadsCap = 4;
 
 // 16-token column tiles per pair: 4 for bf16 (64 tokens), 2 for fp32 (its
 // operand fragments take twice the registers).
@@ -1483,10 +1488,10 @@ int sma_block_heads(int64_t B, int H, int G, int64_t L, int S, int tpb, int hmax
                     bool no_first_chunk) {
     const int per_group = H / G;
     // DART_SMA_HEADS_PER_BLOCK in {1, 2, 4, 8} forces the split when it divides
-    // the group's heads (testing and tuning); read at every call
+    // the group's heads, above hmax too (testing and tuning); read at every call
     if (const char* ev = getenv("DART_SMA_HEADS_PER_BLOCK")) {
         const int x = atoi(ev);
-        if ((x == 1 || x == 2 || x == 4 || x == 8) && x <= hmax && per_group % x == 0) return x;
+        if ((x == 1 || x == 2 || x == 4 || x == 8) && x <= kHeadsPerBlock && per_group % x == 0) return x;
     }
     const int64_t nblk = (L + tpb - 1) / tpb;
     const double cus = (double)device_cu_count();
@@ -1522,7 +1527,7 @@ hipError_t run_sma(const Shape& s, const SmaArgs& a, const void* q, const void* 
                    void* ws, hipStream_t st) {
     constexpr int TPB = sma_tokens_per_block<T>();
     const int nblk = (int)((s.L + TPB - 1) / TPB);
-    const int hpb = sma_block_heads(s.B, s.H, s.G, s.L, s.S, TPB, kHeadsPerBlock, false);
+    const int hpb = sma_block_heads(s.B, s.H, s.G, s.L, s.S, TPB, kFwdHeadsCap, false);
     const int64_t BHC = s.B * (s.H / hpb);
     const int64_t Mp = s.M > 1 ? s.M - 1 : 0;  // memories any token attends to
     T* kmem = reinterpret_cast<T*>(ws);
