@@ -999,21 +999,28 @@ __global__ __launch_bounds__(kThreads) void k_sma(
     Dma tdma;
     tdma.init(wave, lane);
     const int tcnt = tdma.count();      // copies per tile issued by this wave
-    // next key and value tiles to copy, as (head, index) in memory order
-    int kh = 0, kj = 0, vh = 0, vj = 0;
-    auto advance = [&](int& h, int& j) __attribute__((always_inline)) {
+    // next key and value tiles to copy (memory order: index within a head,
+    // then head), as tile addresses advanced by a stride or, at a head's last
+    // memory, back to the next head's first one
+    const char* kp = kbase0;
+    const char* vp = vbase0;
+    int kj = 0, vj = 0;
+    const int64_t hstep = (int64_t)MEMB - (int64_t)(jmax - 1) * jstride;
+    auto advance = [&](const char*& p, int& j) __attribute__((always_inline)) {
         if (++j == jmax) {
             j = 0;
-            ++h;
+            p += hstep;
+        } else {
+            p += jstride;
         }
     };
     auto fetch_k = [&](int st) __attribute__((always_inline)) {
-        tdma.issue(kbase0 + (int64_t)kh * MEMB + (int64_t)kj * jstride, kring + st * MEMB);
-        advance(kh, kj);
+        tdma.issue(kp, kring + st * MEMB);
+        advance(kp, kj);
     };
     auto fetch_v = [&](int st) __attribute__((always_inline)) {
-        tdma.issue(vbase0 + (int64_t)vh * MEMB + (int64_t)vj * jstride, vring + st * MEMB);
-        advance(vh, vj);
+        tdma.issue(vp, vring + st * MEMB);
+        advance(vp, vj);
     };
     if (nmem > 0) {
         fetch_k(0);
@@ -1214,7 +1221,6 @@ __global__ __launch_bounds__(kThreads) void k_sma(
         Frag<T> fr[4];            // fragment ring
         int jm = 0;               // index within its head of memory s
         int hm = 0;               // head of memory s
-        bool tail_pending = false;  // memory s-1 was scored by this wave
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) u[1][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
         // partial logit sums of slice pt (in u[pt & 1]) for column tile rt
@@ -1223,7 +1229,13 @@ __global__ __launch_bounds__(kThreads) void k_sma(
             for (int i = 0; i < 4; ++i) lp[rt] += u[pt & 1][rt][i] * ef[rt][pt][i];
         };
         run_stream([&](int s, int kc, int) __attribute__((always_inline)) {
-            const bool mm = s < nmem && jm < nj;
+            // memory s is scored by this wave iff mmi < 0 (a scalar integer, so
+            // the flag never takes a lane-mask round trip between its uses)
+            int mmi = (s - nmem) & (jm - nj);
+            asm("" : "+s"(mmi));
+            const bool mm = mmi < 0;
+            // memory s-1 was scored by this wave
+            const bool tail_pending = s >= 1 && s <= nmem && (jm == 0 ? jmax - 1 : jm - 1) < nj;
             const char* kt = kring + kc * MEMB;
             // slice 0 of memory s, with the last slice's logit sums of memory s-1
             if (mm) {
@@ -1241,14 +1253,19 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 // exceeds it by more than 2^8; R = O/d and LSE = m + log2 d do
                 // not depend on that choice
                 const bool rescale = __builtin_amdgcn_ballot_w64(l > m_own + kRescaleLog2) != 0;
-                const float mn = rescale ? fmaxf(m_own, l) : m_own;
-                const float al = fast_exp2(m_own - mn);
-                const float pw = fast_exp2(l - mn);
-                d_own = d_own * al + pw;
-                m_own = mn;
                 const int slot = (s - 1) & 1;
+                // the factor for O is needed (and written) only when the
+                // maximum moves; otherwise it is exactly 1
+                float al = 1.0f;
+                if (rescale) {
+                    const float mn = fmaxf(m_own, l);
+                    al = fast_exp2(m_own - mn);
+                    m_own = mn;
+                    xa[slot][pair][lane] = al;
+                }
+                const float pw = fast_exp2(l - m_own);
+                d_own = d_own * al + pw;
                 xw[slot][pair][lane] = pw;
-                xa[slot][pair][lane] = al;
                 if (lane == 0) xr[slot][pair] = rescale ? 1 : 0;
             }
             // the head of memory s-1 is complete
@@ -1257,20 +1274,26 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 m_own = -INFINITY;
                 d_own = 0.f;
             }
-            tail_pending = mm;
-            if (mm) {
+            // (the sums restart every step, so no step carries them into a
+            // step that does not score)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
+            asm("" : "+s"(mmi));
+            if (mmi < 0) {
                 // ---- U^T = (r (.) dH_s)^T Qbar^T, slices 1..3; each slice's
                 // MFMAs are interleaved with the logit sums of the slice before
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) lp[rt] = 0.f;
 #pragma unroll
                 for (int pt = 1; pt < 4; ++pt)
                     slice_region(fr, kt, pt, u[pt & 1], qf, [&](int rt) { lp_fma(pt - 1, rt); });
             }
-            if (++jm == jmax) {
-                jm = 0;
-                ++hm;
-            }
+            // (jm, hm) advance in scalar registers
+            asm("s_add_i32 %0, %0, 1\n\t"
+                "s_cmp_eq_u32 %0, %2\n\t"
+                "s_cselect_b32 %0, 0, %0\n\t"
+                "s_addc_u32 %1, %1, 0"
+                : "+s"(jm), "+s"(hm)
+                : "s"(jmax)
+                : "scc");
         });
     } else {
         // ---- value wave: C of the pair's tokens, accumulator O ----------------
@@ -1419,6 +1442,8 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                         for (int rt = 0; rt < RT; ++rt) pwp[rt] = 0.f;
                     }
                     slice_region(fr, vt, 0, v[0], cf, [&](int rt) { o[rt][3] += pwp[rt] * v[1][rt]; });
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(o[rt][3]));
                     // start of a head, or the running maximum moved: O (which
                     // already holds every earlier memory) is reset or rescaled
                     if (jv == 0) {
@@ -1434,10 +1459,16 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                             for (int pt = 0; pt < 4; ++pt) o[rt][pt] *= al;
                         }
                     }
+                    // (each slice's O updates are pinned behind its region, so
+                    // they stay interleaved with its MFMAs instead of being
+                    // sunk to the end of the step)
 #pragma unroll
-                    for (int pt = 1; pt < 4; ++pt)
+                    for (int pt = 1; pt < 4; ++pt) {
                         slice_region(fr, vt, pt, v[pt & 1], cf,
                                      [&](int rt) { o[rt][pt - 1] += pw[rt] * v[(pt - 1) & 1][rt]; });
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) asm volatile("" : "+v"(o[rt][pt - 1]));
+                    }
                     // the last slice waits for the next memory of the head, if it
                     // is attended; otherwise it completes O now
                     pend = jv + 1 < nj;
