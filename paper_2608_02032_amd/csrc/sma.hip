@@ -1386,8 +1386,14 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                 const int r = rt * 16 + c;
                 const int64_t t = pbase + r;
                 if (t >= L) continue;
-                const float gate = silu(__builtin_bit_cast(float, zbuf[pair][r] << 16));
-                const float invd = hist ? 1.0f / xd[hh & 1][pair][r] : 0.f;
+                // SiLU(z) / d folded into one factor per token, both
+                // reciprocals by the hardware rcp (the epilogue's IEEE divides
+                // and separate products had made it cost about one stream step
+                // per head)
+                const float zv = __builtin_bit_cast(float, zbuf[pair][r] << 16);
+                const float gd = hist ? zv * __builtin_amdgcn_rcpf(1.0f + __expf(-zv)) *
+                                            __builtin_amdgcn_rcpf(xd[hh & 1][pair][r])
+                                      : 0.f;
                 bf16* yrow = y + ((b * L + t) * H + h) * kP + gq * 4;
 #pragma unroll
                 for (int pt = 0; pt < 4; ++pt) {
@@ -1398,7 +1404,7 @@ __global__ __launch_bounds__(kThreads) void k_sma(
                     for (int i = 0; i < 4; ++i) yv[i] = to_f(ys[i]);
                     if (hist) {
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) yv[i] += gate * (o[rt][pt][i] * invd);
+                        for (int i = 0; i < 4; ++i) yv[i] = fmaf(gd, o[rt][pt][i], yv[i]);
                     }
                     store4(yrow + pt * 16, yv);
                 }
