@@ -840,9 +840,13 @@ __global__ __launch_bounds__(256) void k_sma_prep(const bf16* __restrict__ mem,
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     __shared__ __attribute__((aligned(16))) char t[N * RB];
     __shared__ float rs[N];
-    const uint4* src = reinterpret_cast<const uint4*>(mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP);
+    // the memories are read once here (streaming loads); the transposed
+    // sides are written with ordinary stores so the attention kernel that
+    // follows finds them in the caches
+    const u32x4_nt* src = reinterpret_cast<const u32x4_nt*>(mem + ((b * Mcap + j) * H + h) * (int64_t)N * kP);
     for (int q = tid; q < PIECES; q += 256) {
-        const uint4 v = src[q];
+        const u32x4_nt vn = __builtin_nontemporal_load(src + q);
+        const uint4 v = make_uint4(vn[0], vn[1], vn[2], vn[3]);
         const int n = q / RPC, pc = q % RPC;
         const float ss = dpp_group_sum<RPC>(piece_sumsq(v, bf16()));
         if (pc == 0) rs[n] = normalize ? __builtin_amdgcn_rsqf(ss * (1.0f / kP) + eps) : 1.0f;
